@@ -1,0 +1,36 @@
+"""Oracle: expert-gathered compensated forward for a MoE layer.
+
+TEST INFRASTRUCTURE ONLY (see ``oracle/__init__.py``).
+
+Section 4.2.2 (cross-expert pipeline reorganisation) and Appendix A.1 (MoE
+windows) group the same projection of every activated expert into one step; for
+a token only its routed experts' weights and compensation factors enter.  With a
+routing table ``ids[T][k]`` the result is, slot by slot,
+
+  y[t][j] = W_hat_e x + B_e[:, :r_e] (A_e[:r_e] x),   e = ids[t][j]
+
+where ``x`` is the token's input (shared by its slots, e.g. gate/up) or the
+slot's own input (e.g. down, whose input is that expert's hidden state), and
+``r_e`` is the expert's compensation rank.  Written as the literal loop.
+"""
+
+import numpy as np
+
+from . import linear
+
+
+def forward(experts, ranks, X, ids, x_per_slot):
+    """``experts[e] = (W_hat_e, A_e, B_e)`` (fp64-convertible arrays);
+    ``ranks[e]`` ints; ``X`` is ``[T][d_in]`` (shared) or ``[T][k][d_in]``
+    (per slot); ``ids`` is ``[T][k]``.  Returns fp64 ``[T][k][d_out]``."""
+    ids = np.asarray(ids)
+    T, k = ids.shape
+    d_out = np.asarray(experts[int(ids[0, 0])][0]).shape[0]
+    Y = np.zeros((T, k, d_out), dtype=np.float64)
+    for t in range(T):
+        for j in range(k):
+            e = int(ids[t, j])
+            W_hat, A, B = experts[e]
+            x = X[t, j] if x_per_slot else X[t]
+            Y[t, j] = linear.forward(W_hat, A, B, int(ranks[e]), np.asarray(x)[None, :])[0]
+    return Y

@@ -1,0 +1,123 @@
+"""Oracle: group-wise asymmetric low-bit quantization, packing and dequantization.
+
+TEST INFRASTRUCTURE ONLY (see ``oracle/__init__.py``).
+
+The paper quantizes its backbones with GPTQ (Section 5.1, Experimental Setup;
+INT4 for the MoE model, INT3 for the dense one).  GPTQ walks the columns of a
+group, rounds each to the nearest point of an asymmetric min/max grid and feeds
+the rounding error back into the not-yet-quantized columns through the inverse
+calibration Hessian.  The synthetic workloads here have no calibration data; with
+an identity Hessian the feedback term vanishes and GPTQ is plain
+round-to-nearest on the same grid.  That special case is what this module writes
+out, in fp64:
+
+  for each row ``o`` and each group ``g`` of ``G`` consecutive input columns
+    lo  = min(min_c w, 0),   hi = max(max_c w, 0)         (grid contains 0)
+    if hi == lo:  lo, hi = -1, +1                         (all-zero group)
+    s   = (hi - lo) / (2**b - 1)                          (fp64)
+    s16 = fp16 round-to-nearest-even of s, kept within [2**-24, 65504]
+    z   = clamp(rint(-lo / s16), 0, 2**b - 1)             (integer zero point)
+    q_c = clamp(rint(w_c / s16) + z, 0, 2**b - 1)         (rint: half to even)
+  dequant:  w_hat_c = s16 * (q_c - z)
+
+Codes are computed against the *stored* fp16 scale, so the kernel that
+dequantizes sees exactly the grid the codes were chosen on.  Packing is
+LSB-first: the code of column ``c`` sits in 32-bit word ``c // (32 // b)`` of its
+row at bit offset ``b * (c % (32 // b))``.
+
+Readings the paper leaves open (fixed here, listed in the design notes): RTN for
+GPTQ without calibration data; 0 inside the grid; the degenerate all-equal
+group; fp16 scale rounded once, directly from fp64; the integer zero point
+stored exactly in fp16; the clamp after ``rint`` (needed because
+``s16 < s`` can push the group maximum one step past ``2**b - 1``); a scale
+that rounds to 0 or overflows fp16 is held at the nearest finite positive fp16.
+"""
+
+import numpy as np
+
+FP16_MIN_SUBNORMAL = 2.0 ** -24
+FP16_MAX = 65504.0
+
+
+def fp16_rne(a):
+    """Round fp64 values to the nearest fp16, ties to even, in one step.
+
+    numpy converts float64 -> float16 directly (no intermediate float32), so a
+    single correctly-rounded step is what ``astype`` gives; the tests pin this
+    against a brute-force nearest-neighbour search over the fp16 grid.
+    """
+    return np.asarray(a, dtype=np.float64).astype(np.float16)
+
+
+def quantize(W, bits, group_size):
+    """Quantize ``W`` (``d_out x d_in``, float32 values) group-wise along d_in.
+
+    Returns ``(codes, scales, zeros)``: codes as int64 ``[d_out][d_in]``,
+    scales and zeros as float16 ``[d_out][d_in // group_size]``.
+    """
+    W = np.asarray(W)
+    d_out, d_in = W.shape
+    G = int(group_size)
+    if d_in % G:
+        raise ValueError("d_in must be a multiple of the group size")
+    qmax = (1 << bits) - 1
+    Wg = W.astype(np.float64).reshape(d_out, d_in // G, G)
+
+    lo = np.minimum(Wg.min(axis=2), 0.0)
+    hi = np.maximum(Wg.max(axis=2), 0.0)
+    flat = hi == lo
+    lo = np.where(flat, -1.0, lo)
+    hi = np.where(flat, 1.0, hi)
+
+    s = (hi - lo) / qmax
+    s16 = fp16_rne(s).astype(np.float64)
+    s16 = np.clip(s16, FP16_MIN_SUBNORMAL, FP16_MAX)
+
+    z = np.clip(np.rint(-lo / s16), 0, qmax)
+    q = np.clip(np.rint(Wg / s16[:, :, None]) + z[:, :, None], 0, qmax)
+
+    codes = q.reshape(d_out, d_in).astype(np.int64)
+    return codes, s16.astype(np.float16), z.astype(np.float16)
+
+
+def pack(codes, bits):
+    """Pack integer codes ``[d_out][d_in]`` LSB-first into uint32 words."""
+    codes = np.asarray(codes, dtype=np.uint64)
+    d_out, d_in = codes.shape
+    per_word = 32 // bits
+    if d_in % per_word:
+        raise ValueError("d_in must be a multiple of 32 / bits")
+    c = codes.reshape(d_out, d_in // per_word, per_word)
+    shifts = (np.arange(per_word, dtype=np.uint64) * np.uint64(bits))
+    words = (c << shifts).sum(axis=2, dtype=np.uint64)
+    return words.astype(np.uint32)
+
+
+def unpack(Q, bits, d_in):
+    """Inverse of :func:`pack`: uint32 ``[d_out][d_in*bits/32]`` -> int64 codes."""
+    Q = np.asarray(Q, dtype=np.uint32)
+    per_word = 32 // bits
+    col = np.arange(d_in)
+    shift = (bits * (col % per_word)).astype(np.uint32)
+    words = Q[:, col // per_word]
+    return ((words >> shift) & np.uint32((1 << bits) - 1)).astype(np.int64)
+
+
+def dequant(codes, scales, zeros, group_size):
+    """``w_hat = s16 * (q - z)`` in fp64 (exact: every value fits in fp32 too)."""
+    codes = np.asarray(codes, dtype=np.float64)
+    g = np.arange(codes.shape[1]) // int(group_size)
+    s = np.asarray(scales, dtype=np.float64)[:, g]
+    z = np.asarray(zeros, dtype=np.float64)[:, g]
+    return s * (codes - z)
+
+
+def quantize_pack(W, bits, group_size):
+    """Quantize then pack: returns ``(Q uint32, scales fp16, zeros fp16)``."""
+    codes, s, z = quantize(W, bits, group_size)
+    return pack(codes, bits), s, z
+
+
+def dequant_packed(Q, scales, zeros, bits, group_size, d_in):
+    """Unpack then dequantize a packed weight to fp64 ``[d_out][d_in]``."""
+    return dequant(unpack(Q, bits, d_in), scales, zeros, group_size)
