@@ -1,0 +1,155 @@
+/*
+ * cl.h -- C ABI of the error-compensated quantized linear layer for AMD
+ * MI355X (gfx950).
+ *
+ * The layer (HCInfer, arXiv 2605.05819, Section 4.1, Theoretical Framework)
+ * replaces a linear layer by a low-bit backbone plus a low-rank correction of
+ * its quantization error.  With column vectors and the weight stored
+ * d_out x d_in, every token x computes
+ *
+ *     y = deq(Q, scales, zeros) x + B[:, :r] (A[:r, :] x)
+ *
+ * where deq(Q, s, z)[o][c] = s[o][c/G] * (q[o][c] - z[o][c/G]) and A, B are
+ * the leading factors of the SVD of W - deq(Q) (sorted by descending singular
+ * value, so every prefix rank r <= r_max is the optimal rank-r correction).
+ *
+ * Conventions for every entry point
+ * ---------------------------------
+ *  - Pointers marked "device" point to device memory of the current HIP
+ *    device; the caller allocates and frees all of it.  The library allocates
+ *    nothing on these calls and keeps no pointer after returning.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *    Calls only enqueue work and return; buffers must stay alive until the
+ *    stream has executed it.
+ *  - Descriptor structs are read during the call and may be reused at once.
+ *  - Arrays are row-major and densely packed.
+ *  - Arguments are validated before anything is enqueued.  On a non-zero
+ *    status nothing was enqueued and cl_last_error() describes the problem.
+ *    No call aborts or throws.
+ *
+ * Packed backbone layout (cl_qweight)
+ * -----------------------------------
+ *  q       uint32 [d_out][d_in * bits / 32]; the code of column c is in word
+ *          c / (32/bits) of its row at bit offset bits * (c % (32/bits))
+ *          (LSB first).  16-byte aligned.
+ *  scales  fp16   [d_out][d_in / group_size], the group's step size.
+ *  zeros   fp16   [d_out][d_in / group_size], integer zero point 0..2^bits-1.
+ *  bits in {2, 4}; group_size a multiple of 128/bits (a 16-byte run of codes
+ *  never straddles two groups); d_in a multiple of group_size.
+ *
+ * Compensation factors (cl_lowrank)
+ * ---------------------------------
+ *  A  fp16 [r_max][d_in]   (rows 0..rank-1 are used)
+ *  B  fp16 [d_out][r_max]  (columns 0..rank-1 of every row are used)
+ *  0 <= rank <= r_max <= 256.  With rank == 0, A and B may be NULL.
+ */
+#ifndef CL_H_
+#define CL_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t cl_status;
+enum {
+    CL_OK = 0,
+    CL_EINVAL = 1,        /* bad argument: null pointer, bad size, misalignment */
+    CL_EUNSUPPORTED = 2,  /* well-formed but not implemented (e.g. bits = 3)    */
+    CL_EWORKSPACE = 3,    /* workspace missing or smaller than required         */
+    CL_EHIP = 4           /* the HIP runtime reported an error at launch        */
+};
+
+/* Element types of activations and outputs. */
+enum { CL_FP16 = 1, CL_BF16 = 2, CL_FP32 = 3 };
+
+typedef struct cl_qweight {
+    const uint32_t* q;        /* device */
+    const uint16_t* scales;   /* device, fp16 bits */
+    const uint16_t* zeros;    /* device, fp16 bits */
+    int32_t d_out;
+    int32_t d_in;
+    int32_t bits;
+    int32_t group_size;
+} cl_qweight;
+
+typedef struct cl_lowrank {
+    const uint16_t* A;        /* device, fp16 bits, [r_max][d_in]  */
+    const uint16_t* B;        /* device, fp16 bits, [d_out][r_max] */
+    int32_t r_max;
+    int32_t rank;
+} cl_lowrank;
+
+/*
+ * cl_quantize_pack -- quantize a float32 weight group-wise and pack it.
+ *
+ * Section 5.1 quantizes the backbone with GPTQ; without calibration data GPTQ
+ * is round-to-nearest on an asymmetric per-group min/max grid, computed here in
+ * fp64 and bit-exact with that definition:
+ *   lo = min(min w, 0), hi = max(max w, 0); an all-equal group uses [-1, 1];
+ *   s16 = fp16(round-to-nearest-even((hi - lo) / (2^bits - 1))), kept within
+ *         [2^-24, 65504];
+ *   z = clamp(rint(-lo / s16), 0, 2^bits - 1);
+ *   q = clamp(rint(w / s16) + z, 0, 2^bits - 1)   (rint: ties to even).
+ *
+ *  W       device float32 [d_out][d_in] (input, finite values)
+ *  q       device uint32  [d_out][d_in*bits/32] (output, 16-byte aligned)
+ *  scales, zeros  device fp16 [d_out][d_in/group_size] (outputs)
+ * Errors: CL_EINVAL for null pointers, non-positive sizes, misaligned q or a
+ * group_size / d_in that breaks the layout rules above; CL_EUNSUPPORTED for
+ * bits other than 2 and 4.
+ */
+cl_status cl_quantize_pack(const float* W, int32_t d_out, int32_t d_in, int32_t bits,
+                           int32_t group_size, uint32_t* q, uint16_t* scales, uint16_t* zeros,
+                           void* stream);
+
+/*
+ * cl_dequantize -- W_hat[o][c] = s[o][c/G] * (q[o][c] - z[o][c/G]) as float32
+ * (exact: an fp16 step times a small integer fits float32).
+ *  W_hat   device float32 [d_out][d_in] (output)
+ * Errors: as cl_quantize_pack.
+ */
+cl_status cl_dequantize(const cl_qweight* w, float* W_hat, void* stream);
+
+/*
+ * cl_linear_workspace -- bytes of device workspace that cl_linear_decode needs
+ * for this weight, factor set and token count (0 if none).  Returns 0 as well
+ * for arguments cl_linear_decode would reject.
+ */
+size_t cl_linear_workspace(const cl_qweight* w, const cl_lowrank* c, int32_t tokens);
+
+/*
+ * cl_linear_decode -- compensated linear for a few decode tokens (Section 4.1):
+ *     y[t] = deq(Q) x[t] + B[:, :rank] (A[:rank] x[t]),   t = 0..T-1.
+ * The backbone's unpack, dequantize and dot products run in one memory-bound
+ * kernel that also folds in the rank-r up-projection; A x is formed first.
+ * Accumulation is float32; the result is rounded once to out_dtype.
+ *
+ *  w, c       the packed backbone and its factors (c may be NULL for rank 0)
+ *  x          device [T][d_in] of act_dtype (CL_FP16 or CL_BF16), 16-byte
+ *             aligned.  bf16 activations are read as fp16: exact for
+ *             2^-17 <= |x| <= 65504, rounded to a multiple of 2^-24 below
+ *             that range and saturated above it.
+ *  T          1..64 tokens
+ *  y          device [T][d_out] of out_dtype (CL_FP16, CL_BF16 or CL_FP32)
+ *  ws         device workspace of at least cl_linear_workspace(w, c, T) bytes
+ *             (may be NULL when that is 0); 256-byte aligned
+ * Errors: CL_EINVAL / CL_EUNSUPPORTED for bad descriptors, dtypes or T,
+ * CL_EWORKSPACE for a missing or short workspace, CL_EHIP on launch failure.
+ * Calls on one stream are ordered; concurrent calls must use separate
+ * workspaces.
+ */
+cl_status cl_linear_decode(const cl_qweight* w, const cl_lowrank* c, const void* x, int32_t T,
+                           int32_t act_dtype, void* y, int32_t out_dtype, void* ws,
+                           size_t ws_bytes, void* stream);
+
+/* Message describing the last non-CL_OK status returned on this thread. */
+const char* cl_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CL_H_ */

@@ -1,0 +1,159 @@
+"""Thin Python binding of ``libcl.so`` (the C ABI declared in ``include/cl.h``).
+
+Argument marshalling only: every step of the layer runs in the HIP kernels of
+the library.  PyTorch provides device memory and the current stream.  If the
+library has not been built, :func:`lib` raises -- there is no fallback path.
+"""
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional
+
+import torch
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libcl.so")
+
+CL_OK, CL_EINVAL, CL_EUNSUPPORTED, CL_EWORKSPACE, CL_EHIP = range(5)
+CL_FP16, CL_BF16, CL_FP32 = 1, 2, 3
+STATUS_NAMES = {0: "CL_OK", 1: "CL_EINVAL", 2: "CL_EUNSUPPORTED", 3: "CL_EWORKSPACE", 4: "CL_EHIP"}
+
+_DTYPE_CODE = {torch.float16: CL_FP16, torch.bfloat16: CL_BF16, torch.float32: CL_FP32}
+
+
+class ClError(RuntimeError):
+    def __init__(self, status, message):
+        super().__init__("%s: %s" % (STATUS_NAMES.get(status, status), message))
+        self.status = status
+
+
+class QWeightC(ctypes.Structure):
+    _fields_ = [("q", ctypes.c_void_p), ("scales", ctypes.c_void_p), ("zeros", ctypes.c_void_p),
+                ("d_out", ctypes.c_int32), ("d_in", ctypes.c_int32), ("bits", ctypes.c_int32),
+                ("group_size", ctypes.c_int32)]
+
+
+class LowRankC(ctypes.Structure):
+    _fields_ = [("A", ctypes.c_void_p), ("B", ctypes.c_void_p), ("r_max", ctypes.c_int32),
+                ("rank", ctypes.c_int32)]
+
+
+_lib = None
+
+_SIGNATURES = {
+    "cl_last_error": (ctypes.c_char_p, []),
+    "cl_quantize_pack": (ctypes.c_int32, [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                          ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                          ctypes.c_void_p]),
+    "cl_dequantize": (ctypes.c_int32, [ctypes.POINTER(QWeightC), ctypes.c_void_p, ctypes.c_void_p]),
+    "cl_linear_workspace": (ctypes.c_size_t, [ctypes.POINTER(QWeightC), ctypes.POINTER(LowRankC), ctypes.c_int32]),
+    "cl_linear_decode": (ctypes.c_int32, [ctypes.POINTER(QWeightC), ctypes.POINTER(LowRankC), ctypes.c_void_p,
+                                          ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32,
+                                          ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
+}
+
+
+def lib():
+    """The loaded library (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError("libcl.so is not built; run `python -m paper_2605_05819_amd.build`")
+        handle = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGNATURES.items():
+            fn = getattr(handle, name)
+            fn.restype, fn.argtypes = res, args
+        _lib = handle
+    return _lib
+
+
+def _check(status):
+    if status != CL_OK:
+        raise ClError(status, lib().cl_last_error().decode())
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+@dataclass
+class QWeight:
+    """A packed backbone on the device: q uint32-as-int32 [d_out][d_in*bits/32],
+    scales/zeros fp16 [d_out][d_in/group_size]."""
+    q: torch.Tensor
+    scales: torch.Tensor
+    zeros: torch.Tensor
+    d_out: int
+    d_in: int
+    bits: int
+    group_size: int
+
+    def c(self):
+        return QWeightC(self.q.data_ptr(), self.scales.data_ptr(), self.zeros.data_ptr(),
+                        self.d_out, self.d_in, self.bits, self.group_size)
+
+
+@dataclass
+class LowRank:
+    """Compensation factors on the device: A fp16 [r_max][d_in], B fp16
+    [d_out][r_max]; ``rank`` leading factors are applied."""
+    A: Optional[torch.Tensor]
+    B: Optional[torch.Tensor]
+    r_max: int
+    rank: int
+
+    def c(self):
+        return LowRankC(0 if self.A is None else self.A.data_ptr(),
+                        0 if self.B is None else self.B.data_ptr(), self.r_max, self.rank)
+
+
+def quantize_pack(W, bits, group_size, stream=None):
+    """``cl_quantize_pack`` on a float32 device tensor; returns a QWeight."""
+    d_out, d_in = W.shape
+    dev = W.device
+    q = torch.empty((d_out, d_in * bits // 32), dtype=torch.int32, device=dev)
+    s = torch.empty((d_out, d_in // group_size), dtype=torch.float16, device=dev)
+    z = torch.empty_like(s)
+    _check(lib().cl_quantize_pack(_ptr(W), d_out, d_in, bits, group_size, _ptr(q), _ptr(s), _ptr(z),
+                                  _stream(stream)))
+    return QWeight(q, s, z, d_out, d_in, bits, group_size)
+
+
+def dequantize(w, stream=None):
+    out = torch.empty((w.d_out, w.d_in), dtype=torch.float32, device=w.q.device)
+    qc = w.c()
+    _check(lib().cl_dequantize(ctypes.byref(qc), _ptr(out), _stream(stream)))
+    return out
+
+
+def linear_workspace(w, c, tokens):
+    qc = w.c()
+    lc = c.c() if c is not None else None
+    return lib().cl_linear_workspace(ctypes.byref(qc), ctypes.byref(lc) if lc else None, tokens)
+
+
+def workspace(nbytes, device):
+    """A device workspace of at least ``nbytes`` (256-byte aligned by torch)."""
+    return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device)
+
+
+def linear_decode(w, c, x, out_dtype=torch.float16, y=None, ws=None, stream=None):
+    """``cl_linear_decode``: x [T][d_in] fp16/bf16 -> y [T][d_out] of out_dtype."""
+    T = x.shape[0]
+    if y is None:
+        y = torch.empty((T, w.d_out), dtype=out_dtype, device=x.device)
+    need = linear_workspace(w, c, T)
+    if ws is None and need:
+        ws = workspace(need, x.device)
+    qc = w.c()
+    lc = c.c() if c is not None else None
+    _check(lib().cl_linear_decode(ctypes.byref(qc), ctypes.byref(lc) if lc else None, _ptr(x), T,
+                                  _DTYPE_CODE[x.dtype], _ptr(y), _DTYPE_CODE[y.dtype], _ptr(ws),
+                                  0 if ws is None else ws.numel(), _stream(stream)))
+    return y

@@ -1,0 +1,134 @@
+// C ABI of the compensated quantized linear: argument validation, workspace
+// sizing, error reporting and dispatch to the gfx950 kernels.  Nothing here
+// touches the HIP runtime before every argument has been checked, so invalid
+// calls return an error without enqueuing work (and without needing a GPU).
+
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "../../include/cl.h"
+#include "cl_internal.h"
+
+namespace {
+
+thread_local char g_err[512] = "no error";
+
+cl_status fail(cl_status code, const char* fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof(g_err), fmt, ap);
+    va_end(ap);
+    return code;
+}
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+cl_status check_shape(int d_out, int d_in, int bits, int G, const char* who) {
+    if (bits == 3) return fail(CL_EUNSUPPORTED, "%s: 3-bit packing is not implemented", who);
+    if (bits != 2 && bits != 4) return fail(CL_EUNSUPPORTED, "%s: bits must be 2 or 4 (got %d)", who, bits);
+    if (d_out <= 0 || d_in <= 0) return fail(CL_EINVAL, "%s: d_out and d_in must be positive", who);
+    const int run = 128 / bits;   // codes in one 16-byte run
+    if (G <= 0 || G % run) return fail(CL_EINVAL, "%s: group_size must be a positive multiple of %d for %d-bit codes (got %d)", who, run, bits, G);
+    if (d_in % G) return fail(CL_EINVAL, "%s: d_in (%d) must be a multiple of group_size (%d)", who, d_in, G);
+    return CL_OK;
+}
+
+cl_status check_qweight(const cl_qweight* w, cl::QW* out, const char* who) {
+    if (!w) return fail(CL_EINVAL, "%s: null weight descriptor", who);
+    cl_status st = check_shape(w->d_out, w->d_in, w->bits, w->group_size, who);
+    if (st) return st;
+    if (!w->q || !w->scales || !w->zeros) return fail(CL_EINVAL, "%s: null q/scales/zeros pointer", who);
+    if (!aligned(w->q, 16)) return fail(CL_EINVAL, "%s: q must be 16-byte aligned", who);
+    if (!aligned(w->scales, 2) || !aligned(w->zeros, 2)) return fail(CL_EINVAL, "%s: scales/zeros must be 2-byte aligned", who);
+    *out = {w->q, w->scales, w->zeros, w->d_out, w->d_in, w->bits, w->group_size};
+    return CL_OK;
+}
+
+cl_status check_lowrank(const cl_lowrank* c, const cl::QW& w, cl::LR* out, const char* who) {
+    *out = {nullptr, nullptr, 0, 0};
+    if (!c) return CL_OK;   // no compensation
+    if (c->rank < 0 || c->r_max < 0 || c->rank > c->r_max || c->r_max > 256)
+        return fail(CL_EINVAL, "%s: need 0 <= rank <= r_max <= 256 (rank %d, r_max %d)", who, c->rank, c->r_max);
+    if (c->rank == 0) return CL_OK;
+    if (!c->A || !c->B) return fail(CL_EINVAL, "%s: null A or B with rank %d", who, c->rank);
+    if (!aligned(c->A, 16)) return fail(CL_EINVAL, "%s: A must be 16-byte aligned", who);
+    if (!aligned(c->B, 2)) return fail(CL_EINVAL, "%s: B must be 2-byte aligned", who);
+    (void)w;
+    *out = {c->A, c->B, c->r_max, c->rank};
+    return CL_OK;
+}
+
+cl_status hip_status(hipError_t e, const char* who) {
+    if (e == hipSuccess) return CL_OK;
+    return fail(CL_EHIP, "%s: HIP error %d (%s)", who, static_cast<int>(e), hipGetErrorString(e));
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* cl_last_error(void) { return g_err; }
+
+cl_status cl_quantize_pack(const float* W, int32_t d_out, int32_t d_in, int32_t bits, int32_t group_size,
+                           uint32_t* q, uint16_t* scales, uint16_t* zeros, void* stream) {
+    const char* who = "cl_quantize_pack";
+    cl_status st = check_shape(d_out, d_in, bits, group_size, who);
+    if (st) return st;
+    if (!W || !q || !scales || !zeros) return fail(CL_EINVAL, "%s: null pointer argument", who);
+    if (!aligned(W, 4) || !aligned(q, 16) || !aligned(scales, 2) || !aligned(zeros, 2))
+        return fail(CL_EINVAL, "%s: misaligned buffer (W 4, q 16, scales/zeros 2 bytes)", who);
+    return hip_status(cl::launch_quantize_pack(W, d_out, d_in, bits, group_size, q, scales, zeros,
+                                               static_cast<hipStream_t>(stream)), who);
+}
+
+cl_status cl_dequantize(const cl_qweight* w, float* W_hat, void* stream) {
+    const char* who = "cl_dequantize";
+    cl::QW qw;
+    cl_status st = check_qweight(w, &qw, who);
+    if (st) return st;
+    if (!W_hat || !aligned(W_hat, 4)) return fail(CL_EINVAL, "%s: null or misaligned output", who);
+    return hip_status(cl::launch_dequantize(qw, W_hat, static_cast<hipStream_t>(stream)), who);
+}
+
+size_t cl_linear_workspace(const cl_qweight* w, const cl_lowrank* c, int32_t tokens) {
+    char saved[sizeof(g_err)];
+    memcpy(saved, g_err, sizeof(g_err));
+    cl::QW qw;
+    cl::LR lr;
+    size_t n = 0;
+    if (tokens >= 1 && check_qweight(w, &qw, "") == CL_OK && check_lowrank(c, qw, &lr, "") == CL_OK)
+        n = cl::decode_workspace_bytes(qw, lr, tokens);
+    memcpy(g_err, saved, sizeof(g_err));   // a size query leaves the last error alone
+    return n;
+}
+
+cl_status cl_linear_decode(const cl_qweight* w, const cl_lowrank* c, const void* x, int32_t T,
+                           int32_t act_dtype, void* y, int32_t out_dtype, void* ws, size_t ws_bytes,
+                           void* stream) {
+    const char* who = "cl_linear_decode";
+    cl::QW qw;
+    cl::LR lr;
+    cl_status st = check_qweight(w, &qw, who);
+    if (st) return st;
+    st = check_lowrank(c, qw, &lr, who);
+    if (st) return st;
+    if (T < 1 || T > 64) return fail(CL_EINVAL, "%s: T must be in 1..64 (got %d)", who, T);
+    if (act_dtype != CL_FP16 && act_dtype != CL_BF16)
+        return fail(CL_EINVAL, "%s: act_dtype must be CL_FP16 or CL_BF16", who);
+    if (out_dtype != CL_FP16 && out_dtype != CL_BF16 && out_dtype != CL_FP32)
+        return fail(CL_EINVAL, "%s: out_dtype must be CL_FP16, CL_BF16 or CL_FP32", who);
+    if (!x || !y) return fail(CL_EINVAL, "%s: null x or y", who);
+    if (!aligned(x, 16)) return fail(CL_EINVAL, "%s: x must be 16-byte aligned", who);
+    if (!aligned(y, out_dtype == CL_FP32 ? 4 : 2)) return fail(CL_EINVAL, "%s: misaligned y", who);
+    if (!cl::decode_fits(qw, lr))
+        return fail(CL_EUNSUPPORTED, "%s: d_in %d with rank %d does not fit the staged activations", who, qw.d_in, lr.rank);
+    const size_t need = cl::decode_workspace_bytes(qw, lr, T);
+    if (need > 0 && (!ws || ws_bytes < need))
+        return fail(CL_EWORKSPACE, "%s: workspace of %zu bytes needed (got %zu)", who, need, ws ? ws_bytes : 0);
+    if (need > 0 && !aligned(ws, 256)) return fail(CL_EINVAL, "%s: workspace must be 256-byte aligned", who);
+    return hip_status(cl::launch_linear_decode(qw, lr, x, T, act_dtype, y, out_dtype, ws,
+                                               static_cast<hipStream_t>(stream)), who);
+}
+
+}  // extern "C"

@@ -1,0 +1,87 @@
+// Device-side helpers shared by the gfx950 kernels of the compensated linear.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace cl {
+
+typedef _Float16 f16;
+typedef f16 f16x2 __attribute__((ext_vector_type(2)));
+typedef f16 f16x8 __attribute__((ext_vector_type(8)));
+typedef short bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+enum { DT_FP16 = 1, DT_BF16 = 2, DT_FP32 = 3 };
+
+__device__ __forceinline__ float f16_bits_to_f32(uint16_t b) {
+    return static_cast<float>(__builtin_bit_cast(f16, b));
+}
+
+__device__ __forceinline__ float bf16_bits_to_f32(uint16_t b) {
+    return __builtin_bit_cast(float, static_cast<uint32_t>(b) << 16);
+}
+
+// float -> bf16, round to nearest, ties to even (NaN kept quiet).
+__device__ __forceinline__ uint16_t f32_to_bf16_bits(float f) {
+    uint32_t u = __builtin_bit_cast(uint32_t, f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<uint16_t>((u >> 16) | 0x40);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return static_cast<uint16_t>(u >> 16);
+}
+
+__device__ __forceinline__ uint16_t f32_to_f16_bits(float f) {
+    return __builtin_bit_cast(uint16_t, static_cast<f16>(f));
+}
+
+// An activation element as fp16.  bf16 inputs are converted (exact inside the
+// fp16 range down to 2^-17, saturated at +-65504 above it).
+__device__ __forceinline__ f16 act_to_f16(uint16_t b, int act) {
+    if (act == DT_FP16) return __builtin_bit_cast(f16, b);
+    float v = bf16_bits_to_f32(b);
+    v = fminf(fmaxf(v, -65504.0f), 65504.0f);
+    return static_cast<f16>(v);
+}
+
+__device__ __forceinline__ float act_to_f32(uint16_t b, int act) {
+    return act == DT_FP16 ? f16_bits_to_f32(b) : bf16_bits_to_f32(b);
+}
+
+__device__ __forceinline__ void store_out(void* y, size_t idx, float v, int out) {
+    if (out == DT_FP32) {
+        static_cast<float*>(y)[idx] = v;
+    } else if (out == DT_FP16) {
+        static_cast<uint16_t*>(y)[idx] = f32_to_f16_bits(v);
+    } else {
+        static_cast<uint16_t*>(y)[idx] = f32_to_bf16_bits(v);
+    }
+}
+
+// v_dot2_f32_f16: a.x*b.x + a.y*b.y + c with float accumulation.
+__device__ __forceinline__ float dot2(f16x2 a, f16x2 b, float c) {
+    return __builtin_amdgcn_fdot2(a, b, c, false);
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+    return v;
+}
+
+// Packed-code extraction into fp16 lanes.
+//
+// A 4-bit code q placed in the low mantissa bits of an fp16 with a zero
+// exponent field is the subnormal q * 2^-24, exactly.  Masking one 32-bit word
+// with 0x000F000F after a right shift by 4p therefore yields the pair
+// (q_p, q_{p+4}) * 2^-24 as two fp16 lanes in a single AND; the 2-bit layout
+// works the same way with mask 0x00030003 and pairs (q_p, q_{p+8}).  Products
+// with fp16 activations are exact in the float accumulator of v_dot2, and the
+// 2^24 is folded into the per-group scale.
+template <int BITS>
+__device__ __forceinline__ f16x2 code_pair(uint32_t w, int p) {
+    constexpr uint32_t mask = BITS == 4 ? 0x000F000Fu : 0x00030003u;
+    return __builtin_bit_cast(f16x2, (w >> (BITS * p)) & mask);
+}
+
+}  // namespace cl

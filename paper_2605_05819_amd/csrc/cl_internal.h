@@ -1,0 +1,35 @@
+// Host-side launchers shared between the ABI layer (api.hip) and the kernel
+// translation units.  Arguments reaching these functions are already
+// validated; each returns the hipError_t of its launch.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace cl {
+
+struct QW {                    // packed backbone, validated
+    const uint32_t* q;
+    const uint16_t* s;
+    const uint16_t* z;
+    int d_out, d_in, bits, G;
+};
+
+struct LR {                    // compensation factors, validated (rank may be 0)
+    const uint16_t* A;
+    const uint16_t* B;
+    int r_max, rank;
+};
+
+hipError_t launch_quantize_pack(const float* W, int d_out, int d_in, int bits, int G, uint32_t* q,
+                                uint16_t* s, uint16_t* z, hipStream_t st);
+hipError_t launch_dequantize(const QW& w, float* out, hipStream_t st);
+
+// Workspace layout of the decode path: t = A[:rank] x as float [T][rank].
+size_t decode_workspace_bytes(const QW& w, const LR& c, int T);
+bool decode_fits(const QW& w, const LR& c);   // activations of one token fit in LDS
+hipError_t launch_linear_decode(const QW& w, const LR& c, const void* x, int T, int act, void* y,
+                                int out, void* ws, hipStream_t st);
+
+}  // namespace cl

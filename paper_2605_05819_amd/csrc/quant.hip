@@ -1,0 +1,118 @@
+// Group-wise asymmetric round-to-nearest quantization + LSB-first packing, and
+// the matching dequantization, for gfx950.
+//
+// The backbone quantizer of the paper is GPTQ (Section 5.1); without
+// calibration data its error feedback vanishes and it is round-to-nearest on a
+// per-group min/max grid that contains 0.  Every step runs in fp64 with IEEE
+// division and round-half-to-even, and the fp16 scale is rounded once,
+// directly from fp64, so the codes are bit-identical to that definition.
+// This file is compiled with -ffp-contract=off.
+
+#include "cl_device.h"
+#include "cl_internal.h"
+
+namespace cl {
+
+// fp64 -> fp16 bits, round to nearest, ties to even, in a single rounding
+// (IEEE 754 binary16: 1 sign, 5 exponent, 10 fraction bits, bias 15).
+__device__ uint16_t f64_to_f16_rne(double v) {
+    uint64_t b = __builtin_bit_cast(uint64_t, v);
+    uint16_t sign = static_cast<uint16_t>((b >> 48) & 0x8000u);
+    double a = fabs(v);
+    if (a != a) return 0x7e00u;
+    if (a >= 65520.0) return sign | 0x7c00u;          // rounds past the largest finite value
+    int e = static_cast<int>((b >> 52) & 0x7ff) - 1023;  // a is finite, possibly subnormal in fp64
+    if (a == 0.0) return sign;
+    if (e < -14) {
+        // subnormal fp16 range: the value in units of 2^-24 (exact scaling)
+        double m = rint(a * 16777216.0);
+        return sign | static_cast<uint16_t>(m);      // m == 1024 encodes the smallest normal
+    }
+    double m = rint(ldexp(a, 10 - e));                // in [1024, 2048]
+    if (m == 2048.0) { m = 1024.0; e += 1; }
+    if (e > 15) return sign | 0x7c00u;
+    return sign | static_cast<uint16_t>(((e + 15) << 10) | (static_cast<int>(m) - 1024));
+}
+
+__device__ double f16_bits_to_f64(uint16_t h) {
+    return static_cast<double>(static_cast<float>(__builtin_bit_cast(f16, h)));
+}
+
+// One thread per (row, group).  Offline step: simple and exact over fast.
+__global__ void quantize_pack_kernel(const float* __restrict__ W, int d_out, int d_in, int bits,
+                                     int G, uint32_t* __restrict__ q, uint16_t* __restrict__ s,
+                                     uint16_t* __restrict__ z) {
+    const int groups = d_in / G;
+    const long long gid = static_cast<long long>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (gid >= static_cast<long long>(d_out) * groups) return;
+    const int o = static_cast<int>(gid / groups);
+    const int g = static_cast<int>(gid % groups);
+    const float* w = W + static_cast<size_t>(o) * d_in + static_cast<size_t>(g) * G;
+    const int qmax = (1 << bits) - 1;
+
+    double lo = 0.0, hi = 0.0;
+    for (int c = 0; c < G; ++c) {
+        double v = static_cast<double>(w[c]);
+        lo = v < lo ? v : lo;
+        hi = v > hi ? v : hi;
+    }
+    if (hi == lo) { lo = -1.0; hi = 1.0; }
+    const double step = (hi - lo) / static_cast<double>(qmax);
+    uint16_t sb = f64_to_f16_rne(step);
+    if (sb == 0) sb = 0x0001u;                 // smallest positive subnormal, 2^-24
+    if (sb >= 0x7c00u) sb = 0x7bffu;           // largest finite, 65504
+    const double s16 = f16_bits_to_f64(sb);
+    double zf = rint(-lo / s16);
+    zf = zf < 0.0 ? 0.0 : (zf > qmax ? static_cast<double>(qmax) : zf);
+
+    const size_t gi = static_cast<size_t>(o) * groups + g;
+    s[gi] = sb;
+    z[gi] = f32_to_f16_bits(static_cast<float>(zf));  // small integer: exact
+
+    const int per_word = 32 / bits;
+    uint32_t* qrow = q + static_cast<size_t>(o) * (d_in / per_word) + static_cast<size_t>(g) * (G / per_word);
+    for (int wi = 0; wi < G / per_word; ++wi) {
+        uint32_t word = 0;
+        for (int j = 0; j < per_word; ++j) {
+            double r = rint(static_cast<double>(w[wi * per_word + j]) / s16) + zf;
+            r = r < 0.0 ? 0.0 : (r > qmax ? static_cast<double>(qmax) : r);
+            word |= static_cast<uint32_t>(r) << (bits * j);
+        }
+        qrow[wi] = word;
+    }
+}
+
+__global__ void dequantize_kernel(const uint32_t* __restrict__ q, const uint16_t* __restrict__ s,
+                                  const uint16_t* __restrict__ z, int d_out, int d_in, int bits,
+                                  int G, float* __restrict__ out) {
+    const long long i = static_cast<long long>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (i >= static_cast<long long>(d_out) * d_in) return;
+    const int o = static_cast<int>(i / d_in);
+    const int c = static_cast<int>(i % d_in);
+    const int per_word = 32 / bits;
+    const uint32_t word = q[static_cast<size_t>(o) * (d_in / per_word) + c / per_word];
+    const int code = static_cast<int>((word >> (bits * (c % per_word))) & ((1u << bits) - 1u));
+    const size_t gi = static_cast<size_t>(o) * (d_in / G) + c / G;
+    out[i] = f16_bits_to_f32(s[gi]) * (static_cast<float>(code) - f16_bits_to_f32(z[gi]));
+}
+
+hipError_t launch_quantize_pack(const float* W, int d_out, int d_in, int bits, int G, uint32_t* q,
+                                uint16_t* s, uint16_t* z, hipStream_t st) {
+    const long long n = static_cast<long long>(d_out) * (d_in / G);
+    const int block = 256;
+    const unsigned grid = static_cast<unsigned>((n + block - 1) / block);
+    hipLaunchKernelGGL(quantize_pack_kernel, dim3(grid), dim3(block), 0, st, W, d_out, d_in, bits,
+                       G, q, s, z);
+    return hipGetLastError();
+}
+
+hipError_t launch_dequantize(const QW& w, float* out, hipStream_t st) {
+    const long long n = static_cast<long long>(w.d_out) * w.d_in;
+    const int block = 256;
+    const unsigned grid = static_cast<unsigned>((n + block - 1) / block);
+    hipLaunchKernelGGL(dequantize_kernel, dim3(grid), dim3(block), 0, st, w.q, w.s, w.z, w.d_out,
+                       w.d_in, w.bits, w.G, out);
+    return hipGetLastError();
+}
+
+}  // namespace cl

@@ -1,0 +1,143 @@
+"""cl_linear_decode against the fp64 oracle (Section 4.1 forward):
+relative L2 <= 1e-3 for every output dtype, across tile-spanning and ragged
+shapes, ranks, token counts, 2/4-bit codes and fp16/bf16 activations; sampled
+rows at the Llama-8B decoder-layer sizes; bitwise determinism."""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import linear, quant
+from paper_2605_05819_amd import cl, workloads as wl
+from tests.helpers import (REL_L2_TOL, dev_f16, dev_u16, dev_u32, oracle_layer, out_to_numpy, rel_l2,
+                           round_to)
+
+pytestmark = pytest.mark.gpu
+
+OUT_DTYPES = [torch.float32, torch.float16, torch.bfloat16]
+
+
+def _device_layer(Q, s, z, A, B, d_out, d_in, bits, G, r_max, rank):
+    w = cl.QWeight(dev_u32(Q), dev_f16(s), dev_f16(z), d_out, d_in, bits, G)
+    c = cl.LowRank(dev_f16(A), dev_f16(B), r_max, rank) if r_max else None
+    return w, c
+
+
+def _check(w, c, Q, s, z, A, B, rank, x, act_dtype, out_dtype, bits, G):
+    xd = dev_u16(x.bits, act_dtype)
+    y = cl.linear_decode(w, c, xd, out_dtype=out_dtype)
+    torch.cuda.synchronize()
+    ref = linear.forward_packed(Q, s, z, bits, G, A, B, rank, x.values)
+    err = rel_l2(out_to_numpy(y), round_to(ref, out_dtype))
+    assert err <= REL_L2_TOL, err
+    return y, ref
+
+
+def test_single_linear_1024_rank16_all_out_dtypes():
+    spec = wl.single_linear().linears[0]
+    W = wl.weight((spec.d_out, spec.d_in), 0)
+    Q, s, z, A, B, _ = oracle_layer(W, 4, 128, 16)
+    w, c = _device_layer(Q, s, z, A, B, 1024, 1024, 4, 128, 16, 16)
+    x = wl.activation((1, 1024), 0)
+    for od in OUT_DTYPES:
+        _check(w, c, Q, s, z, A, B, 16, x, torch.float16, od, 4, 128)
+
+
+@pytest.mark.parametrize("bits,G", [(4, 128), (2, 64), (4, 32)])
+@pytest.mark.parametrize("d_out,d_in", [(37, 256), (1000, 768), (4099, 1536)])
+@pytest.mark.parametrize("T", [1, 3, 4, 5, 16])
+def test_ragged_shapes_tokens_and_bits(bits, G, d_out, d_in, T):
+    g = np.random.default_rng(d_out + d_in + T + bits)
+    W = wl.weight((d_out, d_in), 7, d_out, d_in)
+    Q, s, z = quant.quantize_pack(W, bits, G)
+    r_max = 24
+    rank = int(g.integers(0, r_max + 1))
+    A, B = wl.standin_factors(d_out, d_in, r_max, 7, 0, d_out, d_in)
+    w, c = _device_layer(Q, s, z, A, B, d_out, d_in, bits, G, r_max, rank)
+    x = wl.activation((T, d_in), 7, 0, d_out, d_in)
+    _check(w, c, Q, s, z, A, B, rank, x, torch.float16, torch.float32, bits, G)
+
+
+@pytest.mark.parametrize("rank", [0, 1, 17, 64, 128, 256])
+def test_ranks_including_zero_and_max(rank):
+    d_out, d_in = 512, 1024
+    W = wl.weight((d_out, d_in), 8, rank)
+    Q, s, z = quant.quantize_pack(W, 4, 128)
+    A, B = wl.standin_factors(d_out, d_in, 256, 8, rank)
+    w, c = _device_layer(Q, s, z, A, B, d_out, d_in, 4, 128, 256, rank)
+    x = wl.activation((2, d_in), 8, rank)
+    _check(w, c, Q, s, z, A, B, rank, x, torch.float16, torch.float16, 4, 128)
+
+
+def test_no_factors_equals_rank_zero():
+    d_out, d_in = 300, 512
+    W = wl.weight((d_out, d_in), 9)
+    Q, s, z = quant.quantize_pack(W, 4, 128)
+    A, B = wl.standin_factors(d_out, d_in, 8, 9)
+    w, c = _device_layer(Q, s, z, A, B, d_out, d_in, 4, 128, 8, 0)
+    x = dev_u16(wl.activation((1, d_in), 9).bits, torch.float16)
+    y0 = cl.linear_decode(w, c, x, out_dtype=torch.float32)
+    y1 = cl.linear_decode(w, None, x, out_dtype=torch.float32)
+    assert torch.equal(y0, y1)
+
+
+@pytest.mark.parametrize("bits,G", [(4, 128), (2, 64)])
+def test_bf16_activations(bits, G):
+    d_out, d_in = 777, 2048
+    W = wl.weight((d_out, d_in), 10, bits)
+    Q, s, z = quant.quantize_pack(W, bits, G)
+    A, B = wl.standin_factors(d_out, d_in, 32, 10, bits)
+    w, c = _device_layer(Q, s, z, A, B, d_out, d_in, bits, G, 32, 32)
+    x = wl.activation((4, d_in), 10, bits, dtype="bf16")
+    for od in OUT_DTYPES:
+        _check(w, c, Q, s, z, A, B, 32, x, torch.bfloat16, od, bits, G)
+
+
+@pytest.mark.parametrize("mat", wl.LLAMA_MATS)
+@pytest.mark.parametrize("T", [1, 4, 16])
+def test_llama_layer_full_size_sampled_rows(mat, T):
+    """Every Llama-8B layer linear at full size with its allocated rank; the
+    backbone is quantized on the GPU and rows sampled over the whole output
+    are checked against the oracle, which quantizes those rows itself."""
+    layer = wl.llama_layer()
+    spec = [l for l in layer.linears if l.name == mat][0]
+    m = wl.LLAMA_MATS.index(mat)
+    W = wl.weight((spec.d_out, spec.d_in), layer.index, 0, m)
+    w = cl.quantize_pack(torch.from_numpy(W).cuda(), 4, 128)
+    A, B = wl.standin_factors(spec.d_out, spec.d_in, spec.r_max, layer.index, 0, m)
+    c = cl.LowRank(dev_f16(A), dev_f16(B), spec.r_max, spec.rank)
+    x = wl.activation((T, spec.d_in), layer.index, 0, m)
+    y = cl.linear_decode(w, c, dev_u16(x.bits, torch.float16), out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    rows = np.r_[0:4, np.random.default_rng(m).choice(spec.d_out, 120, replace=False), spec.d_out - 4:spec.d_out]
+    Q, s, z = quant.quantize_pack(W[rows], 4, 128)
+    ref = linear.forward_packed(Q, s, z, 4, 128, A, B[rows], spec.rank, x.values)
+    assert rel_l2(out_to_numpy(y)[:, rows], ref) <= REL_L2_TOL
+
+
+def test_2bit_gate_rank_sweep_sampled_rows():
+    layer = wl.llama_layer_2bit()
+    W = wl.weight((14336, 4096), layer.index, 0, 4)
+    w = cl.quantize_pack(torch.from_numpy(W).cuda(), 2, 64)
+    A, B = wl.standin_factors(14336, 4096, 256, layer.index, 0, 4)
+    x = wl.activation((1, 4096), layer.index, 0, 4)
+    rows = np.random.default_rng(5).choice(14336, 100, replace=False)
+    Q, s, z = quant.quantize_pack(W[rows], 2, 64)
+    for rank in (0, 32, 128, 256):
+        c = cl.LowRank(dev_f16(A), dev_f16(B), 256, rank)
+        y = cl.linear_decode(w, c, dev_u16(x.bits, torch.float16), out_dtype=torch.float32)
+        torch.cuda.synchronize()
+        ref = linear.forward_packed(Q, s, z, 2, 64, A, B[rows], rank, x.values)
+        assert rel_l2(out_to_numpy(y)[:, rows], ref) <= REL_L2_TOL
+
+
+def test_deterministic_bitwise():
+    d_out, d_in = 4096, 4096
+    W = wl.weight((d_out, d_in), 11)
+    w = cl.quantize_pack(torch.from_numpy(W).cuda(), 4, 128)
+    A, B = wl.standin_factors(d_out, d_in, 64, 11)
+    c = cl.LowRank(dev_f16(A), dev_f16(B), 64, 64)
+    x = dev_u16(wl.activation((4, d_in), 11).bits, torch.float16)
+    y1 = cl.linear_decode(w, c, x, out_dtype=torch.float32)
+    y2 = cl.linear_decode(w, c, x, out_dtype=torch.float32)
+    assert torch.equal(y1, y2)
