@@ -115,17 +115,19 @@ cl_status cl_dequantize(const cl_qweight* w, float* W_hat, void* stream);
 
 /*
  * cl_linear_workspace -- bytes of device workspace that cl_linear_decode needs
- * for this weight, factor set and token count (0 if none).  Returns 0 as well
- * for arguments cl_linear_decode would reject.
+ * for this weight, factor set (NULL for none) and token count.  Returns 0 for
+ * arguments cl_linear_decode would reject.
  */
 size_t cl_linear_workspace(const cl_qweight* w, const cl_lowrank* c, int32_t tokens);
 
 /*
  * cl_linear_decode -- compensated linear for a few decode tokens (Section 4.1):
  *     y[t] = deq(Q) x[t] + B[:, :rank] (A[:rank] x[t]),   t = 0..T-1.
- * The backbone's unpack, dequantize and dot products run in one memory-bound
- * kernel that also folds in the rank-r up-projection; A x is formed first.
- * Accumulation is float32; the result is rounded once to out_dtype.
+ * Two kernels are enqueued: a small one that forms A[:rank] x and the
+ * activations in the layout the backbone consumes (in the workspace), then
+ * one memory-bound kernel that unpacks, dequantizes and multiplies the
+ * backbone and folds in the rank-r up-projection B t.  Accumulation is
+ * float32; the result is rounded once to out_dtype.
  *
  *  w, c       the packed backbone and its factors (c may be NULL for rank 0)
  *  x          device [T][d_in] of act_dtype (CL_FP16 or CL_BF16), 16-byte
@@ -134,12 +136,12 @@ size_t cl_linear_workspace(const cl_qweight* w, const cl_lowrank* c, int32_t tok
  *             that range and saturated above it.
  *  T          1..64 tokens
  *  y          device [T][d_out] of out_dtype (CL_FP16, CL_BF16 or CL_FP32)
- *  ws         device workspace of at least cl_linear_workspace(w, c, T) bytes
- *             (may be NULL when that is 0); 256-byte aligned
+ *  ws         device workspace of at least cl_linear_workspace(w, c, T) bytes,
+ *             256-byte aligned.  It receives A x and the prepared
+ *             activations; calls that may overlap must use separate
+ *             workspaces.
  * Errors: CL_EINVAL / CL_EUNSUPPORTED for bad descriptors, dtypes or T,
  * CL_EWORKSPACE for a missing or short workspace, CL_EHIP on launch failure.
- * Calls on one stream are ordered; concurrent calls must use separate
- * workspaces.
  */
 cl_status cl_linear_decode(const cl_qweight* w, const cl_lowrank* c, const void* x, int32_t T,
                            int32_t act_dtype, void* y, int32_t out_dtype, void* ws,

@@ -139,8 +139,9 @@ def linear_workspace(w, c, tokens):
 
 
 def workspace(nbytes, device):
-    """A device workspace of at least ``nbytes`` (256-byte aligned by torch)."""
-    return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device)
+    """A device workspace of at least ``nbytes`` (torch allocations are
+    256-byte aligned)."""
+    return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
 
 
 def linear_decode(w, c, x, out_dtype=torch.float16, y=None, ws=None, stream=None):
@@ -148,9 +149,8 @@ def linear_decode(w, c, x, out_dtype=torch.float16, y=None, ws=None, stream=None
     T = x.shape[0]
     if y is None:
         y = torch.empty((T, w.d_out), dtype=out_dtype, device=x.device)
-    need = linear_workspace(w, c, T)
-    if ws is None and need:
-        ws = workspace(need, x.device)
+    if ws is None:
+        ws = workspace(linear_workspace(w, c, T), x.device)
     qc = w.c()
     lc = c.c() if c is not None else None
     _check(lib().cl_linear_decode(ctypes.byref(qc), ctypes.byref(lc) if lc else None, _ptr(x), T,

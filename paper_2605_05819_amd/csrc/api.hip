@@ -124,9 +124,9 @@ cl_status cl_linear_decode(const cl_qweight* w, const cl_lowrank* c, const void*
     if (!cl::decode_fits(qw, lr))
         return fail(CL_EUNSUPPORTED, "%s: d_in %d with rank %d does not fit the staged activations", who, qw.d_in, lr.rank);
     const size_t need = cl::decode_workspace_bytes(qw, lr, T);
-    if (need > 0 && (!ws || ws_bytes < need))
+    if (!ws || ws_bytes < need)
         return fail(CL_EWORKSPACE, "%s: workspace of %zu bytes needed (got %zu)", who, need, ws ? ws_bytes : 0);
-    if (need > 0 && !aligned(ws, 256)) return fail(CL_EINVAL, "%s: workspace must be 256-byte aligned", who);
+    if (!aligned(ws, 256)) return fail(CL_EINVAL, "%s: workspace must be 256-byte aligned", who);
     return hip_status(cl::launch_linear_decode(qw, lr, x, T, act_dtype, y, out_dtype, ws,
                                                static_cast<hipStream_t>(stream)), who);
 }

@@ -91,8 +91,8 @@ def test_workspace_query_is_pure_and_sized_by_rank_and_tokens():
     lr = cl.LowRankC(FAKE, FAKE, 64, 32)
     n1 = lib.cl_linear_workspace(ctypes.byref(qw), ctypes.byref(lr), 1)
     n4 = lib.cl_linear_workspace(ctypes.byref(qw), ctypes.byref(lr), 4)
-    assert n1 >= 32 * 4 and n4 >= 4 * n1 - 1
-    assert lib.cl_linear_workspace(ctypes.byref(qw), None, 4) >= 0
+    assert n1 >= 32 * 4 and n4 - n1 >= 3 * 32 * 4       # A x for every token
+    assert 0 < lib.cl_linear_workspace(ctypes.byref(qw), None, 4) < n4     # rank 0: activations only
     assert lib.cl_linear_workspace(ctypes.byref(_qw(bits=3)), ctypes.byref(lr), 1) == 0
     assert lib.cl_last_error() == before
 

@@ -141,3 +141,46 @@ def test_deterministic_bitwise():
     y1 = cl.linear_decode(w, c, x, out_dtype=torch.float32)
     y2 = cl.linear_decode(w, c, x, out_dtype=torch.float32)
     assert torch.equal(y1, y2)
+
+
+def _layer_dev(d_out, d_in, bits, G, r_max, rank, seed):
+    W = wl.weight((d_out, d_in), 12, seed)
+    Q, s, z = quant.quantize_pack(W, bits, G)
+    A, B = wl.standin_factors(d_out, d_in, r_max, 12, seed)
+    w, c = _device_layer(Q, s, z, A, B, d_out, d_in, bits, G, r_max, rank)
+    return w, c, (Q, s, z, A, B)
+
+
+def test_one_workspace_reused_across_shapes_ranks_and_token_counts():
+    """One workspace serves consecutive calls of different shapes, ranks and
+    token counts."""
+    cases = [(4096, 4096, 64, 1), (37, 512, 8, 3), (14336, 4096, 128, 4), (5, 256, 256, 2),
+             (4096, 14336, 32, 1), (4096, 4096, 64, 5)]
+    ws = cl.workspace(1 << 20, "cuda")
+    for i, (d_out, d_in, rank, T) in enumerate(cases):
+        w, c, (Q, s, z, A, B) = _layer_dev(d_out, d_in, 4, 128, 256, rank, i)
+        x = wl.activation((T, d_in), 12, i)
+        y = cl.linear_decode(w, c, dev_u16(x.bits, torch.float16), out_dtype=torch.float32, ws=ws)
+        rows = np.arange(d_out) if d_out < 512 else np.random.default_rng(i).choice(d_out, 256, replace=False)
+        ref = linear.forward_rows(Q, s, z, 4, 128, A, B, rank, x.values, rows)
+        assert rel_l2(out_to_numpy(y)[:, rows], ref) <= REL_L2_TOL, (d_out, d_in, rank, T)
+
+
+def test_few_rows_many_factor_rows():
+    """Three output rows against 256 factor rows."""
+    w, c, (Q, s, z, A, B) = _layer_dev(3, 4096, 4, 128, 256, 256, 40)
+    x = wl.activation((2, 4096), 12, 40)
+    y = cl.linear_decode(w, c, dev_u16(x.bits, torch.float16), out_dtype=torch.float32)
+    ref = linear.forward_packed(Q, s, z, 4, 128, A, B, 256, x.values)
+    assert rel_l2(out_to_numpy(y), ref) <= REL_L2_TOL
+
+
+@pytest.mark.parametrize("bits,G", [(4, 128), (2, 64)])
+def test_wide_input_uses_eight_k_slices(bits, G):
+    """d_in = 20480 (4-bit: 640 chunks of 32 codes) splits K over 8 waves."""
+    d_out, d_in = 300, 20480
+    w, c, (Q, s, z, A, B) = _layer_dev(d_out, d_in, bits, G, 32, 32, 41 + bits)
+    x = wl.activation((1, d_in), 12, 41 + bits)
+    y = cl.linear_decode(w, c, dev_u16(x.bits, torch.float16), out_dtype=torch.float32)
+    ref = linear.forward_packed(Q, s, z, bits, G, A, B, 32, x.values)
+    assert rel_l2(out_to_numpy(y), ref) <= REL_L2_TOL
