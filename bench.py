@@ -5,14 +5,15 @@ down; 4-bit, group 128; per-matrix ranks from the seeded allocator under a
 budget of 64 x 7) decoding one batch of tokens through the C ABI.  Weights are
 seeded N(0, 0.02) draws quantized by the library on the GPU; compensation
 factors are seeded fp16 stand-ins (the forward's cost does not depend on their
-values).  Steps rotate over enough distinct copies of the layer (>= 1 GiB) that
-every step streams its weights from HBM rather than from the 256 MB
-Infinity Cache.
+values).  Steps rotate over enough distinct copies of the layer (>= 1.5 GiB)
+that every step streams its weights from HBM, not from the 256 MB Infinity
+Cache.  Each step is a captured HIP graph of the seven calls, so host launch
+overhead is outside the timed region; the inputs are resident in HBM.
 
-Prints one JSON line: whole-job algorithmic HBM throughput (GB/s), the
-roofline of the dominant kernel (the gate matrix's decode launch, timed with
-HIP events on the stream it runs on) and the fp64 CPU oracle timed on a
-bounded sample of the same layer.
+Prints one JSON line: whole-job algorithmic HBM throughput (GB/s) of the step,
+the roofline of the dominant call (the gate matrix, 14336 x 4096) timed with
+HIP events on the stream it runs on, and the fp64 CPU oracle timed on the
+same layer.
 """
 
 import argparse
@@ -32,8 +33,8 @@ HBM_PEAK_GBS = 8000.0
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=200)
-    p.add_argument("--warmup", type=int, default=20)
+    p.add_argument("--steps", type=int, default=240)
+    p.add_argument("--warmup", type=int, default=24)
     p.add_argument("--tokens", type=int, default=1)
     p.add_argument("--rotate-gib", type=float, default=1.5)
     p.add_argument("--no-cpu-baseline", action="store_true")
@@ -42,8 +43,8 @@ def parse():
 
 def algorithmic_bytes(spec, T):
     """HBM bytes a compensated decode must move at minimum: packed codes,
-    fp16 scales and zeros, the used factor rows/columns, activations in and
-    fp16 outputs out."""
+    fp16 scales and zeros, the used rows of A and columns of B, activations in
+    and fp16 outputs out."""
     q = spec.d_out * spec.d_in * spec.bits // 8
     sz = 2 * 2 * spec.d_out * (spec.d_in // spec.group_size)
     ab = 2 * spec.rank * (spec.d_in + spec.d_out)
@@ -53,8 +54,8 @@ def algorithmic_bytes(spec, T):
 def main():
     args = parse()
     if args.gpus != 1:
-        print("bench.py measures one GPU: the compensated linear runs on a single device "
-              "(multi-GPU sharding is described in DESIGN.md, not run).", file=sys.stderr)
+        print("bench.py measures one GPU: the compensated linear runs on a single device; "
+              "multi-GPU sharding is described in DESIGN.md and not run.", file=sys.stderr)
         sys.exit(2)
 
     import torch
@@ -66,7 +67,7 @@ def main():
     layer = wl.llama_layer()
     specs = layer.linears
 
-    # ---- build one layer on the device (library quantizer), then copies
+    # ---- one layer on the device (library quantizer), then copies
     base = []
     for m, spec in enumerate(specs):
         W = torch.from_numpy(wl.weight((spec.d_out, spec.d_in), layer.index, 0, m)).to(dev)
@@ -92,54 +93,67 @@ def main():
         wss.append(cl.workspace(cl.linear_workspace(base[m][0], base[m][1], T), dev))
     torch.cuda.synchronize()
 
-    stream = torch.cuda.current_stream()
+    stream = torch.cuda.Stream()
 
-    def step(i):
-        lay = copies[i % ncopies]
-        for m in range(len(specs)):
-            w, c = lay[m]
-            cl.linear_decode(w, c, xs[m], y=ys[m], ws=wss[m], stream=stream)
+    def capture(fn):
+        """A HIP graph of fn() recorded on `stream` (after one eager run)."""
+        with torch.cuda.stream(stream):
+            fn()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=stream):
+            fn()
+        torch.cuda.synchronize()
+        return g
 
-    for i in range(args.warmup):
-        step(i)
-    torch.cuda.synchronize()
+    def layer_calls(k):
+        def run():
+            for m in range(len(specs)):
+                w, c = copies[k][m]
+                cl.linear_decode(w, c, xs[m], y=ys[m], ws=wss[m], stream=stream)
+        return run
+
+    step_graphs = [capture(layer_calls(k)) for k in range(ncopies)]
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record(stream)
-    for i in range(args.steps):
-        step(i)
-    e1.record(stream)
+
+    def timed(graphs, n):
+        """Average ms per replay of n replays cycling through graphs, with
+        events on the stream the kernels run on."""
+        with torch.cuda.stream(stream):
+            for i in range(min(n, len(graphs))):
+                graphs[i % len(graphs)].replay()
+            stream.synchronize()
+            e0.record(stream)
+            for i in range(n):
+                graphs[i % len(graphs)].replay()
+            e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n
+
+    with torch.cuda.stream(stream):
+        for i in range(args.warmup):
+            step_graphs[i % ncopies].replay()
     torch.cuda.synchronize()
-    ms_step = e0.elapsed_time(e1) / args.steps
+    ms_step = timed(step_graphs, args.steps)
     step_bytes = sum(algorithmic_bytes(s, T) for s in specs)
     value = step_bytes / (ms_step * 1e-3) / 1e9
 
-    # ---- dominant kernel: the gate matrix's decode, one launch per call,
-    # timed back to back over the rotating copies on the same stream
+    # ---- per matrix: graphs of one call on each copy, back to back
+    per_matrix_us = {}
+    per_matrix_gbs = {}
+    for m, spec in enumerate(specs):
+        def calls(m=m):
+            for k in range(ncopies):
+                w, c = copies[k][m]
+                cl.linear_decode(w, c, xs[m], y=ys[m], ws=wss[m], stream=stream)
+        g = capture(calls)
+        us = timed([g], 20) * 1e3 / ncopies
+        per_matrix_us[spec.name] = round(us, 3)
+        per_matrix_gbs[spec.name] = round(algorithmic_bytes(spec, T) / us / 1e3, 1)
     gi = [s.name for s in specs].index("gate")
-    n_calls = max(50, args.steps)
-    for i in range(10):
-        w, c = copies[i % ncopies][gi]
-        cl.linear_decode(w, c, xs[gi], y=ys[gi], ws=wss[gi], stream=stream)
-    torch.cuda.synchronize()
-    e0.record(stream)
-    for i in range(n_calls):
-        w, c = copies[i % ncopies][gi]
-        cl.linear_decode(w, c, xs[gi], y=ys[gi], ws=wss[gi], stream=stream)
-    e1.record(stream)
-    torch.cuda.synchronize()
-    gate_us = e0.elapsed_time(e1) * 1e3 / n_calls
+    gate_us = per_matrix_us["gate"]
     gate_bytes = algorithmic_bytes(specs[gi], T)
     achieved = gate_bytes / (gate_us * 1e-6) / 1e9
-
-    per_matrix_us = {}
-    for m, spec in enumerate(specs):
-        e0.record(stream)
-        for i in range(50):
-            w, c = copies[i % ncopies][m]
-            cl.linear_decode(w, c, xs[m], y=ys[m], ws=wss[m], stream=stream)
-        e1.record(stream)
-        torch.cuda.synchronize()
-        per_matrix_us[spec.name] = round(e0.elapsed_time(e1) * 1e3 / 50, 2)
 
     cpu = None if args.no_cpu_baseline else cpu_baseline(specs, layer, T)
 
@@ -154,37 +168,35 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "u4 codes, fp16 activations, fp32 accumulate",
+        "dtype": "u4 codes x fp16 activations, fp32 accumulate, fp16 out",
         "data": "synthetic",
-        "config": {"workload": "llama8b-decoder-layer 7 linears w4g128 ranks %s, T=%d decode" %
+        "config": {"workload": "llama8b-decoder-layer: 7 compensated linears, w4 g128, ranks %s, T=%d decode" %
                    ("/".join(str(s.rank) for s in specs), T),
                    "tokens": T, "step_bytes": step_bytes, "rotating_copies": ncopies,
-                   "per_matrix_us": per_matrix_us},
-        "roofline": {"bound": "hbm", "kernel": "gate 14336x4096 decode call", "achieved": round(achieved, 1),
-                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "us_per_launch": round(gate_us, 3), "bytes_per_launch": gate_bytes, "traffic": None},
+                   "per_matrix_us": per_matrix_us, "per_matrix_gbs": per_matrix_gbs},
+        "roofline": {"bound": "hbm", "kernel": "cl_linear_decode on gate 14336x4096 (prepare + backbone launches)",
+                     "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "us_per_launch": gate_us,
+                     "bytes_per_launch": gate_bytes, "traffic": None},
         "cpu_baseline": cpu,
     }
     print(json.dumps(out))
 
 
 def cpu_baseline(specs, layer, T):
-    """The fp64 oracle on a bounded sample: the first 2048 rows of each of the
-    seven matrices (about a third of the layer), same inputs, median of 3."""
+    """The fp64 oracle on the same layer (all seven matrices, every row):
+    unpack + dequantize + forward, median of 5 after one warm-up."""
     from oracle import linear, quant
     from paper_2605_05819_amd import workloads as wl
-    rows = 2048
     prepared = []
     nbytes = 0
     for m, spec in enumerate(specs):
-        W = wl.weight((spec.d_out, spec.d_in), layer.index, 0, m)[:rows]
+        W = wl.weight((spec.d_out, spec.d_in), layer.index, 0, m)
         Q, s, z = quant.quantize_pack(W, spec.bits, spec.group_size)
         A, B = wl.standin_factors(spec.d_out, spec.d_in, spec.r_max, layer.index, 0, m)
         x = wl.activation((T, spec.d_in), layer.index, 0, m).values
-        prepared.append((Q, s, z, spec, A, B[:rows], x))
-        sub = wl.LinearSpec(spec.name, min(rows, spec.d_out), spec.d_in, spec.bits, spec.group_size,
-                            spec.r_max, spec.rank)
-        nbytes += algorithmic_bytes(sub, T)
+        prepared.append((Q, s, z, spec, A, B, x))
+        nbytes += algorithmic_bytes(spec, T)
 
     def run():
         for Q, s, z, spec, A, B, x in prepared:
@@ -192,7 +204,7 @@ def cpu_baseline(specs, layer, T):
 
     run()
     times = []
-    for _ in range(3):
+    for _ in range(5):
         t0 = time.perf_counter()
         run()
         times.append(time.perf_counter() - t0)
@@ -203,8 +215,7 @@ def cpu_baseline(specs, layer, T):
     except Exception:
         threads = os.cpu_count()
     return {"value": round(nbytes / sec / 1e9, 4), "unit": "GB/s", "cores": threads, "kind": "oracle",
-            "sample": "first %d rows of each of the 7 layer matrices, T=%d, median of 3 (%.2f s each)" %
-                      (rows, T, sec)}
+            "sample": "whole layer (7 matrices, all rows), T=%d, median of 5 runs of %.2f s" % (T, sec)}
 
 
 if __name__ == "__main__":

@@ -147,6 +147,34 @@ cl_status cl_linear_decode(const cl_qweight* w, const cl_lowrank* c, const void*
                            int32_t act_dtype, void* y, int32_t out_dtype, void* ws,
                            size_t ws_bytes, void* stream);
 
+/*
+ * cl_linear_decode_window -- one compensation window: n linears that read the
+ * same activations x, each with its own backbone, factors and output.  The
+ * paper groups the Q, K and V projections, and the gate and up projections,
+ * into such windows so they share one hand-off of the activations and one
+ * compensation pass (Section 4.2.2, Communication Fusion; Appendix A.1).
+ * Here a window costs one A x / activation-preparation launch and one
+ * backbone launch over all n matrices; each output equals what
+ * cl_linear_decode would give for that linear alone (bitwise).
+ *
+ *  n          1..8 linears, all with the same d_in, bits and group_size
+ *  w          host array of n weight descriptors
+ *  c          host array of n factor descriptors (rank 0 allowed), or NULL
+ *             for no compensation at all
+ *  x          device [T][d_in] of act_dtype, 16-byte aligned (as above)
+ *  y          host array of n device pointers, y[i] is [T][w[i].d_out]
+ *  ws         device workspace of cl_linear_window_workspace(n, w, c, T)
+ *             bytes, 256-byte aligned
+ * Errors: as cl_linear_decode, and CL_EINVAL for n outside 1..8 or linears
+ * that differ in d_in, bits or group_size.
+ */
+cl_status cl_linear_decode_window(int32_t n, const cl_qweight* w, const cl_lowrank* c, const void* x,
+                                  int32_t T, int32_t act_dtype, void* const* y, int32_t out_dtype,
+                                  void* ws, size_t ws_bytes, void* stream);
+
+/* Workspace bytes for cl_linear_decode_window (0 for arguments it would reject). */
+size_t cl_linear_window_workspace(int32_t n, const cl_qweight* w, const cl_lowrank* c, int32_t tokens);
+
 /* Message describing the last non-CL_OK status returned on this thread. */
 const char* cl_last_error(void);
 

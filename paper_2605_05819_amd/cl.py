@@ -50,6 +50,12 @@ _SIGNATURES = {
     "cl_linear_decode": (ctypes.c_int32, [ctypes.POINTER(QWeightC), ctypes.POINTER(LowRankC), ctypes.c_void_p,
                                           ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32,
                                           ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
+    "cl_linear_window_workspace": (ctypes.c_size_t, [ctypes.c_int32, ctypes.POINTER(QWeightC),
+                                                     ctypes.POINTER(LowRankC), ctypes.c_int32]),
+    "cl_linear_decode_window": (ctypes.c_int32, [ctypes.c_int32, ctypes.POINTER(QWeightC), ctypes.POINTER(LowRankC),
+                                                 ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
+                                                 ctypes.POINTER(ctypes.c_void_p), ctypes.c_int32, ctypes.c_void_p,
+                                                 ctypes.c_size_t, ctypes.c_void_p]),
 }
 
 
@@ -157,3 +163,33 @@ def linear_decode(w, c, x, out_dtype=torch.float16, y=None, ws=None, stream=None
                                   _DTYPE_CODE[x.dtype], _ptr(y), _DTYPE_CODE[y.dtype], _ptr(ws),
                                   0 if ws is None else ws.numel(), _stream(stream)))
     return y
+
+
+def _window_structs(ws_, cs):
+    n = len(ws_)
+    qa = (QWeightC * n)(*[w.c() for w in ws_])
+    la = None
+    if cs is not None and any(c is not None for c in cs):
+        la = (LowRankC * n)(*[(c.c() if c is not None else LowRankC(0, 0, 0, 0)) for c in cs])
+    return qa, la
+
+
+def window_workspace(ws_, cs, tokens):
+    qa, la = _window_structs(ws_, cs)
+    return lib().cl_linear_window_workspace(len(ws_), qa, la, tokens)
+
+
+def linear_decode_window(ws_, cs, x, out_dtype=torch.float16, ys=None, ws=None, stream=None):
+    """``cl_linear_decode_window``: n linears sharing x [T][d_in]; returns the
+    list of outputs y_i [T][d_out_i]."""
+    T = x.shape[0]
+    n = len(ws_)
+    if ys is None:
+        ys = [torch.empty((T, w.d_out), dtype=out_dtype, device=x.device) for w in ws_]
+    qa, la = _window_structs(ws_, cs)
+    if ws is None:
+        ws = workspace(lib().cl_linear_window_workspace(n, qa, la, T), x.device)
+    yp = (ctypes.c_void_p * n)(*[y.data_ptr() for y in ys])
+    _check(lib().cl_linear_decode_window(n, qa, la, _ptr(x), T, _DTYPE_CODE[x.dtype], yp,
+                                         _DTYPE_CODE[ys[0].dtype], _ptr(ws), ws.numel(), _stream(stream)))
+    return ys

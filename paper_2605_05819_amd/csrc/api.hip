@@ -91,27 +91,34 @@ cl_status cl_dequantize(const cl_qweight* w, float* W_hat, void* stream) {
     return hip_status(cl::launch_dequantize(qw, W_hat, static_cast<hipStream_t>(stream)), who);
 }
 
-size_t cl_linear_workspace(const cl_qweight* w, const cl_lowrank* c, int32_t tokens) {
-    char saved[sizeof(g_err)];
-    memcpy(saved, g_err, sizeof(g_err));
-    cl::QW qw;
-    cl::LR lr;
-    size_t n = 0;
-    if (tokens >= 1 && check_qweight(w, &qw, "") == CL_OK && check_lowrank(c, qw, &lr, "") == CL_OK)
-        n = cl::decode_workspace_bytes(qw, lr, tokens);
-    memcpy(g_err, saved, sizeof(g_err));   // a size query leaves the last error alone
-    return n;
+}  // extern "C"
+
+namespace {
+
+// Validate a window of n linears (c may be NULL: no compensation anywhere).
+cl_status check_window(int32_t n, const cl_qweight* w, const cl_lowrank* c, cl::QW* qw, cl::LR* lr,
+                       const char* who) {
+    if (n < 1 || n > 8) return fail(CL_EINVAL, "%s: a window holds 1..8 linears (got %d)", who, n);
+    if (!w) return fail(CL_EINVAL, "%s: null weight descriptor array", who);
+    for (int i = 0; i < n; ++i) {
+        cl_status st = check_qweight(&w[i], &qw[i], who);
+        if (st) return st;
+        if (qw[i].d_in != qw[0].d_in || qw[i].bits != qw[0].bits || qw[i].G != qw[0].G)
+            return fail(CL_EINVAL, "%s: linears of one window must share d_in, bits and group_size", who);
+        st = check_lowrank(c ? &c[i] : nullptr, qw[i], &lr[i], who);
+        if (st) return st;
+    }
+    if (!cl::decode_fits(qw[0]))
+        return fail(CL_EUNSUPPORTED, "%s: d_in %d exceeds the decode kernel's limit", who, qw[0].d_in);
+    return CL_OK;
 }
 
-cl_status cl_linear_decode(const cl_qweight* w, const cl_lowrank* c, const void* x, int32_t T,
-                           int32_t act_dtype, void* y, int32_t out_dtype, void* ws, size_t ws_bytes,
-                           void* stream) {
-    const char* who = "cl_linear_decode";
-    cl::QW qw;
-    cl::LR lr;
-    cl_status st = check_qweight(w, &qw, who);
-    if (st) return st;
-    st = check_lowrank(c, qw, &lr, who);
+cl_status decode_common(int32_t n, const cl_qweight* w, const cl_lowrank* c, const void* x, int32_t T,
+                        int32_t act_dtype, void* const* y, int32_t out_dtype, void* ws, size_t ws_bytes,
+                        void* stream, const char* who) {
+    cl::QW qw[8];
+    cl::LR lr[8];
+    cl_status st = check_window(n, w, c, qw, lr, who);
     if (st) return st;
     if (T < 1 || T > 64) return fail(CL_EINVAL, "%s: T must be in 1..64 (got %d)", who, T);
     if (act_dtype != CL_FP16 && act_dtype != CL_BF16)
@@ -120,15 +127,55 @@ cl_status cl_linear_decode(const cl_qweight* w, const cl_lowrank* c, const void*
         return fail(CL_EINVAL, "%s: out_dtype must be CL_FP16, CL_BF16 or CL_FP32", who);
     if (!x || !y) return fail(CL_EINVAL, "%s: null x or y", who);
     if (!aligned(x, 16)) return fail(CL_EINVAL, "%s: x must be 16-byte aligned", who);
-    if (!aligned(y, out_dtype == CL_FP32 ? 4 : 2)) return fail(CL_EINVAL, "%s: misaligned y", who);
-    if (!cl::decode_fits(qw, lr))
-        return fail(CL_EUNSUPPORTED, "%s: d_in %d with rank %d does not fit the staged activations", who, qw.d_in, lr.rank);
-    const size_t need = cl::decode_workspace_bytes(qw, lr, T);
+    for (int i = 0; i < n; ++i) {
+        if (!y[i]) return fail(CL_EINVAL, "%s: null y", who);
+        if (!aligned(y[i], out_dtype == CL_FP32 ? 4 : 2)) return fail(CL_EINVAL, "%s: misaligned y", who);
+    }
+    const size_t need = cl::decode_workspace_bytes(n, qw, lr, T);
     if (!ws || ws_bytes < need)
         return fail(CL_EWORKSPACE, "%s: workspace of %zu bytes needed (got %zu)", who, need, ws ? ws_bytes : 0);
     if (!aligned(ws, 256)) return fail(CL_EINVAL, "%s: workspace must be 256-byte aligned", who);
-    return hip_status(cl::launch_linear_decode(qw, lr, x, T, act_dtype, y, out_dtype, ws,
+    return hip_status(cl::launch_linear_decode(n, qw, lr, x, T, act_dtype, y, out_dtype, ws,
                                                static_cast<hipStream_t>(stream)), who);
+}
+
+size_t window_workspace(int32_t n, const cl_qweight* w, const cl_lowrank* c, int32_t tokens) {
+    char saved[sizeof(g_err)];
+    memcpy(saved, g_err, sizeof(g_err));
+    cl::QW qw[8];
+    cl::LR lr[8];
+    size_t bytes = 0;
+    if (tokens >= 1 && tokens <= 64 && check_window(n, w, c, qw, lr, "") == CL_OK)
+        bytes = cl::decode_workspace_bytes(n, qw, lr, tokens);
+    memcpy(g_err, saved, sizeof(g_err));   // a size query leaves the last error alone
+    return bytes;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t cl_linear_workspace(const cl_qweight* w, const cl_lowrank* c, int32_t tokens) {
+    return window_workspace(1, w, c, tokens);
+}
+
+size_t cl_linear_window_workspace(int32_t n, const cl_qweight* w, const cl_lowrank* c, int32_t tokens) {
+    return window_workspace(n, w, c, tokens);
+}
+
+cl_status cl_linear_decode(const cl_qweight* w, const cl_lowrank* c, const void* x, int32_t T,
+                           int32_t act_dtype, void* y, int32_t out_dtype, void* ws, size_t ws_bytes,
+                           void* stream) {
+    void* ys[1] = {y};
+    return decode_common(1, w, c, x, T, act_dtype, y ? ys : nullptr, out_dtype, ws, ws_bytes, stream,
+                         "cl_linear_decode");
+}
+
+cl_status cl_linear_decode_window(int32_t n, const cl_qweight* w, const cl_lowrank* c, const void* x,
+                                  int32_t T, int32_t act_dtype, void* const* y, int32_t out_dtype, void* ws,
+                                  size_t ws_bytes, void* stream) {
+    return decode_common(n, w, c, x, T, act_dtype, y, out_dtype, ws, ws_bytes, stream,
+                         "cl_linear_decode_window");
 }
 
 }  // extern "C"

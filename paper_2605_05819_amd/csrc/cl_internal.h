@@ -26,10 +26,11 @@ hipError_t launch_quantize_pack(const float* W, int d_out, int d_in, int bits, i
                                 uint16_t* s, uint16_t* z, hipStream_t st);
 hipError_t launch_dequantize(const QW& w, float* out, hipStream_t st);
 
-// Workspace layout of the decode path: t = A[:rank] x as float [T][rank].
-size_t decode_workspace_bytes(const QW& w, const LR& c, int T);
-bool decode_fits(const QW& w, const LR& c);   // activations of one token fit in LDS
-hipError_t launch_linear_decode(const QW& w, const LR& c, const void* x, int T, int act, void* y,
-                                int out, void* ws, hipStream_t st);
+// Decode of a window of n (1..8) linears sharing d_in, bits, group size and
+// the activations x; arguments already validated.
+size_t decode_workspace_bytes(int n, const QW* w, const LR* c, int T);
+bool decode_fits(const QW& w);   // d_in within the kernel's K-slice limit
+hipError_t launch_linear_decode(int n, const QW* w, const LR* c, const void* x, int T, int act,
+                                void* const* y, int out, void* ws, hipStream_t st);
 
 }  // namespace cl

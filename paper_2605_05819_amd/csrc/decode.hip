@@ -1,33 +1,41 @@
 // Decode path of the error-compensated quantized linear (few tokens):
 //
-//     y[t] = deq(Q) x[t] + B[:, :r] (A[:r] x[t])          (Section 4.1)
+//     y_i[t] = deq(Q_i) x[t] + B_i[:, :r_i] (A_i[:r_i] x[t])     (Section 4.1)
 //
-// Two launches per call (one when rank = 0).  The backbone is HBM-bound (about half a byte per
-// weight at 4 bits, a quarter at 2 bits), so the kernel is built around the
-// memory stream:
+// for a compensation window of n <= 8 linears that read the same activations
+// x (the paper fuses Q/K/V and gate/up into such windows, Section 4.2.2 and
+// Appendix A.1); a single linear is the window n = 1.
 //
-//  * A "row group" of KS waves owns R consecutive rows.  The row's 16-byte
-//    chunks of packed codes are split into KS slices; lane l of slice k
-//    handles chunks k*cps + l + 64j (j < CPL).  Every wave issues all R*CPL of
-//    its 16-byte loads before it computes anything, so each lane has 8-16
-//    independent loads in flight and each load instruction reads R fully
-//    coalesced segments.
-//  * Codes are unpacked with one AND per pair straight into fp16 lanes (the
-//    code q in the low mantissa bits of a zero-exponent fp16 is the subnormal
-//    q * 2^-24, exact), multiplied with the lane's activations by v_dot2 into
-//    fp32, and each chunk's scale and zero point are applied in fp32:
-//    s * (sum q x) - s * z * (sum x), with the 2^24 folded into s.
-//  * Activations of the lane's chunks live in registers for the whole kernel,
-//    pre-permuted to the (q_p, q_{p+CPW/2}) pair order of the unpacked codes.
-//  * The rank-r term needs t = A[:r] x before any row can finish.  A small
-//    kernel ahead of the backbone kernel computes it (one workgroup per row
-//    of A, every load in flight at once, fixed-order reduction) into the
-//    workspace; the stream order makes it visible to the backbone kernel.
-//    Synchronising inside one launch instead would need device-scope
-//    release/acquire between workgroups on different XCDs, whose L2
-//    writeback/invalidate costs far more than the second launch.
-//  * Sums over lanes use a transposing butterfly (R values in log steps), the
-//    KS slices are combined through LDS in a fixed order: results are bitwise
+// Two launches per call:
+//  * prep: t_i = A_i[:r_i] x for every linear (one workgroup per row of
+//    A_i) and the activations converted to fp16, permuted into the pair order
+//    of the unpacked codes, with each 16-byte chunk's sum of activations --
+//    all into the workspace;
+//  * backbone: one grouped, persistent kernel over all row batches of all the
+//    window's linears.
+// A x stays in its own launch: handing it from producer to consumer
+// workgroups inside one launch needs device-scope release/acquire between
+// XCDs, whose L2 writeback/invalidate measured 12-90 us on MI355X against a
+// few us for the extra launch.
+//
+// The backbone is HBM-bound (about half a byte per weight at 4 bits, a
+// quarter at 2 bits):
+//  * a "row group" of KS waves owns R consecutive rows of one linear; the
+//    row's 16-byte chunks of packed codes are split into KS slices and lane l
+//    of slice k handles chunks k*cps + l + 64j (j < CPL), so every load
+//    instruction reads R fully coalesced segments;
+//  * workgroups loop over batches with the next batch's loads (codes, scales,
+//    zeros, factor entries, A x) in flight during the current batch's
+//    arithmetic, and raw loads only -- nothing consumes a prefetched value
+//    before the compute that needs it;
+//  * codes are unpacked with one AND per pair straight into fp16 lanes (a
+//    code in the mantissa bits of a zero-exponent fp16 is an exact subnormal)
+//    and multiplied with the prepared activations by v_dot2 into fp32; each
+//    chunk's scale and zero point are applied in fp32:
+//        s * (sum q x - z * sum x);
+//  * the rank-r term B[row, :r] . t rides in the same lane partial sums;
+//  * sums over lanes use a transposing butterfly (R values in log steps),
+//    K slices are combined through LDS in a fixed order: results are bitwise
 //    reproducible.
 
 #include "cl_device.h"
@@ -37,19 +45,39 @@ namespace cl {
 
 namespace {
 
-struct DecodeArgs {
+constexpr int kMaxWin = 8;   // linears per window
+
+// One linear of a window, as the backbone kernel sees it.
+struct Lin {
     const uint32_t* q;
     const uint16_t* s;
     const uint16_t* z;
-    const uint16_t* A;
     const uint16_t* B;
-    const f16x2* xp;       // [T][d_in / 2] activations, fp16, pair-permuted
-    const float* sx;       // [T][chunks] per-chunk sums of activations
-    void* y;               // [T][d_out]
-    const float* t;        // [T][rank]
-    int d_out, d_in, G, rank, r_max, T, tok0, act, out;
-    int ks;                // K slices (waves per row group)
-    int cps;               // chunks per slice
+    void* y;                 // [T][d_out]
+    const float* t;          // [T][rank] (workspace)
+    int d_out, rank, r_max;
+    int batch_end;           // exclusive prefix sum of the linears' batches
+};
+
+struct DecodeArgs {
+    Lin lin[kMaxWin];
+    int n;
+    const f16x2* xp;         // [T][d_in / 2] activations, fp16, pair-permuted
+    const float* sx;         // [T][chunks] per-chunk sums of activations
+    int d_in, G, T, tok0, out;
+    int ks;                  // K slices (waves per row group)
+    int cps;                 // chunks per slice
+};
+
+struct PrepArgs {
+    const uint16_t* A[kMaxWin];
+    float* t[kMaxWin];
+    int rank_end[kMaxWin];   // exclusive prefix sum of the ranks
+    int n;
+    const uint16_t* x;       // [T][d_in] fp16/bf16 bits
+    f16x2* xp;
+    float* sx;
+    int d_in, T, act;
 };
 
 // Load 8 consecutive activations as four f16x2 words (fp16 or bf16 input).
@@ -122,20 +150,12 @@ __device__ __forceinline__ float wave_sum_multi(float (&v)[R]) {
     return r;
 }
 
-// Preparation kernel, run once per call ahead of the backbone kernel:
-//  * workgroups [0, rank): t[tok][i] = A[i] . x[tok] for every token (one row
-//    of A per workgroup, every thread's 16-byte loads issued before any
-//    arithmetic, fixed-order reduction);
-//  * the remaining workgroups: the activations converted to fp16 and
-//    permuted into the pair order of the unpacked codes (word w, pair p =
-//    (x[w*CPW + p], x[w*CPW + p + CPW/2])), plus each 16-byte chunk's sum of
-//    activations, so the backbone kernel only loads them.
+// Preparation kernel: workgroups [0, sum of ranks) compute one row i of some
+// linear's A x for every token (all of the row's 16-byte loads issued before
+// any arithmetic, fixed-order reduction); the remaining workgroups prepare the
+// activations, one thread per (token, chunk).
 template <int BITS>
-__global__ __launch_bounds__(256) void decode_prep_kernel(const uint16_t* __restrict__ A,
-                                                          const uint16_t* __restrict__ x,
-                                                          float* __restrict__ t, f16x2* __restrict__ xp,
-                                                          float* __restrict__ sx, int d_in, int rank, int T,
-                                                          int act) {
+__global__ __launch_bounds__(256) void decode_prep_kernel(PrepArgs a) {
     constexpr int CPW = 32 / BITS, HPW = CPW / 2, PPC = 4 * HPW;
     constexpr int KB = 4;                   // 16-byte loads per thread per batch
     constexpr int TB = 4;                   // tokens per pass over a row of A
@@ -143,9 +163,16 @@ __global__ __launch_bounds__(256) void decode_prep_kernel(const uint16_t* __rest
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
     const int tid = threadIdx.x;
-    if (static_cast<int>(blockIdx.x) < rank) {
-        const int i = blockIdx.x;
-        const uint16_t* ar = A + static_cast<size_t>(i) * d_in;
+    const int d_in = a.d_in, T = a.T;
+    const int nrank = a.n > 0 ? a.rank_end[a.n - 1] : 0;
+    const int blk = blockIdx.x;
+    if (blk < nrank) {
+        int li = 0;
+        while (blk >= a.rank_end[li]) ++li;
+        const int i = blk - (li ? a.rank_end[li - 1] : 0);
+        const int rank = a.rank_end[li] - (li ? a.rank_end[li - 1] : 0);
+        const uint16_t* ar = a.A[li] + static_cast<size_t>(i) * d_in;
+        float* t = a.t[li];
         for (int base = 0; base < d_in; base += 256 * 8 * KB) {
             u32x4 av[KB];
             int col[KB];
@@ -160,11 +187,11 @@ __global__ __launch_bounds__(256) void decode_prep_kernel(const uint16_t* __rest
                 for (int tk = 0; tk < TB; ++tk) {
                     acc[tk] = 0.f;
                     if (tb + tk >= T) continue;
-                    const uint16_t* xr = x + static_cast<size_t>(tb + tk) * d_in;
+                    const uint16_t* xr = a.x + static_cast<size_t>(tb + tk) * d_in;
 #pragma unroll
                     for (int k = 0; k < KB; ++k) {
                         uint32_t xw[4];
-                        load8_f16(xr + (col[k] < d_in ? col[k] : 0), act, xw);
+                        load8_f16(xr + (col[k] < d_in ? col[k] : 0), a.act, xw);
                         float d = 0.f;
 #pragma unroll
                         for (int e = 0; e < 4; ++e) {
@@ -192,23 +219,22 @@ __global__ __launch_bounds__(256) void decode_prep_kernel(const uint16_t* __rest
         }
         return;
     }
-    // activation preparation: one thread per (token, chunk)
     const int chunks = d_in / CPW / 4;
-    const long long item = static_cast<long long>(blockIdx.x - rank) * 256 + tid;
+    const long long item = static_cast<long long>(blk - nrank) * 256 + tid;
     if (item >= static_cast<long long>(T) * chunks) return;
     const int tok = static_cast<int>(item / chunks);
     const int c = static_cast<int>(item % chunks);
     f16x2 v[PPC];
-    load_chunk_x<BITS>(x + static_cast<size_t>(tok) * d_in, c, act, v);
+    load_chunk_x<BITS>(a.x + static_cast<size_t>(tok) * d_in, c, a.act, v);
     const f16x2 one = {static_cast<f16>(1.0f), static_cast<f16>(1.0f)};
     float sum = 0.f;
-    f16x2* dst = xp + static_cast<size_t>(tok) * (d_in / 2) + static_cast<size_t>(c) * PPC;
+    f16x2* dst = a.xp + static_cast<size_t>(tok) * (d_in / 2) + static_cast<size_t>(c) * PPC;
 #pragma unroll
     for (int p = 0; p < PPC; ++p) {
         sum = dot2(v[p], one, sum);
         dst[p] = v[p];
     }
-    sx[static_cast<size_t>(tok) * chunks + c] = sum;
+    a.sx[static_cast<size_t>(tok) * chunks + c] = sum;
 }
 
 // Unpack one 32-bit word of codes into fp16 pairs with masks only where the
@@ -244,18 +270,20 @@ __device__ __forceinline__ float combine(const float* d) {
 }
 
 // One batch of a wave: R rows x CPL chunks of packed codes, the matching
-// scale/zero pairs and the rows' factor entries.
-// Raw loads only: nothing may consume a value at load time, or the wave
-// would stall on the prefetch it is meant to overlap.
-template <int R, int CPL, int NB>
+// scales and zeros, the rows' factor entries and this lane's entries of A x.
+// Raw loads only: nothing may consume a value at load time, or the wave would
+// stall on the prefetch it is meant to overlap.
+template <int R, int CPL, int NB, int NT>
 struct Batch {
     u32x4 q[R][CPL];
     uint16_t s[R][CPL];      // fp16 scale bits
     uint16_t z[R][CPL];      // fp16 zero-point bits
-    uint16_t b[R][NB];       // B[row][i] for this lane's factor columns (NB >= 1)
+    uint16_t b[R][NB];       // B[row][i] for this lane's factor columns
+    float t[NT][NB];         // (A x)[tok][i] for the same columns
 };
 
-// NB: factor columns of B per lane (rank <= NB * 64 * ks); 0 for rank 0.
+// NB: factor columns of B per lane (rank <= NB * 64 * ks); 0 when every
+// linear of the window has rank 0.
 template <int BITS, int NT, int CPL, int R, int NB>
 __global__ __launch_bounds__(512) void decode_kernel(DecodeArgs a) {
     constexpr int CPW = 32 / BITS;    // codes per word
@@ -279,8 +307,7 @@ __global__ __launch_bounds__(512) void decode_kernel(DecodeArgs a) {
     const int rg_per_block = waves / ks;
     const int slice = wave % ks;
     const int rgw = wave / ks;
-    const int rgroups = (a.d_out + R - 1) / R;
-    const int nbatch = (rgroups + rg_per_block - 1) / rg_per_block;
+    const int nbatch = a.lin[a.n - 1].batch_end;
     const int c_begin = slice * a.cps;
     const int c_end = min(chunks, c_begin + a.cps);
 
@@ -294,8 +321,7 @@ __global__ __launch_bounds__(512) void decode_kernel(DecodeArgs a) {
         if (!valid) cidx[j] = c_begin;     // in-bounds dummy chunk, weighted by 0
     }
 
-    // activations of this lane's chunks (prepared: fp16, pair-permuted) and
-    // their sums
+    // prepared activations of this lane's chunks and their sums
     f16x2 xv[XREG ? NT : 1][XREG ? CPL : 1][PPC];
     float sx[NT][CPL];
 #pragma unroll
@@ -319,43 +345,60 @@ __global__ __launch_bounds__(512) void decode_kernel(DecodeArgs a) {
             }
         }
     }
-    // this lane's entries of t = A x (factor columns lane + 64*(slice + ks*m))
-    float tv[NT][NBA];
-#pragma unroll
-    for (int tk = 0; tk < NT; ++tk)
-#pragma unroll
-        for (int m = 0; m < NBA; ++m) {
-            const int i = lane + 64 * (slice + ks * m);
-            tv[tk][m] = (i < a.rank && a.tok0 + tk < a.T) ? a.t[static_cast<size_t>(tk) * a.rank + i] : 0.f;
-        }
 
-    auto load_batch = [&](Batch<R, CPL, NBA>& bt, int b) {
-        const int row0 = (b * rg_per_block + rgw) * R;
-        const int base = row0 < a.d_out ? row0 : 0;
-        const int nrows = row0 < a.d_out ? min(R, a.d_out - row0) : 1;
+    // global batch b -> (linear, first row of this wave's row group)
+    auto locate = [&](int b, int& li, int& row0) {
+        li = 0;
+        while (b >= a.lin[li].batch_end) ++li;
+        const int lb = b - (li ? a.lin[li - 1].batch_end : 0);
+        row0 = (lb * rg_per_block + rgw) * R;
+    };
+
+    auto load_batch = [&](Batch<R, CPL, NBA, NT>& bt, int b) {
+        int li, row0;
+        locate(b, li, row0);
+        const Lin& L = a.lin[li];
+        const int base = row0 < L.d_out ? row0 : 0;
+        const int nrows = row0 < L.d_out ? min(R, L.d_out - row0) : 1;
+        // a rank-0 linear has no factors: its loads read valid placeholder
+        // memory (masked to zero in compute_batch) instead of branching on data
+        const uint16_t* Bp = L.rank > 0 ? L.B : L.s;
+        const int bstride = L.rank > 0 ? L.r_max : 0;
+        const float* tp = L.rank > 0 ? L.t : a.sx;
+        const int tstride = L.rank > 0 ? L.rank : 0;
 #pragma unroll
         for (int r = 0; r < R; ++r) {
             const int row = base + (r < nrows ? r : 0);
-            const u32x4* qr = reinterpret_cast<const u32x4*>(a.q + static_cast<size_t>(row) * words);
+            const u32x4* qr = reinterpret_cast<const u32x4*>(L.q + static_cast<size_t>(row) * words);
 #pragma unroll
             for (int j = 0; j < CPL; ++j) bt.q[r][j] = __builtin_nontemporal_load(qr + cidx[j]);
 #pragma unroll
             for (int j = 0; j < CPL; ++j) {
                 const size_t gi = static_cast<size_t>(row) * groups + (cidx[j] * CPC) / a.G;
-                bt.s[r][j] = a.s[gi];
-                bt.z[r][j] = a.z[gi];
+                bt.s[r][j] = L.s[gi];
+                bt.z[r][j] = L.z[gi];
             }
 #pragma unroll
             for (int m = 0; m < NB; ++m) {
                 // columns past the rank read column 0 (valid data) and meet t = 0
                 const int i = lane + 64 * (slice + ks * m);
-                bt.b[r][m] = a.B[static_cast<size_t>(row) * a.r_max + (i < a.rank ? i : 0)];
+                bt.b[r][m] = Bp[static_cast<size_t>(row) * bstride + (i < L.rank ? i : 0)];
             }
         }
+#pragma unroll
+        for (int tk = 0; tk < NT; ++tk)
+#pragma unroll
+            for (int m = 0; m < NB; ++m) {
+                const int i = lane + 64 * (slice + ks * m);
+                const int tok = min(a.tok0 + tk, a.T - 1);
+                bt.t[tk][m] = tp[static_cast<size_t>(tok) * tstride + (i < L.rank ? i : 0)];
+            }
     };
 
-    auto compute_batch = [&](const Batch<R, CPL, NBA>& bt, int b, int buf) {
-        const int row0 = (b * rg_per_block + rgw) * R;
+    auto compute_batch = [&](const Batch<R, CPL, NBA, NT>& bt, int b, int buf) {
+        int li, row0;
+        locate(b, li, row0);
+        const Lin& L = a.lin[li];
         float acc[R][NT];
 #pragma unroll
         for (int r = 0; r < R; ++r)
@@ -379,14 +422,14 @@ __global__ __launch_bounds__(512) void decode_kernel(DecodeArgs a) {
                         }
                     }
                 }
-                const f16x2* xp = XREG ? xv[XREG ? tk : 0][XREG ? j : 0] : xl;
+                const f16x2* xq = XREG ? xv[XREG ? tk : 0][XREG ? j : 0] : xl;
 #pragma unroll
                 for (int r = 0; r < R; ++r) {
                     float d[NACC];
 #pragma unroll
                     for (int k = 0; k < NACC; ++k) d[k] = 0.f;
 #pragma unroll
-                    for (int w = 0; w < 4; ++w) dot_word<BITS>(bt.q[r][j][w], xp + w * HPW, d);
+                    for (int w = 0; w < 4; ++w) dot_word<BITS>(bt.q[r][j][w], xq + w * HPW, d);
                     const float sc = f16_bits_to_f32(bt.s[r][j]) * cmask[j];
                     const float zc = f16_bits_to_f32(bt.z[r][j]);
                     // s * (2^24 * sum q x - z * sum x): the codes were subnormals q * 2^-24
@@ -395,15 +438,19 @@ __global__ __launch_bounds__(512) void decode_kernel(DecodeArgs a) {
                 }
             }
         }
-        // rank-r up-projection: B[row, i] * t[i] over this lane's factor columns
+        // rank-r up-projection B[row, i] * t[i] over this lane's factor columns
+        // (entries past the rank were loaded from column 0 and are masked here)
 #pragma unroll
-        for (int r = 0; r < R; ++r)
+        for (int m = 0; m < NB; ++m) {
+            const int i = lane + 64 * (slice + ks * m);
+            const float on = i < L.rank ? 1.f : 0.f;
 #pragma unroll
-            for (int m = 0; m < NB; ++m) {
-                const float bv = f16_bits_to_f32(bt.b[r][m]);
+            for (int r = 0; r < R; ++r) {
+                const float bv = f16_bits_to_f32(bt.b[r][m]) * on;
 #pragma unroll
-                for (int tk = 0; tk < NT; ++tk) acc[r][tk] = fmaf(bv, tv[tk][m], acc[r][tk]);
+                for (int tk = 0; tk < NT; ++tk) acc[r][tk] = fmaf(bv, bt.t[tk][m], acc[r][tk]);
             }
+        }
         // reduce over lanes, then over the K slices in a fixed order, store
 #pragma unroll
         for (int tk = 0; tk < NT; ++tk) {
@@ -415,8 +462,8 @@ __global__ __launch_bounds__(512) void decode_kernel(DecodeArgs a) {
             const int rr = (lane / SPAN) & (R - 1);
             if ((lane & (SPAN - 1)) == 0) {
                 if (ks == 1) {
-                    if (row0 + rr < a.d_out && a.tok0 + tk < a.T)
-                        store_out(a.y, static_cast<size_t>(a.tok0 + tk) * a.d_out + row0 + rr, tot, a.out);
+                    if (row0 + rr < L.d_out && a.tok0 + tk < a.T)
+                        store_out(L.y, static_cast<size_t>(a.tok0 + tk) * L.d_out + row0 + rr, tot, a.out);
                 } else {
                     red[buf][wave][rr][tk] = tot;
                 }
@@ -427,10 +474,10 @@ __global__ __launch_bounds__(512) void decode_kernel(DecodeArgs a) {
         if (slice == 0 && lane < R * NT) {
             const int r = lane / NT, tk = lane - r * NT;
             const int row = row0 + r;
-            if (row < a.d_out && a.tok0 + tk < a.T) {
+            if (row < L.d_out && a.tok0 + tk < a.T) {
                 float v = 0.f;
                 for (int k = 0; k < ks; ++k) v += red[buf][wave + k][r][tk];
-                store_out(a.y, static_cast<size_t>(a.tok0 + tk) * a.d_out + row, v, a.out);
+                store_out(L.y, static_cast<size_t>(a.tok0 + tk) * L.d_out + row, v, a.out);
             }
         }
     };
@@ -443,7 +490,7 @@ __global__ __launch_bounds__(512) void decode_kernel(DecodeArgs a) {
     const int stride = gridDim.x;
     int b = blockIdx.x;
     if (b >= nbatch) return;
-    Batch<R, CPL, NBA> b0, b1;
+    Batch<R, CPL, NBA, NT> b0, b1;
     load_batch(b0, b);
     for (;;) {
         if (b + stride >= nbatch) { compute_batch(b0, b, 0); break; }
@@ -461,9 +508,9 @@ struct Plan {
     int cpl, R, ks, cps, nt, nb, threads;
 };
 
-Plan plan(const QW& w, const LR& c, int T) {
-    const int CPW = 32 / w.bits;
-    const int chunks = w.d_in / CPW / 4;
+Plan plan(int d_in, int bits, int max_rank, int T) {
+    const int CPW = 32 / bits;
+    const int chunks = d_in / CPW / 4;
     Plan p;
     p.nt = T >= 4 ? 4 : (T >= 2 ? 2 : 1);
     // One 16-byte chunk per lane and 4 rows per batch measured best on
@@ -481,7 +528,7 @@ Plan plan(const QW& w, const LR& c, int T) {
     p.cps = (chunks + p.ks - 1) / p.ks;
     p.threads = 64 * (p.ks > 4 ? p.ks : 4);
     const int per = 64 * p.ks;                     // factor columns per lane pass
-    p.nb = c.rank == 0 ? 0 : (c.rank <= per ? 1 : (c.rank <= 2 * per ? 2 : 4));
+    p.nb = max_rank == 0 ? 0 : (max_rank <= per ? 1 : (max_rank <= 2 * per ? 2 : 4));
     return p;
 }
 
@@ -507,9 +554,7 @@ hipError_t launch5(const DecodeArgs& a, const Plan& p, hipStream_t st) {
         if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kern, p.threads, 0) != hipSuccess || n <= 0) n = 1;
         occ = n;
     }
-    const int rgroups = (a.d_out + R - 1) / R;
-    const int rg_per_block = p.threads / 64 / p.ks;
-    const int nbatch = (rgroups + rg_per_block - 1) / rg_per_block;
+    const int nbatch = a.lin[a.n - 1].batch_end;
     // at most one resident wave of workgroups, each with the same number of
     // batches (no partial second wave)
     const int cap = occ * device_cus();
@@ -519,89 +564,104 @@ hipError_t launch5(const DecodeArgs& a, const Plan& p, hipStream_t st) {
     return hipGetLastError();
 }
 
-template <int BITS, int NT, int CPL, int R>
+template <int BITS, int NT, int CPL>
 hipError_t launch4(const DecodeArgs& a, const Plan& p, hipStream_t st) {
     switch (p.nb) {
-        case 0: return launch5<BITS, NT, CPL, R, 0>(a, p, st);
-        case 1: return launch5<BITS, NT, CPL, R, 1>(a, p, st);
-        case 2: return launch5<BITS, NT, CPL, R, 2>(a, p, st);
-        default: return launch5<BITS, NT, CPL, R, 4>(a, p, st);
+        case 0: return launch5<BITS, NT, CPL, 4, 0>(a, p, st);
+        case 1: return launch5<BITS, NT, CPL, 4, 1>(a, p, st);
+        case 2: return launch5<BITS, NT, CPL, 4, 2>(a, p, st);
+        default: return launch5<BITS, NT, CPL, 4, 4>(a, p, st);
     }
-}
-
-template <int BITS, int NT, int CPL>
-hipError_t launch_r(const DecodeArgs& a, const Plan& p, hipStream_t st) {
-    return launch4<BITS, NT, CPL, 4>(a, p, st);
 }
 
 template <int BITS, int NT>
 hipError_t launch3(const DecodeArgs& a, const Plan& p, hipStream_t st) {
-    return p.cpl == 2 ? launch_r<BITS, NT, 2>(a, p, st) : launch_r<BITS, NT, 1>(a, p, st);
+    return p.cpl == 2 ? launch4<BITS, NT, 2>(a, p, st) : launch4<BITS, NT, 1>(a, p, st);
 }
 
 template <int BITS>
-hipError_t launch2(const DecodeArgs& a, const Plan& p, int nt, hipStream_t st) {
-    if (nt == 1) return launch3<BITS, 1>(a, p, st);
-    if (nt == 2) return launch3<BITS, 2>(a, p, st);
+hipError_t launch2(const DecodeArgs& a, const Plan& p, hipStream_t st) {
+    if (p.nt == 1) return launch3<BITS, 1>(a, p, st);
+    if (p.nt == 2) return launch3<BITS, 2>(a, p, st);
     return launch3<BITS, 4>(a, p, st);
 }
 
+// Workspace: per linear t_i [T][rank_i] float | xp [T][d_in/2] fp16 pairs |
+// sx [T][chunks] float; every region 256-byte aligned.
+size_t up256(size_t n) { return (n + 255) / 256 * 256; }
+
 }  // namespace
 
-// Workspace: t [T][rank] float | xp [T][d_in/2] fp16 pairs | sx [T][chunks]
-// float, each region 256-byte aligned.
-struct WsLayout {
-    size_t t, xp, sx, total;
-};
-
-WsLayout ws_layout(const QW& w, const LR& c, int T) {
-    auto up = [](size_t n) { return (n + 255) / 256 * 256; };
-    const size_t chunks = static_cast<size_t>(w.d_in) / (32 / w.bits) / 4;
-    WsLayout l;
-    l.t = 0;
-    l.xp = up(static_cast<size_t>(c.rank) * T * sizeof(float));
-    l.sx = l.xp + up(static_cast<size_t>(T) * w.d_in * 2);
-    l.total = l.sx + up(static_cast<size_t>(T) * chunks * sizeof(float));
-    return l;
+size_t decode_workspace_bytes(int n, const QW* w, const LR* c, int T) {
+    size_t total = 0;
+    for (int i = 0; i < n; ++i) total += up256(static_cast<size_t>(c[i].rank) * T * sizeof(float));
+    const size_t chunks = static_cast<size_t>(w[0].d_in) / (32 / w[0].bits) / 4;
+    total += up256(static_cast<size_t>(T) * w[0].d_in * 2);
+    total += up256(static_cast<size_t>(T) * chunks * sizeof(float));
+    return total;
 }
 
-size_t decode_workspace_bytes(const QW& w, const LR& c, int T) { return ws_layout(w, c, T).total; }
-
-bool decode_fits(const QW& w, const LR&) {
+bool decode_fits(const QW& w) {
     const int chunks = w.d_in / (32 / w.bits) / 4;
     return chunks <= 8 * 64 * 2;     // at most 8 K slices of 128 chunks
 }
 
-hipError_t launch_linear_decode(const QW& w, const LR& c, const void* x, int T, int act, void* y,
-                                int out, void* ws, hipStream_t st) {
-    const Plan p = plan(w, c, T);
+hipError_t launch_linear_decode(int n, const QW* w, const LR* c, const void* x, int T, int act,
+                                void* const* y, int out, void* ws, hipStream_t st) {
+    const int d_in = w[0].d_in, bits = w[0].bits;
+    int max_rank = 0;
+    for (int i = 0; i < n; ++i) max_rank = max(max_rank, c[i].rank);
+    const Plan p = plan(d_in, bits, max_rank, T);
     // the kernel is built for at most 8 waves (launch bounds, LDS arrays)
-    if (p.ks > 8 || p.threads > 512 || p.threads % (64 * p.ks)) return hipErrorInvalidConfiguration;
-    const WsLayout l = ws_layout(w, c, T);
+    if (n < 1 || n > kMaxWin || p.ks > 8 || p.threads > 512 || p.threads % (64 * p.ks))
+        return hipErrorInvalidConfiguration;
     char* wsb = static_cast<char*>(ws);
-    float* t = reinterpret_cast<float*>(wsb + l.t);
-    f16x2* xp = reinterpret_cast<f16x2*>(wsb + l.xp);
-    float* sx = reinterpret_cast<float*>(wsb + l.sx);
-    const int chunks = w.d_in / (32 / w.bits) / 4;
-    const long long items = static_cast<long long>(T) * chunks;
-    const unsigned grid = static_cast<unsigned>(c.rank + (items + 255) / 256);
-    const uint16_t* xs = static_cast<const uint16_t*>(x);
-    if (w.bits == 4)
-        hipLaunchKernelGGL(decode_prep_kernel<4>, dim3(grid), dim3(256), 0, st, c.A, xs, t, xp, sx, w.d_in, c.rank, T, act);
-    else
-        hipLaunchKernelGGL(decode_prep_kernel<2>, dim3(grid), dim3(256), 0, st, c.A, xs, t, xp, sx, w.d_in, c.rank, T, act);
-    hipError_t e = hipGetLastError();
+    PrepArgs pa;
     DecodeArgs a;
-    a.q = w.q; a.s = w.s; a.z = w.z; a.A = c.A; a.B = c.B;
-    a.xp = xp; a.y = y;
-    a.d_out = w.d_out; a.d_in = w.d_in; a.G = w.G; a.rank = c.rank; a.r_max = c.r_max;
-    a.T = T; a.act = act; a.out = out;
-    a.ks = p.ks; a.cps = p.cps;
+    size_t off = 0;
+    int rank_end = 0, batch_end = 0;
+    const int rg_per_block = p.threads / 64 / p.ks;
+    for (int i = 0; i < n; ++i) {
+        float* t = reinterpret_cast<float*>(wsb + off);
+        off += up256(static_cast<size_t>(c[i].rank) * T * sizeof(float));
+        rank_end += c[i].rank;
+        pa.A[i] = c[i].A;
+        pa.t[i] = t;
+        pa.rank_end[i] = rank_end;
+        const int rgroups = (w[i].d_out + p.R - 1) / p.R;
+        batch_end += (rgroups + rg_per_block - 1) / rg_per_block;
+        a.lin[i] = Lin{w[i].q, w[i].s, w[i].z, c[i].B, y[i], t, w[i].d_out, c[i].rank, c[i].r_max, batch_end};
+    }
+    const int chunks = d_in / (32 / bits) / 4;
+    f16x2* xp = reinterpret_cast<f16x2*>(wsb + off);
+    off += up256(static_cast<size_t>(T) * d_in * 2);
+    float* sx = reinterpret_cast<float*>(wsb + off);
+    pa.n = n;
+    pa.x = static_cast<const uint16_t*>(x);
+    pa.xp = xp;
+    pa.sx = sx;
+    pa.d_in = d_in;
+    pa.T = T;
+    pa.act = act;
+    const long long items = static_cast<long long>(T) * chunks;
+    const unsigned grid = static_cast<unsigned>(rank_end + (items + 255) / 256);
+    if (bits == 4)
+        hipLaunchKernelGGL(decode_prep_kernel<4>, dim3(grid), dim3(256), 0, st, pa);
+    else
+        hipLaunchKernelGGL(decode_prep_kernel<2>, dim3(grid), dim3(256), 0, st, pa);
+    hipError_t e = hipGetLastError();
+    a.n = n;
+    a.xp = xp;
+    a.sx = sx;
+    a.d_in = d_in;
+    a.G = w[0].G;
+    a.T = T;
+    a.out = out;
+    a.ks = p.ks;
+    a.cps = p.cps;
     for (int tok0 = 0; tok0 < T && e == hipSuccess; tok0 += p.nt) {
         a.tok0 = tok0;
-        a.t = t + static_cast<size_t>(tok0) * c.rank;
-        a.sx = sx;
-        e = w.bits == 4 ? launch2<4>(a, p, p.nt, st) : launch2<2>(a, p, p.nt, st);
+        e = bits == 4 ? launch2<4>(a, p, st) : launch2<2>(a, p, st);
     }
     return e;
 }

@@ -108,3 +108,22 @@ def test_quantize_pack_and_dequantize_validate():
     assert lib.cl_dequantize(ctypes.byref(qw), p, None) == cl.CL_EINVAL
     qw = _qw()
     assert lib.cl_dequantize(ctypes.byref(qw), None, None) == cl.CL_EINVAL
+
+
+def test_window_validation():
+    lib = cl.lib()
+    q = (cl.QWeightC * 3)(_qw(), _qw(d_out=32), _qw(d_in=512))
+    yp = (ctypes.c_void_p * 3)(FAKE, FAKE, FAKE)
+    args = lambda n, qa, **kw: lib.cl_linear_decode_window(
+        n, qa, None, ctypes.c_void_p(FAKE), kw.get("T", 1), cl.CL_FP16, yp, cl.CL_FP16,
+        ctypes.c_void_p(FAKE), 1 << 20, None)
+    assert args(0, q) == cl.CL_EINVAL
+    assert args(9, q) == cl.CL_EINVAL
+    assert args(3, q) == cl.CL_EINVAL and b"share d_in" in lib.cl_last_error()
+    assert lib.cl_linear_window_workspace(3, q, None, 1) == 0
+    q2 = (cl.QWeightC * 2)(_qw(), _qw(d_out=32))
+    n2 = lib.cl_linear_window_workspace(2, q2, None, 1)
+    assert n2 > 0
+    ybad = (ctypes.c_void_p * 2)(FAKE, 0)
+    assert lib.cl_linear_decode_window(2, q2, None, ctypes.c_void_p(FAKE), 1, cl.CL_FP16, ybad, cl.CL_FP16,
+                                       ctypes.c_void_p(FAKE), 1 << 20, None) == cl.CL_EINVAL

@@ -184,3 +184,38 @@ def test_wide_input_uses_eight_k_slices(bits, G):
     y = cl.linear_decode(w, c, dev_u16(x.bits, torch.float16), out_dtype=torch.float32)
     ref = linear.forward_packed(Q, s, z, bits, G, A, B, 32, x.values)
     assert rel_l2(out_to_numpy(y), ref) <= REL_L2_TOL
+
+
+@pytest.mark.parametrize("T,act", [(1, "fp16"), (4, "bf16"), (16, "fp16")])
+def test_window_matches_single_calls_bitwise_and_oracle(T, act):
+    """A Q/K/V-shaped window (4096/1024/1024 x 2048, ranks 64/0/17) equals the
+    three single calls bit for bit, and the oracle within tolerance."""
+    dt = torch.float16 if act == "fp16" else torch.bfloat16
+    shapes, ranks = [(4096, 2048), (1024, 2048), (1024, 2048)], [64, 0, 17]
+    ws_, cs, host = [], [], []
+    for i, ((d_out, d_in), rank) in enumerate(zip(shapes, ranks)):
+        w, c, h = _layer_dev(d_out, d_in, 4, 128, 64, rank, 60 + i)
+        ws_.append(w); cs.append(c); host.append(h)
+    x = wl.activation((T, 2048), 12, 60, dtype=act)
+    xd = dev_u16(x.bits, dt)
+    ys = cl.linear_decode_window(ws_, cs, xd, out_dtype=torch.float32)
+    for i, (w, c, (Q, s, z, A, B), rank) in enumerate(zip(ws_, cs, host, ranks)):
+        y1 = cl.linear_decode(w, c, xd, out_dtype=torch.float32)
+        assert torch.equal(ys[i], y1), i
+        rows = np.random.default_rng(i).choice(w.d_out, 200, replace=False)
+        ref = linear.forward_rows(Q, s, z, 4, 128, A, B, rank, x.values, rows)
+        assert rel_l2(out_to_numpy(ys[i])[:, rows], ref) <= REL_L2_TOL
+
+
+def test_window_without_factors_and_two_bit():
+    ws_, host = [], []
+    for i in range(2):
+        W = wl.weight((700 + 100 * i, 1024), 13, i)
+        Q, s, z = quant.quantize_pack(W, 2, 64)
+        ws_.append(cl.QWeight(dev_u32(Q), dev_f16(s), dev_f16(z), W.shape[0], 1024, 2, 64))
+        host.append((Q, s, z))
+    x = wl.activation((3, 1024), 13, 9)
+    ys = cl.linear_decode_window(ws_, None, dev_u16(x.bits, torch.float16), out_dtype=torch.float32)
+    for y, (Q, s, z) in zip(ys, host):
+        ref = linear.forward_packed(Q, s, z, 2, 64, None, None, 0, x.values)
+        assert rel_l2(out_to_numpy(y), ref) <= REL_L2_TOL
