@@ -50,6 +50,10 @@ _SIGNATURES = {
     "cl_linear_decode": (ctypes.c_int32, [ctypes.POINTER(QWeightC), ctypes.POINTER(LowRankC), ctypes.c_void_p,
                                           ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32,
                                           ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
+    "cl_prefill_workspace": (ctypes.c_size_t, [ctypes.POINTER(QWeightC), ctypes.POINTER(LowRankC), ctypes.c_int32]),
+    "cl_linear_prefill": (ctypes.c_int32, [ctypes.POINTER(QWeightC), ctypes.POINTER(LowRankC), ctypes.c_void_p,
+                                           ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32,
+                                           ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
     "cl_linear_window_workspace": (ctypes.c_size_t, [ctypes.c_int32, ctypes.POINTER(QWeightC),
                                                      ctypes.POINTER(LowRankC), ctypes.c_int32]),
     "cl_linear_decode_window": (ctypes.c_int32, [ctypes.c_int32, ctypes.POINTER(QWeightC), ctypes.POINTER(LowRankC),
@@ -193,3 +197,25 @@ def linear_decode_window(ws_, cs, x, out_dtype=torch.float16, ys=None, ws=None, 
     _check(lib().cl_linear_decode_window(n, qa, la, _ptr(x), T, _DTYPE_CODE[x.dtype], yp,
                                          _DTYPE_CODE[ys[0].dtype], _ptr(ws), ws.numel(), _stream(stream)))
     return ys
+
+
+def prefill_workspace(w, c, M):
+    qc = w.c()
+    lc = c.c() if c is not None else None
+    return lib().cl_prefill_workspace(ctypes.byref(qc), ctypes.byref(lc) if lc else None, M)
+
+
+def linear_prefill(w, c, X, out_dtype=torch.float16, Y=None, ws=None, stream=None):
+    """``cl_linear_prefill``: X [M][d_in] fp16/bf16 -> Y [M][d_out] of out_dtype."""
+    M = X.shape[0]
+    if Y is None:
+        Y = torch.empty((M, w.d_out), dtype=out_dtype, device=X.device)
+    need = prefill_workspace(w, c, M)
+    if ws is None and need:
+        ws = workspace(need, X.device)
+    qc = w.c()
+    lc = c.c() if c is not None else None
+    _check(lib().cl_linear_prefill(ctypes.byref(qc), ctypes.byref(lc) if lc else None, _ptr(X), M,
+                                   _DTYPE_CODE[X.dtype], _ptr(Y), _DTYPE_CODE[Y.dtype], _ptr(ws),
+                                   0 if ws is None else ws.numel(), _stream(stream)))
+    return Y

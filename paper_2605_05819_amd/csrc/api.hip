@@ -171,6 +171,44 @@ cl_status cl_linear_decode(const cl_qweight* w, const cl_lowrank* c, const void*
                          "cl_linear_decode");
 }
 
+size_t cl_prefill_workspace(const cl_qweight* w, const cl_lowrank* c, int32_t M) {
+    char saved[sizeof(g_err)];
+    memcpy(saved, g_err, sizeof(g_err));
+    cl::QW qw;
+    cl::LR lr;
+    size_t bytes = 0;
+    if (M >= 1 && check_qweight(w, &qw, "") == CL_OK && check_lowrank(c, qw, &lr, "") == CL_OK)
+        bytes = cl::prefill_workspace_bytes(qw, lr, M);
+    memcpy(g_err, saved, sizeof(g_err));
+    return bytes;
+}
+
+cl_status cl_linear_prefill(const cl_qweight* w, const cl_lowrank* c, const void* X, int32_t M, int32_t act_dtype,
+                            void* Y, int32_t out_dtype, void* ws, size_t ws_bytes, void* stream) {
+    const char* who = "cl_linear_prefill";
+    cl::QW qw;
+    cl::LR lr;
+    cl_status st = check_qweight(w, &qw, who);
+    if (st) return st;
+    st = check_lowrank(c, qw, &lr, who);
+    if (st) return st;
+    if (qw.d_in % 64) return fail(CL_EUNSUPPORTED, "%s: d_in must be a multiple of 64 (got %d)", who, qw.d_in);
+    if (M < 1) return fail(CL_EINVAL, "%s: M must be >= 1 (got %d)", who, M);
+    if (act_dtype != CL_FP16 && act_dtype != CL_BF16)
+        return fail(CL_EINVAL, "%s: act_dtype must be CL_FP16 or CL_BF16", who);
+    if (out_dtype != CL_FP16 && out_dtype != CL_BF16 && out_dtype != CL_FP32)
+        return fail(CL_EINVAL, "%s: out_dtype must be CL_FP16, CL_BF16 or CL_FP32", who);
+    if (!X || !Y) return fail(CL_EINVAL, "%s: null X or Y", who);
+    if (!aligned(X, 16)) return fail(CL_EINVAL, "%s: X must be 16-byte aligned", who);
+    if (!aligned(Y, out_dtype == CL_FP32 ? 4 : 2)) return fail(CL_EINVAL, "%s: misaligned Y", who);
+    const size_t need = cl::prefill_workspace_bytes(qw, lr, M);
+    if (need > 0 && (!ws || ws_bytes < need))
+        return fail(CL_EWORKSPACE, "%s: workspace of %zu bytes needed (got %zu)", who, need, ws ? ws_bytes : 0);
+    if (need > 0 && !aligned(ws, 256)) return fail(CL_EINVAL, "%s: workspace must be 256-byte aligned", who);
+    return hip_status(cl::launch_linear_prefill(qw, lr, X, M, act_dtype, Y, out_dtype, ws,
+                                                static_cast<hipStream_t>(stream)), who);
+}
+
 cl_status cl_linear_decode_window(int32_t n, const cl_qweight* w, const cl_lowrank* c, const void* x,
                                   int32_t T, int32_t act_dtype, void* const* y, int32_t out_dtype, void* ws,
                                   size_t ws_bytes, void* stream) {

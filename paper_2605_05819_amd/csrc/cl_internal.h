@@ -33,4 +33,10 @@ bool decode_fits(const QW& w);   // d_in within the kernel's K-slice limit
 hipError_t launch_linear_decode(int n, const QW* w, const LR* c, const void* x, int T, int act,
                                 void* const* y, int out, void* ws, hipStream_t st);
 
+// Prefill: T = X A^T into the workspace, then the MFMA GEMM with the rank
+// fold; d_in must be a multiple of 64.
+size_t prefill_workspace_bytes(const QW& w, const LR& c, int M);
+hipError_t launch_linear_prefill(const QW& w, const LR& c, const void* X, int M, int act, void* Y, int out,
+                                 void* ws, hipStream_t st);
+
 }  // namespace cl
