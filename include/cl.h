@@ -200,6 +200,41 @@ cl_status cl_linear_prefill(const cl_qweight* w, const cl_lowrank* c, const void
 /* Workspace bytes for cl_linear_prefill (0 for rank 0 or rejected arguments). */
 size_t cl_prefill_workspace(const cl_qweight* w, const cl_lowrank* c, int32_t M);
 
+/*
+ * cl_moe_linear_decode -- compensated linear of a MoE layer for a few decode
+ * tokens: for every token t and routing slot j with expert e = ids[t][j],
+ *     y[t][j] = deq(Q_e) x + B_e[:, :r_e] (A_e[:r_e] x),
+ * x = x[t] (x_per_slot = 0, e.g. gate/up) or x[t][j] (x_per_slot = 1, e.g.
+ * down).  All routed experts' same projection is processed in one step, the
+ * paper's cross-expert reorganisation (Section 4.2.2; Appendix A.1, MoE
+ * Layer); only routed experts' codes, scales, zeros and factors are read.
+ * Two kernels are enqueued (routing + A x + activation preparation, then the
+ * backbone over every routed expert).
+ *
+ *  w_expert0  descriptor of expert 0; experts are stacked contiguously: expert
+ *             e's q, scales and zeros start e times one expert's size after
+ *             expert 0's
+ *  A          device fp16 [E][r_max][d_in];  B  device fp16 [E][d_out][r_max]
+ *             (both may be NULL when r_max = 0)
+ *  ranks      device int32 [E], expert e's rank (clamped to 0..r_max)
+ *  x          device [T][d_in] or [T][k][d_in] of act_dtype, 16-byte aligned
+ *  topk_ids   device int32 [T][k]; an id outside 0..E-1 gives a zero row
+ *  y          device [T][k][d_out] of out_dtype
+ *  ws         device workspace of cl_moe_workspace(...) bytes, 256-byte aligned
+ * Limits: E <= 1024, T in 1..64, T*k <= 1024, r_max <= 256, d_in <= 8192 * bits
+ *         (16384 for 4-bit); beyond them CL_EUNSUPPORTED.
+ * Errors: as cl_linear_decode.
+ */
+cl_status cl_moe_linear_decode(const cl_qweight* w_expert0, const uint16_t* A, const uint16_t* B,
+                               int32_t r_max, const int32_t* ranks, int32_t num_experts, const void* x,
+                               int32_t x_per_slot, const int32_t* topk_ids, int32_t T, int32_t k,
+                               int32_t act_dtype, void* y, int32_t out_dtype, void* ws, size_t ws_bytes,
+                               void* stream);
+
+/* Workspace bytes for cl_moe_linear_decode (0 for rejected arguments). */
+size_t cl_moe_workspace(const cl_qweight* w_expert0, int32_t r_max, int32_t num_experts, int32_t T,
+                        int32_t k, int32_t x_per_slot);
+
 /* Message describing the last non-CL_OK status returned on this thread. */
 const char* cl_last_error(void);
 

@@ -34,3 +34,21 @@ def forward(experts, ranks, X, ids, x_per_slot):
             x = X[t, j] if x_per_slot else X[t]
             Y[t, j] = linear.forward(W_hat, A, B, int(ranks[e]), np.asarray(x)[None, :])[0]
     return Y
+
+
+def forward_rows(packed, ranks, X, ids, x_per_slot, rows, bits, group_size):
+    """:func:`forward` on output rows ``rows`` only, from packed experts
+    ``packed[e] = (Q_e, scales_e, zeros_e, A_e, B_e)``: each slot's rows come
+    from :func:`linear.forward_rows` of its expert.  Returns fp64
+    ``[T][k][len(rows)]``."""
+    ids = np.asarray(ids)
+    T, k = ids.shape
+    rows = np.asarray(rows)
+    Y = np.zeros((T, k, len(rows)), dtype=np.float64)
+    for t in range(T):
+        for j in range(k):
+            Q, s, z, A, B = packed[int(ids[t, j])]
+            x = X[t, j] if x_per_slot else X[t]
+            Y[t, j] = linear.forward_rows(Q, s, z, bits, group_size, A, B, int(ranks[int(ids[t, j])]),
+                                          np.asarray(x)[None, :], rows)[0]
+    return Y

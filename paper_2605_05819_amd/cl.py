@@ -54,6 +54,13 @@ _SIGNATURES = {
     "cl_linear_prefill": (ctypes.c_int32, [ctypes.POINTER(QWeightC), ctypes.POINTER(LowRankC), ctypes.c_void_p,
                                            ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32,
                                            ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
+    "cl_moe_workspace": (ctypes.c_size_t, [ctypes.POINTER(QWeightC), ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                            ctypes.c_int32, ctypes.c_int32]),
+    "cl_moe_linear_decode": (ctypes.c_int32, [ctypes.POINTER(QWeightC), ctypes.c_void_p, ctypes.c_void_p,
+                                              ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p,
+                                              ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
+                                              ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p,
+                                              ctypes.c_size_t, ctypes.c_void_p]),
     "cl_linear_window_workspace": (ctypes.c_size_t, [ctypes.c_int32, ctypes.POINTER(QWeightC),
                                                      ctypes.POINTER(LowRankC), ctypes.c_int32]),
     "cl_linear_decode_window": (ctypes.c_int32, [ctypes.c_int32, ctypes.POINTER(QWeightC), ctypes.POINTER(LowRankC),
@@ -219,3 +226,48 @@ def linear_prefill(w, c, X, out_dtype=torch.float16, Y=None, ws=None, stream=Non
                                    _DTYPE_CODE[X.dtype], _ptr(Y), _DTYPE_CODE[Y.dtype], _ptr(ws),
                                    0 if ws is None else ws.numel(), _stream(stream)))
     return Y
+
+
+@dataclass
+class MoeExperts:
+    """Stacked experts of one MoE projection on the device: q [E][d_out][...],
+    scales/zeros [E][d_out][d_in/G], A [E][r_max][d_in], B [E][d_out][r_max],
+    ranks int32 [E]."""
+    q: torch.Tensor
+    scales: torch.Tensor
+    zeros: torch.Tensor
+    A: Optional[torch.Tensor]
+    B: Optional[torch.Tensor]
+    ranks: Optional[torch.Tensor]
+    num_experts: int
+    d_out: int
+    d_in: int
+    bits: int
+    group_size: int
+    r_max: int
+
+    def expert0(self):
+        return QWeightC(self.q.data_ptr(), self.scales.data_ptr(), self.zeros.data_ptr(), self.d_out, self.d_in,
+                        self.bits, self.group_size)
+
+
+def moe_workspace(ex, T, k, x_per_slot):
+    q0 = ex.expert0()
+    return lib().cl_moe_workspace(ctypes.byref(q0), ex.r_max, ex.num_experts, T, k, int(bool(x_per_slot)))
+
+
+def moe_linear_decode(ex, x, topk_ids, out_dtype=torch.float16, y=None, ws=None, stream=None):
+    """``cl_moe_linear_decode``: x [T][d_in] (shared) or [T][k][d_in] (per
+    slot), topk_ids int32 [T][k] -> y [T][k][d_out]."""
+    T, k = topk_ids.shape
+    x_per_slot = x.dim() == 3
+    if y is None:
+        y = torch.empty((T, k, ex.d_out), dtype=out_dtype, device=x.device)
+    if ws is None:
+        ws = workspace(moe_workspace(ex, T, k, x_per_slot), x.device)
+    q0 = ex.expert0()
+    _check(lib().cl_moe_linear_decode(ctypes.byref(q0), _ptr(ex.A), _ptr(ex.B), ex.r_max, _ptr(ex.ranks),
+                                      ex.num_experts, _ptr(x), int(x_per_slot), _ptr(topk_ids), T, k,
+                                      _DTYPE_CODE[x.dtype], _ptr(y), _DTYPE_CODE[y.dtype], _ptr(ws), ws.numel(),
+                                      _stream(stream)))
+    return y

@@ -39,4 +39,12 @@ size_t prefill_workspace_bytes(const QW& w, const LR& c, int M);
 hipError_t launch_linear_prefill(const QW& w, const LR& c, const void* X, int M, int act, void* Y, int out,
                                  void* ws, hipStream_t st);
 
+// MoE decode over stacked experts (expert e's arrays at e times one expert's
+// size); arguments already validated.
+bool moe_fits(const QW& w, int E, int T, int k);
+size_t moe_workspace_bytes(const QW& w, int r_max, int E, int T, int k, int x_per_slot);
+hipError_t launch_moe_decode(const QW& w, const uint16_t* A, const uint16_t* B, int r_max, const int32_t* ranks,
+                             int E, const void* x, int x_per_slot, const int32_t* ids, int T, int k, int act,
+                             void* y, int out, void* ws, hipStream_t st);
+
 }  // namespace cl

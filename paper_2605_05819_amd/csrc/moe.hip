@@ -1,0 +1,408 @@
+// Expert-gathered compensated linear for a MoE layer (decode):
+//
+//     y[t][j] = deq(Q_e) x + B_e[:, :r_e] (A_e[:r_e] x),   e = ids[t][j]
+//
+// with x = x[t] (shared by a token's slots, e.g. gate/up) or x[t][j] (the
+// slot's own input, e.g. down).  The paper regroups the same projection of
+// all activated experts into one step (Section 4.2.2, Cross-Expert Pipeline
+// Reorganization; Appendix A.1, MoE Layer); here that is one pair of launches
+// over every routed expert, and only routed experts' codes, scales, zeros and
+// factors are read.
+//
+//  * moe_prep_kernel: workgroup e (one per expert) scans the routing table --
+//    so no workgroup ever waits for another -- and, if expert e is routed,
+//    writes its entry of the active-expert table (index = number of routed
+//    experts below e), its slots in slot order into the sorted slot list, and
+//    t = A_e[:r_e] x for each of its slots (A_e read once).  Workgroup 0 also
+//    writes the number of routed experts and zero rows for slots whose id is
+//    out of range.  The remaining workgroups prepare the activations (fp16,
+//    pair-permuted, per-chunk sums) exactly as the dense decode does.
+//  * moe_kernel: one workgroup per (active expert, row batch); the grid is
+//    sized for the most experts T*k slots can reach and surplus workgroups
+//    exit on the device-side count.  Each loads its 4-row x 1-chunk-per-lane
+//    slice of the expert's backbone and factor entries once and applies them
+//    to every slot routed to that expert (same arithmetic as the dense
+//    decode kernel: mask-only unpack into subnormal fp16 lanes, v_dot2,
+//    per-chunk scale and zero in fp32, B t in the same partial sums,
+//    transposing butterfly, fixed-order K-slice reduction).
+
+#include "cl_device.h"
+#include "cl_internal.h"
+#include "gemv_common.h"
+
+namespace cl {
+
+namespace {
+
+constexpr int kR = 4;                // rows per wave batch
+constexpr int kMaxSlots = 1024;      // T * k
+constexpr int kMaxExperts = 1024;
+
+struct MoeArgs {
+    const uint32_t* q;
+    const uint16_t* s;
+    const uint16_t* z;
+    const uint16_t* A;
+    const uint16_t* B;
+    const int32_t* ranks;
+    const int32_t* ids;
+    const uint16_t* x;
+    void* y;
+    size_t q_stride, sz_stride, a_stride, b_stride;   // elements per expert
+    int E, T, k, d_out, d_in, G, r_max, act, out, x_per_slot;
+    // workspace
+    int* n_active;
+    int* table;              // [max_active][4]: expert, first slot, slot count, rank
+    int* sorted;             // [T*k] slot ids grouped by expert, slot order within
+    float* t;                // [T*k][r_max]
+    f16x2* xp;               // [rows][d_in/2]
+    float* sx;               // [rows][chunks]
+    int ks, cps, bpe;        // K slices, chunks per slice, batches per expert
+};
+
+template <int BITS>
+__global__ __launch_bounds__(256) void moe_prep_kernel(MoeArgs a) {
+    constexpr int CPW = 32 / BITS, HPW = CPW / 2, PPC = 4 * HPW;
+    __shared__ int sids[kMaxSlots];
+    __shared__ int mys[kMaxSlots];          // this expert's slots, in slot order
+    __shared__ unsigned routed[kMaxExperts / 32];
+    __shared__ int cnt_lt, cnt_eq;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int S = a.T * a.k;
+    const int blk = blockIdx.x;
+
+    if (blk < a.E) {
+        const int e = blk;
+        for (int i = tid; i < kMaxExperts / 32; i += 256) routed[i] = 0u;
+        if (tid == 0) { cnt_lt = 0; cnt_eq = 0; }
+        __syncthreads();
+        int lt = 0, eq = 0;
+        for (int sl = tid; sl < S; sl += 256) {
+            const int id = a.ids[sl];
+            sids[sl] = id;
+            if (id >= 0 && id < a.E) {
+                atomicOr(&routed[id >> 5], 1u << (id & 31));
+                lt += id < e;
+                eq += id == e;
+            }
+        }
+        atomicAdd(&cnt_lt, lt);
+        atomicAdd(&cnt_eq, eq);
+        __syncthreads();
+        if (e == 0) {
+            if (tid == 0) {
+                int n = 0;
+                for (int i = 0; i < (a.E + 31) / 32; ++i) n += __popc(routed[i]);
+                *a.n_active = n;
+            }
+            // out-of-range ids: their output rows are zero
+            for (int sl = 0; sl < S; ++sl) {
+                const int id = sids[sl];
+                if (id >= 0 && id < a.E) continue;
+                for (int o = tid; o < a.d_out; o += 256) store_out(a.y, static_cast<size_t>(sl) * a.d_out + o, 0.f, a.out);
+            }
+        }
+        const int ne = cnt_eq;
+        if (ne == 0) return;
+        int ae = 0;
+        for (int i = 0; i < (e >> 5); ++i) ae += __popc(routed[i]);
+        ae += __popc(routed[e >> 5] & ((1u << (e & 31)) - 1u));
+        int rank = a.r_max > 0 ? a.ranks[e] : 0;     // ranks may be null when r_max is 0
+        rank = rank < 0 ? 0 : (rank > a.r_max ? a.r_max : rank);
+        if (tid == 0) {
+            a.table[4 * ae + 0] = e;
+            a.table[4 * ae + 1] = cnt_lt;
+            a.table[4 * ae + 2] = ne;
+            a.table[4 * ae + 3] = rank;
+        }
+        // this expert's slots in slot order
+        for (int sl = tid; sl < S; sl += 256) {
+            if (sids[sl] != e) continue;
+            int pos = 0;
+            for (int s2 = 0; s2 < sl; ++s2) pos += sids[s2] == e;
+            a.sorted[cnt_lt + pos] = sl;
+            mys[pos] = sl;
+        }
+        __syncthreads();
+        // t[slot][i] = A_e[i] . x_slot for i < rank: one wave per (slot, i)
+        if (rank > 0) {
+            const uint16_t* Ae = a.A + static_cast<size_t>(e) * a.a_stride;
+            for (int item = wave; item < ne * rank; item += 4) {
+                const int jj = item / rank, i = item - jj * rank;
+                const int sl = mys[jj];
+                const int xrow = a.x_per_slot ? sl : sl / a.k;
+                const uint16_t* xr = a.x + static_cast<size_t>(xrow) * a.d_in;
+                const uint16_t* ar = Ae + static_cast<size_t>(i) * a.d_in;
+                float acc = 0.f;
+                for (int c = lane * 8; c < a.d_in; c += 64 * 8) {
+                    const u32x4 av = *reinterpret_cast<const u32x4*>(ar + c);
+                    uint32_t xw[4];
+                    load8_f16(xr + c, a.act, xw);
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        // copy the vector element to a scalar first: a bit_cast
+                        // of a subscripted ext_vector reads element 0
+                        const uint32_t aq = av[q], xq = xw[q];
+                        acc = dot2(__builtin_bit_cast(f16x2, aq), __builtin_bit_cast(f16x2, xq), acc);
+                    }
+                }
+                acc = wave_sum(acc);
+                if (lane == 0) a.t[static_cast<size_t>(sl) * a.r_max + i] = acc;
+            }
+        }
+        return;
+    }
+    // activation preparation, one thread per (row, chunk)
+    const int rows = a.x_per_slot ? S : a.T;
+    const int chunks = a.d_in / CPW / 4;
+    const long long item = static_cast<long long>(blk - a.E) * 256 + tid;
+    if (item >= static_cast<long long>(rows) * chunks) return;
+    const int row = static_cast<int>(item / chunks);
+    const int c = static_cast<int>(item % chunks);
+    f16x2 v[PPC];
+    load_chunk_x<BITS>(a.x + static_cast<size_t>(row) * a.d_in, c, a.act, v);
+    const f16x2 one = {static_cast<f16>(1.0f), static_cast<f16>(1.0f)};
+    float sum = 0.f;
+    f16x2* dst = a.xp + static_cast<size_t>(row) * (a.d_in / 2) + static_cast<size_t>(c) * PPC;
+#pragma unroll
+    for (int p = 0; p < PPC; ++p) {
+        sum = dot2(v[p], one, sum);
+        dst[p] = v[p];
+    }
+    a.sx[static_cast<size_t>(row) * chunks + c] = sum;
+}
+
+// NB: factor columns per lane (r_max <= NB * 64 * ks); 0 when r_max is 0.
+template <int BITS, int CPL, int NB>
+__global__ __launch_bounds__(512) void moe_kernel(MoeArgs a) {
+    constexpr int R = kR;
+    constexpr int CPW = 32 / BITS;
+    constexpr int HPW = CPW / 2;
+    constexpr int CPC = 4 * CPW;
+    constexpr int PPC = 4 * HPW;
+    constexpr int NACC = BITS == 4 ? 2 : 4;
+    constexpr int NBA = NB > 0 ? NB : 1;
+    __shared__ float red[8][R];
+
+    const int ae = blockIdx.x / a.bpe;
+    if (ae >= *a.n_active) return;                  // whole workgroup: no routed expert here
+    const int batch = blockIdx.x - ae * a.bpe;
+    const int e = a.table[4 * ae + 0];
+    const int sbeg = a.table[4 * ae + 1];
+    const int scnt = a.table[4 * ae + 2];
+    const int rank = a.table[4 * ae + 3];
+
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int waves = blockDim.x >> 6;
+    const int ks = a.ks;
+    const int rg_per_block = waves / ks;
+    const int slice = wave % ks;
+    const int rgw = wave / ks;
+    const int words = a.d_in / CPW;
+    const int chunks = words / 4;
+    const int groups = a.d_in / a.G;
+    const int c_begin = slice * a.cps;
+    const int c_end = min(chunks, c_begin + a.cps);
+    const int row0 = (batch * rg_per_block + rgw) * R;
+    const bool active = row0 < a.d_out;
+    const int base = active ? row0 : 0;
+    const int nrows = active ? min(R, a.d_out - row0) : 1;
+
+    int cidx[CPL];
+    float cmask[CPL];
+#pragma unroll
+    for (int j = 0; j < CPL; ++j) {
+        cidx[j] = c_begin + lane + 64 * j;
+        const bool valid = cidx[j] < c_end;
+        cmask[j] = valid ? 1.f : 0.f;
+        if (!valid) cidx[j] = c_begin;
+    }
+
+    // this expert's rows: codes, scales, zeros, factor entries (loaded once)
+    const uint32_t* qe = a.q + static_cast<size_t>(e) * a.q_stride;
+    const uint16_t* se = a.s + static_cast<size_t>(e) * a.sz_stride;
+    const uint16_t* ze = a.z + static_cast<size_t>(e) * a.sz_stride;
+    u32x4 qv[R][CPL];
+    float sc[R][CPL], zc[R][CPL];
+    float bv[R][NBA];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const int row = base + (r < nrows ? r : 0);
+        const u32x4* qr = reinterpret_cast<const u32x4*>(qe + static_cast<size_t>(row) * words);
+#pragma unroll
+        for (int j = 0; j < CPL; ++j) {
+            qv[r][j] = __builtin_nontemporal_load(qr + cidx[j]);
+            const size_t gi = static_cast<size_t>(row) * groups + (cidx[j] * CPC) / a.G;
+            sc[r][j] = f16_bits_to_f32(se[gi]) * cmask[j];
+            zc[r][j] = f16_bits_to_f32(ze[gi]);
+        }
+#pragma unroll
+        for (int m = 0; m < NB; ++m) {
+            const int i = lane + 64 * (slice + ks * m);
+            const uint16_t* Be = a.B + static_cast<size_t>(e) * a.b_stride;
+            bv[r][m] = i < rank ? f16_bits_to_f32(Be[static_cast<size_t>(row) * a.r_max + i]) : 0.f;
+        }
+    }
+
+    for (int jslot = 0; jslot < scnt; ++jslot) {
+        const int sl = a.sorted[sbeg + jslot];
+        const int xrow = a.x_per_slot ? sl : sl / a.k;
+        float acc[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r) acc[r] = 0.f;
+#pragma unroll
+        for (int j = 0; j < CPL; ++j) {
+            f16x2 xv[PPC];
+            const u32x4* src = reinterpret_cast<const u32x4*>(a.xp + static_cast<size_t>(xrow) * (a.d_in / 2) +
+                                                              static_cast<size_t>(cidx[j]) * PPC);
+#pragma unroll
+            for (int p4 = 0; p4 < PPC / 4; ++p4) {
+                const u32x4 u = src[p4];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const uint32_t uq = u[q];
+                    xv[4 * p4 + q] = __builtin_bit_cast(f16x2, uq);
+                }
+            }
+            const float sxv = a.sx[static_cast<size_t>(xrow) * chunks + cidx[j]];
+#pragma unroll
+            for (int r = 0; r < R; ++r) {
+                float d[NACC];
+#pragma unroll
+                for (int q = 0; q < NACC; ++q) d[q] = 0.f;
+#pragma unroll
+                for (int w = 0; w < 4; ++w) dot_word<BITS>(qv[r][j][w], xv + w * HPW, d);
+                const float v = fmaf(combine<BITS>(d), 16777216.0f, -zc[r][j] * sxv);
+                acc[r] = fmaf(sc[r][j], v, acc[r]);
+            }
+        }
+#pragma unroll
+        for (int m = 0; m < NB; ++m) {
+            const int i = lane + 64 * (slice + ks * m);
+            const float tv = i < rank ? a.t[static_cast<size_t>(sl) * a.r_max + i] : 0.f;
+#pragma unroll
+            for (int r = 0; r < R; ++r) acc[r] = fmaf(bv[r][m], tv, acc[r]);
+        }
+        const float tot = wave_sum_multi<R>(acc);
+        constexpr int SPAN = 64 / R;
+        const int rr = (lane / SPAN) & (R - 1);
+        if (ks == 1) {
+            if ((lane & (SPAN - 1)) == 0 && active && row0 + rr < a.d_out)
+                store_out(a.y, static_cast<size_t>(sl) * a.d_out + row0 + rr, tot, a.out);
+        } else {
+            if ((lane & (SPAN - 1)) == 0) red[wave][rr] = tot;
+            __syncthreads();
+            if (slice == 0 && lane < R && active && row0 + lane < a.d_out) {
+                float v = 0.f;
+                for (int kk = 0; kk < ks; ++kk) v += red[wave + kk][lane];
+                store_out(a.y, static_cast<size_t>(sl) * a.d_out + row0 + lane, v, a.out);
+            }
+            __syncthreads();
+        }
+    }
+}
+
+size_t up256(size_t n) { return (n + 255) / 256 * 256; }
+
+struct MoeLayout {
+    size_t n_active, table, sorted, t, xp, sx, total;
+};
+
+MoeLayout moe_layout(const QW& w, int r_max, int E, int T, int k, int x_per_slot) {
+    const int S = T * k;
+    const int max_active = S < E ? S : E;
+    const int rows = x_per_slot ? S : T;
+    const size_t chunks = static_cast<size_t>(w.d_in) / (32 / w.bits) / 4;
+    MoeLayout l;
+    l.n_active = 0;
+    l.table = 256;
+    l.sorted = l.table + up256(static_cast<size_t>(max_active) * 4 * sizeof(int));
+    l.t = l.sorted + up256(static_cast<size_t>(S) * sizeof(int));
+    l.xp = l.t + up256(static_cast<size_t>(S) * r_max * sizeof(float));
+    l.sx = l.xp + up256(static_cast<size_t>(rows) * w.d_in * 2);
+    l.total = l.sx + up256(static_cast<size_t>(rows) * chunks * sizeof(float));
+    return l;
+}
+
+template <int BITS, int CPL, int NB>
+hipError_t launch_moe3(const MoeArgs& a, int blocks, int threads, hipStream_t st) {
+    hipLaunchKernelGGL((moe_kernel<BITS, CPL, NB>), dim3(blocks), dim3(threads), 0, st, a);
+    return hipGetLastError();
+}
+
+template <int BITS>
+hipError_t launch_moe2(const MoeArgs& a, int nb, int blocks, int threads, hipStream_t st) {
+    switch (nb) {
+        case 0: return launch_moe3<BITS, 1, 0>(a, blocks, threads, st);
+        case 1: return launch_moe3<BITS, 1, 1>(a, blocks, threads, st);
+        case 2: return launch_moe3<BITS, 1, 2>(a, blocks, threads, st);
+        default: return launch_moe3<BITS, 1, 4>(a, blocks, threads, st);
+    }
+}
+
+}  // namespace
+
+bool moe_fits(const QW& w, int E, int T, int k) {
+    // one chunk per lane over at most 8 K slices: d_in <= 16384 (4-bit), 32768 (2-bit)
+    const int chunks = w.d_in / (32 / w.bits) / 4;
+    return chunks <= 8 * 64 && E <= kMaxExperts && T * k <= kMaxSlots;
+}
+
+size_t moe_workspace_bytes(const QW& w, int r_max, int E, int T, int k, int x_per_slot) {
+    return moe_layout(w, r_max, E, T, k, x_per_slot).total;
+}
+
+hipError_t launch_moe_decode(const QW& w, const uint16_t* A, const uint16_t* B, int r_max, const int32_t* ranks,
+                             int E, const void* x, int x_per_slot, const int32_t* ids, int T, int k, int act,
+                             void* y, int out, void* ws, hipStream_t st) {
+    const MoeLayout l = moe_layout(w, r_max, E, T, k, x_per_slot);
+    char* wsb = static_cast<char*>(ws);
+    MoeArgs a;
+    a.q = w.q; a.s = w.s; a.z = w.z; a.A = A; a.B = B; a.ranks = ranks; a.ids = ids;
+    a.x = static_cast<const uint16_t*>(x); a.y = y;
+    a.q_stride = static_cast<size_t>(w.d_out) * (w.d_in / (32 / w.bits));
+    a.sz_stride = static_cast<size_t>(w.d_out) * (w.d_in / w.G);
+    a.a_stride = static_cast<size_t>(r_max) * w.d_in;
+    a.b_stride = static_cast<size_t>(w.d_out) * r_max;
+    a.E = E; a.T = T; a.k = k; a.d_out = w.d_out; a.d_in = w.d_in; a.G = w.G; a.r_max = r_max;
+    a.act = act; a.out = out; a.x_per_slot = x_per_slot;
+    a.n_active = reinterpret_cast<int*>(wsb + l.n_active);
+    a.table = reinterpret_cast<int*>(wsb + l.table);
+    a.sorted = reinterpret_cast<int*>(wsb + l.sorted);
+    a.t = reinterpret_cast<float*>(wsb + l.t);
+    a.xp = reinterpret_cast<f16x2*>(wsb + l.xp);
+    a.sx = reinterpret_cast<float*>(wsb + l.sx);
+    // K split as in the dense decode: one chunk per lane, a power-of-two
+    // number of slices (at most 8, which moe_fits guarantees)
+    const int chunks = w.d_in / (32 / w.bits) / 4;
+    int ks = (chunks + 63) / 64;
+    while (ks & (ks - 1)) ++ks;
+    a.ks = ks;
+    a.cps = (chunks + a.ks - 1) / a.ks;
+    const int threads = 64 * (a.ks > 4 ? a.ks : 4);
+    if (a.ks > 8 || threads > 512 || threads % (64 * a.ks)) return hipErrorInvalidConfiguration;
+    const int rg_per_block = threads / 64 / a.ks;
+    const int rgroups = (w.d_out + kR - 1) / kR;
+    a.bpe = (rgroups + rg_per_block - 1) / rg_per_block;
+    const int S = T * k;
+    const int max_active = S < E ? S : E;
+    const int per = 64 * a.ks;
+    const int nb = r_max == 0 ? 0 : (r_max <= per ? 1 : (r_max <= 2 * per ? 2 : 4));
+
+    const int rows = x_per_slot ? S : T;
+    const long long items = static_cast<long long>(rows) * chunks;
+    const unsigned pgrid = static_cast<unsigned>(E + (items + 255) / 256);
+    if (w.bits == 4)
+        hipLaunchKernelGGL(moe_prep_kernel<4>, dim3(pgrid), dim3(256), 0, st, a);
+    else
+        hipLaunchKernelGGL(moe_prep_kernel<2>, dim3(pgrid), dim3(256), 0, st, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int blocks = max_active * a.bpe;
+    return w.bits == 4 ? launch_moe2<4>(a, nb, blocks, threads, st) : launch_moe2<2>(a, nb, blocks, threads, st);
+}
+
+}  // namespace cl

@@ -13,7 +13,7 @@ seeded Gaussian draws.
 Seeding: every array draws from
 ``numpy.random.default_rng(SeedSequence([workload, layer, matrix, expert, tag]))``
 with tag 0 = weight, 1 = activation, 2 = sensitivity score, 3 = routing logits,
-4 = per-expert rank, 5 = stand-in factors.  Matrices of a decoder layer are
+4 = per-expert rank, 5 = stand-in factors, 6 = stand-in packed codes.  Matrices of a decoder layer are
 numbered q, k, v, o, gate, up, down = 0..6.
 """
 
@@ -21,7 +21,7 @@ from dataclasses import dataclass, field
 
 import numpy as np
 
-TAG_WEIGHT, TAG_ACT, TAG_SCORE, TAG_ROUTE, TAG_RANK, TAG_FACTOR = range(6)
+TAG_WEIGHT, TAG_ACT, TAG_SCORE, TAG_ROUTE, TAG_RANK, TAG_FACTOR, TAG_CODES = range(7)
 
 LLAMA_MATS = ("q", "k", "v", "o", "gate", "up", "down")
 # (d_out, d_in) of the Llama-3.1-8B decoder-layer linears (GQA: 8 kv heads).
@@ -91,6 +91,26 @@ def standin_factors(d_out, d_in, r_max, workload, layer=0, matrix=0, expert=0, s
     A = (scale * g.standard_normal((r_max, d_in))).astype(np.float16)
     B = (scale * g.standard_normal((d_out, r_max))).astype(np.float16)
     return A, B
+
+
+def standin_codes(num_experts, d_out, d_in, bits, group_size, workload, layer=0, matrix=0):
+    """Stand-in quantized experts: uniformly random packed words
+    ``uint32 [E][d_out][d_in*bits/32]`` (every bit pattern is a valid set of
+    codes), fp16 scales ``[E][d_out][d_in/G]`` in the range a group of
+    N(0, 0.02) weights gets, and integer fp16 zero points in ``0..2^bits-1``.
+
+    For timing and sampled parity at stacked-expert sizes where quantizing every
+    expert on the host is too slow: the forward reads codes, scales and zeros,
+    not the weights they came from.
+    """
+    g = rng(workload, layer, matrix, 0, TAG_CODES)
+    words = d_in * bits // 32
+    groups = d_in // group_size
+    q = g.integers(0, 2 ** 32, size=(num_experts, d_out, words), dtype=np.uint64).astype(np.uint32)
+    step = 0.1 / (2 ** bits - 1)
+    s = (step * (0.75 + 0.5 * g.random((num_experts, d_out, groups)))).astype(np.float16)
+    z = g.integers(0, 2 ** bits, size=(num_experts, d_out, groups)).astype(np.float16)
+    return q, s, z
 
 
 # ---------------------------------------------------------------- rank tables

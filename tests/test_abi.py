@@ -127,3 +127,41 @@ def test_window_validation():
     ybad = (ctypes.c_void_p * 2)(FAKE, 0)
     assert lib.cl_linear_decode_window(2, q2, None, ctypes.c_void_p(FAKE), 1, cl.CL_FP16, ybad, cl.CL_FP16,
                                        ctypes.c_void_p(FAKE), 1 << 20, None) == cl.CL_EINVAL
+
+
+def test_moe_validation():
+    lib = cl.lib()
+    def call(qw=None, A=FAKE, B=FAKE, r_max=8, ranks=FAKE, E=16, x=FAKE, xps=0, ids=FAKE, T=2, k=4,
+             act=cl.CL_FP16, out=cl.CL_FP16, y=FAKE, ws=FAKE, ws_bytes=1 << 20):
+        qw = qw or _qw()
+        v = ctypes.c_void_p
+        return lib.cl_moe_linear_decode(ctypes.byref(qw), v(A), v(B), r_max, v(ranks), E, v(x), xps, v(ids), T, k,
+                                        act, v(y), out, v(ws), ws_bytes, None)
+
+    assert call(qw=_qw(bits=3)) == cl.CL_EUNSUPPORTED
+    assert call(E=0) == cl.CL_EINVAL
+    assert call(E=1025) == cl.CL_EUNSUPPORTED
+    assert call(T=0) == cl.CL_EINVAL and call(T=65) == cl.CL_EINVAL
+    assert call(k=0) == cl.CL_EINVAL
+    assert call(T=64, k=17) == cl.CL_EUNSUPPORTED and b"slots" in lib.cl_last_error()
+    assert call(qw=_qw(d_in=16384 + 128)) == cl.CL_EUNSUPPORTED
+    assert call(r_max=257) == cl.CL_EINVAL
+    assert call(A=0) == cl.CL_EINVAL and call(ranks=0) == cl.CL_EINVAL
+    assert call(A=FAKE + 8) == cl.CL_EINVAL
+    assert call(ids=0) == cl.CL_EINVAL and call(ids=FAKE + 2) == cl.CL_EINVAL
+    assert call(act=cl.CL_FP32) == cl.CL_EINVAL and call(out=9) == cl.CL_EINVAL
+    assert call(x=FAKE + 8) == cl.CL_EINVAL and call(y=0) == cl.CL_EINVAL
+    assert call(ws=0) == cl.CL_EWORKSPACE and call(ws_bytes=64) == cl.CL_EWORKSPACE
+    assert call(ws=FAKE + 64) == cl.CL_EINVAL
+    # workspace query: pure, grows with slots and per-slot inputs, 0 when rejected
+    _decode(_qw(bits=3))
+    before = lib.cl_last_error()
+    qw = _qw(d_in=2048)
+    n1 = lib.cl_moe_workspace(ctypes.byref(qw), 32, 128, 1, 8, 0)
+    n64 = lib.cl_moe_workspace(ctypes.byref(qw), 32, 128, 64, 8, 0)
+    n64s = lib.cl_moe_workspace(ctypes.byref(qw), 32, 128, 64, 8, 1)
+    assert 0 < n1 < n64 < n64s
+    assert n64 - n1 >= 63 * 8 * 32 * 4                 # A x per slot
+    assert lib.cl_moe_workspace(ctypes.byref(qw), 32, 128, 64, 17, 0) == 0
+    assert lib.cl_last_error() == before
+    assert call(r_max=0, A=0, B=0, ranks=0, ws_bytes=64) == cl.CL_EWORKSPACE   # factors optional at r_max 0

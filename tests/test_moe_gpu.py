@@ -1,0 +1,183 @@
+"""cl_moe_linear_decode against the fp64 oracle (Section 4.2.2 and
+Appendix A.1: every routed expert's same projection in one step, only routed
+experts read).  Full outputs at sizes the oracle finishes in seconds (oracle
+quantizer, SVD factors, ragged rows, duplicate and invalid ids, rank 0 and
+clamped ranks, 2/4-bit, fp16/bf16 activations, every output dtype); sampled
+rows at the 128-expert, hidden-2048 / FFN-768 layer with top-8 routing for
+1, 8 and 64 tokens; bitwise determinism and workspace reuse."""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import moe, quant
+from paper_2605_05819_amd import cl, workloads as wl
+from tests.helpers import REL_L2_TOL, dev_f16, dev_u16, dev_u32, oracle_layer, out_to_numpy, rel_l2, round_to
+
+pytestmark = pytest.mark.gpu
+
+OUT_DTYPES = [torch.float32, torch.float16, torch.bfloat16]
+
+
+def _stack(arrs):
+    return np.ascontiguousarray(np.stack(arrs))
+
+
+def _device_experts(Q, s, z, A, B, ranks, d_out, d_in, bits, G, r_max):
+    """Stacked host arrays [E][...] -> cl.MoeExperts on the device."""
+    return cl.MoeExperts(dev_u32(Q), dev_f16(s), dev_f16(z),
+                         dev_f16(A) if r_max else None, dev_f16(B) if r_max else None,
+                         torch.from_numpy(np.asarray(ranks, dtype=np.int32)).cuda() if r_max else None,
+                         len(Q), d_out, d_in, bits, G, r_max)
+
+
+def _oracle_experts(E, d_out, d_in, bits, G, r_max, seed, svd=True):
+    """E experts quantized by the oracle; factors from the SVD of the error
+    (or seeded stand-ins)."""
+    Qs, ss, zs, As, Bs = [], [], [], [], []
+    for e in range(E):
+        W = wl.weight((d_out, d_in), seed, 0, 0, e)
+        if svd:
+            Q, s, z, A, B, _ = oracle_layer(W, bits, G, r_max)
+        else:
+            Q, s, z = quant.quantize_pack(W, bits, G)
+            A, B = wl.standin_factors(d_out, d_in, r_max, seed, 0, 0, e)
+        Qs.append(Q), ss.append(s), zs.append(z), As.append(A), Bs.append(B)
+    return _stack(Qs), _stack(ss), _stack(zs), _stack(As), _stack(Bs)
+
+
+def _full_ref(Q, s, z, A, B, ranks, X, ids, x_per_slot, bits, G, d_in):
+    """The oracle over all rows; out-of-range ids give zero rows."""
+    E = len(Q)
+    ids = np.asarray(ids)
+    experts = [(quant.dequant_packed(Q[e], s[e], z[e], bits, G, d_in), A[e], B[e]) for e in range(E)]
+    valid = (ids >= 0) & (ids < E)
+    safe = np.where(valid, ids, 0)
+    Y = moe.forward(experts, ranks, X, safe, x_per_slot)
+    Y[~valid] = 0.0
+    return Y
+
+
+def _run(ex, X_bits, act, ids, out_dtype, x_per_slot):
+    x = dev_u16(X_bits, act)
+    idd = torch.from_numpy(np.ascontiguousarray(ids, dtype=np.int32)).cuda()
+    y = cl.moe_linear_decode(ex, x, idd, out_dtype=out_dtype)
+    torch.cuda.synchronize()
+    assert tuple(y.shape) == (ids.shape[0], ids.shape[1], ex.d_out)
+    return out_to_numpy(y)
+
+
+@pytest.mark.parametrize("x_per_slot", [False, True])
+@pytest.mark.parametrize("T,k", [(1, 4), (5, 3), (16, 8)])
+def test_small_experts_svd_factors_full_outputs(T, k, x_per_slot):
+    E, d_out, d_in, bits, G, r_max = 12, 100, 512, 4, 128, 16
+    Q, s, z, A, B = _oracle_experts(E, d_out, d_in, bits, G, r_max, 40)
+    ranks = wl.moe_expert_ranks(40, 0, 0, E, levels=(0, 4, 8, 16))
+    ids, _ = wl.routing(T, 40, 0, E, k)
+    shape = (T, k, d_in) if x_per_slot else (T, d_in)
+    x = wl.activation(shape, 40, 0, 1)
+    ex = _device_experts(Q, s, z, A, B, ranks, d_out, d_in, bits, G, r_max)
+    ref = _full_ref(Q, s, z, A, B, ranks, x.values, ids, x_per_slot, bits, G, d_in)
+    for od in OUT_DTYPES:
+        got = _run(ex, x.bits, torch.float16, ids, od, x_per_slot)
+        assert rel_l2(got, round_to(ref, od)) <= REL_L2_TOL
+
+
+@pytest.mark.parametrize("bits,G", [(2, 64), (4, 32)])
+@pytest.mark.parametrize("act", [torch.float16, torch.bfloat16])
+def test_bits_groups_and_bf16_activations(bits, G, act):
+    E, d_out, d_in, r_max, T, k = 9, 37, 1536, 24, 6, 4
+    Q, s, z, A, B = _oracle_experts(E, d_out, d_in, bits, G, r_max, 41, svd=False)
+    ranks = np.array([0, 24, 8, 17, 24, 1, 0, 12, 5], dtype=np.int32)
+    ids, _ = wl.routing(T, 41, 0, E, k)
+    x = wl.activation((T, d_in), 41, 0, 1, dtype="bf16" if act == torch.bfloat16 else "fp16")
+    ex = _device_experts(Q, s, z, A, B, ranks, d_out, d_in, bits, G, r_max)
+    ref = _full_ref(Q, s, z, A, B, ranks, x.values, ids, False, bits, G, d_in)
+    got = _run(ex, x.bits, act, ids, torch.float32, False)
+    assert rel_l2(got, ref) <= REL_L2_TOL
+
+
+def test_duplicate_invalid_ids_and_clamped_ranks():
+    E, d_out, d_in, bits, G, r_max, T, k = 6, 64, 256, 4, 128, 8, 4, 5
+    Q, s, z, A, B = _oracle_experts(E, d_out, d_in, bits, G, r_max, 42, svd=False)
+    ranks = np.array([-3, 8, 100, 0, 5, 2], dtype=np.int32)       # clamped to 0..r_max
+    ids = np.array([[2, 2, 2, -1, 0],
+                    [6, 1, 99, 5, 5],
+                    [3, 3, 3, 3, 3],
+                    [-7, 4, 1, 0, 2]], dtype=np.int32)
+    x = wl.activation((T, d_in), 42, 0, 1)
+    ex = _device_experts(Q, s, z, A, B, ranks, d_out, d_in, bits, G, r_max)
+    got = _run(ex, x.bits, torch.float16, ids, torch.float32, False)
+    ref = _full_ref(Q, s, z, A, B, np.clip(ranks, 0, r_max), x.values, ids, False, bits, G, d_in)
+    invalid = (ids < 0) | (ids >= E)
+    assert (got[invalid] == 0).all()
+    assert rel_l2(got, ref) <= REL_L2_TOL
+    # all slots invalid: zeros only
+    bad = np.full((2, 3), E, dtype=np.int32)
+    assert (_run(ex, x.bits[:2], torch.float16, bad, torch.float16, False) == 0).all()
+
+
+def test_rank_zero_without_factors():
+    E, d_out, d_in, bits, G, T, k = 5, 70, 384, 4, 128, 3, 2
+    Q, s, z, A, B = _oracle_experts(E, d_out, d_in, bits, G, 4, 43, svd=False)
+    ex = _device_experts(Q, s, z, None, None, None, d_out, d_in, bits, G, 0)
+    ids, _ = wl.routing(T, 43, 0, E, k)
+    x = wl.activation((T, k, d_in), 43, 0, 1)
+    got = _run(ex, x.bits, torch.float16, ids, torch.float32, True)
+    ref = _full_ref(Q, s, z, A, B, np.zeros(E, dtype=np.int32), x.values, ids, True, bits, G, d_in)
+    assert rel_l2(got, ref) <= REL_L2_TOL
+
+
+# ---------------------------------------------- the 128-expert MoE layer
+
+
+@pytest.fixture(scope="module")
+def moe_layer():
+    """gate and down of one layer: 128 stacked experts of stand-in codes and
+    factors, per-expert ranks from {0, 8, 16, 32}."""
+    out = {}
+    for m, name in ((0, "gate"), (2, "down")):
+        d_out, d_in = wl.MOE_SHAPES[name]
+        Q, s, z = wl.standin_codes(wl.MOE_EXPERTS, d_out, d_in, 4, 128, 44, 0, m)
+        A = np.empty((wl.MOE_EXPERTS, 32, d_in), np.float16)
+        B = np.empty((wl.MOE_EXPERTS, d_out, 32), np.float16)
+        for e in range(wl.MOE_EXPERTS):
+            A[e], B[e] = wl.standin_factors(d_out, d_in, 32, 44, 0, m, e)
+        ranks = wl.moe_expert_ranks(44, 0, m)
+        ex = _device_experts(Q, s, z, A, B, ranks, d_out, d_in, 4, 128, 32)
+        out[name] = (ex, Q, s, z, A, B, ranks)
+    return out
+
+
+@pytest.mark.parametrize("name", ["gate", "down"])
+@pytest.mark.parametrize("T", [1, 8, 64])
+def test_layer_sampled_rows(moe_layer, name, T):
+    ex, Q, s, z, A, B, ranks = moe_layer[name]
+    x_per_slot = name == "down"
+    ids, _ = wl.routing(T, 44, 0)
+    shape = (T, wl.MOE_TOPK, ex.d_in) if x_per_slot else (T, ex.d_in)
+    x = wl.activation(shape, 44, 0, 7)
+    got = _run(ex, x.bits, torch.float16, ids, torch.float32, x_per_slot)
+    g = np.random.default_rng(T)
+    rows = np.unique(np.concatenate([[0, ex.d_out - 1], g.integers(0, ex.d_out, 40)]))
+    packed = [(Q[e], s[e], z[e], A[e], B[e]) for e in range(wl.MOE_EXPERTS)]
+    ref = moe.forward_rows(packed, ranks, x.values, ids, x_per_slot, rows, 4, 128)
+    assert rel_l2(got[:, :, rows], ref) <= REL_L2_TOL
+    # bitwise deterministic, and the workspace carries nothing between calls
+    again = _run(ex, x.bits, torch.float16, ids, torch.float32, x_per_slot)
+    assert np.array_equal(got, again)
+
+
+def test_layer_workspace_reuse_across_routings(moe_layer):
+    ex, Q, s, z, A, B, ranks = moe_layer["gate"]
+    ws = cl.workspace(cl.moe_workspace(ex, 64, 8, False), torch.device("cuda"))
+    packed = [(Q[e], s[e], z[e], A[e], B[e]) for e in range(wl.MOE_EXPERTS)]
+    rows = np.arange(0, ex.d_out, 97)
+    for T, seed in ((64, 45), (3, 46), (17, 47)):
+        ids, _ = wl.routing(T, seed, 0)
+        x = wl.activation((T, ex.d_in), seed, 0, 7)
+        y = cl.moe_linear_decode(ex, dev_u16(x.bits, torch.float16),
+                                 torch.from_numpy(ids).cuda(), out_dtype=torch.float32, ws=ws)
+        torch.cuda.synchronize()
+        ref = moe.forward_rows(packed, ranks, x.values, ids, False, rows, 4, 128)
+        assert rel_l2(out_to_numpy(y)[:, :, rows], ref) <= REL_L2_TOL

@@ -370,3 +370,22 @@ def test_moe_matches_scalar_loops_and_reduces_to_dense():
     # permuting tokens permutes outputs
     perm = np.array([2, 0, 1])
     np.testing.assert_array_equal(moe.forward(experts, ranks, X[perm], ids[perm], False), Y[perm])
+
+
+def test_moe_forward_rows_is_forward_restricted_to_rows():
+    g = np.random.default_rng(31)
+    E, d_out, d_in, r_max, T, k = 4, 6, 16, 3, 2, 3
+    packed, experts = [], []
+    for _ in range(E):
+        W = (0.02 * g.standard_normal((d_out, d_in))).astype(np.float32)
+        Q, s, z = quant.quantize_pack(W, 4, 8)
+        A, B = g.standard_normal((r_max, d_in)), g.standard_normal((d_out, r_max))
+        packed.append((Q, s, z, A, B))
+        experts.append((quant.dequant_packed(Q, s, z, 4, 8, d_in), A, B))
+    ranks = [3, 0, 2, 1]
+    ids = np.array([[0, 3, 1], [2, 2, 0]])
+    rows = np.array([5, 0, 3])
+    for x_per_slot, X in ((False, g.standard_normal((T, d_in))), (True, g.standard_normal((T, k, d_in)))):
+        full = moe.forward(experts, ranks, X, ids, x_per_slot)
+        np.testing.assert_allclose(moe.forward_rows(packed, ranks, X, ids, x_per_slot, rows, 4, 8),
+                                   full[:, :, rows], rtol=1e-12, atol=1e-15)

@@ -85,3 +85,18 @@ def test_routing_is_topk_of_softmax_and_normalised():
         assert abs(w[t].sum() - 1) < 1e-12 and np.all(np.diff(w[t]) <= 0)
         # expert activation score k * g_e averages to 1 over the slots
         assert abs((8 * w[t]).mean() - 1) < 1e-12
+
+
+def test_standin_codes_shapes_ranges_and_seeding():
+    q, s, z = wl.standin_codes(3, 5, 256, 4, 128, 9, 1, 2)
+    assert q.shape == (3, 5, 32) and q.dtype == np.uint32
+    assert s.shape == z.shape == (3, 5, 2) and s.dtype == z.dtype == np.float16
+    assert (s > 0).all() and np.isfinite(s).all()
+    assert (z == np.round(z)).all() and z.min() >= 0 and z.max() <= 15
+    q2, s2, z2 = wl.standin_codes(3, 5, 256, 4, 128, 9, 1, 2)
+    assert (q == q2).all() and (s == s2).all() and (z == z2).all()
+    # every nibble value occurs (uniform words)
+    nib = (q[..., None] >> (4 * np.arange(8, dtype=np.uint32))) & 15
+    assert set(np.unique(nib)) == set(range(16))
+    q3, _, z3 = wl.standin_codes(2, 4, 128, 2, 64, 9)
+    assert q3.shape == (2, 4, 8) and z3.max() <= 3
