@@ -114,6 +114,39 @@ cl_status cl_quantize_pack(const float* W, int32_t d_out, int32_t d_in, int32_t 
 cl_status cl_dequantize(const cl_qweight* w, float* W_hat, void* stream);
 
 /*
+ * cl_build_compensation -- compensation factors from the quantization error
+ * (Section 4.1: SVD of the residual; Appendix B.2: the truncated SVD is the
+ * best rank-r approximation, error = the tail singular values).  With
+ * E = W - deq(q, scales, zeros) = U diag(sigma) V^T, sigma descending:
+ *     A = diag(sqrt(sigma[:r_max])) V^T[:r_max],   B = U[:, :r_max] diag(sqrt(sigma[:r_max])),
+ * each singular pair signed so that the largest-magnitude entry of its U
+ * column is positive (first index on ties); rounded once to fp16.  Any prefix
+ * rank r <= r_max of the stored factors is the optimal rank-r truncation.
+ *
+ *  W      device fp32 [d_out][d_in], the weight w was quantized from
+ *  w      its packed backbone (as for cl_linear_decode)
+ *  r_max  0..min(256, d_out, d_in)
+ *  A      device fp16 [r_max][d_in] (output; may be NULL when r_max = 0)
+ *  B      device fp16 [d_out][r_max] (output; may be NULL when r_max = 0)
+ *  sigma  device fp32 [min(d_out, d_in)], every singular value, descending
+ *         (output; may be NULL)
+ *  ws     device workspace of cl_build_compensation_workspace(...) bytes,
+ *         256-byte aligned (fp64 residual, Gram matrix and eigenvectors)
+ * Computed in fp64 from the Gram matrix of E over its smaller side with a
+ * parallel cyclic Jacobi eigensolver; singular values far below
+ * 1e-8 * sigma[0] have absolute accuracy only.  An offline step: the call
+ * waits on the stream once per Jacobi sweep and returns when the factors are
+ * enqueued.  Limits: min(d_out, d_in) <= 8192, d_out * d_in <= 2^31
+ * (CL_EUNSUPPORTED beyond); CL_EUNSUPPORTED also if the eigensolver does not
+ * converge in 40 sweeps.
+ */
+cl_status cl_build_compensation(const float* W, const cl_qweight* w, int32_t r_max, uint16_t* A, uint16_t* B,
+                                float* sigma, void* ws, size_t ws_bytes, void* stream);
+
+/* Workspace bytes for cl_build_compensation (0 for rejected sizes). */
+size_t cl_build_compensation_workspace(int32_t d_out, int32_t d_in, int32_t r_max);
+
+/*
  * cl_linear_workspace -- bytes of device workspace that cl_linear_decode needs
  * for this weight, factor set (NULL for none) and token count.  Returns 0 for
  * arguments cl_linear_decode would reject.

@@ -18,8 +18,8 @@ CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(os.path.dirname(HERE), "_build")
 LIB = os.path.join(HERE, "libcl.so")
 
-SOURCES = ["api.hip", "quant.hip", "decode.hip", "prefill.hip", "moe.hip"]
-EXTRA = {"quant.hip": ["-ffp-contract=off"]}
+SOURCES = ["api.hip", "quant.hip", "decode.hip", "prefill.hip", "moe.hip", "comp.hip"]
+EXTRA = {"quant.hip": ["-ffp-contract=off"], "comp.hip": ["-ffp-contract=off"]}
 ARCH = "gfx950"
 FLAGS = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=" + ARCH,
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

@@ -54,6 +54,10 @@ _SIGNATURES = {
     "cl_linear_prefill": (ctypes.c_int32, [ctypes.POINTER(QWeightC), ctypes.POINTER(LowRankC), ctypes.c_void_p,
                                            ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32,
                                            ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
+    "cl_build_compensation_workspace": (ctypes.c_size_t, [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32]),
+    "cl_build_compensation": (ctypes.c_int32, [ctypes.c_void_p, ctypes.POINTER(QWeightC), ctypes.c_int32,
+                                               ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                               ctypes.c_size_t, ctypes.c_void_p]),
     "cl_moe_workspace": (ctypes.c_size_t, [ctypes.POINTER(QWeightC), ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
                                             ctypes.c_int32, ctypes.c_int32]),
     "cl_moe_linear_decode": (ctypes.c_int32, [ctypes.POINTER(QWeightC), ctypes.c_void_p, ctypes.c_void_p,
@@ -271,3 +275,18 @@ def moe_linear_decode(ex, x, topk_ids, out_dtype=torch.float16, y=None, ws=None,
                                       _DTYPE_CODE[x.dtype], _ptr(y), _DTYPE_CODE[y.dtype], _ptr(ws), ws.numel(),
                                       _stream(stream)))
     return y
+
+
+def build_compensation(W, w, r_max, stream=None):
+    """``cl_build_compensation``: fp32 weight ``W`` [d_out][d_in] and its
+    packed backbone ``w`` -> ``(A fp16 [r_max][d_in], B fp16 [d_out][r_max],
+    sigma fp32 [min(d_out, d_in)])``.  Waits on the stream once per sweep."""
+    A = torch.empty((r_max, w.d_in), dtype=torch.float16, device=W.device)
+    B = torch.empty((w.d_out, r_max), dtype=torch.float16, device=W.device)
+    sigma = torch.empty((min(w.d_out, w.d_in),), dtype=torch.float32, device=W.device)
+    nbytes = lib().cl_build_compensation_workspace(w.d_out, w.d_in, r_max)
+    ws = workspace(nbytes, W.device)
+    q = w.c()
+    _check(lib().cl_build_compensation(_ptr(W), ctypes.byref(q), r_max, _ptr(A), _ptr(B), _ptr(sigma), _ptr(ws),
+                                       ws.numel(), _stream(stream)))
+    return A, B, sigma

@@ -91,6 +91,39 @@ cl_status cl_dequantize(const cl_qweight* w, float* W_hat, void* stream) {
     return hip_status(cl::launch_dequantize(qw, W_hat, static_cast<hipStream_t>(stream)), who);
 }
 
+size_t cl_build_compensation_workspace(int32_t d_out, int32_t d_in, int32_t r_max) {
+    const int n = d_in <= d_out ? d_in : d_out;
+    if (d_out < 1 || d_in < 1 || r_max < 0 || r_max > 256 || r_max > n || !cl::comp_fits(d_out, d_in)) return 0;
+    return cl::comp_workspace_bytes(d_out, d_in, r_max);
+}
+
+cl_status cl_build_compensation(const float* W, const cl_qweight* w, int32_t r_max, uint16_t* A, uint16_t* B,
+                                float* sigma, void* ws, size_t ws_bytes, void* stream) {
+    const char* who = "cl_build_compensation";
+    cl::QW qw;
+    cl_status st = check_qweight(w, &qw, who);
+    if (st) return st;
+    const int n = qw.d_in <= qw.d_out ? qw.d_in : qw.d_out;
+    if (!cl::comp_fits(qw.d_out, qw.d_in))
+        return fail(CL_EUNSUPPORTED, "%s: min(d_out, d_in) must be <= 8192 and d_out * d_in <= 2^31", who);
+    if (r_max < 0 || r_max > 256 || r_max > n)
+        return fail(CL_EINVAL, "%s: r_max must be in 0..min(256, d_out, d_in) (got %d)", who, r_max);
+    if (!W || !aligned(W, 4)) return fail(CL_EINVAL, "%s: null or misaligned W", who);
+    if (r_max > 0 && (!A || !B || !aligned(A, 2) || !aligned(B, 2)))
+        return fail(CL_EINVAL, "%s: null or misaligned A or B", who);
+    if (sigma && !aligned(sigma, 4)) return fail(CL_EINVAL, "%s: misaligned sigma", who);
+    const size_t need = cl::comp_workspace_bytes(qw.d_out, qw.d_in, r_max);
+    if (!ws || ws_bytes < need)
+        return fail(CL_EWORKSPACE, "%s: workspace of %zu bytes needed (got %zu)", who, need, ws ? ws_bytes : 0);
+    if (!aligned(ws, 256)) return fail(CL_EINVAL, "%s: workspace must be 256-byte aligned", who);
+    int sweeps = 0;
+    const hipError_t e = cl::launch_build_compensation(W, qw, r_max, A, B, sigma, ws,
+                                                       static_cast<hipStream_t>(stream), &sweeps);
+    if (e == hipErrorNotReady)
+        return fail(CL_EUNSUPPORTED, "%s: the Jacobi eigensolver did not converge in %d sweeps", who, sweeps);
+    return hip_status(e, who);
+}
+
 }  // extern "C"
 
 namespace {

@@ -39,6 +39,14 @@ size_t prefill_workspace_bytes(const QW& w, const LR& c, int M);
 hipError_t launch_linear_prefill(const QW& w, const LR& c, const void* X, int M, int act, void* Y, int out,
                                  void* ws, hipStream_t st);
 
+// Compensation factors from the SVD of W - deq(Q) (fp64 Gram + Jacobi);
+// synchronizes the stream once per Jacobi sweep.  hipErrorNotReady: no
+// convergence within the sweep limit.
+bool comp_fits(int d_out, int d_in);
+size_t comp_workspace_bytes(int d_out, int d_in, int r_max);
+hipError_t launch_build_compensation(const float* W, const QW& w, int r_max, uint16_t* A, uint16_t* B, float* sigma,
+                                     void* ws, hipStream_t st, int* sweeps_out);
+
 // MoE decode over stacked experts (expert e's arrays at e times one expert's
 // size); arguments already validated.
 bool moe_fits(const QW& w, int E, int T, int k);

@@ -13,27 +13,6 @@
 
 namespace cl {
 
-// fp64 -> fp16 bits, round to nearest, ties to even, in a single rounding
-// (IEEE 754 binary16: 1 sign, 5 exponent, 10 fraction bits, bias 15).
-__device__ uint16_t f64_to_f16_rne(double v) {
-    uint64_t b = __builtin_bit_cast(uint64_t, v);
-    uint16_t sign = static_cast<uint16_t>((b >> 48) & 0x8000u);
-    double a = fabs(v);
-    if (a != a) return 0x7e00u;
-    if (a >= 65520.0) return sign | 0x7c00u;          // rounds past the largest finite value
-    int e = static_cast<int>((b >> 52) & 0x7ff) - 1023;  // a is finite, possibly subnormal in fp64
-    if (a == 0.0) return sign;
-    if (e < -14) {
-        // subnormal fp16 range: the value in units of 2^-24 (exact scaling)
-        double m = rint(a * 16777216.0);
-        return sign | static_cast<uint16_t>(m);      // m == 1024 encodes the smallest normal
-    }
-    double m = rint(ldexp(a, 10 - e));                // in [1024, 2048]
-    if (m == 2048.0) { m = 1024.0; e += 1; }
-    if (e > 15) return sign | 0x7c00u;
-    return sign | static_cast<uint16_t>(((e + 15) << 10) | (static_cast<int>(m) - 1024));
-}
-
 __device__ double f16_bits_to_f64(uint16_t h) {
     return static_cast<double>(static_cast<float>(__builtin_bit_cast(f16, h)));
 }

@@ -165,3 +165,28 @@ def test_moe_validation():
     assert lib.cl_moe_workspace(ctypes.byref(qw), 32, 128, 64, 17, 0) == 0
     assert lib.cl_last_error() == before
     assert call(r_max=0, A=0, B=0, ranks=0, ws_bytes=64) == cl.CL_EWORKSPACE   # factors optional at r_max 0
+
+
+def test_build_compensation_validation():
+    lib = cl.lib()
+    v = ctypes.c_void_p
+
+    def call(qw=None, W=FAKE, r_max=16, A=FAKE, B=FAKE, sigma=FAKE, ws=FAKE, ws_bytes=1 << 30):
+        qw = qw or _qw(d_out=64, d_in=256)
+        return lib.cl_build_compensation(v(W), ctypes.byref(qw), r_max, v(A), v(B), v(sigma), v(ws), ws_bytes, None)
+
+    assert call(qw=_qw(bits=3)) == cl.CL_EUNSUPPORTED
+    assert call(r_max=65) == cl.CL_EINVAL and b"r_max" in lib.cl_last_error()     # > min(d_out, d_in)
+    assert call(r_max=-1) == cl.CL_EINVAL
+    assert call(qw=_qw(d_out=300, d_in=512), r_max=257) == cl.CL_EINVAL
+    assert call(W=0) == cl.CL_EINVAL and call(W=FAKE + 2) == cl.CL_EINVAL
+    assert call(A=0) == cl.CL_EINVAL and call(B=FAKE + 1) == cl.CL_EINVAL
+    assert call(sigma=FAKE + 2) == cl.CL_EINVAL
+    assert call(qw=_qw(d_out=9000, d_in=8448)) == cl.CL_EUNSUPPORTED                 # n > 8192
+    assert call(ws=0) == cl.CL_EWORKSPACE and call(ws_bytes=1024) == cl.CL_EWORKSPACE
+    assert call(ws=FAKE + 128) == cl.CL_EINVAL
+    # workspace: fp64 residual, Gram and eigenvectors at least; 0 when rejected
+    n = lib.cl_build_compensation_workspace(1024, 4096, 64)
+    assert n >= 8 * (1024 * 4096 + 2 * 1024 * 1024)
+    assert lib.cl_build_compensation_workspace(64, 256, 65) == 0
+    assert lib.cl_build_compensation_workspace(64, 256, 0) > 0

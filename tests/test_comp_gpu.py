@@ -1,0 +1,149 @@
+"""cl_build_compensation against the fp64 oracle (Section 4.1: factors from
+the SVD of W - W_hat; Appendix B.2: Eckart-Young-Mirsky).  Several factor
+sets are correct when singular values nearly coincide, so parity is:
+  * every singular value within 1e-4 relative (leading r_max + 1) and
+    1e-6 sigma_0 absolute (all);
+  * the residual energy of the GPU's fp16 factors, for every prefix rank,
+    equals the tail energy sum_{j>r} sigma_j^2 within 1e-3 of ||E||_F^2;
+  * factor columns of isolated singular values (relative gap > 1e-2 on both
+    sides) equal the oracle's sign-fixed fp16 factors;
+  * the decode forward with the GPU-built factors matches the oracle's
+    forward with the same factors.
+Shapes cover d_out > d_in, d_out < d_in, odd sizes, full rank, 2/4-bit, the
+1024 x 1024 rank-16 linear and an all-zero residual."""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import comp, linear, quant
+from paper_2605_05819_amd import cl, workloads as wl
+from tests.helpers import REL_L2_TOL, dev_f16, dev_u32, out_to_numpy, rel_l2
+
+pytestmark = pytest.mark.gpu
+
+
+def _host16(t):
+    return t.detach().cpu().numpy().astype(np.float64)
+
+
+def _setup(W, bits, G):
+    Q, s, z = quant.quantize_pack(W, bits, G)
+    d_out, d_in = W.shape
+    w = cl.QWeight(dev_u32(Q), dev_f16(s), dev_f16(z), d_out, d_in, bits, G)
+    W_hat = quant.dequant_packed(Q, s, z, bits, G, d_in)
+    return w, Q, s, z, W_hat
+
+
+def _check_factors(W, W_hat, A, B, sigma, r_max):
+    E = comp.residual(W, W_hat)
+    A_ref, B_ref, s_ref = comp.build_compensation(W, W_hat, r_max)
+    s_gpu = sigma.cpu().numpy().astype(np.float64)
+    assert s_gpu.shape == s_ref.shape
+    lead = min(r_max + 1, len(s_ref))
+    scale = max(s_ref[0], 1e-300)
+    assert np.all(np.abs(s_gpu[:lead] - s_ref[:lead]) <= 1e-4 * s_ref[:lead] + 1e-7 * scale)
+    assert np.max(np.abs(s_gpu - s_ref)) <= 1e-6 * scale
+    Ag, Bg = _host16(A), _host16(B)
+    energy = float(np.sum(E * E))
+    for r in sorted({1, r_max // 2, r_max} - {0}):
+        R = E - Bg[:, :r] @ Ag[:r]
+        tail = float(np.sum(s_ref[r:] ** 2))
+        assert abs(float(np.sum(R * R)) - tail) <= 1e-3 * energy, r
+    # isolated singular values: the factor columns themselves
+    A16, B16 = comp.to_fp16(A_ref).astype(np.float64), comp.to_fp16(B_ref).astype(np.float64)
+    checked = 0
+    for j in range(r_max):
+        lo = s_ref[j + 1] if j + 1 < len(s_ref) else 0.0
+        hi = s_ref[j - 1] if j > 0 else np.inf
+        if s_ref[j] > 0 and (s_ref[j] - lo) > 1e-2 * s_ref[j] and (hi - s_ref[j]) > 1e-2 * s_ref[j]:
+            assert rel_l2(Bg[:, j], B16[:, j]) <= 1e-3, j
+            assert rel_l2(Ag[j], A16[j]) <= 1e-3, j
+            checked += 1
+    return checked
+
+
+@pytest.mark.parametrize("d_out,d_in,bits,G,r_max", [
+    (1024, 1024, 4, 128, 16),      # the single-linear workload
+    (300, 128, 4, 128, 24),        # d_out > d_in: eigenvectors are V
+    (96, 384, 4, 32, 40),          # d_out < d_in: eigenvectors are U
+    (97, 256, 2, 64, 97),          # odd size, full rank
+    (81, 320, 4, 64, 20),          # odd size, eigenvectors are U
+])
+def test_factors_match_the_oracle(d_out, d_in, bits, G, r_max):
+    W = wl.weight((d_out, d_in), 50, d_out, d_in)
+    w, Q, s, z, W_hat = _setup(W, bits, G)
+    Wd = torch.from_numpy(W).cuda()
+    A, B, sigma = cl.build_compensation(Wd, w, r_max)
+    torch.cuda.synchronize()
+    assert A.shape == (r_max, d_in) and B.shape == (d_out, r_max)
+    _check_factors(W, W_hat, A, B, sigma, r_max)
+
+
+def test_full_rank_factors_reconstruct_the_residual():
+    W = wl.weight((160, 96), 51)
+    w, Q, s, z, W_hat = _setup(W, 4, 32)
+    A, B, sigma = cl.build_compensation(torch.from_numpy(W).cuda(), w, 96)
+    E = comp.residual(W, W_hat)
+    R = E - _host16(B) @ _host16(A)
+    # only the fp16 rounding of the factors remains
+    assert np.linalg.norm(R) <= 2e-3 * np.linalg.norm(E)
+
+
+def test_isolated_columns_are_compared():
+    """Rows of very different scale give a residual whose leading singular
+    values are far apart, so the leading factor columns are unique up to sign
+    and are compared entry by entry."""
+    d_out, d_in = 256, 128
+    W = wl.weight((d_out, d_in), 52).astype(np.float64)
+    W[:6] *= np.array([64.0, 32.0, 16.0, 8.0, 4.0, 2.0])[:, None]
+    W = W.astype(np.float32)
+    w, Q, s, z, W_hat = _setup(W, 2, 64)
+    A, B, sigma = cl.build_compensation(torch.from_numpy(W).cuda(), w, 8)
+    torch.cuda.synchronize()
+    assert _check_factors(W, W_hat, A, B, sigma, 8) >= 4
+
+
+def test_zero_residual_gives_zero_factors():
+    W = np.zeros((64, 256), np.float32)          # all-zero groups dequantize to exactly 0
+    w, Q, s, z, W_hat = _setup(W, 4, 128)
+    assert not W_hat.any()
+    A, B, sigma = cl.build_compensation(torch.from_numpy(W).cuda(), w, 16)
+    assert not _host16(A).any() and not _host16(B).any()
+    assert not sigma.cpu().numpy().any()
+
+
+def test_rank_zero_returns_sigma_only():
+    W = wl.weight((200, 64), 53)
+    w, Q, s, z, W_hat = _setup(W, 4, 64)
+    A, B, sigma = cl.build_compensation(torch.from_numpy(W).cuda(), w, 0)
+    s_ref = np.linalg.svd(comp.residual(W, W_hat), compute_uv=False)
+    np.testing.assert_allclose(sigma.cpu().numpy(), s_ref, rtol=1e-5, atol=1e-7 * s_ref[0])
+
+
+def test_forward_with_gpu_built_factors():
+    """Build on the GPU, decode on the GPU; the oracle forward with the same
+    fp16 factors agrees (the end-to-end compensated linear)."""
+    d_out, d_in, r_max, rank = 1024, 1024, 16, 16
+    W = wl.weight((d_out, d_in), 0)
+    w, Q, s, z, W_hat = _setup(W, 4, 128)
+    A, B, _ = cl.build_compensation(torch.from_numpy(W).cuda(), w, r_max)
+    c = cl.LowRank(A, B, r_max, rank)
+    x = wl.activation((1, d_in), 0)
+    xd = torch.from_numpy(x.bits.view(np.int16)).view(torch.float16).cuda()
+    y = cl.linear_decode(w, c, xd, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    ref = linear.forward_packed(Q, s, z, 4, 128, _host16(A), _host16(B), rank, x.values)
+    assert rel_l2(out_to_numpy(y), ref) <= REL_L2_TOL
+    # and the compensation moves the output toward W x (the residual's top-16 part)
+    exact = x.values @ W.astype(np.float64).T
+    assert rel_l2(ref, exact) < rel_l2(linear.forward(W_hat, None, None, 0, x.values), exact)
+
+
+def test_deterministic():
+    W = wl.weight((192, 320), 54)
+    w, *_ = _setup(W, 4, 64)
+    Wd = torch.from_numpy(W).cuda()
+    A1, B1, s1 = cl.build_compensation(Wd, w, 32)
+    A2, B2, s2 = cl.build_compensation(Wd, w, 32)
+    assert torch.equal(A1, A2) and torch.equal(B1, B2) and torch.equal(s1, s2)
