@@ -9,22 +9,27 @@
 // over every routed expert, and only routed experts' codes, scales, zeros and
 // factors are read.
 //
-//  * moe_prep_kernel: workgroup e (one per expert) scans the routing table --
-//    so no workgroup ever waits for another -- and, if expert e is routed,
-//    writes its entry of the active-expert table (index = number of routed
-//    experts below e), its slots in slot order into the sorted slot list, and
-//    t = A_e[:r_e] x for each of its slots (A_e read once).  Workgroup 0 also
-//    writes the number of routed experts and zero rows for slots whose id is
-//    out of range.  The remaining workgroups prepare the activations (fp16,
-//    pair-permuted, per-chunk sums) exactly as the dense decode does.
+//  * moe_prep_kernel: workgroup (j, q), j < min(E, T*k), scans the routing
+//    table -- so no workgroup ever waits for another -- and takes e = the
+//    j-th routed expert in ascending id order (none: it exits).  Each of its
+//    four waves computes t[slot][i] = A_e[i] . x_slot for one rank row
+//    i = 4q + wave over all of e's slots (four slots per pass).  Workgroup
+//    (j, 0) also writes entry j of the active-expert table and e's slots, in
+//    slot order, into the sorted slot list; workgroup (0, 0) writes the
+//    number of routed experts and zero rows for slots whose id is out of
+//    range.  The remaining workgroups
+//    prepare the activations (fp16, pair-permuted, per-chunk sums) exactly as
+//    the dense decode does.
 //  * moe_kernel: one workgroup per (active expert, row batch); the grid is
 //    sized for the most experts T*k slots can reach and surplus workgroups
-//    exit on the device-side count.  Each loads its 4-row x 1-chunk-per-lane
-//    slice of the expert's backbone and factor entries once and applies them
-//    to every slot routed to that expert (same arithmetic as the dense
-//    decode kernel: mask-only unpack into subnormal fp16 lanes, v_dot2,
-//    per-chunk scale and zero in fp32, B t in the same partial sums,
-//    transposing butterfly, fixed-order K-slice reduction).
+//    exit on the device-side count.  Each wave loads its slice (4 rows for
+//    4-bit codes, 2 for 2-bit; one 16-byte chunk per lane) of the expert's
+//    backbone and factor entries once and applies it to every slot routed to
+//    that expert, loading the next slot's activations while it computes the
+//    current one.  Same arithmetic as the dense decode kernel: mask-only
+//    unpack into subnormal fp16 lanes, v_dot2, per-chunk scale and zero in
+//    fp32, B t in the same partial sums, transposing butterfly, fixed-order
+//    K-slice reduction.
 
 #include "cl_device.h"
 #include "cl_internal.h"
@@ -34,7 +39,9 @@ namespace cl {
 
 namespace {
 
-constexpr int kR = 4;                // rows per wave batch
+// rows per wave batch: 4 for 4-bit codes, 2 for 2-bit (twice the
+// activation registers per chunk)
+constexpr int rows_per_wave(int bits) { return bits == 4 ? 4 : 2; }
 constexpr int kMaxSlots = 1024;      // T * k
 constexpr int kMaxExperts = 1024;
 
@@ -58,6 +65,7 @@ struct MoeArgs {
     f16x2* xp;               // [rows][d_in/2]
     float* sx;               // [rows][chunks]
     int ks, cps, bpe;        // K slices, chunks per slice, batches per expert
+    int rq;                  // prep workgroups per expert (4 rank rows each)
 };
 
 template <int BITS>
@@ -66,37 +74,46 @@ __global__ __launch_bounds__(256) void moe_prep_kernel(MoeArgs a) {
     __shared__ int sids[kMaxSlots];
     __shared__ int mys[kMaxSlots];          // this expert's slots, in slot order
     __shared__ unsigned routed[kMaxExperts / 32];
-    __shared__ int cnt_lt, cnt_eq;
+    __shared__ int cnt_lt, cnt_eq, sel;
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
     const int S = a.T * a.k;
     const int blk = blockIdx.x;
 
-    if (blk < a.E) {
-        const int e = blk;
+    const int max_active = S < a.E ? S : a.E;
+    if (blk < max_active * a.rq) {
+        // workgroup (j, quad): the j-th routed expert (ascending id), its
+        // rank rows 4 quad .. 4 quad + 3
+        const int j = blk / a.rq;
+        const int quad = blk - j * a.rq;
         for (int i = tid; i < kMaxExperts / 32; i += 256) routed[i] = 0u;
-        if (tid == 0) { cnt_lt = 0; cnt_eq = 0; }
+        if (tid == 0) { cnt_lt = 0; cnt_eq = 0; sel = -1; }
         __syncthreads();
-        int lt = 0, eq = 0;
         for (int sl = tid; sl < S; sl += 256) {
             const int id = a.ids[sl];
             sids[sl] = id;
-            if (id >= 0 && id < a.E) {
-                atomicOr(&routed[id >> 5], 1u << (id & 31));
-                lt += id < e;
-                eq += id == e;
+            if (id >= 0 && id < a.E) atomicOr(&routed[id >> 5], 1u << (id & 31));
+        }
+        __syncthreads();
+        // the j-th set bit of the routed bitmap: one thread per 32-expert word
+        if (tid < (a.E + 31) / 32) {
+            int below = 0;
+            for (int i = 0; i < tid; ++i) below += __popc(routed[i]);
+            unsigned m = routed[tid];
+            const int here = __popc(m);
+            if (j >= below && j < below + here) {
+                for (int k = below; k < j; ++k) m &= m - 1u;     // drop the lower set bits
+                sel = 32 * tid + __builtin_ctz(m);
             }
         }
-        atomicAdd(&cnt_lt, lt);
-        atomicAdd(&cnt_eq, eq);
+        if (j == 0 && quad == 0 && tid == 0) {
+            int n = 0;
+            for (int i = 0; i < (a.E + 31) / 32; ++i) n += __popc(routed[i]);
+            *a.n_active = n;
+        }
         __syncthreads();
-        if (e == 0) {
-            if (tid == 0) {
-                int n = 0;
-                for (int i = 0; i < (a.E + 31) / 32; ++i) n += __popc(routed[i]);
-                *a.n_active = n;
-            }
+        if (j == 0 && quad == 0) {
             // out-of-range ids: their output rows are zero
             for (int sl = 0; sl < S; ++sl) {
                 const int id = sids[sl];
@@ -104,60 +121,75 @@ __global__ __launch_bounds__(256) void moe_prep_kernel(MoeArgs a) {
                 for (int o = tid; o < a.d_out; o += 256) store_out(a.y, static_cast<size_t>(sl) * a.d_out + o, 0.f, a.out);
             }
         }
+        const int e = sel;
+        if (e < 0) return;                      // fewer than j + 1 routed experts
+        int lt = 0, eq = 0;
+        for (int sl = tid; sl < S; sl += 256) {
+            const int id = sids[sl];
+            lt += id >= 0 && id < e;
+            eq += id == e;
+        }
+        atomicAdd(&cnt_lt, lt);
+        atomicAdd(&cnt_eq, eq);
+        __syncthreads();
         const int ne = cnt_eq;
-        if (ne == 0) return;
-        int ae = 0;
-        for (int i = 0; i < (e >> 5); ++i) ae += __popc(routed[i]);
-        ae += __popc(routed[e >> 5] & ((1u << (e & 31)) - 1u));
         int rank = a.r_max > 0 ? a.ranks[e] : 0;     // ranks may be null when r_max is 0
         rank = rank < 0 ? 0 : (rank > a.r_max ? a.r_max : rank);
-        if (tid == 0) {
-            a.table[4 * ae + 0] = e;
-            a.table[4 * ae + 1] = cnt_lt;
-            a.table[4 * ae + 2] = ne;
-            a.table[4 * ae + 3] = rank;
+        if (quad == 0 && tid == 0) {
+            a.table[4 * j + 0] = e;
+            a.table[4 * j + 1] = cnt_lt;
+            a.table[4 * j + 2] = ne;
+            a.table[4 * j + 3] = rank;
         }
         // this expert's slots in slot order
         for (int sl = tid; sl < S; sl += 256) {
             if (sids[sl] != e) continue;
             int pos = 0;
             for (int s2 = 0; s2 < sl; ++s2) pos += sids[s2] == e;
-            a.sorted[cnt_lt + pos] = sl;
+            if (quad == 0) a.sorted[cnt_lt + pos] = sl;
             mys[pos] = sl;
         }
         __syncthreads();
-        // t[slot][i] = A_e[i] . x_slot for i < rank: one wave per (slot, i)
-        if (rank > 0) {
-            const uint16_t* Ae = a.A + static_cast<size_t>(e) * a.a_stride;
-            for (int item = wave; item < ne * rank; item += 4) {
-                const int jj = item / rank, i = item - jj * rank;
-                const int sl = mys[jj];
-                const int xrow = a.x_per_slot ? sl : sl / a.k;
-                const uint16_t* xr = a.x + static_cast<size_t>(xrow) * a.d_in;
-                const uint16_t* ar = Ae + static_cast<size_t>(i) * a.d_in;
-                float acc = 0.f;
-                for (int c = lane * 8; c < a.d_in; c += 64 * 8) {
-                    const u32x4 av = *reinterpret_cast<const u32x4*>(ar + c);
-                    uint32_t xw[4];
-                    load8_f16(xr + c, a.act, xw);
+        // t[slot][i] = A_e[i] . x_slot: one wave per rank row, four slots at a time
+        const int i = 4 * quad + wave;
+        if (i >= rank) return;
+        const uint16_t* ar = a.A + static_cast<size_t>(e) * a.a_stride + static_cast<size_t>(i) * a.d_in;
+        for (int j0 = 0; j0 < ne; j0 += 4) {
+            const uint16_t* xr[4];
+            int sl4[4];
 #pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        // copy the vector element to a scalar first: a bit_cast
-                        // of a subscripted ext_vector reads element 0
-                        const uint32_t aq = av[q], xq = xw[q];
-                        acc = dot2(__builtin_bit_cast(f16x2, aq), __builtin_bit_cast(f16x2, xq), acc);
-                    }
-                }
-                acc = wave_sum(acc);
-                if (lane == 0) a.t[static_cast<size_t>(sl) * a.r_max + i] = acc;
+            for (int u = 0; u < 4; ++u) {
+                sl4[u] = mys[j0 + u < ne ? j0 + u : j0];
+                const int xrow = a.x_per_slot ? sl4[u] : sl4[u] / a.k;
+                xr[u] = a.x + static_cast<size_t>(xrow) * a.d_in;
             }
+            float acc[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 2
+            for (int c = lane * 8; c < a.d_in; c += 64 * 8) {
+                const u32x4 av = *reinterpret_cast<const u32x4*>(ar + c);
+                uint32_t xw[4][4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) load8_f16(xr[u] + c, a.act, xw[u]);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    // copy the vector element to a scalar first: a bit_cast
+                    // of a subscripted ext_vector reads element 0
+                    const uint32_t aq = av[q];
+#pragma unroll
+                    for (int u = 0; u < 4; ++u)
+                        acc[u] = dot2(__builtin_bit_cast(f16x2, aq), __builtin_bit_cast(f16x2, xw[u][q]), acc[u]);
+                }
+            }
+            const float tot = wave_sum_multi<4>(acc);      // lane l: slot j0 + l / 16
+            const int u = lane >> 4;
+            if ((lane & 15) == 0 && j0 + u < ne) a.t[static_cast<size_t>(sl4[u]) * a.r_max + i] = tot;
         }
         return;
     }
     // activation preparation, one thread per (row, chunk)
     const int rows = a.x_per_slot ? S : a.T;
     const int chunks = a.d_in / CPW / 4;
-    const long long item = static_cast<long long>(blk - a.E) * 256 + tid;
+    const long long item = static_cast<long long>(blk - max_active * a.rq) * 256 + tid;
     if (item >= static_cast<long long>(rows) * chunks) return;
     const int row = static_cast<int>(item / chunks);
     const int c = static_cast<int>(item % chunks);
@@ -177,7 +209,7 @@ __global__ __launch_bounds__(256) void moe_prep_kernel(MoeArgs a) {
 // NB: factor columns per lane (r_max <= NB * 64 * ks); 0 when r_max is 0.
 template <int BITS, int CPL, int NB>
 __global__ __launch_bounds__(512) void moe_kernel(MoeArgs a) {
-    constexpr int R = kR;
+    constexpr int R = rows_per_wave(BITS);
     constexpr int CPW = 32 / BITS;
     constexpr int HPW = CPW / 2;
     constexpr int CPC = 4 * CPW;
@@ -247,45 +279,63 @@ __global__ __launch_bounds__(512) void moe_kernel(MoeArgs a) {
         }
     }
 
-    for (int jslot = 0; jslot < scnt; ++jslot) {
-        const int sl = a.sorted[sbeg + jslot];
+    // The expert's slot ids, 64 at a time in the lanes (read back with a
+    // shuffle); each slot's activations are loaded one slot ahead.
+    auto load_x = [&](int sl, f16x2 (&xv)[PPC], float& sxv, float (&tv)[NBA]) {
         const int xrow = a.x_per_slot ? sl : sl / a.k;
-        float acc[R];
+        const u32x4* src = reinterpret_cast<const u32x4*>(a.xp + static_cast<size_t>(xrow) * (a.d_in / 2) +
+                                                          static_cast<size_t>(cidx[0]) * PPC);
 #pragma unroll
-        for (int r = 0; r < R; ++r) acc[r] = 0.f;
+        for (int p4 = 0; p4 < PPC / 4; ++p4) {
+            const u32x4 u = src[p4];
 #pragma unroll
-        for (int j = 0; j < CPL; ++j) {
-            f16x2 xv[PPC];
-            const u32x4* src = reinterpret_cast<const u32x4*>(a.xp + static_cast<size_t>(xrow) * (a.d_in / 2) +
-                                                              static_cast<size_t>(cidx[j]) * PPC);
-#pragma unroll
-            for (int p4 = 0; p4 < PPC / 4; ++p4) {
-                const u32x4 u = src[p4];
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const uint32_t uq = u[q];
-                    xv[4 * p4 + q] = __builtin_bit_cast(f16x2, uq);
-                }
-            }
-            const float sxv = a.sx[static_cast<size_t>(xrow) * chunks + cidx[j]];
-#pragma unroll
-            for (int r = 0; r < R; ++r) {
-                float d[NACC];
-#pragma unroll
-                for (int q = 0; q < NACC; ++q) d[q] = 0.f;
-#pragma unroll
-                for (int w = 0; w < 4; ++w) dot_word<BITS>(qv[r][j][w], xv + w * HPW, d);
-                const float v = fmaf(combine<BITS>(d), 16777216.0f, -zc[r][j] * sxv);
-                acc[r] = fmaf(sc[r][j], v, acc[r]);
+            for (int q = 0; q < 4; ++q) {
+                const uint32_t uq = u[q];
+                xv[4 * p4 + q] = __builtin_bit_cast(f16x2, uq);
             }
         }
+        sxv = a.sx[static_cast<size_t>(xrow) * chunks + cidx[0]];
 #pragma unroll
         for (int m = 0; m < NB; ++m) {
             const int i = lane + 64 * (slice + ks * m);
-            const float tv = i < rank ? a.t[static_cast<size_t>(sl) * a.r_max + i] : 0.f;
-#pragma unroll
-            for (int r = 0; r < R; ++r) acc[r] = fmaf(bv[r][m], tv, acc[r]);
+            tv[m] = i < rank ? a.t[static_cast<size_t>(sl) * a.r_max + i] : 0.f;
         }
+    };
+    int lane_slot = lane < scnt ? a.sorted[sbeg + lane] : 0;
+    f16x2 xn[PPC];
+    float sxn, tn[NBA];
+    load_x(__shfl(lane_slot, 0, 64), xn, sxn, tn);
+    for (int jslot = 0; jslot < scnt; ++jslot) {
+        const int sl = __shfl(lane_slot, jslot & 63, 64);
+        f16x2 xv[PPC];
+        float tv[NBA];
+#pragma unroll
+        for (int p = 0; p < PPC; ++p) xv[p] = xn[p];
+        const float sxv = sxn;
+#pragma unroll
+        for (int m = 0; m < NBA; ++m) tv[m] = tn[m];
+        if (jslot + 1 < scnt) {
+            if (((jslot + 1) & 63) == 0) {
+                const int j = jslot + 1 + lane;
+                lane_slot = j < scnt ? a.sorted[sbeg + j] : 0;
+            }
+            load_x(__shfl(lane_slot, (jslot + 1) & 63, 64), xn, sxn, tn);
+        }
+        float acc[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            float d[NACC];
+#pragma unroll
+            for (int q = 0; q < NACC; ++q) d[q] = 0.f;
+#pragma unroll
+            for (int w = 0; w < 4; ++w) dot_word<BITS>(qv[r][0][w], xv + w * HPW, d);
+            const float v = fmaf(combine<BITS>(d), 16777216.0f, -zc[r][0] * sxv);
+            acc[r] = sc[r][0] * v;
+        }
+#pragma unroll
+        for (int m = 0; m < NB; ++m)
+#pragma unroll
+            for (int r = 0; r < R; ++r) acc[r] = fmaf(bv[r][m], tv[m], acc[r]);
         const float tot = wave_sum_multi<R>(acc);
         constexpr int SPAN = 64 / R;
         const int rr = (lane / SPAN) & (R - 1);
@@ -385,7 +435,8 @@ hipError_t launch_moe_decode(const QW& w, const uint16_t* A, const uint16_t* B, 
     const int threads = 64 * (a.ks > 4 ? a.ks : 4);
     if (a.ks > 8 || threads > 512 || threads % (64 * a.ks)) return hipErrorInvalidConfiguration;
     const int rg_per_block = threads / 64 / a.ks;
-    const int rgroups = (w.d_out + kR - 1) / kR;
+    a.rq = r_max > 0 ? (r_max + 3) / 4 : 1;
+    const int rgroups = (w.d_out + rows_per_wave(w.bits) - 1) / rows_per_wave(w.bits);
     a.bpe = (rgroups + rg_per_block - 1) / rg_per_block;
     const int S = T * k;
     const int max_active = S < E ? S : E;
@@ -394,7 +445,7 @@ hipError_t launch_moe_decode(const QW& w, const uint16_t* A, const uint16_t* B, 
 
     const int rows = x_per_slot ? S : T;
     const long long items = static_cast<long long>(rows) * chunks;
-    const unsigned pgrid = static_cast<unsigned>(E + (items + 255) / 256);
+    const unsigned pgrid = static_cast<unsigned>(max_active * a.rq + (items + 255) / 256);
     if (w.bits == 4)
         hipLaunchKernelGGL(moe_prep_kernel<4>, dim3(pgrid), dim3(256), 0, st, a);
     else
