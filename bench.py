@@ -9,13 +9,21 @@ seeded N(0, 0.02) draws quantized by the library on the GPU; compensation
 factors are seeded fp16 stand-ins (the forward's cost does not depend on their
 values).  Steps rotate over enough distinct copies of the layer (>= 1.5 GiB)
 that every step streams its weights from HBM, not from the 256 MB Infinity
-Cache.  Each step is a captured HIP graph of the four window calls, so host launch
-overhead is outside the timed region; the inputs are resident in HBM.
+Cache.  Each step is a captured HIP graph of the four window calls, so host
+launch overhead is outside the timed region; the inputs are resident in HBM.
 
 Prints one JSON line: whole-job algorithmic HBM throughput (GB/s) of the step,
 the roofline of the dominant call (the gate matrix, 14336 x 4096) timed with
-HIP events on the stream it runs on, and the fp64 CPU oracle timed on the
-same layer.
+HIP events on the stream it runs on, the fp64 CPU oracle timed on a bounded
+sample of the same layer, and (unless --no-extras) the other measured
+workloads: the layer at 4 and 16 tokens, the 2-bit layer with its gate rank
+sweep, prefill (M = 2048) in TFLOP/s and the 48-layer MoE decode.
+
+--copy-calibration runs only a plain 256 MiB device-to-device copy (the
+reference kernel for scaling HBM traffic counters) and prints its size;
+--only {decode,tokens,layer2bit,prefill,moe} runs one workload (for
+profiling): "decode" prints the line above without extras or CPU baseline,
+the others print their own results.
 """
 
 import argparse
@@ -30,6 +38,32 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+MFMA_F16_PEAK_TFLOPS = 2500.0
+
+# HBM traffic of one gate-matrix decode call (prepare + backbone), from
+# rocprofv3 FETCH_SIZE and WRITE_SIZE passes over `bench.py --only decode`,
+# scaled by the same counters on a plain 256 MiB device copy (FETCH_SIZE
+# reads half the copied bytes: x2; WRITE_SIZE exact: x1).  Valid only for the
+# kernel sources it was measured on (their SHA-256 below); null otherwise.
+GATE_TRAFFIC = {"fetch_bytes": (32507 + 688) * 1024, "write_bytes": (56 + 10) * 1024,
+                "sources": ("paper_2605_05819_amd/csrc/decode.hip", "paper_2605_05819_amd/csrc/gemv_common.h",
+                            "paper_2605_05819_amd/csrc/cl_device.h"),
+                "sha256": "6919f644bd6d48ca5103e3af79dce2d00e46f677f25c141a3159caedd62fc5c0"}
+
+
+def sources_sha256(paths):
+    import hashlib
+    h = hashlib.sha256()
+    for p in paths:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def gate_traffic():
+    if GATE_TRAFFIC["sha256"] != sources_sha256(GATE_TRAFFIC["sources"]):
+        return None
+    return GATE_TRAFFIC["fetch_bytes"] + GATE_TRAFFIC["write_bytes"]
 
 
 def parse():
@@ -40,17 +74,246 @@ def parse():
     p.add_argument("--tokens", type=int, default=1)
     p.add_argument("--rotate-gib", type=float, default=1.5)
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-extras", action="store_true")
+    p.add_argument("--copy-calibration", action="store_true")
+    p.add_argument("--only", choices=("decode", "tokens", "layer2bit", "prefill", "moe"), default=None,
+                   help="run one workload and print its own JSON line (for profiling)")
     return p.parse_args()
 
 
-def algorithmic_bytes(spec, T):
+def algorithmic_bytes(spec, T, rank=None):
     """HBM bytes a compensated decode must move at minimum: packed codes,
     fp16 scales and zeros, the used rows of A and columns of B, activations in
     and fp16 outputs out."""
+    r = spec.rank if rank is None else rank
     q = spec.d_out * spec.d_in * spec.bits // 8
     sz = 2 * 2 * spec.d_out * (spec.d_in // spec.group_size)
-    ab = 2 * spec.rank * (spec.d_in + spec.d_out)
+    ab = 2 * r * (spec.d_in + spec.d_out)
     return q + sz + ab + 2 * T * spec.d_in + 2 * T * spec.d_out
+
+
+class Timer:
+    """HIP graphs captured and replayed on one stream, timed with events
+    recorded on that stream."""
+
+    def __init__(self, torch):
+        self.torch = torch
+        self.stream = torch.cuda.Stream()
+        self.e0 = torch.cuda.Event(enable_timing=True)
+        self.e1 = torch.cuda.Event(enable_timing=True)
+
+    def capture(self, fn):
+        torch = self.torch
+        with torch.cuda.stream(self.stream):
+            fn()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=self.stream):
+            fn()
+        torch.cuda.synchronize()
+        return g
+
+    def time(self, graphs, n, warm=None):
+        """Average ms per replay of n replays cycling through graphs."""
+        torch = self.torch
+        with torch.cuda.stream(self.stream):
+            for i in range(min(n, len(graphs)) if warm is None else warm):
+                graphs[i % len(graphs)].replay()
+            self.stream.synchronize()
+            self.e0.record(self.stream)
+            for i in range(n):
+                graphs[i % len(graphs)].replay()
+            self.e1.record(self.stream)
+        torch.cuda.synchronize()
+        return self.e0.elapsed_time(self.e1) / n
+
+
+def device_layer(torch, cl, wl, layer, dev, rotate_gib):
+    """The layer quantized by the library, plus copies for HBM-cold steps."""
+    base = []
+    for m, spec in enumerate(layer.linears):
+        W = torch.from_numpy(wl.weight((spec.d_out, spec.d_in), layer.index, 0, m)).to(dev)
+        w = cl.quantize_pack(W, spec.bits, spec.group_size)
+        del W
+        A, B = wl.standin_factors(spec.d_out, spec.d_in, spec.r_max, layer.index, 0, m)
+        c = cl.LowRank(torch.from_numpy(A).to(dev), torch.from_numpy(B).to(dev), spec.r_max, spec.rank)
+        base.append((w, c))
+    torch.cuda.synchronize()
+    layer_bytes = sum(w.q.numel() * 4 + w.scales.numel() * 4 + c.A.numel() * 2 + c.B.numel() * 2 for w, c in base)
+    ncopies = max(2, int(np.ceil(rotate_gib * 2 ** 30 / layer_bytes)))
+    copies = [base]
+    for _ in range(ncopies - 1):
+        copies.append([(cl.QWeight(w.q.clone(), w.scales.clone(), w.zeros.clone(), w.d_out, w.d_in, w.bits,
+                                   w.group_size), cl.LowRank(c.A.clone(), c.B.clone(), c.r_max, c.rank))
+                       for w, c in base])
+    return copies
+
+
+WINDOWS = (("q", "k", "v"), ("o",), ("gate", "up"), ("down",))
+
+
+def layer_step(torch, cl, wl, timer, copies, layer, T, dev, steps, warmup):
+    """ms per step of the layer's four windows (graph per copy), and the
+    inputs/outputs used."""
+    specs = layer.linears
+    names = [s.name for s in specs]
+    windows = [[names.index(n) for n in grp] for grp in WINDOWS]
+    xs, ys = [], []
+    for m, spec in enumerate(specs):
+        x = wl.activation((T, spec.d_in), layer.index, 0, m)
+        xs.append(torch.from_numpy(x.bits.view(np.int16)).view(torch.float16).to(dev))
+        ys.append(torch.empty((T, spec.d_out), dtype=torch.float16, device=dev))
+    base = copies[0]
+    wxs = [xs[grp[0]] for grp in windows]
+    wwss = [cl.workspace(cl.window_workspace([base[m][0] for m in grp], [base[m][1] for m in grp], T), dev)
+            for grp in windows]
+
+    def calls(k):
+        def run():
+            for wi, grp in enumerate(windows):
+                cl.linear_decode_window([copies[k][m][0] for m in grp], [copies[k][m][1] for m in grp],
+                                        wxs[wi], ys=[ys[m] for m in grp], ws=wwss[wi], stream=timer.stream)
+        return run
+
+    graphs = [timer.capture(calls(k)) for k in range(len(copies))]
+    ms = timer.time(graphs, steps, warm=warmup)
+    return ms, xs, ys
+
+
+def per_matrix(torch, cl, timer, copies, specs, xs, ys, T, dev, rank=None, m_only=None):
+    """us per single-linear call of each matrix (graph of one call per copy)."""
+    out = {}
+    for m, spec in enumerate(specs):
+        if m_only is not None and m != m_only:
+            continue
+        cs = []
+        for k in range(len(copies)):
+            w, c = copies[k][m]
+            cs.append((w, c if rank is None else cl.LowRank(c.A, c.B, c.r_max, rank)))
+        ws = cl.workspace(cl.linear_workspace(cs[0][0], cs[0][1], T), dev)
+
+        def run():
+            for w, c in cs:
+                cl.linear_decode(w, c, xs[m], y=ys[m], ws=ws, stream=timer.stream)
+        g = timer.capture(run)
+        out[spec.name] = timer.time([g], 20) * 1e3 / len(cs)
+    return out
+
+
+def bench_tokens(torch, cl, wl, timer, copies, layer, dev):
+    """The layer step at 4 and 16 decode tokens."""
+    res = {}
+    for T in (4, 16):
+        ms, _, _ = layer_step(torch, cl, wl, timer, copies, layer, T, dev, 40, 8)
+        b = sum(algorithmic_bytes(s, T) for s in layer.linears)
+        res["layer_T%d" % T] = {"ms_per_step": round(ms, 5), "gbs": round(b / (ms * 1e-3) / 1e9, 1)}
+    return res
+
+
+def bench_layer2bit(torch, cl, wl, timer, dev, rotate_gib):
+    """The 2-bit group-64 layer (ranks up to 256 under 128 x 7) at one token,
+    and the rank sweep r in {0, 32, 128, 256} on its 14336 x 4096 gate."""
+    layer2 = wl.llama_layer_2bit()
+    copies2 = device_layer(torch, cl, wl, layer2, dev, rotate_gib)
+    ms2, xs2, ys2 = layer_step(torch, cl, wl, timer, copies2, layer2, 1, dev, 80, 8)
+    b2 = sum(algorithmic_bytes(s, 1) for s in layer2.linears)
+    sweep = {}
+    g2 = [s.name for s in layer2.linears].index("gate")
+    for r in (0, 32, 128, 256):
+        u = per_matrix(torch, cl, timer, copies2, layer2.linears, xs2, ys2, 1, dev, rank=r, m_only=g2)["gate"]
+        sweep["r%d" % r] = {"us": round(u, 3), "gbs": round(algorithmic_bytes(layer2.linears[g2], 1, r) / u / 1e3, 1)}
+    return {"ms_per_step": round(ms2, 5), "gbs": round(b2 / (ms2 * 1e-3) / 1e9, 1),
+            "ranks": "/".join(str(s.rank) for s in layer2.linears), "gate_rank_sweep": sweep}
+
+
+def bench_prefill(torch, cl, wl, timer, dev):
+    """M = 2048 tokens through 4096 x 4096 and 14336 x 4096, rank 64, fp16
+    and bf16 activations: us per call and TFLOP/s (2MNK + 2Mr(K + N))."""
+    M, r = 2048, 64
+    res = {}
+    for (N, K) in ((4096, 4096), (14336, 4096)):
+        W = torch.from_numpy(wl.weight((N, K), 3, 0, N)).to(dev)
+        w = cl.quantize_pack(W, 4, 128)
+        del W
+        A, B = wl.standin_factors(N, K, r, 3, 0, N)
+        c = cl.LowRank(torch.from_numpy(A).to(dev), torch.from_numpy(B).to(dev), r, r)
+        for act in ("fp16", "bf16"):
+            x = wl.activation((M, K), 3, 0, N, dtype=act)
+            dt = torch.float16 if act == "fp16" else torch.bfloat16
+            X = torch.from_numpy(x.bits.view(np.int16)).view(dt).to(dev)
+            Y = torch.empty((M, N), dtype=torch.float16, device=dev)
+            need = cl.prefill_workspace(w, c, M)
+            ws = cl.workspace(need, dev) if need else None
+            g = timer.capture(lambda: cl.linear_prefill(w, c, X, Y=Y, ws=ws, stream=timer.stream))
+            us = timer.time([g], 30) * 1e3
+            flops = 2.0 * M * N * K + 2.0 * M * r * (K + N)
+            res["%dx%d_%s" % (N, K, act)] = {"us": round(us, 2), "tflops": round(flops / us / 1e6, 1)}
+    return res
+
+
+def bench_moe(torch, cl, wl, timer, dev):
+    """48 stacked MoE layers (128 experts, gate/up 768 x 2048, down
+    2048 x 768, 4-bit g128, per-expert ranks from {0, 8, 16, 32}), top-8
+    routing: per layer gate and up on the token's input, down on each slot's
+    input.  Codes, scales and factors of the stacked experts are seeded random
+    device data (the cost does not depend on the values).  GB/s counts only the
+    routed experts' bytes."""
+    L, E, K = wl.MOE_LAYERS, wl.MOE_EXPERTS, wl.MOE_TOPK
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(5)
+    mats = (("gate", 0), ("up", 1), ("down", 2))
+    layers = {}
+    for name, m in mats:
+        d_out, d_in = wl.MOE_SHAPES[name]
+        lst = []
+        for l in range(L):
+            q = torch.randint(-2 ** 31, 2 ** 31 - 1, (E, d_out, d_in // 8), dtype=torch.int32, device=dev,
+                              generator=gen)
+            s = (torch.rand((E, d_out, d_in // 128), device=dev, generator=gen) * 0.004 + 0.005).half()
+            z = torch.randint(0, 16, (E, d_out, d_in // 128), device=dev, generator=gen).half()
+            A = (torch.randn((E, 32, d_in), device=dev, generator=gen) * 0.05).half()
+            B = (torch.randn((E, d_out, 32), device=dev, generator=gen) * 0.05).half()
+            ranks = torch.from_numpy(wl.moe_expert_ranks(5, l, m)).to(dev)
+            lst.append(cl.MoeExperts(q, s, z, A, B, ranks, E, d_out, d_in, 4, 128, 32))
+        layers[name] = lst
+    res = {}
+    for T in (1, 8, 64):
+        ids = [torch.from_numpy(wl.routing(T, 5, l)[0]).to(dev) for l in range(L)]
+        xs = {n: torch.from_numpy(wl.activation((T, K, wl.MOE_SHAPES[n][1]) if n == "down"
+                                                else (T, wl.MOE_SHAPES[n][1]), 5, 0, m).bits.view(np.int16))
+              .view(torch.float16).to(dev) for n, m in mats}
+        ys = {n: torch.empty((T, K, wl.MOE_SHAPES[n][0]), dtype=torch.float16, device=dev) for n, _ in mats}
+        wss = {n: cl.workspace(cl.moe_workspace(layers[n][0], T, K, n == "down"), dev) for n, _ in mats}
+
+        def run():
+            for l in range(L):
+                for n, _ in mats:
+                    cl.moe_linear_decode(layers[n][l], xs[n], ids[l], y=ys[n], ws=wss[n], stream=timer.stream)
+        g = timer.capture(run)
+        us = timer.time([g], 10) * 1e3
+        nbytes = 0
+        for l in range(L):
+            routed = np.unique(ids[l].cpu().numpy())
+            for n, _ in mats:
+                d_out, d_in = wl.MOE_SHAPES[n]
+                rk = layers[n][l].ranks.cpu().numpy()
+                for e in routed:
+                    nbytes += d_out * d_in // 2 + 4 * d_out * (d_in // 128) + 2 * int(rk[e]) * (d_in + d_out)
+                nbytes += 2 * xs[n].numel() + 2 * ys[n].numel()
+        res["T%d" % T] = {"us_per_layer": round(us / L, 2), "gbs": round(nbytes / us / 1e3, 1),
+                          "bytes_per_layer": nbytes // L}
+    return res
+
+
+def copy_calibration(torch, dev):
+    n = 64 << 20                                   # 256 MiB of fp32
+    a = torch.ones(n, dtype=torch.float32, device=dev)
+    b = torch.empty_like(a)
+    for _ in range(5):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes_read": 4 * n, "copy_calibration_bytes_written": 4 * n,
+                      "calls": 5}))
 
 
 def main():
@@ -65,106 +328,50 @@ def main():
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.copy_calibration:
+        copy_calibration(torch, dev)
+        return
+    timer = Timer(torch)
     T = args.tokens
     layer = wl.llama_layer()
     specs = layer.linears
+    only = args.only
+    if only in ("prefill", "moe"):
+        fn = bench_prefill if only == "prefill" else bench_moe
+        print(json.dumps({only: fn(torch, cl, wl, timer, dev)}))
+        return
+    if only == "layer2bit":
+        print(json.dumps({"layer_2bit_g64_T1": bench_layer2bit(torch, cl, wl, timer, dev, args.rotate_gib)}))
+        return
+    copies = device_layer(torch, cl, wl, layer, dev, args.rotate_gib)
+    ncopies = len(copies)
+    if only == "tokens":
+        print(json.dumps(bench_tokens(torch, cl, wl, timer, copies, layer, dev)))
+        return
 
-    # ---- one layer on the device (library quantizer), then copies
-    base = []
-    for m, spec in enumerate(specs):
-        W = torch.from_numpy(wl.weight((spec.d_out, spec.d_in), layer.index, 0, m)).to(dev)
-        w = cl.quantize_pack(W, spec.bits, spec.group_size)
-        del W
-        A, B = wl.standin_factors(spec.d_out, spec.d_in, spec.r_max, layer.index, 0, m)
-        c = cl.LowRank(torch.from_numpy(A).to(dev), torch.from_numpy(B).to(dev), spec.r_max, spec.rank)
-        base.append((w, c))
-    torch.cuda.synchronize()
-    layer_bytes = sum(w.q.numel() * 4 + w.scales.numel() * 4 + c.A.numel() * 2 + c.B.numel() * 2
-                      for w, c in base)
-    ncopies = max(2, int(np.ceil(args.rotate_gib * 2 ** 30 / layer_bytes)))
-    copies = [base]
-    for _ in range(ncopies - 1):
-        copies.append([(cl.QWeight(w.q.clone(), w.scales.clone(), w.zeros.clone(), w.d_out, w.d_in, w.bits,
-                                   w.group_size), cl.LowRank(c.A.clone(), c.B.clone(), c.r_max, c.rank))
-                       for w, c in base])
-    xs, ys, wss = [], [], []
-    for m, spec in enumerate(specs):
-        x = wl.activation((T, spec.d_in), layer.index, 0, m)
-        xs.append(torch.from_numpy(x.bits.view(np.int16)).view(torch.float16).to(dev))
-        ys.append(torch.empty((T, spec.d_out), dtype=torch.float16, device=dev))
-        wss.append(cl.workspace(cl.linear_workspace(base[m][0], base[m][1], T), dev))
-    torch.cuda.synchronize()
-
-    stream = torch.cuda.Stream()
-
-    def capture(fn):
-        """A HIP graph of fn() recorded on `stream` (after one eager run)."""
-        with torch.cuda.stream(stream):
-            fn()
-        torch.cuda.synchronize()
-        g = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(g, stream=stream):
-            fn()
-        torch.cuda.synchronize()
-        return g
-
-    # the layer's compensation windows: matrices that read the same input
-    names = [s.name for s in specs]
-    windows = [[names.index(n) for n in grp] for grp in (("q", "k", "v"), ("o",), ("gate", "up"), ("down",))]
-    wxs = [xs[grp[0]] for grp in windows]          # one input per window
-    wwss = [cl.workspace(cl.window_workspace([base[m][0] for m in grp], [base[m][1] for m in grp], T), dev)
-            for grp in windows]
-
-    def layer_calls(k):
-        def run():
-            for wi, grp in enumerate(windows):
-                cl.linear_decode_window([copies[k][m][0] for m in grp], [copies[k][m][1] for m in grp],
-                                        wxs[wi], ys=[ys[m] for m in grp], ws=wwss[wi], stream=stream)
-        return run
-
-    step_graphs = [capture(layer_calls(k)) for k in range(ncopies)]
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-
-    def timed(graphs, n):
-        """Average ms per replay of n replays cycling through graphs, with
-        events on the stream the kernels run on."""
-        with torch.cuda.stream(stream):
-            for i in range(min(n, len(graphs))):
-                graphs[i % len(graphs)].replay()
-            stream.synchronize()
-            e0.record(stream)
-            for i in range(n):
-                graphs[i % len(graphs)].replay()
-            e1.record(stream)
-        torch.cuda.synchronize()
-        return e0.elapsed_time(e1) / n
-
-    with torch.cuda.stream(stream):
-        for i in range(args.warmup):
-            step_graphs[i % ncopies].replay()
-    torch.cuda.synchronize()
-    ms_step = timed(step_graphs, args.steps)
+    ms_step, xs, ys = layer_step(torch, cl, wl, timer, copies, layer, T, dev, args.steps, args.warmup)
     step_bytes = sum(algorithmic_bytes(s, T) for s in specs)
     value = step_bytes / (ms_step * 1e-3) / 1e9
 
-    # ---- per matrix: graphs of one call on each copy, back to back
-    per_matrix_us = {}
-    per_matrix_gbs = {}
-    for m, spec in enumerate(specs):
-        def calls(m=m):
-            for k in range(ncopies):
-                w, c = copies[k][m]
-                cl.linear_decode(w, c, xs[m], y=ys[m], ws=wss[m], stream=stream)
-        g = capture(calls)
-        us = timed([g], 20) * 1e3 / ncopies
-        per_matrix_us[spec.name] = round(us, 3)
-        per_matrix_gbs[spec.name] = round(algorithmic_bytes(spec, T) / us / 1e3, 1)
+    us = per_matrix(torch, cl, timer, copies, specs, xs, ys, T, dev)
+    per_matrix_us = {k: round(v, 3) for k, v in us.items()}
+    per_matrix_gbs = {s.name: round(algorithmic_bytes(s, T) / us[s.name] / 1e3, 1) for s in specs}
     gi = [s.name for s in specs].index("gate")
-    gate_us = per_matrix_us["gate"]
+    gate_us = us["gate"]
     gate_bytes = algorithmic_bytes(specs[gi], T)
     achieved = gate_bytes / (gate_us * 1e-6) / 1e9
 
-    cpu = None if args.no_cpu_baseline else cpu_baseline(specs, layer, T)
+    extras = None
+    if only is None and not args.no_extras:
+        extras = bench_tokens(torch, cl, wl, timer, copies, layer, dev)
+        del copies
+        torch.cuda.empty_cache()
+        extras["layer_2bit_g64_T1"] = bench_layer2bit(torch, cl, wl, timer, dev, args.rotate_gib)
+        torch.cuda.empty_cache()
+        extras["prefill_M2048_r64"] = bench_prefill(torch, cl, wl, timer, dev)
+        extras["moe_48_layers"] = bench_moe(torch, cl, wl, timer, dev)
+
+    cpu = None if (args.no_cpu_baseline or only) else cpu_baseline(layer, T)
 
     out = {
         "metric": "achieved HBM GB/s + us/call, compensated W4A16 decode linear; prefill TFLOP/s",
@@ -185,21 +392,27 @@ def main():
                    "per_matrix_us": per_matrix_us, "per_matrix_gbs": per_matrix_gbs},
         "roofline": {"bound": "hbm", "kernel": "cl_linear_decode on gate 14336x4096 (prepare + backbone launches)",
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBS, 4), "us_per_launch": gate_us,
-                     "bytes_per_launch": gate_bytes, "traffic": None},
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "us_per_launch": round(gate_us, 3),
+                     "bytes_per_launch": gate_bytes, "traffic": gate_traffic()},
         "cpu_baseline": cpu,
     }
+    if extras is not None:
+        pf = extras["prefill_M2048_r64"]["14336x4096_fp16"]
+        extras["prefill_roofline"] = {"bound": "mfma", "kernel": "cl_linear_prefill 14336x4096 M=2048 r=64 fp16",
+                                      "achieved": pf["tflops"], "peak": MFMA_F16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                                      "frac": round(pf["tflops"] / MFMA_F16_PEAK_TFLOPS, 4)}
+        out["extras"] = extras
     print(json.dumps(out))
 
 
-def cpu_baseline(specs, layer, T):
-    """The fp64 oracle on the same layer (all seven matrices, every row):
-    unpack + dequantize + forward, median of 5 after one warm-up."""
+def cpu_baseline(layer, T):
+    """The fp64 oracle (unpack + dequantize + forward) on the whole layer
+    (all seven matrices, every row): median of 3 runs after one warm-up."""
     from oracle import linear, quant
     from paper_2605_05819_amd import workloads as wl
     prepared = []
     nbytes = 0
-    for m, spec in enumerate(specs):
+    for m, spec in enumerate(layer.linears):
         W = wl.weight((spec.d_out, spec.d_in), layer.index, 0, m)
         Q, s, z = quant.quantize_pack(W, spec.bits, spec.group_size)
         A, B = wl.standin_factors(spec.d_out, spec.d_in, spec.r_max, layer.index, 0, m)
@@ -213,7 +426,7 @@ def cpu_baseline(specs, layer, T):
 
     run()
     times = []
-    for _ in range(5):
+    for _ in range(3):
         t0 = time.perf_counter()
         run()
         times.append(time.perf_counter() - t0)
@@ -224,7 +437,8 @@ def cpu_baseline(specs, layer, T):
     except Exception:
         threads = os.cpu_count()
     return {"value": round(nbytes / sec / 1e9, 4), "unit": "GB/s", "cores": threads, "kind": "oracle",
-            "sample": "whole layer (7 matrices, all rows), T=%d, median of 5 runs of %.2f s" % (T, sec)}
+            "sample": "whole layer (7 matrices, all rows, %d bytes), T=%d, median of 3 runs of %.2f s"
+                      % (nbytes, T, sec)}
 
 
 if __name__ == "__main__":
