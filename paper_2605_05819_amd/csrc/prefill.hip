@@ -6,18 +6,25 @@
 // This is a dense contraction, so it runs on MFMA (v_mfma_f32_16x16x32_f16):
 //
 //  1. lowrank_t_kernel: T = X A[:r]^T in fp32, rounded to fp16, zero-padded
-//     to a multiple of 32 columns (a few percent of the work).
-//  2. prefill_kernel: 256 x 128 output tiles (tokens x weight rows), K in
-//     steps of 64, double-buffered LDS.  Each K step's packed codes are
-//     dequantized by the workgroup into an fp16 tile s * (q - z) (exact q - z
-//     via the 1024 + q trick, one rounding for the scale) and written to LDS
-//     in the pair order the unpack produces; the activation tile is written
-//     in the same permuted k order (bf16 converted to fp16 on the way), so
-//     the contraction is unchanged.  Four waves compute 128 x 64 each
-//     (8 x 4 MFMA tiles).  The rank-r correction is one or more extra K steps
-//     over [T | B] accumulated into the same tile before the store.
-//  Workgroups are numbered so that the N tiles of one 256-token block run on
-//  one XCD (workgroup i runs on XCD i mod 8) and share its L2 copy of X.
+//     to a multiple of 32 columns; it also writes X' (below).  Without a
+//     rank term, xprep_kernel writes X' alone.
+//     X' = X as fp16 (bf16 converted) with every 8 consecutive k reordered
+//     (k0,k4,k1,k5,k2,k6,k3,k7): the order in which the code unpack below
+//     produces weights, so the contraction is unchanged.
+//  2. prefill_kernel: 128 x 256 output tiles (tokens x weight rows), K in
+//     steps of 128 codes.  X' tiles go from global memory straight into LDS
+//     (global_load_lds, 16 bytes per lane, two 32 KB stages, chunks XOR-
+//     swizzled by row so the MFMA operand reads are bank-conflict free).  Each
+//     of the four waves owns 128 tokens x 64 weight rows (8 x 4 MFMA tiles):
+//     it loads its rows' packed codes for the next K step into registers (one
+//     16-byte load per lane and fragment: 32 codes of one quantization group,
+//     so one scale and zero per lane) and dequantizes them per MFMA step as
+//     s * (q - z) in fp16 ((q | 0x6400) - (1024 + z) is exact, one rounding
+//     for the scale).  No weight tile goes through LDS and no wave repeats
+//     another's dequantization.  The rank-r correction is extra MFMA steps
+//     over [T | B] (read from global memory) into the same accumulators.
+//  Workgroups are numbered so that the N tiles of one 128-token block run on
+//  one XCD (workgroup i runs on XCD i mod 8) and share its L2 copy of X'.
 
 #include "cl_device.h"
 #include "cl_internal.h"
@@ -26,8 +33,7 @@ namespace cl {
 
 namespace {
 
-constexpr int BM = 256, BN = 128, BK = 64;
-constexpr int LDK = BK + 8;          // LDS row pitch in halves (padding against bank conflicts)
+constexpr int BM = 128, BN = 256, BK = 128;
 
 // 8 activations -> fp16, in the pair order (x0,x4),(x1,x5),(x2,x6),(x3,x7)
 __device__ __forceinline__ u32x4 act8_permuted(u32x4 u, int act) {
@@ -102,20 +108,35 @@ struct PrefillArgs {
     const uint16_t* s;
     const uint16_t* z;
     const uint16_t* B;       // [N][r_max] fp16
-    const uint16_t* X;       // [M][K] fp16/bf16 bits
+    const uint16_t* Xp;      // [M][K] X' fp16, k-reordered (workspace)
     const uint16_t* T;       // [M][r_pad] fp16 (workspace)
     void* Y;                 // [M][N]
-    int M, N, K, G, rank, r_max, r_pad, act, out;
+    int M, N, K, G, rank, r_max, r_pad, out;
     int mblocks;             // ceil(M / BM)
 };
+
+// X' for 8 activations of a 16-byte chunk: fp16, order (k0,k4,k1,k5,...).
+__device__ __forceinline__ void store_xp(uint16_t* Xp, size_t idx, u32x4 raw, int act) {
+    *reinterpret_cast<u32x4*>(Xp + idx) = act8_permuted(raw, act);
+}
+
+// X' alone (no rank term): one thread per 16-byte chunk of X.
+__global__ __launch_bounds__(256) void xprep_kernel(const uint16_t* __restrict__ X, uint16_t* __restrict__ Xp,
+                                                    long long chunks, int act) {
+    const long long c = static_cast<long long>(blockIdx.x) * 256 + threadIdx.x;
+    if (c >= chunks) return;
+    store_xp(Xp, static_cast<size_t>(c) * 8, *reinterpret_cast<const u32x4*>(X + static_cast<size_t>(c) * 8), act);
+}
 
 // T = X A[:r]^T for 16 tokens x 64 factor columns per workgroup; the four
 // waves split K and every wave keeps 8 k-blocks of loads in flight; partial
 // tiles are summed through LDS in a fixed order.  MFMA A operand = X rows,
-// B operand = rows of A.  Output fp16, zero for columns >= rank.
+// B operand = rows of A.  Output fp16, zero for columns >= rank.  Workgroups
+// of the first column block also write X'.
 __global__ __launch_bounds__(256) void lowrank_t_kernel(const uint16_t* __restrict__ X,
                                                         const uint16_t* __restrict__ A, uint16_t* __restrict__ T,
-                                                        int M, int K, int rank, int r_pad, int act) {
+                                                        uint16_t* __restrict__ Xp, int M, int K, int rank,
+                                                        int r_pad, int act) {
     constexpr int U = 8;                               // k blocks of 32 per batch
     __shared__ f32x4 part[4][4][64];
     const int lane = threadIdx.x & 63;
@@ -152,6 +173,9 @@ __global__ __launch_bounds__(256) void lowrank_t_kernel(const uint16_t* __restri
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const bool live = k0 + 32 * u < kend;
+            // the first column block of workgroups also writes X' (every
+            // chunk of its 16 rows is loaded by exactly one lane here)
+            if (ntile == 0 && mval && live) store_xp(Xp, static_cast<size_t>(m) * K + k0 + 32 * u + kq, xa[u], act);
             u32x4 x8 = act8_natural(xa[u], act);
             if (!mval || !live) x8 = u32x4{0, 0, 0, 0};
 #pragma unroll
@@ -181,94 +205,70 @@ __global__ __launch_bounds__(256) void lowrank_t_kernel(const uint16_t* __restri
     }
 }
 
+// One K step's packed codes of a lane: 32 codes of one weight row (4-bit:
+// four words; 2-bit: two words), with their group's scale and zero.
 template <int BITS>
-__global__ __launch_bounds__(256) void prefill_kernel(PrefillArgs a) {
-    extern __shared__ uint32_t smem[];
-    // two stages of [BM][LDK] activations and [BN][LDK] weights (fp16)
-    constexpr int XS = BM * LDK / 2;   // words per activation stage
-    constexpr int WS = BN * LDK / 2;   // words per weight stage
-    // stage b: activations at smem + b (XS + WS), weights right after them
+struct WStep {
+    uint32_t w[BITS];        // 4-bit: 4 words, 2-bit: 2 words
+    uint16_t s, z;
+};
+
+template <int BITS>
+__global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
+    // two stages of X': [BM rows][16 chunks of 8 k], chunk c of row r stored
+    // at slot c ^ (r & 15)
+    __shared__ u32x4 xs[2][BM * 16];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int g = lane >> 4;               // lane group: k sub-block of an MFMA step
+    const int r = lane & 15;
     // XCD-aware order: consecutive workgroups take consecutive M blocks
     const int mb = blockIdx.x % a.mblocks;
     const int nb = blockIdx.x / a.mblocks;
-    const int m0 = mb * BM, n0 = nb * BN;
-    const int wm = (wave & 1) * 128;    // this wave's rows within the tile
-    const int wn = (wave >> 1) * 64;    // and columns
-
+    const int m0 = mb * BM, n0 = nb * BN + wave * 64;
+    const int nk = (a.K + BK - 1) / BK;
     const int groups = a.K / a.G;
     const int words_row = a.K * BITS / 32;
-    const int nsteps = a.K / BK;
 
-    // ---- global -> register staging for one K step
-    // activations: 256 rows x 64 k = 2048 x 16 B; thread t loads rows
-    // (t / 8) + 32 i, 16-byte column (t % 8)
-    u32x4 xr[8];
-    u32x4 wr;
-    uint16_t sr = 0, zr = 0;
-    const int xcol = (tid & 7) * 8;
-    auto load_stage = [&](int step) {
-        const int k0 = step * BK;
+    // X' tile of K step kb into stage st: wave w fills slots [512 w, 512 w + 512)
+    auto load_x = [&](int kb, int st) {
+        const int k0 = kb * BK;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            const int m = m0 + (tid >> 3) + 32 * i;
-            xr[i] = *reinterpret_cast<const u32x4*>(a.X + static_cast<size_t>(m < a.M ? m : 0) * a.K + k0 + xcol);
+        for (int j = 0; j < 8; ++j) {
+            const int blk = wave * 8 + j;                  // 64 slots = 4 rows
+            const int row = 4 * blk + (lane >> 4);
+            const int chunk = (lane & 15) ^ (row & 15);
+            const int m = m0 + row < a.M ? m0 + row : a.M - 1;
+            int k = k0 + 8 * chunk;
+            if (k >= a.K) k = k0;                          // half K step: weights there are zero
+            __builtin_amdgcn_global_load_lds(a.Xp + static_cast<size_t>(m) * a.K + k, &xs[st][blk * 64], 16, 0, 0);
         }
-        // weights: 4-bit: thread t -> row t/2, 32 codes (k0 + 32 (t%2)); 2-bit:
-        // thread t -> row t/2, 32 codes too (half of the row's 16-byte load)
-        const int row = n0 + (tid >> 1);
-        const int rowc = row < a.N ? row : 0;
-        if (BITS == 4) {
-            wr = *reinterpret_cast<const u32x4*>(a.q + static_cast<size_t>(rowc) * words_row + k0 / 8 + 4 * (tid & 1));
-        } else {
-            wr = *reinterpret_cast<const u32x4*>(a.q + static_cast<size_t>(rowc) * words_row + k0 / 16);
-        }
-        const int g = (k0 + 32 * (tid & 1)) / a.G;
-        sr = a.s[static_cast<size_t>(rowc) * groups + g];
-        zr = a.z[static_cast<size_t>(rowc) * groups + g];
     };
-    auto store_stage = [&](int buf, int step) {
-        uint32_t* xd = smem + buf * (XS + WS);
-        const int k0 = step * BK;
+    // this lane's codes of K step kb for its four weight rows
+    auto load_w = [&](int kb, WStep<BITS> (&ws)[4]) {
+        const int kc = kb * BK + 32 * g;                   // first code of this lane's 32
+        const bool kval = kc < a.K;
+        const int gi = kval ? kc / a.G : 0;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            const int r = (tid >> 3) + 32 * i;
-            const bool ok = m0 + r < a.M;
-            u32x4 v = act8_permuted(xr[i], a.act);
-            if (!ok) v = u32x4{0, 0, 0, 0};
-            *reinterpret_cast<u32x4*>(xd + r * (LDK / 2) + xcol / 2) = v;
-        }
-        const int r = tid >> 1;
-        const bool ok = n0 + r < a.N;
-        const f16 s = __builtin_bit_cast(f16, sr);
-        const f16 zf = static_cast<f16>(1024.0f) + __builtin_bit_cast(f16, zr);   // exact: z <= 15
-        const f16x2 s2 = {s, s}, zz = {zf, zf};
-        uint32_t* wd = smem + buf * (XS + WS) + XS + r * (LDK / 2) + 16 * (tid & 1);
-        if (BITS == 4) {
+        for (int j = 0; j < 4; ++j) {
+            const int n = n0 + 16 * j + r;
+            const int nc = n < a.N ? n : a.N - 1;
+            const uint32_t* src = a.q + static_cast<size_t>(nc) * words_row + (kval ? kc * BITS / 32 : 0);
+            if constexpr (BITS == 4) {
+                const u32x4 v = *reinterpret_cast<const u32x4*>(src);
 #pragma unroll
-            for (int w = 0; w < 4; ++w) {
-                u32x4 v = dequant_word4(wr[w], s2, zz);
-                if (!ok) v = u32x4{0, 0, 0, 0};
-                *reinterpret_cast<u32x4*>(wd + 4 * w) = v;
+                for (int e = 0; e < 4; ++e) { const uint32_t ve = v[e]; ws[j].w[e] = ve; }
+            } else {
+                const uint2 v = *reinterpret_cast<const uint2*>(src);
+                ws[j].w[0] = v.x;
+                ws[j].w[1] = v.y;
             }
-        } else {
-            // the row's 64 codes are 4 words of 16; this thread takes words
-            // 2 (t%2) and 2 (t%2) + 1, each as two halves of 8 codes
-#pragma unroll
-            for (int w = 0; w < 2; ++w) {
-                const uint32_t word = wr[2 * (tid & 1) + w];
-#pragma unroll
-                for (int h = 0; h < 2; ++h) {
-                    u32x4 v = dequant_half2(word, h, s2, zz);
-                    if (!ok) v = u32x4{0, 0, 0, 0};
-                    *reinterpret_cast<u32x4*>(wd + 8 * w + 4 * h) = v;
-                }
-            }
+            ws[j].s = a.s[static_cast<size_t>(nc) * groups + gi];
+            ws[j].z = a.z[static_cast<size_t>(nc) * groups + gi];
+            if (!kval || n >= a.N) ws[j].s = 0;            // zero weights (q - z finite, times 0)
         }
-        (void)k0;
     };
 
     f32x4 acc[8][4];
@@ -277,81 +277,89 @@ __global__ __launch_bounds__(256) void prefill_kernel(PrefillArgs a) {
 #pragma unroll
         for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    // MFMA over one LDS stage: A operand from activations, B from weights
-    auto mma_stage = [&](int buf) {
-        const uint32_t* xsb = smem + buf * (XS + WS);
-        const uint32_t* wsb = xsb + XS;
+    // four MFMA steps of 32 codes: lane group g's 8 codes of step t are codes
+    // 32 g + 8 t .. + 7 of the K step, X' chunk 4 g + t
+    auto compute = [&](int st, const WStep<BITS> (&ws)[4]) {
+        f16x2 s2[4], zz[4];
 #pragma unroll
-        for (int kk = 0; kk < BK; kk += 32) {
-            const int kq = kk + 8 * (lane >> 4);        // this lane's 8 k
+        for (int j = 0; j < 4; ++j) {
+            const f16 sv = __builtin_bit_cast(f16, ws[j].s);
+            const f16 zf = static_cast<f16>(1024.0f) + __builtin_bit_cast(f16, ws[j].z);   // exact: z < 16
+            s2[j] = f16x2{sv, sv};
+            zz[j] = f16x2{zf, zf};
+        }
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
             u32x4 bf[4];
 #pragma unroll
-            for (int j = 0; j < 4; ++j)
-                bf[j] = *reinterpret_cast<const u32x4*>(wsb + (wn + 16 * j + (lane & 15)) * (LDK / 2) + kq / 2);
+            for (int j = 0; j < 4; ++j) {
+                if constexpr (BITS == 4) bf[j] = dequant_word4(ws[j].w[t], s2[j], zz[j]);
+                else bf[j] = dequant_half2(ws[j].w[t >> 1], t & 1, s2[j], zz[j]);
+            }
+            const int chunk = 4 * g + t;
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
-                const u32x4 af = *reinterpret_cast<const u32x4*>(xsb + (wm + 16 * i + (lane & 15)) * (LDK / 2) + kq / 2);
+                const u32x4 af = xs[st][(16 * i + r) * 16 + (chunk ^ r)];
 #pragma unroll
                 for (int j = 0; j < 4; ++j) acc[i][j] = mfma(af, bf[j], acc[i][j]);
             }
         }
     };
 
-    // ---- main loop: double-buffered LDS, next step's global loads in flight
-    load_stage(0);
-    store_stage(0, 0);
+    // ---- main loop: double-buffered X' stages, next step's codes in registers
+    WStep<BITS> wa[4], wb[4];
+    load_x(0, 0);
+    load_w(0, wa);
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    for (int step = 0; step < nsteps; ++step) {
-        const int buf = step & 1;
-        if (step + 1 < nsteps) load_stage(step + 1);
-        mma_stage(buf);
-        if (step + 1 < nsteps) store_stage(buf ^ 1, step + 1);
+    for (int kb = 0; kb < nk; kb += 2) {
+        if (kb + 1 < nk) { load_x(kb + 1, 1); load_w(kb + 1, wb); }
+        compute(0, wa);
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+        if (kb + 1 >= nk) break;
+        if (kb + 2 < nk) { load_x(kb + 2, 0); load_w(kb + 2, wa); }
+        compute(1, wb);
+        __builtin_amdgcn_s_waitcnt(0);
         __syncthreads();
     }
 
-    // ---- rank-r correction: K steps over [T | B] (natural order), same tile
-    for (int k0 = 0; k0 < a.r_pad; k0 += BK) {
-        const int buf = 0;
-        uint32_t* xd = smem + buf * (XS + WS);
-        uint32_t* wd = xd + XS;
-        // T tile: 256 rows x 64 (zero past r_pad); B tile: 128 rows x 64
+    // ---- rank-r correction: MFMA steps of 32 over [T | B] (natural k order)
+    for (int kr = 0; kr < a.r_pad; kr += 32) {
+        const int k = kr + 8 * g;
+        u32x4 bf[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int n = n0 + 16 * j + r;
+            uint32_t v[4] = {0, 0, 0, 0};
+            if (n < a.N) {
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const uint16_t bv = k + e < a.rank ? a.B[static_cast<size_t>(n) * a.r_max + k + e] : 0;
+                    v[e / 2] |= static_cast<uint32_t>(bv) << (16 * (e & 1));
+                }
+            }
+            bf[j] = u32x4{v[0], v[1], v[2], v[3]};
+        }
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
-            const int r = (tid >> 3) + 32 * i;
-            const int m = m0 + r;
-            const int k = k0 + xcol;
-            u32x4 v = u32x4{0, 0, 0, 0};
-            if (m < a.M && k < a.r_pad) v = *reinterpret_cast<const u32x4*>(a.T + static_cast<size_t>(m) * a.r_pad + k);
-            *reinterpret_cast<u32x4*>(xd + r * (LDK / 2) + xcol / 2) = v;
-        }
+            const int m = m0 + 16 * i + r;
+            const u32x4 af = *reinterpret_cast<const u32x4*>(a.T + static_cast<size_t>(m < a.M ? m : a.M - 1) * a.r_pad + k);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int r = (tid >> 3) + 32 * i;          // 128 rows, 8 x 8 halves each
-            const int n = n0 + r;
-            uint32_t v[4] = {0, 0, 0, 0};
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const int k = k0 + xcol + e;
-                const uint16_t bv = (n < a.N && k < a.rank) ? a.B[static_cast<size_t>(n) * a.r_max + k] : 0;
-                v[e / 2] |= static_cast<uint32_t>(bv) << (16 * (e & 1));
-            }
-            *reinterpret_cast<u32x4*>(wd + r * (LDK / 2) + xcol / 2) = u32x4{v[0], v[1], v[2], v[3]};
+            for (int j = 0; j < 4; ++j) acc[i][j] = mfma(af, bf[j], acc[i][j]);
         }
-        __syncthreads();
-        mma_stage(buf);
-        __syncthreads();
     }
 
-    // ---- store: acc[i][j][e] = Y[m0 + wm + 16 i + 4 (lane/16) + e][n0 + wn + 16 j + lane%16]
+    // ---- store: acc[i][j][e] = Y[m0 + 16 i + 4 g + e][n0 + 16 j + r]
 #pragma unroll
     for (int i = 0; i < 8; ++i)
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            const int n = n0 + wn + 16 * j + (lane & 15);
+            const int n = n0 + 16 * j + r;
             if (n >= a.N) continue;
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                const int m = m0 + wm + 16 * i + 4 * (lane >> 4) + e;
+                const int m = m0 + 16 * i + 4 * g + e;
                 if (m < a.M) store_out(a.Y, static_cast<size_t>(m) * a.N + n, acc[i][j][e], a.out);
             }
         }
@@ -361,50 +369,40 @@ size_t up256(size_t n) { return (n + 255) / 256 * 256; }
 
 }  // namespace
 
-size_t prefill_workspace_bytes(const QW&, const LR& c, int M) {
+size_t prefill_workspace_bytes(const QW& w, const LR& c, int M) {
     const int r_pad = (c.rank + 31) / 32 * 32;
-    return up256(static_cast<size_t>(M) * r_pad * 2);
+    return up256(static_cast<size_t>(M) * w.d_in * 2) + up256(static_cast<size_t>(M) * r_pad * 2);
 }
-
-size_t prefill_lds_bytes() { return static_cast<size_t>(2) * (BM + BN) * LDK * 2; }
 
 hipError_t launch_linear_prefill(const QW& w, const LR& c, const void* X, int M, int act, void* Y, int out,
                                  void* ws, hipStream_t st) {
+    uint16_t* Xp = static_cast<uint16_t*>(ws);
+    uint16_t* T = reinterpret_cast<uint16_t*>(static_cast<char*>(ws) + up256(static_cast<size_t>(M) * w.d_in * 2));
     PrefillArgs a;
     a.q = w.q; a.s = w.s; a.z = w.z; a.B = c.B;
-    a.X = static_cast<const uint16_t*>(X);
-    a.T = static_cast<const uint16_t*>(ws);
+    a.Xp = Xp;
+    a.T = T;
     a.Y = Y;
     a.M = M; a.N = w.d_out; a.K = w.d_in; a.G = w.G;
     a.rank = c.rank; a.r_max = c.r_max; a.r_pad = (c.rank + 31) / 32 * 32;
-    a.act = act; a.out = out;
+    a.out = out;
     a.mblocks = (M + BM - 1) / BM;
+    const uint16_t* Xa = static_cast<const uint16_t*>(X);
     if (c.rank > 0) {
         const dim3 grid((M + 15) / 16, (a.r_pad + 63) / 64);
-        hipLaunchKernelGGL(lowrank_t_kernel, grid, dim3(256), 0, st, a.X, c.A, static_cast<uint16_t*>(ws), M, w.d_in,
-                           c.rank, a.r_pad, act);
-        hipError_t e = hipGetLastError();
-        if (e != hipSuccess) return e;
-    }
-    const size_t lds = prefill_lds_bytes();
-    const unsigned blocks = static_cast<unsigned>(a.mblocks * ((w.d_out + BN - 1) / BN));
-    if (w.bits == 4) {
-        static bool attr4 = false;
-        if (!attr4) {
-            (void)hipFuncSetAttribute(reinterpret_cast<const void*>(prefill_kernel<4>),
-                                hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
-            attr4 = true;
-        }
-        hipLaunchKernelGGL(prefill_kernel<4>, dim3(blocks), dim3(256), lds, st, a);
+        hipLaunchKernelGGL(lowrank_t_kernel, grid, dim3(256), 0, st, Xa, c.A, T, Xp, M, w.d_in, c.rank, a.r_pad, act);
     } else {
-        static bool attr2 = false;
-        if (!attr2) {
-            (void)hipFuncSetAttribute(reinterpret_cast<const void*>(prefill_kernel<2>),
-                                hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
-            attr2 = true;
-        }
-        hipLaunchKernelGGL(prefill_kernel<2>, dim3(blocks), dim3(256), lds, st, a);
+        const long long chunks = static_cast<long long>(M) * w.d_in / 8;
+        hipLaunchKernelGGL(xprep_kernel, dim3(static_cast<unsigned>((chunks + 255) / 256)), dim3(256), 0, st, Xa, Xp,
+                           chunks, act);
     }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const unsigned blocks = static_cast<unsigned>(a.mblocks * ((w.d_out + BN - 1) / BN));
+    if (w.bits == 4)
+        hipLaunchKernelGGL(prefill_kernel<4>, dim3(blocks), dim3(256), 0, st, a);
+    else
+        hipLaunchKernelGGL(prefill_kernel<2>, dim3(blocks), dim3(256), 0, st, a);
     return hipGetLastError();
 }
 
