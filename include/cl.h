@@ -211,20 +211,24 @@ size_t cl_linear_window_workspace(int32_t n, const cl_qweight* w, const cl_lowra
 /*
  * cl_linear_prefill -- compensated linear for many tokens (Section 4.1):
  *     Y = X deq(Q)^T + (X A[:rank]^T) B[:, :rank]^T.
- * A dense contraction on MFMA: a small kernel forms T = X A^T (fp16, in the
- * workspace), then one GEMM dequantizes weight tiles into LDS (fp16
- * s * (q - z), one rounding per weight), multiplies on v_mfma_f32_16x16x32_f16
- * with float32 accumulation, folds the rank-r term in as extra K steps over
- * [T | B] into the same output tile and rounds once to out_dtype.  bf16
- * activations are converted to fp16 on the way into LDS (exact for
- * 2^-17 <= |x| <= 65504, as in cl_linear_decode).
+ * A dense contraction on MFMA: a first kernel writes X' (X as fp16 in the
+ * k order the code unpack produces, into the workspace) and, with a rank
+ * term, T = X A^T (fp16, in the workspace); then one GEMM streams X' tiles
+ * into LDS, dequantizes the weight codes in registers (fp16 s * (q - z), one
+ * rounding per weight), multiplies on v_mfma_f32_16x16x32_f16 with float32
+ * accumulation, folds the rank-r term in as extra K steps over [T | B] into
+ * the same output tile and rounds once to out_dtype.  bf16 activations are
+ * converted to fp16 (exact for 2^-17 <= |x| <= 65504, as in
+ * cl_linear_decode).
  *
  *  X          device [M][d_in] of act_dtype, 16-byte aligned
- *  M          >= 1 tokens
+ *  M          >= 1 tokens, M * d_in < 2^31
  *  Y          device [M][d_out] of out_dtype
- *  ws         device workspace of cl_prefill_workspace(w, c, M) bytes (0 for
- *             rank 0, then ws may be NULL), 256-byte aligned
- * Errors: as cl_linear_decode; CL_EUNSUPPORTED if d_in is not a multiple of 64.
+ *  ws         device workspace of cl_prefill_workspace(w, c, M) bytes
+ *             (2 M d_in for X' plus 2 M rank rounded up to 32 for T),
+ *             256-byte aligned
+ * Errors: as cl_linear_decode; CL_EUNSUPPORTED if d_in is not a multiple of
+ * 64 or M * d_in >= 2^31.
  */
 cl_status cl_linear_prefill(const cl_qweight* w, const cl_lowrank* c, const void* X, int32_t M,
                             int32_t act_dtype, void* Y, int32_t out_dtype, void* ws, size_t ws_bytes,

@@ -227,6 +227,8 @@ cl_status cl_linear_prefill(const cl_qweight* w, const cl_lowrank* c, const void
     if (st) return st;
     if (qw.d_in % 64) return fail(CL_EUNSUPPORTED, "%s: d_in must be a multiple of 64 (got %d)", who, qw.d_in);
     if (M < 1) return fail(CL_EINVAL, "%s: M must be >= 1 (got %d)", who, M);
+    if (static_cast<long long>(M) * qw.d_in > (1ll << 31) - 1)
+        return fail(CL_EUNSUPPORTED, "%s: M * d_in must be below 2^31 (split the tokens)", who);
     if (act_dtype != CL_FP16 && act_dtype != CL_BF16)
         return fail(CL_EINVAL, "%s: act_dtype must be CL_FP16 or CL_BF16", who);
     if (out_dtype != CL_FP16 && out_dtype != CL_BF16 && out_dtype != CL_FP32)

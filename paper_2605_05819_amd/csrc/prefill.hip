@@ -98,6 +98,46 @@ __device__ __forceinline__ u32x4 dequant_half2(uint32_t w, int h, f16x2 s2, f16x
     return r;
 }
 
+// (x & m) | c in one instruction; m comes from a scalar register, c from a
+// vector register (one scalar operand per instruction on this target).
+__device__ __forceinline__ uint32_t and_or(uint32_t x, uint32_t m, uint32_t c) {
+    uint32_t r;
+    asm("v_and_or_b32 %0, %1, %2, %3" : "=v"(r) : "v"(x), "s"(m), "v"(c));
+    return r;
+}
+
+// Per-fragment constants of one quantization group for dequant_word4x, two
+// halves per register: (s, s/16) and (1024 + z, 1024 + 16 z).
+struct Dq {
+    f16x2 s, z;
+};
+
+__device__ __forceinline__ Dq make_dq(uint32_t sbits, uint32_t zbits) {
+    const f16 s = __builtin_bit_cast(f16, static_cast<uint16_t>(sbits));
+    const f16 z = __builtin_bit_cast(f16, static_cast<uint16_t>(zbits));
+    const f16 s16 = s * static_cast<f16>(0.0625f);                     // exact unless subnormal
+    const f16 z1 = static_cast<f16>(1024.0f) + z;                      // exact: z < 16
+    const f16 z16 = static_cast<f16>(1024.0f) + z * static_cast<f16>(16.0f);
+    return Dq{f16x2{s, s16}, f16x2{z1, z16}};
+}
+
+// One 32-bit word of 4-bit codes -> 8 fp16 values s (q - z), pair order
+// (q0,q4),(q1,q5),(q2,q6),(q3,q7), with one shift and four masks: a code
+// left in bits 4..7 of a half reads as 1024 + 16 q, so its pair subtracts
+// 1024 + 16 z (exact) and scales by s/16.
+__device__ __forceinline__ u32x4 dequant_word4x(uint32_t w, const Dq& d, uint32_t mlo, uint32_t mhi,
+                                               uint32_t bias) {
+    const uint32_t w8 = w >> 8;
+    const f16x2 s1 = {d.s.x, d.s.x}, s16 = {d.s.y, d.s.y};
+    const f16x2 z1 = {d.z.x, d.z.x}, z16 = {d.z.y, d.z.y};
+    u32x4 r;
+    r[0] = __builtin_bit_cast(uint32_t, (__builtin_bit_cast(f16x2, and_or(w, mlo, bias)) - z1) * s1);
+    r[1] = __builtin_bit_cast(uint32_t, (__builtin_bit_cast(f16x2, and_or(w, mhi, bias)) - z16) * s16);
+    r[2] = __builtin_bit_cast(uint32_t, (__builtin_bit_cast(f16x2, and_or(w8, mlo, bias)) - z1) * s1);
+    r[3] = __builtin_bit_cast(uint32_t, (__builtin_bit_cast(f16x2, and_or(w8, mhi, bias)) - z16) * s16);
+    return r;
+}
+
 __device__ __forceinline__ f32x4 mfma(const u32x4& a, const u32x4& b, const f32x4& c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), c,
                                                   0, 0, 0);
@@ -210,7 +250,7 @@ __global__ __launch_bounds__(256) void lowrank_t_kernel(const uint16_t* __restri
 template <int BITS>
 struct WStep {
     uint32_t w[BITS];        // 4-bit: 4 words, 2-bit: 2 words
-    uint16_t s, z;
+    uint32_t s, z;           // fp16 bits, zero-extended by the load
 };
 
 template <int BITS>
@@ -243,7 +283,9 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
             const int m = m0 + row < a.M ? m0 + row : a.M - 1;
             int k = k0 + 8 * chunk;
             if (k >= a.K) k = k0;                          // half K step: weights there are zero
-            __builtin_amdgcn_global_load_lds(a.Xp + static_cast<size_t>(m) * a.K + k, &xs[st][blk * 64], 16, 0, 0);
+            // 32-bit element offsets (the entry point bounds M K): scalar base + vector offset
+            const unsigned off = static_cast<unsigned>(m) * static_cast<unsigned>(a.K) + static_cast<unsigned>(k);
+            __builtin_amdgcn_global_load_lds(a.Xp + off, &xs[st][blk * 64], 16, 0, 0);
         }
     };
     // this lane's codes of K step kb for its four weight rows
@@ -255,7 +297,8 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
         for (int j = 0; j < 4; ++j) {
             const int n = n0 + 16 * j + r;
             const int nc = n < a.N ? n : a.N - 1;
-            const uint32_t* src = a.q + static_cast<size_t>(nc) * words_row + (kval ? kc * BITS / 32 : 0);
+            const uint32_t* src = a.q + (static_cast<unsigned>(nc) * static_cast<unsigned>(words_row) +
+                                         static_cast<unsigned>(kval ? kc * BITS / 32 : 0));
             if constexpr (BITS == 4) {
                 const u32x4 v = *reinterpret_cast<const u32x4*>(src);
 #pragma unroll
@@ -265,9 +308,11 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
                 ws[j].w[0] = v.x;
                 ws[j].w[1] = v.y;
             }
-            ws[j].s = a.s[static_cast<size_t>(nc) * groups + gi];
-            ws[j].z = a.z[static_cast<size_t>(nc) * groups + gi];
-            if (!kval || n >= a.N) ws[j].s = 0;            // zero weights (q - z finite, times 0)
+            // raw loads only: nothing here consumes a loaded value, so the
+            // loads stay in flight through the current step's MFMAs
+            const unsigned sgi = static_cast<unsigned>(nc) * static_cast<unsigned>(groups) + static_cast<unsigned>(gi);
+            ws[j].s = a.s[sgi];
+            ws[j].z = a.z[sgi];
         }
     };
 
@@ -279,21 +324,33 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
 
     // four MFMA steps of 32 codes: lane group g's 8 codes of step t are codes
     // 32 g + 8 t .. + 7 of the K step, X' chunk 4 g + t
-    auto compute = [&](int st, const WStep<BITS> (&ws)[4]) {
+    // loop-invariant operands of the unpack: masks in scalar registers
+    const uint32_t mlo = __builtin_amdgcn_readfirstlane(0x000F000Fu);
+    const uint32_t mhi = __builtin_amdgcn_readfirstlane(0x00F000F0u);
+    const uint32_t bias = 0x64006400u;
+    auto compute = [&](int kb, int st, const WStep<BITS> (&ws)[4]) {
+        Dq dq[4];
         f16x2 s2[4], zz[4];
+        const bool kval = kb * BK + 32 * g < a.K;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            const f16 sv = __builtin_bit_cast(f16, ws[j].s);
-            const f16 zf = static_cast<f16>(1024.0f) + __builtin_bit_cast(f16, ws[j].z);   // exact: z < 16
-            s2[j] = f16x2{sv, sv};
-            zz[j] = f16x2{zf, zf};
+            // past K or N the scale is 0: q - z is finite, so the weight is 0
+            const uint32_t sb = (kval && n0 + 16 * j + r < a.N) ? ws[j].s : 0u;
+            if constexpr (BITS == 4) {
+                dq[j] = make_dq(sb, ws[j].z);
+            } else {
+                const f16 sv = __builtin_bit_cast(f16, static_cast<uint16_t>(sb));
+                const f16 zf = static_cast<f16>(1024.0f) + __builtin_bit_cast(f16, static_cast<uint16_t>(ws[j].z));
+                s2[j] = f16x2{sv, sv};
+                zz[j] = f16x2{zf, zf};
+            }
         }
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
             u32x4 bf[4];
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                if constexpr (BITS == 4) bf[j] = dequant_word4(ws[j].w[t], s2[j], zz[j]);
+                if constexpr (BITS == 4) bf[j] = dequant_word4x(ws[j].w[t], dq[j], mlo, mhi, bias);
                 else bf[j] = dequant_half2(ws[j].w[t >> 1], t & 1, s2[j], zz[j]);
             }
             const int chunk = 4 * g + t;
@@ -314,12 +371,12 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
     __syncthreads();
     for (int kb = 0; kb < nk; kb += 2) {
         if (kb + 1 < nk) { load_x(kb + 1, 1); load_w(kb + 1, wb); }
-        compute(0, wa);
+        compute(kb, 0, wa);
         __builtin_amdgcn_s_waitcnt(0);
         __syncthreads();
         if (kb + 1 >= nk) break;
         if (kb + 2 < nk) { load_x(kb + 2, 0); load_w(kb + 2, wa); }
-        compute(1, wb);
+        compute(kb + 1, 1, wb);
         __builtin_amdgcn_s_waitcnt(0);
         __syncthreads();
     }
