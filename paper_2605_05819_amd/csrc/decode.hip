@@ -41,12 +41,15 @@
 #include "cl_device.h"
 #include "cl_internal.h"
 #include "gemv_common.h"
+#include "mfma_common.h"
 
 namespace cl {
 
 namespace {
 
 constexpr int kMaxWin = 8;   // linears per window
+constexpr int kMaxKp = 4;    // K parts of the many-token A x partials
+constexpr int kMfmaMinTokens = 8;   // 4-bit windows with this many tokens use the MFMA backbone
 
 // One linear of a window, as the backbone kernel sees it.
 struct Lin {
@@ -55,9 +58,10 @@ struct Lin {
     const uint16_t* z;
     const uint16_t* B;
     void* y;                 // [T][d_out]
-    const float* t;          // [T][rank] (workspace)
+    const float* t;          // [T][rank] (workspace); MFMA path: [kp][T][rpad] partials
     int d_out, rank, r_max;
     int batch_end;           // exclusive prefix sum of the linears' batches
+    int rpad;                // MFMA path: rank rounded up to 32
 };
 
 struct DecodeArgs {
@@ -68,6 +72,23 @@ struct DecodeArgs {
     int d_in, G, T, tok0, out;
     int ks;                  // K slices (waves per row group)
     int cps;                 // chunks per slice
+    int kp;                  // MFMA path: K parts of the A x partials
+};
+
+// Preparation for the MFMA path: A x on MFMA as K-part partials.
+struct PrepMArgs {
+    const uint16_t* A[kMaxWin];
+    float* tp[kMaxWin];      // [kp][T][rpad]
+    int rank[kMaxWin];
+    int rpad[kMaxWin];
+    int tile_end[kMaxWin];   // exclusive prefix sum of (rpad / 16) * kp
+    int n;
+    const uint16_t* x;       // [T][d_in] fp16/bf16 bits
+    f16x2* xp;
+    float* sx;
+    int d_in, T, act;
+    int kp;                  // K parts
+    int spw;                 // 32-code steps per wave and K part
 };
 
 struct PrepArgs {
@@ -403,6 +424,256 @@ __global__ __launch_bounds__(512) void decode_kernel(DecodeArgs a) {
     }
 }
 
+// 8 activations as fp16 (bf16 converted), natural order.
+__device__ __forceinline__ u32x4 act8_f16(u32x4 u, int act) {
+    if (act == DT_FP16) return u;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        f16x2 h;
+        h.x = act_to_f16(static_cast<uint16_t>(u[k] & 0xffff), act);
+        h.y = act_to_f16(static_cast<uint16_t>(u[k] >> 16), act);
+        const uint32_t hb = __builtin_bit_cast(uint32_t, h);
+        u[k] = hb;
+    }
+    return u;
+}
+
+// Preparation for the MFMA backbone.  Workgroups [0, tiles): (linear, 16 rows
+// of A, K part kp): t partial[kp][tok][i] = sum over the part's k of
+// A[i][k] x[tok][k] for up to 16 tokens on v_mfma_f32_16x16x32_f16 (A rows as
+// the A operand, tokens as the B operand; four waves split the part, eight
+// 32-code steps of loads in flight per wave; the waves' tiles are summed
+// through LDS in a fixed order).  Rows past the rank are written as zero.
+// The remaining workgroups prepare the activations as decode_prep_kernel.
+__global__ __launch_bounds__(256) void decode_prep_mfma_kernel(PrepMArgs a) {
+    constexpr int CPW = 8, HPW = 4, PPC = 16;        // 4-bit codes
+    __shared__ f32x4 red[4][64];
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int g = lane >> 4, r = lane & 15;
+    const int tid = threadIdx.x;
+    const int d_in = a.d_in, T = a.T;
+    const int ntile = a.n > 0 ? a.tile_end[a.n - 1] : 0;
+    const int blk = blockIdx.x;
+    if (blk < ntile) {
+        int li = 0;
+        while (blk >= a.tile_end[li]) ++li;
+        const int local = blk - (li ? a.tile_end[li - 1] : 0);
+        const int tile = local / a.kp, kp = local - tile * a.kp;
+        const int rank = a.rank[li];
+        const int arow = tile * 16 + r;
+        const bool av = arow < rank;
+        const uint16_t* ar = a.A[li] + static_cast<size_t>(av ? arow : 0) * d_in;
+        const bool tv = r < T;
+        const uint16_t* xr = a.x + static_cast<size_t>(tv ? r : 0) * d_in;
+        const int nsteps = d_in / 32;
+        const int s0 = (kp * 4 + wave) * a.spw;
+        const int s1 = min(s0 + a.spw, nsteps);
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+        for (int sb = s0; sb < s1; sb += 8) {
+            u32x4 am[8], xm[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const int k = (sb + u < s1 ? sb + u : s0) * 32 + 8 * g;
+                am[u] = *reinterpret_cast<const u32x4*>(ar + k);
+                xm[u] = *reinterpret_cast<const u32x4*>(xr + k);
+            }
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const bool live = sb + u < s1;
+                const u32x4 zero = {0, 0, 0, 0};
+                const u32x4 a8 = (av && live) ? am[u] : zero;
+                const u32x4 x8 = (tv && live) ? act8_f16(xm[u], a.act) : zero;
+                acc = mfma(a8, x8, acc);
+            }
+        }
+        red[wave][lane] = acc;
+        __syncthreads();
+        if (wave != 0 || !tv) return;
+        acc = red[0][lane] + red[1][lane] + red[2][lane] + red[3][lane];
+        // acc[e] = partial t[tok r][row tile*16 + 4 g + e]
+        float* dst = a.tp[li] + (static_cast<size_t>(kp) * T + r) * a.rpad[li] + tile * 16 + 4 * g;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) dst[e] = tile * 16 + 4 * g + e < rank ? acc[e] : 0.f;
+        return;
+    }
+    const int chunks = d_in / CPW / 4;
+    const long long item = static_cast<long long>(blk - ntile) * 256 + tid;
+    if (item >= static_cast<long long>(T) * chunks) return;
+    const int tok = static_cast<int>(item / chunks);
+    const int c = static_cast<int>(item % chunks);
+    f16x2 v[PPC];
+    load_chunk_x<4>(a.x + static_cast<size_t>(tok) * d_in, c, a.act, v);
+    const f16x2 one = {static_cast<f16>(1.0f), static_cast<f16>(1.0f)};
+    float sum = 0.f;
+    f16x2* dst = a.xp + static_cast<size_t>(tok) * (d_in / 2) + static_cast<size_t>(c) * PPC;
+#pragma unroll
+    for (int p = 0; p < PPC; ++p) {
+        sum = dot2(v[p], one, sum);
+        dst[p] = v[p];
+    }
+    a.sx[static_cast<size_t>(tok) * chunks + c] = sum;
+    (void)HPW;
+}
+
+// Many-token backbone (4-bit codes, T >= 8): the contraction has enough
+// columns to use MFMA.  One workgroup per 16-row tile of one linear; its four
+// waves split the row's 128-code blocks (wave w takes blocks w, w + 4, ...),
+// four blocks per wave in flight.  Per block a lane loads 16 bytes of codes of
+// row r = lane % 16 (32 codes of one quantization group), dequantizes them in
+// registers to fp16 s (q - z) (one rounding) and feeds four
+// v_mfma_f32_16x16x32_f16 with up to 16 tokens
+// of the prepared activations (the prep kernel's pair order is the unpack's
+// order).  The rank-r term is extra MFMA steps over [B | t] spread over the
+// waves (t from the K-part partials of decode_prep_mfma_kernel, summed in a
+// fixed order and rounded to fp16); the waves' tiles are summed through LDS
+// in a fixed order; one rounding to the output dtype.
+__global__ __launch_bounds__(256) void decode_mfma_kernel(DecodeArgs a) {
+    __shared__ f32x4 red[4][64];
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int g = lane >> 4, r = lane & 15;
+    // workgroup -> (linear, 16-row tile); batch_end counts tiles here
+    int li = 0;
+    while (static_cast<int>(blockIdx.x) >= a.lin[li].batch_end) ++li;
+    const Lin& L = a.lin[li];
+    const int row0 = (blockIdx.x - (li ? a.lin[li - 1].batch_end : 0)) * 16;
+    const int row = row0 + r < L.d_out ? row0 + r : L.d_out - 1;
+    const bool rowv = row0 + r < L.d_out;
+    const int tok = a.tok0 + r;                    // this lane's token column of the B operand
+    const bool tokv = tok < a.T;
+    const int K = a.d_in;
+    const int nkb = (K + 127) / 128;
+    const int words_row = K / 8;
+    const int groups = K / a.G;
+    const uint32_t mlo = __builtin_amdgcn_readfirstlane(0x000F000Fu);
+    const uint32_t mhi = __builtin_amdgcn_readfirstlane(0x00F000F0u);
+    const uint32_t bias = 0x64006400u;
+    const u32x4* xrow = reinterpret_cast<const u32x4*>(a.xp + static_cast<size_t>(tokv ? tok : 0) * (K / 2));
+
+    struct Blk {
+        u32x4 w;
+        uint32_t s, z;
+        u32x4 x[4];
+    };
+    // rank-r term, 32 factor columns per step, wave w taking steps w, w + 4:
+    // A operand B[row][k .. k + 8), B operand t[tok][k .. k + 8) = the sum of
+    // the K-part partials in order, rounded to fp16.  The first step's
+    // operands are loaded before the K loop, so their latency is hidden.
+    const bool bvec = (L.r_max & 7) == 0 && (reinterpret_cast<uintptr_t>(L.B) & 15) == 0;
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    struct RankOp {
+        uint32_t bw[4];
+        f32x4 tp[kMaxKp][2];
+    };
+    auto rank_load = [&](int kr, RankOp& o) {
+        const int k = kr + 8 * g;
+        if (kr >= L.rank) return;
+        const uint16_t* brow = L.B + static_cast<size_t>(row) * L.r_max;
+        if (bvec && k + 8 <= L.r_max) {
+            const u32x4 v = *reinterpret_cast<const u32x4*>(brow + k);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) { const uint32_t ve = v[e]; o.bw[e] = ve; }
+        } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const uint32_t lo = k + 2 * e < L.r_max ? brow[k + 2 * e] : 0u;
+                const uint32_t hi = k + 2 * e + 1 < L.r_max ? brow[k + 2 * e + 1] : 0u;
+                o.bw[e] = lo | (hi << 16);
+            }
+        }
+        const int tk = tokv ? tok : 0;
+#pragma unroll
+        for (int p = 0; p < kMaxKp; ++p) {
+            const int pp = p < a.kp ? p : 0;
+            const f32x4* src = reinterpret_cast<const f32x4*>(L.t + (static_cast<size_t>(pp) * a.T + tk) * L.rpad + k);
+            o.tp[p][0] = src[0];
+            o.tp[p][1] = src[1];
+        }
+    };
+    auto rank_mma = [&](int kr, const RankOp& o) {
+        if (kr >= L.rank) return;
+        const int k = kr + 8 * g;
+        float tsum[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int p = 0; p < kMaxKp; ++p) {
+            if (p >= a.kp) break;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) { tsum[e] += o.tp[p][0][e]; tsum[4 + e] += o.tp[p][1][e]; }
+        }
+        uint32_t aw[4], tw[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            // entries past the rank (or past the matrix) and absent tokens are zero
+            const uint32_t lo = (rowv && k + 2 * e < L.rank) ? (o.bw[e] & 0xffffu) : 0u;
+            const uint32_t hi = (rowv && k + 2 * e + 1 < L.rank) ? (o.bw[e] >> 16) : 0u;
+            aw[e] = lo | (hi << 16);
+            tw[e] = tokv ? (static_cast<uint32_t>(f32_to_f16_bits(tsum[2 * e])) |
+                            (static_cast<uint32_t>(f32_to_f16_bits(tsum[2 * e + 1])) << 16))
+                         : 0u;
+        }
+        acc = mfma(u32x4{aw[0], aw[1], aw[2], aw[3]}, u32x4{tw[0], tw[1], tw[2], tw[3]}, acc);
+    };
+    RankOp rb;
+    rank_load(32 * wave, rb);
+
+    // loads are unconditional (valid addresses always) and nothing consumes a
+    // loaded value before compute: the compiler's wait counts then let every
+    // prefetched block stay in flight
+    auto load = [&](int kb, Blk& b) {
+        const int kc = kb * 128 + 32 * g;          // first of this lane's 32 codes
+        const int wi = kc < K ? kc / 8 : 0;
+        b.w = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(L.q + static_cast<size_t>(row) * words_row + wi));
+        const size_t gi = static_cast<size_t>(row) * groups + (kc < K ? kc / a.G : 0);
+        b.s = L.s[gi];
+        b.z = L.z[gi];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) b.x[t] = xrow[wi + t];
+    };
+    auto compute = [&](int kb, const Blk& b) {
+        // past K, past the matrix or a padding block: scale 0, the weight is 0
+        const bool on = rowv && kb < nkb && kb * 128 + 32 * g < K;
+        const Dq dq = make_dq(on ? b.s : 0u, b.z);
+        const u32x4 zero = {0, 0, 0, 0};
+#pragma unroll
+        for (int t = 0; t < 4; ++t) acc = mfma(dequant_word4x(b.w[t], dq, mlo, mhi, bias), tokv ? b.x[t] : zero, acc);
+    };
+    // blocks of this wave: kb = wave + 4 i, four in flight.  Rounds of four:
+    // block j of a round is computed, then its registers take block j + 4
+    // (past the last block they reload the current one, already cached).
+    const int rounds = (nkb + 15) / 16;
+    Blk b[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) load(wave + 4 * j < nkb ? wave + 4 * j : 0, b[j]);
+    for (int rd = 0; rd < rounds; ++rd) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int kb = wave + 16 * rd + 4 * j;
+            compute(kb, b[j]);
+            const int kn = kb + 16;
+            load(kn < nkb ? kn : (kb < nkb ? kb : 0), b[j]);
+        }
+    }
+    // rank-r term (operands loaded before the K loop, see rank_load)
+    rank_mma(32 * wave, rb);
+    for (int kr = 32 * wave + 128; kr < L.rank; kr += 128) {
+        RankOp ro;
+        rank_load(kr, ro);
+        rank_mma(kr, ro);
+    }
+    red[wave][lane] = acc;
+    __syncthreads();
+    if (wave != 0) return;
+    acc = red[0][lane] + red[1][lane] + red[2][lane] + red[3][lane];
+    // acc[e] = y[tok0 + r][row0 + 4 g + e]
+    if (!tokv) return;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const int rr = row0 + 4 * g + e;
+        if (rr < L.d_out) store_out(L.y, static_cast<size_t>(tok) * L.d_out + rr, acc[e], a.out);
+    }
+}
+
 struct Plan {
     int cpl, R, ks, cps, nt, nb, threads;
 };
@@ -491,9 +762,34 @@ size_t up256(size_t n) { return (n + 255) / 256 * 256; }
 
 }  // namespace
 
+namespace {
+
+bool use_mfma(int bits, int T) { return bits == 4 && T >= kMfmaMinTokens; }
+
+// K parts of the MFMA preparation (at most 4, about 1024 codes each) and the
+// 32-code steps each of a part's four waves takes
+struct MfmaPlan {
+    int kp, spw;
+};
+
+MfmaPlan mfma_plan(int d_in) {
+    const int nsteps = d_in / 32;
+    int kp = (d_in + 1023) / 1024;
+    if (kp > kMaxKp) kp = kMaxKp;
+    return MfmaPlan{kp, (nsteps + 4 * kp - 1) / (4 * kp)};
+}
+
+int pad32(int r) { return (r + 31) / 32 * 32; }
+
+}  // namespace
+
 size_t decode_workspace_bytes(int n, const QW* w, const LR* c, int T) {
     size_t total = 0;
-    for (int i = 0; i < n; ++i) total += up256(static_cast<size_t>(c[i].rank) * T * sizeof(float));
+    const bool mf = use_mfma(w[0].bits, T);
+    const int kp = mf ? mfma_plan(w[0].d_in).kp : 0;
+    for (int i = 0; i < n; ++i)
+        total += mf ? up256(static_cast<size_t>(kp) * T * pad32(c[i].rank) * sizeof(float))
+                    : up256(static_cast<size_t>(c[i].rank) * T * sizeof(float));
     const size_t chunks = static_cast<size_t>(w[0].d_in) / (32 / w[0].bits) / 4;
     total += up256(static_cast<size_t>(T) * w[0].d_in * 2);
     total += up256(static_cast<size_t>(T) * chunks * sizeof(float));
@@ -505,9 +801,74 @@ bool decode_fits(const QW& w) {
     return chunks <= 8 * 64 * 2;     // at most 8 K slices of 128 chunks
 }
 
+namespace {
+
+// The many-token path: MFMA preparation (A x partials, activations), then
+// the MFMA backbone in passes of 16 tokens.
+hipError_t launch_decode_mfma(int n, const QW* w, const LR* c, const void* x, int T, int act, void* const* y,
+                              int out, void* ws, hipStream_t st) {
+    const int d_in = w[0].d_in;
+    const MfmaPlan mp = mfma_plan(d_in);
+    char* wsb = static_cast<char*>(ws);
+    PrepMArgs pa;
+    DecodeArgs a;
+    size_t off = 0;
+    int tile_end = 0, rtiles = 0;
+    for (int i = 0; i < n; ++i) {
+        float* tp = reinterpret_cast<float*>(wsb + off);
+        const int rp = pad32(c[i].rank);
+        off += up256(static_cast<size_t>(mp.kp) * T * rp * sizeof(float));
+        pa.A[i] = c[i].A;
+        pa.tp[i] = tp;
+        pa.rank[i] = c[i].rank;
+        pa.rpad[i] = rp;
+        rtiles += rp / 16 * mp.kp;
+        pa.tile_end[i] = rtiles;
+        tile_end += (w[i].d_out + 15) / 16;
+        a.lin[i] = Lin{w[i].q, w[i].s, w[i].z, c[i].B, y[i], tp, w[i].d_out, c[i].rank, c[i].r_max, tile_end, rp};
+    }
+    const int chunks = d_in / 8 / 4;
+    f16x2* xp = reinterpret_cast<f16x2*>(wsb + off);
+    off += up256(static_cast<size_t>(T) * d_in * 2);
+    float* sx = reinterpret_cast<float*>(wsb + off);
+    pa.n = n;
+    pa.x = static_cast<const uint16_t*>(x);
+    pa.xp = xp;
+    pa.sx = sx;
+    pa.d_in = d_in;
+    pa.T = T;
+    pa.act = act;
+    pa.kp = mp.kp;
+    pa.spw = mp.spw;
+    const long long items = static_cast<long long>(T) * chunks;
+    const unsigned grid = static_cast<unsigned>(rtiles + (items + 255) / 256);
+    hipLaunchKernelGGL(decode_prep_mfma_kernel, dim3(grid), dim3(256), 0, st, pa);
+    hipError_t e = hipGetLastError();
+    a.n = n;
+    a.xp = xp;
+    a.sx = sx;
+    a.d_in = d_in;
+    a.G = w[0].G;
+    a.T = T;
+    a.out = out;
+    a.ks = 4;
+    a.cps = 0;
+    a.kp = mp.kp;
+    for (int tok0 = 0; tok0 < T && e == hipSuccess; tok0 += 16) {
+        a.tok0 = tok0;
+        hipLaunchKernelGGL(decode_mfma_kernel, dim3(tile_end), dim3(256), 0, st, a);
+        e = hipGetLastError();
+    }
+    return e;
+}
+
+}  // namespace
+
 hipError_t launch_linear_decode(int n, const QW* w, const LR* c, const void* x, int T, int act,
                                 void* const* y, int out, void* ws, hipStream_t st) {
     const int d_in = w[0].d_in, bits = w[0].bits;
+    if (n < 1 || n > kMaxWin) return hipErrorInvalidConfiguration;
+    if (use_mfma(bits, T)) return launch_decode_mfma(n, w, c, x, T, act, y, out, ws, st);
     int max_rank = 0;
     for (int i = 0; i < n; ++i) max_rank = max(max_rank, c[i].rank);
     const Plan p = plan(d_in, bits, max_rank, T);

@@ -28,6 +28,7 @@
 
 #include "cl_device.h"
 #include "cl_internal.h"
+#include "mfma_common.h"
 
 namespace cl {
 
@@ -96,51 +97,6 @@ __device__ __forceinline__ u32x4 dequant_half2(uint32_t w, int h, f16x2 s2, f16x
         r[p] = __builtin_bit_cast(uint32_t, (q - zz) * s2);
     }
     return r;
-}
-
-// (x & m) | c in one instruction; m comes from a scalar register, c from a
-// vector register (one scalar operand per instruction on this target).
-__device__ __forceinline__ uint32_t and_or(uint32_t x, uint32_t m, uint32_t c) {
-    uint32_t r;
-    asm("v_and_or_b32 %0, %1, %2, %3" : "=v"(r) : "v"(x), "s"(m), "v"(c));
-    return r;
-}
-
-// Per-fragment constants of one quantization group for dequant_word4x, two
-// halves per register: (s, s/16) and (1024 + z, 1024 + 16 z).
-struct Dq {
-    f16x2 s, z;
-};
-
-__device__ __forceinline__ Dq make_dq(uint32_t sbits, uint32_t zbits) {
-    const f16 s = __builtin_bit_cast(f16, static_cast<uint16_t>(sbits));
-    const f16 z = __builtin_bit_cast(f16, static_cast<uint16_t>(zbits));
-    const f16 s16 = s * static_cast<f16>(0.0625f);                     // exact unless subnormal
-    const f16 z1 = static_cast<f16>(1024.0f) + z;                      // exact: z < 16
-    const f16 z16 = static_cast<f16>(1024.0f) + z * static_cast<f16>(16.0f);
-    return Dq{f16x2{s, s16}, f16x2{z1, z16}};
-}
-
-// One 32-bit word of 4-bit codes -> 8 fp16 values s (q - z), pair order
-// (q0,q4),(q1,q5),(q2,q6),(q3,q7), with one shift and four masks: a code
-// left in bits 4..7 of a half reads as 1024 + 16 q, so its pair subtracts
-// 1024 + 16 z (exact) and scales by s/16.
-__device__ __forceinline__ u32x4 dequant_word4x(uint32_t w, const Dq& d, uint32_t mlo, uint32_t mhi,
-                                               uint32_t bias) {
-    const uint32_t w8 = w >> 8;
-    const f16x2 s1 = {d.s.x, d.s.x}, s16 = {d.s.y, d.s.y};
-    const f16x2 z1 = {d.z.x, d.z.x}, z16 = {d.z.y, d.z.y};
-    u32x4 r;
-    r[0] = __builtin_bit_cast(uint32_t, (__builtin_bit_cast(f16x2, and_or(w, mlo, bias)) - z1) * s1);
-    r[1] = __builtin_bit_cast(uint32_t, (__builtin_bit_cast(f16x2, and_or(w, mhi, bias)) - z16) * s16);
-    r[2] = __builtin_bit_cast(uint32_t, (__builtin_bit_cast(f16x2, and_or(w8, mlo, bias)) - z1) * s1);
-    r[3] = __builtin_bit_cast(uint32_t, (__builtin_bit_cast(f16x2, and_or(w8, mhi, bias)) - z16) * s16);
-    return r;
-}
-
-__device__ __forceinline__ f32x4 mfma(const u32x4& a, const u32x4& b, const f32x4& c) {
-    return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), c,
-                                                  0, 0, 0);
 }
 
 struct PrefillArgs {
@@ -245,6 +201,14 @@ __global__ __launch_bounds__(256) void lowrank_t_kernel(const uint16_t* __restri
     }
 }
 
+// LDS slot of X' chunk c in a row whose low four index bits are r: c ^ f(r)
+// with f(r) = (r >> 1 & 3) | (r & 1) << 2 | (r & 8), a permutation of 0..15.
+// An MFMA operand read has lanes r = 0..15 of lane group g on chunk 4 g + t;
+// the 16 rows give 16 distinct slots, and the two lane groups of one 32-lane
+// half (chunks differing in bit 2) land in opposite bank halves for odd and
+// even rows, so a 128-bit read has no bank conflict.
+__device__ __forceinline__ int xswz(int r) { return ((r >> 1) & 3) | ((r & 1) << 2) | (r & 8); }
+
 // One K step's packed codes of a lane: 32 codes of one weight row (4-bit:
 // four words; 2-bit: two words), with their group's scale and zero.
 template <int BITS>
@@ -256,7 +220,7 @@ struct WStep {
 template <int BITS>
 __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
     // two stages of X': [BM rows][16 chunks of 8 k], chunk c of row r stored
-    // at slot c ^ (r & 15)
+    // at slot c ^ xswz(r & 15)
     __shared__ u32x4 xs[2][BM * 16];
 
     const int tid = threadIdx.x;
@@ -279,7 +243,7 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
         for (int j = 0; j < 8; ++j) {
             const int blk = wave * 8 + j;                  // 64 slots = 4 rows
             const int row = 4 * blk + (lane >> 4);
-            const int chunk = (lane & 15) ^ (row & 15);
+            const int chunk = (lane & 15) ^ xswz(row & 15);
             const int m = m0 + row < a.M ? m0 + row : a.M - 1;
             int k = k0 + 8 * chunk;
             if (k >= a.K) k = k0;                          // half K step: weights there are zero
@@ -328,6 +292,7 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
     const uint32_t mlo = __builtin_amdgcn_readfirstlane(0x000F000Fu);
     const uint32_t mhi = __builtin_amdgcn_readfirstlane(0x00F000F0u);
     const uint32_t bias = 0x64006400u;
+    const int fr = xswz(r);
     auto compute = [&](int kb, int st, const WStep<BITS> (&ws)[4]) {
         Dq dq[4];
         f16x2 s2[4], zz[4];
@@ -353,10 +318,10 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
                 if constexpr (BITS == 4) bf[j] = dequant_word4x(ws[j].w[t], dq[j], mlo, mhi, bias);
                 else bf[j] = dequant_half2(ws[j].w[t >> 1], t & 1, s2[j], zz[j]);
             }
-            const int chunk = 4 * g + t;
+            const int slot = (4 * g + t) ^ fr;
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
-                const u32x4 af = xs[st][(16 * i + r) * 16 + (chunk ^ r)];
+                const u32x4 af = xs[st][(16 * i + r) * 16 + slot];
 #pragma unroll
                 for (int j = 0; j < 4; ++j) acc[i][j] = mfma(af, bf[j], acc[i][j]);
             }
