@@ -99,6 +99,51 @@ __device__ __forceinline__ void dot_word(uint32_t w, const f16x2* xv, float* d) 
     }
 }
 
+// dot_word split in two: the unpacked fp16 lanes of a word (4-bit: 4 pairs,
+// 2-bit: 8 pairs), kept in registers when one word meets several activation
+// vectors, and the v_dot2 accumulation into the same per-scale accumulators.
+// (x & m) as an instruction the compiler keeps where it is written: the
+// unpacked lanes then stay in registers across the activation vectors
+// instead of being recomputed for each one.
+__device__ __forceinline__ uint32_t and_kept(uint32_t x, uint32_t m) {
+    uint32_t r;
+    asm("v_and_b32 %0, %1, %2" : "=v"(r) : "v"(x), "s"(m));
+    return r;
+}
+
+template <int BITS>
+__device__ __forceinline__ void unpack_word(uint32_t w, f16x2* u) {
+    const uint32_t w8 = w >> 8;
+    if (BITS == 4) {
+        u[0] = __builtin_bit_cast(f16x2, and_kept(w, 0x000F000Fu));
+        u[1] = __builtin_bit_cast(f16x2, and_kept(w, 0x00F000F0u));
+        u[2] = __builtin_bit_cast(f16x2, and_kept(w8, 0x000F000Fu));
+        u[3] = __builtin_bit_cast(f16x2, and_kept(w8, 0x00F000F0u));
+    } else {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            u[k] = __builtin_bit_cast(f16x2, and_kept(w, 0x00030003u << (2 * k)));
+            u[4 + k] = __builtin_bit_cast(f16x2, and_kept(w8, 0x00030003u << (2 * k)));
+        }
+    }
+}
+
+template <int BITS>
+__device__ __forceinline__ void dot_unpacked(const f16x2* u, const f16x2* xv, float* d) {
+    if (BITS == 4) {
+        d[0] = dot2(u[0], xv[0], d[0]);
+        d[1] = dot2(u[1], xv[1], d[1]);
+        d[0] = dot2(u[2], xv[2], d[0]);
+        d[1] = dot2(u[3], xv[3], d[1]);
+    } else {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            d[k] = dot2(u[k], xv[k], d[k]);
+            d[k] = dot2(u[4 + k], xv[4 + k], d[k]);
+        }
+    }
+}
+
 // sum of q * x * 2^-24 over the word(s): the per-scale accumulators with
 // their power-of-two scales removed
 template <int BITS>

@@ -9,9 +9,10 @@
 // over every routed expert, and only routed experts' codes, scales, zeros and
 // factors are read.
 //
-//  * moe_prep_kernel: workgroup (j, q), j < min(E, T*k), scans the routing
-//    table -- so no workgroup ever waits for another -- and takes e = the
-//    j-th routed expert in ascending id order (none: it exits).  Each of its
+//  * moe_prep_kernel: workgroup (j, q), j < min(E, T*k), reads the routing
+//    table -- so no workgroup ever waits for another -- counts slots per
+//    expert, scans the counts and takes e = the j-th routed expert in
+//    ascending id order (none: it exits).  Each of its
 //    four waves computes t[slot][i] = A_e[i] . x_slot for one rank row
 //    i = 4q + wave over all of e's slots (four slots per pass).  Workgroup
 //    (j, 0) also writes entry j of the active-expert table and e's slots, in
@@ -73,8 +74,10 @@ __global__ __launch_bounds__(256) void moe_prep_kernel(MoeArgs a) {
     constexpr int CPW = 32 / BITS, HPW = CPW / 2, PPC = 4 * HPW;
     __shared__ int sids[kMaxSlots];
     __shared__ int mys[kMaxSlots];          // this expert's slots, in slot order
-    __shared__ unsigned routed[kMaxExperts / 32];
-    __shared__ int cnt_lt, cnt_eq, sel;
+    __shared__ int hist[kMaxExperts];       // slots per expert
+    __shared__ int wsum[4][2];
+    __shared__ int wcnt[4];
+    __shared__ int sel, sel_lt, sel_n;
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
@@ -87,31 +90,45 @@ __global__ __launch_bounds__(256) void moe_prep_kernel(MoeArgs a) {
         // rank rows 4 quad .. 4 quad + 3
         const int j = blk / a.rq;
         const int quad = blk - j * a.rq;
-        for (int i = tid; i < kMaxExperts / 32; i += 256) routed[i] = 0u;
-        if (tid == 0) { cnt_lt = 0; cnt_eq = 0; sel = -1; }
+        // slots per expert (LDS atomics contend only within one expert)
+        for (int i = tid; i < a.E; i += 256) hist[i] = 0;
+        if (tid == 0) sel = -1;
         __syncthreads();
         for (int sl = tid; sl < S; sl += 256) {
             const int id = a.ids[sl];
             sids[sl] = id;
-            if (id >= 0 && id < a.E) atomicOr(&routed[id >> 5], 1u << (id & 31));
+            if (id >= 0 && id < a.E) atomicAdd(&hist[id], 1);
         }
         __syncthreads();
-        // the j-th set bit of the routed bitmap: one thread per 32-expert word
-        if (tid < (a.E + 31) / 32) {
-            int below = 0;
-            for (int i = 0; i < tid; ++i) below += __popc(routed[i]);
-            unsigned m = routed[tid];
-            const int here = __popc(m);
-            if (j >= below && j < below + here) {
-                for (int k = below; k < j; ++k) m &= m - 1u;     // drop the lower set bits
-                sel = 32 * tid + __builtin_ctz(m);
+        // block scan over the experts (thread t owns experts 4 t .. 4 t + 3):
+        // the first sorted slot of each expert and its index among the
+        // routed experts; expert e with index j is this workgroup's
+        int c[4], cs = 0, fs = 0;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int ex = 4 * tid + q;
+            c[q] = ex < a.E ? hist[ex] : 0;
+            cs += c[q];
+            fs += c[q] > 0;
+        }
+        int ic = cs, ifl = fs;                   // inclusive scan within the wave
+        for (int off = 1; off < 64; off <<= 1) {
+            const int tc = __shfl_up(ic, off, 64), tf = __shfl_up(ifl, off, 64);
+            if (lane >= off) { ic += tc; ifl += tf; }
+        }
+        if (lane == 63) { wsum[wave][0] = ic; wsum[wave][1] = ifl; }
+        __syncthreads();
+        int pc = ic - cs, pf = ifl - fs;
+        for (int w2 = 0; w2 < wave; ++w2) { pc += wsum[w2][0]; pf += wsum[w2][1]; }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            if (c[q] > 0) {
+                if (pf == j) { sel = 4 * tid + q; sel_lt = pc; sel_n = c[q]; }
+                pc += c[q];
+                pf += 1;
             }
         }
-        if (j == 0 && quad == 0 && tid == 0) {
-            int n = 0;
-            for (int i = 0; i < (a.E + 31) / 32; ++i) n += __popc(routed[i]);
-            *a.n_active = n;
-        }
+        if (j == 0 && quad == 0 && tid == 0) *a.n_active = wsum[0][1] + wsum[1][1] + wsum[2][1] + wsum[3][1];
         __syncthreads();
         if (j == 0 && quad == 0) {
             // out-of-range ids: their output rows are zero
@@ -123,16 +140,7 @@ __global__ __launch_bounds__(256) void moe_prep_kernel(MoeArgs a) {
         }
         const int e = sel;
         if (e < 0) return;                      // fewer than j + 1 routed experts
-        int lt = 0, eq = 0;
-        for (int sl = tid; sl < S; sl += 256) {
-            const int id = sids[sl];
-            lt += id >= 0 && id < e;
-            eq += id == e;
-        }
-        atomicAdd(&cnt_lt, lt);
-        atomicAdd(&cnt_eq, eq);
-        __syncthreads();
-        const int ne = cnt_eq;
+        const int ne = sel_n, cnt_lt = sel_lt;
         int rank = a.r_max > 0 ? a.ranks[e] : 0;     // ranks may be null when r_max is 0
         rank = rank < 0 ? 0 : (rank > a.r_max ? a.r_max : rank);
         if (quad == 0 && tid == 0) {
@@ -141,15 +149,24 @@ __global__ __launch_bounds__(256) void moe_prep_kernel(MoeArgs a) {
             a.table[4 * j + 2] = ne;
             a.table[4 * j + 3] = rank;
         }
-        // this expert's slots in slot order
-        for (int sl = tid; sl < S; sl += 256) {
-            if (sids[sl] != e) continue;
-            int pos = 0;
-            for (int s2 = 0; s2 < sl; ++s2) pos += sids[s2] == e;
-            if (quad == 0) a.sorted[cnt_lt + pos] = sl;
-            mys[pos] = sl;
+        // this expert's slots in slot order (ballots, 256 slots per pass)
+        int base_pos = 0;
+        for (int b0 = 0; b0 < S; b0 += 256) {
+            const int sl = b0 + tid;
+            const bool mine = sl < S && sids[sl] == e;
+            const unsigned long long m = __ballot(mine);
+            if (lane == 0) wcnt[wave] = __popcll(m);
+            __syncthreads();
+            int off = base_pos;
+            for (int w2 = 0; w2 < wave; ++w2) off += wcnt[w2];
+            if (mine) {
+                const int pos = off + __popcll(m & ((1ull << lane) - 1ull));
+                if (quad == 0) a.sorted[cnt_lt + pos] = sl;
+                mys[pos] = sl;
+            }
+            base_pos += wcnt[0] + wcnt[1] + wcnt[2] + wcnt[3];
+            __syncthreads();
         }
-        __syncthreads();
         // t[slot][i] = A_e[i] . x_slot: one wave per rank row, four slots at a time
         const int i = 4 * quad + wave;
         if (i >= rank) return;
@@ -207,7 +224,9 @@ __global__ __launch_bounds__(256) void moe_prep_kernel(MoeArgs a) {
 }
 
 // NB: factor columns per lane (r_max <= NB * 64 * ks); 0 when r_max is 0.
-template <int BITS, int CPL, int NB>
+// HOIST: unpack the codes once into fp16 lanes held in registers (for
+// experts that meet several slots); otherwise unpack per slot.
+template <int BITS, int CPL, int NB, bool HOIST>
 __global__ __launch_bounds__(512) void moe_kernel(MoeArgs a) {
     constexpr int R = rows_per_wave(BITS);
     constexpr int CPW = 32 / BITS;
@@ -301,6 +320,18 @@ __global__ __launch_bounds__(512) void moe_kernel(MoeArgs a) {
             tv[m] = i < rank ? a.t[static_cast<size_t>(sl) * a.r_max + i] : 0.f;
         }
     };
+    // the unpacked codes (HOIST), from the raw loads above
+    constexpr int UPW = BITS == 4 ? 4 : 8;       // fp16 pairs per word
+    f16x2 un[HOIST ? R : 1][HOIST ? 4 * UPW : 1];
+    if constexpr (HOIST) {
+#pragma unroll
+        for (int rr0 = 0; rr0 < R; ++rr0)
+#pragma unroll
+            for (int w = 0; w < 4; ++w) {
+                const uint32_t qw = qv[rr0][0][w];
+                unpack_word<BITS>(qw, &un[rr0][w * UPW]);
+            }
+    }
     int lane_slot = lane < scnt ? a.sorted[sbeg + lane] : 0;
     f16x2 xn[PPC];
     float sxn, tn[NBA];
@@ -328,7 +359,10 @@ __global__ __launch_bounds__(512) void moe_kernel(MoeArgs a) {
 #pragma unroll
             for (int q = 0; q < NACC; ++q) d[q] = 0.f;
 #pragma unroll
-            for (int w = 0; w < 4; ++w) dot_word<BITS>(qv[r][0][w], xv + w * HPW, d);
+            for (int w = 0; w < 4; ++w) {
+                if constexpr (HOIST) dot_unpacked<BITS>(&un[r][w * UPW], xv + w * HPW, d);
+                else dot_word<BITS>(qv[r][0][w], xv + w * HPW, d);
+            }
             const float v = fmaf(combine<BITS>(d), 16777216.0f, -zc[r][0] * sxv);
             acc[r] = sc[r][0] * v;
         }
@@ -378,18 +412,21 @@ MoeLayout moe_layout(const QW& w, int r_max, int E, int T, int k, int x_per_slot
 }
 
 template <int BITS, int CPL, int NB>
-hipError_t launch_moe3(const MoeArgs& a, int blocks, int threads, hipStream_t st) {
-    hipLaunchKernelGGL((moe_kernel<BITS, CPL, NB>), dim3(blocks), dim3(threads), 0, st, a);
+hipError_t launch_moe3(const MoeArgs& a, bool hoist, int blocks, int threads, hipStream_t st) {
+    if (hoist)
+        hipLaunchKernelGGL((moe_kernel<BITS, CPL, NB, true>), dim3(blocks), dim3(threads), 0, st, a);
+    else
+        hipLaunchKernelGGL((moe_kernel<BITS, CPL, NB, false>), dim3(blocks), dim3(threads), 0, st, a);
     return hipGetLastError();
 }
 
 template <int BITS>
-hipError_t launch_moe2(const MoeArgs& a, int nb, int blocks, int threads, hipStream_t st) {
+hipError_t launch_moe2(const MoeArgs& a, int nb, bool hoist, int blocks, int threads, hipStream_t st) {
     switch (nb) {
-        case 0: return launch_moe3<BITS, 1, 0>(a, blocks, threads, st);
-        case 1: return launch_moe3<BITS, 1, 1>(a, blocks, threads, st);
-        case 2: return launch_moe3<BITS, 1, 2>(a, blocks, threads, st);
-        default: return launch_moe3<BITS, 1, 4>(a, blocks, threads, st);
+        case 0: return launch_moe3<BITS, 1, 0>(a, hoist, blocks, threads, st);
+        case 1: return launch_moe3<BITS, 1, 1>(a, hoist, blocks, threads, st);
+        case 2: return launch_moe3<BITS, 1, 2>(a, hoist, blocks, threads, st);
+        default: return launch_moe3<BITS, 1, 4>(a, hoist, blocks, threads, st);
     }
 }
 
@@ -453,7 +490,10 @@ hipError_t launch_moe_decode(const QW& w, const uint16_t* A, const uint16_t* B, 
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int blocks = max_active * a.bpe;
-    return w.bits == 4 ? launch_moe2<4>(a, nb, blocks, threads, st) : launch_moe2<2>(a, nb, blocks, threads, st);
+    // experts meeting two or more slots on average: unpack once per batch
+    const bool many = S >= 2 * max_active;
+    return w.bits == 4 ? launch_moe2<4>(a, nb, many, blocks, threads, st)
+                       : launch_moe2<2>(a, nb, many, blocks, threads, st);
 }
 
 }  // namespace cl
