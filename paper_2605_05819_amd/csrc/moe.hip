@@ -131,11 +131,18 @@ __global__ __launch_bounds__(256) void moe_prep_kernel(MoeArgs a) {
         if (j == 0 && quad == 0 && tid == 0) *a.n_active = wsum[0][1] + wsum[1][1] + wsum[2][1] + wsum[3][1];
         __syncthreads();
         if (j == 0 && quad == 0) {
-            // out-of-range ids: their output rows are zero
-            for (int sl = 0; sl < S; ++sl) {
-                const int id = sids[sl];
-                if (id >= 0 && id < a.E) continue;
-                for (int o = tid; o < a.d_out; o += 256) store_out(a.y, static_cast<size_t>(sl) * a.d_out + o, 0.f, a.out);
+            // out-of-range ids: their output rows are zero.  One parallel
+            // check first (valid routing skips the rest), then each wave
+            // zeroes the rows of its share of the slots.
+            int bad = 0;
+            for (int sl = tid; sl < S; sl += 256) bad |= !(sids[sl] >= 0 && sids[sl] < a.E);
+            if (__syncthreads_or(bad)) {
+                for (int sl = wave; sl < S; sl += 4) {
+                    const int id = sids[sl];
+                    if (id >= 0 && id < a.E) continue;
+                    for (int o = lane; o < a.d_out; o += 64)
+                        store_out(a.y, static_cast<size_t>(sl) * a.d_out + o, 0.f, a.out);
+                }
             }
         }
         const int e = sel;
@@ -181,7 +188,8 @@ __global__ __launch_bounds__(256) void moe_prep_kernel(MoeArgs a) {
                 xr[u] = a.x + static_cast<size_t>(xrow) * a.d_in;
             }
             float acc[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll 2
+            // all of the row's loads in flight for rows up to 2048 codes
+#pragma unroll 4
             for (int c = lane * 8; c < a.d_in; c += 64 * 8) {
                 const u32x4 av = *reinterpret_cast<const u32x4*>(ar + c);
                 uint32_t xw[4][4];
