@@ -45,6 +45,7 @@ namespace {
 constexpr int rows_per_wave(int bits) { return bits == 4 ? 4 : 2; }
 constexpr int kMaxSlots = 1024;      // T * k
 constexpr int kMaxExperts = 1024;
+constexpr int kTab = 8;              // ints per active-expert table entry
 
 struct MoeArgs {
     const uint32_t* q;
@@ -60,7 +61,7 @@ struct MoeArgs {
     int E, T, k, d_out, d_in, G, r_max, act, out, x_per_slot;
     // workspace
     int* n_active;
-    int* table;              // [max_active][4]: expert, first slot, slot count, rank
+    int* table;              // [max_active][kTab]: expert, first sorted index, slot count, rank, first slot
     int* sorted;             // [T*k] slot ids grouped by expert, slot order within
     float* t;                // [T*k][r_max]
     f16x2* xp;               // [rows][d_in/2]
@@ -151,10 +152,10 @@ __global__ __launch_bounds__(256) void moe_prep_kernel(MoeArgs a) {
         int rank = a.r_max > 0 ? a.ranks[e] : 0;     // ranks may be null when r_max is 0
         rank = rank < 0 ? 0 : (rank > a.r_max ? a.r_max : rank);
         if (quad == 0 && tid == 0) {
-            a.table[4 * j + 0] = e;
-            a.table[4 * j + 1] = cnt_lt;
-            a.table[4 * j + 2] = ne;
-            a.table[4 * j + 3] = rank;
+            a.table[kTab * j + 0] = e;
+            a.table[kTab * j + 1] = cnt_lt;
+            a.table[kTab * j + 2] = ne;
+            a.table[kTab * j + 3] = rank;
         }
         // this expert's slots in slot order (ballots, 256 slots per pass)
         int base_pos = 0;
@@ -168,7 +169,10 @@ __global__ __launch_bounds__(256) void moe_prep_kernel(MoeArgs a) {
             for (int w2 = 0; w2 < wave; ++w2) off += wcnt[w2];
             if (mine) {
                 const int pos = off + __popcll(m & ((1ull << lane) - 1ull));
-                if (quad == 0) a.sorted[cnt_lt + pos] = sl;
+                if (quad == 0) {
+                    a.sorted[cnt_lt + pos] = sl;
+                    if (pos == 0) a.table[kTab * j + 4] = sl;
+                }
                 mys[pos] = sl;
             }
             base_pos += wcnt[0] + wcnt[1] + wcnt[2] + wcnt[3];
@@ -245,13 +249,14 @@ __global__ __launch_bounds__(512) void moe_kernel(MoeArgs a) {
     constexpr int NBA = NB > 0 ? NB : 1;
     __shared__ float red[8][R];
 
+    // the active-expert count and this entry are read together (the entry
+    // exists for every ae below min(E, T k); it is used only if ae is active)
     const int ae = blockIdx.x / a.bpe;
-    if (ae >= *a.n_active) return;                  // whole workgroup: no routed expert here
+    const int n_active = *a.n_active;
+    const int* ent = a.table + kTab * ae;
+    const int e = ent[0], sbeg = ent[1], scnt = ent[2], rank = ent[3], slot0 = ent[4];
+    if (ae >= n_active) return;                     // whole workgroup: no routed expert here
     const int batch = blockIdx.x - ae * a.bpe;
-    const int e = a.table[4 * ae + 0];
-    const int sbeg = a.table[4 * ae + 1];
-    const int scnt = a.table[4 * ae + 2];
-    const int rank = a.table[4 * ae + 3];
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -340,10 +345,12 @@ __global__ __launch_bounds__(512) void moe_kernel(MoeArgs a) {
                 unpack_word<BITS>(qw, &un[rr0][w * UPW]);
             }
     }
+    // the first slot comes with the table entry, so its activations load
+    // together with the codes; the rest of the slot ids are read meanwhile
     int lane_slot = lane < scnt ? a.sorted[sbeg + lane] : 0;
     f16x2 xn[PPC];
     float sxn, tn[NBA];
-    load_x(__shfl(lane_slot, 0, 64), xn, sxn, tn);
+    load_x(slot0, xn, sxn, tn);
     for (int jslot = 0; jslot < scnt; ++jslot) {
         const int sl = __shfl(lane_slot, jslot & 63, 64);
         f16x2 xv[PPC];
@@ -411,7 +418,7 @@ MoeLayout moe_layout(const QW& w, int r_max, int E, int T, int k, int x_per_slot
     MoeLayout l;
     l.n_active = 0;
     l.table = 256;
-    l.sorted = l.table + up256(static_cast<size_t>(max_active) * 4 * sizeof(int));
+    l.sorted = l.table + up256(static_cast<size_t>(max_active) * kTab * sizeof(int));
     l.t = l.sorted + up256(static_cast<size_t>(S) * sizeof(int));
     l.xp = l.t + up256(static_cast<size_t>(S) * r_max * sizeof(float));
     l.sx = l.xp + up256(static_cast<size_t>(rows) * w.d_in * 2);
