@@ -7,16 +7,20 @@
 // Appendix A.1); a single linear is the window n = 1.
 //
 // Two launches per call:
-//  * prep: t_i = A_i[:r_i] x for every linear (one workgroup per row of
-//    A_i) and the activations converted to fp16, permuted into the pair order
+//  * prep: t_i = A_i[:r_i] x for every linear (one wave per row of A_i)
+//    and the activations converted to fp16, permuted into the pair order
 //    of the unpacked codes, with each 16-byte chunk's sum of activations --
 //    all into the workspace;
 //  * backbone: one grouped, persistent kernel over all row batches of all the
 //    window's linears.
-// A x stays in its own launch: handing it from producer to consumer
-// workgroups inside one launch needs device-scope release/acquire between
-// XCDs, whose L2 writeback/invalidate measured 12-90 us on MI355X against a
-// few us for the extra launch.
+// A x stays in its own launch.  Handing it from producer to backbone
+// workgroups of one launch was built and measured on MI355X: with
+// release/acquire fences the per-XCD L2 writeback/invalidate cost 12-90 us;
+// with fence-free device-coherent accesses (replicated, call-tagged
+// entries) it still lost above ~8 MB of weights, because the producers'
+// loads, their stores and the consumers' poll each wait in memory queues
+// filled by the backbone's own streaming loads -- three round trips that
+// take about as long as the stream.
 //
 // The backbone is HBM-bound (about half a byte per weight at 4 bits, a
 // quarter at 2 bits):
@@ -37,6 +41,8 @@
 //  * sums over lanes use a transposing butterfly (R values in log steps),
 //    K slices are combined through LDS in a fixed order: results are bitwise
 //    reproducible.
+
+#include <type_traits>
 
 #include "cl_device.h"
 #include "cl_internal.h"
@@ -102,77 +108,89 @@ struct PrepArgs {
     int d_in, T, act;
 };
 
-// Preparation kernel: workgroups [0, sum of ranks) compute one row i of some
-// linear's A x for every token (all of the row's 16-byte loads issued before
-// any arithmetic, fixed-order reduction); the remaining workgroups prepare the
-// activations, one thread per (token, chunk).
+// One row of A times the activations of tokens tok0 .. tok0 + NTOK - 1, by
+// one wave: lane l takes the 8-element runs starting at 8 l + 512 m in
+// increasing m (eight 16-byte loads of A in flight per lane), adds each
+// run's v_dot2 chain to a float accumulator, and the wave sums its lanes
+// with a butterfly.  Each token's result does not depend on NTOK.
+template <int NTOK>
+__device__ __forceinline__ void row_times_x(const uint16_t* ar, const uint16_t* x, int d_in, int tok0, int act,
+                                            float (&out)[NTOK]) {
+    constexpr int KB = 8;
+    const int lane = threadIdx.x & 63;
+    float acc[NTOK];
+#pragma unroll
+    for (int tk = 0; tk < NTOK; ++tk) acc[tk] = 0.f;
+    for (int base = 0; base < d_in; base += 64 * 8 * KB) {
+        u32x4 av[KB];
+        int col[KB];
+#pragma unroll
+        for (int k = 0; k < KB; ++k) {
+            col[k] = base + (lane + 64 * k) * 8;
+            av[k] = *reinterpret_cast<const u32x4*>(ar + (col[k] < d_in ? col[k] : 0));
+        }
+#pragma unroll
+        for (int tk = 0; tk < NTOK; ++tk) {
+            const uint16_t* xr = x + static_cast<size_t>(tok0 + tk) * d_in;
+#pragma unroll
+            for (int k = 0; k < KB; ++k) {
+                uint32_t xw[4];
+                load8_f16(xr + (col[k] < d_in ? col[k] : 0), act, xw);
+                float d = 0.f;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    // copy the vector element to a scalar first: a bit_cast
+                    // of a subscripted ext_vector reads element 0
+                    const uint32_t ak = av[k][e], xk = xw[e];
+                    d = dot2(__builtin_bit_cast(f16x2, ak), __builtin_bit_cast(f16x2, xk), d);
+                }
+                acc[tk] += col[k] < d_in ? d : 0.f;
+            }
+        }
+    }
+#pragma unroll
+    for (int tk = 0; tk < NTOK; ++tk) out[tk] = wave_sum(acc[tk]);
+}
+
+// Preparation kernel: each wave of workgroups [0, ceil(sum of ranks / 4))
+// computes one row i of some linear's A x for every token (tokens in passes
+// of 4, then 2, then 1); the remaining workgroups prepare the activations,
+// one thread per (token, chunk).
 template <int BITS>
 __global__ __launch_bounds__(256) void decode_prep_kernel(PrepArgs a) {
     constexpr int CPW = 32 / BITS, HPW = CPW / 2, PPC = 4 * HPW;
-    constexpr int KB = 4;                   // 16-byte loads per thread per batch
-    constexpr int TB = 4;                   // tokens per pass over a row of A
-    __shared__ float part[4][TB];
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
     const int tid = threadIdx.x;
     const int d_in = a.d_in, T = a.T;
     const int nrank = a.n > 0 ? a.rank_end[a.n - 1] : 0;
+    const int rank_blocks = (nrank + 3) / 4;
     const int blk = blockIdx.x;
-    if (blk < nrank) {
+    if (blk < rank_blocks) {
+        const int j = blk * 4 + wave;
+        if (j >= nrank) return;
         int li = 0;
-        while (blk >= a.rank_end[li]) ++li;
-        const int i = blk - (li ? a.rank_end[li - 1] : 0);
+        while (j >= a.rank_end[li]) ++li;
+        const int i = j - (li ? a.rank_end[li - 1] : 0);
         const int rank = a.rank_end[li] - (li ? a.rank_end[li - 1] : 0);
         const uint16_t* ar = a.A[li] + static_cast<size_t>(i) * d_in;
         float* t = a.t[li];
-        for (int base = 0; base < d_in; base += 256 * 8 * KB) {
-            u32x4 av[KB];
-            int col[KB];
+        auto pass = [&](auto ntok, int tb) {
+            constexpr int N = decltype(ntok)::value;
+            float v[N];
+            row_times_x<N>(ar, a.x, d_in, tb, a.act, v);
 #pragma unroll
-            for (int k = 0; k < KB; ++k) {
-                col[k] = base + (tid + k * 256) * 8;
-                av[k] = *reinterpret_cast<const u32x4*>(ar + (col[k] < d_in ? col[k] : 0));
-            }
-            for (int tb = 0; tb < T; tb += TB) {
-                float acc[TB];
-#pragma unroll
-                for (int tk = 0; tk < TB; ++tk) {
-                    acc[tk] = 0.f;
-                    if (tb + tk >= T) continue;
-                    const uint16_t* xr = a.x + static_cast<size_t>(tb + tk) * d_in;
-#pragma unroll
-                    for (int k = 0; k < KB; ++k) {
-                        uint32_t xw[4];
-                        load8_f16(xr + (col[k] < d_in ? col[k] : 0), a.act, xw);
-                        float d = 0.f;
-#pragma unroll
-                        for (int e = 0; e < 4; ++e) {
-                            // copy the vector element to a scalar first: a bit_cast
-                            // of a subscripted ext_vector reads element 0
-                            const uint32_t ak = av[k][e], xk = xw[e];
-                            d = dot2(__builtin_bit_cast(f16x2, ak), __builtin_bit_cast(f16x2, xk), d);
-                        }
-                        acc[tk] += col[k] < d_in ? d : 0.f;
-                    }
-                }
-#pragma unroll
-                for (int tk = 0; tk < TB; ++tk) {
-                    const float v = wave_sum(acc[tk]);
-                    if (lane == 0) part[wave][tk] = v;
-                }
-                __syncthreads();
-                if (tid < TB && tb + tid < T) {
-                    float* dst = t + static_cast<size_t>(tb + tid) * rank + i;
-                    const float v = part[0][tid] + part[1][tid] + part[2][tid] + part[3][tid];
-                    *dst = base == 0 ? v : *dst + v;
-                }
-                __syncthreads();
-            }
-        }
+            for (int tk = 0; tk < N; ++tk)
+                if (lane == tk) t[static_cast<size_t>(tb + tk) * rank + i] = v[tk];
+        };
+        int tb = 0;
+        for (; tb + 4 <= T; tb += 4) pass(std::integral_constant<int, 4>{}, tb);
+        if (tb + 2 <= T) { pass(std::integral_constant<int, 2>{}, tb); tb += 2; }
+        if (tb < T) pass(std::integral_constant<int, 1>{}, tb);
         return;
     }
     const int chunks = d_in / CPW / 4;
-    const long long item = static_cast<long long>(blk - nrank) * 256 + tid;
+    const long long item = static_cast<long long>(blk - rank_blocks) * 256 + tid;
     if (item >= static_cast<long long>(T) * chunks) return;
     const int tok = static_cast<int>(item / chunks);
     const int c = static_cast<int>(item % chunks);
@@ -717,17 +735,19 @@ int device_cus() {
 template <int BITS, int NT, int CPL, int R, int NB>
 hipError_t launch5(const DecodeArgs& a, const Plan& p, hipStream_t st) {
     auto kern = decode_kernel<BITS, NT, CPL, R, NB>;
-    // resident workgroups per CU for this instance (cached once per process)
-    static int occ = 0;
-    if (!occ) {
+    // resident workgroups per CU for this instance and block size (cached
+    // once per process)
+    static int occ[2] = {0, 0};
+    int& o = occ[p.threads > 256 ? 1 : 0];
+    if (!o) {
         int n = 0;
         if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kern, p.threads, 0) != hipSuccess || n <= 0) n = 1;
-        occ = n;
+        o = n;
     }
     const int nbatch = a.lin[a.n - 1].batch_end;
     // at most one resident wave of workgroups, each with the same number of
     // batches (no partial second wave)
-    const int cap = occ * device_cus();
+    const int cap = o * device_cus();
     const int per = (nbatch + cap - 1) / cap;
     const int blocks = (nbatch + per - 1) / per;
     hipLaunchKernelGGL(kern, dim3(blocks), dim3(p.threads), 0, st, a);
@@ -904,7 +924,7 @@ hipError_t launch_linear_decode(int n, const QW* w, const LR* c, const void* x, 
     pa.T = T;
     pa.act = act;
     const long long items = static_cast<long long>(T) * chunks;
-    const unsigned grid = static_cast<unsigned>(rank_end + (items + 255) / 256);
+    const unsigned grid = static_cast<unsigned>((rank_end + 3) / 4 + (items + 255) / 256);
     if (bits == 4)
         hipLaunchKernelGGL(decode_prep_kernel<4>, dim3(grid), dim3(256), 0, st, pa);
     else
