@@ -79,6 +79,7 @@ struct DecodeArgs {
     int ks;                  // K slices (waves per row group)
     int cps;                 // chunks per slice
     int kp;                  // MFMA path: K parts of the A x partials
+    const u32x4* xf;         // MFMA path: activations, word-major and token-minor (see PrepMArgs)
 };
 
 // Preparation for the MFMA path: A x on MFMA as K-part partials.
@@ -87,14 +88,14 @@ struct PrepMArgs {
     float* tp[kMaxWin];      // [kp][T][rpad]
     int rank[kMaxWin];
     int rpad[kMaxWin];
-    int tile_end[kMaxWin];   // exclusive prefix sum of (rpad / 16) * kp
+    int tile_end[kMaxWin];   // exclusive prefix sum of (rpad / 16) * npass * kp
     int n;
     const uint16_t* x;       // [T][d_in] fp16/bf16 bits
-    f16x2* xp;
-    float* sx;
+    u32x4* xf;               // [pass][d_in / 8][16]: 8 activations of one token, unpack order
     int d_in, T, act;
     int kp;                  // K parts
     int spw;                 // 32-code steps per wave and K part
+    int npass;               // passes of 16 tokens
 };
 
 struct PrepArgs {
@@ -457,12 +458,16 @@ __device__ __forceinline__ u32x4 act8_f16(u32x4 u, int act) {
 }
 
 // Preparation for the MFMA backbone.  Workgroups [0, tiles): (linear, 16 rows
-// of A, K part kp): t partial[kp][tok][i] = sum over the part's k of
-// A[i][k] x[tok][k] for up to 16 tokens on v_mfma_f32_16x16x32_f16 (A rows as
+// of A, pass of 16 tokens, K part kp): t partial[kp][tok][i] = sum over the
+// part's k of A[i][k] x[tok][k] for the pass's tokens on
+// v_mfma_f32_16x16x32_f16 (A rows as
 // the A operand, tokens as the B operand; four waves split the part, eight
 // 32-code steps of loads in flight per wave; the waves' tiles are summed
 // through LDS in a fixed order).  Rows past the rank are written as zero.
-// The remaining workgroups prepare the activations as decode_prep_kernel.
+// The remaining workgroups write the activations in the backbone's operand
+// layout: for each pass of 16 tokens and each 8-code word of K, the 16
+// tokens' 8 activations (16 bytes each, unpack order) side by side, so one
+// load instruction reads 256 contiguous bytes per lane group.
 __global__ __launch_bounds__(256) void decode_prep_mfma_kernel(PrepMArgs a) {
     constexpr int CPW = 8, HPW = 4, PPC = 16;        // 4-bit codes
     __shared__ f32x4 red[4][64];
@@ -477,13 +482,15 @@ __global__ __launch_bounds__(256) void decode_prep_mfma_kernel(PrepMArgs a) {
         int li = 0;
         while (blk >= a.tile_end[li]) ++li;
         const int local = blk - (li ? a.tile_end[li - 1] : 0);
-        const int tile = local / a.kp, kp = local - tile * a.kp;
+        const int tp_ = local / a.kp, kp = local - tp_ * a.kp;
+        const int tile = tp_ / a.npass, pass = tp_ - tile * a.npass;
         const int rank = a.rank[li];
         const int arow = tile * 16 + r;
         const bool av = arow < rank;
         const uint16_t* ar = a.A[li] + static_cast<size_t>(av ? arow : 0) * d_in;
-        const bool tv = r < T;
-        const uint16_t* xr = a.x + static_cast<size_t>(tv ? r : 0) * d_in;
+        const int tokr = pass * 16 + r;
+        const bool tv = tokr < T;
+        const uint16_t* xr = a.x + static_cast<size_t>(tv ? tokr : 0) * d_in;
         const int nsteps = d_in / 32;
         const int s0 = (kp * 4 + wave) * a.spw;
         const int s1 = min(s0 + a.spw, nsteps);
@@ -509,55 +516,71 @@ __global__ __launch_bounds__(256) void decode_prep_mfma_kernel(PrepMArgs a) {
         __syncthreads();
         if (wave != 0 || !tv) return;
         acc = red[0][lane] + red[1][lane] + red[2][lane] + red[3][lane];
-        // acc[e] = partial t[tok r][row tile*16 + 4 g + e]
-        float* dst = a.tp[li] + (static_cast<size_t>(kp) * T + r) * a.rpad[li] + tile * 16 + 4 * g;
+        // acc[e] = partial t[tok tokr][row tile*16 + 4 g + e]
+        float* dst = a.tp[li] + (static_cast<size_t>(kp) * T + tokr) * a.rpad[li] + tile * 16 + 4 * g;
 #pragma unroll
         for (int e = 0; e < 4; ++e) dst[e] = tile * 16 + 4 * g + e < rank ? acc[e] : 0.f;
         return;
     }
-    const int chunks = d_in / CPW / 4;
+    // activations: item (pass, word wi, token lane r) -> 16 bytes, the 8
+    // activations of codes 8 wi .. 8 wi + 7 of token 16 pass + r in the
+    // unpack's pair order (x0, x4), (x1, x5), (x2, x6), (x3, x7); absent
+    // tokens are zero
+    const int wpr = d_in / CPW;
+    const int npass = (T + 15) / 16;
     const long long item = static_cast<long long>(blk - ntile) * 256 + tid;
-    if (item >= static_cast<long long>(T) * chunks) return;
-    const int tok = static_cast<int>(item / chunks);
-    const int c = static_cast<int>(item % chunks);
-    f16x2 v[PPC];
-    load_chunk_x<4>(a.x + static_cast<size_t>(tok) * d_in, c, a.act, v);
-    const f16x2 one = {static_cast<f16>(1.0f), static_cast<f16>(1.0f)};
-    float sum = 0.f;
-    f16x2* dst = a.xp + static_cast<size_t>(tok) * (d_in / 2) + static_cast<size_t>(c) * PPC;
+    if (item >= static_cast<long long>(npass) * wpr * 16) return;
+    const int rt = static_cast<int>(item & 15);
+    const int wi = static_cast<int>((item >> 4) % wpr);
+    const int tok = static_cast<int>(item / (16ll * wpr)) * 16 + rt;
+    u32x4 o = {0u, 0u, 0u, 0u};
+    if (tok < T) {
+        const u32x4 u = act8_f16(*reinterpret_cast<const u32x4*>(a.x + static_cast<size_t>(tok) * d_in + 8 * wi),
+                                 a.act);
+        // u[i] holds (x[2i], x[2i + 1]); pair p needs (x[p], x[p + 4])
 #pragma unroll
-    for (int p = 0; p < PPC; ++p) {
-        sum = dot2(v[p], one, sum);
-        dst[p] = v[p];
+        for (int pp = 0; pp < HPW; ++pp) {
+            const uint32_t lo = u[pp / 2], hi = u[(pp + HPW) / 2];
+            const uint32_t av = (pp & 1) ? (lo >> 16) : (lo & 0xffff);
+            const uint32_t bv = (pp & 1) ? (hi & 0xffff0000u) : (hi << 16);
+            o[pp] = av | bv;
+        }
     }
-    a.sx[static_cast<size_t>(tok) * chunks + c] = sum;
-    (void)HPW;
+    a.xf[item] = o;
+    (void)PPC;
 }
 
 // Many-token backbone (4-bit codes, T >= 8): the contraction has enough
-// columns to use MFMA.  One workgroup per 16-row tile of one linear; its four
-// waves split the row's 128-code blocks (wave w takes blocks w, w + 4, ...),
-// four blocks per wave in flight.  Per block a lane loads 16 bytes of codes of
-// row r = lane % 16 (32 codes of one quantization group), dequantizes them in
-// registers to fp16 s (q - z) (one rounding) and feeds four
-// v_mfma_f32_16x16x32_f16 with up to 16 tokens
-// of the prepared activations (the prep kernel's pair order is the unpack's
-// order).  The rank-r term is extra MFMA steps over [B | t] spread over the
-// waves (t from the K-part partials of decode_prep_mfma_kernel, summed in a
-// fixed order and rounded to fp16); the waves' tiles are summed through LDS
-// in a fixed order; one rounding to the output dtype.
+// columns to use MFMA.  One workgroup per TPW 16-row tiles of one linear; its
+// four waves split the 128-code blocks of K (wave w takes blocks w, w + 4,
+// ...), NBUF blocks per wave in flight.  Per block a lane loads, for each of
+// its TPW tiles, 16 bytes of codes of row r = lane % 16 (32 codes of one
+// quantization group), and once for all tiles the matching activations of
+// token r (four 16-byte loads from the word-major layout, 256 contiguous
+// bytes per lane group); the codes are dequantized in registers to fp16
+// s (q - z) (one rounding) and feed four v_mfma_f32_16x16x32_f16 per tile.
+// The rank-r term is extra MFMA steps over [B | t] spread over the waves (t
+// from the K-part partials of decode_prep_mfma_kernel, summed in a fixed
+// order and rounded to fp16); the waves' tiles are summed through LDS in a
+// fixed order; one rounding to the output dtype.
+template <int TPW, int NBUF>
 __global__ __launch_bounds__(256) void decode_mfma_kernel(DecodeArgs a) {
-    __shared__ f32x4 red[4][64];
+    __shared__ f32x4 red[4][TPW][64];
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int g = lane >> 4, r = lane & 15;
-    // workgroup -> (linear, 16-row tile); batch_end counts tiles here
+    // workgroup -> (linear, TPW tiles of 16 rows); batch_end counts workgroups
     int li = 0;
     while (static_cast<int>(blockIdx.x) >= a.lin[li].batch_end) ++li;
     const Lin& L = a.lin[li];
-    const int row0 = (blockIdx.x - (li ? a.lin[li - 1].batch_end : 0)) * 16;
-    const int row = row0 + r < L.d_out ? row0 + r : L.d_out - 1;
-    const bool rowv = row0 + r < L.d_out;
+    const int row0 = (blockIdx.x - (li ? a.lin[li - 1].batch_end : 0)) * 16 * TPW;
+    int row[TPW];
+    bool rowv[TPW];
+#pragma unroll
+    for (int j = 0; j < TPW; ++j) {
+        rowv[j] = row0 + 16 * j + r < L.d_out;
+        row[j] = rowv[j] ? row0 + 16 * j + r : L.d_out - 1;
+    }
     const int tok = a.tok0 + r;                    // this lane's token column of the B operand
     const bool tokv = tok < a.T;
     const int K = a.d_in;
@@ -567,11 +590,12 @@ __global__ __launch_bounds__(256) void decode_mfma_kernel(DecodeArgs a) {
     const uint32_t mlo = __builtin_amdgcn_readfirstlane(0x000F000Fu);
     const uint32_t mhi = __builtin_amdgcn_readfirstlane(0x00F000F0u);
     const uint32_t bias = 0x64006400u;
-    const u32x4* xrow = reinterpret_cast<const u32x4*>(a.xp + static_cast<size_t>(tokv ? tok : 0) * (K / 2));
+    // this pass's activations; absent tokens were written as zero
+    const u32x4* xf = a.xf + static_cast<size_t>(a.tok0 / 16) * words_row * 16 + r;
 
     struct Blk {
-        u32x4 w;
-        uint32_t s, z;
+        u32x4 w[TPW];
+        uint32_t s[TPW], z[TPW];
         u32x4 x[4];
     };
     // rank-r term, 32 factor columns per step, wave w taking steps w, w + 4:
@@ -579,25 +603,30 @@ __global__ __launch_bounds__(256) void decode_mfma_kernel(DecodeArgs a) {
     // the K-part partials in order, rounded to fp16.  The first step's
     // operands are loaded before the K loop, so their latency is hidden.
     const bool bvec = (L.r_max & 7) == 0 && (reinterpret_cast<uintptr_t>(L.B) & 15) == 0;
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    f32x4 acc[TPW];
+#pragma unroll
+    for (int j = 0; j < TPW; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
     struct RankOp {
-        uint32_t bw[4];
+        uint32_t bw[TPW][4];
         f32x4 tp[kMaxKp][2];
     };
     auto rank_load = [&](int kr, RankOp& o) {
         const int k = kr + 8 * g;
         if (kr >= L.rank) return;
-        const uint16_t* brow = L.B + static_cast<size_t>(row) * L.r_max;
-        if (bvec && k + 8 <= L.r_max) {
-            const u32x4 v = *reinterpret_cast<const u32x4*>(brow + k);
 #pragma unroll
-            for (int e = 0; e < 4; ++e) { const uint32_t ve = v[e]; o.bw[e] = ve; }
-        } else {
+        for (int j = 0; j < TPW; ++j) {
+            const uint16_t* brow = L.B + static_cast<size_t>(row[j]) * L.r_max;
+            if (bvec && k + 8 <= L.r_max) {
+                const u32x4 v = *reinterpret_cast<const u32x4*>(brow + k);
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const uint32_t lo = k + 2 * e < L.r_max ? brow[k + 2 * e] : 0u;
-                const uint32_t hi = k + 2 * e + 1 < L.r_max ? brow[k + 2 * e + 1] : 0u;
-                o.bw[e] = lo | (hi << 16);
+                for (int e = 0; e < 4; ++e) { const uint32_t ve = v[e]; o.bw[j][e] = ve; }
+            } else {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const uint32_t lo = k + 2 * e < L.r_max ? brow[k + 2 * e] : 0u;
+                    const uint32_t hi = k + 2 * e + 1 < L.r_max ? brow[k + 2 * e + 1] : 0u;
+                    o.bw[j][e] = lo | (hi << 16);
+                }
             }
         }
         const int tk = tokv ? tok : 0;
@@ -619,18 +648,24 @@ __global__ __launch_bounds__(256) void decode_mfma_kernel(DecodeArgs a) {
 #pragma unroll
             for (int e = 0; e < 4; ++e) { tsum[e] += o.tp[p][0][e]; tsum[4 + e] += o.tp[p][1][e]; }
         }
-        uint32_t aw[4], tw[4];
+        uint32_t tw[4];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            // entries past the rank (or past the matrix) and absent tokens are zero
-            const uint32_t lo = (rowv && k + 2 * e < L.rank) ? (o.bw[e] & 0xffffu) : 0u;
-            const uint32_t hi = (rowv && k + 2 * e + 1 < L.rank) ? (o.bw[e] >> 16) : 0u;
-            aw[e] = lo | (hi << 16);
+        for (int e = 0; e < 4; ++e)
             tw[e] = tokv ? (static_cast<uint32_t>(f32_to_f16_bits(tsum[2 * e])) |
                             (static_cast<uint32_t>(f32_to_f16_bits(tsum[2 * e + 1])) << 16))
                          : 0u;
+#pragma unroll
+        for (int j = 0; j < TPW; ++j) {
+            uint32_t aw[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                // entries past the rank (or past the matrix) and absent tokens are zero
+                const uint32_t lo = (rowv[j] && k + 2 * e < L.rank) ? (o.bw[j][e] & 0xffffu) : 0u;
+                const uint32_t hi = (rowv[j] && k + 2 * e + 1 < L.rank) ? (o.bw[j][e] >> 16) : 0u;
+                aw[e] = lo | (hi << 16);
+            }
+            acc[j] = mfma(u32x4{aw[0], aw[1], aw[2], aw[3]}, u32x4{tw[0], tw[1], tw[2], tw[3]}, acc[j]);
         }
-        acc = mfma(u32x4{aw[0], aw[1], aw[2], aw[3]}, u32x4{tw[0], tw[1], tw[2], tw[3]}, acc);
     };
     RankOp rb;
     rank_load(32 * wave, rb);
@@ -641,34 +676,43 @@ __global__ __launch_bounds__(256) void decode_mfma_kernel(DecodeArgs a) {
     auto load = [&](int kb, Blk& b) {
         const int kc = kb * 128 + 32 * g;          // first of this lane's 32 codes
         const int wi = kc < K ? kc / 8 : 0;
-        b.w = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(L.q + static_cast<size_t>(row) * words_row + wi));
-        const size_t gi = static_cast<size_t>(row) * groups + (kc < K ? kc / a.G : 0);
-        b.s = L.s[gi];
-        b.z = L.z[gi];
+        const int gs = kc < K ? kc / a.G : 0;
 #pragma unroll
-        for (int t = 0; t < 4; ++t) b.x[t] = xrow[wi + t];
+        for (int j = 0; j < TPW; ++j) {
+            b.w[j] = __builtin_nontemporal_load(
+                reinterpret_cast<const u32x4*>(L.q + static_cast<size_t>(row[j]) * words_row + wi));
+            const size_t gi = static_cast<size_t>(row[j]) * groups + gs;
+            b.s[j] = L.s[gi];
+            b.z[j] = L.z[gi];
+        }
+#pragma unroll
+        for (int t = 0; t < 4; ++t) b.x[t] = xf[static_cast<size_t>(wi + t) * 16];
     };
     auto compute = [&](int kb, const Blk& b) {
         // past K, past the matrix or a padding block: scale 0, the weight is 0
-        const bool on = rowv && kb < nkb && kb * 128 + 32 * g < K;
-        const Dq dq = make_dq(on ? b.s : 0u, b.z);
-        const u32x4 zero = {0, 0, 0, 0};
+        const bool on = kb < nkb && kb * 128 + 32 * g < K;
 #pragma unroll
-        for (int t = 0; t < 4; ++t) acc = mfma(dequant_word4x(b.w[t], dq, mlo, mhi, bias), tokv ? b.x[t] : zero, acc);
+        for (int j = 0; j < TPW; ++j) {
+            const Dq dq = make_dq((on && rowv[j]) ? b.s[j] : 0u, b.z[j]);
+#pragma unroll
+            for (int t = 0; t < 4; ++t) acc[j] = mfma(dequant_word4x(b.w[j][t], dq, mlo, mhi, bias), b.x[t], acc[j]);
+        }
     };
-    // blocks of this wave: kb = wave + 4 i, four in flight.  Rounds of four:
-    // block j of a round is computed, then its registers take block j + 4
-    // (past the last block they reload the current one, already cached).
-    const int rounds = (nkb + 15) / 16;
-    Blk b[4];
+    // blocks of this wave: kb = wave + 4 i, NBUF in flight.  Rounds of NBUF:
+    // block j of a round is computed, then its registers take block
+    // j + NBUF (past the last block they reload the current one, already
+    // cached).
+    constexpr int SPAN = 4 * NBUF;                 // blocks per round over the four waves
+    const int rounds = (nkb + SPAN - 1) / SPAN;
+    Blk b[NBUF];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) load(wave + 4 * j < nkb ? wave + 4 * j : 0, b[j]);
+    for (int j = 0; j < NBUF; ++j) load(wave + 4 * j < nkb ? wave + 4 * j : 0, b[j]);
     for (int rd = 0; rd < rounds; ++rd) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int kb = wave + 16 * rd + 4 * j;
+        for (int j = 0; j < NBUF; ++j) {
+            const int kb = wave + SPAN * rd + 4 * j;
             compute(kb, b[j]);
-            const int kn = kb + 16;
+            const int kn = kb + SPAN;
             load(kn < nkb ? kn : (kb < nkb ? kb : 0), b[j]);
         }
     }
@@ -679,16 +723,21 @@ __global__ __launch_bounds__(256) void decode_mfma_kernel(DecodeArgs a) {
         rank_load(kr, ro);
         rank_mma(kr, ro);
     }
-    red[wave][lane] = acc;
+#pragma unroll
+    for (int j = 0; j < TPW; ++j) red[wave][j][lane] = acc[j];
     __syncthreads();
-    if (wave != 0) return;
-    acc = red[0][lane] + red[1][lane] + red[2][lane] + red[3][lane];
-    // acc[e] = y[tok0 + r][row0 + 4 g + e]
+    // wave w sums and stores tiles w, w + 4, ... in a fixed order
     if (!tokv) return;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-        const int rr = row0 + 4 * g + e;
-        if (rr < L.d_out) store_out(L.y, static_cast<size_t>(tok) * L.d_out + rr, acc[e], a.out);
+    for (int j = 0; j < TPW; ++j) {
+        if (j % 4 != wave) continue;
+        const f32x4 v = red[0][j][lane] + red[1][j][lane] + red[2][j][lane] + red[3][j][lane];
+        // v[e] = y[tok][row0 + 16 j + 4 g + e]
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int rr = row0 + 16 * j + 4 * g + e;
+            if (rr < L.d_out) store_out(L.y, static_cast<size_t>(tok) * L.d_out + rr, v[e], a.out);
+        }
     }
 }
 
@@ -810,6 +859,7 @@ size_t decode_workspace_bytes(int n, const QW* w, const LR* c, int T) {
     for (int i = 0; i < n; ++i)
         total += mf ? up256(static_cast<size_t>(kp) * T * pad32(c[i].rank) * sizeof(float))
                     : up256(static_cast<size_t>(c[i].rank) * T * sizeof(float));
+    if (mf) return total + up256(static_cast<size_t>((T + 15) / 16) * 16 * w[0].d_in * 2);
     const size_t chunks = static_cast<size_t>(w[0].d_in) / (32 / w[0].bits) / 4;
     total += up256(static_cast<size_t>(T) * w[0].d_in * 2);
     total += up256(static_cast<size_t>(T) * chunks * sizeof(float));
@@ -830,10 +880,17 @@ hipError_t launch_decode_mfma(int n, const QW* w, const LR* c, const void* x, in
     const int d_in = w[0].d_in;
     const MfmaPlan mp = mfma_plan(d_in);
     char* wsb = static_cast<char*>(ws);
-    PrepMArgs pa;
-    DecodeArgs a;
+    PrepMArgs pa{};
+    DecodeArgs a{};
     size_t off = 0;
-    int tile_end = 0, rtiles = 0;
+    // row tiles per wave: four share each activation load (a quarter of the
+    // activation traffic from L2: the gate+up window at 16 tokens went from
+    // 45 us with one tile to ~34 us); small windows keep one tile per wave
+    // for enough workgroups
+    int tiles = 0;
+    for (int i = 0; i < n; ++i) tiles += (w[i].d_out + 15) / 16;
+    const int tpw = tiles >= 1024 ? 4 : 1;
+    int wg_end = 0, rtiles = 0;
     for (int i = 0; i < n; ++i) {
         float* tp = reinterpret_cast<float*>(wsb + off);
         const int rp = pad32(c[i].rank);
@@ -842,31 +899,28 @@ hipError_t launch_decode_mfma(int n, const QW* w, const LR* c, const void* x, in
         pa.tp[i] = tp;
         pa.rank[i] = c[i].rank;
         pa.rpad[i] = rp;
-        rtiles += rp / 16 * mp.kp;
+        rtiles += rp / 16 * ((T + 15) / 16) * mp.kp;
         pa.tile_end[i] = rtiles;
-        tile_end += (w[i].d_out + 15) / 16;
-        a.lin[i] = Lin{w[i].q, w[i].s, w[i].z, c[i].B, y[i], tp, w[i].d_out, c[i].rank, c[i].r_max, tile_end, rp};
+        wg_end += ((w[i].d_out + 15) / 16 + tpw - 1) / tpw;
+        a.lin[i] = Lin{w[i].q, w[i].s, w[i].z, c[i].B, y[i], tp, w[i].d_out, c[i].rank, c[i].r_max, wg_end, rp};
     }
-    const int chunks = d_in / 8 / 4;
-    f16x2* xp = reinterpret_cast<f16x2*>(wsb + off);
-    off += up256(static_cast<size_t>(T) * d_in * 2);
-    float* sx = reinterpret_cast<float*>(wsb + off);
+    const int npass = (T + 15) / 16;
+    u32x4* xf = reinterpret_cast<u32x4*>(wsb + off);
     pa.n = n;
     pa.x = static_cast<const uint16_t*>(x);
-    pa.xp = xp;
-    pa.sx = sx;
+    pa.xf = xf;
     pa.d_in = d_in;
     pa.T = T;
     pa.act = act;
     pa.kp = mp.kp;
     pa.spw = mp.spw;
-    const long long items = static_cast<long long>(T) * chunks;
+    pa.npass = npass;
+    const long long items = static_cast<long long>(npass) * (d_in / 8) * 16;
     const unsigned grid = static_cast<unsigned>(rtiles + (items + 255) / 256);
     hipLaunchKernelGGL(decode_prep_mfma_kernel, dim3(grid), dim3(256), 0, st, pa);
     hipError_t e = hipGetLastError();
     a.n = n;
-    a.xp = xp;
-    a.sx = sx;
+    a.xf = xf;
     a.d_in = d_in;
     a.G = w[0].G;
     a.T = T;
@@ -874,9 +928,10 @@ hipError_t launch_decode_mfma(int n, const QW* w, const LR* c, const void* x, in
     a.ks = 4;
     a.cps = 0;
     a.kp = mp.kp;
+    auto kern = tpw == 4 ? decode_mfma_kernel<4, 2> : decode_mfma_kernel<1, 4>;
     for (int tok0 = 0; tok0 < T && e == hipSuccess; tok0 += 16) {
         a.tok0 = tok0;
-        hipLaunchKernelGGL(decode_mfma_kernel, dim3(tile_end), dim3(256), 0, st, a);
+        hipLaunchKernelGGL(kern, dim3(wg_end), dim3(256), 0, st, a);
         e = hipGetLastError();
     }
     return e;

@@ -115,6 +115,33 @@ def test_llama_layer_full_size_sampled_rows(mat, T):
     assert rel_l2(out_to_numpy(y)[:, rows], ref) <= REL_L2_TOL
 
 
+@pytest.mark.parametrize("T", [9, 16, 40])
+def test_gate_up_window_many_tokens_sampled_rows(T):
+    """The gate and up projections as one window (1792 row tiles: the MFMA
+    backbone's four-tiles-per-wave form) for 9, 16 and 40 tokens (one to
+    three passes of 16): equal to the single calls (one tile per wave) bit
+    for bit, and to the oracle on sampled rows."""
+    layer = wl.llama_layer()
+    ws_, cs, host = [], [], []
+    for m in (4, 5):
+        spec = layer.linears[m]
+        W = wl.weight((spec.d_out, spec.d_in), layer.index, 0, m)
+        ws_.append(cl.quantize_pack(torch.from_numpy(W).cuda(), 4, 128))
+        A, B = wl.standin_factors(spec.d_out, spec.d_in, spec.r_max, layer.index, 0, m)
+        cs.append(cl.LowRank(dev_f16(A), dev_f16(B), spec.r_max, spec.rank))
+        host.append((W, A, B, spec.rank))
+    x = wl.activation((T, 4096), layer.index, 0, 4)
+    xd = dev_u16(x.bits, torch.float16)
+    ys = cl.linear_decode_window(ws_, cs, xd, out_dtype=torch.float32)
+    for i, (W, A, B, rank) in enumerate(host):
+        y1 = cl.linear_decode(ws_[i], cs[i], xd, out_dtype=torch.float32)
+        assert torch.equal(ys[i], y1), i
+        rows = np.r_[0:4, np.random.default_rng(70 + i).choice(14336, 60, replace=False), 14332:14336]
+        Q, s, z = quant.quantize_pack(W[rows], 4, 128)
+        ref = linear.forward_packed(Q, s, z, 4, 128, A, B[rows], rank, x.values)
+        assert rel_l2(out_to_numpy(ys[i])[:, rows], ref) <= REL_L2_TOL
+
+
 def test_2bit_gate_rank_sweep_sampled_rows():
     layer = wl.llama_layer_2bit()
     W = wl.weight((14336, 4096), layer.index, 0, 4)
