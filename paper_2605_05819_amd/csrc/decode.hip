@@ -566,6 +566,7 @@ __global__ __launch_bounds__(256) void decode_prep_mfma_kernel(PrepMArgs a) {
 template <int TPW, int NBUF>
 __global__ __launch_bounds__(256) void decode_mfma_kernel(DecodeArgs a) {
     __shared__ f32x4 red[4][TPW][64];
+    extern __shared__ uint16_t szl[];             // [2][16 TPW][groups]: the rows' scales, then zeros
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int g = lane >> 4, r = lane & 15;
@@ -592,10 +593,31 @@ __global__ __launch_bounds__(256) void decode_mfma_kernel(DecodeArgs a) {
     const uint32_t bias = 0x64006400u;
     // this pass's activations; absent tokens were written as zero
     const u32x4* xf = a.xf + static_cast<size_t>(a.tok0 / 16) * words_row * 16 + r;
+    // the workgroup's scales and zeros into LDS (rows are consecutive, so
+    // each array's part is one contiguous run starting 16-byte aligned, as
+    // row0 is a multiple of 16): whole 16-byte pieces, then the last few
+    // values of a partial last tile one by one; rows past the matrix are not
+    // loaded and never used
+    {
+        const int nrows = min(16 * TPW, L.d_out - row0);
+        const int nval = nrows * groups;
+        const int n16 = nval / 8;
+        const uint16_t* ssrc = L.s + static_cast<size_t>(row0) * groups;
+        const uint16_t* zsrc = L.z + static_cast<size_t>(row0) * groups;
+        uint16_t* zl = szl + 16 * TPW * groups;
+        for (int i = threadIdx.x; i < n16; i += 256) {
+            reinterpret_cast<u32x4*>(szl)[i] = reinterpret_cast<const u32x4*>(ssrc)[i];
+            reinterpret_cast<u32x4*>(zl)[i] = reinterpret_cast<const u32x4*>(zsrc)[i];
+        }
+        for (int i = 8 * n16 + static_cast<int>(threadIdx.x); i < nval; i += 256) {
+            szl[i] = ssrc[i];
+            zl[i] = zsrc[i];
+        }
+        __syncthreads();
+    }
 
     struct Blk {
         u32x4 w[TPW];
-        uint32_t s[TPW], z[TPW];
         u32x4 x[4];
     };
     // rank-r term, 32 factor columns per step, wave w taking steps w, w + 4:
@@ -676,24 +698,23 @@ __global__ __launch_bounds__(256) void decode_mfma_kernel(DecodeArgs a) {
     auto load = [&](int kb, Blk& b) {
         const int kc = kb * 128 + 32 * g;          // first of this lane's 32 codes
         const int wi = kc < K ? kc / 8 : 0;
-        const int gs = kc < K ? kc / a.G : 0;
 #pragma unroll
-        for (int j = 0; j < TPW; ++j) {
+        for (int j = 0; j < TPW; ++j)
             b.w[j] = __builtin_nontemporal_load(
                 reinterpret_cast<const u32x4*>(L.q + static_cast<size_t>(row[j]) * words_row + wi));
-            const size_t gi = static_cast<size_t>(row[j]) * groups + gs;
-            b.s[j] = L.s[gi];
-            b.z[j] = L.z[gi];
-        }
 #pragma unroll
         for (int t = 0; t < 4; ++t) b.x[t] = xf[static_cast<size_t>(wi + t) * 16];
     };
     auto compute = [&](int kb, const Blk& b) {
         // past K, past the matrix or a padding block: scale 0, the weight is 0
-        const bool on = kb < nkb && kb * 128 + 32 * g < K;
+        const int kc = kb * 128 + 32 * g;
+        const bool on = kb < nkb && kc < K;
+        const int gs = on ? kc / a.G : 0;
 #pragma unroll
         for (int j = 0; j < TPW; ++j) {
-            const Dq dq = make_dq((on && rowv[j]) ? b.s[j] : 0u, b.z[j]);
+            const int lr = (16 * j + r) * groups + gs;
+            const uint32_t sb = szl[lr], zb = szl[16 * TPW * groups + lr];
+            const Dq dq = make_dq((on && rowv[j]) ? sb : 0u, zb);
 #pragma unroll
             for (int t = 0; t < 4; ++t) acc[j] = mfma(dequant_word4x(b.w[j][t], dq, mlo, mhi, bias), b.x[t], acc[j]);
         }
@@ -833,7 +854,9 @@ size_t up256(size_t n) { return (n + 255) / 256 * 256; }
 
 namespace {
 
-bool use_mfma(int bits, int T) { return bits == 4 && T >= kMfmaMinTokens; }
+// 4-bit codes, enough tokens, and at most 512 quantization groups per row
+// (the MFMA backbone keeps its rows' scales and zeros in LDS)
+bool use_mfma(const QW& w, int T) { return w.bits == 4 && T >= kMfmaMinTokens && w.d_in / w.G <= 512; }
 
 // K parts of the MFMA preparation (at most 4, about 1024 codes each) and the
 // 32-code steps each of a part's four waves takes
@@ -854,7 +877,7 @@ int pad32(int r) { return (r + 31) / 32 * 32; }
 
 size_t decode_workspace_bytes(int n, const QW* w, const LR* c, int T) {
     size_t total = 0;
-    const bool mf = use_mfma(w[0].bits, T);
+    const bool mf = use_mfma(w[0], T);
     const int kp = mf ? mfma_plan(w[0].d_in).kp : 0;
     for (int i = 0; i < n; ++i)
         total += mf ? up256(static_cast<size_t>(kp) * T * pad32(c[i].rank) * sizeof(float))
@@ -889,7 +912,9 @@ hipError_t launch_decode_mfma(int n, const QW* w, const LR* c, const void* x, in
     // for enough workgroups
     int tiles = 0;
     for (int i = 0; i < n; ++i) tiles += (w[i].d_out + 15) / 16;
-    const int tpw = tiles >= 1024 ? 4 : 1;
+    const int groups = d_in / w[0].G;
+    // four tiles per wave when the workgroup's scales and zeros fit 32 KB of LDS
+    const int tpw = tiles >= 1024 && 2 * 64 * groups * 2 <= 32768 ? 4 : 1;
     int wg_end = 0, rtiles = 0;
     for (int i = 0; i < n; ++i) {
         float* tp = reinterpret_cast<float*>(wsb + off);
@@ -929,9 +954,10 @@ hipError_t launch_decode_mfma(int n, const QW* w, const LR* c, const void* x, in
     a.cps = 0;
     a.kp = mp.kp;
     auto kern = tpw == 4 ? decode_mfma_kernel<4, 2> : decode_mfma_kernel<1, 4>;
+    const size_t lds = static_cast<size_t>(2) * 16 * tpw * groups * 2;
     for (int tok0 = 0; tok0 < T && e == hipSuccess; tok0 += 16) {
         a.tok0 = tok0;
-        hipLaunchKernelGGL(kern, dim3(wg_end), dim3(256), 0, st, a);
+        hipLaunchKernelGGL(kern, dim3(wg_end), dim3(256), lds, st, a);
         e = hipGetLastError();
     }
     return e;
@@ -943,7 +969,7 @@ hipError_t launch_linear_decode(int n, const QW* w, const LR* c, const void* x, 
                                 void* const* y, int out, void* ws, hipStream_t st) {
     const int d_in = w[0].d_in, bits = w[0].bits;
     if (n < 1 || n > kMaxWin) return hipErrorInvalidConfiguration;
-    if (use_mfma(bits, T)) return launch_decode_mfma(n, w, c, x, T, act, y, out, ws, st);
+    if (use_mfma(w[0], T)) return launch_decode_mfma(n, w, c, x, T, act, y, out, ws, st);
     int max_rank = 0;
     for (int i = 0; i < n; ++i) max_rank = max(max_rank, c[i].rank);
     const Plan p = plan(d_in, bits, max_rank, T);
