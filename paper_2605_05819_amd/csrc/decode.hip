@@ -55,7 +55,10 @@ namespace {
 
 constexpr int kMaxWin = 8;   // linears per window
 constexpr int kMaxKp = 4;    // K parts of the many-token A x partials
-constexpr int kMfmaMinTokens = 8;   // 4-bit windows with this many tokens use the MFMA backbone
+// 4-bit windows with this many tokens use the MFMA backbone (measured on the
+// Llama-8B layer: 2 tokens 72 us on the dot2 backbone against 88 us on MFMA,
+// 3 tokens 123 against 88, 5-7 tokens ~185 against ~90)
+constexpr int kMfmaMinTokens = 3;
 
 // One linear of a window, as the backbone kernel sees it.
 struct Lin {
@@ -550,8 +553,8 @@ __global__ __launch_bounds__(256) void decode_prep_mfma_kernel(PrepMArgs a) {
     (void)PPC;
 }
 
-// Many-token backbone (4-bit codes, T >= 8): the contraction has enough
-// columns to use MFMA.  One workgroup per TPW 16-row tiles of one linear; its
+// Many-token backbone (4-bit codes, T >= 3): the contraction has enough
+// columns to use MFMA (tokens padded to 16).  One workgroup per TPW 16-row tiles of one linear; its
 // four waves split the 128-code blocks of K (wave w takes blocks w, w + 4,
 // ...), NBUF blocks per wave in flight.  Per block a lane loads, for each of
 // its TPW tiles, 16 bytes of codes of row r = lane % 16 (32 codes of one
