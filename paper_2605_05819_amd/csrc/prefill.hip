@@ -21,7 +21,10 @@
 //     so one scale and zero per lane) and dequantizes them per MFMA step as
 //     s * (q - z) in fp16 ((q | 0x6400) - (1024 + z) is exact, one rounding
 //     for the scale).  No weight tile goes through LDS and no wave repeats
-//     another's dequantization.  The rank-r correction is extra MFMA steps
+//     another's dequantization.  The workgroup's scales and zeros do go
+//     through LDS, in double-buffered windows of 8 groups per row (one
+//     16-byte load per thread and array per window): per-lane 2-byte
+//     gathers had cost 13 % of the kernel's time.  The rank-r correction is extra MFMA steps
 //     over [T | B] (read from global memory) into the same accumulators.
 //  Workgroups are numbered so that the N tiles of one 128-token block run on
 //  one XCD (workgroup i runs on XCD i mod 8) and share its L2 copy of X'.
@@ -214,7 +217,6 @@ __device__ __forceinline__ int xswz(int r) { return ((r >> 1) & 3) | ((r & 1) <<
 template <int BITS>
 struct WStep {
     uint32_t w[BITS];        // 4-bit: 4 words, 2-bit: 2 words
-    uint32_t s, z;           // fp16 bits, zero-extended by the load
 };
 
 template <int BITS>
@@ -222,6 +224,9 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
     // two stages of X': [BM rows][16 chunks of 8 k], chunk c of row r stored
     // at slot c ^ xswz(r & 15)
     __shared__ u32x4 xs[2][BM * 16];
+    // scales and zeros of the workgroup's BN rows, windows of 8 consecutive
+    // groups, double-buffered: [buffer][scale, zero][row][8]
+    __shared__ uint16_t szw[2][2][BN][8];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -252,11 +257,36 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
             __builtin_amdgcn_global_load_lds(a.Xp + off, &xs[st][blk * 64], 16, 0, 0);
         }
     };
+    // scales and zeros, window wnd (groups 8 wnd .. 8 wnd + 7) of the
+    // workgroup's rows into buffer wnd % 2: thread tid takes row nb BN + tid
+    // (one 16-byte load per array when the rows are 16-byte aligned)
+    const bool sz16 = groups % 8 == 0 && (reinterpret_cast<uintptr_t>(a.s) & 15) == 0 &&
+                      (reinterpret_cast<uintptr_t>(a.z) & 15) == 0;
+    auto load_sz = [&](int wnd) {
+        const int n = nb * BN + tid;
+        const int nc = n < a.N ? n : a.N - 1;
+        const unsigned base = static_cast<unsigned>(nc) * static_cast<unsigned>(groups) + 8u * wnd;
+        uint16_t* ds = szw[wnd & 1][0][tid];
+        uint16_t* dz = szw[wnd & 1][1][tid];
+        if (sz16 && 8 * wnd + 8 <= groups) {
+            *reinterpret_cast<u32x4*>(ds) = *reinterpret_cast<const u32x4*>(a.s + base);
+            *reinterpret_cast<u32x4*>(dz) = *reinterpret_cast<const u32x4*>(a.z + base);
+        } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const bool v = 8 * wnd + e < groups;
+                ds[e] = v ? a.s[base + e] : 0;
+                dz[e] = v ? a.z[base + e] : 0;
+            }
+        }
+    };
+    // K steps per window of 8 groups (G / 16 >= 2: G is a multiple of 128 / bits)
+    const int spw = a.G / 16;
+
     // this lane's codes of K step kb for its four weight rows
     auto load_w = [&](int kb, WStep<BITS> (&ws)[4]) {
         const int kc = kb * BK + 32 * g;                   // first code of this lane's 32
         const bool kval = kc < a.K;
-        const int gi = kval ? kc / a.G : 0;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const int n = n0 + 16 * j + r;
@@ -274,9 +304,6 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
             }
             // raw loads only: nothing here consumes a loaded value, so the
             // loads stay in flight through the current step's MFMAs
-            const unsigned sgi = static_cast<unsigned>(nc) * static_cast<unsigned>(groups) + static_cast<unsigned>(gi);
-            ws[j].s = a.s[sgi];
-            ws[j].z = a.z[sgi];
         }
     };
 
@@ -297,15 +324,19 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
         Dq dq[4];
         f16x2 s2[4], zz[4];
         const bool kval = kb * BK + 32 * g < a.K;
+        const int gi = kval ? (kb * BK + 32 * g) / a.G : 0;
+        const int wb = (gi >> 3) & 1, we = gi & 7;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             // past K or N the scale is 0: q - z is finite, so the weight is 0
-            const uint32_t sb = (kval && n0 + 16 * j + r < a.N) ? ws[j].s : 0u;
+            const int nl = wave * 64 + 16 * j + r;
+            const uint32_t zb = szw[wb][1][nl][we];
+            const uint32_t sb = (kval && n0 + 16 * j + r < a.N) ? static_cast<uint32_t>(szw[wb][0][nl][we]) : 0u;
             if constexpr (BITS == 4) {
-                dq[j] = make_dq(sb, ws[j].z);
+                dq[j] = make_dq(sb, zb);
             } else {
                 const f16 sv = __builtin_bit_cast(f16, static_cast<uint16_t>(sb));
-                const f16 zf = static_cast<f16>(1024.0f) + __builtin_bit_cast(f16, static_cast<uint16_t>(ws[j].z));
+                const f16 zf = static_cast<f16>(1024.0f) + __builtin_bit_cast(f16, static_cast<uint16_t>(zb));
                 s2[j] = f16x2{sv, sv};
                 zz[j] = f16x2{zf, zf};
             }
@@ -328,18 +359,25 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
         }
     };
 
-    // ---- main loop: double-buffered X' stages, next step's codes in registers
+    // ---- main loop: double-buffered X' stages, next step's codes in
+    // registers; the scale/zero window after the current one is loaded at
+    // the first step of each window (its buffer's previous window retired at
+    // the barrier before) and is complete at the barrier after
+    const int nwnd = (groups + 7) / 8;
     WStep<BITS> wa[4], wb[4];
     load_x(0, 0);
     load_w(0, wa);
+    load_sz(0);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     for (int kb = 0; kb < nk; kb += 2) {
+        if (kb % spw == 0 && kb / spw + 1 < nwnd) load_sz(kb / spw + 1);
         if (kb + 1 < nk) { load_x(kb + 1, 1); load_w(kb + 1, wb); }
         compute(kb, 0, wa);
         __builtin_amdgcn_s_waitcnt(0);
         __syncthreads();
         if (kb + 1 >= nk) break;
+        if ((kb + 1) % spw == 0 && (kb + 1) / spw + 1 < nwnd) load_sz((kb + 1) / spw + 1);
         if (kb + 2 < nk) { load_x(kb + 2, 0); load_w(kb + 2, wa); }
         compute(kb + 1, 1, wb);
         __builtin_amdgcn_s_waitcnt(0);

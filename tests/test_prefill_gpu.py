@@ -23,8 +23,8 @@ def _layer(d_out, d_in, bits, G, r_max, seed):
     return w, (Q, s, z, A, B)
 
 
-@pytest.mark.parametrize("bits,G", [(4, 128), (2, 64), (4, 64)])
-@pytest.mark.parametrize("M,d_out,d_in", [(37, 300, 256), (256, 128, 512), (300, 1000, 1024)])
+@pytest.mark.parametrize("bits,G", [(4, 128), (2, 64), (4, 64), (4, 32)])
+@pytest.mark.parametrize("M,d_out,d_in", [(37, 300, 256), (256, 128, 512), (300, 1000, 1024), (70, 260, 2560)])
 @pytest.mark.parametrize("rank", [0, 17, 64])
 def test_prefill_ragged_vs_oracle(bits, G, M, d_out, d_in, rank):
     w, (Q, s, z, A, B) = _layer(d_out, d_in, bits, G, 64, M + d_out + rank + bits)
