@@ -28,10 +28,15 @@
 //    row's 16-byte chunks of packed codes are split into KS slices and lane l
 //    of slice k handles chunks k*cps + l + 64j (j < CPL), so every load
 //    instruction reads R fully coalesced segments;
-//  * workgroups loop over batches with the next batch's loads (codes, scales,
-//    zeros, factor entries, A x) in flight during the current batch's
-//    arithmetic, and raw loads only -- nothing consumes a prefetched value
-//    before the compute that needs it;
+//  * one token per pass: each wave holds one batch (codes, scales, zeros,
+//    factor entries, A x) at a time and the chip holds many waves -- the
+//    single-batch kernel needs 72 VGPRs against 120 with a second batch
+//    prefetched, so 7 waves per SIMD stay resident instead of 4, and on
+//    MI355X the gate matrix call went from 13.8 us to 11.9 us; several
+//    tokens per pass at 4 bits keep the next batch's loads in flight during
+//    the current batch's arithmetic, with raw loads only -- nothing consumes
+//    a prefetched value before the compute that needs it; other shapes hold
+//    one batch per wave (a second set would spill to scratch);
 //  * codes are unpacked with one AND per pair straight into fp16 lanes (a
 //    code in the mantissa bits of a zero-exponent fp16 is an exact subnormal)
 //    and multiplied with the prepared activations by v_dot2 into fp32; each
@@ -226,8 +231,12 @@ struct Batch {
 
 // NB: factor columns of B per lane (rank <= NB * 64 * ks); 0 when every
 // linear of the window has rank 0.
+// The one-token 4-bit kernel with at most one factor column per lane fits
+// 72 VGPRs without spills: it is held to that (7 waves per SIMD).
 template <int BITS, int NT, int CPL, int R, int NB>
-__global__ __launch_bounds__(512) void decode_kernel(DecodeArgs a) {
+__global__ __launch_bounds__(512)
+__attribute__((amdgpu_waves_per_eu(BITS == 4 && NT == 1 && CPL == 1 && NB <= 1 ? 7 : 1)))
+void decode_kernel(DecodeArgs a) {
     constexpr int CPW = 32 / BITS;    // codes per word
     constexpr int HPW = CPW / 2;      // fp16 pairs per word
     constexpr int CPC = 4 * CPW;      // codes per chunk
@@ -424,14 +433,27 @@ __global__ __launch_bounds__(512) void decode_kernel(DecodeArgs a) {
         }
     };
 
+    const int stride = gridDim.x;
+    int b = blockIdx.x;
+    if (b >= nbatch) return;
+    // A second register set for the next batch pays where it costs no
+    // spills: two tokens per pass at 4 bits and one chunk per lane (measured
+    // on MI355X: the T = 2 layer 72 us with it, 73 us without).  Everywhere
+    // else a wave holds one batch at a time (alternating LDS buffers).
+    constexpr bool kPrefetch = BITS == 4 && CPL == 1 && NT == 2;
+    if constexpr (!kPrefetch) {
+        for (int it = 0; b < nbatch; b += stride, ++it) {
+            Batch<R, CPL, NBA, NT> bt;
+            load_batch(bt, b);
+            compute_batch(bt, b, it & 1);
+        }
+        return;
+    }
     // Persistent loop over batches with the next batch's loads in flight
     // during the current batch's arithmetic (two register sets, alternating
     // LDS buffers).  Every compute site has a single predecessor shape (next
     // batch issued, or this is the last batch) so the compiler's wait counts
     // let the prefetch stay in flight.
-    const int stride = gridDim.x;
-    int b = blockIdx.x;
-    if (b >= nbatch) return;
     Batch<R, CPL, NBA, NT> b0, b1;
     load_batch(b0, b);
     for (;;) {
