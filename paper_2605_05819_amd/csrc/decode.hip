@@ -115,28 +115,30 @@ struct PrepArgs {
     f16x2* xp;
     float* sx;
     int d_in, T, act;
+    int wpr;                 // waves per row of A (1, 2 or 4)
 };
 
-// One row of A times the activations of tokens tok0 .. tok0 + NTOK - 1, by
-// one wave: lane l takes the 8-element runs starting at 8 l + 512 m in
-// increasing m (eight 16-byte loads of A in flight per lane), adds each
-// run's v_dot2 chain to a float accumulator, and the wave sums its lanes
-// with a butterfly.  Each token's result does not depend on NTOK.
+// Columns [k0, k1) of one row of A times the activations of tokens tok0 ..
+// tok0 + NTOK - 1, by one wave: lane l takes the 8-element runs starting at
+// k0 + 8 l + 512 m in increasing m (eight 16-byte loads of A in flight per
+// lane), adds each run's v_dot2 chain to a float accumulator, and the wave
+// sums its lanes with a butterfly.  Each token's result does not depend on
+// NTOK.  k0 and k1 - k0 are multiples of 8.
 template <int NTOK>
-__device__ __forceinline__ void row_times_x(const uint16_t* ar, const uint16_t* x, int d_in, int tok0, int act,
-                                            float (&out)[NTOK]) {
+__device__ __forceinline__ void row_times_x(const uint16_t* ar, const uint16_t* x, int d_in, int k0, int k1, int tok0,
+                                            int act, float (&out)[NTOK]) {
     constexpr int KB = 8;
     const int lane = threadIdx.x & 63;
     float acc[NTOK];
 #pragma unroll
     for (int tk = 0; tk < NTOK; ++tk) acc[tk] = 0.f;
-    for (int base = 0; base < d_in; base += 64 * 8 * KB) {
+    for (int base = k0; base < k1; base += 64 * 8 * KB) {
         u32x4 av[KB];
         int col[KB];
 #pragma unroll
         for (int k = 0; k < KB; ++k) {
             col[k] = base + (lane + 64 * k) * 8;
-            av[k] = *reinterpret_cast<const u32x4*>(ar + (col[k] < d_in ? col[k] : 0));
+            av[k] = *reinterpret_cast<const u32x4*>(ar + (col[k] < k1 ? col[k] : k0));
         }
 #pragma unroll
         for (int tk = 0; tk < NTOK; ++tk) {
@@ -144,7 +146,7 @@ __device__ __forceinline__ void row_times_x(const uint16_t* ar, const uint16_t* 
 #pragma unroll
             for (int k = 0; k < KB; ++k) {
                 uint32_t xw[4];
-                load8_f16(xr + (col[k] < d_in ? col[k] : 0), act, xw);
+                load8_f16(xr + (col[k] < k1 ? col[k] : k0), act, xw);
                 float d = 0.f;
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
@@ -153,7 +155,7 @@ __device__ __forceinline__ void row_times_x(const uint16_t* ar, const uint16_t* 
                     const uint32_t ak = av[k][e], xk = xw[e];
                     d = dot2(__builtin_bit_cast(f16x2, ak), __builtin_bit_cast(f16x2, xk), d);
                 }
-                acc[tk] += col[k] < d_in ? d : 0.f;
+                acc[tk] += col[k] < k1 ? d : 0.f;
             }
         }
     }
@@ -161,36 +163,59 @@ __device__ __forceinline__ void row_times_x(const uint16_t* ar, const uint16_t* 
     for (int tk = 0; tk < NTOK; ++tk) out[tk] = wave_sum(acc[tk]);
 }
 
-// Preparation kernel: each wave of workgroups [0, ceil(sum of ranks / 4))
-// computes one row i of some linear's A x for every token (tokens in passes
-// of 4, then 2, then 1); the remaining workgroups prepare the activations,
-// one thread per (token, chunk).
+// Preparation kernel.  Workgroups [0, rank_blocks) compute A x: each row i
+// of some linear's A is split over wpr waves (wpr = 1, 2 or 4 by the row
+// length, so a wave issues one round of loads: rows of 14336 took four
+// dependent round trips on one wave), for every token in passes of 4, then 2,
+// then 1 tokens; the wpr partial sums meet in LDS and are added in part
+// order.  The remaining workgroups prepare the activations, one thread per
+// (token, chunk).
 template <int BITS>
 __global__ __launch_bounds__(256) void decode_prep_kernel(PrepArgs a) {
     constexpr int CPW = 32 / BITS, HPW = CPW / 2, PPC = 4 * HPW;
+    __shared__ float part[4][4];
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
     const int tid = threadIdx.x;
     const int d_in = a.d_in, T = a.T;
     const int nrank = a.n > 0 ? a.rank_end[a.n - 1] : 0;
-    const int rank_blocks = (nrank + 3) / 4;
+    const int wpr = a.wpr;
+    const int rows_per_block = 4 / wpr;
+    const int rank_blocks = (nrank + rows_per_block - 1) / rows_per_block;
     const int blk = blockIdx.x;
     if (blk < rank_blocks) {
-        const int j = blk * 4 + wave;
-        if (j >= nrank) return;
+        const int j = blk * rows_per_block + wave / wpr;
+        const int pi = wave % wpr;                       // this wave's part of the row
+        const bool valid = j < nrank;                    // every wave reaches the barriers
+        const int jj = valid ? j : nrank - 1;
         int li = 0;
-        while (j >= a.rank_end[li]) ++li;
-        const int i = j - (li ? a.rank_end[li - 1] : 0);
+        while (jj >= a.rank_end[li]) ++li;
+        const int i = jj - (li ? a.rank_end[li - 1] : 0);
         const int rank = a.rank_end[li] - (li ? a.rank_end[li - 1] : 0);
         const uint16_t* ar = a.A[li] + static_cast<size_t>(i) * d_in;
         float* t = a.t[li];
+        const int kc = (d_in / 8 + wpr - 1) / wpr * 8;   // columns per part, a multiple of 8
+        const int k0 = min(d_in, pi * kc), k1 = min(d_in, k0 + kc);
         auto pass = [&](auto ntok, int tb) {
             constexpr int N = decltype(ntok)::value;
             float v[N];
-            row_times_x<N>(ar, a.x, d_in, tb, a.act, v);
+            row_times_x<N>(ar, a.x, d_in, k0, k1, tb, a.act, v);
+            if (wpr == 1) {
+#pragma unroll
+                for (int tk = 0; tk < N; ++tk)
+                    if (valid && lane == tk) t[static_cast<size_t>(tb + tk) * rank + i] = v[tk];
+                return;
+            }
 #pragma unroll
             for (int tk = 0; tk < N; ++tk)
-                if (lane == tk) t[static_cast<size_t>(tb + tk) * rank + i] = v[tk];
+                if (lane == tk) part[wave][tk] = v[tk];
+            __syncthreads();
+            if (valid && pi == 0 && lane < N) {
+                float sum = 0.f;
+                for (int q = 0; q < wpr; ++q) sum += part[wave + q][lane];
+                t[static_cast<size_t>(tb + lane) * rank + i] = sum;
+            }
+            __syncthreads();
         };
         int tb = 0;
         for (; tb + 4 <= T; tb += 4) pass(std::integral_constant<int, 4>{}, tb);
@@ -871,6 +896,10 @@ hipError_t launch2(const DecodeArgs& a, const Plan& p, hipStream_t st) {
     return launch3<BITS, 4>(a, p, st);
 }
 
+// Waves per row of A in the preparation: one round of eight 16-byte loads
+// per lane covers 4096 columns.
+int prep_waves_per_row(int d_in) { return d_in <= 4096 ? 1 : (d_in <= 8192 ? 2 : 4); }
+
 // Workspace: per linear t_i [T][rank_i] float | xp [T][d_in/2] fp16 pairs |
 // sx [T][chunks] float; every region 256-byte aligned.
 size_t up256(size_t n) { return (n + 255) / 256 * 256; }
@@ -1029,8 +1058,10 @@ hipError_t launch_linear_decode(int n, const QW* w, const LR* c, const void* x, 
     pa.d_in = d_in;
     pa.T = T;
     pa.act = act;
+    pa.wpr = prep_waves_per_row(d_in);
     const long long items = static_cast<long long>(T) * chunks;
-    const unsigned grid = static_cast<unsigned>((rank_end + 3) / 4 + (items + 255) / 256);
+    const int rows_per_block = 4 / pa.wpr;
+    const unsigned grid = static_cast<unsigned>((rank_end + rows_per_block - 1) / rows_per_block + (items + 255) / 256);
     if (bits == 4)
         hipLaunchKernelGGL(decode_prep_kernel<4>, dim3(grid), dim3(256), 0, st, pa);
     else

@@ -58,6 +58,21 @@ def test_ragged_shapes_tokens_and_bits(bits, G, d_out, d_in, T):
     _check(w, c, Q, s, z, A, B, rank, x, torch.float16, torch.float32, bits, G)
 
 
+@pytest.mark.parametrize("bits,G", [(4, 128), (2, 64)])
+@pytest.mark.parametrize("d_in", [5120, 12416])
+@pytest.mark.parametrize("T", [1, 2, 5])
+def test_long_rows_split_preparation(bits, G, d_in, T):
+    """Rows of A longer than 4096 are split over 2 (5120) or 4 (12416) waves
+    in the preparation; the parts meet in LDS."""
+    d_out, r_max, rank = 300, 48, 41
+    W = wl.weight((d_out, d_in), 8, d_out, d_in)
+    Q, s, z = quant.quantize_pack(W, bits, G)
+    A, B = wl.standin_factors(d_out, d_in, r_max, 8, 0, d_out, d_in)
+    w, c = _device_layer(Q, s, z, A, B, d_out, d_in, bits, G, r_max, rank)
+    x = wl.activation((T, d_in), 8, 0, d_out, d_in)
+    _check(w, c, Q, s, z, A, B, rank, x, torch.float16, torch.float32, bits, G)
+
+
 @pytest.mark.parametrize("rank", [0, 1, 17, 64, 128, 256])
 def test_ranks_including_zero_and_max(rank):
     d_out, d_in = 512, 1024
