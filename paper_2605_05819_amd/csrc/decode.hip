@@ -510,17 +510,18 @@ __device__ __forceinline__ u32x4 act8_f16(u32x4 u, int act) {
 // Preparation for the MFMA backbone.  Workgroups [0, tiles): (linear, 16 rows
 // of A, pass of 16 tokens, K part kp): t partial[kp][tok][i] = sum over the
 // part's k of A[i][k] x[tok][k] for the pass's tokens on
-// v_mfma_f32_16x16x32_f16 (A rows as
-// the A operand, tokens as the B operand; four waves split the part, eight
+// v_mfma_f32_16x16x32_f16 (A rows as the A operand, tokens as the B
+// operand; the workgroup's 4, 8 or 16 waves split the part, up to eight
 // 32-code steps of loads in flight per wave; the waves' tiles are summed
 // through LDS in a fixed order).  Rows past the rank are written as zero.
 // The remaining workgroups write the activations in the backbone's operand
 // layout: for each pass of 16 tokens and each 8-code word of K, the 16
 // tokens' 8 activations (16 bytes each, unpack order) side by side, so one
 // load instruction reads 256 contiguous bytes per lane group.
-__global__ __launch_bounds__(256) void decode_prep_mfma_kernel(PrepMArgs a) {
+__global__ __launch_bounds__(1024) void decode_prep_mfma_kernel(PrepMArgs a) {
     constexpr int CPW = 8, HPW = 4, PPC = 16;        // 4-bit codes
-    __shared__ f32x4 red[4][64];
+    __shared__ f32x4 red[16][64];
+    const int nw = blockDim.x >> 6;                  // waves per K part: 4, 8 or 16
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int g = lane >> 4, r = lane & 15;
@@ -542,7 +543,7 @@ __global__ __launch_bounds__(256) void decode_prep_mfma_kernel(PrepMArgs a) {
         const bool tv = tokr < T;
         const uint16_t* xr = a.x + static_cast<size_t>(tv ? tokr : 0) * d_in;
         const int nsteps = d_in / 32;
-        const int s0 = (kp * 4 + wave) * a.spw;
+        const int s0 = (kp * nw + wave) * a.spw;
         const int s1 = min(s0 + a.spw, nsteps);
         f32x4 acc = {0.f, 0.f, 0.f, 0.f};
         for (int sb = s0; sb < s1; sb += 8) {
@@ -565,7 +566,8 @@ __global__ __launch_bounds__(256) void decode_prep_mfma_kernel(PrepMArgs a) {
         red[wave][lane] = acc;
         __syncthreads();
         if (wave != 0 || !tv) return;
-        acc = red[0][lane] + red[1][lane] + red[2][lane] + red[3][lane];
+        acc = red[0][lane];
+        for (int w = 1; w < nw; ++w) acc += red[w][lane];
         // acc[e] = partial t[tok tokr][row tile*16 + 4 g + e]
         float* dst = a.tp[li] + (static_cast<size_t>(kp) * T + tokr) * a.rpad[li] + tile * 16 + 4 * g;
 #pragma unroll
@@ -578,7 +580,7 @@ __global__ __launch_bounds__(256) void decode_prep_mfma_kernel(PrepMArgs a) {
     // tokens are zero
     const int wpr = d_in / CPW;
     const int npass = (T + 15) / 16;
-    const long long item = static_cast<long long>(blk - ntile) * 256 + tid;
+    const long long item = static_cast<long long>(blk - ntile) * blockDim.x + tid;
     if (item >= static_cast<long long>(npass) * wpr * 16) return;
     const int rt = static_cast<int>(item & 15);
     const int wi = static_cast<int>((item >> 4) % wpr);
@@ -912,17 +914,21 @@ namespace {
 // (the MFMA backbone keeps its rows' scales and zeros in LDS)
 bool use_mfma(const QW& w, int T) { return w.bits == 4 && T >= kMfmaMinTokens && w.d_in / w.G <= 512; }
 
-// K parts of the MFMA preparation (at most 4, about 1024 codes each) and the
-// 32-code steps each of a part's four waves takes
+// K parts of the MFMA preparation (at most 4, about 1024 codes each), the
+// waves of a part's workgroup (4, 8 or 16: enough that each wave has at most
+// eight 32-code steps, one round of loads -- the 14336-code rows took four
+// dependent rounds on four waves) and the steps each wave takes
 struct MfmaPlan {
-    int kp, spw;
+    int kp, nw, spw;
 };
 
 MfmaPlan mfma_plan(int d_in) {
     const int nsteps = d_in / 32;
     int kp = (d_in + 1023) / 1024;
     if (kp > kMaxKp) kp = kMaxKp;
-    return MfmaPlan{kp, (nsteps + 4 * kp - 1) / (4 * kp)};
+    int nw = 4;
+    while (nw < 16 && nsteps > nw * kp * 8) nw *= 2;
+    return MfmaPlan{kp, nw, (nsteps + nw * kp - 1) / (nw * kp)};
 }
 
 int pad32(int r) { return (r + 31) / 32 * 32; }
@@ -995,8 +1001,9 @@ hipError_t launch_decode_mfma(int n, const QW* w, const LR* c, const void* x, in
     pa.spw = mp.spw;
     pa.npass = npass;
     const long long items = static_cast<long long>(npass) * (d_in / 8) * 16;
-    const unsigned grid = static_cast<unsigned>(rtiles + (items + 255) / 256);
-    hipLaunchKernelGGL(decode_prep_mfma_kernel, dim3(grid), dim3(256), 0, st, pa);
+    const int pthreads = 64 * mp.nw;
+    const unsigned grid = static_cast<unsigned>(rtiles + (items + pthreads - 1) / pthreads);
+    hipLaunchKernelGGL(decode_prep_mfma_kernel, dim3(grid), dim3(pthreads), 0, st, pa);
     hipError_t e = hipGetLastError();
     a.n = n;
     a.xf = xf;

@@ -76,6 +76,7 @@ __global__ __launch_bounds__(256) void moe_prep_kernel(MoeArgs a) {
     __shared__ int sids[kMaxSlots];
     __shared__ int mys[kMaxSlots];          // this expert's slots, in slot order
     __shared__ int hist[kMaxExperts];       // slots per expert
+    __shared__ int rk[kMaxExperts];         // the experts' ranks, loaded beside the ids
     __shared__ int wsum[4][2];
     __shared__ int wcnt[4];
     __shared__ int sel, sel_lt, sel_n;
@@ -92,7 +93,12 @@ __global__ __launch_bounds__(256) void moe_prep_kernel(MoeArgs a) {
         const int j = blk / a.rq;
         const int quad = blk - j * a.rq;
         // slots per expert (LDS atomics contend only within one expert)
-        for (int i = tid; i < a.E; i += 256) hist[i] = 0;
+        // the ranks are loaded together with the ids: the selected expert's
+        // rank then costs no further memory round trip
+        for (int i = tid; i < a.E; i += 256) {
+            hist[i] = 0;
+            rk[i] = a.r_max > 0 ? a.ranks[i] : 0;     // ranks may be null when r_max is 0
+        }
         if (tid == 0) sel = -1;
         __syncthreads();
         for (int sl = tid; sl < S; sl += 256) {
@@ -149,7 +155,7 @@ __global__ __launch_bounds__(256) void moe_prep_kernel(MoeArgs a) {
         const int e = sel;
         if (e < 0) return;                      // fewer than j + 1 routed experts
         const int ne = sel_n, cnt_lt = sel_lt;
-        int rank = a.r_max > 0 ? a.ranks[e] : 0;     // ranks may be null when r_max is 0
+        int rank = rk[e];
         rank = rank < 0 ? 0 : (rank > a.r_max ? a.r_max : rank);
         if (quad == 0 && tid == 0) {
             a.table[kTab * j + 0] = e;
