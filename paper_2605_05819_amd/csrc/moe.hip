@@ -70,6 +70,21 @@ struct MoeArgs {
     int rq;                  // prep workgroups per expert (4 rank rows each)
 };
 
+// 8 activations (one 16-byte load) as fp16, natural order; bf16 converted.
+__device__ __forceinline__ u32x4 act8_to_f16(u32x4 u, int act) {
+    if (act == DT_FP16) return u;
+    u32x4 o;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const uint32_t uk = u[k];
+        f16x2 h;
+        h.x = act_to_f16(static_cast<uint16_t>(uk & 0xffff), act);
+        h.y = act_to_f16(static_cast<uint16_t>(uk >> 16), act);
+        o[k] = __builtin_bit_cast(uint32_t, h);
+    }
+    return o;
+}
+
 template <int BITS>
 __global__ __launch_bounds__(256) void moe_prep_kernel(MoeArgs a) {
     constexpr int CPW = 32 / BITS, HPW = CPW / 2, PPC = 4 * HPW;
@@ -198,21 +213,35 @@ __global__ __launch_bounds__(256) void moe_prep_kernel(MoeArgs a) {
                 xr[u] = a.x + static_cast<size_t>(xrow) * a.d_in;
             }
             float acc[4] = {0.f, 0.f, 0.f, 0.f};
-            // all of the row's loads in flight for rows up to 2048 codes
-#pragma unroll 4
-            for (int c = lane * 8; c < a.d_in; c += 64 * 8) {
-                const u32x4 av = *reinterpret_cast<const u32x4*>(ar + c);
-                uint32_t xw[4][4];
-#pragma unroll
-                for (int u = 0; u < 4; ++u) load8_f16(xr[u] + c, a.act, xw[u]);
+            // passes of 2048 columns: every load of a pass is issued before
+            // any is used (a conversion branch between the loads had made
+            // each load wait for the one before: ~3 us per call at T = 1)
+            for (int c0 = 0; c0 < a.d_in; c0 += 4 * 512) {
+                u32x4 av[4], xv[4][4];
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
-                    // copy the vector element to a scalar first: a bit_cast
-                    // of a subscripted ext_vector reads element 0
-                    const uint32_t aq = av[q];
+                    const int c = c0 + 512 * q + 8 * lane;
+                    const int cc = c < a.d_in ? c : 0;
+                    av[q] = *reinterpret_cast<const u32x4*>(ar + cc);
 #pragma unroll
-                    for (int u = 0; u < 4; ++u)
-                        acc[u] = dot2(__builtin_bit_cast(f16x2, aq), __builtin_bit_cast(f16x2, xw[u][q]), acc[u]);
+                    for (int u = 0; u < 4; ++u) xv[u][q] = *reinterpret_cast<const u32x4*>(xr[u] + cc);
+                }
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const bool valid = c0 + 512 * q + 8 * lane < a.d_in;
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) {
+                        const u32x4 xw = act8_to_f16(xv[u][q], a.act);
+                        float d = 0.f;
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            // copy the vector elements to scalars first: a
+                            // bit_cast of a subscripted ext_vector reads element 0
+                            const uint32_t ae = av[q][e], xe = xw[e];
+                            d = dot2(__builtin_bit_cast(f16x2, ae), __builtin_bit_cast(f16x2, xe), d);
+                        }
+                        acc[u] += valid ? d : 0.f;
+                    }
                 }
             }
             const float tot = wave_sum_multi<4>(acc);      // lane l: slot j0 + l / 16
