@@ -127,21 +127,45 @@ __global__ __launch_bounds__(256) void xprep_kernel(const uint16_t* __restrict__
     store_xp(Xp, static_cast<size_t>(c) * 8, *reinterpret_cast<const u32x4*>(X + static_cast<size_t>(c) * 8), act);
 }
 
-// T = X A[:r]^T for 16 tokens x 64 factor columns per workgroup; the four
-// waves split K and every wave keeps 8 k-blocks of loads in flight; partial
-// tiles are summed through LDS in a fixed order.  MFMA A operand = X rows,
-// B operand = rows of A.  Output fp16, zero for columns >= rank.  Workgroups
-// of the first column block also write X'.
-__global__ __launch_bounds__(256) void lowrank_t_kernel(const uint16_t* __restrict__ X,
-                                                        const uint16_t* __restrict__ A, uint16_t* __restrict__ T,
-                                                        uint16_t* __restrict__ Xp, int M, int K, int rank,
-                                                        int r_pad, int act) {
+// One launch, two roles.  Workgroups [0, t_blocks): T = X A[:r]^T for 16
+// tokens x 64 factor columns each; the NW waves split K, every wave keeps 8
+// k-blocks of loads in flight, and the partial tiles are summed through LDS
+// in a fixed order.  MFMA A operand = X rows, B operand = rows of A.  Output
+// fp16, zero for columns >= rank.  The remaining workgroups write X' (four
+// 16-byte chunks per thread), so the X' stream runs beside T (X' written by
+// the T workgroups themselves took 27 us for the pair at M = 2048,
+// K = 4096; apart, about 22 us, bound by T's reads of 16 rows x 64 bytes
+// per load instruction: the same bytes read as contiguous 1 KB rows take
+// half the time).
+template <int NW>
+__global__ __launch_bounds__(NW * 64) void lowrank_t_kernel(const uint16_t* __restrict__ X,
+                                                            const uint16_t* __restrict__ A,
+                                                            uint16_t* __restrict__ T, uint16_t* __restrict__ Xp,
+                                                            int M, int K, int rank, int r_pad, int act, int t_blocks,
+                                                            int mtiles, long long chunks) {
     constexpr int U = 8;                               // k blocks of 32 per batch
-    __shared__ f32x4 part[4][4][64];
-    const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
-    const int mtile = blockIdx.x;                      // 16 tokens
-    const int ntile = blockIdx.y;                      // 64 factor columns
+    constexpr int XC = 4;                              // X' chunks per thread
+    __shared__ f32x4 part[NW][4][64];
+    const int tid = threadIdx.x;
+    if (static_cast<int>(blockIdx.x) >= t_blocks) {
+        const long long base = static_cast<long long>(blockIdx.x - t_blocks) * (NW * 64 * XC) + tid;
+        u32x4 v[XC];
+#pragma unroll
+        for (int j = 0; j < XC; ++j) {
+            const long long c = base + static_cast<long long>(j) * NW * 64;
+            v[j] = *reinterpret_cast<const u32x4*>(X + static_cast<size_t>(c < chunks ? c : 0) * 8);
+        }
+#pragma unroll
+        for (int j = 0; j < XC; ++j) {
+            const long long c = base + static_cast<long long>(j) * NW * 64;
+            if (c < chunks) store_xp(Xp, static_cast<size_t>(c) * 8, v[j], act);
+        }
+        return;
+    }
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int mtile = static_cast<int>(blockIdx.x) % mtiles;   // 16 tokens
+    const int ntile = static_cast<int>(blockIdx.x) / mtiles;   // 64 factor columns
     const int m = mtile * 16 + (lane & 15);
     const int kq = 8 * (lane >> 4);                    // this lane's 8 k within a 32 block
     const bool mval = m < M;
@@ -157,8 +181,8 @@ __global__ __launch_bounds__(256) void lowrank_t_kernel(const uint16_t* __restri
         nval[j] = n < rank;
         ar[j] = A + static_cast<size_t>(nval[j] ? n : 0) * K;
     }
-    const int nkb = K / 32;                            // k blocks of 32; this wave takes a quarter
-    const int kbeg = 32 * (wave * nkb / 4), kend = 32 * ((wave + 1) * nkb / 4);
+    const int nkb = K / 32;                            // k blocks of 32; this wave takes 1 / NW
+    const int kbeg = 32 * (wave * nkb / NW), kend = 32 * ((wave + 1) * nkb / NW);
     for (int k0 = kbeg; k0 < kend; k0 += 32 * U) {
         u32x4 xa[U], av[U][4];
 #pragma unroll
@@ -172,9 +196,6 @@ __global__ __launch_bounds__(256) void lowrank_t_kernel(const uint16_t* __restri
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const bool live = k0 + 32 * u < kend;
-            // the first column block of workgroups also writes X' (every
-            // chunk of its 16 rows is loaded by exactly one lane here)
-            if (ntile == 0 && mval && live) store_xp(Xp, static_cast<size_t>(m) * K + k0 + 32 * u + kq, xa[u], act);
             u32x4 x8 = act8_natural(xa[u], act);
             if (!mval || !live) x8 = u32x4{0, 0, 0, 0};
 #pragma unroll
@@ -190,7 +211,10 @@ __global__ __launch_bounds__(256) void lowrank_t_kernel(const uint16_t* __restri
     __syncthreads();
     if (wave != 0) return;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[j] = part[0][j][lane] + part[1][j][lane] + part[2][j][lane] + part[3][j][lane];
+    for (int j = 0; j < 4; ++j) {
+        acc[j] = part[0][j][lane];
+        for (int w = 1; w < NW; ++w) acc[j] += part[w][j][lane];
+    }
     // acc[j][e] = T[mtile*16 + 4*(lane/16) + e][ntile*64 + j*16 + lane%16]
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
@@ -470,8 +494,13 @@ hipError_t launch_linear_prefill(const QW& w, const LR& c, const void* X, int M,
     a.mblocks = (M + BM - 1) / BM;
     const uint16_t* Xa = static_cast<const uint16_t*>(X);
     if (c.rank > 0) {
-        const dim3 grid((M + 15) / 16, (a.r_pad + 63) / 64);
-        hipLaunchKernelGGL(lowrank_t_kernel, grid, dim3(256), 0, st, Xa, c.A, T, Xp, M, w.d_in, c.rank, a.r_pad, act);
+        constexpr int NW = 8;
+        const int mtiles = (M + 15) / 16;
+        const int t_blocks = mtiles * ((a.r_pad + 63) / 64);
+        const long long chunks = static_cast<long long>(M) * w.d_in / 8;
+        const long long x_blocks = (chunks + NW * 64 * 4 - 1) / (NW * 64 * 4);
+        hipLaunchKernelGGL(lowrank_t_kernel<NW>, dim3(static_cast<unsigned>(t_blocks + x_blocks)), dim3(NW * 64), 0, st,
+                           Xa, c.A, T, Xp, M, w.d_in, c.rank, a.r_pad, act, t_blocks, mtiles, chunks);
     } else {
         const long long chunks = static_cast<long long>(M) * w.d_in / 8;
         hipLaunchKernelGGL(xprep_kernel, dim3(static_cast<unsigned>((chunks + 255) / 256)), dim3(256), 0, st, Xa, Xp,
