@@ -117,6 +117,26 @@ def test_duplicate_invalid_ids_and_clamped_ranks():
     assert (_run(ex, x.bits[:2], torch.float16, bad, torch.float16, False) == 0).all()
 
 
+@pytest.mark.parametrize("x_per_slot", [False, True])
+def test_expert_with_more_than_64_slots_without_hoist(x_per_slot):
+    """200 slots over 128 experts keep the per-slot unpack (slots < 2 x active
+    experts); one expert takes 70 of them, so its slot ids are re-read into the
+    lanes after the first 64."""
+    E, d_out, d_in, bits, G, r_max, T, k = 128, 64, 256, 4, 128, 8, 25, 8
+    Q, s, z, A, B = _oracle_experts(E, d_out, d_in, bits, G, r_max, 44, svd=False)
+    ranks = wl.moe_expert_ranks(44, 0, 0, E, levels=(0, 4, 8))
+    g = np.random.default_rng(44)
+    flat = g.integers(0, E, T * k).astype(np.int32)
+    flat[g.permutation(T * k)[:70]] = 7
+    ids = flat.reshape(T, k)
+    x = wl.activation((T, k, d_in) if x_per_slot else (T, d_in), 44, 0, 1)
+    ex = _device_experts(Q, s, z, A, B, ranks, d_out, d_in, bits, G, r_max)
+    got = _run(ex, x.bits, torch.float16, ids, torch.float32, x_per_slot)
+    ref = _full_ref(Q, s, z, A, B, ranks, x.values, ids, x_per_slot, bits, G, d_in)
+    assert rel_l2(got, ref) <= REL_L2_TOL
+    assert rel_l2(got[ids == 7], ref[ids == 7]) <= REL_L2_TOL
+
+
 def test_rank_zero_without_factors():
     E, d_out, d_in, bits, G, T, k = 5, 70, 384, 4, 128, 3, 2
     Q, s, z, A, B = _oracle_experts(E, d_out, d_in, bits, G, 4, 43, svd=False)
