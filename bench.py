@@ -254,8 +254,8 @@ def bench_prefill(torch, cl, wl, timer, dev):
 def bench_moe(torch, cl, wl, timer, dev):
     """48 stacked MoE layers (128 experts, gate/up 768 x 2048, down
     2048 x 768, 4-bit g128, per-expert ranks from {0, 8, 16, 32}), top-8
-    routing: per layer gate and up on the token's input, down on each slot's
-    input.  Codes, scales and factors of the stacked experts are seeded random
+    routing: per layer gate and up as one window on the token's input, down
+    on each slot's input.  Codes, scales and factors of the stacked experts are seeded random
     device data (the cost does not depend on the values).  GB/s counts only the
     routed experts' bytes."""
     L, E, K = wl.MOE_LAYERS, wl.MOE_EXPERTS, wl.MOE_TOPK
@@ -283,12 +283,16 @@ def bench_moe(torch, cl, wl, timer, dev):
                                                 else (T, wl.MOE_SHAPES[n][1]), 5, 0, m).bits.view(np.int16))
               .view(torch.float16).to(dev) for n, m in mats}
         ys = {n: torch.empty((T, K, wl.MOE_SHAPES[n][0]), dtype=torch.float16, device=dev) for n, _ in mats}
-        wss = {n: cl.workspace(cl.moe_workspace(layers[n][0], T, K, n == "down"), dev) for n, _ in mats}
+        ws_gu = cl.workspace(cl.moe_window_workspace([layers["gate"][0], layers["up"][0]], T, K, False), dev)
+        ws_dn = cl.workspace(cl.moe_workspace(layers["down"][0], T, K, True), dev)
 
         def run():
+            # gate and up share the token's input and routing: one window
             for l in range(L):
-                for n, _ in mats:
-                    cl.moe_linear_decode(layers[n][l], xs[n], ids[l], y=ys[n], ws=wss[n], stream=timer.stream)
+                cl.moe_linear_decode_window([layers["gate"][l], layers["up"][l]], xs["gate"], ids[l],
+                                            ys=[ys["gate"], ys["up"]], ws=ws_gu, stream=timer.stream)
+                cl.moe_linear_decode(layers["down"][l], xs["down"], ids[l], y=ys["down"], ws=ws_dn,
+                                     stream=timer.stream)
         g = timer.capture(run)
         us = timer.time([g], 10) * 1e3
         nbytes = 0

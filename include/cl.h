@@ -272,6 +272,38 @@ cl_status cl_moe_linear_decode(const cl_qweight* w_expert0, const uint16_t* A, c
 size_t cl_moe_workspace(const cl_qweight* w_expert0, int32_t r_max, int32_t num_experts, int32_t T,
                         int32_t k, int32_t x_per_slot);
 
+/*
+ * cl_moe_linear_decode_window -- n MoE linears (1 <= n <= 4) over the same
+ * routing and the same activations, e.g. a layer's gate and up projections:
+ * the paper groups a MoE layer's Gate/Up work into one window (Section
+ * 4.2.2; Appendix A.1, MoE Layer).  One preparation kernel derives the
+ * routing once per workgroup and computes A_e x for every linear, and one
+ * backbone kernel covers every linear's routed experts; linear i's result
+ * equals cl_moe_linear_decode on it alone, bit for bit.
+ *
+ *  n          number of linears
+ *  w_expert0  host array [n] of expert-0 descriptors; all share d_in, bits
+ *             and group size (d_out may differ)
+ *  A, B       host arrays [n] of device factor pointers, as in
+ *             cl_moe_linear_decode (entries may be NULL where r_max[i] = 0)
+ *  r_max      host int32 [n];  ranks  host array [n] of device int32 [E]
+ *  y          host array [n] of device outputs [T][k][d_out_i] of out_dtype
+ *  ws         device workspace of cl_moe_window_workspace(...) bytes
+ * The host arrays are read during the call only.  Other arguments, limits and
+ * errors as cl_moe_linear_decode; linears that differ in d_in, bits or group
+ * size give CL_EINVAL.
+ */
+cl_status cl_moe_linear_decode_window(int32_t n, const cl_qweight* w_expert0, const uint16_t* const* A,
+                                      const uint16_t* const* B, const int32_t* r_max,
+                                      const int32_t* const* ranks, int32_t num_experts, const void* x,
+                                      int32_t x_per_slot, const int32_t* topk_ids, int32_t T, int32_t k,
+                                      int32_t act_dtype, void* const* y, int32_t out_dtype, void* ws,
+                                      size_t ws_bytes, void* stream);
+
+/* Workspace bytes for cl_moe_linear_decode_window (0 for rejected arguments). */
+size_t cl_moe_window_workspace(int32_t n, const cl_qweight* w_expert0, const int32_t* r_max,
+                               int32_t num_experts, int32_t T, int32_t k, int32_t x_per_slot);
+
 /* Message describing the last non-CL_OK status returned on this thread. */
 const char* cl_last_error(void);
 

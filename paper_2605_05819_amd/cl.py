@@ -65,6 +65,13 @@ _SIGNATURES = {
                                               ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
                                               ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p,
                                               ctypes.c_size_t, ctypes.c_void_p]),
+    "cl_moe_window_workspace": (ctypes.c_size_t, [ctypes.c_int32, ctypes.POINTER(QWeightC), ctypes.c_void_p,
+                                                  ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32]),
+    "cl_moe_linear_decode_window": (ctypes.c_int32, [ctypes.c_int32, ctypes.POINTER(QWeightC), ctypes.c_void_p,
+                                                     ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
+                                                     ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32,
+                                                     ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32,
+                                                     ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
     "cl_linear_window_workspace": (ctypes.c_size_t, [ctypes.c_int32, ctypes.POINTER(QWeightC),
                                                      ctypes.POINTER(LowRankC), ctypes.c_int32]),
     "cl_linear_decode_window": (ctypes.c_int32, [ctypes.c_int32, ctypes.POINTER(QWeightC), ctypes.POINTER(LowRankC),
@@ -275,6 +282,39 @@ def moe_linear_decode(ex, x, topk_ids, out_dtype=torch.float16, y=None, ws=None,
                                       _DTYPE_CODE[x.dtype], _ptr(y), _DTYPE_CODE[y.dtype], _ptr(ws), ws.numel(),
                                       _stream(stream)))
     return y
+
+
+def _moe_window_arrays(exs):
+    n = len(exs)
+    q0 = (QWeightC * n)(*[ex.expert0() for ex in exs])
+    A = (ctypes.c_void_p * n)(*[_ptr(ex.A) for ex in exs])
+    B = (ctypes.c_void_p * n)(*[_ptr(ex.B) for ex in exs])
+    rm = (ctypes.c_int32 * n)(*[ex.r_max for ex in exs])
+    rk = (ctypes.c_void_p * n)(*[_ptr(ex.ranks) for ex in exs])
+    return n, q0, A, B, rm, rk
+
+
+def moe_window_workspace(exs, T, k, x_per_slot):
+    n, q0, _, _, rm, _ = _moe_window_arrays(exs)
+    return lib().cl_moe_window_workspace(n, q0, rm, exs[0].num_experts, T, k, int(bool(x_per_slot)))
+
+
+def moe_linear_decode_window(exs, x, topk_ids, out_dtype=torch.float16, ys=None, ws=None, stream=None):
+    """``cl_moe_linear_decode_window``: the MoE linears ``exs`` (same d_in,
+    bits, group size and expert count) over one routing and one activation
+    tensor -> one ``y [T][k][d_out_i]`` per linear."""
+    T, k = topk_ids.shape
+    x_per_slot = x.dim() == 3
+    if ys is None:
+        ys = [torch.empty((T, k, ex.d_out), dtype=out_dtype, device=x.device) for ex in exs]
+    if ws is None:
+        ws = workspace(moe_window_workspace(exs, T, k, x_per_slot), x.device)
+    n, q0, A, B, rm, rk = _moe_window_arrays(exs)
+    yp = (ctypes.c_void_p * n)(*[_ptr(y) for y in ys])
+    _check(lib().cl_moe_linear_decode_window(n, q0, A, B, rm, rk, exs[0].num_experts, _ptr(x), int(x_per_slot),
+                                             _ptr(topk_ids), T, k, _DTYPE_CODE[x.dtype], yp,
+                                             _DTYPE_CODE[ys[0].dtype], _ptr(ws), ws.numel(), _stream(stream)))
+    return ys
 
 
 def build_compensation(W, w, r_max, stream=None):

@@ -244,53 +244,105 @@ cl_status cl_linear_prefill(const cl_qweight* w, const cl_lowrank* c, const void
                                                 static_cast<hipStream_t>(stream)), who);
 }
 
-size_t cl_moe_workspace(const cl_qweight* w_expert0, int32_t r_max, int32_t num_experts, int32_t T, int32_t k,
-                        int32_t x_per_slot) {
+}  // extern "C"
+
+namespace {
+
+// Shared validation of the MoE entry points: n linears over one routing and
+// one activation tensor (same d_in, bits and group size).
+cl_status moe_common(int32_t n, const cl_qweight* w, const uint16_t* const* A, const uint16_t* const* B,
+                     const int32_t* r_max, const int32_t* const* ranks, int32_t num_experts, const void* x,
+                     int32_t x_per_slot, const int32_t* topk_ids, int32_t T, int32_t k, int32_t act_dtype,
+                     void* const* y, int32_t out_dtype, void* ws, size_t ws_bytes, void* stream, const char* who) {
+    if (n < 1 || n > 4) return fail(CL_EINVAL, "%s: n must be in 1..4 (got %d)", who, n);
+    if (!w || !A || !B || !r_max || !ranks || !y) return fail(CL_EINVAL, "%s: null argument array", who);
+    cl::QW qw[4];
+    int rm[4];
+    for (int i = 0; i < n; ++i) {
+        cl_status st = check_qweight(&w[i], &qw[i], who);
+        if (st) return st;
+        if (qw[i].d_in != qw[0].d_in || qw[i].bits != qw[0].bits || qw[i].G != qw[0].G)
+            return fail(CL_EINVAL, "%s: the linears of a window must share d_in, bits and group size", who);
+        if (r_max[i] < 0 || r_max[i] > 256) return fail(CL_EINVAL, "%s: r_max must be in 0..256", who);
+        if (r_max[i] > 0) {
+            if (!A[i] || !B[i] || !ranks[i]) return fail(CL_EINVAL, "%s: null A, B or ranks with r_max %d", who, r_max[i]);
+            if (!aligned(A[i], 16) || !aligned(B[i], 2) || !aligned(ranks[i], 4))
+                return fail(CL_EINVAL, "%s: A must be 16-byte, B 2-byte, ranks 4-byte aligned", who);
+        }
+        if (!y[i]) return fail(CL_EINVAL, "%s: null y", who);
+        if (!aligned(y[i], out_dtype == CL_FP32 ? 4 : 2)) return fail(CL_EINVAL, "%s: misaligned y", who);
+        rm[i] = r_max[i];
+    }
+    if (num_experts < 1) return fail(CL_EINVAL, "%s: num_experts must be >= 1", who);
+    if (T < 1 || T > 64) return fail(CL_EINVAL, "%s: T must be in 1..64 (got %d)", who, T);
+    if (k < 1) return fail(CL_EINVAL, "%s: k must be >= 1", who);
+    if (!cl::moe_fits(qw[0], num_experts, T, k))
+        return fail(CL_EUNSUPPORTED, "%s: at most 1024 experts, 1024 slots (T*k) and d_in <= 8192 * bits", who);
+    if (!topk_ids || !aligned(topk_ids, 4)) return fail(CL_EINVAL, "%s: null or misaligned topk_ids", who);
+    if (act_dtype != CL_FP16 && act_dtype != CL_BF16)
+        return fail(CL_EINVAL, "%s: act_dtype must be CL_FP16 or CL_BF16", who);
+    if (out_dtype != CL_FP16 && out_dtype != CL_BF16 && out_dtype != CL_FP32)
+        return fail(CL_EINVAL, "%s: out_dtype must be CL_FP16, CL_BF16 or CL_FP32", who);
+    if (!x) return fail(CL_EINVAL, "%s: null x", who);
+    if (!aligned(x, 16)) return fail(CL_EINVAL, "%s: x must be 16-byte aligned", who);
+    const int xs = x_per_slot ? 1 : 0;
+    const size_t need = cl::moe_workspace_bytes(n, qw, rm, num_experts, T, k, xs);
+    if (!ws || ws_bytes < need)
+        return fail(CL_EWORKSPACE, "%s: workspace of %zu bytes needed (got %zu)", who, need, ws ? ws_bytes : 0);
+    if (!aligned(ws, 256)) return fail(CL_EINVAL, "%s: workspace must be 256-byte aligned", who);
+    return hip_status(cl::launch_moe_decode(n, qw, A, B, rm, ranks, num_experts, x, xs, topk_ids, T, k, act_dtype,
+                                            y, out_dtype, ws, static_cast<hipStream_t>(stream)),
+                      who);
+}
+
+size_t moe_ws(int32_t n, const cl_qweight* w, const int32_t* r_max, int32_t num_experts, int32_t T, int32_t k,
+              int32_t x_per_slot) {
     char saved[sizeof(g_err)];
     memcpy(saved, g_err, sizeof(g_err));
-    cl::QW qw;
     size_t bytes = 0;
-    if (check_qweight(w_expert0, &qw, "") == CL_OK && r_max >= 0 && r_max <= 256 && num_experts >= 1 && T >= 1 &&
-        T <= 64 && k >= 1 && cl::moe_fits(qw, num_experts, T, k))
-        bytes = cl::moe_workspace_bytes(qw, r_max, num_experts, T, k, x_per_slot ? 1 : 0);
+    cl::QW qw[4];
+    int rm[4];
+    bool ok = n >= 1 && n <= 4 && w && r_max && num_experts >= 1 && T >= 1 && T <= 64 && k >= 1;
+    for (int i = 0; ok && i < n; ++i) {
+        ok = check_qweight(&w[i], &qw[i], "") == CL_OK && r_max[i] >= 0 && r_max[i] <= 256 &&
+             qw[i].d_in == qw[0].d_in && qw[i].bits == qw[0].bits && qw[i].G == qw[0].G;
+        rm[i] = ok ? r_max[i] : 0;
+    }
+    if (ok && cl::moe_fits(qw[0], num_experts, T, k))
+        bytes = cl::moe_workspace_bytes(n, qw, rm, num_experts, T, k, x_per_slot ? 1 : 0);
     memcpy(g_err, saved, sizeof(g_err));
     return bytes;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t cl_moe_workspace(const cl_qweight* w_expert0, int32_t r_max, int32_t num_experts, int32_t T, int32_t k,
+                        int32_t x_per_slot) {
+    return moe_ws(1, w_expert0, &r_max, num_experts, T, k, x_per_slot);
+}
+
+size_t cl_moe_window_workspace(int32_t n, const cl_qweight* w_expert0, const int32_t* r_max, int32_t num_experts,
+                               int32_t T, int32_t k, int32_t x_per_slot) {
+    return moe_ws(n, w_expert0, r_max, num_experts, T, k, x_per_slot);
 }
 
 cl_status cl_moe_linear_decode(const cl_qweight* w_expert0, const uint16_t* A, const uint16_t* B, int32_t r_max,
                                const int32_t* ranks, int32_t num_experts, const void* x, int32_t x_per_slot,
                                const int32_t* topk_ids, int32_t T, int32_t k, int32_t act_dtype, void* y,
                                int32_t out_dtype, void* ws, size_t ws_bytes, void* stream) {
-    const char* who = "cl_moe_linear_decode";
-    cl::QW qw;
-    cl_status st = check_qweight(w_expert0, &qw, who);
-    if (st) return st;
-    if (num_experts < 1) return fail(CL_EINVAL, "%s: num_experts must be >= 1", who);
-    if (T < 1 || T > 64) return fail(CL_EINVAL, "%s: T must be in 1..64 (got %d)", who, T);
-    if (k < 1) return fail(CL_EINVAL, "%s: k must be >= 1", who);
-    if (!cl::moe_fits(qw, num_experts, T, k))
-        return fail(CL_EUNSUPPORTED, "%s: at most 1024 experts, 1024 slots (T*k) and d_in <= 8192 * bits", who);
-    if (r_max < 0 || r_max > 256) return fail(CL_EINVAL, "%s: r_max must be in 0..256", who);
-    if (r_max > 0) {
-        if (!A || !B || !ranks) return fail(CL_EINVAL, "%s: null A, B or ranks with r_max %d", who, r_max);
-        if (!aligned(A, 16) || !aligned(B, 2) || !aligned(ranks, 4))
-            return fail(CL_EINVAL, "%s: A must be 16-byte, B 2-byte, ranks 4-byte aligned", who);
-    }
-    if (!topk_ids || !aligned(topk_ids, 4)) return fail(CL_EINVAL, "%s: null or misaligned topk_ids", who);
-    if (act_dtype != CL_FP16 && act_dtype != CL_BF16)
-        return fail(CL_EINVAL, "%s: act_dtype must be CL_FP16 or CL_BF16", who);
-    if (out_dtype != CL_FP16 && out_dtype != CL_BF16 && out_dtype != CL_FP32)
-        return fail(CL_EINVAL, "%s: out_dtype must be CL_FP16, CL_BF16 or CL_FP32", who);
-    if (!x || !y) return fail(CL_EINVAL, "%s: null x or y", who);
-    if (!aligned(x, 16)) return fail(CL_EINVAL, "%s: x must be 16-byte aligned", who);
-    if (!aligned(y, out_dtype == CL_FP32 ? 4 : 2)) return fail(CL_EINVAL, "%s: misaligned y", who);
-    const int xs = x_per_slot ? 1 : 0;
-    const size_t need = cl::moe_workspace_bytes(qw, r_max, num_experts, T, k, xs);
-    if (!ws || ws_bytes < need)
-        return fail(CL_EWORKSPACE, "%s: workspace of %zu bytes needed (got %zu)", who, need, ws ? ws_bytes : 0);
-    if (!aligned(ws, 256)) return fail(CL_EINVAL, "%s: workspace must be 256-byte aligned", who);
-    return hip_status(cl::launch_moe_decode(qw, A, B, r_max, ranks, num_experts, x, xs, topk_ids, T, k, act_dtype, y,
-                                            out_dtype, ws, static_cast<hipStream_t>(stream)), who);
+    return moe_common(1, w_expert0, &A, &B, &r_max, &ranks, num_experts, x, x_per_slot, topk_ids, T, k, act_dtype,
+                      &y, out_dtype, ws, ws_bytes, stream, "cl_moe_linear_decode");
+}
+
+cl_status cl_moe_linear_decode_window(int32_t n, const cl_qweight* w_expert0, const uint16_t* const* A,
+                                      const uint16_t* const* B, const int32_t* r_max, const int32_t* const* ranks,
+                                      int32_t num_experts, const void* x, int32_t x_per_slot,
+                                      const int32_t* topk_ids, int32_t T, int32_t k, int32_t act_dtype,
+                                      void* const* y, int32_t out_dtype, void* ws, size_t ws_bytes, void* stream) {
+    return moe_common(n, w_expert0, A, B, r_max, ranks, num_experts, x, x_per_slot, topk_ids, T, k, act_dtype, y,
+                      out_dtype, ws, ws_bytes, stream, "cl_moe_linear_decode_window");
 }
 
 cl_status cl_linear_decode_window(int32_t n, const cl_qweight* w, const cl_lowrank* c, const void* x,

@@ -48,11 +48,13 @@ hipError_t launch_build_compensation(const float* W, const QW& w, int r_max, uin
                                      void* ws, hipStream_t st, int* sweeps_out);
 
 // MoE decode over stacked experts (expert e's arrays at e times one expert's
-// size); arguments already validated.
+// size) for a window of n <= 4 linears sharing the routing and activations;
+// arguments already validated.
 bool moe_fits(const QW& w, int E, int T, int k);
-size_t moe_workspace_bytes(const QW& w, int r_max, int E, int T, int k, int x_per_slot);
-hipError_t launch_moe_decode(const QW& w, const uint16_t* A, const uint16_t* B, int r_max, const int32_t* ranks,
-                             int E, const void* x, int x_per_slot, const int32_t* ids, int T, int k, int act,
-                             void* y, int out, void* ws, hipStream_t st);
+size_t moe_workspace_bytes(int n, const QW* w, const int* r_max, int E, int T, int k, int x_per_slot);
+hipError_t launch_moe_decode(int n, const QW* w, const uint16_t* const* A, const uint16_t* const* B,
+                             const int* r_max, const int32_t* const* ranks, int E, const void* x, int x_per_slot,
+                             const int32_t* ids, int T, int k, int act, void* const* y, int out, void* ws,
+                             hipStream_t st);
 
 }  // namespace cl

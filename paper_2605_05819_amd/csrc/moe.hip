@@ -46,28 +46,42 @@ constexpr int rows_per_wave(int bits) { return bits == 4 ? 4 : 2; }
 constexpr int kMaxSlots = 1024;      // T * k
 constexpr int kMaxExperts = 1024;
 constexpr int kTab = 8;              // ints per active-expert table entry
+constexpr int kMaxMoeWin = 4;        // linears per window
 
-struct MoeArgs {
+// One linear of a window: its stacked experts and its share of the grids.
+struct MoeLin {
     const uint32_t* q;
     const uint16_t* s;
     const uint16_t* z;
     const uint16_t* A;
     const uint16_t* B;
     const int32_t* ranks;
+    void* y;
+    float* t;                // [T*k][r_max] (workspace)
+    size_t q_stride, sz_stride, a_stride, b_stride;   // elements per expert
+    int d_out, r_max;
+    int rq;                  // preparation workgroups per expert (4 rank rows each)
+    int bpe;                 // backbone batches per expert
+    int prep_end;            // rank workgroups of linears 0 .. this one (prefix sum)
+    int blk_end;             // backbone workgroups of linears 0 .. this one (prefix sum)
+};
+
+// A window of n linears over the same routing and activations (one linear
+// is the window n = 1).
+struct MoeArgs {
+    MoeLin lin[kMaxMoeWin];
+    int n;
     const int32_t* ids;
     const uint16_t* x;
-    void* y;
-    size_t q_stride, sz_stride, a_stride, b_stride;   // elements per expert
-    int E, T, k, d_out, d_in, G, r_max, act, out, x_per_slot;
+    int E, T, k, d_in, G, act, out, x_per_slot;
     // workspace
     int* n_active;
-    int* table;              // [max_active][kTab]: expert, first sorted index, slot count, rank, first slot
+    int* table;              // [max_active][kTab]: expert, first sorted index, slot count, first slot,
+                             // then each linear's rank
     int* sorted;             // [T*k] slot ids grouped by expert, slot order within
-    float* t;                // [T*k][r_max]
     f16x2* xp;               // [rows][d_in/2]
     float* sx;               // [rows][chunks]
-    int ks, cps, bpe;        // K slices, chunks per slice, batches per expert
-    int rq;                  // prep workgroups per expert (4 rank rows each)
+    int ks, cps;             // K slices, chunks per slice
 };
 
 // 8 activations (one 16-byte load) as fp16, natural order; bf16 converted.
@@ -102,17 +116,22 @@ __global__ __launch_bounds__(256) void moe_prep_kernel(MoeArgs a) {
     const int blk = blockIdx.x;
 
     const int max_active = S < a.E ? S : a.E;
-    if (blk < max_active * a.rq) {
-        // workgroup (j, quad): the j-th routed expert (ascending id), its
-        // rank rows 4 quad .. 4 quad + 3
-        const int j = blk / a.rq;
-        const int quad = blk - j * a.rq;
+    if (blk < a.lin[a.n - 1].prep_end) {
+        // workgroup (linear li, j, quad): the j-th routed expert (ascending
+        // id), its rank rows 4 quad .. 4 quad + 3 of linear li; every
+        // workgroup derives the routing itself
+        int li = 0;
+        while (blk >= a.lin[li].prep_end) ++li;
+        const MoeLin& L = a.lin[li];
+        const int local = blk - (li ? a.lin[li - 1].prep_end : 0);
+        const int j = local / L.rq;
+        const int quad = local - j * L.rq;
         // slots per expert (LDS atomics contend only within one expert)
         // the ranks are loaded together with the ids: the selected expert's
         // rank then costs no further memory round trip
         for (int i = tid; i < a.E; i += 256) {
             hist[i] = 0;
-            rk[i] = a.r_max > 0 ? a.ranks[i] : 0;     // ranks may be null when r_max is 0
+            rk[i] = L.r_max > 0 ? L.ranks[i] : 0;     // ranks may be null when r_max is 0
         }
         if (tid == 0) sel = -1;
         __syncthreads();
@@ -150,7 +169,8 @@ __global__ __launch_bounds__(256) void moe_prep_kernel(MoeArgs a) {
                 pf += 1;
             }
         }
-        if (j == 0 && quad == 0 && tid == 0) *a.n_active = wsum[0][1] + wsum[1][1] + wsum[2][1] + wsum[3][1];
+        if (li == 0 && j == 0 && quad == 0 && tid == 0)
+            *a.n_active = wsum[0][1] + wsum[1][1] + wsum[2][1] + wsum[3][1];
         __syncthreads();
         if (j == 0 && quad == 0) {
             // out-of-range ids: their output rows are zero.  One parallel
@@ -162,8 +182,8 @@ __global__ __launch_bounds__(256) void moe_prep_kernel(MoeArgs a) {
                 for (int sl = wave; sl < S; sl += 4) {
                     const int id = sids[sl];
                     if (id >= 0 && id < a.E) continue;
-                    for (int o = lane; o < a.d_out; o += 64)
-                        store_out(a.y, static_cast<size_t>(sl) * a.d_out + o, 0.f, a.out);
+                    for (int o = lane; o < L.d_out; o += 64)
+                        store_out(L.y, static_cast<size_t>(sl) * L.d_out + o, 0.f, a.out);
                 }
             }
         }
@@ -171,12 +191,14 @@ __global__ __launch_bounds__(256) void moe_prep_kernel(MoeArgs a) {
         if (e < 0) return;                      // fewer than j + 1 routed experts
         const int ne = sel_n, cnt_lt = sel_lt;
         int rank = rk[e];
-        rank = rank < 0 ? 0 : (rank > a.r_max ? a.r_max : rank);
+        rank = rank < 0 ? 0 : (rank > L.r_max ? L.r_max : rank);
         if (quad == 0 && tid == 0) {
-            a.table[kTab * j + 0] = e;
-            a.table[kTab * j + 1] = cnt_lt;
-            a.table[kTab * j + 2] = ne;
-            a.table[kTab * j + 3] = rank;
+            if (li == 0) {
+                a.table[kTab * j + 0] = e;
+                a.table[kTab * j + 1] = cnt_lt;
+                a.table[kTab * j + 2] = ne;
+            }
+            a.table[kTab * j + 4 + li] = rank;
         }
         // this expert's slots in slot order (ballots, 256 slots per pass)
         int base_pos = 0;
@@ -190,9 +212,9 @@ __global__ __launch_bounds__(256) void moe_prep_kernel(MoeArgs a) {
             for (int w2 = 0; w2 < wave; ++w2) off += wcnt[w2];
             if (mine) {
                 const int pos = off + __popcll(m & ((1ull << lane) - 1ull));
-                if (quad == 0) {
+                if (li == 0 && quad == 0) {
                     a.sorted[cnt_lt + pos] = sl;
-                    if (pos == 0) a.table[kTab * j + 4] = sl;
+                    if (pos == 0) a.table[kTab * j + 3] = sl;
                 }
                 mys[pos] = sl;
             }
@@ -202,7 +224,7 @@ __global__ __launch_bounds__(256) void moe_prep_kernel(MoeArgs a) {
         // t[slot][i] = A_e[i] . x_slot: one wave per rank row, four slots at a time
         const int i = 4 * quad + wave;
         if (i >= rank) return;
-        const uint16_t* ar = a.A + static_cast<size_t>(e) * a.a_stride + static_cast<size_t>(i) * a.d_in;
+        const uint16_t* ar = L.A + static_cast<size_t>(e) * L.a_stride + static_cast<size_t>(i) * a.d_in;
         for (int j0 = 0; j0 < ne; j0 += 4) {
             const uint16_t* xr[4];
             int sl4[4];
@@ -246,14 +268,14 @@ __global__ __launch_bounds__(256) void moe_prep_kernel(MoeArgs a) {
             }
             const float tot = wave_sum_multi<4>(acc);      // lane l: slot j0 + l / 16
             const int u = lane >> 4;
-            if ((lane & 15) == 0 && j0 + u < ne) a.t[static_cast<size_t>(sl4[u]) * a.r_max + i] = tot;
+            if ((lane & 15) == 0 && j0 + u < ne) L.t[static_cast<size_t>(sl4[u]) * L.r_max + i] = tot;
         }
         return;
     }
     // activation preparation, one thread per (row, chunk)
     const int rows = a.x_per_slot ? S : a.T;
     const int chunks = a.d_in / CPW / 4;
-    const long long item = static_cast<long long>(blk - max_active * a.rq) * 256 + tid;
+    const long long item = static_cast<long long>(blk - a.lin[a.n - 1].prep_end) * 256 + tid;
     if (item >= static_cast<long long>(rows) * chunks) return;
     const int row = static_cast<int>(item / chunks);
     const int c = static_cast<int>(item % chunks);
@@ -292,12 +314,18 @@ void moe_kernel(MoeArgs a) {
 
     // the active-expert count and this entry are read together (the entry
     // exists for every ae below min(E, T k); it is used only if ae is active)
-    const int ae = blockIdx.x / a.bpe;
+    // workgroup -> (linear li, active expert ae, row batch)
+    const int blk = blockIdx.x;
+    int li = 0;
+    while (blk >= a.lin[li].blk_end) ++li;
+    const MoeLin& L = a.lin[li];
+    const int local = blk - (li ? a.lin[li - 1].blk_end : 0);
+    const int ae = local / L.bpe;
     const int n_active = *a.n_active;
     const int* ent = a.table + kTab * ae;
-    const int e = ent[0], sbeg = ent[1], scnt = ent[2], rank = ent[3], slot0 = ent[4];
+    const int e = ent[0], sbeg = ent[1], scnt = ent[2], slot0 = ent[3], rank = ent[4 + li];
     if (ae >= n_active) return;                     // whole workgroup: no routed expert here
-    const int batch = blockIdx.x - ae * a.bpe;
+    const int batch = local - ae * L.bpe;
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -312,9 +340,9 @@ void moe_kernel(MoeArgs a) {
     const int c_begin = slice * a.cps;
     const int c_end = min(chunks, c_begin + a.cps);
     const int row0 = (batch * rg_per_block + rgw) * R;
-    const bool active = row0 < a.d_out;
+    const bool active = row0 < L.d_out;
     const int base = active ? row0 : 0;
-    const int nrows = active ? min(R, a.d_out - row0) : 1;
+    const int nrows = active ? min(R, L.d_out - row0) : 1;
 
     int cidx[CPL];
     float cmask[CPL];
@@ -327,9 +355,9 @@ void moe_kernel(MoeArgs a) {
     }
 
     // this expert's rows: codes, scales, zeros, factor entries (loaded once)
-    const uint32_t* qe = a.q + static_cast<size_t>(e) * a.q_stride;
-    const uint16_t* se = a.s + static_cast<size_t>(e) * a.sz_stride;
-    const uint16_t* ze = a.z + static_cast<size_t>(e) * a.sz_stride;
+    const uint32_t* qe = L.q + static_cast<size_t>(e) * L.q_stride;
+    const uint16_t* se = L.s + static_cast<size_t>(e) * L.sz_stride;
+    const uint16_t* ze = L.z + static_cast<size_t>(e) * L.sz_stride;
     u32x4 qv[R][CPL];
     float sc[R][CPL], zc[R][CPL];
     float bv[R][NBA];
@@ -347,8 +375,8 @@ void moe_kernel(MoeArgs a) {
 #pragma unroll
         for (int m = 0; m < NB; ++m) {
             const int i = lane + 64 * (slice + ks * m);
-            const uint16_t* Be = a.B + static_cast<size_t>(e) * a.b_stride;
-            bv[r][m] = i < rank ? f16_bits_to_f32(Be[static_cast<size_t>(row) * a.r_max + i]) : 0.f;
+            const uint16_t* Be = L.B + static_cast<size_t>(e) * L.b_stride;
+            bv[r][m] = i < rank ? f16_bits_to_f32(Be[static_cast<size_t>(row) * L.r_max + i]) : 0.f;
         }
     }
 
@@ -372,7 +400,7 @@ void moe_kernel(MoeArgs a) {
 #pragma unroll
         for (int m = 0; m < NB; ++m) {
             const int i = lane + 64 * (slice + ks * m);
-            tv[m] = i < rank ? a.t[static_cast<size_t>(sl) * a.r_max + i] : 0.f;
+            tv[m] = i < rank ? L.t[static_cast<size_t>(sl) * L.r_max + i] : 0.f;
         }
     };
     // the unpacked codes (HOIST), from the raw loads above
@@ -442,15 +470,15 @@ void moe_kernel(MoeArgs a) {
         constexpr int SPAN = 64 / R;
         const int rr = (lane / SPAN) & (R - 1);
         if (ks == 1) {
-            if ((lane & (SPAN - 1)) == 0 && active && row0 + rr < a.d_out)
-                store_out(a.y, static_cast<size_t>(sl) * a.d_out + row0 + rr, tot, a.out);
+            if ((lane & (SPAN - 1)) == 0 && active && row0 + rr < L.d_out)
+                store_out(L.y, static_cast<size_t>(sl) * L.d_out + row0 + rr, tot, a.out);
         } else {
             if ((lane & (SPAN - 1)) == 0) red[wave][rr] = tot;
             __syncthreads();
-            if (slice == 0 && lane < R && active && row0 + lane < a.d_out) {
+            if (slice == 0 && lane < R && active && row0 + lane < L.d_out) {
                 float v = 0.f;
                 for (int kk = 0; kk < ks; ++kk) v += red[wave + kk][lane];
-                store_out(a.y, static_cast<size_t>(sl) * a.d_out + row0 + lane, v, a.out);
+                store_out(L.y, static_cast<size_t>(sl) * L.d_out + row0 + lane, v, a.out);
             }
             __syncthreads();
         }
@@ -460,21 +488,25 @@ void moe_kernel(MoeArgs a) {
 size_t up256(size_t n) { return (n + 255) / 256 * 256; }
 
 struct MoeLayout {
-    size_t n_active, table, sorted, t, xp, sx, total;
+    size_t n_active, table, sorted, t[kMaxMoeWin], xp, sx, total;
 };
 
-MoeLayout moe_layout(const QW& w, int r_max, int E, int T, int k, int x_per_slot) {
+MoeLayout moe_layout(int n, const QW* w, const int* r_max, int E, int T, int k, int x_per_slot) {
     const int S = T * k;
     const int max_active = S < E ? S : E;
     const int rows = x_per_slot ? S : T;
-    const size_t chunks = static_cast<size_t>(w.d_in) / (32 / w.bits) / 4;
+    const size_t chunks = static_cast<size_t>(w[0].d_in) / (32 / w[0].bits) / 4;
     MoeLayout l;
     l.n_active = 0;
     l.table = 256;
     l.sorted = l.table + up256(static_cast<size_t>(max_active) * kTab * sizeof(int));
-    l.t = l.sorted + up256(static_cast<size_t>(S) * sizeof(int));
-    l.xp = l.t + up256(static_cast<size_t>(S) * r_max * sizeof(float));
-    l.sx = l.xp + up256(static_cast<size_t>(rows) * w.d_in * 2);
+    size_t off = l.sorted + up256(static_cast<size_t>(S) * sizeof(int));
+    for (int i = 0; i < n; ++i) {
+        l.t[i] = off;
+        off += up256(static_cast<size_t>(S) * r_max[i] * sizeof(float));
+    }
+    l.xp = off;
+    l.sx = l.xp + up256(static_cast<size_t>(rows) * w[0].d_in * 2);
     l.total = l.sx + up256(static_cast<size_t>(rows) * chunks * sizeof(float));
     return l;
 }
@@ -506,33 +538,32 @@ bool moe_fits(const QW& w, int E, int T, int k) {
     return chunks <= 8 * 64 && E <= kMaxExperts && T * k <= kMaxSlots;
 }
 
-size_t moe_workspace_bytes(const QW& w, int r_max, int E, int T, int k, int x_per_slot) {
-    return moe_layout(w, r_max, E, T, k, x_per_slot).total;
+size_t moe_workspace_bytes(int n, const QW* w, const int* r_max, int E, int T, int k, int x_per_slot) {
+    return moe_layout(n, w, r_max, E, T, k, x_per_slot).total;
 }
 
-hipError_t launch_moe_decode(const QW& w, const uint16_t* A, const uint16_t* B, int r_max, const int32_t* ranks,
-                             int E, const void* x, int x_per_slot, const int32_t* ids, int T, int k, int act,
-                             void* y, int out, void* ws, hipStream_t st) {
-    const MoeLayout l = moe_layout(w, r_max, E, T, k, x_per_slot);
+hipError_t launch_moe_decode(int n, const QW* w, const uint16_t* const* A, const uint16_t* const* B,
+                             const int* r_max, const int32_t* const* ranks, int E, const void* x, int x_per_slot,
+                             const int32_t* ids, int T, int k, int act, void* const* y, int out, void* ws,
+                             hipStream_t st) {
+    if (n < 1 || n > kMaxMoeWin) return hipErrorInvalidConfiguration;
+    const MoeLayout l = moe_layout(n, w, r_max, E, T, k, x_per_slot);
     char* wsb = static_cast<char*>(ws);
-    MoeArgs a;
-    a.q = w.q; a.s = w.s; a.z = w.z; a.A = A; a.B = B; a.ranks = ranks; a.ids = ids;
-    a.x = static_cast<const uint16_t*>(x); a.y = y;
-    a.q_stride = static_cast<size_t>(w.d_out) * (w.d_in / (32 / w.bits));
-    a.sz_stride = static_cast<size_t>(w.d_out) * (w.d_in / w.G);
-    a.a_stride = static_cast<size_t>(r_max) * w.d_in;
-    a.b_stride = static_cast<size_t>(w.d_out) * r_max;
-    a.E = E; a.T = T; a.k = k; a.d_out = w.d_out; a.d_in = w.d_in; a.G = w.G; a.r_max = r_max;
+    const int d_in = w[0].d_in, bits = w[0].bits;
+    MoeArgs a{};
+    a.n = n;
+    a.ids = ids;
+    a.x = static_cast<const uint16_t*>(x);
+    a.E = E; a.T = T; a.k = k; a.d_in = d_in; a.G = w[0].G;
     a.act = act; a.out = out; a.x_per_slot = x_per_slot;
     a.n_active = reinterpret_cast<int*>(wsb + l.n_active);
     a.table = reinterpret_cast<int*>(wsb + l.table);
     a.sorted = reinterpret_cast<int*>(wsb + l.sorted);
-    a.t = reinterpret_cast<float*>(wsb + l.t);
     a.xp = reinterpret_cast<f16x2*>(wsb + l.xp);
     a.sx = reinterpret_cast<float*>(wsb + l.sx);
     // K split as in the dense decode: one chunk per lane, a power-of-two
     // number of slices (at most 8, which moe_fits guarantees)
-    const int chunks = w.d_in / (32 / w.bits) / 4;
+    const int chunks = d_in / (32 / bits) / 4;
     int ks = (chunks + 63) / 64;
     while (ks & (ks - 1)) ++ks;
     a.ks = ks;
@@ -540,28 +571,45 @@ hipError_t launch_moe_decode(const QW& w, const uint16_t* A, const uint16_t* B, 
     const int threads = 64 * (a.ks > 4 ? a.ks : 4);
     if (a.ks > 8 || threads > 512 || threads % (64 * a.ks)) return hipErrorInvalidConfiguration;
     const int rg_per_block = threads / 64 / a.ks;
-    a.rq = r_max > 0 ? (r_max + 3) / 4 : 1;
-    const int rgroups = (w.d_out + rows_per_wave(w.bits) - 1) / rows_per_wave(w.bits);
-    a.bpe = (rgroups + rg_per_block - 1) / rg_per_block;
     const int S = T * k;
     const int max_active = S < E ? S : E;
+    int prep_end = 0, blk_end = 0, rmax = 0;
+    for (int i = 0; i < n; ++i) {
+        MoeLin& L = a.lin[i];
+        L.q = w[i].q; L.s = w[i].s; L.z = w[i].z; L.A = A[i]; L.B = B[i]; L.ranks = ranks[i];
+        L.y = y[i];
+        L.t = reinterpret_cast<float*>(wsb + l.t[i]);
+        L.q_stride = static_cast<size_t>(w[i].d_out) * (d_in / (32 / bits));
+        L.sz_stride = static_cast<size_t>(w[i].d_out) * (d_in / w[i].G);
+        L.a_stride = static_cast<size_t>(r_max[i]) * d_in;
+        L.b_stride = static_cast<size_t>(w[i].d_out) * r_max[i];
+        L.d_out = w[i].d_out;
+        L.r_max = r_max[i];
+        L.rq = r_max[i] > 0 ? (r_max[i] + 3) / 4 : 1;
+        const int rgroups = (w[i].d_out + rows_per_wave(bits) - 1) / rows_per_wave(bits);
+        L.bpe = (rgroups + rg_per_block - 1) / rg_per_block;
+        prep_end += max_active * L.rq;
+        blk_end += max_active * L.bpe;
+        L.prep_end = prep_end;
+        L.blk_end = blk_end;
+        rmax = max(rmax, r_max[i]);
+    }
     const int per = 64 * a.ks;
-    const int nb = r_max == 0 ? 0 : (r_max <= per ? 1 : (r_max <= 2 * per ? 2 : 4));
+    const int nb = rmax == 0 ? 0 : (rmax <= per ? 1 : (rmax <= 2 * per ? 2 : 4));
 
     const int rows = x_per_slot ? S : T;
     const long long items = static_cast<long long>(rows) * chunks;
-    const unsigned pgrid = static_cast<unsigned>(max_active * a.rq + (items + 255) / 256);
-    if (w.bits == 4)
+    const unsigned pgrid = static_cast<unsigned>(prep_end + (items + 255) / 256);
+    if (bits == 4)
         hipLaunchKernelGGL(moe_prep_kernel<4>, dim3(pgrid), dim3(256), 0, st, a);
     else
         hipLaunchKernelGGL(moe_prep_kernel<2>, dim3(pgrid), dim3(256), 0, st, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    const int blocks = max_active * a.bpe;
     // experts meeting two or more slots on average: unpack once per batch
     const bool many = S >= 2 * max_active;
-    return w.bits == 4 ? launch_moe2<4>(a, nb, many, blocks, threads, st)
-                       : launch_moe2<2>(a, nb, many, blocks, threads, st);
+    return bits == 4 ? launch_moe2<4>(a, nb, many, blk_end, threads, st)
+                     : launch_moe2<2>(a, nb, many, blk_end, threads, st);
 }
 
 }  // namespace cl

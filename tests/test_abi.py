@@ -167,6 +167,37 @@ def test_moe_validation():
     assert call(r_max=0, A=0, B=0, ranks=0, ws_bytes=64) == cl.CL_EWORKSPACE   # factors optional at r_max 0
 
 
+def test_moe_window_validation():
+    lib = cl.lib()
+    v = ctypes.c_void_p
+
+    def call(n=2, qws=None, r_max=(8, 8), A=FAKE, ranks=FAKE, y=FAKE, ws_bytes=1 << 22):
+        qws = qws or [_qw(), _qw(d_out=96)]
+        q = (cl.QWeightC * len(qws))(*qws)
+        Ap = (v * 2)(v(A), v(A))
+        Bp = (v * 2)(v(FAKE), v(FAKE))
+        rm = (ctypes.c_int32 * 2)(*r_max)
+        rk = (v * 2)(v(ranks), v(ranks))
+        yp = (v * 2)(v(y), v(y))
+        return lib.cl_moe_linear_decode_window(n, q, Ap, Bp, rm, rk, 16, v(FAKE), 0, v(FAKE), 2, 4, cl.CL_FP16,
+                                               yp, cl.CL_FP16, v(FAKE), ws_bytes, None)
+
+    assert call(n=0) == cl.CL_EINVAL and call(n=5) == cl.CL_EINVAL
+    assert call(qws=[_qw(), _qw(d_in=512)]) == cl.CL_EINVAL and b"share" in lib.cl_last_error()
+    assert call(qws=[_qw(), _qw(group_size=64)]) == cl.CL_EINVAL
+    assert call(qws=[_qw(), _qw(bits=2)]) == cl.CL_EINVAL
+    assert call(r_max=(8, 300)) == cl.CL_EINVAL
+    assert call(A=0) == cl.CL_EINVAL and call(ranks=0) == cl.CL_EINVAL and call(y=0) == cl.CL_EINVAL
+    assert call(ws_bytes=64) == cl.CL_EWORKSPACE
+    # workspace: one routing table, per-linear A x, shared activations
+    qws = (cl.QWeightC * 2)(_qw(d_in=2048), _qw(d_in=2048, d_out=96))
+    one = lib.cl_moe_workspace(ctypes.byref(qws[0]), 32, 128, 8, 8, 0)
+    two = lib.cl_moe_window_workspace(2, qws, (ctypes.c_int32 * 2)(32, 16), 128, 8, 8, 0)
+    assert lib.cl_moe_window_workspace(1, qws, (ctypes.c_int32 * 1)(32), 128, 8, 8, 0) == one
+    assert two >= one + 64 * 16 * 4
+    assert lib.cl_moe_window_workspace(0, qws, (ctypes.c_int32 * 2)(32, 16), 128, 8, 8, 0) == 0
+
+
 def test_build_compensation_validation():
     lib = cl.lib()
     v = ctypes.c_void_p

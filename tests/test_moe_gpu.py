@@ -201,3 +201,58 @@ def test_layer_workspace_reuse_across_routings(moe_layer):
         torch.cuda.synchronize()
         ref = moe.forward_rows(packed, ranks, x.values, ids, False, rows, 4, 128)
         assert rel_l2(out_to_numpy(y)[:, :, rows], ref) <= REL_L2_TOL
+
+
+def _random_experts(E, d_out, d_in, r_max, seed):
+    """Seeded device experts (packed codes, scales, zeros, factors, ranks)."""
+    g = torch.Generator(device="cuda").manual_seed(seed)
+    q = torch.randint(-2 ** 31, 2 ** 31 - 1, (E, d_out, d_in // 8), dtype=torch.int32, device="cuda", generator=g)
+    s = (torch.rand((E, d_out, d_in // 128), device="cuda", generator=g) * 0.004 + 0.005).half()
+    z = torch.randint(0, 16, (E, d_out, d_in // 128), device="cuda", generator=g).half()
+    A = (torch.randn((E, r_max, d_in), device="cuda", generator=g) * 0.05).half()
+    B = (torch.randn((E, d_out, r_max), device="cuda", generator=g) * 0.05).half()
+    ranks = torch.randint(0, r_max + 1, (E,), dtype=torch.int32, device="cuda", generator=g)
+    return cl.MoeExperts(q, s, z, A, B, ranks, E, d_out, d_in, 4, 128, r_max)
+
+
+@pytest.mark.parametrize("x_per_slot", [False, True])
+@pytest.mark.parametrize("T", [1, 8, 64])
+def test_window_equals_singles_bitwise(T, x_per_slot):
+    """A gate/up-style window (two linears of different d_out and r_max) over
+    one routing gives each linear exactly its single-call result."""
+    E, d_in, k = 128, 512, 8
+    exs = [_random_experts(E, 96, d_in, 16, 50), _random_experts(E, 160, d_in, 8, 51)]
+    ids = torch.from_numpy(wl.routing(T, 52, 0)[0]).cuda()
+    x = torch.from_numpy(wl.activation((T, k, d_in) if x_per_slot else (T, d_in), 52, 0, 1).bits.view(np.int16))
+    x = x.view(torch.float16).cuda()
+    ys = cl.moe_linear_decode_window(exs, x, ids)
+    singles = [cl.moe_linear_decode(ex, x, ids) for ex in exs]
+    torch.cuda.synchronize()
+    for y, ys1 in zip(ys, singles):
+        assert torch.equal(y, ys1)
+    # the window again, on a workspace reused from a different routing
+    ws = cl.workspace(cl.moe_window_workspace(exs, T, k, x_per_slot), x.device)
+    ids2 = torch.from_numpy(wl.routing(T, 53, 0)[0]).cuda()
+    cl.moe_linear_decode_window(exs, x, ids2, ws=ws)
+    again = cl.moe_linear_decode_window(exs, x, ids, ws=ws)
+    torch.cuda.synchronize()
+    for y, y2 in zip(ys, again):
+        assert torch.equal(y, y2)
+
+
+def test_window_matches_oracle():
+    E, d_in, bits, G, k, T = 12, 512, 4, 128, 3, 5
+    exs, host = [], []
+    for i, (d_out, r_max) in enumerate(((100, 16), (60, 8))):
+        Q, s, z, A, B = _oracle_experts(E, d_out, d_in, bits, G, r_max, 60 + i)
+        ranks = wl.moe_expert_ranks(60 + i, 0, 0, E, levels=(0, 4, 8, r_max))
+        exs.append(_device_experts(Q, s, z, A, B, ranks, d_out, d_in, bits, G, r_max))
+        host.append((Q, s, z, A, B, ranks))
+    ids = np.random.default_rng(62).integers(0, E, (T, k)).astype(np.int32)
+    x = wl.activation((T, d_in), 62, 0, 1)
+    ys = cl.moe_linear_decode_window(exs, dev_u16(x.bits, torch.float16),
+                                     torch.from_numpy(ids).cuda(), out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    for y, (Q, s, z, A, B, ranks) in zip(ys, host):
+        ref = _full_ref(Q, s, z, A, B, ranks, x.values, ids, False, bits, G, d_in)
+        assert rel_l2(out_to_numpy(y), ref) <= REL_L2_TOL
