@@ -295,11 +295,49 @@ __global__ __launch_bounds__(256) void moe_prep_kernel(MoeArgs a) {
 // NB: factor columns per lane (r_max <= NB * 64 * ks); 0 when r_max is 0.
 // HOIST: unpack the codes once into fp16 lanes held in registers (for
 // experts that meet several slots); otherwise unpack per slot.
+// Sum R values over each group of LG consecutive lanes (LG = 16, 32 or 64,
+// a power of two >= R) with a transposing butterfly; on return lane l holds
+// the total of value index (l % LG) / (LG / R) of its group.
+template <int R, int LG>
+__device__ __forceinline__ float group_sum_multi(float (&v)[R]) {
+    const int lane = threadIdx.x & 63;
+    float a[R];
+#pragma unroll
+    for (int i = 0; i < R; ++i) a[i] = v[i];
+    int n = R;
+    int bit = LG / 2;
+#pragma unroll
+    for (int step = 0; step < 3; ++step) {
+        if (n > 1) {
+            const bool up = (lane & bit) != 0;
+            const int h = n / 2;
+#pragma unroll
+            for (int i = 0; i < R / 2; ++i) {
+                if (i < h) {
+                    const float mine = up ? a[i + h] : a[i];
+                    const float other = up ? a[i] : a[i + h];
+                    a[i] = mine + __shfl_xor(other, bit, 64);
+                }
+            }
+            n = h;
+            bit >>= 1;
+        }
+    }
+    float r = a[0];
+    for (; bit > 0; bit >>= 1) r += __shfl_xor(r, bit, 64);
+    return r;
+}
+
 // Without the hoisted unpack the kernel keeps no next-slot prefetch (it
 // cost 19 VGPRs) and the 4-bit, one-factor-column instance is held to 128
 // VGPRs (4 waves per SIMD, no spills): measured on MI355X, the 48-layer
 // T = 1 and T = 8 steps went from 39.3 and 102.9 us to 37.3 and 94.1 us.
-template <int BITS, int CPL, int NB, bool HOIST>
+//
+// LG: lanes per row set.  Rows of at least 64 chunks use the whole wave
+// (LG = 64); shorter rows (the 768-wide down projection: 24 chunks) give
+// each group of LG = 32 or 16 lanes its own R rows, so a wave covers
+// 64 / LG row sets and fewer lanes idle (24 of 64 lanes were busy).
+template <int BITS, int CPL, int NB, bool HOIST, int LG>
 __global__ __launch_bounds__(512)
 __attribute__((amdgpu_waves_per_eu(!HOIST && BITS == 4 && NB <= 1 ? 4 : 1)))
 void moe_kernel(MoeArgs a) {
@@ -339,7 +377,9 @@ void moe_kernel(MoeArgs a) {
     const int groups = a.d_in / a.G;
     const int c_begin = slice * a.cps;
     const int c_end = min(chunks, c_begin + a.cps);
-    const int row0 = (batch * rg_per_block + rgw) * R;
+    constexpr int SETS = 64 / LG;                  // row sets per wave
+    const int lg = lane % LG;                      // lane within its row set
+    const int row0 = ((batch * rg_per_block + rgw) * SETS + lane / LG) * R;
     const bool active = row0 < L.d_out;
     const int base = active ? row0 : 0;
     const int nrows = active ? min(R, L.d_out - row0) : 1;
@@ -348,7 +388,7 @@ void moe_kernel(MoeArgs a) {
     float cmask[CPL];
 #pragma unroll
     for (int j = 0; j < CPL; ++j) {
-        cidx[j] = c_begin + lane + 64 * j;
+        cidx[j] = c_begin + lg + LG * j;
         const bool valid = cidx[j] < c_end;
         cmask[j] = valid ? 1.f : 0.f;
         if (!valid) cidx[j] = c_begin;
@@ -374,7 +414,7 @@ void moe_kernel(MoeArgs a) {
         }
 #pragma unroll
         for (int m = 0; m < NB; ++m) {
-            const int i = lane + 64 * (slice + ks * m);
+            const int i = lg + LG * (slice + ks * m);
             const uint16_t* Be = L.B + static_cast<size_t>(e) * L.b_stride;
             bv[r][m] = i < rank ? f16_bits_to_f32(Be[static_cast<size_t>(row) * L.r_max + i]) : 0.f;
         }
@@ -399,7 +439,7 @@ void moe_kernel(MoeArgs a) {
         sxv = a.sx[static_cast<size_t>(xrow) * chunks + cidx[0]];
 #pragma unroll
         for (int m = 0; m < NB; ++m) {
-            const int i = lane + 64 * (slice + ks * m);
+            const int i = lg + LG * (slice + ks * m);
             tv[m] = i < rank ? L.t[static_cast<size_t>(sl) * L.r_max + i] : 0.f;
         }
     };
@@ -466,10 +506,10 @@ void moe_kernel(MoeArgs a) {
         for (int m = 0; m < NB; ++m)
 #pragma unroll
             for (int r = 0; r < R; ++r) acc[r] = fmaf(bv[r][m], tv[m], acc[r]);
-        const float tot = wave_sum_multi<R>(acc);
-        constexpr int SPAN = 64 / R;
-        const int rr = (lane / SPAN) & (R - 1);
-        if (ks == 1) {
+        const float tot = group_sum_multi<R, LG>(acc);
+        constexpr int SPAN = LG / R;
+        const int rr = (lg / SPAN) & (R - 1);
+        if (ks == 1 || LG < 64) {               // short rows always have one K slice
             if ((lane & (SPAN - 1)) == 0 && active && row0 + rr < L.d_out)
                 store_out(L.y, static_cast<size_t>(sl) * L.d_out + row0 + rr, tot, a.out);
         } else {
@@ -511,23 +551,30 @@ MoeLayout moe_layout(int n, const QW* w, const int* r_max, int E, int T, int k, 
     return l;
 }
 
-template <int BITS, int CPL, int NB>
-hipError_t launch_moe3(const MoeArgs& a, bool hoist, int blocks, int threads, hipStream_t st) {
+template <int BITS, int CPL, int NB, int LG>
+hipError_t launch_moe4(const MoeArgs& a, bool hoist, int blocks, int threads, hipStream_t st) {
     if (hoist)
-        hipLaunchKernelGGL((moe_kernel<BITS, CPL, NB, true>), dim3(blocks), dim3(threads), 0, st, a);
+        hipLaunchKernelGGL((moe_kernel<BITS, CPL, NB, true, LG>), dim3(blocks), dim3(threads), 0, st, a);
     else
-        hipLaunchKernelGGL((moe_kernel<BITS, CPL, NB, false>), dim3(blocks), dim3(threads), 0, st, a);
+        hipLaunchKernelGGL((moe_kernel<BITS, CPL, NB, false, LG>), dim3(blocks), dim3(threads), 0, st, a);
     return hipGetLastError();
 }
 
-template <int BITS>
-hipError_t launch_moe2(const MoeArgs& a, int nb, bool hoist, int blocks, int threads, hipStream_t st) {
+template <int BITS, int LG>
+hipError_t launch_moe3(const MoeArgs& a, int nb, bool hoist, int blocks, int threads, hipStream_t st) {
     switch (nb) {
-        case 0: return launch_moe3<BITS, 1, 0>(a, hoist, blocks, threads, st);
-        case 1: return launch_moe3<BITS, 1, 1>(a, hoist, blocks, threads, st);
-        case 2: return launch_moe3<BITS, 1, 2>(a, hoist, blocks, threads, st);
-        default: return launch_moe3<BITS, 1, 4>(a, hoist, blocks, threads, st);
+        case 0: return launch_moe4<BITS, 1, 0, LG>(a, hoist, blocks, threads, st);
+        case 1: return launch_moe4<BITS, 1, 1, LG>(a, hoist, blocks, threads, st);
+        case 2: return launch_moe4<BITS, 1, 2, LG>(a, hoist, blocks, threads, st);
+        default: return launch_moe4<BITS, 1, 4, LG>(a, hoist, blocks, threads, st);
     }
+}
+
+template <int BITS>
+hipError_t launch_moe2(const MoeArgs& a, int lg, int nb, bool hoist, int blocks, int threads, hipStream_t st) {
+    if (lg == 16) return launch_moe3<BITS, 16>(a, nb, hoist, blocks, threads, st);
+    if (lg == 32) return launch_moe3<BITS, 32>(a, nb, hoist, blocks, threads, st);
+    return launch_moe3<BITS, 64>(a, nb, hoist, blocks, threads, st);
 }
 
 }  // namespace
@@ -568,12 +615,20 @@ hipError_t launch_moe_decode(int n, const QW* w, const uint16_t* const* A, const
     while (ks & (ks - 1)) ++ks;
     a.ks = ks;
     a.cps = (chunks + a.ks - 1) / a.ks;
+    // lanes per row set: rows shorter than 64 chunks share a wave between
+    // 2 or 4 row sets (one K slice)
+    int rmax = 0;
+    for (int i = 0; i < n; ++i) rmax = max(rmax, r_max[i]);
+    int lg = chunks <= 16 ? 16 : (chunks <= 32 ? 32 : 64);
+    if (rmax > 4 * lg) lg = 64;                    // at most 4 factor columns per lane
+    const int sets = 64 / lg;
     const int threads = 64 * (a.ks > 4 ? a.ks : 4);
     if (a.ks > 8 || threads > 512 || threads % (64 * a.ks)) return hipErrorInvalidConfiguration;
-    const int rg_per_block = threads / 64 / a.ks;
+    if (lg < 64 && a.ks != 1) return hipErrorInvalidConfiguration;
+    const int rg_per_block = threads / 64 / a.ks * sets;
     const int S = T * k;
     const int max_active = S < E ? S : E;
-    int prep_end = 0, blk_end = 0, rmax = 0;
+    int prep_end = 0, blk_end = 0;
     for (int i = 0; i < n; ++i) {
         MoeLin& L = a.lin[i];
         L.q = w[i].q; L.s = w[i].s; L.z = w[i].z; L.A = A[i]; L.B = B[i]; L.ranks = ranks[i];
@@ -592,10 +647,10 @@ hipError_t launch_moe_decode(int n, const QW* w, const uint16_t* const* A, const
         blk_end += max_active * L.bpe;
         L.prep_end = prep_end;
         L.blk_end = blk_end;
-        rmax = max(rmax, r_max[i]);
     }
-    const int per = 64 * a.ks;
+    const int per = lg * a.ks;                     // factor columns per lane pass
     const int nb = rmax == 0 ? 0 : (rmax <= per ? 1 : (rmax <= 2 * per ? 2 : 4));
+    if (rmax > 4 * per) return hipErrorInvalidConfiguration;
 
     const int rows = x_per_slot ? S : T;
     const long long items = static_cast<long long>(rows) * chunks;
@@ -608,8 +663,8 @@ hipError_t launch_moe_decode(int n, const QW* w, const uint16_t* const* A, const
     if (e != hipSuccess) return e;
     // experts meeting two or more slots on average: unpack once per batch
     const bool many = S >= 2 * max_active;
-    return bits == 4 ? launch_moe2<4>(a, nb, many, blk_end, threads, st)
-                     : launch_moe2<2>(a, nb, many, blk_end, threads, st);
+    return bits == 4 ? launch_moe2<4>(a, lg, nb, many, blk_end, threads, st)
+                     : launch_moe2<2>(a, lg, nb, many, blk_end, threads, st);
 }
 
 }  // namespace cl
