@@ -35,6 +35,7 @@
 #include "cl_device.h"
 #include "cl_internal.h"
 #include "gemv_common.h"
+#include "mfma_common.h"
 
 namespace cl {
 
@@ -47,6 +48,12 @@ constexpr int kMaxSlots = 1024;      // T * k
 constexpr int kMaxExperts = 1024;
 constexpr int kTab = 8;              // ints per active-expert table entry
 constexpr int kMaxMoeWin = 4;        // linears per window
+// MFMA path: 16-row tiles per workgroup and K blocks in flight per wave.
+// Measured on the 48-layer T = 64 step: 4 x 2 199.6 us, 8 x 1 202.4, 2 x 2
+// 208.4, 4 x 4 287.1, 2 x 4 331.9 (one tile of 16 rows: 389, every
+// workgroup re-reading its slots' activations).
+constexpr int kMoeTpw = 4;
+constexpr int kMoeNbuf = 2;
 
 // One linear of a window: its stacked experts and its share of the grids.
 struct MoeLin {
@@ -525,6 +532,175 @@ void moe_kernel(MoeArgs a) {
     }
 }
 
+// Many slots per expert, 4-bit codes: the expert's rows against its slots on
+// MFMA (v_mfma_f32_16x16x32_f16), so the per-slot VALU work of the kernel
+// above (every slot's dot products on every lane) becomes MFMA columns.
+// Workgroup = (linear, active expert, TPW tiles of 16 rows); its four waves
+// split the 128-code blocks of K (wave w takes blocks w, w + 4, ..., NBUF in
+// flight); the expert's slots go in passes of 16 (the MFMA's columns).  Per
+// block a lane loads, for each tile, 16 bytes of codes of row r = lane % 16
+// (32 codes of one quantization group), and once for all tiles the matching
+// four 16-byte words of prepared activations of its pass's slot r; the codes
+// are dequantized in registers to fp16 s (q - z) with the group's scale and
+// zero from LDS and feed four MFMAs per tile.  The rank term is extra MFMA
+// steps over [B_e | t] (t rounded to fp16); the waves' tiles are summed
+// through LDS in a fixed order; one rounding to the output dtype.
+template <int TPW, int NBUF>
+__global__ __launch_bounds__(256) void moe_mfma_kernel(MoeArgs a) {
+    __shared__ f32x4 red[4][TPW][64];
+    extern __shared__ uint16_t szl[];             // [2][16 TPW][groups]: the rows' scales, then zeros
+    const int blk = blockIdx.x;
+    int li = 0;
+    while (blk >= a.lin[li].blk_end) ++li;
+    const MoeLin& L = a.lin[li];
+    const int local = blk - (li ? a.lin[li - 1].blk_end : 0);
+    const int ae = local / L.bpe;                 // bpe: workgroups (16 TPW rows) per expert
+    const int n_active = *a.n_active;
+    const int* ent = a.table + kTab * ae;
+    const int e = ent[0], sbeg = ent[1], scnt = ent[2], rank = ent[4 + li];
+    if (ae >= n_active) return;                   // whole workgroup: no routed expert here
+    const int row0 = (local - ae * L.bpe) * 16 * TPW;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int g = lane >> 4, r = lane & 15;
+    int row[TPW];
+    bool rowv[TPW];
+#pragma unroll
+    for (int j = 0; j < TPW; ++j) {
+        rowv[j] = row0 + 16 * j + r < L.d_out;
+        row[j] = rowv[j] ? row0 + 16 * j + r : L.d_out - 1;
+    }
+    const int K = a.d_in;
+    const int nkb = (K + 127) / 128;
+    const int words_row = K / 8;
+    const int groups = K / a.G;
+    const uint32_t* qe = L.q + static_cast<size_t>(e) * L.q_stride;
+    const uint16_t* se = L.s + static_cast<size_t>(e) * L.sz_stride;
+    const uint16_t* ze = L.z + static_cast<size_t>(e) * L.sz_stride;
+    const uint32_t mlo = __builtin_amdgcn_readfirstlane(0x000F000Fu);
+    const uint32_t mhi = __builtin_amdgcn_readfirstlane(0x00F000F0u);
+    const uint32_t bias = 0x64006400u;
+    // the rows' scales and zeros into LDS (one contiguous run per array;
+    // rows past the matrix are not loaded and never used)
+    {
+        const int nval = min(16 * TPW, L.d_out - row0) * groups;
+        const uint16_t* ssrc = se + static_cast<size_t>(row0) * groups;
+        const uint16_t* zsrc = ze + static_cast<size_t>(row0) * groups;
+        uint16_t* zl = szl + 16 * TPW * groups;
+        const bool al = ((reinterpret_cast<uintptr_t>(ssrc) | reinterpret_cast<uintptr_t>(zsrc)) & 15) == 0;
+        const int n16 = al ? nval / 8 : 0;
+        for (int i = threadIdx.x; i < n16; i += 256) {
+            reinterpret_cast<u32x4*>(szl)[i] = reinterpret_cast<const u32x4*>(ssrc)[i];
+            reinterpret_cast<u32x4*>(zl)[i] = reinterpret_cast<const u32x4*>(zsrc)[i];
+        }
+        for (int i = 8 * n16 + static_cast<int>(threadIdx.x); i < nval; i += 256) {
+            szl[i] = ssrc[i];
+            zl[i] = zsrc[i];
+        }
+        __syncthreads();
+    }
+    struct Blk {
+        u32x4 w[TPW];
+        u32x4 x[4];
+    };
+    for (int p0 = 0; p0 < scnt; p0 += 16) {
+        // this lane's slot (MFMA column r) of the pass; absent slots read a
+        // present one and are masked to zero
+        const bool sv = p0 + r < scnt;
+        const int sl = a.sorted[sbeg + (sv ? p0 + r : 0)];
+        const int xrow = a.x_per_slot ? sl : sl / a.k;
+        const u32x4* xr = reinterpret_cast<const u32x4*>(a.xp + static_cast<size_t>(xrow) * (K / 2));
+        const u32x4 zero = {0u, 0u, 0u, 0u};
+        f32x4 acc[TPW];
+#pragma unroll
+        for (int j = 0; j < TPW; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+        auto load = [&](int kb, Blk& b) {
+            const int wi = min(kb * 16 + 4 * g, words_row - 4);   // first of this lane's 4 words
+#pragma unroll
+            for (int j = 0; j < TPW; ++j)
+                b.w[j] = __builtin_nontemporal_load(
+                    reinterpret_cast<const u32x4*>(qe + static_cast<size_t>(row[j]) * words_row + wi));
+#pragma unroll
+            for (int t = 0; t < 4; ++t) b.x[t] = xr[wi + t];
+        };
+        auto compute = [&](int kb, const Blk& b) {
+            // past K or a padding block: scale 0, the weight is 0
+            const int kc = kb * 128 + 32 * g;
+            const bool on = kb < nkb && kc < K;
+            const int gs = on ? kc / a.G : 0;
+            u32x4 xv[4];
+#pragma unroll
+            for (int t = 0; t < 4; ++t) xv[t] = sv ? b.x[t] : zero;
+#pragma unroll
+            for (int j = 0; j < TPW; ++j) {
+                const int lr = (16 * j + r) * groups + gs;
+                const Dq dq = make_dq((on && rowv[j]) ? static_cast<uint32_t>(szl[lr]) : 0u,
+                                      szl[16 * TPW * groups + lr]);
+#pragma unroll
+                for (int t = 0; t < 4; ++t) acc[j] = mfma(dequant_word4x(b.w[j][t], dq, mlo, mhi, bias), xv[t], acc[j]);
+            }
+        };
+        constexpr int SPAN = 4 * NBUF;
+        const int rounds = (nkb + SPAN - 1) / SPAN;
+        Blk b[NBUF];
+#pragma unroll
+        for (int j = 0; j < NBUF; ++j) load(wave + 4 * j < nkb ? wave + 4 * j : 0, b[j]);
+        for (int rd = 0; rd < rounds; ++rd) {
+#pragma unroll
+            for (int j = 0; j < NBUF; ++j) {
+                const int kb = wave + SPAN * rd + 4 * j;
+                compute(kb, b[j]);
+                const int kn = kb + SPAN;
+                load(kn < nkb ? kn : (kb < nkb ? kb : 0), b[j]);
+            }
+        }
+        // rank-r term: 32 factor columns per step, wave w taking steps w, w + 4
+        for (int kr = 32 * wave; kr < rank; kr += 128) {
+            const int k = kr + 8 * g;
+            const float* trow = L.t + static_cast<size_t>(sl) * L.r_max;
+            uint32_t tw[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int k0 = k + 2 * q, k1 = k + 2 * q + 1;
+                const uint32_t tl = (sv && k0 < rank) ? f32_to_f16_bits(trow[k0]) : 0u;
+                const uint32_t th = (sv && k1 < rank) ? f32_to_f16_bits(trow[k1]) : 0u;
+                tw[q] = tl | (th << 16);
+            }
+#pragma unroll
+            for (int j = 0; j < TPW; ++j) {
+                const uint16_t* brow = L.B + static_cast<size_t>(e) * L.b_stride + static_cast<size_t>(row[j]) * L.r_max;
+                uint32_t aw[4];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int k0 = k + 2 * q, k1 = k + 2 * q + 1;
+                    const uint32_t lo = (rowv[j] && k0 < rank) ? brow[k0] : 0u;
+                    const uint32_t hi = (rowv[j] && k1 < rank) ? brow[k1] : 0u;
+                    aw[q] = lo | (hi << 16);
+                }
+                acc[j] = mfma(u32x4{aw[0], aw[1], aw[2], aw[3]}, u32x4{tw[0], tw[1], tw[2], tw[3]}, acc[j]);
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < TPW; ++j) red[wave][j][lane] = acc[j];
+        __syncthreads();
+        // wave w sums and stores tiles w, w + 4, ... in a fixed order
+        if (sv) {
+#pragma unroll
+            for (int j = 0; j < TPW; ++j) {
+                if (j % 4 != wave) continue;
+                const f32x4 v = red[0][j][lane] + red[1][j][lane] + red[2][j][lane] + red[3][j][lane];
+                // v[q] = y[slot sl][row0 + 16 j + 4 g + q]
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int rr = row0 + 16 * j + 4 * g + q;
+                    if (rr < L.d_out) store_out(L.y, static_cast<size_t>(sl) * L.d_out + rr, v[q], a.out);
+                }
+            }
+        }
+        __syncthreads();                           // red is reused by the next pass
+    }
+}
+
 size_t up256(size_t n) { return (n + 255) / 256 * 256; }
 
 struct MoeLayout {
@@ -628,6 +804,10 @@ hipError_t launch_moe_decode(int n, const QW* w, const uint16_t* const* A, const
     const int rg_per_block = threads / 64 / a.ks * sets;
     const int S = T * k;
     const int max_active = S < E ? S : E;
+    // experts meeting two or more slots on average: 4-bit codes go to MFMA
+    // (tiles of 16 rows), 2-bit codes are unpacked once per batch
+    const bool many = S >= 2 * max_active;
+    const bool on_mfma = many && bits == 4;
     int prep_end = 0, blk_end = 0;
     for (int i = 0; i < n; ++i) {
         MoeLin& L = a.lin[i];
@@ -642,7 +822,8 @@ hipError_t launch_moe_decode(int n, const QW* w, const uint16_t* const* A, const
         L.r_max = r_max[i];
         L.rq = r_max[i] > 0 ? (r_max[i] + 3) / 4 : 1;
         const int rgroups = (w[i].d_out + rows_per_wave(bits) - 1) / rows_per_wave(bits);
-        L.bpe = (rgroups + rg_per_block - 1) / rg_per_block;
+        L.bpe = on_mfma ? (w[i].d_out + 16 * kMoeTpw - 1) / (16 * kMoeTpw)
+                        : (rgroups + rg_per_block - 1) / rg_per_block;
         prep_end += max_active * L.rq;
         blk_end += max_active * L.bpe;
         L.prep_end = prep_end;
@@ -661,8 +842,11 @@ hipError_t launch_moe_decode(int n, const QW* w, const uint16_t* const* A, const
         hipLaunchKernelGGL(moe_prep_kernel<2>, dim3(pgrid), dim3(256), 0, st, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    // experts meeting two or more slots on average: unpack once per batch
-    const bool many = S >= 2 * max_active;
+    if (on_mfma) {
+        const size_t lds = static_cast<size_t>(2) * 16 * kMoeTpw * (d_in / w[0].G) * 2;
+        hipLaunchKernelGGL((moe_mfma_kernel<kMoeTpw, kMoeNbuf>), dim3(blk_end), dim3(256), lds, st, a);
+        return hipGetLastError();
+    }
     return bits == 4 ? launch_moe2<4>(a, lg, nb, many, blk_end, threads, st)
                      : launch_moe2<2>(a, lg, nb, many, blk_end, threads, st);
 }
