@@ -9,28 +9,32 @@
 // over every routed expert, and only routed experts' codes, scales, zeros and
 // factors are read.
 //
-//  * moe_prep_kernel: workgroup (j, q), j < min(E, T*k), reads the routing
-//    table -- so no workgroup ever waits for another -- counts slots per
-//    expert, scans the counts and takes e = the j-th routed expert in
-//    ascending id order (none: it exits).  Each of its
-//    four waves computes t[slot][i] = A_e[i] . x_slot for one rank row
-//    i = 4q + wave over all of e's slots (four slots per pass).  Workgroup
-//    (j, 0) also writes entry j of the active-expert table and e's slots, in
-//    slot order, into the sorted slot list; workgroup (0, 0) writes the
-//    number of routed experts and zero rows for slots whose id is out of
-//    range.  The remaining workgroups
-//    prepare the activations (fp16, pair-permuted, per-chunk sums) exactly as
-//    the dense decode does.
-//  * moe_kernel: one workgroup per (active expert, row batch); the grid is
-//    sized for the most experts T*k slots can reach and surplus workgroups
-//    exit on the device-side count.  Each wave loads its slice (4 rows for
-//    4-bit codes, 2 for 2-bit; one 16-byte chunk per lane) of the expert's
-//    backbone and factor entries once and applies it to every slot routed to
-//    that expert, loading the next slot's activations while it computes the
-//    current one.  Same arithmetic as the dense decode kernel: mask-only
-//    unpack into subnormal fp16 lanes, v_dot2, per-chunk scale and zero in
-//    fp32, B t in the same partial sums, transposing butterfly, fixed-order
-//    K-slice reduction.
+// A call covers a window of up to 4 linears over the same routing and input
+// (e.g. a layer's gate and up); a single linear is the window of one.
+//
+//  * moe_prep_kernel: workgroup (linear, j, q), j < min(E, T*k), reads the
+//    routing table -- so no workgroup ever waits for another -- counts slots
+//    per expert, scans the counts and takes e = the j-th routed expert in
+//    ascending id order (none: it exits).  Each of its four waves computes
+//    t[slot][i] = A_e[i] . x_slot for one rank row i = 4q + wave of its
+//    linear over all of e's slots (four slots per pass).  Workgroup
+//    (0, j, 0) also writes entry j of the active-expert table and e's slots,
+//    in slot order, into the sorted slot list, and (linear, j, 0) that
+//    linear's rank of e; workgroups (linear, 0, 0) write the number of
+//    routed experts and zero rows for slots whose id is out of range.  The
+//    remaining workgroups prepare the activations (fp16, pair-permuted,
+//    per-chunk sums) exactly as the dense decode does.
+//  * moe_kernel: one workgroup per (linear, active expert, row batch); the
+//    grid is sized for the most experts T*k slots can reach and surplus
+//    workgroups exit on the device-side count.  Each wave loads its slice
+//    (4 rows for 4-bit codes, 2 for 2-bit, per row set of LG lanes; one
+//    16-byte chunk per lane) of the expert's backbone and factor entries
+//    once and applies it to every slot routed to that expert.  Same
+//    arithmetic as the dense decode kernel: mask-only unpack into subnormal
+//    fp16 lanes, v_dot2, per-chunk scale and zero in fp32, B t in the same
+//    partial sums, transposing butterfly, fixed-order K-slice reduction.
+//  * moe_mfma_kernel: with several slots per expert (4-bit codes), the
+//    expert's rows against its slots on MFMA (slots as the columns).
 
 #include "cl_device.h"
 #include "cl_internal.h"
