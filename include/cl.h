@@ -287,6 +287,13 @@ size_t cl_moe_workspace(const cl_qweight* w_expert0, int32_t r_max, int32_t num_
  *  A, B       host arrays [n] of device factor pointers, as in
  *             cl_moe_linear_decode (entries may be NULL where r_max[i] = 0)
  *  r_max      host int32 [n];  ranks  host array [n] of device int32 [E]
+ *  slot_ranks NULL, or host array [n] of device int32 [T][k] (entries may be
+ *             NULL): per-slot ranks, clamped to 0..r_max[i], in place of
+ *             ranks[i][e].  The paper's expert-activation term scales each
+ *             routed expert's compensation priority by k times its routing
+ *             weight (Section 4.3.3, Expert Activation for MoE Models), so a
+ *             slot's rank can differ from its expert's static rank; slot
+ *             (t, j) then uses the prefix A_e[:r_tj], B_e[:, :r_tj]
  *  y          host array [n] of device outputs [T][k][d_out_i] of out_dtype
  *  ws         device workspace of cl_moe_window_workspace(...) bytes
  * The host arrays are read during the call only.  Other arguments, limits and
@@ -295,10 +302,11 @@ size_t cl_moe_workspace(const cl_qweight* w_expert0, int32_t r_max, int32_t num_
  */
 cl_status cl_moe_linear_decode_window(int32_t n, const cl_qweight* w_expert0, const uint16_t* const* A,
                                       const uint16_t* const* B, const int32_t* r_max,
-                                      const int32_t* const* ranks, int32_t num_experts, const void* x,
-                                      int32_t x_per_slot, const int32_t* topk_ids, int32_t T, int32_t k,
-                                      int32_t act_dtype, void* const* y, int32_t out_dtype, void* ws,
-                                      size_t ws_bytes, void* stream);
+                                      const int32_t* const* ranks, const int32_t* const* slot_ranks,
+                                      int32_t num_experts, const void* x, int32_t x_per_slot,
+                                      const int32_t* topk_ids, int32_t T, int32_t k, int32_t act_dtype,
+                                      void* const* y, int32_t out_dtype, void* ws, size_t ws_bytes,
+                                      void* stream);
 
 /* Workspace bytes for cl_moe_linear_decode_window (0 for rejected arguments). */
 size_t cl_moe_window_workspace(int32_t n, const cl_qweight* w_expert0, const int32_t* r_max,

@@ -19,10 +19,13 @@ import numpy as np
 from . import linear
 
 
-def forward(experts, ranks, X, ids, x_per_slot):
+def forward(experts, ranks, X, ids, x_per_slot, slot_ranks=None):
     """``experts[e] = (W_hat_e, A_e, B_e)`` (fp64-convertible arrays);
     ``ranks[e]`` ints; ``X`` is ``[T][d_in]`` (shared) or ``[T][k][d_in]``
-    (per slot); ``ids`` is ``[T][k]``.  Returns fp64 ``[T][k][d_out]``."""
+    (per slot); ``ids`` is ``[T][k]``; ``slot_ranks`` (optional ``[T][k]``)
+    replaces ``ranks[e]`` slot by slot (Section 4.3.3: each routed expert's
+    compensation follows its routing weight).  Returns fp64
+    ``[T][k][d_out]``."""
     ids = np.asarray(ids)
     T, k = ids.shape
     d_out = np.asarray(experts[int(ids[0, 0])][0]).shape[0]
@@ -32,7 +35,8 @@ def forward(experts, ranks, X, ids, x_per_slot):
             e = int(ids[t, j])
             W_hat, A, B = experts[e]
             x = X[t, j] if x_per_slot else X[t]
-            Y[t, j] = linear.forward(W_hat, A, B, int(ranks[e]), np.asarray(x)[None, :])[0]
+            r = int(ranks[e]) if slot_ranks is None else int(slot_ranks[t][j])
+            Y[t, j] = linear.forward(W_hat, A, B, r, np.asarray(x)[None, :])[0]
     return Y
 
 

@@ -68,7 +68,8 @@ _SIGNATURES = {
     "cl_moe_window_workspace": (ctypes.c_size_t, [ctypes.c_int32, ctypes.POINTER(QWeightC), ctypes.c_void_p,
                                                   ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32]),
     "cl_moe_linear_decode_window": (ctypes.c_int32, [ctypes.c_int32, ctypes.POINTER(QWeightC), ctypes.c_void_p,
-                                                     ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
+                                                     ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                                     ctypes.c_int32,
                                                      ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32,
                                                      ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32,
                                                      ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
@@ -299,10 +300,13 @@ def moe_window_workspace(exs, T, k, x_per_slot):
     return lib().cl_moe_window_workspace(n, q0, rm, exs[0].num_experts, T, k, int(bool(x_per_slot)))
 
 
-def moe_linear_decode_window(exs, x, topk_ids, out_dtype=torch.float16, ys=None, ws=None, stream=None):
+def moe_linear_decode_window(exs, x, topk_ids, out_dtype=torch.float16, ys=None, ws=None, stream=None,
+                             slot_ranks=None):
     """``cl_moe_linear_decode_window``: the MoE linears ``exs`` (same d_in,
     bits, group size and expert count) over one routing and one activation
-    tensor -> one ``y [T][k][d_out_i]`` per linear."""
+    tensor -> one ``y [T][k][d_out_i]`` per linear.  ``slot_ranks``: None, or
+    one device int32 ``[T][k]`` tensor (or None) per linear, used in place of
+    the experts' ranks."""
     T, k = topk_ids.shape
     x_per_slot = x.dim() == 3
     if ys is None:
@@ -311,7 +315,8 @@ def moe_linear_decode_window(exs, x, topk_ids, out_dtype=torch.float16, ys=None,
         ws = workspace(moe_window_workspace(exs, T, k, x_per_slot), x.device)
     n, q0, A, B, rm, rk = _moe_window_arrays(exs)
     yp = (ctypes.c_void_p * n)(*[_ptr(y) for y in ys])
-    _check(lib().cl_moe_linear_decode_window(n, q0, A, B, rm, rk, exs[0].num_experts, _ptr(x), int(x_per_slot),
+    sr = None if slot_ranks is None else (ctypes.c_void_p * n)(*[_ptr(r) for r in slot_ranks])
+    _check(lib().cl_moe_linear_decode_window(n, q0, A, B, rm, rk, sr, exs[0].num_experts, _ptr(x), int(x_per_slot),
                                              _ptr(topk_ids), T, k, _DTYPE_CODE[x.dtype], yp,
                                              _DTYPE_CODE[ys[0].dtype], _ptr(ws), ws.numel(), _stream(stream)))
     return ys

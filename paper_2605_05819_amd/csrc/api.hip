@@ -251,7 +251,8 @@ namespace {
 // Shared validation of the MoE entry points: n linears over one routing and
 // one activation tensor (same d_in, bits and group size).
 cl_status moe_common(int32_t n, const cl_qweight* w, const uint16_t* const* A, const uint16_t* const* B,
-                     const int32_t* r_max, const int32_t* const* ranks, int32_t num_experts, const void* x,
+                     const int32_t* r_max, const int32_t* const* ranks, const int32_t* const* slot_ranks,
+                     int32_t num_experts, const void* x,
                      int32_t x_per_slot, const int32_t* topk_ids, int32_t T, int32_t k, int32_t act_dtype,
                      void* const* y, int32_t out_dtype, void* ws, size_t ws_bytes, void* stream, const char* who) {
     if (n < 1 || n > 4) return fail(CL_EINVAL, "%s: n must be in 1..4 (got %d)", who, n);
@@ -269,6 +270,8 @@ cl_status moe_common(int32_t n, const cl_qweight* w, const uint16_t* const* A, c
             if (!aligned(A[i], 16) || !aligned(B[i], 2) || !aligned(ranks[i], 4))
                 return fail(CL_EINVAL, "%s: A must be 16-byte, B 2-byte, ranks 4-byte aligned", who);
         }
+        if (slot_ranks && slot_ranks[i] && !aligned(slot_ranks[i], 4))
+            return fail(CL_EINVAL, "%s: slot_ranks must be 4-byte aligned", who);
         if (!y[i]) return fail(CL_EINVAL, "%s: null y", who);
         if (!aligned(y[i], out_dtype == CL_FP32 ? 4 : 2)) return fail(CL_EINVAL, "%s: misaligned y", who);
         rm[i] = r_max[i];
@@ -290,7 +293,8 @@ cl_status moe_common(int32_t n, const cl_qweight* w, const uint16_t* const* A, c
     if (!ws || ws_bytes < need)
         return fail(CL_EWORKSPACE, "%s: workspace of %zu bytes needed (got %zu)", who, need, ws ? ws_bytes : 0);
     if (!aligned(ws, 256)) return fail(CL_EINVAL, "%s: workspace must be 256-byte aligned", who);
-    return hip_status(cl::launch_moe_decode(n, qw, A, B, rm, ranks, num_experts, x, xs, topk_ids, T, k, act_dtype,
+    return hip_status(cl::launch_moe_decode(n, qw, A, B, rm, ranks, slot_ranks, num_experts, x, xs, topk_ids, T, k,
+                                            act_dtype,
                                             y, out_dtype, ws, static_cast<hipStream_t>(stream)),
                       who);
 }
@@ -332,17 +336,18 @@ cl_status cl_moe_linear_decode(const cl_qweight* w_expert0, const uint16_t* A, c
                                const int32_t* ranks, int32_t num_experts, const void* x, int32_t x_per_slot,
                                const int32_t* topk_ids, int32_t T, int32_t k, int32_t act_dtype, void* y,
                                int32_t out_dtype, void* ws, size_t ws_bytes, void* stream) {
-    return moe_common(1, w_expert0, &A, &B, &r_max, &ranks, num_experts, x, x_per_slot, topk_ids, T, k, act_dtype,
-                      &y, out_dtype, ws, ws_bytes, stream, "cl_moe_linear_decode");
+    return moe_common(1, w_expert0, &A, &B, &r_max, &ranks, nullptr, num_experts, x, x_per_slot, topk_ids, T, k,
+                      act_dtype, &y, out_dtype, ws, ws_bytes, stream, "cl_moe_linear_decode");
 }
 
 cl_status cl_moe_linear_decode_window(int32_t n, const cl_qweight* w_expert0, const uint16_t* const* A,
                                       const uint16_t* const* B, const int32_t* r_max, const int32_t* const* ranks,
-                                      int32_t num_experts, const void* x, int32_t x_per_slot,
+                                      const int32_t* const* slot_ranks, int32_t num_experts, const void* x,
+                                      int32_t x_per_slot,
                                       const int32_t* topk_ids, int32_t T, int32_t k, int32_t act_dtype,
                                       void* const* y, int32_t out_dtype, void* ws, size_t ws_bytes, void* stream) {
-    return moe_common(n, w_expert0, A, B, r_max, ranks, num_experts, x, x_per_slot, topk_ids, T, k, act_dtype, y,
-                      out_dtype, ws, ws_bytes, stream, "cl_moe_linear_decode_window");
+    return moe_common(n, w_expert0, A, B, r_max, ranks, slot_ranks, num_experts, x, x_per_slot, topk_ids, T, k,
+                      act_dtype, y, out_dtype, ws, ws_bytes, stream, "cl_moe_linear_decode_window");
 }
 
 cl_status cl_linear_decode_window(int32_t n, const cl_qweight* w, const cl_lowrank* c, const void* x,

@@ -53,7 +53,8 @@ hipError_t launch_build_compensation(const float* W, const QW& w, int r_max, uin
 bool moe_fits(const QW& w, int E, int T, int k);
 size_t moe_workspace_bytes(int n, const QW* w, const int* r_max, int E, int T, int k, int x_per_slot);
 hipError_t launch_moe_decode(int n, const QW* w, const uint16_t* const* A, const uint16_t* const* B,
-                             const int* r_max, const int32_t* const* ranks, int E, const void* x, int x_per_slot,
+                             const int* r_max, const int32_t* const* ranks, const int32_t* const* slot_ranks,
+                             int E, const void* x, int x_per_slot,
                              const int32_t* ids, int T, int k, int act, void* const* y, int out, void* ws,
                              hipStream_t st);
 

@@ -67,6 +67,7 @@ struct MoeLin {
     const uint16_t* A;
     const uint16_t* B;
     const int32_t* ranks;
+    const int32_t* slot_rank;  // [T*k] per-slot ranks (clamped to 0..r_max), or null: ranks[e]
     void* y;
     float* t;                // [T*k][r_max] (workspace)
     size_t q_stride, sz_stride, a_stride, b_stride;   // elements per expert
@@ -119,7 +120,7 @@ __global__ __launch_bounds__(256) void moe_prep_kernel(MoeArgs a) {
     __shared__ int rk[kMaxExperts];         // the experts' ranks, loaded beside the ids
     __shared__ int wsum[4][2];
     __shared__ int wcnt[4];
-    __shared__ int sel, sel_lt, sel_n;
+    __shared__ int sel, sel_lt, sel_n, srank;
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
@@ -203,14 +204,10 @@ __global__ __launch_bounds__(256) void moe_prep_kernel(MoeArgs a) {
         const int ne = sel_n, cnt_lt = sel_lt;
         int rank = rk[e];
         rank = rank < 0 ? 0 : (rank > L.r_max ? L.r_max : rank);
-        if (quad == 0 && tid == 0) {
-            if (li == 0) {
-                a.table[kTab * j + 0] = e;
-                a.table[kTab * j + 1] = cnt_lt;
-                a.table[kTab * j + 2] = ne;
-            }
-            a.table[kTab * j + 4 + li] = rank;
-        }
+        // per-slot ranks: the expert's rank here is the largest of its slots'
+        // (A_e x is computed that far; each slot reads its own prefix)
+        const bool dyn = L.slot_rank != nullptr;
+        if (dyn && tid == 0) srank = 0;
         // this expert's slots in slot order (ballots, 256 slots per pass)
         int base_pos = 0;
         for (int b0 = 0; b0 < S; b0 += 256) {
@@ -228,9 +225,22 @@ __global__ __launch_bounds__(256) void moe_prep_kernel(MoeArgs a) {
                     if (pos == 0) a.table[kTab * j + 3] = sl;
                 }
                 mys[pos] = sl;
+                if (dyn) {
+                    const int rs = L.slot_rank[sl];
+                    atomicMax(&srank, rs < 0 ? 0 : (rs > L.r_max ? L.r_max : rs));
+                }
             }
             base_pos += wcnt[0] + wcnt[1] + wcnt[2] + wcnt[3];
             __syncthreads();
+        }
+        if (dyn) rank = srank;
+        if (quad == 0 && tid == 0) {
+            if (li == 0) {
+                a.table[kTab * j + 0] = e;
+                a.table[kTab * j + 1] = cnt_lt;
+                a.table[kTab * j + 2] = ne;
+            }
+            a.table[kTab * j + 4 + li] = rank;
         }
         // t[slot][i] = A_e[i] . x_slot: one wave per rank row, four slots at a time
         const int i = 4 * quad + wave;
@@ -436,6 +446,12 @@ void moe_kernel(MoeArgs a) {
     // one slot ahead, otherwise at the slot itself.
     auto load_x = [&](int sl, f16x2 (&xv)[PPC], float& sxv, float (&tv)[NBA]) {
         const int xrow = a.x_per_slot ? sl : sl / a.k;
+        // this slot's rank: its own (per-slot ranks) or the expert's
+        int rs = rank;
+        if (L.slot_rank) {
+            const int v = L.slot_rank[sl];
+            rs = v < 0 ? 0 : (v > L.r_max ? L.r_max : v);
+        }
         const u32x4* src = reinterpret_cast<const u32x4*>(a.xp + static_cast<size_t>(xrow) * (a.d_in / 2) +
                                                           static_cast<size_t>(cidx[0]) * PPC);
 #pragma unroll
@@ -451,7 +467,7 @@ void moe_kernel(MoeArgs a) {
 #pragma unroll
         for (int m = 0; m < NB; ++m) {
             const int i = lg + LG * (slice + ks * m);
-            tv[m] = i < rank ? L.t[static_cast<size_t>(sl) * L.r_max + i] : 0.f;
+            tv[m] = i < rs ? L.t[static_cast<size_t>(sl) * L.r_max + i] : 0.f;
         }
     };
     // the unpacked codes (HOIST), from the raw loads above
@@ -614,6 +630,12 @@ __global__ __launch_bounds__(256) void moe_mfma_kernel(MoeArgs a) {
         const int sl = a.sorted[sbeg + (sv ? p0 + r : 0)];
         const int xrow = a.x_per_slot ? sl : sl / a.k;
         const u32x4* xr = reinterpret_cast<const u32x4*>(a.xp + static_cast<size_t>(xrow) * (K / 2));
+        // this lane's slot's rank: its own (per-slot ranks) or the expert's
+        int rs = rank;
+        if (L.slot_rank) {
+            const int v = L.slot_rank[sl];
+            rs = v < 0 ? 0 : (v > L.r_max ? L.r_max : v);
+        }
         const u32x4 zero = {0u, 0u, 0u, 0u};
         f32x4 acc[TPW];
 #pragma unroll
@@ -666,8 +688,8 @@ __global__ __launch_bounds__(256) void moe_mfma_kernel(MoeArgs a) {
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
                 const int k0 = k + 2 * q, k1 = k + 2 * q + 1;
-                const uint32_t tl = (sv && k0 < rank) ? f32_to_f16_bits(trow[k0]) : 0u;
-                const uint32_t th = (sv && k1 < rank) ? f32_to_f16_bits(trow[k1]) : 0u;
+                const uint32_t tl = (sv && k0 < rs) ? f32_to_f16_bits(trow[k0]) : 0u;
+                const uint32_t th = (sv && k1 < rs) ? f32_to_f16_bits(trow[k1]) : 0u;
                 tw[q] = tl | (th << 16);
             }
 #pragma unroll
@@ -770,7 +792,8 @@ size_t moe_workspace_bytes(int n, const QW* w, const int* r_max, int E, int T, i
 }
 
 hipError_t launch_moe_decode(int n, const QW* w, const uint16_t* const* A, const uint16_t* const* B,
-                             const int* r_max, const int32_t* const* ranks, int E, const void* x, int x_per_slot,
+                             const int* r_max, const int32_t* const* ranks, const int32_t* const* slot_ranks,
+                             int E, const void* x, int x_per_slot,
                              const int32_t* ids, int T, int k, int act, void* const* y, int out, void* ws,
                              hipStream_t st) {
     if (n < 1 || n > kMaxMoeWin) return hipErrorInvalidConfiguration;
@@ -816,6 +839,7 @@ hipError_t launch_moe_decode(int n, const QW* w, const uint16_t* const* A, const
     for (int i = 0; i < n; ++i) {
         MoeLin& L = a.lin[i];
         L.q = w[i].q; L.s = w[i].s; L.z = w[i].z; L.A = A[i]; L.B = B[i]; L.ranks = ranks[i];
+        L.slot_rank = slot_ranks ? slot_ranks[i] : nullptr;
         L.y = y[i];
         L.t = reinterpret_cast<float*>(wsb + l.t[i]);
         L.q_stride = static_cast<size_t>(w[i].d_out) * (d_in / (32 / bits));

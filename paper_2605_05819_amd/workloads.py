@@ -160,6 +160,20 @@ def moe_expert_ranks(workload, layer, matrix, num_experts=MOE_EXPERTS, levels=(0
     return np.asarray(levels, dtype=np.int32)[g.integers(0, len(levels), num_experts)]
 
 
+def dynamic_slot_ranks(ids, weights, ranks, levels, r_max):
+    """Per-slot ranks from the expert-activation term (Section 4.3.3): slot
+    (t, j) routed to expert e with weight g gets ``align(k g r_e)`` capped at
+    ``r_max``, with ``k`` the routing width.  An even split (g = 1/k) leaves
+    the expert's own rank.  Returns int32 ``[T][k]``."""
+    ids = np.asarray(ids)
+    k = ids.shape[1]
+    out = np.zeros(ids.shape, dtype=np.int32)
+    for t in range(ids.shape[0]):
+        for j in range(k):
+            out[t, j] = min(align(k * float(weights[t][j]) * int(ranks[int(ids[t, j])]), levels), r_max)
+    return out
+
+
 # ------------------------------------------------------------------- routing
 
 def routing(T, workload, layer=0, num_experts=MOE_EXPERTS, k=MOE_TOPK):

@@ -171,7 +171,7 @@ def test_moe_window_validation():
     lib = cl.lib()
     v = ctypes.c_void_p
 
-    def call(n=2, qws=None, r_max=(8, 8), A=FAKE, ranks=FAKE, y=FAKE, ws_bytes=1 << 22):
+    def call(n=2, qws=None, r_max=(8, 8), A=FAKE, ranks=FAKE, y=FAKE, ws_bytes=1 << 22, slot=None):
         qws = qws or [_qw(), _qw(d_out=96)]
         q = (cl.QWeightC * len(qws))(*qws)
         Ap = (v * 2)(v(A), v(A))
@@ -179,7 +179,8 @@ def test_moe_window_validation():
         rm = (ctypes.c_int32 * 2)(*r_max)
         rk = (v * 2)(v(ranks), v(ranks))
         yp = (v * 2)(v(y), v(y))
-        return lib.cl_moe_linear_decode_window(n, q, Ap, Bp, rm, rk, 16, v(FAKE), 0, v(FAKE), 2, 4, cl.CL_FP16,
+        sr = None if slot is None else (v * 2)(v(slot), v(slot))
+        return lib.cl_moe_linear_decode_window(n, q, Ap, Bp, rm, rk, sr, 16, v(FAKE), 0, v(FAKE), 2, 4, cl.CL_FP16,
                                                yp, cl.CL_FP16, v(FAKE), ws_bytes, None)
 
     assert call(n=0) == cl.CL_EINVAL and call(n=5) == cl.CL_EINVAL
@@ -189,6 +190,8 @@ def test_moe_window_validation():
     assert call(r_max=(8, 300)) == cl.CL_EINVAL
     assert call(A=0) == cl.CL_EINVAL and call(ranks=0) == cl.CL_EINVAL and call(y=0) == cl.CL_EINVAL
     assert call(ws_bytes=64) == cl.CL_EWORKSPACE
+    assert call(slot=FAKE + 2) == cl.CL_EINVAL and b"slot_ranks" in lib.cl_last_error()
+    assert call(slot=FAKE, ws_bytes=64) == cl.CL_EWORKSPACE      # per-slot ranks accepted
     # workspace: one routing table, per-linear A x, shared activations
     qws = (cl.QWeightC * 2)(_qw(d_in=2048), _qw(d_in=2048, d_out=96))
     one = lib.cl_moe_workspace(ctypes.byref(qws[0]), 32, 128, 8, 8, 0)

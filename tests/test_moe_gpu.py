@@ -256,3 +256,39 @@ def test_window_matches_oracle():
     for y, (Q, s, z, A, B, ranks) in zip(ys, host):
         ref = _full_ref(Q, s, z, A, B, ranks, x.values, ids, False, bits, G, d_in)
         assert rel_l2(out_to_numpy(y), ref) <= REL_L2_TOL
+
+
+@pytest.mark.parametrize("x_per_slot", [False, True])
+@pytest.mark.parametrize("T,k", [(3, 4), (16, 8)])
+def test_slot_ranks_match_oracle(T, k, x_per_slot):
+    """Per-slot ranks from the routing weights (Section 4.3.3) on the VALU
+    path (3 x 4 slots) and the MFMA path (16 x 8 slots over 12 experts), against
+    the oracle with the same per-slot ranks."""
+    E, d_out, d_in, bits, G, r_max = 12, 100, 512, 4, 128, 16
+    Q, s, z, A, B = _oracle_experts(E, d_out, d_in, bits, G, r_max, 70)
+    ranks = wl.moe_expert_ranks(70, 0, 0, E, levels=(0, 4, 8, 16))
+    ids, w = wl.routing(T, 70, 0, E, k)
+    slot = wl.dynamic_slot_ranks(ids, w, ranks, (0, 4, 8, 16), r_max)
+    x = wl.activation((T, k, d_in) if x_per_slot else (T, d_in), 70, 0, 1)
+    ex = _device_experts(Q, s, z, A, B, ranks, d_out, d_in, bits, G, r_max)
+    ys = cl.moe_linear_decode_window([ex], dev_u16(x.bits, torch.float16), torch.from_numpy(ids).cuda(),
+                                     out_dtype=torch.float32, slot_ranks=[torch.from_numpy(slot).cuda()])
+    torch.cuda.synchronize()
+    experts = [(quant.dequant_packed(Q[e], s[e], z[e], bits, G, d_in), A[e], B[e]) for e in range(E)]
+    ref = moe.forward(experts, ranks, x.values, ids, x_per_slot, slot_ranks=slot)
+    assert rel_l2(out_to_numpy(ys[0]), ref) <= REL_L2_TOL
+    # the per-slot ranks matter here: the static ranks miss the reference
+    assert rel_l2(moe.forward(experts, ranks, x.values, ids, x_per_slot), ref) > 10 * REL_L2_TOL
+
+
+@pytest.mark.parametrize("T", [1, 64])
+def test_static_ranks_as_slot_ranks_are_bitwise_static(T):
+    E, d_in, k = 128, 512, 8
+    ex = _random_experts(E, 96, d_in, 16, 71)
+    ids = torch.from_numpy(wl.routing(T, 72, 0)[0]).cuda()
+    x = torch.from_numpy(wl.activation((T, d_in), 72, 0, 1).bits.view(np.int16)).view(torch.float16).cuda()
+    slot = ex.ranks[ids.long()].to(torch.int32).contiguous()
+    a = cl.moe_linear_decode_window([ex], x, ids)[0]
+    b = cl.moe_linear_decode_window([ex], x, ids, slot_ranks=[slot])[0]
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)

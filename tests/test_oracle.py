@@ -372,6 +372,28 @@ def test_moe_matches_scalar_loops_and_reduces_to_dense():
     np.testing.assert_array_equal(moe.forward(experts, ranks, X[perm], ids[perm], False), Y[perm])
 
 
+def test_moe_slot_ranks_follow_each_slot():
+    """Per-slot ranks (Section 4.3.3): each slot is its expert's dense layer at
+    that slot's own rank (scalar loops); the experts' ranks as slot ranks give
+    the static result exactly."""
+    g = np.random.default_rng(32)
+    E, d_out, d_in, r_max, T, k = 4, 3, 8, 3, 3, 2
+    experts = _tiny_experts(g, E, d_out, d_in, r_max)
+    ranks = [3, 1, 2, 0]
+    ids = np.array([[1, 0], [0, 0], [3, 2]])
+    slot = np.array([[0, 3], [1, 2], [3, 1]])
+    X = g.standard_normal((T, d_in))
+    Y = moe.forward(experts, ranks, X, ids, False, slot_ranks=slot)
+    for t in range(T):
+        for j in range(k):
+            W_hat, A, B = experts[ids[t, j]]
+            ref = _forward_scalar_loops(W_hat, A, B, slot[t, j], X[t:t + 1])[0]
+            np.testing.assert_allclose(Y[t, j], ref, rtol=1e-12, atol=1e-15)
+    static = np.array([[ranks[e] for e in row] for row in ids])
+    np.testing.assert_array_equal(moe.forward(experts, ranks, X, ids, False, slot_ranks=static),
+                                  moe.forward(experts, ranks, X, ids, False))
+
+
 def test_moe_forward_rows_is_forward_restricted_to_rows():
     g = np.random.default_rng(31)
     E, d_out, d_in, r_max, T, k = 4, 6, 16, 3, 2, 3

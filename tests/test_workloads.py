@@ -100,3 +100,25 @@ def test_standin_codes_shapes_ranges_and_seeding():
     assert set(np.unique(nib)) == set(range(16))
     q3, _, z3 = wl.standin_codes(2, 4, 128, 2, 64, 9)
     assert q3.shape == (2, 4, 8) and z3.max() <= 3
+
+
+def test_dynamic_slot_ranks_scale_with_routing_weight():
+    levels, r_max = (0, 8, 16, 32), 32
+    ranks = np.array([0, 8, 16, 32, 16], dtype=np.int32)
+    ids = np.array([[1, 2, 3, 4], [4, 3, 2, 1], [2, 2, 0, 3]])
+    k = ids.shape[1]
+    # an even split (g = 1/k) keeps every expert's own rank
+    even = np.full(ids.shape, 1.0 / k)
+    np.testing.assert_array_equal(wl.dynamic_slot_ranks(ids, even, ranks, levels, r_max), ranks[ids])
+    # real routing weights: every rank is a level, capped at r_max, and for one
+    # expert the rank does not fall as its weight grows
+    T = 32
+    ids, w = wl.routing(T, 9, 0, num_experts=5, k=4)
+    r = wl.dynamic_slot_ranks(ids, w, ranks, levels, r_max)
+    assert set(np.unique(r)) <= set(levels) and r.max() <= r_max
+    for e in range(5):
+        sel = ids == e
+        order = np.argsort(w[sel], kind="stable")
+        assert np.all(np.diff(r[sel][order]) >= 0)
+    # a heavy slot gets more than its expert's rank, a light one less
+    assert wl.dynamic_slot_ranks(np.array([[1, 4]]), np.array([[0.9, 0.1]]), ranks, levels, r_max).tolist() == [[16, 0]]
