@@ -65,6 +65,21 @@ __device__ __forceinline__ f16 act_to_f16(uint16_t b, int act) {
     return static_cast<f16>(v);
 }
 
+// 8 activations (one 16-byte load) as fp16, natural order; bf16 converted.
+__device__ __forceinline__ u32x4 act8_to_f16(u32x4 u, int act) {
+    if (act == DT_FP16) return u;
+    u32x4 o;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const uint32_t uk = u[k];
+        f16x2 h;
+        h.x = act_to_f16(static_cast<uint16_t>(uk & 0xffff), act);
+        h.y = act_to_f16(static_cast<uint16_t>(uk >> 16), act);
+        o[k] = __builtin_bit_cast(uint32_t, h);
+    }
+    return o;
+}
+
 __device__ __forceinline__ float act_to_f32(uint16_t b, int act) {
     return act == DT_FP16 ? f16_bits_to_f32(b) : bf16_bits_to_f32(b);
 }

@@ -493,20 +493,6 @@ void decode_kernel(DecodeArgs a) {
     }
 }
 
-// 8 activations as fp16 (bf16 converted), natural order.
-__device__ __forceinline__ u32x4 act8_f16(u32x4 u, int act) {
-    if (act == DT_FP16) return u;
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-        f16x2 h;
-        h.x = act_to_f16(static_cast<uint16_t>(u[k] & 0xffff), act);
-        h.y = act_to_f16(static_cast<uint16_t>(u[k] >> 16), act);
-        const uint32_t hb = __builtin_bit_cast(uint32_t, h);
-        u[k] = hb;
-    }
-    return u;
-}
-
 // Preparation for the MFMA backbone.  Workgroups [0, tiles): (linear, 16 rows
 // of A, pass of 16 tokens, K part kp): t partial[kp][tok][i] = sum over the
 // part's k of A[i][k] x[tok][k] for the pass's tokens on
@@ -559,7 +545,7 @@ __global__ __launch_bounds__(1024) void decode_prep_mfma_kernel(PrepMArgs a) {
                 const bool live = sb + u < s1;
                 const u32x4 zero = {0, 0, 0, 0};
                 const u32x4 a8 = (av && live) ? am[u] : zero;
-                const u32x4 x8 = (tv && live) ? act8_f16(xm[u], a.act) : zero;
+                const u32x4 x8 = (tv && live) ? act8_to_f16(xm[u], a.act) : zero;
                 acc = mfma(a8, x8, acc);
             }
         }
@@ -587,7 +573,7 @@ __global__ __launch_bounds__(1024) void decode_prep_mfma_kernel(PrepMArgs a) {
     const int tok = static_cast<int>(item / (16ll * wpr)) * 16 + rt;
     u32x4 o = {0u, 0u, 0u, 0u};
     if (tok < T) {
-        const u32x4 u = act8_f16(*reinterpret_cast<const u32x4*>(a.x + static_cast<size_t>(tok) * d_in + 8 * wi),
+        const u32x4 u = act8_to_f16(*reinterpret_cast<const u32x4*>(a.x + static_cast<size_t>(tok) * d_in + 8 * wi),
                                  a.act);
         // u[i] holds (x[2i], x[2i + 1]); pair p needs (x[p], x[p + 4])
 #pragma unroll

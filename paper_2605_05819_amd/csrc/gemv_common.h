@@ -7,17 +7,11 @@ namespace cl {
 
 // Load 8 consecutive activations as four f16x2 words (fp16 or bf16 input).
 __device__ __forceinline__ void load8_f16(const uint16_t* p, int act, uint32_t out[4]) {
-    const u32x4 u = *reinterpret_cast<const u32x4*>(p);
-    if (act == DT_FP16) {
-        out[0] = u[0]; out[1] = u[1]; out[2] = u[2]; out[3] = u[3];
-    } else {
+    const u32x4 u = act8_to_f16(*reinterpret_cast<const u32x4*>(p), act);
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            f16x2 h;
-            h.x = act_to_f16(static_cast<uint16_t>(u[k] & 0xffff), act);
-            h.y = act_to_f16(static_cast<uint16_t>(u[k] >> 16), act);
-            out[k] = __builtin_bit_cast(uint32_t, h);
-        }
+    for (int k = 0; k < 4; ++k) {
+        const uint32_t uk = u[k];
+        out[k] = uk;
     }
 }
 

@@ -96,21 +96,6 @@ struct MoeArgs {
     int ks, cps;             // K slices, chunks per slice
 };
 
-// 8 activations (one 16-byte load) as fp16, natural order; bf16 converted.
-__device__ __forceinline__ u32x4 act8_to_f16(u32x4 u, int act) {
-    if (act == DT_FP16) return u;
-    u32x4 o;
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-        const uint32_t uk = u[k];
-        f16x2 h;
-        h.x = act_to_f16(static_cast<uint16_t>(uk & 0xffff), act);
-        h.y = act_to_f16(static_cast<uint16_t>(uk >> 16), act);
-        o[k] = __builtin_bit_cast(uint32_t, h);
-    }
-    return o;
-}
-
 template <int BITS>
 __global__ __launch_bounds__(256) void moe_prep_kernel(MoeArgs a) {
     constexpr int CPW = 32 / BITS, HPW = CPW / 2, PPC = 4 * HPW;

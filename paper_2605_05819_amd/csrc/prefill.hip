@@ -41,15 +41,7 @@ constexpr int BM = 128, BN = 256, BK = 128;
 
 // 8 activations -> fp16, in the pair order (x0,x4),(x1,x5),(x2,x6),(x3,x7)
 __device__ __forceinline__ u32x4 act8_permuted(u32x4 u, int act) {
-    if (act != DT_FP16) {
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            f16x2 h;
-            h.x = act_to_f16(static_cast<uint16_t>(u[k] & 0xffff), act);
-            h.y = act_to_f16(static_cast<uint16_t>(u[k] >> 16), act);
-            u[k] = __builtin_bit_cast(uint32_t, h);
-        }
-    }
+    u = act8_to_f16(u, act);
     const uint32_t u0 = u[0], u1 = u[1], u2 = u[2], u3 = u[3];
     u32x4 r;
     r[0] = (u0 & 0xffffu) | (u2 << 16);           // x0, x4
@@ -57,20 +49,6 @@ __device__ __forceinline__ u32x4 act8_permuted(u32x4 u, int act) {
     r[2] = (u1 & 0xffffu) | (u3 << 16);           // x2, x6
     r[3] = (u1 >> 16) | (u3 & 0xffff0000u);       // x3, x7
     return r;
-}
-
-// 8 activations -> fp16, natural order
-__device__ __forceinline__ u32x4 act8_natural(u32x4 u, int act) {
-    if (act != DT_FP16) {
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            f16x2 h;
-            h.x = act_to_f16(static_cast<uint16_t>(u[k] & 0xffff), act);
-            h.y = act_to_f16(static_cast<uint16_t>(u[k] >> 16), act);
-            u[k] = __builtin_bit_cast(uint32_t, h);
-        }
-    }
-    return u;
 }
 
 // One 32-bit word of 4-bit codes -> 8 fp16 values s * (q - z) in the order
@@ -196,7 +174,7 @@ __global__ __launch_bounds__(NW * 64) void lowrank_t_kernel(const uint16_t* __re
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const bool live = k0 + 32 * u < kend;
-            u32x4 x8 = act8_natural(xa[u], act);
+            u32x4 x8 = act8_to_f16(xa[u], act);
             if (!mval || !live) x8 = u32x4{0, 0, 0, 0};
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
