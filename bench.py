@@ -48,7 +48,7 @@ MFMA_F16_PEAK_TFLOPS = 2500.0
 GATE_TRAFFIC = {"fetch_bytes": (32405 + 706) * 1024, "write_bytes": (56 + 9) * 1024,
                 "sources": ("paper_2605_05819_amd/csrc/decode.hip", "paper_2605_05819_amd/csrc/gemv_common.h",
                             "paper_2605_05819_amd/csrc/cl_device.h"),
-                "sha256": "0a6e73388edd9d66506a0eecbffb39e677b6ab9a4403cbd7ca2e3ab7bedc6b18"}
+                "sha256": "6ed14557afe52542d98a2a71641fb02c7a0ee3d596df14f413df2312f5e6fbe9"}
 
 
 def sources_sha256(paths):
