@@ -209,6 +209,28 @@ cl_status cl_linear_decode_window(int32_t n, const cl_qweight* w, const cl_lowra
 size_t cl_linear_window_workspace(int32_t n, const cl_qweight* w, const cl_lowrank* c, int32_t tokens);
 
 /*
+ * cl_linear_decode_glu -- the gate/up window of a gated MLP with its
+ * elementwise epilogue fused into the backbone launch:
+ *     h = SiLU(g) * u,  g = gate(x), u = up(x),  SiLU(v) = v / (1 + e^-v),
+ * each of g and u the compensated linear of cl_linear_decode (Section 4.1)
+ * taken as one window (Section 4.2.2, Communication Fusion).  g and u stay in
+ * fp32 registers: the epilogue is applied to them unrounded and h is rounded
+ * once to out_dtype; neither g nor u is written to memory.
+ *
+ *  w          host array {gate, up}: same d_in, d_out, bits and group_size
+ *  c          host array {gate factors, up factors} (rank 0 allowed), or NULL
+ *  x          device [T][d_in] of act_dtype, 16-byte aligned
+ *  h          device [T][d_out] of out_dtype
+ *  ws         device workspace of cl_linear_window_workspace(2, w, c, T)
+ *             bytes, 256-byte aligned
+ * Errors: as cl_linear_decode_window with n = 2, and CL_EINVAL when gate and
+ * up differ in d_out.
+ */
+cl_status cl_linear_decode_glu(const cl_qweight* w, const cl_lowrank* c, const void* x, int32_t T,
+                               int32_t act_dtype, void* h, int32_t out_dtype, void* ws, size_t ws_bytes,
+                               void* stream);
+
+/*
  * cl_linear_prefill -- compensated linear for many tokens (Section 4.1):
  *     Y = X deq(Q)^T + (X A[:rank]^T) B[:, :rank]^T.
  * A dense contraction on MFMA: a first kernel writes X' (X as fp16 in the

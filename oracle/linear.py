@@ -12,6 +12,12 @@ the returned compensation) is the ``+``; the compensation worker's inner product
 (Algorithm 2) is the bracketed term.  Decode (few tokens) and prefill (many
 tokens) compute the same function; only the kernels differ.  Everything is fp64
 and unrounded; the caller rounds to the output dtype when it compares.
+
+The gate and up projections of a gated MLP (the Llama and Qwen models the
+paper evaluates) read the same input and form one compensation window
+(Section 4.2.2, Communication Fusion); their outputs meet elementwise as
+``SiLU(g) * u``.  :func:`forward_glu` is that product of two compensated
+forwards, unrounded.
 """
 
 import numpy as np
@@ -51,3 +57,18 @@ def forward_rows(Q, scales, zeros, bits, group_size, A, B, rank, X, rows):
     zr = np.asarray(zeros)[rows]
     Br = np.asarray(B)[rows] if int(rank) > 0 else B
     return forward_packed(Qr, sr, zr, bits, group_size, A, Br, rank, X)
+
+
+def silu(v):
+    """``SiLU(v) = v / (1 + e^-v)`` in fp64 (for ``v`` far below zero ``e^-v``
+    overflows to inf and the quotient is a signed zero)."""
+    v = np.asarray(v, dtype=np.float64)
+    with np.errstate(over="ignore"):
+        return v / (1.0 + np.exp(-v))
+
+
+def forward_glu(gate, up, X):
+    """``SiLU(g) * u`` with ``g`` and ``u`` the compensated forwards of the
+    gate and up linears, each given as ``(W_hat, A, B, rank)``; fp64
+    ``[T][d_out]``."""
+    return silu(forward(*gate, X)) * forward(*up, X)

@@ -79,6 +79,9 @@ _SIGNATURES = {
                                                  ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
                                                  ctypes.POINTER(ctypes.c_void_p), ctypes.c_int32, ctypes.c_void_p,
                                                  ctypes.c_size_t, ctypes.c_void_p]),
+    "cl_linear_decode_glu": (ctypes.c_int32, [ctypes.POINTER(QWeightC), ctypes.POINTER(LowRankC), ctypes.c_void_p,
+                                              ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32,
+                                              ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
 }
 
 
@@ -216,6 +219,20 @@ def linear_decode_window(ws_, cs, x, out_dtype=torch.float16, ys=None, ws=None, 
     _check(lib().cl_linear_decode_window(n, qa, la, _ptr(x), T, _DTYPE_CODE[x.dtype], yp,
                                          _DTYPE_CODE[ys[0].dtype], _ptr(ws), ws.numel(), _stream(stream)))
     return ys
+
+
+def linear_decode_glu(gate_up, cs, x, out_dtype=torch.float16, h=None, ws=None, stream=None):
+    """``cl_linear_decode_glu``: h = SiLU(gate x) * (up x) [T][d_out] for
+    gate_up = (gate, up) and their factors cs (or None)."""
+    T = x.shape[0]
+    if h is None:
+        h = torch.empty((T, gate_up[0].d_out), dtype=out_dtype, device=x.device)
+    qa, la = _window_structs(gate_up, cs)
+    if ws is None:
+        ws = workspace(lib().cl_linear_window_workspace(2, qa, la, T), x.device)
+    _check(lib().cl_linear_decode_glu(qa, la, _ptr(x), T, _DTYPE_CODE[x.dtype], _ptr(h), _DTYPE_CODE[h.dtype],
+                                      _ptr(ws), ws.numel(), _stream(stream)))
+    return h
 
 
 def prefill_workspace(w, c, M):

@@ -148,11 +148,13 @@ cl_status check_window(int32_t n, const cl_qweight* w, const cl_lowrank* c, cl::
 
 cl_status decode_common(int32_t n, const cl_qweight* w, const cl_lowrank* c, const void* x, int32_t T,
                         int32_t act_dtype, void* const* y, int32_t out_dtype, void* ws, size_t ws_bytes,
-                        void* stream, const char* who) {
+                        void* stream, const char* who, bool glu = false) {
     cl::QW qw[8];
     cl::LR lr[8];
     cl_status st = check_window(n, w, c, qw, lr, who);
     if (st) return st;
+    if (glu && qw[0].d_out != qw[1].d_out)
+        return fail(CL_EINVAL, "%s: gate and up differ in d_out (%d, %d)", who, qw[0].d_out, qw[1].d_out);
     if (T < 1 || T > 64) return fail(CL_EINVAL, "%s: T must be in 1..64 (got %d)", who, T);
     if (act_dtype != CL_FP16 && act_dtype != CL_BF16)
         return fail(CL_EINVAL, "%s: act_dtype must be CL_FP16 or CL_BF16", who);
@@ -169,7 +171,7 @@ cl_status decode_common(int32_t n, const cl_qweight* w, const cl_lowrank* c, con
         return fail(CL_EWORKSPACE, "%s: workspace of %zu bytes needed (got %zu)", who, need, ws ? ws_bytes : 0);
     if (!aligned(ws, 256)) return fail(CL_EINVAL, "%s: workspace must be 256-byte aligned", who);
     return hip_status(cl::launch_linear_decode(n, qw, lr, x, T, act_dtype, y, out_dtype, ws,
-                                               static_cast<hipStream_t>(stream)), who);
+                                               static_cast<hipStream_t>(stream), glu), who);
 }
 
 size_t window_workspace(int32_t n, const cl_qweight* w, const cl_lowrank* c, int32_t tokens) {
@@ -355,6 +357,14 @@ cl_status cl_linear_decode_window(int32_t n, const cl_qweight* w, const cl_lowra
                                   size_t ws_bytes, void* stream) {
     return decode_common(n, w, c, x, T, act_dtype, y, out_dtype, ws, ws_bytes, stream,
                          "cl_linear_decode_window");
+}
+
+cl_status cl_linear_decode_glu(const cl_qweight* w, const cl_lowrank* c, const void* x, int32_t T,
+                               int32_t act_dtype, void* h, int32_t out_dtype, void* ws, size_t ws_bytes,
+                               void* stream) {
+    void* hs[2] = {h, h};
+    return decode_common(2, w, c, x, T, act_dtype, h ? hs : nullptr, out_dtype, ws, ws_bytes, stream,
+                         "cl_linear_decode_glu", true);
 }
 
 }  // extern "C"

@@ -27,11 +27,12 @@ hipError_t launch_quantize_pack(const float* W, int d_out, int d_in, int bits, i
 hipError_t launch_dequantize(const QW& w, float* out, hipStream_t st);
 
 // Decode of a window of n (1..8) linears sharing d_in, bits, group size and
-// the activations x; arguments already validated.
+// the activations x; arguments already validated.  glu: n = 2 linears of the
+// same d_out (gate, up) and one output y[0] = SiLU(gate x) * (up x).
 size_t decode_workspace_bytes(int n, const QW* w, const LR* c, int T);
 bool decode_fits(const QW& w);   // d_in within the kernel's K-slice limit
 hipError_t launch_linear_decode(int n, const QW* w, const LR* c, const void* x, int T, int act,
-                                void* const* y, int out, void* ws, hipStream_t st);
+                                void* const* y, int out, void* ws, hipStream_t st, bool glu = false);
 
 // Prefill: T = X A^T into the workspace, then the MFMA GEMM with the rank
 // fold; d_in must be a multiple of 64.

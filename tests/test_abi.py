@@ -129,6 +129,21 @@ def test_window_validation():
                                        ctypes.c_void_p(FAKE), 1 << 20, None) == cl.CL_EINVAL
 
 
+def test_glu_validation():
+    lib = cl.lib()
+    v = ctypes.c_void_p
+
+    def call(qws=None, h=FAKE, ws_bytes=1 << 20):
+        q = (cl.QWeightC * 2)(*(qws or [_qw(), _qw()]))
+        return lib.cl_linear_decode_glu(q, None, v(FAKE), 1, cl.CL_FP16, v(h), cl.CL_FP16, v(FAKE), ws_bytes, None)
+
+    assert call(qws=[_qw(), _qw(d_out=32)]) == cl.CL_EINVAL and b"d_out" in lib.cl_last_error()
+    assert call(qws=[_qw(), _qw(d_in=512)]) == cl.CL_EINVAL and b"share d_in" in lib.cl_last_error()
+    assert call(h=0) == cl.CL_EINVAL
+    assert call(h=FAKE + 1) == cl.CL_EINVAL
+    assert call(ws_bytes=64) == cl.CL_EWORKSPACE
+
+
 def test_moe_validation():
     lib = cl.lib()
     def call(qw=None, A=FAKE, B=FAKE, r_max=8, ranks=FAKE, E=16, x=FAKE, xps=0, ids=FAKE, T=2, k=4,

@@ -261,3 +261,70 @@ def test_window_without_factors_and_two_bit():
     for y, (Q, s, z) in zip(ys, host):
         ref = linear.forward_packed(Q, s, z, 2, 64, None, None, 0, x.values)
         assert rel_l2(out_to_numpy(y), ref) <= REL_L2_TOL
+
+
+def _glu_pair(d_out, d_in, bits, G, ranks, seed):
+    pair = [_layer_dev(d_out, d_in, bits, G, 64, r, seed + i) for i, r in enumerate(ranks)]
+    return [p[0] for p in pair], [p[1] for p in pair], [p[2] for p in pair]
+
+
+def _glu_ref_rows(host, ranks, bits, G, d_in, X, rows):
+    """Oracle SiLU(gate x) * (up x) on a row sample (each output element
+    depends only on its own rows of the backbone and of B)."""
+    mats = []
+    for (Q, s, z, A, B), r in zip(host, ranks):
+        W_hat = quant.dequant_packed(Q[rows], s[rows], z[rows], bits, G, d_in)
+        mats.append((W_hat, A, B[rows], r))
+    return linear.forward_glu(mats[0], mats[1], X)
+
+
+@pytest.mark.parametrize("T,act,out,bits,G,d_out,d_in", [
+    (1, torch.float16, torch.float16, 4, 128, 1000, 2048),      # one token per pass, one K slice
+    (2, torch.bfloat16, torch.float32, 4, 128, 1000, 4096),     # two tokens per pass (prefetch), 2 K slices
+    (3, torch.float16, torch.bfloat16, 4, 128, 1000, 2048),     # MFMA backbone, ragged last tile
+    (5, torch.float16, torch.float16, 2, 64, 700, 1024),        # 2-bit, two passes of 4 tokens
+    (1, torch.float16, torch.float32, 4, 128, 14336, 4096),     # Llama-8B gate/up, one token
+    (16, torch.float16, torch.float32, 4, 128, 14336, 4096),    # Llama-8B gate/up, MFMA with 4 tiles per wave
+])
+def test_glu_matches_oracle(T, act, out, bits, G, d_out, d_in):
+    """cl_linear_decode_glu = SiLU(gate x) * (up x) of the fp64 oracle (gate
+    rank 64, up rank 17): the fp32 result within the bar, and the fp16/bf16
+    result its round-to-nearest-even, bit for bit.  (On the MFMA backbone the
+    fp16 rounding of dequantized weights leaves 2-3e-4 before the output
+    rounding, which moves enough bf16 rounding decisions to put a bf16 result
+    at 1.06e-3 from the rounded oracle in the 3-token case.)"""
+    ranks = (64, 17)
+    ws_, cs, host = _glu_pair(d_out, d_in, bits, G, ranks, 70 + T)
+    x = wl.activation((T, d_in), 12, 70, dtype="fp16" if act == torch.float16 else "bf16")
+    xd = dev_u16(x.bits, act)
+    h32 = cl.linear_decode_glu(ws_, cs, xd, out_dtype=torch.float32)
+    rows = np.arange(d_out) if d_out <= 1000 else np.random.default_rng(T).choice(d_out, 300, replace=False)
+    ref = _glu_ref_rows(host, ranks, bits, G, d_in, x.values, rows)
+    err = rel_l2(out_to_numpy(h32)[:, rows], ref)
+    assert err <= REL_L2_TOL, err
+    if out != torch.float32:
+        h = cl.linear_decode_glu(ws_, cs, xd, out_dtype=out)
+        assert torch.equal(h, h32.to(out))
+
+
+@pytest.mark.parametrize("T", [1, 2, 16])
+def test_glu_is_the_window_with_its_epilogue(T):
+    """The fused epilogue sees the same fp32 gate and up values as the window
+    call writes: SiLU(y_gate) * y_up from the window's fp32 outputs matches to
+    fp32 rounding; two calls agree bit for bit."""
+    ws_, cs, _ = _glu_pair(1536, 2048, 4, 128, (32, 0), 80)
+    x = wl.activation((T, 2048), 12, 80)
+    xd = dev_u16(x.bits, torch.float16)
+    yg, yu = cl.linear_decode_window(ws_, cs, xd, out_dtype=torch.float32)
+    want = torch.nn.functional.silu(yg) * yu
+    h = cl.linear_decode_glu(ws_, cs, xd, out_dtype=torch.float32)
+    torch.testing.assert_close(h, want, rtol=1e-5, atol=1e-6)
+    assert torch.equal(cl.linear_decode_glu(ws_, cs, xd, out_dtype=torch.float32), h)
+
+
+def test_glu_without_factors():
+    ws_, _, host = _glu_pair(512, 1024, 4, 128, (0, 0), 90)
+    x = wl.activation((1, 1024), 12, 90)
+    h = cl.linear_decode_glu(ws_, None, dev_u16(x.bits, torch.float16), out_dtype=torch.float32)
+    ref = _glu_ref_rows(host, (0, 0), 4, 128, 1024, x.values, np.arange(512))
+    assert rel_l2(out_to_numpy(h), ref) <= REL_L2_TOL

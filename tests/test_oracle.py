@@ -303,6 +303,42 @@ def test_forward_matches_scalar_triple_loops(rank):
     np.testing.assert_allclose(got, _forward_scalar_loops(W_hat, A, B, rank, X), rtol=1e-12, atol=1e-14)
 
 
+def test_silu_against_logistic_function_and_lambert_w_minimum():
+    """SiLU(v) = v * sigma(v) with scipy's logistic function; its odd part is
+    v / 2 (SiLU(v) - SiLU(-v) = v); its minimum, where 1 + v (1 - sigma(v)) = 0,
+    is at v* = -1 - W(1/e) with value v* + 1 = -W(1/e) (Lambert W)."""
+    from scipy import special
+    v = np.concatenate([np.linspace(-60.0, 60.0, 2001), [-1000.0, -745.0, 0.0, 745.0, 1000.0]])
+    got = linear.silu(v)
+    np.testing.assert_allclose(got, v * special.expit(v), rtol=1e-14, atol=1e-300)
+    np.testing.assert_allclose(linear.silu(v) - linear.silu(-v), v, rtol=1e-14, atol=1e-14)
+    w = float(np.real(special.lambertw(np.exp(-1.0))))
+    vmin = -1.0 - w
+    assert abs(float(linear.silu(vmin)) - (-w)) < 1e-15
+    grid = np.linspace(vmin - 0.5, vmin + 0.5, 100001)
+    assert float(linear.silu(grid).min()) >= -w - 1e-15
+    assert linear.silu(np.array([-1000.0]))[0] == 0.0 and linear.silu(np.array([1000.0]))[0] == 1000.0
+
+
+def test_forward_glu_matches_scalar_loops():
+    """SiLU(gate x) * (up x) on a 5 x 16 pair of compensated linears, every
+    output by scalar loops and math.exp."""
+    import math
+    g = np.random.default_rng(24)
+    d_out, d_in, T = 5, 16, 3
+    mats = []
+    for rank in (3, 0):
+        W = (0.05 * g.standard_normal((d_out, d_in))).astype(np.float32)
+        Q, s, z = quant.quantize_pack(W, 4, 8)
+        mats.append((quant.dequant_packed(Q, s, z, 4, 8, d_in), g.standard_normal((4, d_in)),
+                     g.standard_normal((d_out, 4)), rank))
+    X = g.standard_normal((T, d_in))
+    yg = _forward_scalar_loops(*mats[0], X)
+    yu = _forward_scalar_loops(*mats[1], X)
+    want = [[yg[t][o] / (1.0 + math.exp(-yg[t][o])) * yu[t][o] for o in range(d_out)] for t in range(T)]
+    np.testing.assert_allclose(linear.forward_glu(mats[0], mats[1], X), want, rtol=1e-12, atol=1e-14)
+
+
 def test_forward_rows_is_a_row_sample_of_forward():
     g = np.random.default_rng(21)
     W = (0.02 * g.standard_normal((40, 64))).astype(np.float32)
