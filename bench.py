@@ -16,12 +16,13 @@ Prints one JSON line: whole-job algorithmic HBM throughput (GB/s) of the step,
 the roofline of the dominant call (the gate matrix, 14336 x 4096) timed with
 HIP events on the stream it runs on, the fp64 CPU oracle timed on a bounded
 sample of the same layer, and (unless --no-extras) the other measured
-workloads: the layer at 4 and 16 tokens, the 2-bit layer with its gate rank
+workloads: the layer at 4 and 16 tokens, the gate,up window against the gated
+call (SiLU(gate x) * (up x) fused), the 2-bit layer with its gate rank
 sweep, prefill (M = 2048) in TFLOP/s and the 48-layer MoE decode.
 
 --copy-calibration runs only a plain 256 MiB device-to-device copy (the
 reference kernel for scaling HBM traffic counters) and prints its size;
---only {decode,tokens,layer2bit,prefill,moe} runs one workload (for
+--only {decode,tokens,glu,layer2bit,prefill,moe} runs one workload (for
 profiling): "decode" prints the line above without extras or CPU baseline,
 the others print their own results.
 """
@@ -76,7 +77,7 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-extras", action="store_true")
     p.add_argument("--copy-calibration", action="store_true")
-    p.add_argument("--only", choices=("decode", "tokens", "layer2bit", "prefill", "moe"), default=None,
+    p.add_argument("--only", choices=("decode", "tokens", "glu", "layer2bit", "prefill", "moe"), default=None,
                    help="run one workload and print its own JSON line (for profiling)")
     return p.parse_args()
 
@@ -207,6 +208,41 @@ def bench_tokens(torch, cl, wl, timer, copies, layer, dev):
         ms, _, _ = layer_step(torch, cl, wl, timer, copies, layer, T, dev, 40, 8)
         b = sum(algorithmic_bytes(s, T) for s in layer.linears)
         res["layer_T%d" % T] = {"ms_per_step": round(ms, 5), "gbs": round(b / (ms * 1e-3) / 1e9, 1)}
+    return res
+
+
+def bench_glu(torch, cl, wl, timer, copies, layer, dev):
+    """The gate,up window alone, the window followed by torch's SiLU and
+    product (the unfused gated MLP input), and the gated call (SiLU(gate x) *
+    (up x) in the backbone launch) at 1 and 16 tokens: us per call over the
+    copies."""
+    names = [s.name for s in layer.linears]
+    gi, ui = names.index("gate"), names.index("up")
+    d_in, d_out = layer.linears[gi].d_in, layer.linears[gi].d_out
+    res = {}
+    for T in (1, 16):
+        x = torch.from_numpy(wl.activation((T, d_in), layer.index, 0, gi).bits.view(np.int16)).view(
+            torch.float16).to(dev)
+        yg, yu, h = (torch.empty((T, d_out), dtype=torch.float16, device=dev) for _ in range(3))
+        pairs = [([k[gi][0], k[ui][0]], [k[gi][1], k[ui][1]]) for k in copies]
+        ws = cl.workspace(cl.window_workspace(*pairs[0], T), dev)
+
+        def win():
+            for w2, c2 in pairs:
+                cl.linear_decode_window(w2, c2, x, ys=[yg, yu], ws=ws, stream=timer.stream)
+
+        def win_then_torch():
+            for w2, c2 in pairs:
+                cl.linear_decode_window(w2, c2, x, ys=[yg, yu], ws=ws, stream=timer.stream)
+                torch.mul(torch.nn.functional.silu(yg), yu, out=h)
+
+        def glu():
+            for w2, c2 in pairs:
+                cl.linear_decode_glu(w2, c2, x, h=h, ws=ws, stream=timer.stream)
+        gw, gt, gg = timer.capture(win), timer.capture(win_then_torch), timer.capture(glu)
+        res["T%d" % T] = {"window_us": round(timer.time([gw], 20) * 1e3 / len(pairs), 3),
+                          "window_then_torch_silu_mul_us": round(timer.time([gt], 20) * 1e3 / len(pairs), 3),
+                          "glu_us": round(timer.time([gg], 20) * 1e3 / len(pairs), 3)}
     return res
 
 
@@ -352,6 +388,9 @@ def main():
     if only == "tokens":
         print(json.dumps(bench_tokens(torch, cl, wl, timer, copies, layer, dev)))
         return
+    if only == "glu":
+        print(json.dumps({"gate_up_window_vs_glu": bench_glu(torch, cl, wl, timer, copies, layer, dev)}))
+        return
 
     ms_step, xs, ys = layer_step(torch, cl, wl, timer, copies, layer, T, dev, args.steps, args.warmup)
     step_bytes = sum(algorithmic_bytes(s, T) for s in specs)
@@ -368,6 +407,7 @@ def main():
     extras = None
     if only is None and not args.no_extras:
         extras = bench_tokens(torch, cl, wl, timer, copies, layer, dev)
+        extras["gate_up_window_vs_glu"] = bench_glu(torch, cl, wl, timer, copies, layer, dev)
         del copies
         torch.cuda.empty_cache()
         extras["layer_2bit_g64_T1"] = bench_layer2bit(torch, cl, wl, timer, dev, args.rotate_gib)

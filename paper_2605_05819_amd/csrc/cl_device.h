@@ -84,9 +84,11 @@ __device__ __forceinline__ float act_to_f32(uint16_t b, int act) {
     return act == DT_FP16 ? f16_bits_to_f32(b) : bf16_bits_to_f32(b);
 }
 
-// SiLU(g) u = g / (1 + e^-g) * u in fp32 (for g far below zero e^-g is
-// inf and the result a signed zero)
-__device__ __forceinline__ float silu_mul(float g, float u) { return g / (1.f + __expf(-g)) * u; }
+// SiLU(g) u = g / (1 + e^-g) * u in fp32 with a reciprocal-based quotient
+// (a few ulp; the IEEE division sequence cost the one-token backbone a
+// spilled register); for g far below zero e^-g is inf, its reciprocal 0 and
+// the result a signed zero
+__device__ __forceinline__ float silu_mul(float g, float u) { return __fdividef(g, 1.f + __expf(-g)) * u; }
 
 __device__ __forceinline__ void store_out(void* y, size_t idx, float v, int out) {
     if (out == DT_FP32) {
