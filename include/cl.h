@@ -334,6 +334,62 @@ cl_status cl_moe_linear_decode_window(int32_t n, const cl_qweight* w_expert0, co
 size_t cl_moe_window_workspace(int32_t n, const cl_qweight* w_expert0, const int32_t* r_max,
                                int32_t num_experts, int32_t T, int32_t k, int32_t x_per_slot);
 
+/*
+ * cl_allocate_ranks -- compensation ranks of the n linears of one
+ * compensation window from their residual spectra (host code; no GPU).
+ * Section 4.3.1 (intrinsic recoverability), Section 4.3.4 (priority and
+ * rank allocation) and Appendix B.1 (second-difference knee, window
+ * normalisation, two-stage allocation, discrete alignment):
+ *   1. per linear, sigma / sigma_1 and its second differences at the
+ *      interior indices; if the first largest exceeds tau, the salient set
+ *      is the leading components up to and including that index and
+ *      phi = mean(salient sigma) / mean(residual sigma), else the salient
+ *      set is empty and phi = 1 (a residual set of zeros gives phi = inf,
+ *      which takes the window's whole recoverability share);
+ *   2. V = phi / sum(phi), S = sens / sum(sens) over the window (all-zero
+ *      sensitivities count as equal), P = (V S) / sum(V S) * layer_score,
+ *      continuous rank P * r_std;
+ *   3. the window's total continuous rank is shared in proportion to the
+ *      continuous ranks, first over the salient sets (each capped at its
+ *      size), what is left over the residual sets (capped likewise), by
+ *      water-filling;
+ *   4. each result goes to the nearest of levels[] not above
+ *      min(r_max, len[i]) (ties to the lower).
+ * All arithmetic is fp64 with sums in index order.  MoE expert activation
+ * (Section 4.3.3) scales a slot's rank afterwards (see slot_ranks above).
+ *
+ *  n            1..64 linears
+ *  sigma        host array of n host pointers; sigma[i] holds len[i] >= 1
+ *               singular values, finite, >= 0, descending (the sigma that
+ *               cl_build_compensation writes, copied to the host)
+ *  sens         host [n] matrix-level sensitivities D_i >= 0 (the paper's
+ *               KL divergences; any non-negative proxy)
+ *  layer_score  S_l >= 0 (see cl_layer_sensitivity)
+ *  r_std        reference rank >= 0 (the largest rank whose compensation
+ *               stays hidden behind the backbone, Section 4.3.4)
+ *  levels       host [nlevels] admissible ranks, strictly increasing,
+ *               levels[0] == 0, 1 <= nlevels <= 64
+ *  r_max        cap on every rank (the stored factor count)
+ *  tau          knee threshold >= 0 (0.01 in the paper)
+ *  ranks        host [n] output
+ * Errors: CL_EINVAL for any argument outside the above (nothing written).
+ */
+cl_status cl_allocate_ranks(int32_t n, const float* const* sigma, const int32_t* len, const double* sens,
+                            double layer_score, double r_std, const int32_t* levels, int32_t nlevels,
+                            int32_t r_max, double tau, int32_t* ranks);
+
+/*
+ * cl_layer_sensitivity -- layer-level scores S_l from layer-level
+ * sensitivities D_l (Section 4.3.2; Appendix B.1; host code): the K layers
+ * with the largest D (ties to the lower index) score 1, every other layer
+ * D_l / min over those K of D (1 when that minimum is 0).
+ *
+ *  L      1..4096 layers;  D  host [L], finite, >= 0
+ *  K      1..L;            S  host [L] output
+ * Errors: CL_EINVAL for any argument outside the above (nothing written).
+ */
+cl_status cl_layer_sensitivity(int32_t L, const double* D, int32_t K, double* S);
+
 /* Message describing the last non-CL_OK status returned on this thread. */
 const char* cl_last_error(void);
 

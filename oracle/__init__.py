@@ -29,6 +29,7 @@ quant   -- fp16 rounding, quantize, pack/unpack, dequantize
 comp    -- compensation factors from the SVD of the residual
 linear  -- the compensated forward (decode and prefill compute the same thing)
 moe     -- expert-gathered compensated forward
+ranks   -- rank allocation from the residual spectra (Section 4.3, Appendix B.1)
 """
 
-from . import quant, comp, linear, moe  # noqa: F401
+from . import quant, comp, linear, moe, ranks  # noqa: F401

@@ -3,9 +3,10 @@
     python -m paper_2605_05819_amd.build
 
 Every source is compiled with hipcc for gfx950 only.  Packed fp32 VALU
-instructions are disabled for all device code; the quantizer is built with
-floating-point contraction off so its fp64 arithmetic is exactly the stated
-sequence of IEEE operations.
+instructions are disabled for all device code; the quantizer, the
+compensation builder and the rank allocator are built with floating-point
+contraction off so their fp64 arithmetic is exactly the stated sequence of
+IEEE operations.
 """
 
 import os
@@ -18,8 +19,8 @@ CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(os.path.dirname(HERE), "_build")
 LIB = os.path.join(HERE, "libcl.so")
 
-SOURCES = ["api.hip", "quant.hip", "decode.hip", "prefill.hip", "moe.hip", "comp.hip"]
-EXTRA = {"quant.hip": ["-ffp-contract=off"], "comp.hip": ["-ffp-contract=off"]}
+SOURCES = ["api.hip", "quant.hip", "decode.hip", "prefill.hip", "moe.hip", "comp.hip", "ranks.hip"]
+EXTRA = {"quant.hip": ["-ffp-contract=off"], "comp.hip": ["-ffp-contract=off"], "ranks.hip": ["-ffp-contract=off"]}
 ARCH = "gfx950"
 FLAGS = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=" + ARCH,
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

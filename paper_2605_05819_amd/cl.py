@@ -10,6 +10,7 @@ import os
 from dataclasses import dataclass
 from typing import Optional
 
+import numpy as np
 import torch
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libcl.so")
@@ -79,6 +80,13 @@ _SIGNATURES = {
                                                  ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
                                                  ctypes.POINTER(ctypes.c_void_p), ctypes.c_int32, ctypes.c_void_p,
                                                  ctypes.c_size_t, ctypes.c_void_p]),
+    "cl_allocate_ranks": (ctypes.c_int32, [ctypes.c_int32, ctypes.POINTER(ctypes.c_void_p),
+                                           ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_double),
+                                           ctypes.c_double, ctypes.c_double, ctypes.POINTER(ctypes.c_int32),
+                                           ctypes.c_int32, ctypes.c_int32, ctypes.c_double,
+                                           ctypes.POINTER(ctypes.c_int32)]),
+    "cl_layer_sensitivity": (ctypes.c_int32, [ctypes.c_int32, ctypes.POINTER(ctypes.c_double), ctypes.c_int32,
+                                              ctypes.POINTER(ctypes.c_double)]),
     "cl_linear_decode_glu": (ctypes.c_int32, [ctypes.POINTER(QWeightC), ctypes.POINTER(LowRankC), ctypes.c_void_p,
                                               ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32,
                                               ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
@@ -233,6 +241,32 @@ def linear_decode_glu(gate_up, cs, x, out_dtype=torch.float16, h=None, ws=None, 
     _check(lib().cl_linear_decode_glu(qa, la, _ptr(x), T, _DTYPE_CODE[x.dtype], _ptr(h), _DTYPE_CODE[h.dtype],
                                       _ptr(ws), ws.numel(), _stream(stream)))
     return h
+
+
+def allocate_ranks(sigmas, sens, layer_score, r_std, levels, r_max, tau=0.01):
+    """``cl_allocate_ranks`` (host code): ranks of one compensation window
+    from the linears' descending singular values (sequences of float32),
+    their sensitivities and the layer score; returns a list of ints."""
+    n = len(sigmas)
+    arrs = [np.ascontiguousarray(np.asarray(sg, dtype=np.float32)) for sg in sigmas]
+    sp = (ctypes.c_void_p * n)(*[a.ctypes.data for a in arrs])
+    ln = (ctypes.c_int32 * n)(*[a.size for a in arrs])
+    sd = (ctypes.c_double * n)(*[float(v) for v in sens])
+    lv = (ctypes.c_int32 * len(levels))(*[int(v) for v in levels])
+    out = (ctypes.c_int32 * n)()
+    _check(lib().cl_allocate_ranks(n, sp, ln, sd, float(layer_score), float(r_std), lv, len(levels), int(r_max),
+                                   float(tau), out))
+    return list(out)
+
+
+def layer_sensitivity(D, K):
+    """``cl_layer_sensitivity`` (host code): layer scores from layer-level
+    sensitivities, the top K scoring 1."""
+    L = len(D)
+    d = (ctypes.c_double * L)(*[float(v) for v in D])
+    out = (ctypes.c_double * L)()
+    _check(lib().cl_layer_sensitivity(L, d, int(K), out))
+    return list(out)
 
 
 def prefill_workspace(w, c, M):

@@ -3,6 +3,7 @@
 // touches the HIP runtime before every argument has been checked, so invalid
 // calls return an error without enqueuing work (and without needing a GPU).
 
+#include <math.h>
 #include <stdarg.h>
 #include <stdio.h>
 #include <string.h>
@@ -357,6 +358,47 @@ cl_status cl_linear_decode_window(int32_t n, const cl_qweight* w, const cl_lowra
                                   size_t ws_bytes, void* stream) {
     return decode_common(n, w, c, x, T, act_dtype, y, out_dtype, ws, ws_bytes, stream,
                          "cl_linear_decode_window");
+}
+
+cl_status cl_allocate_ranks(int32_t n, const float* const* sigma, const int32_t* len, const double* sens,
+                            double layer_score, double r_std, const int32_t* levels, int32_t nlevels, int32_t r_max,
+                            double tau, int32_t* ranks) {
+    const char* who = "cl_allocate_ranks";
+    if (n < 1 || n > cl::kMaxRankWin) return fail(CL_EINVAL, "%s: n must be in 1..%d (got %d)", who, cl::kMaxRankWin, n);
+    if (!sigma || !len || !sens || !levels || !ranks) return fail(CL_EINVAL, "%s: null argument", who);
+    if (!(layer_score >= 0.0) || !isfinite(layer_score) || !(r_std >= 0.0) || !isfinite(r_std))
+        return fail(CL_EINVAL, "%s: layer_score and r_std must be finite and >= 0", who);
+    if (!(tau >= 0.0) || !isfinite(tau)) return fail(CL_EINVAL, "%s: tau must be finite and >= 0", who);
+    if (r_max < 0) return fail(CL_EINVAL, "%s: r_max must be >= 0", who);
+    if (nlevels < 1 || nlevels > 64 || levels[0] != 0)
+        return fail(CL_EINVAL, "%s: levels must hold 1..64 values starting with 0", who);
+    for (int l = 1; l < nlevels; ++l)
+        if (levels[l] <= levels[l - 1]) return fail(CL_EINVAL, "%s: levels must be strictly increasing", who);
+    for (int i = 0; i < n; ++i) {
+        if (!sigma[i] || len[i] < 1) return fail(CL_EINVAL, "%s: spectrum %d is null or empty", who, i);
+        if (!(sens[i] >= 0.0) || !isfinite(sens[i]))
+            return fail(CL_EINVAL, "%s: sensitivity %d must be finite and >= 0", who, i);
+        for (int j = 0; j < len[i]; ++j)
+            if (!(sigma[i][j] >= 0.0f) || !isfinite(sigma[i][j]) || (j > 0 && sigma[i][j] > sigma[i][j - 1]))
+                return fail(CL_EINVAL, "%s: spectrum %d must be finite, >= 0 and descending (index %d)", who, i, j);
+    }
+    int lens[cl::kMaxRankWin], lv[64], out[cl::kMaxRankWin];
+    for (int i = 0; i < n; ++i) lens[i] = len[i];
+    for (int l = 0; l < nlevels; ++l) lv[l] = levels[l];
+    cl::allocate_window_ranks(n, sigma, lens, sens, layer_score, r_std, lv, nlevels, r_max, tau, out, nullptr);
+    for (int i = 0; i < n; ++i) ranks[i] = out[i];
+    return CL_OK;
+}
+
+cl_status cl_layer_sensitivity(int32_t L, const double* D, int32_t K, double* S) {
+    const char* who = "cl_layer_sensitivity";
+    if (L < 1 || L > cl::kMaxLayers) return fail(CL_EINVAL, "%s: L must be in 1..%d (got %d)", who, cl::kMaxLayers, L);
+    if (K < 1 || K > L) return fail(CL_EINVAL, "%s: K must be in 1..L (got %d)", who, K);
+    if (!D || !S) return fail(CL_EINVAL, "%s: null argument", who);
+    for (int l = 0; l < L; ++l)
+        if (!(D[l] >= 0.0) || !isfinite(D[l])) return fail(CL_EINVAL, "%s: D[%d] must be finite and >= 0", who, l);
+    cl::layer_sensitivity(L, D, K, S);
+    return CL_OK;
 }
 
 cl_status cl_linear_decode_glu(const cl_qweight* w, const cl_lowrank* c, const void* x, int32_t T,

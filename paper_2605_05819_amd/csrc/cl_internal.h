@@ -59,4 +59,16 @@ hipError_t launch_moe_decode(int n, const QW* w, const uint16_t* const* A, const
                              const int32_t* ids, int T, int k, int act, void* const* y, int out, void* ws,
                              hipStream_t st);
 
+// Rank allocation (host code, ranks.hip): salient-set size and salience
+// ratio of one descending spectrum; ranks of one compensation window (cont,
+// if not null, receives the continuous ranks before alignment); layer scores
+// from layer-level sensitivities.  Arguments already validated.
+constexpr int kMaxRankWin = 64;
+constexpr int kMaxLayers = 4096;
+int salient_count(const float* sigma, int n, double tau, double* phi);
+void allocate_window_ranks(int n, const float* const* sigma, const int* len, const double* sens, double layer_score,
+                           double r_std, const int* levels, int nlevels, int r_max, double tau, int* ranks,
+                           double* cont);
+void layer_sensitivity(int L, const double* D, int K, double* S);
+
 }  // namespace cl

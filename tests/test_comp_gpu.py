@@ -147,3 +147,36 @@ def test_deterministic():
     A1, B1, s1 = cl.build_compensation(Wd, w, 32)
     A2, B2, s2 = cl.build_compensation(Wd, w, 32)
     assert torch.equal(A1, A2) and torch.equal(B1, B2) and torch.equal(s1, s2)
+
+
+def test_spectra_to_ranks_to_window():
+    """The offline chain of Section 4.3 on one window: factors and singular
+    values built on the GPU, ranks from the spectra (host library = oracle,
+    exactly), then the window decode at those ranks against the oracle
+    forward with the GPU-built factors.  Outlier input columns (x16) give
+    the residuals a salient head."""
+    from oracle import ranks as oranks
+    shapes, r_max = [(512, 512), (256, 512), (256, 512)], 64
+    g = np.random.default_rng(31)
+    host, dev, sigmas = [], [], []
+    for i, (d_out, d_in) in enumerate(shapes):
+        W = wl.weight((d_out, d_in), 14, i)
+        W[:, g.choice(d_in, 6 + 6 * i, replace=False)] *= 16.0
+        w, Q, s, z, _ = _setup(W, 4, 128)
+        A, B, sigma = cl.build_compensation(torch.from_numpy(W).cuda(), w, r_max)
+        host.append((Q, s, z, _host16(A), _host16(B)))
+        dev.append((w, A, B))
+        sigmas.append(sigma.cpu().numpy())
+    sens = list(g.random(3))
+    levels = (0, 8, 16, 32, 64)
+    got = cl.allocate_ranks(sigmas, sens, 1.0, 96.0, levels, r_max)
+    assert got == oranks.window_ranks(sigmas, sens, 1.0, 96.0, levels, r_max)
+    assert any(oranks.salience(sg, 0.01)[0] > 0 for sg in sigmas)
+    x = wl.activation((2, 512), 14, 9)
+    xd = torch.from_numpy(x.bits.view(np.int16)).view(torch.float16).cuda()
+    ws_ = [d[0] for d in dev]
+    cs = [cl.LowRank(d[1], d[2], r_max, r) for d, r in zip(dev, got)]
+    ys = cl.linear_decode_window(ws_, cs, xd, out_dtype=torch.float32)
+    for y, (Q, s, z, A, B), r in zip(ys, host, got):
+        ref = linear.forward_packed(Q, s, z, 4, 128, A, B, r, x.values)
+        assert rel_l2(out_to_numpy(y), ref) <= REL_L2_TOL
