@@ -264,7 +264,8 @@ def bench_layer2bit(torch, cl, wl, timer, dev, rotate_gib):
 
 def bench_prefill(torch, cl, wl, timer, dev):
     """M = 2048 tokens through 4096 x 4096 and 14336 x 4096, rank 64, fp16
-    and bf16 activations: us per call and TFLOP/s (2MNK + 2Mr(K + N))."""
+    and bf16 activations: us per call and TFLOP/s (2MNK + 2Mr(K + N)); and,
+    for scale, torch's fp16 matrix product of the same shape (2MNK)."""
     M, r = 2048, 64
     res = {}
     for (N, K) in ((4096, 4096), (14336, 4096)):
@@ -284,6 +285,16 @@ def bench_prefill(torch, cl, wl, timer, dev):
             us = timer.time([g], 30) * 1e3
             flops = 2.0 * M * N * K + 2.0 * M * r * (K + N)
             res["%dx%d_%s" % (N, K, act)] = {"us": round(us, 2), "tflops": round(flops / us / 1e6, 1)}
+        # reference: the bare fp16 contraction through torch (hipBLASLt) on
+        # the same shape, no dequantization and no rank term
+        Xr = torch.randn((M, K), dtype=torch.float16, device=dev)
+        Wt = torch.randn((K, N), dtype=torch.float16, device=dev)
+        Yr = torch.empty((M, N), dtype=torch.float16, device=dev)
+        g = timer.capture(lambda: torch.mm(Xr, Wt, out=Yr))
+        us = timer.time([g], 30) * 1e3
+        res["%dx%d_torch_mm_fp16_reference" % (N, K)] = {"us": round(us, 2),
+                                                         "tflops": round(2.0 * M * N * K / us / 1e6, 1)}
+        del Xr, Wt, Yr
     return res
 
 
