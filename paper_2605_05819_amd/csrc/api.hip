@@ -161,11 +161,12 @@ cl_status decode_common(int32_t n, const cl_qweight* w, const cl_lowrank* c, con
         return fail(CL_EINVAL, "%s: act_dtype must be CL_FP16 or CL_BF16", who);
     if (out_dtype != CL_FP16 && out_dtype != CL_BF16 && out_dtype != CL_FP32)
         return fail(CL_EINVAL, "%s: out_dtype must be CL_FP16, CL_BF16 or CL_FP32", who);
-    if (!x || !y) return fail(CL_EINVAL, "%s: null x or y", who);
+    const char* out = glu ? "h" : "y";
+    if (!x || !y) return fail(CL_EINVAL, "%s: null x or %s", who, out);
     if (!aligned(x, 16)) return fail(CL_EINVAL, "%s: x must be 16-byte aligned", who);
     for (int i = 0; i < n; ++i) {
-        if (!y[i]) return fail(CL_EINVAL, "%s: null y", who);
-        if (!aligned(y[i], out_dtype == CL_FP32 ? 4 : 2)) return fail(CL_EINVAL, "%s: misaligned y", who);
+        if (!y[i]) return fail(CL_EINVAL, "%s: null %s", who, out);
+        if (!aligned(y[i], out_dtype == CL_FP32 ? 4 : 2)) return fail(CL_EINVAL, "%s: misaligned %s", who, out);
     }
     const size_t need = cl::decode_workspace_bytes(n, qw, lr, T);
     if (!ws || ws_bytes < need)

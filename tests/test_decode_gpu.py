@@ -285,6 +285,8 @@ def _glu_ref_rows(host, ranks, bits, G, d_in, X, rows):
     (5, torch.float16, torch.float16, 2, 64, 700, 1024),        # 2-bit, two passes of 4 tokens
     (1, torch.float16, torch.float32, 4, 128, 14336, 4096),     # Llama-8B gate/up, one token
     (16, torch.float16, torch.float32, 4, 128, 14336, 4096),    # Llama-8B gate/up, MFMA with 4 tiles per wave
+    (64, torch.bfloat16, torch.float16, 4, 128, 1000, 2048),    # the most tokens: four MFMA passes
+    (4, torch.float16, torch.bfloat16, 2, 64, 1000, 4096),      # 2-bit, one pass of 4 tokens
 ])
 def test_glu_matches_oracle(T, act, out, bits, G, d_out, d_in):
     """cl_linear_decode_glu = SiLU(gate x) * (up x) of the fp64 oracle (gate
