@@ -622,230 +622,215 @@ __global__ __launch_bounds__(1024) void decode_prep_mfma_kernel(PrepMArgs a) {
 // from the K-part partials of decode_prep_mfma_kernel, summed in a fixed
 // order and rounded to fp16); the waves' tiles are summed through LDS in a
 // fixed order; one rounding to the output dtype.
-// a.lin[i] for a wave-uniform i, read with constant indices only (indexed by
-// the phase counter, the gated MFMA backbone needed 254 VGPRs + 16 AGPRs,
-// one wave per SIMD; with this, 227 + 16 and two waves as without the gate)
-__device__ __forceinline__ Lin lin_at(const DecodeArgs& a, int i) {
-    Lin L = a.lin[0];
-#pragma unroll
-    for (int k = 1; k < kMaxWin; ++k)
-        if (i == k) L = a.lin[k];
-    return L;
-}
-
 template <int TPW, int NBUF, bool GLU>
-__global__ __launch_bounds__(256) void decode_mfma_kernel(DecodeArgs a) {
-    __shared__ f32x4 red[4][TPW][64];
-    extern __shared__ uint16_t szl[];             // [2][16 TPW][groups]: the rows' scales, then zeros
+__global__ __launch_bounds__(GLU ? 512 : 256) void decode_mfma_kernel(DecodeArgs a) {
+    // GLU: eight waves, the first four on the gate's tiles and the other four
+    // on the up tiles of the same rows (phase 1); the two sets of sums meet
+    // in LDS and the first four waves store SiLU(gate) * up
+    constexpr int NPH = GLU ? 2 : 1;
+    static_assert(TPW <= 4, "one stored tile per wave");
+    __shared__ f32x4 red[4 * NPH][TPW][64];
+    extern __shared__ uint16_t szl_all[];         // per phase [2][16 TPW][groups]: the rows' scales, then zeros
     const int lane = threadIdx.x & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int wave_all = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int ph = GLU ? wave_all >> 2 : 0;
+    const int wave = wave_all & 3;                // wave within the phase
+    const int tid = threadIdx.x & 255;            // thread within the phase
     const int g = lane >> 4, r = lane & 15;
     // workgroup -> (linear, TPW tiles of 16 rows); batch_end counts workgroups
     int li0 = 0;
     while (static_cast<int>(blockIdx.x) >= a.lin[li0].batch_end) ++li0;
     const int row0 = (blockIdx.x - (li0 ? a.lin[li0 - 1].batch_end : 0)) * 16 * TPW;
-    // GLU: the gate's tiles (phase 0), then the up tiles of the same rows
-    // (phase 1); gv keeps this wave's gate sums between the phases
-    static_assert(TPW <= 4, "one stored tile per wave");
-    f32x4 gv = {0.f, 0.f, 0.f, 0.f};
-    // one body for both phases (unrolled, the up phase's loads were hoisted
-    // into the gate phase: 254 VGPRs)
-#pragma clang loop unroll(disable)
-    for (int ph = 0; ph < (GLU ? 2 : 1); ++ph) {
-        const Lin L = lin_at(a, GLU ? ph : li0);
-        int row[TPW];
-        bool rowv[TPW];
+    const Lin& L = a.lin[GLU ? ph : li0];
+    int row[TPW];
+    bool rowv[TPW];
+#pragma unroll
+    for (int j = 0; j < TPW; ++j) {
+        rowv[j] = row0 + 16 * j + r < L.d_out;
+        row[j] = rowv[j] ? row0 + 16 * j + r : L.d_out - 1;
+    }
+    const int tok = a.tok0 + r;                    // this lane's token column of the B operand
+    const bool tokv = tok < a.T;
+    const int K = a.d_in;
+    const int nkb = (K + 127) / 128;
+    const int words_row = K / 8;
+    const int groups = K / a.G;
+    uint16_t* const szl = szl_all + ph * (2 * 16 * TPW * groups);
+    const uint32_t mlo = __builtin_amdgcn_readfirstlane(0x000F000Fu);
+    const uint32_t mhi = __builtin_amdgcn_readfirstlane(0x00F000F0u);
+    const uint32_t bias = 0x64006400u;
+    // this pass's activations; absent tokens were written as zero
+    const u32x4* xf = a.xf + static_cast<size_t>(a.tok0 / 16) * words_row * 16 + r;
+    // the workgroup's scales and zeros into LDS (rows are consecutive, so
+    // each array's part is one contiguous run starting 16-byte aligned, as
+    // row0 is a multiple of 16): whole 16-byte pieces, then the last few
+    // values of a partial last tile one by one; rows past the matrix are not
+    // loaded and never used
+    {
+        const int nrows = min(16 * TPW, L.d_out - row0);
+        const int nval = nrows * groups;
+        const int n16 = nval / 8;
+        const uint16_t* ssrc = L.s + static_cast<size_t>(row0) * groups;
+        const uint16_t* zsrc = L.z + static_cast<size_t>(row0) * groups;
+        uint16_t* zl = szl + 16 * TPW * groups;
+        for (int i = tid; i < n16; i += 256) {
+            reinterpret_cast<u32x4*>(szl)[i] = reinterpret_cast<const u32x4*>(ssrc)[i];
+            reinterpret_cast<u32x4*>(zl)[i] = reinterpret_cast<const u32x4*>(zsrc)[i];
+        }
+        for (int i = 8 * n16 + tid; i < nval; i += 256) {
+            szl[i] = ssrc[i];
+            zl[i] = zsrc[i];
+        }
+        __syncthreads();
+    }
+
+    struct Blk {
+        u32x4 w[TPW];
+        u32x4 x[4];
+    };
+    // rank-r term, 32 factor columns per step, wave w taking steps w, w + 4:
+    // A operand B[row][k .. k + 8), B operand t[tok][k .. k + 8) = the sum of
+    // the K-part partials in order, rounded to fp16.  The first step's
+    // operands are loaded before the K loop, so their latency is hidden.
+    const bool bvec = (L.r_max & 7) == 0 && (reinterpret_cast<uintptr_t>(L.B) & 15) == 0;
+    f32x4 acc[TPW];
+#pragma unroll
+    for (int j = 0; j < TPW; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    struct RankOp {
+        uint32_t bw[TPW][4];
+        f32x4 tp[kMaxKp][2];
+    };
+    auto rank_load = [&](int kr, RankOp& o) {
+        const int k = kr + 8 * g;
+        if (kr >= L.rank) return;
 #pragma unroll
         for (int j = 0; j < TPW; ++j) {
-            rowv[j] = row0 + 16 * j + r < L.d_out;
-            row[j] = rowv[j] ? row0 + 16 * j + r : L.d_out - 1;
-        }
-        const int tok = a.tok0 + r;                    // this lane's token column of the B operand
-        const bool tokv = tok < a.T;
-        const int K = a.d_in;
-        const int nkb = (K + 127) / 128;
-        const int words_row = K / 8;
-        const int groups = K / a.G;
-        const uint32_t mlo = __builtin_amdgcn_readfirstlane(0x000F000Fu);
-        const uint32_t mhi = __builtin_amdgcn_readfirstlane(0x00F000F0u);
-        const uint32_t bias = 0x64006400u;
-        // this pass's activations; absent tokens were written as zero
-        const u32x4* xf = a.xf + static_cast<size_t>(a.tok0 / 16) * words_row * 16 + r;
-        // the workgroup's scales and zeros into LDS (rows are consecutive, so
-        // each array's part is one contiguous run starting 16-byte aligned, as
-        // row0 is a multiple of 16): whole 16-byte pieces, then the last few
-        // values of a partial last tile one by one; rows past the matrix are not
-        // loaded and never used
-        {
-            const int nrows = min(16 * TPW, L.d_out - row0);
-            const int nval = nrows * groups;
-            const int n16 = nval / 8;
-            const uint16_t* ssrc = L.s + static_cast<size_t>(row0) * groups;
-            const uint16_t* zsrc = L.z + static_cast<size_t>(row0) * groups;
-            uint16_t* zl = szl + 16 * TPW * groups;
-            for (int i = threadIdx.x; i < n16; i += 256) {
-                reinterpret_cast<u32x4*>(szl)[i] = reinterpret_cast<const u32x4*>(ssrc)[i];
-                reinterpret_cast<u32x4*>(zl)[i] = reinterpret_cast<const u32x4*>(zsrc)[i];
-            }
-            for (int i = 8 * n16 + static_cast<int>(threadIdx.x); i < nval; i += 256) {
-                szl[i] = ssrc[i];
-                zl[i] = zsrc[i];
-            }
-            __syncthreads();
-        }
-
-        struct Blk {
-            u32x4 w[TPW];
-            u32x4 x[4];
-        };
-        // rank-r term, 32 factor columns per step, wave w taking steps w, w + 4:
-        // A operand B[row][k .. k + 8), B operand t[tok][k .. k + 8) = the sum of
-        // the K-part partials in order, rounded to fp16.  The first step's
-        // operands are loaded before the K loop, so their latency is hidden.
-        const bool bvec = (L.r_max & 7) == 0 && (reinterpret_cast<uintptr_t>(L.B) & 15) == 0;
-        f32x4 acc[TPW];
+            const uint16_t* brow = L.B + static_cast<size_t>(row[j]) * L.r_max;
+            if (bvec && k + 8 <= L.r_max) {
+                const u32x4 v = *reinterpret_cast<const u32x4*>(brow + k);
 #pragma unroll
-        for (int j = 0; j < TPW; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
-        struct RankOp {
-            uint32_t bw[TPW][4];
-            f32x4 tp[kMaxKp][2];
-        };
-        auto rank_load = [&](int kr, RankOp& o) {
-            const int k = kr + 8 * g;
-            if (kr >= L.rank) return;
-#pragma unroll
-            for (int j = 0; j < TPW; ++j) {
-                const uint16_t* brow = L.B + static_cast<size_t>(row[j]) * L.r_max;
-                if (bvec && k + 8 <= L.r_max) {
-                    const u32x4 v = *reinterpret_cast<const u32x4*>(brow + k);
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) { const uint32_t ve = v[e]; o.bw[j][e] = ve; }
-                } else {
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const uint32_t lo = k + 2 * e < L.r_max ? brow[k + 2 * e] : 0u;
-                        const uint32_t hi = k + 2 * e + 1 < L.r_max ? brow[k + 2 * e + 1] : 0u;
-                        o.bw[j][e] = lo | (hi << 16);
-                    }
-                }
-            }
-            const int tk = tokv ? tok : 0;
-#pragma unroll
-            for (int p = 0; p < kMaxKp; ++p) {
-                const int pp = p < a.kp ? p : 0;
-                const f32x4* src = reinterpret_cast<const f32x4*>(L.t + (static_cast<size_t>(pp) * a.T + tk) * L.rpad + k);
-                o.tp[p][0] = src[0];
-                o.tp[p][1] = src[1];
-            }
-        };
-        auto rank_mma = [&](int kr, const RankOp& o) {
-            if (kr >= L.rank) return;
-            const int k = kr + 8 * g;
-            float tsum[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int p = 0; p < kMaxKp; ++p) {
-                if (p >= a.kp) break;
-#pragma unroll
-                for (int e = 0; e < 4; ++e) { tsum[e] += o.tp[p][0][e]; tsum[4 + e] += o.tp[p][1][e]; }
-            }
-            uint32_t tw[4];
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-                tw[e] = tokv ? (static_cast<uint32_t>(f32_to_f16_bits(tsum[2 * e])) |
-                                (static_cast<uint32_t>(f32_to_f16_bits(tsum[2 * e + 1])) << 16))
-                             : 0u;
-#pragma unroll
-            for (int j = 0; j < TPW; ++j) {
-                uint32_t aw[4];
+                for (int e = 0; e < 4; ++e) { const uint32_t ve = v[e]; o.bw[j][e] = ve; }
+            } else {
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    // entries past the rank (or past the matrix) and absent tokens are zero
-                    const uint32_t lo = (rowv[j] && k + 2 * e < L.rank) ? (o.bw[j][e] & 0xffffu) : 0u;
-                    const uint32_t hi = (rowv[j] && k + 2 * e + 1 < L.rank) ? (o.bw[j][e] >> 16) : 0u;
-                    aw[e] = lo | (hi << 16);
+                    const uint32_t lo = k + 2 * e < L.r_max ? brow[k + 2 * e] : 0u;
+                    const uint32_t hi = k + 2 * e + 1 < L.r_max ? brow[k + 2 * e + 1] : 0u;
+                    o.bw[j][e] = lo | (hi << 16);
                 }
-                acc[j] = mfma(u32x4{aw[0], aw[1], aw[2], aw[3]}, u32x4{tw[0], tw[1], tw[2], tw[3]}, acc[j]);
             }
-        };
-        RankOp rb;
-        rank_load(32 * wave, rb);
+        }
+        const int tk = tokv ? tok : 0;
+#pragma unroll
+        for (int p = 0; p < kMaxKp; ++p) {
+            const int pp = p < a.kp ? p : 0;
+            const f32x4* src = reinterpret_cast<const f32x4*>(L.t + (static_cast<size_t>(pp) * a.T + tk) * L.rpad + k);
+            o.tp[p][0] = src[0];
+            o.tp[p][1] = src[1];
+        }
+    };
+    auto rank_mma = [&](int kr, const RankOp& o) {
+        if (kr >= L.rank) return;
+        const int k = kr + 8 * g;
+        float tsum[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int p = 0; p < kMaxKp; ++p) {
+            if (p >= a.kp) break;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) { tsum[e] += o.tp[p][0][e]; tsum[4 + e] += o.tp[p][1][e]; }
+        }
+        uint32_t tw[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            tw[e] = tokv ? (static_cast<uint32_t>(f32_to_f16_bits(tsum[2 * e])) |
+                            (static_cast<uint32_t>(f32_to_f16_bits(tsum[2 * e + 1])) << 16))
+                         : 0u;
+#pragma unroll
+        for (int j = 0; j < TPW; ++j) {
+            uint32_t aw[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                // entries past the rank (or past the matrix) and absent tokens are zero
+                const uint32_t lo = (rowv[j] && k + 2 * e < L.rank) ? (o.bw[j][e] & 0xffffu) : 0u;
+                const uint32_t hi = (rowv[j] && k + 2 * e + 1 < L.rank) ? (o.bw[j][e] >> 16) : 0u;
+                aw[e] = lo | (hi << 16);
+            }
+            acc[j] = mfma(u32x4{aw[0], aw[1], aw[2], aw[3]}, u32x4{tw[0], tw[1], tw[2], tw[3]}, acc[j]);
+        }
+    };
+    RankOp rb;
+    rank_load(32 * wave, rb);
 
-        // loads are unconditional (valid addresses always) and nothing consumes a
-        // loaded value before compute: the compiler's wait counts then let every
-        // prefetched block stay in flight
-        auto load = [&](int kb, Blk& b) {
-            const int kc = kb * 128 + 32 * g;          // first of this lane's 32 codes
-            const int wi = kc < K ? kc / 8 : 0;
+    // loads are unconditional (valid addresses always) and nothing consumes a
+    // loaded value before compute: the compiler's wait counts then let every
+    // prefetched block stay in flight
+    auto load = [&](int kb, Blk& b) {
+        const int kc = kb * 128 + 32 * g;          // first of this lane's 32 codes
+        const int wi = kc < K ? kc / 8 : 0;
 #pragma unroll
-            for (int j = 0; j < TPW; ++j)
-                b.w[j] = __builtin_nontemporal_load(
-                    reinterpret_cast<const u32x4*>(L.q + static_cast<size_t>(row[j]) * words_row + wi));
+        for (int j = 0; j < TPW; ++j)
+            b.w[j] = __builtin_nontemporal_load(
+                reinterpret_cast<const u32x4*>(L.q + static_cast<size_t>(row[j]) * words_row + wi));
 #pragma unroll
-            for (int t = 0; t < 4; ++t) b.x[t] = xf[static_cast<size_t>(wi + t) * 16];
-        };
-        auto compute = [&](int kb, const Blk& b) {
-            // past K, past the matrix or a padding block: scale 0, the weight is 0
-            const int kc = kb * 128 + 32 * g;
-            const bool on = kb < nkb && kc < K;
-            const int gs = on ? kc / a.G : 0;
+        for (int t = 0; t < 4; ++t) b.x[t] = xf[static_cast<size_t>(wi + t) * 16];
+    };
+    auto compute = [&](int kb, const Blk& b) {
+        // past K, past the matrix or a padding block: scale 0, the weight is 0
+        const int kc = kb * 128 + 32 * g;
+        const bool on = kb < nkb && kc < K;
+        const int gs = on ? kc / a.G : 0;
 #pragma unroll
-            for (int j = 0; j < TPW; ++j) {
-                const int lr = (16 * j + r) * groups + gs;
-                const uint32_t sb = szl[lr], zb = szl[16 * TPW * groups + lr];
-                const Dq dq = make_dq((on && rowv[j]) ? sb : 0u, zb);
+        for (int j = 0; j < TPW; ++j) {
+            const int lr = (16 * j + r) * groups + gs;
+            const uint32_t sb = szl[lr], zb = szl[16 * TPW * groups + lr];
+            const Dq dq = make_dq((on && rowv[j]) ? sb : 0u, zb);
 #pragma unroll
-                for (int t = 0; t < 4; ++t) acc[j] = mfma(dequant_word4x(b.w[j][t], dq, mlo, mhi, bias), b.x[t], acc[j]);
-            }
-        };
-        // blocks of this wave: kb = wave + 4 i, NBUF in flight.  Rounds of NBUF:
-        // block j of a round is computed, then its registers take block
-        // j + NBUF (past the last block they reload the current one, already
-        // cached).
-        constexpr int SPAN = 4 * NBUF;                 // blocks per round over the four waves
-        const int rounds = (nkb + SPAN - 1) / SPAN;
-        Blk b[NBUF];
-#pragma unroll
-        for (int j = 0; j < NBUF; ++j) load(wave + 4 * j < nkb ? wave + 4 * j : 0, b[j]);
-        for (int rd = 0; rd < rounds; ++rd) {
-#pragma unroll
-            for (int j = 0; j < NBUF; ++j) {
-                const int kb = wave + SPAN * rd + 4 * j;
-                compute(kb, b[j]);
-                const int kn = kb + SPAN;
-                load(kn < nkb ? kn : (kb < nkb ? kb : 0), b[j]);
-            }
+            for (int t = 0; t < 4; ++t) acc[j] = mfma(dequant_word4x(b.w[j][t], dq, mlo, mhi, bias), b.x[t], acc[j]);
         }
-        // rank-r term (operands loaded before the K loop, see rank_load)
-        rank_mma(32 * wave, rb);
-        for (int kr = 32 * wave + 128; kr < L.rank; kr += 128) {
-            RankOp ro;
-            rank_load(kr, ro);
-            rank_mma(kr, ro);
+    };
+    // blocks of this wave: kb = wave + 4 i, NBUF in flight.  Rounds of NBUF:
+    // block j of a round is computed, then its registers take block
+    // j + NBUF (past the last block they reload the current one, already
+    // cached).
+    constexpr int SPAN = 4 * NBUF;                 // blocks per round over the four waves
+    const int rounds = (nkb + SPAN - 1) / SPAN;
+    Blk b[NBUF];
+#pragma unroll
+    for (int j = 0; j < NBUF; ++j) load(wave + 4 * j < nkb ? wave + 4 * j : 0, b[j]);
+    for (int rd = 0; rd < rounds; ++rd) {
+#pragma unroll
+        for (int j = 0; j < NBUF; ++j) {
+            const int kb = wave + SPAN * rd + 4 * j;
+            compute(kb, b[j]);
+            const int kn = kb + SPAN;
+            load(kn < nkb ? kn : (kb < nkb ? kb : 0), b[j]);
         }
+    }
+    // rank-r term (operands loaded before the K loop, see rank_load)
+    rank_mma(32 * wave, rb);
+    for (int kr = 32 * wave + 128; kr < L.rank; kr += 128) {
+        RankOp ro;
+        rank_load(kr, ro);
+        rank_mma(kr, ro);
+    }
 #pragma unroll
-        for (int j = 0; j < TPW; ++j) red[wave][j][lane] = acc[j];
-        __syncthreads();
-        // wave w sums and stores tiles w, w + 4, ... in a fixed order
-        // (no early exit for absent tokens: a gated workgroup meets the barriers
-        // of its second phase with all its waves)
-        if (tokv) {
+    for (int j = 0; j < TPW; ++j) red[4 * ph + wave][j][lane] = acc[j];
+    __syncthreads();
+    // wave w sums and stores tiles w, w + 4, ... in a fixed order
+    if (tokv && ph == 0) {
 #pragma unroll
-            for (int j = 0; j < TPW; ++j) {
-                if (j % 4 != wave) continue;
-                const f32x4 v = red[0][j][lane] + red[1][j][lane] + red[2][j][lane] + red[3][j][lane];
-                if (GLU && ph == 0) {
-                    gv = v;
-                    continue;
-                }
-                // v[e] = y[tok][row0 + 16 j + 4 g + e]
+        for (int j = 0; j < TPW; ++j) {
+            if (j % 4 != wave) continue;
+            const f32x4 v = red[0][j][lane] + red[1][j][lane] + red[2][j][lane] + red[3][j][lane];
+            f32x4 u = {0.f, 0.f, 0.f, 0.f};
+            if constexpr (GLU) u = red[4][j][lane] + red[5][j][lane] + red[6][j][lane] + red[7][j][lane];
+            // v[e] = y[tok][row0 + 16 j + 4 g + e] (GLU: the gate's; u the up's)
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const int rr = row0 + 16 * j + 4 * g + e;
-                    if (rr >= L.d_out) continue;
-                    const size_t idx = static_cast<size_t>(tok) * L.d_out + rr;
-                    if (GLU) store_out(a.h, idx, silu_mul(gv[e], v[e]), a.out);
-                    else store_out(L.y, idx, v[e], a.out);
-                }
+            for (int e = 0; e < 4; ++e) {
+                const int rr = row0 + 16 * j + 4 * g + e;
+                if (rr >= L.d_out) continue;
+                const size_t idx = static_cast<size_t>(tok) * L.d_out + rr;
+                if (GLU) store_out(a.h, idx, silu_mul(v[e], u[e]), a.out);
+                else store_out(L.y, idx, v[e], a.out);
             }
         }
     }
@@ -1017,10 +1002,6 @@ hipError_t launch_decode_mfma(int n, const QW* w, const LR* c, const void* x, in
     for (int i = 0; i < n; ++i) tiles += (w[i].d_out + 15) / 16;
     const int groups = d_in / w[0].G;
     // four tiles per wave when the workgroup's scales and zeros fit 32 KB of LDS
-    // (a gated window runs gate and up one after the other in each
-    // workgroup, so it has half the workgroups; two tiles per wave, which
-    // keeps their number, measured slower: 38 us against 32 us for the
-    // Llama-8B gate/up at 16 tokens)
     const int tpw = tiles >= 1024 && 2 * 64 * groups * 2 <= 32768 ? 4 : 1;
     int wg_end = 0, rtiles = 0, wg_first = 0;
     for (int i = 0; i < n; ++i) {
@@ -1065,12 +1046,14 @@ hipError_t launch_decode_mfma(int n, const QW* w, const LR* c, const void* x, in
     a.h = glu ? y[0] : nullptr;
     auto kern = glu ? (tpw == 4 ? decode_mfma_kernel<4, 2, true> : decode_mfma_kernel<1, 4, true>)
                     : (tpw == 4 ? decode_mfma_kernel<4, 2, false> : decode_mfma_kernel<1, 4, false>);
-    const size_t lds = static_cast<size_t>(2) * 16 * tpw * groups * 2;
-    // a gated window runs one workgroup per gate workgroup (gate, then up)
+    // a gated window runs one workgroup of eight waves per gate workgroup
+    // (four waves on the gate's tiles, four on the up tiles of the same rows),
+    // with both linears' scales and zeros in LDS
+    const size_t lds = static_cast<size_t>(2) * 16 * tpw * groups * 2 * (glu ? 2 : 1);
     const int bgrid = glu ? wg_first : wg_end;
     for (int tok0 = 0; tok0 < T && e == hipSuccess; tok0 += 16) {
         a.tok0 = tok0;
-        hipLaunchKernelGGL(kern, dim3(bgrid), dim3(256), lds, st, a);
+        hipLaunchKernelGGL(kern, dim3(bgrid), dim3(glu ? 512 : 256), lds, st, a);
         e = hipGetLastError();
     }
     return e;
