@@ -106,16 +106,18 @@ __global__ __launch_bounds__(256) void xprep_kernel(const uint16_t* __restrict__
 }
 
 // One launch, two roles.  Workgroups [0, t_blocks): T = X A[:r]^T for 16
-// tokens x 64 factor columns each; the NW waves split K, every wave keeps 8
-// k-blocks of loads in flight, and the partial tiles are summed through LDS
-// in a fixed order.  MFMA A operand = X rows, B operand = rows of A.  Output
-// fp16, zero for columns >= rank.  The remaining workgroups write X' (four
-// 16-byte chunks per thread), so the X' stream runs beside T (X' written by
-// the T workgroups themselves took 27 us for the pair at M = 2048,
-// K = 4096; apart, about 22 us, bound by T's reads of 16 rows x 64 bytes
-// per load instruction: the same bytes read as contiguous 1 KB rows take
-// half the time).
-template <int NW>
+// tokens x 16 NJ factor columns each; the NW waves split K, every wave keeps
+// 8 k-blocks of loads in flight, and the partial tiles are summed through
+// LDS in a fixed order.  MFMA A operand = X rows, B operand = rows of A.
+// Output fp16, zero for columns >= rank.  The remaining workgroups write X'
+// (four 16-byte chunks per thread), so the X' stream runs beside T (X'
+// written by the T workgroups themselves took 27 us for the pair at
+// M = 2048, K = 4096; apart, about 22 us, bound by T's reads of 16 rows x
+// 64 bytes per load instruction: the same bytes read as contiguous 1 KB
+// rows take half the time).  32 factor columns per workgroup (NJ = 2)
+// spread those reads over twice the workgroups: 20.4 us against 22.7 us
+// with 64, the same output bit for bit.
+template <int NW, int NJ>
 __global__ __launch_bounds__(NW * 64) void lowrank_t_kernel(const uint16_t* __restrict__ X,
                                                             const uint16_t* __restrict__ A,
                                                             uint16_t* __restrict__ T, uint16_t* __restrict__ Xp,
@@ -123,7 +125,7 @@ __global__ __launch_bounds__(NW * 64) void lowrank_t_kernel(const uint16_t* __re
                                                             int mtiles, long long chunks) {
     constexpr int U = 8;                               // k blocks of 32 per batch
     constexpr int XC = 4;                              // X' chunks per thread
-    __shared__ f32x4 part[NW][4][64];
+    __shared__ f32x4 part[NW][NJ][64];
     const int tid = threadIdx.x;
     if (static_cast<int>(blockIdx.x) >= t_blocks) {
         const long long base = static_cast<long long>(blockIdx.x - t_blocks) * (NW * 64 * XC) + tid;
@@ -143,33 +145,33 @@ __global__ __launch_bounds__(NW * 64) void lowrank_t_kernel(const uint16_t* __re
     const int lane = tid & 63;
     const int wave = tid >> 6;
     const int mtile = static_cast<int>(blockIdx.x) % mtiles;   // 16 tokens
-    const int ntile = static_cast<int>(blockIdx.x) / mtiles;   // 64 factor columns
+    const int ntile = static_cast<int>(blockIdx.x) / mtiles;   // 16 NJ factor columns
     const int m = mtile * 16 + (lane & 15);
     const int kq = 8 * (lane >> 4);                    // this lane's 8 k within a 32 block
     const bool mval = m < M;
     const uint16_t* xr = X + static_cast<size_t>(mval ? m : 0) * K;
-    f32x4 acc[4];
+    f32x4 acc[NJ];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
-    const uint16_t* ar[4];
-    bool nval[4];
+    for (int j = 0; j < NJ; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const uint16_t* ar[NJ];
+    bool nval[NJ];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        const int n = ntile * 64 + j * 16 + (lane & 15);
+    for (int j = 0; j < NJ; ++j) {
+        const int n = ntile * (16 * NJ) + j * 16 + (lane & 15);
         nval[j] = n < rank;
         ar[j] = A + static_cast<size_t>(nval[j] ? n : 0) * K;
     }
     const int nkb = K / 32;                            // k blocks of 32; this wave takes 1 / NW
     const int kbeg = 32 * (wave * nkb / NW), kend = 32 * ((wave + 1) * nkb / NW);
     for (int k0 = kbeg; k0 < kend; k0 += 32 * U) {
-        u32x4 xa[U], av[U][4];
+        u32x4 xa[U], av[U][NJ];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int k = k0 + 32 * u;
             const int kc = k < kend ? k : (kbeg < kend ? kbeg : 0);
             xa[u] = *reinterpret_cast<const u32x4*>(xr + kc + kq);
 #pragma unroll
-            for (int j = 0; j < 4; ++j) av[u][j] = *reinterpret_cast<const u32x4*>(ar[j] + kc + kq);
+            for (int j = 0; j < NJ; ++j) av[u][j] = *reinterpret_cast<const u32x4*>(ar[j] + kc + kq);
         }
 #pragma unroll
         for (int u = 0; u < U; ++u) {
@@ -177,7 +179,7 @@ __global__ __launch_bounds__(NW * 64) void lowrank_t_kernel(const uint16_t* __re
             u32x4 x8 = act8_to_f16(xa[u], act);
             if (!mval || !live) x8 = u32x4{0, 0, 0, 0};
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
+            for (int j = 0; j < NJ; ++j) {
                 u32x4 a8 = av[u][j];
                 if (!nval[j]) a8 = u32x4{0, 0, 0, 0};
                 acc[j] = mfma(x8, a8, acc[j]);
@@ -185,18 +187,18 @@ __global__ __launch_bounds__(NW * 64) void lowrank_t_kernel(const uint16_t* __re
         }
     }
 #pragma unroll
-    for (int j = 0; j < 4; ++j) part[wave][j][lane] = acc[j];
+    for (int j = 0; j < NJ; ++j) part[wave][j][lane] = acc[j];
     __syncthreads();
     if (wave != 0) return;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < NJ; ++j) {
         acc[j] = part[0][j][lane];
         for (int w = 1; w < NW; ++w) acc[j] += part[w][j][lane];
     }
     // acc[j][e] = T[mtile*16 + 4*(lane/16) + e][ntile*64 + j*16 + lane%16]
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        const int n = ntile * 64 + j * 16 + (lane & 15);
+    for (int j = 0; j < NJ; ++j) {
+        const int n = ntile * (16 * NJ) + j * 16 + (lane & 15);
         if (n >= r_pad) continue;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
@@ -474,10 +476,11 @@ hipError_t launch_linear_prefill(const QW& w, const LR& c, const void* X, int M,
     if (c.rank > 0) {
         constexpr int NW = 8;
         const int mtiles = (M + 15) / 16;
-        const int t_blocks = mtiles * ((a.r_pad + 63) / 64);
+        constexpr int NJ = 2;                 // 32 factor columns per workgroup
+        const int t_blocks = mtiles * ((a.r_pad + 16 * NJ - 1) / (16 * NJ));
         const long long chunks = static_cast<long long>(M) * w.d_in / 8;
         const long long x_blocks = (chunks + NW * 64 * 4 - 1) / (NW * 64 * 4);
-        hipLaunchKernelGGL(lowrank_t_kernel<NW>, dim3(static_cast<unsigned>(t_blocks + x_blocks)), dim3(NW * 64), 0, st,
+        hipLaunchKernelGGL((lowrank_t_kernel<NW, NJ>), dim3(static_cast<unsigned>(t_blocks + x_blocks)), dim3(NW * 64), 0, st,
                            Xa, c.A, T, Xp, M, w.d_in, c.rank, a.r_pad, act, t_blocks, mtiles, chunks);
     } else {
         const long long chunks = static_cast<long long>(M) * w.d_in / 8;
