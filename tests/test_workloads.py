@@ -122,3 +122,15 @@ def test_dynamic_slot_ranks_scale_with_routing_weight():
         assert np.all(np.diff(r[sel][order]) >= 0)
     # a heavy slot gets more than its expert's rank, a light one less
     assert wl.dynamic_slot_ranks(np.array([[1, 4]]), np.array([[0.9, 0.1]]), ranks, levels, r_max).tolist() == [[16, 0]]
+
+
+def test_bench_refuses_more_than_one_gpu():
+    """bench.py measures one GPU: --gpus above 1 exits with a message before
+    touching a device."""
+    import os
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    r = subprocess.run([sys.executable, os.path.join(root, "bench.py"), "--gpus", "2"], capture_output=True,
+                       text=True, timeout=120)
+    assert r.returncode == 2 and "one GPU" in r.stderr
