@@ -277,7 +277,10 @@ size_t cl_prefill_workspace(const cl_qweight* w, const cl_lowrank* c, int32_t M)
  *             (both may be NULL when r_max = 0)
  *  ranks      device int32 [E], expert e's rank (clamped to 0..r_max)
  *  x          device [T][d_in] or [T][k][d_in] of act_dtype, 16-byte aligned
- *  topk_ids   device int32 [T][k]; an id outside 0..E-1 gives a zero row
+ *  topk_ids   device int32 [T][k].  The ids are read on the device only, so
+ *             an id outside 0..E-1 cannot fail the call: that slot's output
+ *             row is written as zeros and the device records the slot and id;
+ *             cl_moe_status() reports the record as CL_EINVAL.
  *  y          device [T][k][d_out] of out_dtype
  *  ws         device workspace of cl_moe_workspace(...) bytes, 256-byte aligned
  * Limits: E <= 1024, T in 1..64, T*k <= 1024, r_max <= 256, d_in <= 8192 * bits
@@ -290,9 +293,28 @@ cl_status cl_moe_linear_decode(const cl_qweight* w_expert0, const uint16_t* A, c
                                int32_t act_dtype, void* y, int32_t out_dtype, void* ws, size_t ws_bytes,
                                void* stream);
 
-/* Workspace bytes for cl_moe_linear_decode (0 for rejected arguments). */
+/*
+ * Workspace bytes for cl_moe_linear_decode (0 for rejected arguments).  The
+ * workspace holds the routing tables, A_e x per slot ([T k][r_max] float) and
+ * the activations prepared for the backbone ([rows][d_in] fp16 plus
+ * per-chunk sums, rows = T or T k), so the size depends on d_in, the code
+ * width and x_per_slot as well as on E, T, k and r_max: the query takes the
+ * expert-0 descriptor (for d_in, bits and group size) and x_per_slot.
+ */
 size_t cl_moe_workspace(const cl_qweight* w_expert0, int32_t r_max, int32_t num_experts, int32_t T,
                         int32_t k, int32_t x_per_slot);
+
+/*
+ * cl_moe_status -- the out-of-range routing ids that MoE calls met on the
+ * current device (Section 4.2.2's cross-expert grouping reads the routing
+ * table on the device; see topk_ids above).  Waits for `stream` (work
+ * enqueued on other streams is not waited for), then reads and clears the
+ * device's record: CL_OK if no MoE call met an id outside 0..E-1 since the
+ * record was last read, else CL_EINVAL with the slot and id of one such
+ * entry in cl_last_error().  CL_EHIP if the runtime fails.  All MoE calls on
+ * a device share one record.
+ */
+cl_status cl_moe_status(void* stream);
 
 /*
  * cl_moe_linear_decode_window -- n MoE linears (1 <= n <= 4) over the same

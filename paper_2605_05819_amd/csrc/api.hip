@@ -391,6 +391,18 @@ cl_status cl_allocate_ranks(int32_t n, const float* const* sigma, const int32_t*
     return CL_OK;
 }
 
+cl_status cl_moe_status(void* stream) {
+    const char* who = "cl_moe_status";
+    unsigned long long v = 0;
+    const hipError_t e = cl::moe_take_routing_error(static_cast<hipStream_t>(stream), &v);
+    if (e != hipSuccess) return hip_status(e, who);
+    if (v)
+        return fail(CL_EINVAL, "%s: a MoE call met routing id %d in slot %d (outside 0..num_experts-1); "
+                    "that slot's output row was written as zeros", who, static_cast<int32_t>(v & 0xffffffffu),
+                    static_cast<int>((v >> 32) & 0x7fffffffu));
+    return CL_OK;
+}
+
 cl_status cl_layer_sensitivity(int32_t L, const double* D, int32_t K, double* S) {
     const char* who = "cl_layer_sensitivity";
     if (L < 1 || L > cl::kMaxLayers) return fail(CL_EINVAL, "%s: L must be in 1..%d (got %d)", who, cl::kMaxLayers, L);

@@ -59,6 +59,10 @@ hipError_t launch_moe_decode(int n, const QW* w, const uint16_t* const* A, const
                              const int32_t* ids, int T, int k, int act, void* const* y, int out, void* ws,
                              hipStream_t st);
 
+// The current device's routing-error record (see moe.hip): waits for the
+// stream, returns the record in *word (0: none) and clears it.
+hipError_t moe_take_routing_error(hipStream_t st, unsigned long long* word);
+
 // Rank allocation (host code, ranks.hip): salient-set size and salience
 // ratio of one descending spectrum; ranks of one compensation window (cont,
 // if not null, receives the continuous ranks before alignment); layer scores

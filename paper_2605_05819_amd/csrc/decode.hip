@@ -610,19 +610,30 @@ __global__ __launch_bounds__(1024) void decode_prep_mfma_kernel(PrepMArgs a) {
 }
 
 // Many-token backbone (4-bit codes, T >= 3): the contraction has enough
-// columns to use MFMA (tokens padded to 16).  One workgroup per TPW 16-row tiles of one linear; its
-// four waves split the 128-code blocks of K (wave w takes blocks w, w + 4,
-// ...), NBUF blocks per wave in flight.  Per block a lane loads, for each of
-// its TPW tiles, 16 bytes of codes of row r = lane % 16 (32 codes of one
-// quantization group), and once for all tiles the matching activations of
-// token r (four 16-byte loads from the word-major layout, 256 contiguous
-// bytes per lane group); the codes are dequantized in registers to fp16
-// s (q - z) (one rounding) and feed four v_mfma_f32_16x16x32_f16 per tile.
-// The rank-r term is extra MFMA steps over [B | t] spread over the waves (t
-// from the K-part partials of decode_prep_mfma_kernel, summed in a fixed
-// order and rounded to fp16); the waves' tiles are summed through LDS in a
-// fixed order; one rounding to the output dtype.
-template <int TPW, int NBUF, bool GLU>
+// columns to use MFMA (tokens padded to 16).  One workgroup per TPW 16-row
+// tiles of one linear; its four waves split the 128-code blocks of K (wave w
+// takes blocks w, w + 4, ...), NBUF blocks per wave in flight.  Per block a
+// lane loads, for each of its TPW tiles, 16 bytes of codes of row r = lane %
+// 16, and once for all tiles the matching activations of token r (four
+// 16-byte loads from the word-major layout, 256 or 1024 contiguous bytes per
+// load instruction).  The MFMA takes the activations as its A operand and the
+// codes as its B operand, so lane (g, r) accumulates tokens 4 g .. 4 g + 3 of
+// weight row r.  The codes become the exact fp16 integers q - z, and every
+// quantization group's MFMA steps run into a fresh fp32 partial that is
+// scaled by the group's fp16 scale in fp32 and added to the accumulator:
+// the backbone is s (sum (q - z) x) with fp32 rounding only, whatever the
+// scale (a weight tile rounded to fp16 would carry 2^-11 relative error, and
+// lose precision once s / 16 falls below the fp16 normal range).  GPB
+// (groups per 128-code block) = 128 / G: with one group per block each MFMA
+// step takes word t of every lane group (the four steps cover the block);
+// with 2 or 4 groups the code words are transposed across the lane groups
+// first, so step t covers the 32 codes 32 t .. 32 t + 31, which lie in one
+// group.  The rank-r term is extra MFMA steps over [t | B] spread over the
+// waves (t from the K-part partials of decode_prep_mfma_kernel, summed in a
+// fixed order and split into fp16 hi and lo parts, one step each); the
+// waves' tiles are summed through LDS in a fixed order; one rounding to the
+// output dtype.
+template <int TPW, int NBUF, bool GLU, int GPB>
 __global__ __launch_bounds__(GLU ? 512 : 256) void decode_mfma_kernel(DecodeArgs a) {
     // GLU: eight waves, the first four on the gate's tiles and the other four
     // on the up tiles of the same rows (phase 1); the two sets of sums meet
@@ -662,16 +673,18 @@ __global__ __launch_bounds__(GLU ? 512 : 256) void decode_mfma_kernel(DecodeArgs
     // this pass's activations; absent tokens were written as zero
     const u32x4* xf = a.xf + static_cast<size_t>(a.tok0 / 16) * words_row * 16 + r;
     // the workgroup's scales and zeros into LDS (rows are consecutive, so
-    // each array's part is one contiguous run starting 16-byte aligned, as
-    // row0 is a multiple of 16): whole 16-byte pieces, then the last few
-    // values of a partial last tile one by one; rows past the matrix are not
-    // loaded and never used
+    // each array's part is one contiguous run): whole 16-byte pieces, then
+    // the last few values one by one; rows past the matrix are not loaded
+    // and never used
     {
         const int nrows = min(16 * TPW, L.d_out - row0);
         const int nval = nrows * groups;
-        const int n16 = nval / 8;
         const uint16_t* ssrc = L.s + static_cast<size_t>(row0) * groups;
         const uint16_t* zsrc = L.z + static_cast<size_t>(row0) * groups;
+        // 16-byte pieces only where both runs start 16-byte aligned (the
+        // caller's arrays need only 2-byte alignment)
+        const bool al = ((reinterpret_cast<uintptr_t>(ssrc) | reinterpret_cast<uintptr_t>(zsrc)) & 15) == 0;
+        const int n16 = al ? nval / 8 : 0;
         uint16_t* zl = szl + 16 * TPW * groups;
         for (int i = tid; i < n16; i += 256) {
             reinterpret_cast<u32x4*>(szl)[i] = reinterpret_cast<const u32x4*>(ssrc)[i];
@@ -689,9 +702,10 @@ __global__ __launch_bounds__(GLU ? 512 : 256) void decode_mfma_kernel(DecodeArgs
         u32x4 x[4];
     };
     // rank-r term, 32 factor columns per step, wave w taking steps w, w + 4:
-    // A operand B[row][k .. k + 8), B operand t[tok][k .. k + 8) = the sum of
-    // the K-part partials in order, rounded to fp16.  The first step's
-    // operands are loaded before the K loop, so their latency is hidden.
+    // A operand t[tok][k .. k + 8) = the sum of the K-part partials in order
+    // (as fp16 hi and lo parts, one MFMA step each), B operand
+    // B[row][k .. k + 8).  The first step's operands are loaded before the K
+    // loop, so their latency is hidden.
     const bool bvec = (L.r_max & 7) == 0 && (reinterpret_cast<uintptr_t>(L.B) & 15) == 0;
     f32x4 acc[TPW];
 #pragma unroll
@@ -738,12 +752,13 @@ __global__ __launch_bounds__(GLU ? 512 : 256) void decode_mfma_kernel(DecodeArgs
 #pragma unroll
             for (int e = 0; e < 4; ++e) { tsum[e] += o.tp[p][0][e]; tsum[4 + e] += o.tp[p][1][e]; }
         }
-        uint32_t tw[4];
+        // t as fp16 hi + lo parts, two MFMA steps (absent tokens zero)
+        uint32_t tw[4], tl[4];
 #pragma unroll
-        for (int e = 0; e < 4; ++e)
-            tw[e] = tokv ? (static_cast<uint32_t>(f32_to_f16_bits(tsum[2 * e])) |
-                            (static_cast<uint32_t>(f32_to_f16_bits(tsum[2 * e + 1])) << 16))
-                         : 0u;
+        for (int e = 0; e < 4; ++e) {
+            split_f16x2(tsum[2 * e], tsum[2 * e + 1], tw[e], tl[e]);
+            if (!tokv) tw[e] = tl[e] = 0u;
+        }
 #pragma unroll
         for (int j = 0; j < TPW; ++j) {
             uint32_t aw[4];
@@ -754,7 +769,9 @@ __global__ __launch_bounds__(GLU ? 512 : 256) void decode_mfma_kernel(DecodeArgs
                 const uint32_t hi = (rowv[j] && k + 2 * e + 1 < L.rank) ? (o.bw[j][e] >> 16) : 0u;
                 aw[e] = lo | (hi << 16);
             }
-            acc[j] = mfma(u32x4{aw[0], aw[1], aw[2], aw[3]}, u32x4{tw[0], tw[1], tw[2], tw[3]}, acc[j]);
+            const u32x4 bop = {aw[0], aw[1], aw[2], aw[3]};
+            acc[j] = mfma(u32x4{tw[0], tw[1], tw[2], tw[3]}, bop, acc[j]);
+            acc[j] = mfma(u32x4{tl[0], tl[1], tl[2], tl[3]}, bop, acc[j]);
         }
     };
     RankOp rb;
@@ -770,21 +787,40 @@ __global__ __launch_bounds__(GLU ? 512 : 256) void decode_mfma_kernel(DecodeArgs
         for (int j = 0; j < TPW; ++j)
             b.w[j] = __builtin_nontemporal_load(
                 reinterpret_cast<const u32x4*>(L.q + static_cast<size_t>(row[j]) * words_row + wi));
+        // the activations of the words this lane feeds to MFMA step t: word
+        // 4 g + t of the block, or 4 t + g once the codes are transposed
+        // (a word past K reads word g, met by a zero scale)
 #pragma unroll
-        for (int t = 0; t < 4; ++t) b.x[t] = xf[static_cast<size_t>(wi + t) * 16];
+        for (int t = 0; t < 4; ++t) {
+            const int xw = GPB == 1 ? wi + t : (kb * 128 + 32 * t < K ? kb * 16 + 4 * t + g : g);
+            b.x[t] = xf[static_cast<size_t>(xw) * 16];
+        }
     };
     auto compute = [&](int kb, const Blk& b) {
-        // past K, past the matrix or a padding block: scale 0, the weight is 0
-        const int kc = kb * 128 + 32 * g;
-        const bool on = kb < nkb && kc < K;
-        const int gs = on ? kc / a.G : 0;
+        // per group: MFMA steps into a fresh partial of sum (q - z) x, then
+        // acc += s * partial in fp32; past K, past the matrix or a padding
+        // block the scale is 0 (the partial is finite)
+        constexpr int SPG = 4 / GPB;               // MFMA steps per group
 #pragma unroll
         for (int j = 0; j < TPW; ++j) {
-            const int lr = (16 * j + r) * groups + gs;
-            const uint32_t sb = szl[lr], zb = szl[16 * TPW * groups + lr];
-            const Dq dq = make_dq((on && rowv[j]) ? sb : 0u, zb);
+            uint32_t w[4];
 #pragma unroll
-            for (int t = 0; t < 4; ++t) acc[j] = mfma(dequant_word4x(b.w[j][t], dq, mlo, mhi, bias), b.x[t], acc[j]);
+            for (int t = 0; t < 4; ++t) { const uint32_t v = b.w[j][t]; w[t] = v; }
+            if constexpr (GPB > 1) transpose_words(w);
+#pragma unroll
+            for (int q = 0; q < GPB; ++q) {
+                const int kc = kb * 128 + 32 * SPG * q;   // first code of the group's steps
+                const bool on = kb < nkb && kc < K && rowv[j];
+                const int lr = (16 * j + r) * groups + (on ? kc / a.G : 0);
+                const uint32_t sb = szl[lr], zb = szl[16 * TPW * groups + lr];
+                const Zq zq = make_zq(zb);
+                f32x4 p = mfma(b.x[SPG * q], codes_minus_zero(w[SPG * q], zq, mlo, mhi, bias),
+                               f32x4{0.f, 0.f, 0.f, 0.f});
+#pragma unroll
+                for (int t = SPG * q + 1; t < SPG * q + SPG; ++t)
+                    p = mfma(b.x[t], codes_minus_zero(w[t], zq, mlo, mhi, bias), p);
+                acc[j] = fma4(on ? f16_bits_to_f32(static_cast<uint16_t>(sb)) : 0.f, p, acc[j]);
+            }
         }
     };
     // blocks of this wave: kb = wave + 4 i, NBUF in flight.  Rounds of NBUF:
@@ -816,19 +852,19 @@ __global__ __launch_bounds__(GLU ? 512 : 256) void decode_mfma_kernel(DecodeArgs
     for (int j = 0; j < TPW; ++j) red[4 * ph + wave][j][lane] = acc[j];
     __syncthreads();
     // wave w sums and stores tiles w, w + 4, ... in a fixed order
-    if (tokv && ph == 0) {
+    if (ph == 0) {
 #pragma unroll
         for (int j = 0; j < TPW; ++j) {
-            if (j % 4 != wave) continue;
+            if (j % 4 != wave || !rowv[j]) continue;
             const f32x4 v = red[0][j][lane] + red[1][j][lane] + red[2][j][lane] + red[3][j][lane];
             f32x4 u = {0.f, 0.f, 0.f, 0.f};
             if constexpr (GLU) u = red[4][j][lane] + red[5][j][lane] + red[6][j][lane] + red[7][j][lane];
-            // v[e] = y[tok][row0 + 16 j + 4 g + e] (GLU: the gate's; u the up's)
+            // v[e] = y[tok0 + 4 g + e][row0 + 16 j + r] (GLU: the gate's; u the up's)
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                const int rr = row0 + 16 * j + 4 * g + e;
-                if (rr >= L.d_out) continue;
-                const size_t idx = static_cast<size_t>(tok) * L.d_out + rr;
+                const int tk = a.tok0 + 4 * g + e;
+                if (tk >= a.T) continue;
+                const size_t idx = static_cast<size_t>(tk) * L.d_out + row[j];
                 if (GLU) store_out(a.h, idx, silu_mul(v[e], u[e]), a.out);
                 else store_out(L.y, idx, v[e], a.out);
             }
@@ -961,6 +997,27 @@ MfmaPlan mfma_plan(int d_in) {
 
 int pad32(int r) { return (r + 31) / 32 * 32; }
 
+// Quantization groups a 128-code block can meet, as the MFMA backbone sees
+// them: 1 when G is a multiple of 128, 2 when it is a multiple of 64 (each
+// half of a block lies in one group), else 4 (each 32-code step does)
+int mfma_groups_per_block(int G) { return G % 128 == 0 ? 1 : (G % 64 == 0 ? 2 : 4); }
+
+// blocks in flight per wave: 2 with four tiles per wave, 4 with one; halved
+// when a block holds several groups (their partials and scales need the
+// registers)
+template <bool GLU, int GPB>
+auto pick_tpw(int tpw) {
+    return tpw == 4 ? decode_mfma_kernel<4, GPB == 1 ? 2 : 1, GLU, GPB>
+                    : decode_mfma_kernel<1, GPB == 1 ? 4 : 2, GLU, GPB>;
+}
+
+template <bool GLU>
+auto pick_gpb(int tpw, int gpb) {
+    return gpb == 1 ? pick_tpw<GLU, 1>(tpw) : (gpb == 2 ? pick_tpw<GLU, 2>(tpw) : pick_tpw<GLU, 4>(tpw));
+}
+
+auto pick_mfma_kernel(int tpw, bool glu, int gpb) { return glu ? pick_gpb<true>(tpw, gpb) : pick_gpb<false>(tpw, gpb); }
+
 }  // namespace
 
 size_t decode_workspace_bytes(int n, const QW* w, const LR* c, int T) {
@@ -1044,8 +1101,8 @@ hipError_t launch_decode_mfma(int n, const QW* w, const LR* c, const void* x, in
     a.cps = 0;
     a.kp = mp.kp;
     a.h = glu ? y[0] : nullptr;
-    auto kern = glu ? (tpw == 4 ? decode_mfma_kernel<4, 2, true> : decode_mfma_kernel<1, 4, true>)
-                    : (tpw == 4 ? decode_mfma_kernel<4, 2, false> : decode_mfma_kernel<1, 4, false>);
+    const int gpb = mfma_groups_per_block(w[0].G);
+    auto kern = pick_mfma_kernel(tpw, glu, gpb);
     // a gated window runs one workgroup of eight waves per gate workgroup
     // (four waves on the gate's tiles, four on the up tiles of the same rows),
     // with both linears' scales and zeros in LDS

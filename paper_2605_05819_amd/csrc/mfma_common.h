@@ -1,5 +1,6 @@
-// Device helpers shared by the MFMA kernels (prefill GEMM, many-token decode):
-// in-register dequantization of 4-bit codes to fp16 and the fp16 MFMA.
+// Device helpers shared by the MFMA kernels (prefill GEMM, many-token decode,
+// MoE): in-register unpack of 4-bit codes to exact fp16 integers q - z, the
+// 4 x 4 transpose of code words across lane groups, and the fp16 MFMA.
 #pragma once
 
 #include "cl_device.h"
@@ -14,41 +15,91 @@ __device__ __forceinline__ uint32_t and_or(uint32_t x, uint32_t m, uint32_t c) {
     return r;
 }
 
-// Per-fragment constants of one quantization group for dequant_word4x, two
-// halves per register: (s, s/16) and (1024 + z, 1024 + 16 z).
-struct Dq {
-    f16x2 s, z;
+// Zero-point constants of one quantization group for codes_minus_zero, both
+// halves of each register equal: -(1024 + z) and -(64 + z) (exact: z < 16).
+struct Zq {
+    f16x2 lo, hi;
 };
 
-__device__ __forceinline__ Dq make_dq(uint32_t sbits, uint32_t zbits) {
-    const f16 s = __builtin_bit_cast(f16, static_cast<uint16_t>(sbits));
+__device__ __forceinline__ Zq make_zq(uint32_t zbits) {
     const f16 z = __builtin_bit_cast(f16, static_cast<uint16_t>(zbits));
-    const f16 s16 = s * static_cast<f16>(0.0625f);                     // exact unless subnormal
-    const f16 z1 = static_cast<f16>(1024.0f) + z;                      // exact: z < 16
-    const f16 z16 = static_cast<f16>(1024.0f) + z * static_cast<f16>(16.0f);
-    return Dq{f16x2{s, s16}, f16x2{z1, z16}};
+    const f16 a = -(static_cast<f16>(1024.0f) + z);
+    const f16 b = -(static_cast<f16>(64.0f) + z);
+    return Zq{f16x2{a, a}, f16x2{b, b}};
 }
 
-// One 32-bit word of 4-bit codes -> 8 fp16 values s (q - z), pair order
-// (q0,q4),(q1,q5),(q2,q6),(q3,q7), with one shift and four masks: a code
-// left in bits 4..7 of a half reads as 1024 + 16 q, so its pair subtracts
-// 1024 + 16 z (exact) and scales by s/16.
-__device__ __forceinline__ u32x4 dequant_word4x(uint32_t w, const Dq& d, uint32_t mlo, uint32_t mhi,
-                                               uint32_t bias) {
+// One 32-bit word of 4-bit codes -> 8 fp16 values q - z, exact integers in
+// -15..15, pair order (q0,q4),(q1,q5),(q2,q6),(q3,q7).  A code OR-ed into the
+// mantissa of 1024.0 (bits 0x6400) reads as 1024 + q, so adding -(1024 + z)
+// is exact; a code left in bits 4..7 of the half reads as 1024 + 16 q, and one
+// fused multiply-add (1024 + 16 q) / 16 - (64 + z) is exact as well.  One
+// shift, four v_and_or_b32, two packed adds and two packed FMAs per word.
+__device__ __forceinline__ u32x4 codes_minus_zero(uint32_t w, const Zq& zq, uint32_t mlo, uint32_t mhi,
+                                                  uint32_t bias) {
     const uint32_t w8 = w >> 8;
-    const f16x2 s1 = {d.s.x, d.s.x}, s16 = {d.s.y, d.s.y};
-    const f16x2 z1 = {d.z.x, d.z.x}, z16 = {d.z.y, d.z.y};
+    const f16x2 sixteenth = {static_cast<f16>(0.0625f), static_cast<f16>(0.0625f)};
     u32x4 r;
-    r[0] = __builtin_bit_cast(uint32_t, (__builtin_bit_cast(f16x2, and_or(w, mlo, bias)) - z1) * s1);
-    r[1] = __builtin_bit_cast(uint32_t, (__builtin_bit_cast(f16x2, and_or(w, mhi, bias)) - z16) * s16);
-    r[2] = __builtin_bit_cast(uint32_t, (__builtin_bit_cast(f16x2, and_or(w8, mlo, bias)) - z1) * s1);
-    r[3] = __builtin_bit_cast(uint32_t, (__builtin_bit_cast(f16x2, and_or(w8, mhi, bias)) - z16) * s16);
+    r[0] = __builtin_bit_cast(uint32_t, __builtin_bit_cast(f16x2, and_or(w, mlo, bias)) + zq.lo);
+    r[1] = __builtin_bit_cast(
+        uint32_t, __builtin_elementwise_fma(__builtin_bit_cast(f16x2, and_or(w, mhi, bias)), sixteenth, zq.hi));
+    r[2] = __builtin_bit_cast(uint32_t, __builtin_bit_cast(f16x2, and_or(w8, mlo, bias)) + zq.lo);
+    r[3] = __builtin_bit_cast(
+        uint32_t, __builtin_elementwise_fma(__builtin_bit_cast(f16x2, and_or(w8, mhi, bias)), sixteenth, zq.hi));
     return r;
+}
+
+// s (q - z) as fp16, one rounding per value (the dequantized tile of the
+// prefill GEMM); the integer q - z is formed exactly first, so the rounding
+// is relative 2^-11 down to the fp16 normal range whatever the scale.
+__device__ __forceinline__ u32x4 dequant_word4x(uint32_t w, const Zq& zq, f16x2 s2, uint32_t mlo, uint32_t mhi,
+                                               uint32_t bias) {
+    u32x4 r = codes_minus_zero(w, zq, mlo, mhi, bias);
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+        const uint32_t v = r[p];
+        r[p] = __builtin_bit_cast(uint32_t, __builtin_bit_cast(f16x2, v) * s2);
+    }
+    return r;
+}
+
+// 4 x 4 transpose across the four 16-lane groups of a wave: on entry lane
+// group g holds words 4 g .. 4 g + 3 of a 16-word run in w[0..3]; on return
+// w[t] holds word 4 t + g.  v_permlane32_swap exchanges rows 2-3 of its first
+// operand with rows 0-1 of its second, v_permlane16_swap the odd rows of the
+// first with the even rows of the second (a row is 16 lanes).
+__device__ __forceinline__ void transpose_words(uint32_t (&w)[4]) {
+    const auto a = __builtin_amdgcn_permlane32_swap(w[0], w[2], false, false);
+    const auto b = __builtin_amdgcn_permlane32_swap(w[1], w[3], false, false);
+    const auto c = __builtin_amdgcn_permlane16_swap(a[0], b[0], false, false);
+    const auto d = __builtin_amdgcn_permlane16_swap(a[1], b[1], false, false);
+    w[0] = c[0];
+    w[1] = c[1];
+    w[2] = d[0];
+    w[3] = d[1];
 }
 
 __device__ __forceinline__ f32x4 mfma(const u32x4& a, const u32x4& b, const f32x4& c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), c,
                                                   0, 0, 0);
+}
+
+// Two fp32 values as fp16 pairs hi = fp16(v) and lo = fp16(v - hi): an
+// MFMA step over hi and one over lo carry v to about 2^-22 relative (the
+// difference v - hi is exact in fp32), where hi alone would round it to
+// 2^-11.
+__device__ __forceinline__ void split_f16x2(float a, float b, uint32_t& hi, uint32_t& lo) {
+    const f16 ha = static_cast<f16>(a), hb = static_cast<f16>(b);
+    const f16 la = static_cast<f16>(a - static_cast<float>(ha)), lb = static_cast<f16>(b - static_cast<float>(hb));
+    hi = __builtin_bit_cast(uint32_t, f16x2{ha, hb});
+    lo = __builtin_bit_cast(uint32_t, f16x2{la, lb});
+}
+
+// acc += s * p, elementwise in fp32
+__device__ __forceinline__ f32x4 fma4(float s, const f32x4& p, const f32x4& acc) {
+    f32x4 r;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) r[e] = fmaf(s, p[e], acc[e]);
+    return r;
 }
 
 }  // namespace cl

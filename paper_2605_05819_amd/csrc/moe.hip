@@ -43,6 +43,12 @@
 
 namespace cl {
 
+// Routing-error record of this device: zero, or bit 63 set with the slot
+// (bits 32..62) and the id (bits 0..31) of an out-of-range routing entry seen
+// by a MoE call since the record was last read.  Each device holds its own
+// copy for the life of the process.
+__device__ unsigned long long moe_routing_error;
+
 namespace {
 
 // rows per wave batch: 4 for 4-bit codes, 2 for 2-bit (twice the
@@ -112,7 +118,6 @@ __global__ __launch_bounds__(256) void moe_prep_kernel(MoeArgs a) {
     const int S = a.T * a.k;
     const int blk = blockIdx.x;
 
-    const int max_active = S < a.E ? S : a.E;
     if (blk < a.lin[a.n - 1].prep_end) {
         // workgroup (linear li, j, quad): the j-th routed expert (ascending
         // id), its rank rows 4 quad .. 4 quad + 3 of linear li; every
@@ -179,6 +184,13 @@ __global__ __launch_bounds__(256) void moe_prep_kernel(MoeArgs a) {
                 for (int sl = wave; sl < S; sl += 4) {
                     const int id = sids[sl];
                     if (id >= 0 && id < a.E) continue;
+                    // the device's routing-error record (reported by
+                    // cl_moe_status): a flag bit, the slot and the id
+                    if (li == 0 && lane == 0)
+                        __hip_atomic_store(&moe_routing_error,
+                                           (1ull << 63) | (static_cast<unsigned long long>(sl) << 32) |
+                                               static_cast<uint32_t>(id),
+                                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                     for (int o = lane; o < L.d_out; o += 64)
                         store_out(L.y, static_cast<size_t>(sl) * L.d_out + o, 0.f, a.out);
                 }
@@ -539,18 +551,23 @@ void moe_kernel(MoeArgs a) {
 
 // Many slots per expert, 4-bit codes: the expert's rows against its slots on
 // MFMA (v_mfma_f32_16x16x32_f16), so the per-slot VALU work of the kernel
-// above (every slot's dot products on every lane) becomes MFMA columns.
+// above (every slot's dot products on every lane) becomes MFMA rows.
 // Workgroup = (linear, active expert, TPW tiles of 16 rows); its four waves
 // split the 128-code blocks of K (wave w takes blocks w, w + 4, ..., NBUF in
-// flight); the expert's slots go in passes of 16 (the MFMA's columns).  Per
-// block a lane loads, for each tile, 16 bytes of codes of row r = lane % 16
-// (32 codes of one quantization group), and once for all tiles the matching
-// four 16-byte words of prepared activations of its pass's slot r; the codes
-// are dequantized in registers to fp16 s (q - z) with the group's scale and
-// zero from LDS and feed four MFMAs per tile.  The rank term is extra MFMA
-// steps over [B_e | t] (t rounded to fp16); the waves' tiles are summed
-// through LDS in a fixed order; one rounding to the output dtype.
-template <int TPW, int NBUF>
+// flight); the expert's slots go in passes of 16.  Per block a lane loads,
+// for each tile, 16 bytes of codes of row r = lane % 16, and once for all
+// tiles the matching four 16-byte words of prepared activations of its
+// pass's slot r.  The activations are the MFMA's A operand and the codes its
+// B operand, so lane (g, r) accumulates slots 4 g .. 4 g + 3 of the pass for
+// weight row r.  As in the many-token dense decode the codes become the
+// exact fp16 integers q - z and each quantization group's steps run into a
+// fresh fp32 partial that the group's scale multiplies in fp32 (GPB groups
+// per 128-code block; with more than one the code words are transposed
+// across the lane groups first).  The rank term is extra MFMA steps over
+// [t | B_e] (t split into fp16 hi and lo parts, one step each); the waves'
+// tiles are summed through LDS in a fixed order; one rounding to the output
+// dtype.
+template <int TPW, int NBUF, int GPB>
 __global__ __launch_bounds__(256) void moe_mfma_kernel(MoeArgs a) {
     __shared__ f32x4 red[4][TPW][64];
     extern __shared__ uint16_t szl[];             // [2][16 TPW][groups]: the rows' scales, then zeros
@@ -631,24 +648,40 @@ __global__ __launch_bounds__(256) void moe_mfma_kernel(MoeArgs a) {
             for (int j = 0; j < TPW; ++j)
                 b.w[j] = __builtin_nontemporal_load(
                     reinterpret_cast<const u32x4*>(qe + static_cast<size_t>(row[j]) * words_row + wi));
+            // activations of the word this lane feeds to MFMA step t: 4 g + t
+            // of the block, or 4 t + g once the codes are transposed (a word
+            // past K reads word g, met by a zero scale)
 #pragma unroll
-            for (int t = 0; t < 4; ++t) b.x[t] = xr[wi + t];
+            for (int t = 0; t < 4; ++t)
+                b.x[t] = xr[GPB == 1 ? wi + t : (kb * 128 + 32 * t < K ? kb * 16 + 4 * t + g : g)];
         };
         auto compute = [&](int kb, const Blk& b) {
-            // past K or a padding block: scale 0, the weight is 0
-            const int kc = kb * 128 + 32 * g;
-            const bool on = kb < nkb && kc < K;
-            const int gs = on ? kc / a.G : 0;
+            // per group: MFMA steps into a fresh partial of sum (q - z) x,
+            // then acc += s * partial in fp32; past K, past the matrix or a
+            // padding block the scale is 0
+            constexpr int SPG = 4 / GPB;
             u32x4 xv[4];
 #pragma unroll
             for (int t = 0; t < 4; ++t) xv[t] = sv ? b.x[t] : zero;
 #pragma unroll
             for (int j = 0; j < TPW; ++j) {
-                const int lr = (16 * j + r) * groups + gs;
-                const Dq dq = make_dq((on && rowv[j]) ? static_cast<uint32_t>(szl[lr]) : 0u,
-                                      szl[16 * TPW * groups + lr]);
+                uint32_t w[4];
 #pragma unroll
-                for (int t = 0; t < 4; ++t) acc[j] = mfma(dequant_word4x(b.w[j][t], dq, mlo, mhi, bias), xv[t], acc[j]);
+                for (int t = 0; t < 4; ++t) { const uint32_t v = b.w[j][t]; w[t] = v; }
+                if constexpr (GPB > 1) transpose_words(w);
+#pragma unroll
+                for (int q = 0; q < GPB; ++q) {
+                    const int kc = kb * 128 + 32 * SPG * q;
+                    const bool on = kb < nkb && kc < K && rowv[j];
+                    const int lr = (16 * j + r) * groups + (on ? kc / a.G : 0);
+                    const Zq zq = make_zq(szl[16 * TPW * groups + lr]);
+                    f32x4 p = mfma(xv[SPG * q], codes_minus_zero(w[SPG * q], zq, mlo, mhi, bias),
+                                   f32x4{0.f, 0.f, 0.f, 0.f});
+#pragma unroll
+                    for (int t = SPG * q + 1; t < SPG * q + SPG; ++t)
+                        p = mfma(xv[t], codes_minus_zero(w[t], zq, mlo, mhi, bias), p);
+                    acc[j] = fma4(on ? f16_bits_to_f32(szl[lr]) : 0.f, p, acc[j]);
+                }
             }
         };
         constexpr int SPAN = 4 * NBUF;
@@ -669,13 +702,12 @@ __global__ __launch_bounds__(256) void moe_mfma_kernel(MoeArgs a) {
         for (int kr = 32 * wave; kr < rank; kr += 128) {
             const int k = kr + 8 * g;
             const float* trow = L.t + static_cast<size_t>(sl) * L.r_max;
-            uint32_t tw[4];
+            // t as fp16 hi + lo parts, two MFMA steps
+            uint32_t tw[4], tlo[4];
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
                 const int k0 = k + 2 * q, k1 = k + 2 * q + 1;
-                const uint32_t tl = (sv && k0 < rs) ? f32_to_f16_bits(trow[k0]) : 0u;
-                const uint32_t th = (sv && k1 < rs) ? f32_to_f16_bits(trow[k1]) : 0u;
-                tw[q] = tl | (th << 16);
+                split_f16x2((sv && k0 < rs) ? trow[k0] : 0.f, (sv && k1 < rs) ? trow[k1] : 0.f, tw[q], tlo[q]);
             }
 #pragma unroll
             for (int j = 0; j < TPW; ++j) {
@@ -688,25 +720,26 @@ __global__ __launch_bounds__(256) void moe_mfma_kernel(MoeArgs a) {
                     const uint32_t hi = (rowv[j] && k1 < rank) ? brow[k1] : 0u;
                     aw[q] = lo | (hi << 16);
                 }
-                acc[j] = mfma(u32x4{aw[0], aw[1], aw[2], aw[3]}, u32x4{tw[0], tw[1], tw[2], tw[3]}, acc[j]);
+                const u32x4 bop = {aw[0], aw[1], aw[2], aw[3]};
+                acc[j] = mfma(u32x4{tw[0], tw[1], tw[2], tw[3]}, bop, acc[j]);
+                acc[j] = mfma(u32x4{tlo[0], tlo[1], tlo[2], tlo[3]}, bop, acc[j]);
             }
         }
 #pragma unroll
         for (int j = 0; j < TPW; ++j) red[wave][j][lane] = acc[j];
         __syncthreads();
-        // wave w sums and stores tiles w, w + 4, ... in a fixed order
-        if (sv) {
+        // wave w sums and stores tiles w, w + 4, ... in a fixed order;
+        // v[e] = y[slot of pass row 4 g + e][row0 + 16 j + r]
+        int osl[4];
 #pragma unroll
-            for (int j = 0; j < TPW; ++j) {
-                if (j % 4 != wave) continue;
-                const f32x4 v = red[0][j][lane] + red[1][j][lane] + red[2][j][lane] + red[3][j][lane];
-                // v[q] = y[slot sl][row0 + 16 j + 4 g + q]
+        for (int e = 0; e < 4; ++e) osl[e] = __shfl(sl, 4 * g + e, 64);
 #pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const int rr = row0 + 16 * j + 4 * g + q;
-                    if (rr < L.d_out) store_out(L.y, static_cast<size_t>(sl) * L.d_out + rr, v[q], a.out);
-                }
-            }
+        for (int j = 0; j < TPW; ++j) {
+            if (j % 4 != wave || !rowv[j]) continue;
+            const f32x4 v = red[0][j][lane] + red[1][j][lane] + red[2][j][lane] + red[3][j][lane];
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                if (p0 + 4 * g + e < scnt) store_out(L.y, static_cast<size_t>(osl[e]) * L.d_out + row[j], v[e], a.out);
         }
         __syncthreads();                           // red is reused by the next pass
     }
@@ -857,11 +890,33 @@ hipError_t launch_moe_decode(int n, const QW* w, const uint16_t* const* A, const
     if (e != hipSuccess) return e;
     if (on_mfma) {
         const size_t lds = static_cast<size_t>(2) * 16 * kMoeTpw * (d_in / w[0].G) * 2;
-        hipLaunchKernelGGL((moe_mfma_kernel<kMoeTpw, kMoeNbuf>), dim3(blk_end), dim3(256), lds, st, a);
+        // quantization groups a 128-code block can meet (see the kernel)
+        const int G = w[0].G;
+        if (G % 128 == 0)
+            hipLaunchKernelGGL((moe_mfma_kernel<kMoeTpw, kMoeNbuf, 1>), dim3(blk_end), dim3(256), lds, st, a);
+        else if (G % 64 == 0)
+            hipLaunchKernelGGL((moe_mfma_kernel<kMoeTpw, 1, 2>), dim3(blk_end), dim3(256), lds, st, a);
+        else
+            hipLaunchKernelGGL((moe_mfma_kernel<kMoeTpw, 1, 4>), dim3(blk_end), dim3(256), lds, st, a);
         return hipGetLastError();
     }
     return bits == 4 ? launch_moe2<4>(a, lg, nb, many, blk_end, threads, st)
                      : launch_moe2<2>(a, lg, nb, many, blk_end, threads, st);
+}
+
+hipError_t moe_take_routing_error(hipStream_t st, unsigned long long* word) {
+    unsigned long long v = 0;
+    hipError_t e = hipMemcpyFromSymbolAsync(&v, HIP_SYMBOL(moe_routing_error), sizeof(v), 0,
+                                            hipMemcpyDeviceToHost, st);
+    if (e == hipSuccess) e = hipStreamSynchronize(st);
+    if (e == hipSuccess && v) {
+        const unsigned long long zero = 0;
+        e = hipMemcpyToSymbolAsync(HIP_SYMBOL(moe_routing_error), &zero, sizeof(zero), 0, hipMemcpyHostToDevice,
+                                   st);
+        if (e == hipSuccess) e = hipStreamSynchronize(st);
+    }
+    *word = v;
+    return e;
 }
 
 }  // namespace cl

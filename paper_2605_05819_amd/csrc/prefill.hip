@@ -19,8 +19,8 @@
 //     it loads its rows' packed codes for the next K step into registers (one
 //     16-byte load per lane and fragment: 32 codes of one quantization group,
 //     so one scale and zero per lane) and dequantizes them per MFMA step as
-//     s * (q - z) in fp16 ((q | 0x6400) - (1024 + z) is exact, one rounding
-//     for the scale).  No weight tile goes through LDS and no wave repeats
+//     s * (q - z) in fp16 (the integer q - z is formed exactly from the code
+//     OR-ed into the mantissa of 1024.0, then one rounding for the scale).  No weight tile goes through LDS and no wave repeats
 //     another's dequantization.  The workgroup's scales and zeros do go
 //     through LDS, in double-buffered windows of 8 groups per row (one
 //     16-byte load per thread and array per window): per-lane 2-byte
@@ -48,19 +48,6 @@ __device__ __forceinline__ u32x4 act8_permuted(u32x4 u, int act) {
     r[1] = (u0 >> 16) | (u2 & 0xffff0000u);       // x1, x5
     r[2] = (u1 & 0xffffu) | (u3 << 16);           // x2, x6
     r[3] = (u1 >> 16) | (u3 & 0xffff0000u);       // x3, x7
-    return r;
-}
-
-// One 32-bit word of 4-bit codes -> 8 fp16 values s * (q - z) in the order
-// (q0,q4),(q1,q5),(q2,q6),(q3,q7).  (q | 0x6400) is the fp16 1024 + q; minus
-// (1024 + z) is the exact small integer q - z; one multiply rounds.
-__device__ __forceinline__ u32x4 dequant_word4(uint32_t w, f16x2 s2, f16x2 zz) {
-    u32x4 r;
-#pragma unroll
-    for (int p = 0; p < 4; ++p) {
-        const f16x2 h = __builtin_bit_cast(f16x2, ((w >> (4 * p)) & 0x000F000Fu) | 0x64006400u);
-        r[p] = __builtin_bit_cast(uint32_t, (h - zz) * s2);
-    }
     return r;
 }
 
@@ -337,7 +324,7 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
     const uint32_t bias = 0x64006400u;
     const int fr = xswz(r);
     auto compute = [&](int kb, int st, const WStep<BITS> (&ws)[4]) {
-        Dq dq[4];
+        Zq zq[4];
         f16x2 s2[4], zz[4];
         const bool kval = kb * BK + 32 * g < a.K;
         const int gi = kval ? (kb * BK + 32 * g) / a.G : 0;
@@ -349,7 +336,9 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
             const uint32_t zb = szw[wb][1][nl][we];
             const uint32_t sb = (kval && n0 + 16 * j + r < a.N) ? static_cast<uint32_t>(szw[wb][0][nl][we]) : 0u;
             if constexpr (BITS == 4) {
-                dq[j] = make_dq(sb, zb);
+                const f16 sv = __builtin_bit_cast(f16, static_cast<uint16_t>(sb));
+                zq[j] = make_zq(zb);
+                s2[j] = f16x2{sv, sv};
             } else {
                 const f16 sv = __builtin_bit_cast(f16, static_cast<uint16_t>(sb));
                 const f16 zf = static_cast<f16>(1024.0f) + __builtin_bit_cast(f16, static_cast<uint16_t>(zb));
@@ -362,7 +351,7 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
             u32x4 bf[4];
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                if constexpr (BITS == 4) bf[j] = dequant_word4x(ws[j].w[t], dq[j], mlo, mhi, bias);
+                if constexpr (BITS == 4) bf[j] = dequant_word4x(ws[j].w[t], zq[j], s2[j], mlo, mhi, bias);
                 else bf[j] = dequant_half2(ws[j].w[t >> 1], t & 1, s2[j], zz[j]);
             }
             const int slot = (4 * g + t) ^ fr;
