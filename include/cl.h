@@ -181,6 +181,27 @@ cl_status cl_linear_decode(const cl_qweight* w, const cl_lowrank* c, const void*
                            size_t ws_bytes, void* stream);
 
 /*
+ * cl_linear_decode_noalloc -- cl_linear_decode for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation): the same kernels and the same result,
+ * bit for bit, with the workspace taken from a scratch array the library
+ * holds on each device instead of a caller's buffer.  The call allocates
+ * nothing; on its first call on a device it looks up that device's array.
+ *
+ *  w, c, x, T, act_dtype, y, out_dtype, stream  as cl_linear_decode
+ * The scratch holds CL_NOALLOC_SCRATCH_BYTES per device (enough for T <= 64,
+ * d_in <= 16384 and rank <= 256); a call needing more (cl_linear_workspace
+ * of its arguments) returns CL_EWORKSPACE.  Every call on a device uses the
+ * same array and overwrites what the last call left there (nothing in it
+ * needs to start at zero), so calls that may overlap on one device -- on
+ * different streams, or from different threads -- race; serialize them.
+ * Errors: as cl_linear_decode.
+ */
+#define CL_NOALLOC_SCRATCH_BYTES (4u << 20)
+cl_status cl_linear_decode_noalloc(const cl_qweight* w, const cl_lowrank* c, const void* x, int32_t T,
+                                   int32_t act_dtype, void* y, int32_t out_dtype, void* stream);
+
+/*
  * cl_linear_decode_window -- one compensation window: n linears that read the
  * same activations x, each with its own backbone, factors and output.  The
  * paper groups the Q, K and V projections, and the gate and up projections,

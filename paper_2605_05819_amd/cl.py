@@ -51,6 +51,9 @@ _SIGNATURES = {
     "cl_linear_decode": (ctypes.c_int32, [ctypes.POINTER(QWeightC), ctypes.POINTER(LowRankC), ctypes.c_void_p,
                                           ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32,
                                           ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
+    "cl_linear_decode_noalloc": (ctypes.c_int32, [ctypes.POINTER(QWeightC), ctypes.POINTER(LowRankC),
+                                                  ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
+                                                  ctypes.c_int32, ctypes.c_void_p]),
     "cl_prefill_workspace": (ctypes.c_size_t, [ctypes.POINTER(QWeightC), ctypes.POINTER(LowRankC), ctypes.c_int32]),
     "cl_linear_prefill": (ctypes.c_int32, [ctypes.POINTER(QWeightC), ctypes.POINTER(LowRankC), ctypes.c_void_p,
                                            ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32,
@@ -273,6 +276,27 @@ def linear_decode(w, c, x, out_dtype=torch.float16, y=None, ws=None, stream=None
     _check(lib().cl_linear_decode(ctypes.byref(qc), ctypes.byref(lc) if lc else None, _ptr(x), T,
                                   _DTYPE_CODE[x.dtype], _ptr(y), _DTYPE_CODE[y.dtype], _ptr(ws),
                                   0 if ws is None else ws.numel(), _stream(stream)))
+    return y
+
+
+def linear_decode_noalloc(w, c, x, out_dtype=torch.float16, y=None, stream=None):
+    """``cl_linear_decode_noalloc``: as :func:`linear_decode`, with the
+    library's per-device scratch in place of a workspace (calls overlapping
+    on one device race)."""
+    chk = _Checked()
+    _check_qweight(w, chk)
+    _check_lowrank(c, w, chk)
+    _check_act(x, chk, "x", w.d_in)
+    _need(x.dim() == 2, "x must be [T][d_in]")
+    T = x.shape[0]
+    if y is None:
+        y = torch.empty((T, w.d_out), dtype=out_dtype, device=x.device)
+    _dev_tensor(y, "y", _OUT, (T, w.d_out), chk)
+    chk.on_gpu()
+    qc = w.c()
+    lc = c.c() if c is not None else None
+    _check(lib().cl_linear_decode_noalloc(ctypes.byref(qc), ctypes.byref(lc) if lc else None, _ptr(x), T,
+                                          _DTYPE_CODE[x.dtype], _ptr(y), _DTYPE_CODE[y.dtype], _stream(stream)))
     return y
 
 

@@ -8,6 +8,8 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <mutex>
+
 #include "../../include/cl.h"
 #include "cl_internal.h"
 
@@ -147,9 +149,37 @@ cl_status check_window(int32_t n, const cl_qweight* w, const cl_lowrank* c, cl::
     return CL_OK;
 }
 
+// Scratch of the no-allocation decode entry point: one array per device,
+// held until the process ends.  In host code `scratch` names a host-side
+// stand-in, not device memory: its device address comes from
+// hipGetSymbolAddress, once per device with that device current, and only
+// that address is ever handed to a kernel.
+constexpr int kMaxDevices = 64;
+static __device__ __align__(256) unsigned char scratch[CL_NOALLOC_SCRATCH_BYTES];
+std::mutex g_scratch_mu;
+void* g_scratch_dev[kMaxDevices];
+
+hipError_t scratch_address(void** out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_dev[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (!p) return hipErrorInvalidSymbol;
+        g_scratch_dev[dev] = p;
+    }
+    *out = g_scratch_dev[dev];
+    return hipSuccess;
+}
+
+// ws == nullptr with noalloc: the call runs on the device's scratch array
 cl_status decode_common(int32_t n, const cl_qweight* w, const cl_lowrank* c, const void* x, int32_t T,
                         int32_t act_dtype, void* const* y, int32_t out_dtype, void* ws, size_t ws_bytes,
-                        void* stream, const char* who, bool glu = false) {
+                        void* stream, const char* who, bool glu = false, bool noalloc = false) {
     cl::QW qw[8];
     cl::LR lr[8];
     cl_status st = check_window(n, w, c, qw, lr, who);
@@ -169,9 +199,18 @@ cl_status decode_common(int32_t n, const cl_qweight* w, const cl_lowrank* c, con
         if (!aligned(y[i], out_dtype == CL_FP32 ? 4 : 2)) return fail(CL_EINVAL, "%s: misaligned %s", who, out);
     }
     const size_t need = cl::decode_workspace_bytes(n, qw, lr, T);
-    if (!ws || ws_bytes < need)
-        return fail(CL_EWORKSPACE, "%s: workspace of %zu bytes needed (got %zu)", who, need, ws ? ws_bytes : 0);
-    if (!aligned(ws, 256)) return fail(CL_EINVAL, "%s: workspace must be 256-byte aligned", who);
+    if (noalloc) {
+        if (need > CL_NOALLOC_SCRATCH_BYTES)
+            return fail(CL_EWORKSPACE, "%s: this call needs %zu bytes of scratch; the no-allocation entry point "
+                        "holds %zu per device (use cl_linear_decode with a workspace)", who, need,
+                        static_cast<size_t>(CL_NOALLOC_SCRATCH_BYTES));
+        const hipError_t e = scratch_address(&ws);
+        if (e != hipSuccess) return hip_status(e, who);
+    } else {
+        if (!ws || ws_bytes < need)
+            return fail(CL_EWORKSPACE, "%s: workspace of %zu bytes needed (got %zu)", who, need, ws ? ws_bytes : 0);
+        if (!aligned(ws, 256)) return fail(CL_EINVAL, "%s: workspace must be 256-byte aligned", who);
+    }
     return hip_status(cl::launch_linear_decode(n, qw, lr, x, T, act_dtype, y, out_dtype, ws,
                                                static_cast<hipStream_t>(stream), glu), who);
 }
@@ -206,6 +245,13 @@ cl_status cl_linear_decode(const cl_qweight* w, const cl_lowrank* c, const void*
     void* ys[1] = {y};
     return decode_common(1, w, c, x, T, act_dtype, y ? ys : nullptr, out_dtype, ws, ws_bytes, stream,
                          "cl_linear_decode");
+}
+
+cl_status cl_linear_decode_noalloc(const cl_qweight* w, const cl_lowrank* c, const void* x, int32_t T,
+                                   int32_t act_dtype, void* y, int32_t out_dtype, void* stream) {
+    void* ys[1] = {y};
+    return decode_common(1, w, c, x, T, act_dtype, y ? ys : nullptr, out_dtype, nullptr, 0, stream,
+                         "cl_linear_decode_noalloc", false, true);
 }
 
 size_t cl_prefill_workspace(const cl_qweight* w, const cl_lowrank* c, int32_t M) {

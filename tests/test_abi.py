@@ -239,3 +239,21 @@ def test_build_compensation_validation():
     assert n >= 8 * (1024 * 4096 + 2 * 1024 * 1024)
     assert lib.cl_build_compensation_workspace(64, 256, 65) == 0
     assert lib.cl_build_compensation_workspace(64, 256, 0) > 0
+
+
+def test_noalloc_decode_validates_and_rejects_calls_beyond_its_scratch():
+    """cl_linear_decode_noalloc checks its arguments as cl_linear_decode does
+    and refuses, before any GPU call, a call whose workspace would exceed the
+    per-device scratch (CL_NOALLOC_SCRATCH_BYTES = 4 MiB)."""
+    lib = cl.lib()
+
+    def call(qw, lr=None, T=1, x=FAKE, y=FAKE):
+        return lib.cl_linear_decode_noalloc(ctypes.byref(qw), ctypes.byref(lr) if lr else None, ctypes.c_void_p(x),
+                                            T, cl.CL_FP16, ctypes.c_void_p(y), cl.CL_FP16, None)
+    assert call(_qw(bits=3)) == cl.CL_EUNSUPPORTED
+    assert call(_qw(), T=65) == cl.CL_EINVAL
+    assert call(_qw(), x=0) == cl.CL_EINVAL
+    big, lr = _qw(d_in=32768), cl.LowRankC(FAKE, FAKE, 256, 256)
+    assert lib.cl_linear_workspace(ctypes.byref(big), ctypes.byref(lr), 64) > 4 << 20
+    assert call(big, lr, T=64) == cl.CL_EWORKSPACE
+    assert b"scratch" in lib.cl_last_error()
