@@ -22,8 +22,12 @@ out, in fp64:
 
 Codes are computed against the *stored* fp16 scale, so the kernel that
 dequantizes sees exactly the grid the codes were chosen on.  Packing is
-LSB-first: the code of column ``c`` sits in 32-bit word ``c // (32 // b)`` of its
-row at bit offset ``b * (c % (32 // b))``.
+LSB-first over the row's bit string: the code of column ``c`` occupies bits
+``b c .. b c + b - 1`` of the row, and bit ``i`` of the row is bit ``i % 32`` of
+its 32-bit word ``i // 32``.  For b = 2 and 4 the code of column ``c`` is then
+in word ``c // (32 // b)`` at bit offset ``b * (c % (32 // b))``; for b = 3 (the
+paper's INT3 backbone) 32 codes fill 3 words and the codes of columns
+``32 k + 10`` and ``32 k + 21`` straddle two words.
 
 Readings the paper leaves open (fixed here, listed in the design notes): RTN for
 GPTQ without calibration data; 0 inside the grid; the degenerate all-equal
@@ -81,26 +85,32 @@ def quantize(W, bits, group_size):
 
 
 def pack(codes, bits):
-    """Pack integer codes ``[d_out][d_in]`` LSB-first into uint32 words."""
-    codes = np.asarray(codes, dtype=np.uint64)
+    """Pack integer codes ``[d_out][d_in]`` LSB-first into uint32 words: the
+    row's codes are written out as a bit string (code ``c`` at bits
+    ``bits * c ..``, least significant bit first) that is cut into 32-bit
+    words, least significant bit first.  ``d_in * bits`` must be a multiple
+    of 32."""
+    codes = np.asarray(codes, dtype=np.int64)
     d_out, d_in = codes.shape
-    per_word = 32 // bits
-    if d_in % per_word:
-        raise ValueError("d_in must be a multiple of 32 / bits")
-    c = codes.reshape(d_out, d_in // per_word, per_word)
-    shifts = (np.arange(per_word, dtype=np.uint64) * np.uint64(bits))
-    words = (c << shifts).sum(axis=2, dtype=np.uint64)
+    if (d_in * bits) % 32:
+        raise ValueError("d_in * bits must be a multiple of 32")
+    if codes.min(initial=0) < 0 or codes.max(initial=0) >= (1 << bits):
+        raise ValueError("codes out of range")
+    # bit j of code c is bit bits * c + j of the row
+    bitstr = ((codes[:, :, None] >> np.arange(bits)) & 1).reshape(d_out, d_in * bits)
+    # bit i of the row is bit i % 32 of word i // 32
+    w = bitstr.reshape(d_out, d_in * bits // 32, 32).astype(np.uint64)
+    words = (w << np.arange(32, dtype=np.uint64)).sum(axis=2, dtype=np.uint64)
     return words.astype(np.uint32)
 
 
 def unpack(Q, bits, d_in):
     """Inverse of :func:`pack`: uint32 ``[d_out][d_in*bits/32]`` -> int64 codes."""
     Q = np.asarray(Q, dtype=np.uint32)
-    per_word = 32 // bits
-    col = np.arange(d_in)
-    shift = (bits * (col % per_word)).astype(np.uint32)
-    words = Q[:, col // per_word]
-    return ((words >> shift) & np.uint32((1 << bits) - 1)).astype(np.int64)
+    d_out = Q.shape[0]
+    bitstr = ((Q[:, :, None].astype(np.int64) >> np.arange(32)) & 1).reshape(d_out, -1)[:, :d_in * bits]
+    b = bitstr.reshape(d_out, d_in, bits)
+    return (b << np.arange(bits)).sum(axis=2).astype(np.int64)
 
 
 def dequant(codes, scales, zeros, group_size):

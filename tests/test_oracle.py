@@ -93,7 +93,7 @@ def test_hand_worked_groups():
         assert int(Q[0, 0]) == int(ex["packed_word_hex"], 16)
 
 
-@pytest.mark.parametrize("bits", [2, 4])
+@pytest.mark.parametrize("bits", [2, 3, 4])
 def test_one_sided_groups_keep_zero_on_the_grid(bits):
     """All-positive and all-negative groups: the grid still contains 0, so a
     group of exact multiples of a power-of-two step is recovered exactly."""
@@ -113,7 +113,7 @@ def test_one_sided_groups_keep_zero_on_the_grid(bits):
     np.testing.assert_array_equal(quant.dequant(codes, s, z, G), W.astype(np.float64))
 
 
-@pytest.mark.parametrize("bits", [2, 4])
+@pytest.mark.parametrize("bits", [2, 3, 4])
 def test_on_grid_weights_are_recovered_exactly(bits):
     """Weights built on a grid with a power-of-two step are fixed points of
     quantize -> dequantize: same codes, same zero point, zero residual."""
@@ -143,7 +143,7 @@ def test_round_half_to_even_on_exact_ties():
     assert (codes[0] - 3).tolist() == [-3, 12, 2, 4, 0, -2, 0, 6]
 
 
-@pytest.mark.parametrize("bits,G", [(4, 8), (2, 8), (4, 128), (2, 64)])
+@pytest.mark.parametrize("bits,G", [(4, 8), (2, 8), (3, 8), (4, 128), (2, 64), (3, 128)])
 def test_codes_are_brute_force_nearest_grid_points(bits, G):
     g = np.random.default_rng(100 + bits + G)
     qmax = (1 << bits) - 1
@@ -168,7 +168,7 @@ def test_codes_are_brute_force_nearest_grid_points(bits, G):
 
 def test_quantizer_invariants():
     g = np.random.default_rng(7)
-    for bits, G in [(4, 128), (2, 64)]:
+    for bits, G in [(4, 128), (2, 64), (3, 128)]:
         qmax = (1 << bits) - 1
         W = (0.02 * g.standard_normal((64, 512))).astype(np.float32)
         codes, s, z = quant.quantize(W, bits, G)
@@ -213,6 +213,68 @@ def test_pack_random_rows_against_integer_arithmetic(bits):
         for wi in range(5):
             expect = sum(int(codes[o, wi * per + j]) << (bits * j) for j in range(per))
             assert int(Q[o, wi]) == expect
+    np.testing.assert_array_equal(quant.unpack(Q, bits, codes.shape[1]), codes)
+
+
+def _pack3_examples():
+    blocks = []
+    cur = {}
+    for line in open(os.path.join(GOLDEN, "pack3_straddling_codes.txt")):
+        line = line.strip()
+        if not line or line.startswith("#"):
+            continue
+        key, val = line.split(":", 1)
+        cur[key] = val.split()
+        if key == "words_hex":
+            blocks.append(cur)
+            cur = {}
+    return blocks
+
+
+def test_pack3_hand_worked_straddling_codes():
+    """3-bit codes: the hand-worked units of the golden file, including the
+    two codes of every 32 that straddle a word boundary."""
+    ex = _pack3_examples()
+    assert len(ex) == 4
+    for e in ex:
+        codes = np.array([int(t) for t in e["codes"]], dtype=np.int64)[None, :]
+        Q = quant.pack(codes, 3)
+        assert [int(v) for v in Q[0]] == [int(h, 16) for h in e["words_hex"]]
+        np.testing.assert_array_equal(quant.unpack(Q, 3, 32), codes)
+
+
+def _row_as_integer_words(codes_row, bits):
+    """Words of a row read off one big integer sum(code_c << (bits c))."""
+    v = 0
+    for c, q in enumerate(codes_row):
+        v += int(q) << (bits * c)
+    n = len(codes_row) * bits // 32
+    return [(v >> (32 * i)) & 0xFFFFFFFF for i in range(n)]
+
+
+def test_pack3_exhaustive_slots_and_values():
+    """Every value 0..7 at every one of the 32 positions of a 3-word unit
+    (codes 10 and 21 straddle words) against the row read as one integer."""
+    rows = []
+    for slot in range(32):
+        for v in range(8):
+            r = np.zeros(32, dtype=np.int64)
+            r[slot] = v
+            rows.append(r)
+    codes = np.array(rows)
+    Q = quant.pack(codes, 3)
+    for i, r in enumerate(rows):
+        assert [int(w) for w in Q[i]] == _row_as_integer_words(r, 3), i
+    np.testing.assert_array_equal(quant.unpack(Q, 3, 32), codes)
+
+
+@pytest.mark.parametrize("bits", [2, 3, 4])
+def test_pack_random_rows_against_one_integer_per_row(bits):
+    g = np.random.default_rng(10 + bits)
+    codes = g.integers(0, 1 << bits, (6, 160))
+    Q = quant.pack(codes, bits)
+    for o in range(codes.shape[0]):
+        assert [int(w) for w in Q[o]] == _row_as_integer_words(codes[o], bits)
     np.testing.assert_array_equal(quant.unpack(Q, bits, codes.shape[1]), codes)
 
 
@@ -357,7 +419,7 @@ def test_8x8_end_to_end_brute_force():
     checked by brute force (scalar loops, exhaustive grid search)."""
     g = np.random.default_rng(8)
     W = (0.02 * g.standard_normal((8, 8))).astype(np.float32)
-    for bits in (2, 4):
+    for bits in (2, 3, 4):
         codes, s, z = quant.quantize(W, bits, 8)
         W_hat = quant.dequant(codes, s, z, 8)
         A, B, sigma = comp.build_compensation(W, W_hat, 8)
