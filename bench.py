@@ -18,11 +18,12 @@ HIP events on the stream it runs on, the fp64 CPU oracle timed on a bounded
 sample of the same layer, and (unless --no-extras) the other measured
 workloads: the layer at 4 and 16 tokens, the gate,up window against the gated
 call (SiLU(gate x) * (up x) fused), the 2-bit layer with its gate rank
-sweep, prefill (M = 2048) in TFLOP/s and the 48-layer MoE decode.
+sweep, the 3-bit layer (the paper's INT3 setting), prefill (M = 2048) in
+TFLOP/s and the 48-layer MoE decode.
 
 --copy-calibration runs only a plain 256 MiB device-to-device copy (the
 reference kernel for scaling HBM traffic counters) and prints its size;
---only {decode,tokens,glu,layer2bit,prefill,moe} runs one workload (for
+--only {decode,tokens,glu,layer2bit,layer3bit,prefill,moe} runs one workload (for
 profiling): "decode" prints the line above without extras or CPU baseline,
 the others print their own results.
 """
@@ -77,7 +78,8 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-extras", action="store_true")
     p.add_argument("--copy-calibration", action="store_true")
-    p.add_argument("--only", choices=("decode", "tokens", "glu", "layer2bit", "prefill", "moe"), default=None,
+    p.add_argument("--only", choices=("decode", "tokens", "glu", "layer2bit", "layer3bit", "prefill", "moe"),
+                   default=None,
                    help="run one workload and print its own JSON line (for profiling)")
     return p.parse_args()
 
@@ -87,7 +89,7 @@ def algorithmic_bytes(spec, T, rank=None):
     fp16 scales and zeros, the used rows of A and columns of B, activations in
     and fp16 outputs out."""
     r = spec.rank if rank is None else rank
-    q = spec.d_out * spec.d_in * spec.bits // 8
+    q = spec.d_out * spec.d_in * spec.bits // 8       # 3-bit: 12 bytes per 32 codes
     sz = 2 * 2 * spec.d_out * (spec.d_in // spec.group_size)
     ab = 2 * r * (spec.d_in + spec.d_out)
     return q + sz + ab + 2 * T * spec.d_in + 2 * T * spec.d_out
@@ -262,6 +264,25 @@ def bench_layer2bit(torch, cl, wl, timer, dev, rotate_gib):
             "ranks": "/".join(str(s.rank) for s in layer2.linears), "gate_rank_sweep": sweep}
 
 
+def bench_layer3bit(torch, cl, wl, timer, dev, rotate_gib):
+    """The 3-bit group-128 layer (the paper's INT3 dense setting; ranks
+    from {0, 16, 32, 64, 128} under 64 x 7) at one and four tokens, on the
+    dot2 backbone."""
+    layer3 = wl.llama_layer_3bit()
+    copies3 = device_layer(torch, cl, wl, layer3, dev, rotate_gib)
+    res = {"ranks": "/".join(str(s.rank) for s in layer3.linears)}
+    for T in (1, 4):
+        ms3, xs3, ys3 = layer_step(torch, cl, wl, timer, copies3, layer3, T, dev, 80, 8)
+        b3 = sum(algorithmic_bytes(s, T) for s in layer3.linears)
+        res["T%d" % T] = {"ms_per_step": round(ms3, 5), "gbs": round(b3 / (ms3 * 1e-3) / 1e9, 1),
+                          "step_bytes": b3}
+        if T == 1:
+            g3 = [s.name for s in layer3.linears].index("gate")
+            u = per_matrix(torch, cl, timer, copies3, layer3.linears, xs3, ys3, 1, dev, m_only=g3)["gate"]
+            res["gate_T1"] = {"us": round(u, 3), "gbs": round(algorithmic_bytes(layer3.linears[g3], 1) / u / 1e3, 1)}
+    return res
+
+
 def bench_prefill(torch, cl, wl, timer, dev):
     """M = 2048 tokens through 4096 x 4096 and 14336 x 4096, rank 64, fp16
     and bf16 activations: us per call and TFLOP/s (2MNK + 2Mr(K + N)); and,
@@ -394,6 +415,9 @@ def main():
     if only == "layer2bit":
         print(json.dumps({"layer_2bit_g64_T1": bench_layer2bit(torch, cl, wl, timer, dev, args.rotate_gib)}))
         return
+    if only == "layer3bit":
+        print(json.dumps({"layer_3bit_g128": bench_layer3bit(torch, cl, wl, timer, dev, args.rotate_gib)}))
+        return
     copies = device_layer(torch, cl, wl, layer, dev, args.rotate_gib)
     ncopies = len(copies)
     if only == "tokens":
@@ -422,6 +446,8 @@ def main():
         del copies
         torch.cuda.empty_cache()
         extras["layer_2bit_g64_T1"] = bench_layer2bit(torch, cl, wl, timer, dev, args.rotate_gib)
+        torch.cuda.empty_cache()
+        extras["layer_3bit_g128"] = bench_layer3bit(torch, cl, wl, timer, dev, args.rotate_gib)
         torch.cuda.empty_cache()
         extras["prefill_M2048_r64"] = bench_prefill(torch, cl, wl, timer, dev)
         extras["moe_48_layers"] = bench_moe(torch, cl, wl, timer, dev)

@@ -28,12 +28,17 @@ cl_status fail(cl_status code, const char* fmt, ...) {
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
 cl_status check_shape(int d_out, int d_in, int bits, int G, const char* who) {
-    if (bits == 3) return fail(CL_EUNSUPPORTED, "%s: 3-bit packing is not implemented", who);
-    if (bits != 2 && bits != 4) return fail(CL_EUNSUPPORTED, "%s: bits must be 2 or 4 (got %d)", who, bits);
+    if (bits != 2 && bits != 3 && bits != 4)
+        return fail(CL_EUNSUPPORTED, "%s: bits must be 2, 3 or 4 (got %d)", who, bits);
     if (d_out <= 0 || d_in <= 0) return fail(CL_EINVAL, "%s: d_out and d_in must be positive", who);
-    const int run = 128 / bits;   // codes in one 16-byte run
+    // codes of one run never straddle two groups: a 16-byte run at 2 and 4
+    // bits, a 3-word run of 32 codes at 3 bits
+    const int run = bits == 3 ? 32 : 128 / bits;
     if (G <= 0 || G % run) return fail(CL_EINVAL, "%s: group_size must be a positive multiple of %d for %d-bit codes (got %d)", who, run, bits, G);
     if (d_in % G) return fail(CL_EINVAL, "%s: d_in (%d) must be a multiple of group_size (%d)", who, d_in, G);
+    // rows of 3-bit codes stay 16-byte aligned: d_in * 3 / 8 bytes per row
+    if (bits == 3 && d_in % 128)
+        return fail(CL_EINVAL, "%s: d_in must be a multiple of 128 for 3-bit codes (got %d)", who, d_in);
     return CL_OK;
 }
 
@@ -260,7 +265,7 @@ size_t cl_prefill_workspace(const cl_qweight* w, const cl_lowrank* c, int32_t M)
     cl::QW qw;
     cl::LR lr;
     size_t bytes = 0;
-    if (M >= 1 && check_qweight(w, &qw, "") == CL_OK && check_lowrank(c, qw, &lr, "") == CL_OK)
+    if (M >= 1 && check_qweight(w, &qw, "") == CL_OK && qw.bits != 3 && check_lowrank(c, qw, &lr, "") == CL_OK)
         bytes = cl::prefill_workspace_bytes(qw, lr, M);
     memcpy(g_err, saved, sizeof(g_err));
     return bytes;
@@ -275,6 +280,7 @@ cl_status cl_linear_prefill(const cl_qweight* w, const cl_lowrank* c, const void
     if (st) return st;
     st = check_lowrank(c, qw, &lr, who);
     if (st) return st;
+    if (qw.bits == 3) return fail(CL_EUNSUPPORTED, "%s: 3-bit codes run on the decode entry points only", who);
     if (qw.d_in % 64) return fail(CL_EUNSUPPORTED, "%s: d_in must be a multiple of 64 (got %d)", who, qw.d_in);
     if (M < 1) return fail(CL_EINVAL, "%s: M must be >= 1 (got %d)", who, M);
     if (static_cast<long long>(M) * qw.d_in > (1ll << 31) - 1)
@@ -314,6 +320,7 @@ cl_status moe_common(int32_t n, const cl_qweight* w, const uint16_t* const* A, c
         if (st) return st;
         if (qw[i].d_in != qw[0].d_in || qw[i].bits != qw[0].bits || qw[i].G != qw[0].G)
             return fail(CL_EINVAL, "%s: the linears of a window must share d_in, bits and group size", who);
+        if (qw[i].bits == 3) return fail(CL_EUNSUPPORTED, "%s: 3-bit codes run on the dense decode entry points only", who);
         if (r_max[i] < 0 || r_max[i] > 256) return fail(CL_EINVAL, "%s: r_max must be in 0..256", who);
         if (r_max[i] > 0) {
             if (!A[i] || !B[i] || !ranks[i]) return fail(CL_EINVAL, "%s: null A, B or ranks with r_max %d", who, r_max[i]);
@@ -358,7 +365,7 @@ size_t moe_ws(int32_t n, const cl_qweight* w, const int32_t* r_max, int32_t num_
     int rm[4];
     bool ok = n >= 1 && n <= 4 && w && r_max && num_experts >= 1 && T >= 1 && T <= 64 && k >= 1;
     for (int i = 0; ok && i < n; ++i) {
-        ok = check_qweight(&w[i], &qw[i], "") == CL_OK && r_max[i] >= 0 && r_max[i] <= 256 &&
+        ok = check_qweight(&w[i], &qw[i], "") == CL_OK && qw[i].bits != 3 && r_max[i] >= 0 && r_max[i] <= 256 &&
              qw[i].d_in == qw[0].d_in && qw[i].bits == qw[0].bits && qw[i].G == qw[0].G;
         rm[i] = ok ? r_max[i] : 0;
     }

@@ -81,9 +81,13 @@ __global__ __launch_bounds__(256) void residual_kernel(const float* __restrict__
     if (idx >= total) return;
     const int o = static_cast<int>(idx / w.d_in);
     const int c = static_cast<int>(idx - static_cast<size_t>(o) * w.d_in);
-    const int per_word = 32 / w.bits;
-    const uint32_t word = w.q[static_cast<size_t>(o) * (w.d_in / per_word) + c / per_word];
-    const uint32_t code = (word >> (w.bits * (c % per_word))) & ((1u << w.bits) - 1u);
+    // code c: bits bits * c .. of the row's bit string (3-bit codes can
+    // straddle two words)
+    const uint32_t* row = w.q + static_cast<size_t>(o) * (static_cast<size_t>(w.d_in) * w.bits / 32);
+    const int bp = w.bits * c;
+    uint64_t two = row[bp >> 5];
+    if ((bp & 31) + w.bits > 32) two |= static_cast<uint64_t>(row[(bp >> 5) + 1]) << 32;
+    const uint32_t code = static_cast<uint32_t>(two >> (bp & 31)) & ((1u << w.bits) - 1u);
     const size_t gi = static_cast<size_t>(o) * (w.d_in / w.G) + c / w.G;
     const double what = h2d(w.s[gi]) * (static_cast<double>(code) - h2d(w.z[gi]));
     E[idx] = static_cast<double>(W[idx]) - what;

@@ -173,7 +173,8 @@ __device__ __forceinline__ void row_times_x(const uint16_t* ar, const uint16_t* 
 // (token, chunk).
 template <int BITS>
 __global__ __launch_bounds__(256) void decode_prep_kernel(PrepArgs a) {
-    constexpr int CPW = 32 / BITS, HPW = CPW / 2, PPC = 4 * HPW;
+    constexpr int CPC = BITS == 3 ? 32 : 128 / BITS;   // codes per chunk
+    constexpr int PPC = CPC / 2;
     __shared__ float part[4][4];
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
@@ -224,13 +225,14 @@ __global__ __launch_bounds__(256) void decode_prep_kernel(PrepArgs a) {
         if (tb < T) pass(std::integral_constant<int, 1>{}, tb);
         return;
     }
-    const int chunks = d_in / CPW / 4;
+    const int chunks = d_in / CPC;
     const long long item = static_cast<long long>(blk - rank_blocks) * 256 + tid;
     if (item >= static_cast<long long>(T) * chunks) return;
     const int tok = static_cast<int>(item / chunks);
     const int c = static_cast<int>(item % chunks);
     f16x2 v[PPC];
-    load_chunk_x<BITS>(a.x + static_cast<size_t>(tok) * d_in, c, a.act, v);
+    if constexpr (BITS == 3) load_chunk_x3(a.x + static_cast<size_t>(tok) * d_in, c, a.act, v);
+    else load_chunk_x<BITS>(a.x + static_cast<size_t>(tok) * d_in, c, a.act, v);
     const f16x2 one = {static_cast<f16>(1.0f), static_cast<f16>(1.0f)};
     float sum = 0.f;
     f16x2* dst = a.xp + static_cast<size_t>(tok) * (d_in / 2) + static_cast<size_t>(c) * PPC;
@@ -246,9 +248,9 @@ __global__ __launch_bounds__(256) void decode_prep_kernel(PrepArgs a) {
 // scales and zeros, the rows' factor entries and this lane's entries of A x.
 // Raw loads only: nothing may consume a value at load time, or the wave would
 // stall on the prefetch it is meant to overlap.
-template <int R, int CPL, int NB, int NT>
+template <int R, int CPL, int NB, int NT, int QW = 4>
 struct Batch {
-    u32x4 q[R][CPL];
+    uint32_t q[R][CPL][QW];  // a chunk's code words: 4 (2/4-bit), 3 (3-bit)
     uint16_t s[R][CPL];      // fp16 scale bits
     uint16_t z[R][CPL];      // fp16 zero-point bits
     uint16_t b[R][NB];       // B[row][i] for this lane's factor columns
@@ -267,11 +269,13 @@ template <int BITS, int NT, int CPL, int R, int NB, bool GLU>
 __global__ __launch_bounds__(512)
 __attribute__((amdgpu_waves_per_eu(BITS == 4 && NT == 1 && CPL == 1 && NB <= 1 ? 7 : 1)))
 void decode_kernel(DecodeArgs a) {
-    constexpr int CPW = 32 / BITS;    // codes per word
-    constexpr int HPW = CPW / 2;      // fp16 pairs per word
-    constexpr int CPC = 4 * CPW;      // codes per chunk
-    constexpr int PPC = 4 * HPW;      // pairs per chunk
-    constexpr int NACC = BITS == 4 ? 2 : 4;
+    // a chunk is one lane's unit of codes: 16 bytes = 4 words of 32 / BITS
+    // codes at 2 and 4 bits, 3 words = 32 codes at 3 bits
+    constexpr int QW = BITS == 3 ? 3 : 4;        // words per chunk
+    constexpr int CPC = BITS == 3 ? 32 : 128 / BITS;   // codes per chunk
+    constexpr int HPW = BITS == 3 ? 0 : 16 / BITS;     // fp16 pairs per word (2/4-bit)
+    constexpr int PPC = CPC / 2;      // pairs per chunk
+    constexpr int NACC = BITS == 4 ? 2 : (BITS == 2 ? 4 : 8);
     constexpr int NBA = NB > 0 ? NB : 1;
     constexpr bool XREG = NT * CPL * PPC <= 32;   // activations stay in registers
 
@@ -284,8 +288,8 @@ void decode_kernel(DecodeArgs a) {
     // wave-uniform values in scalar registers: row addressing stays scalar
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int waves = blockDim.x >> 6;
-    const int words = a.d_in / CPW;
-    const int chunks = words / 4;
+    const int words = a.d_in / CPC * QW;          // per row
+    const int chunks = a.d_in / CPC;
     const int groups = a.d_in / a.G;
     const int ks = a.ks;
     const int rg_per_block = waves / ks;
@@ -338,7 +342,7 @@ void decode_kernel(DecodeArgs a) {
         row0 = (lb * rg_per_block + rgw) * R;
     };
 
-    auto load_batch = [&](Batch<R, CPL, NBA, NT>& bt, int b) {
+    auto load_batch = [&](Batch<R, CPL, NBA, NT, QW>& bt, int b) {
         int li, row0;
         locate(b, li, row0);
         const Lin& L = a.lin[li];
@@ -353,9 +357,18 @@ void decode_kernel(DecodeArgs a) {
 #pragma unroll
         for (int r = 0; r < R; ++r) {
             const int row = base + (r < nrows ? r : 0);
-            const u32x4* qr = reinterpret_cast<const u32x4*>(L.q + static_cast<size_t>(row) * words);
+            const uint32_t* qrow = L.q + static_cast<size_t>(row) * words;
 #pragma unroll
-            for (int j = 0; j < CPL; ++j) bt.q[r][j] = __builtin_nontemporal_load(qr + cidx[j]);
+            for (int j = 0; j < CPL; ++j) {
+                if constexpr (QW == 4) {
+                    const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(qrow) + cidx[j]);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) { const uint32_t ve = v[e]; bt.q[r][j][e] = ve; }
+                } else {
+#pragma unroll
+                    for (int e = 0; e < QW; ++e) bt.q[r][j][e] = __builtin_nontemporal_load(qrow + QW * cidx[j] + e);
+                }
+            }
 #pragma unroll
             for (int j = 0; j < CPL; ++j) {
                 const size_t gi = static_cast<size_t>(row) * groups + (cidx[j] * CPC) / a.G;
@@ -379,7 +392,7 @@ void decode_kernel(DecodeArgs a) {
             }
     };
 
-    auto compute_batch = [&](const Batch<R, CPL, NBA, NT>& bt, int b, int buf) {
+    auto compute_batch = [&](const Batch<R, CPL, NBA, NT, QW>& bt, int b, int buf) {
         int li, row0;
         locate(b, li, row0);
         const Lin& L = a.lin[li];
@@ -412,8 +425,12 @@ void decode_kernel(DecodeArgs a) {
                     float d[NACC];
 #pragma unroll
                     for (int k = 0; k < NACC; ++k) d[k] = 0.f;
+                    if constexpr (BITS == 3) {
+                        dot_chunk3(bt.q[r][j][0], bt.q[r][j][1], bt.q[r][j][2], xq, d);
+                    } else {
 #pragma unroll
-                    for (int w = 0; w < 4; ++w) dot_word<BITS>(bt.q[r][j][w], xq + w * HPW, d);
+                        for (int w = 0; w < 4; ++w) dot_word<BITS>(bt.q[r][j][w], xq + w * HPW, d);
+                    }
                     const float sc = f16_bits_to_f32(bt.s[r][j]) * cmask[j];
                     const float zc = f16_bits_to_f32(bt.z[r][j]);
                     // s * (2^24 * sum q x - z * sum x): the codes were subnormals q * 2^-24
@@ -489,7 +506,7 @@ void decode_kernel(DecodeArgs a) {
     constexpr bool kPrefetch = BITS == 4 && CPL == 1 && NT == 2;
     if constexpr (!kPrefetch) {
         for (int it = 0; b < nbatch; b += stride, ++it) {
-            Batch<R, CPL, NBA, NT> bt;
+            Batch<R, CPL, NBA, NT, QW> bt;
             load_batch(bt, b);
             compute_batch(bt, b, it & 1);
         }
@@ -500,7 +517,7 @@ void decode_kernel(DecodeArgs a) {
     // LDS buffers).  Every compute site has a single predecessor shape (next
     // batch issued, or this is the last batch) so the compiler's wait counts
     // let the prefetch stay in flight.
-    Batch<R, CPL, NBA, NT> b0, b1;
+    Batch<R, CPL, NBA, NT, QW> b0, b1;
     load_batch(b0, b);
     for (;;) {
         if (b + stride >= nbatch) { compute_batch(b0, b, 0); break; }
@@ -876,9 +893,11 @@ struct Plan {
     int cpl, R, ks, cps, nt, nb, threads;
 };
 
+// codes per lane chunk: 16 bytes at 2 and 4 bits, 3 words at 3 bits
+int codes_per_chunk(int bits) { return bits == 3 ? 32 : 128 / bits; }
+
 Plan plan(int d_in, int bits, int max_rank, int T) {
-    const int CPW = 32 / bits;
-    const int chunks = d_in / CPW / 4;
+    const int chunks = d_in / codes_per_chunk(bits);
     Plan p;
     p.nt = T >= 4 ? 4 : (T >= 2 ? 2 : 1);
     // One 16-byte chunk per lane and 4 rows per batch measured best on
@@ -1028,14 +1047,14 @@ size_t decode_workspace_bytes(int n, const QW* w, const LR* c, int T) {
         total += mf ? up256(static_cast<size_t>(kp) * T * pad32(c[i].rank) * sizeof(float))
                     : up256(static_cast<size_t>(c[i].rank) * T * sizeof(float));
     if (mf) return total + up256(static_cast<size_t>((T + 15) / 16) * 16 * w[0].d_in * 2);
-    const size_t chunks = static_cast<size_t>(w[0].d_in) / (32 / w[0].bits) / 4;
+    const size_t chunks = static_cast<size_t>(w[0].d_in) / codes_per_chunk(w[0].bits);
     total += up256(static_cast<size_t>(T) * w[0].d_in * 2);
     total += up256(static_cast<size_t>(T) * chunks * sizeof(float));
     return total;
 }
 
 bool decode_fits(const QW& w) {
-    const int chunks = w.d_in / (32 / w.bits) / 4;
+    const int chunks = w.d_in / codes_per_chunk(w.bits);
     return chunks <= 8 * 64 * 2;     // at most 8 K slices of 128 chunks
 }
 
@@ -1147,7 +1166,7 @@ hipError_t launch_linear_decode(int n, const QW* w, const LR* c, const void* x, 
         batch_end += (rgroups + rg_per_block - 1) / rg_per_block;
         a.lin[i] = Lin{w[i].q, w[i].s, w[i].z, c[i].B, y[i], t, w[i].d_out, c[i].rank, c[i].r_max, batch_end};
     }
-    const int chunks = d_in / (32 / bits) / 4;
+    const int chunks = d_in / codes_per_chunk(bits);
     f16x2* xp = reinterpret_cast<f16x2*>(wsb + off);
     off += up256(static_cast<size_t>(T) * d_in * 2);
     float* sx = reinterpret_cast<float*>(wsb + off);
@@ -1164,6 +1183,8 @@ hipError_t launch_linear_decode(int n, const QW* w, const LR* c, const void* x, 
     const unsigned grid = static_cast<unsigned>((rank_end + rows_per_block - 1) / rows_per_block + (items + 255) / 256);
     if (bits == 4)
         hipLaunchKernelGGL(decode_prep_kernel<4>, dim3(grid), dim3(256), 0, st, pa);
+    else if (bits == 3)
+        hipLaunchKernelGGL(decode_prep_kernel<3>, dim3(grid), dim3(256), 0, st, pa);
     else
         hipLaunchKernelGGL(decode_prep_kernel<2>, dim3(grid), dim3(256), 0, st, pa);
     hipError_t e = hipGetLastError();
@@ -1179,7 +1200,7 @@ hipError_t launch_linear_decode(int n, const QW* w, const LR* c, const void* x, 
     a.h = glu ? y[0] : nullptr;
     for (int tok0 = 0; tok0 < T && e == hipSuccess; tok0 += p.nt) {
         a.tok0 = tok0;
-        e = bits == 4 ? launch2<4>(a, p, st) : launch2<2>(a, p, st);
+        e = bits == 4 ? launch2<4>(a, p, st) : (bits == 3 ? launch2<3>(a, p, st) : launch2<2>(a, p, st));
     }
     return e;
 }

@@ -37,6 +37,25 @@ __device__ __forceinline__ void load_chunk_x(const uint16_t* xr, int chunk, int 
     }
 }
 
+// 3-bit codes come in chunks of 32 codes = 3 words (the row's bit string cut
+// into words: codes 8k .. 8k + 7 fill bytes 3k .. 3k + 2 of the chunk's 12).
+// The activations of a chunk are prepared as 16 fp16 pairs: pair i < 8 is
+// (x[i], x[i + 8]), pair 8 + i is (x[16 + i], x[24 + i]); see dot_chunk3.
+__device__ __forceinline__ void load_chunk_x3(const uint16_t* xr, int chunk, int act, f16x2* xv) {
+    uint32_t u[16];                                // u[i] holds (x[2i], x[2i+1]) of the chunk
+#pragma unroll
+    for (int j = 0; j < 4; ++j) load8_f16(xr + chunk * 32 + 8 * j, act, u + 4 * j);
+#pragma unroll
+    for (int h = 0; h < 2; ++h)                    // codes 0..15, then 16..31
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const uint32_t lo = u[8 * h + i / 2], hi = u[8 * h + 4 + i / 2];
+            const uint32_t a = (i & 1) ? (lo >> 16) : (lo & 0xffff);
+            const uint32_t b = (i & 1) ? (hi & 0xffff0000u) : (hi << 16);
+            xv[8 * h + i] = __builtin_bit_cast(f16x2, a | b);
+        }
+}
+
 // Sum R (2, 4 or 8) values over the 64 lanes of a wave with a transposing
 // butterfly.  On return lane l holds the total of value index (l / (64/R)).
 template <int R>
@@ -138,11 +157,54 @@ __device__ __forceinline__ void dot_unpacked(const f16x2* u, const f16x2* xv, fl
     }
 }
 
+// One chunk of 3-bit codes (words w0, w1, w2) against its 16 prepared
+// activation pairs, into 8 accumulators.  A byte permute puts two 8-code
+// groups side by side, one in each fp16 half: bytes (b0 b1 | b3 b4) hold bits
+// 0..15 of codes 0..7 and of codes 8..15, so code i and code i + 8 sit at the
+// same bit offset in both halves and one AND leaves the pair as exact fp16
+// subnormals (code << k) * 2^-24 with the code in mantissa bits k .. k + 2,
+// k <= 7.  Codes 0, 1, 2 come from (b0 b1 | b3 b4) at offsets 0, 3, 6; codes
+// 3, 4, 5 from (b1 b2 | b4 b5) at 1, 4, 7; codes 6, 7 from (b2 | b5) at 2, 5;
+// bytes b6 .. b11 give codes 16 .. 31 the same way.  Accumulator i collects
+// code i's pairs (scale 2^k(i)); combine<3> divides the scales out.  Six
+// permutes, 16 ANDs and 16 v_dot2 per 32 codes.
+__device__ __forceinline__ uint32_t byte_perm(uint32_t hi, uint32_t lo, uint32_t sel) {
+    // byte j of the result is byte s_j of the 8 bytes (hi:lo), s_j = byte j of
+    // the selector: 0..3 pick bytes of lo, 4..7 bytes of hi, 12 gives 0
+    return __builtin_amdgcn_perm(hi, lo, sel);
+}
+
+__device__ __forceinline__ void dot_chunk3(uint32_t w0, uint32_t w1, uint32_t w2, const f16x2* xv, float* d) {
+    constexpr uint32_t m[8] = {0x00070007u, 0x00380038u, 0x01C001C0u, 0x000E000Eu,
+                               0x00700070u, 0x03800380u, 0x001C001Cu, 0x00E000E0u};
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const uint32_t lo = h ? w1 : w0, hi = h ? w2 : w1;
+        // h = 0: bytes b0..b5 (w0 bytes 0-3, w1 bytes 0-1); h = 1: b6..b11
+        // (w1 bytes 2-3, w2 bytes 0-3)
+        const uint32_t p1 = byte_perm(hi, lo, h ? 0x06050302u : 0x04030100u);
+        const uint32_t p2 = byte_perm(hi, lo, h ? 0x07060403u : 0x05040201u);
+        const uint32_t p3 = byte_perm(hi, lo, h ? 0x0C070C04u : 0x0C050C02u);
+        const f16x2* x = xv + 8 * h;
+        d[0] = dot2(__builtin_bit_cast(f16x2, p1 & m[0]), x[0], d[0]);
+        d[1] = dot2(__builtin_bit_cast(f16x2, p1 & m[1]), x[1], d[1]);
+        d[2] = dot2(__builtin_bit_cast(f16x2, p1 & m[2]), x[2], d[2]);
+        d[3] = dot2(__builtin_bit_cast(f16x2, p2 & m[3]), x[3], d[3]);
+        d[4] = dot2(__builtin_bit_cast(f16x2, p2 & m[4]), x[4], d[4]);
+        d[5] = dot2(__builtin_bit_cast(f16x2, p2 & m[5]), x[5], d[5]);
+        d[6] = dot2(__builtin_bit_cast(f16x2, p3 & m[6]), x[6], d[6]);
+        d[7] = dot2(__builtin_bit_cast(f16x2, p3 & m[7]), x[7], d[7]);
+    }
+}
+
 // sum of q * x * 2^-24 over the word(s): the per-scale accumulators with
 // their power-of-two scales removed
 template <int BITS>
 __device__ __forceinline__ float combine(const float* d) {
     if (BITS == 4) return fmaf(d[1], 0.0625f, d[0]);
+    if (BITS == 3)   // code i's accumulator carries 2^k(i), k = 0 3 6 1 4 7 2 5
+        return fmaf(d[5], 0.0078125f, fmaf(d[2], 0.015625f, fmaf(d[7], 0.03125f, fmaf(d[4], 0.0625f,
+                    fmaf(d[1], 0.125f, fmaf(d[6], 0.25f, fmaf(d[3], 0.5f, d[0])))))));
     return fmaf(d[3], 0.015625f, fmaf(d[2], 0.0625f, fmaf(d[1], 0.25f, d[0])));
 }
 

@@ -1,5 +1,6 @@
-// Group-wise asymmetric round-to-nearest quantization + LSB-first packing, and
-// the matching dequantization, for gfx950.
+// Group-wise asymmetric round-to-nearest quantization + LSB-first packing (2,
+// 3 or 4 bits; the row is one bit string cut into 32-bit words), and the
+// matching dequantization, for gfx950.
 //
 // The backbone quantizer of the paper is GPTQ (Section 5.1); without
 // calibration data its error feedback vanishes and it is round-to-nearest on a
@@ -48,14 +49,21 @@ __global__ void quantize_pack_kernel(const float* __restrict__ W, int d_out, int
     s[gi] = sb;
     z[gi] = f32_to_f16_bits(static_cast<float>(zf));  // small integer: exact
 
-    const int per_word = 32 / bits;
-    uint32_t* qrow = q + static_cast<size_t>(o) * (d_in / per_word) + static_cast<size_t>(g) * (G / per_word);
-    for (int wi = 0; wi < G / per_word; ++wi) {
+    // the group's codes as a bit string, LSB first (code j at bits bits * j ..
+    // bits * j + bits - 1), cut into 32-bit words; G * bits is a multiple of
+    // 32, so the group owns whole words.  A 3-bit code can straddle two words:
+    // each word takes the bits of every code that overlaps it.
+    const int wpg = G * bits / 32;
+    uint32_t* qrow = q + static_cast<size_t>(o) * (static_cast<size_t>(d_in) * bits / 32) +
+                     static_cast<size_t>(g) * wpg;
+    for (int wi = 0; wi < wpg; ++wi) {
         uint32_t word = 0;
-        for (int j = 0; j < per_word; ++j) {
-            double r = rint(static_cast<double>(w[wi * per_word + j]) / s16) + zf;
+        for (int j = (32 * wi) / bits; j < G && bits * j < 32 * wi + 32; ++j) {
+            double r = rint(static_cast<double>(w[j]) / s16) + zf;
             r = r < 0.0 ? 0.0 : (r > qmax ? static_cast<double>(qmax) : r);
-            word |= static_cast<uint32_t>(r) << (bits * j);
+            const uint32_t code = static_cast<uint32_t>(r);
+            const int bp = bits * j - 32 * wi;        // -bits < bp < 32
+            word |= bp >= 0 ? code << bp : code >> (-bp);
         }
         qrow[wi] = word;
     }
@@ -68,9 +76,13 @@ __global__ void dequantize_kernel(const uint32_t* __restrict__ q, const uint16_t
     if (i >= static_cast<long long>(d_out) * d_in) return;
     const int o = static_cast<int>(i / d_in);
     const int c = static_cast<int>(i % d_in);
-    const int per_word = 32 / bits;
-    const uint32_t word = q[static_cast<size_t>(o) * (d_in / per_word) + c / per_word];
-    const int code = static_cast<int>((word >> (bits * (c % per_word))) & ((1u << bits) - 1u));
+    // code c: bits bits * c .. of the row's bit string (possibly two words)
+    const uint32_t* row = q + static_cast<size_t>(o) * (static_cast<size_t>(d_in) * bits / 32);
+    const int bp = bits * c;
+    const int wi = bp >> 5, off = bp & 31;
+    uint64_t two = row[wi];
+    if (off + bits > 32) two |= static_cast<uint64_t>(row[wi + 1]) << 32;
+    const int code = static_cast<int>((two >> off) & ((1u << bits) - 1u));
     const size_t gi = static_cast<size_t>(o) * (d_in / G) + c / G;
     out[i] = f16_bits_to_f32(s[gi]) * (static_cast<float>(code) - f16_bits_to_f32(z[gi]));
 }

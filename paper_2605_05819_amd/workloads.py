@@ -236,3 +236,9 @@ def llama_layer(bits=4, group_size=128, levels=(0, 16, 32, 64, 128), per_matrix_
 def llama_layer_2bit():
     """Aggressive variant: 2-bit, group 64, ranks up to 256 under 128 x 7."""
     return llama_layer(2, 64, (0, 16, 32, 64, 128, 256), 128, index=2, tokens=(1,))
+
+
+def llama_layer_3bit():
+    """The paper's dense-model setting: 3-bit codes (INT3, Section 5.1),
+    group 128, ranks from {0, 16, 32, 64, 128} under 64 x 7."""
+    return llama_layer(3, 128, index=7, tokens=(1, 4, 16))

@@ -47,8 +47,10 @@ def _decode(qw, lr=None, T=1, act=cl.CL_FP16, out=cl.CL_FP16, x=FAKE, y=FAKE, ws
 
 
 @pytest.mark.parametrize("kw,status,needle", [
-    (dict(bits=3), cl.CL_EUNSUPPORTED, "3-bit"),
+    (dict(bits=5), cl.CL_EUNSUPPORTED, "bits"),
     (dict(bits=8), cl.CL_EUNSUPPORTED, "bits"),
+    (dict(bits=3, d_in=192, group_size=64), cl.CL_EINVAL, "multiple of 128 for 3-bit"),
+    (dict(bits=3, group_size=48), cl.CL_EINVAL, "group_size"),     # a 32-code run would straddle groups
     (dict(group_size=100), cl.CL_EINVAL, "group_size"),
     (dict(group_size=16), cl.CL_EINVAL, "group_size"),     # a 16-byte run would straddle groups
     (dict(d_in=320), cl.CL_EINVAL, "multiple of group_size"),
@@ -85,7 +87,7 @@ def test_decode_rejects_bad_calls():
 
 def test_workspace_query_is_pure_and_sized_by_rank_and_tokens():
     lib = cl.lib()
-    _decode(_qw(bits=3))
+    _decode(_qw(bits=5))
     before = lib.cl_last_error()
     qw = _qw()
     lr = cl.LowRankC(FAKE, FAKE, 64, 32)
@@ -93,14 +95,17 @@ def test_workspace_query_is_pure_and_sized_by_rank_and_tokens():
     n4 = lib.cl_linear_workspace(ctypes.byref(qw), ctypes.byref(lr), 4)
     assert n1 >= 32 * 4 and n4 - n1 >= 3 * 32 * 4       # A x for every token
     assert 0 < lib.cl_linear_workspace(ctypes.byref(qw), None, 4) < n4     # rank 0: activations only
-    assert lib.cl_linear_workspace(ctypes.byref(_qw(bits=3)), ctypes.byref(lr), 1) == 0
+    assert lib.cl_linear_workspace(ctypes.byref(_qw(bits=5)), ctypes.byref(lr), 1) == 0
+    n3 = lib.cl_linear_workspace(ctypes.byref(_qw(bits=3)), ctypes.byref(lr), 4)
+    assert n3 >= 4 * 32 * 4 + 4 * 256 * 2 + 4 * (256 // 32) * 4    # A x, activations, 32-code chunk sums
     assert lib.cl_last_error() == before
 
 
 def test_quantize_pack_and_dequantize_validate():
     lib = cl.lib()
     p = ctypes.c_void_p(FAKE)
-    assert lib.cl_quantize_pack(p, 64, 256, 3, 128, p, p, p, None) == cl.CL_EUNSUPPORTED
+    assert lib.cl_quantize_pack(p, 64, 256, 5, 128, p, p, p, None) == cl.CL_EUNSUPPORTED
+    assert lib.cl_quantize_pack(p, 64, 320, 3, 32, p, p, p, None) == cl.CL_EINVAL       # 3-bit rows: d_in % 128
     assert lib.cl_quantize_pack(p, 64, 256, 4, 96, p, p, p, None) == cl.CL_EINVAL
     assert lib.cl_quantize_pack(None, 64, 256, 4, 128, p, p, p, None) == cl.CL_EINVAL
     assert lib.cl_quantize_pack(p, 64, 256, 4, 128, ctypes.c_void_p(FAKE + 4), p, p, None) == cl.CL_EINVAL
@@ -153,7 +158,8 @@ def test_moe_validation():
         return lib.cl_moe_linear_decode(ctypes.byref(qw), v(A), v(B), r_max, v(ranks), E, v(x), xps, v(ids), T, k,
                                         act, v(y), out, v(ws), ws_bytes, None)
 
-    assert call(qw=_qw(bits=3)) == cl.CL_EUNSUPPORTED
+    assert call(qw=_qw(bits=3)) == cl.CL_EUNSUPPORTED and b"3-bit" in lib.cl_last_error()
+    assert call(qw=_qw(bits=5)) == cl.CL_EUNSUPPORTED
     assert call(E=0) == cl.CL_EINVAL
     assert call(E=1025) == cl.CL_EUNSUPPORTED
     assert call(T=0) == cl.CL_EINVAL and call(T=65) == cl.CL_EINVAL
@@ -169,7 +175,8 @@ def test_moe_validation():
     assert call(ws=0) == cl.CL_EWORKSPACE and call(ws_bytes=64) == cl.CL_EWORKSPACE
     assert call(ws=FAKE + 64) == cl.CL_EINVAL
     # workspace query: pure, grows with slots and per-slot inputs, 0 when rejected
-    _decode(_qw(bits=3))
+    assert lib.cl_moe_workspace(ctypes.byref(_qw(bits=3)), 8, 16, 2, 4, 0) == 0
+    _decode(_qw(bits=5))
     before = lib.cl_last_error()
     qw = _qw(d_in=2048)
     n1 = lib.cl_moe_workspace(ctypes.byref(qw), 32, 128, 1, 8, 0)
@@ -224,7 +231,7 @@ def test_build_compensation_validation():
         qw = qw or _qw(d_out=64, d_in=256)
         return lib.cl_build_compensation(v(W), ctypes.byref(qw), r_max, v(A), v(B), v(sigma), v(ws), ws_bytes, None)
 
-    assert call(qw=_qw(bits=3)) == cl.CL_EUNSUPPORTED
+    assert call(qw=_qw(bits=5)) == cl.CL_EUNSUPPORTED
     assert call(r_max=65) == cl.CL_EINVAL and b"r_max" in lib.cl_last_error()     # > min(d_out, d_in)
     assert call(r_max=-1) == cl.CL_EINVAL
     assert call(qw=_qw(d_out=300, d_in=512), r_max=257) == cl.CL_EINVAL
@@ -250,10 +257,24 @@ def test_noalloc_decode_validates_and_rejects_calls_beyond_its_scratch():
     def call(qw, lr=None, T=1, x=FAKE, y=FAKE):
         return lib.cl_linear_decode_noalloc(ctypes.byref(qw), ctypes.byref(lr) if lr else None, ctypes.c_void_p(x),
                                             T, cl.CL_FP16, ctypes.c_void_p(y), cl.CL_FP16, None)
-    assert call(_qw(bits=3)) == cl.CL_EUNSUPPORTED
+    assert call(_qw(bits=5)) == cl.CL_EUNSUPPORTED
     assert call(_qw(), T=65) == cl.CL_EINVAL
     assert call(_qw(), x=0) == cl.CL_EINVAL
     big, lr = _qw(d_in=32768), cl.LowRankC(FAKE, FAKE, 256, 256)
     assert lib.cl_linear_workspace(ctypes.byref(big), ctypes.byref(lr), 64) > 4 << 20
     assert call(big, lr, T=64) == cl.CL_EWORKSPACE
     assert b"scratch" in lib.cl_last_error()
+
+
+def test_three_bit_codes_run_on_the_decode_entry_points_only():
+    """3-bit backbones (the paper's INT3, 32 codes in 3 words) are accepted by
+    the quantizer, the dequantizer and the dense decode calls; prefill and the
+    MoE calls refuse them with CL_EUNSUPPORTED."""
+    lib = cl.lib()
+    v = ctypes.c_void_p
+    qw = _qw(bits=3)
+    assert lib.cl_linear_workspace(ctypes.byref(qw), None, 1) > 0
+    assert lib.cl_prefill_workspace(ctypes.byref(qw), None, 16) == 0
+    assert lib.cl_linear_prefill(ctypes.byref(qw), None, v(FAKE), 16, cl.CL_FP16, v(FAKE), cl.CL_FP16, v(FAKE),
+                                 1 << 20, None) == cl.CL_EUNSUPPORTED
+    assert b"3-bit" in lib.cl_last_error()

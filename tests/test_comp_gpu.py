@@ -69,6 +69,7 @@ def _check_factors(W, W_hat, A, B, sigma, r_max):
     (96, 384, 4, 32, 40),          # d_out < d_in: eigenvectors are U
     (97, 256, 2, 64, 97),          # odd size, full rank
     (81, 320, 4, 64, 20),          # odd size, eigenvectors are U
+    (200, 384, 3, 128, 32),        # 3-bit backbone: the residual reads codes that straddle words
 ])
 def test_factors_match_the_oracle(d_out, d_in, bits, G, r_max):
     W = wl.weight((d_out, d_in), 50, d_out, d_in)

@@ -42,7 +42,7 @@ def test_single_linear_1024_rank16_all_out_dtypes():
         _check(w, c, Q, s, z, A, B, 16, x, torch.float16, od, 4, 128)
 
 
-@pytest.mark.parametrize("bits,G", [(4, 128), (2, 64), (4, 32)])
+@pytest.mark.parametrize("bits,G", [(4, 128), (2, 64), (4, 32), (3, 128), (3, 32)])
 @pytest.mark.parametrize("d_out,d_in", [(37, 256), (1000, 768), (4099, 1536)])
 @pytest.mark.parametrize("T", [1, 3, 4, 5, 16])
 def test_ragged_shapes_tokens_and_bits(bits, G, d_out, d_in, T):
@@ -95,7 +95,7 @@ def test_no_factors_equals_rank_zero():
     assert torch.equal(y0, y1)
 
 
-@pytest.mark.parametrize("bits,G", [(4, 128), (2, 64)])
+@pytest.mark.parametrize("bits,G", [(4, 128), (2, 64), (3, 128)])
 def test_bf16_activations(bits, G):
     d_out, d_in = 777, 2048
     W = wl.weight((d_out, d_in), 10, bits)
@@ -127,6 +127,29 @@ def test_llama_layer_full_size_sampled_rows(mat, T):
     Q, s, z = quant.quantize_pack(W[rows], 4, 128)
     ref = linear.forward_packed(Q, s, z, 4, 128, A, B[rows], spec.rank, x.values)
     assert_oracle(out_to_numpy(y)[:, rows], ref)
+
+
+@pytest.mark.parametrize("mat", wl.LLAMA_MATS)
+@pytest.mark.parametrize("T", [1, 4])
+def test_llama_layer_3bit_full_size_sampled_rows(mat, T):
+    """The paper's INT3 setting: every Llama-8B layer linear with 3-bit codes
+    (group 128) at full size, quantized on the GPU, with its allocated rank;
+    sampled rows against the oracle, which quantizes those rows itself."""
+    layer = wl.llama_layer_3bit()
+    spec = [l for l in layer.linears if l.name == mat][0]
+    m = wl.LLAMA_MATS.index(mat)
+    W = wl.weight((spec.d_out, spec.d_in), layer.index, 0, m)
+    w = cl.quantize_pack(torch.from_numpy(W).cuda(), 3, 128)
+    A, B = wl.standin_factors(spec.d_out, spec.d_in, spec.r_max, layer.index, 0, m)
+    c = cl.LowRank(dev_f16(A), dev_f16(B), spec.r_max, spec.rank)
+    x = wl.activation((T, spec.d_in), layer.index, 0, m)
+    for od in (torch.float32, torch.float16):
+        y = cl.linear_decode(w, c, dev_u16(x.bits, torch.float16), out_dtype=od)
+        torch.cuda.synchronize()
+        rows = np.r_[0:4, np.random.default_rng(m).choice(spec.d_out, 120, replace=False), spec.d_out - 4:spec.d_out]
+        Q, s, z = quant.quantize_pack(W[rows], 3, 128)
+        ref = linear.forward_packed(Q, s, z, 3, 128, A, B[rows], spec.rank, x.values)
+        assert_oracle(out_to_numpy(y)[:, rows], ref, od)
 
 
 @pytest.mark.parametrize("T", [9, 16, 40])
@@ -216,7 +239,7 @@ def test_few_rows_many_factor_rows():
     assert_oracle(out_to_numpy(y), ref)
 
 
-@pytest.mark.parametrize("bits,G", [(4, 128), (2, 64)])
+@pytest.mark.parametrize("bits,G", [(4, 128), (2, 64), (3, 128)])
 def test_wide_input_uses_eight_k_slices(bits, G):
     """d_in = 20480 (4-bit: 640 chunks of 32 codes) splits K over 8 waves."""
     d_out, d_in = 300, 20480
@@ -286,6 +309,8 @@ def _glu_ref_rows(host, ranks, bits, G, d_in, X, rows):
     (16, torch.float16, torch.float32, 4, 128, 14336, 4096),    # Llama-8B gate/up, MFMA with 4 tiles per wave
     (64, torch.bfloat16, torch.float16, 4, 128, 1000, 2048),    # the most tokens: four MFMA passes
     (4, torch.float16, torch.bfloat16, 2, 64, 1000, 4096),      # 2-bit, one pass of 4 tokens
+    (1, torch.float16, torch.bfloat16, 3, 128, 1000, 2048),     # 3-bit, one token
+    (6, torch.bfloat16, torch.float16, 3, 32, 700, 1024),       # 3-bit, passes of 4 and 2 tokens
 ])
 def test_glu_matches_oracle(T, act, out, bits, G, d_out, d_in):
     """cl_linear_decode_glu = SiLU(gate x) * (up x) of the fp64 oracle (gate
@@ -333,7 +358,7 @@ def test_glu_without_factors():
 
 
 @pytest.mark.parametrize("T", [1, 3, 16])
-@pytest.mark.parametrize("bits,G", [(4, 128), (4, 64), (4, 32), (2, 64)])
+@pytest.mark.parametrize("bits,G", [(4, 128), (4, 64), (4, 32), (2, 64), (3, 128)])
 @pytest.mark.parametrize("std", [5e-4, 1e-4])
 def test_small_weight_scales(T, bits, G, std):
     """Weights N(0, std^2) with std 5e-4 and 1e-4 put the group scales at

@@ -35,7 +35,7 @@ def _adversarial(bits, G, rows):
     return W.astype(np.float32)
 
 
-@pytest.mark.parametrize("bits,G", [(4, 128), (2, 64), (4, 32), (2, 128)])
+@pytest.mark.parametrize("bits,G", [(4, 128), (2, 64), (4, 32), (2, 128), (3, 128), (3, 32)])
 def test_quantize_pack_bit_exact(bits, G):
     rows = 37                                       # ragged: not a multiple of anything
     W = np.concatenate([_adversarial(bits, G, 8),
@@ -61,10 +61,24 @@ def test_quantize_pack_llama_gate_rows_bit_exact():
     np.testing.assert_array_equal(host_u16(w.zeros)[rows], z.view(np.uint16))
 
 
-@pytest.mark.parametrize("bits,G", [(4, 128), (2, 64)])
+@pytest.mark.parametrize("bits,G", [(4, 128), (2, 64), (3, 128), (3, 32)])
 def test_dequantize_exact(bits, G):
     W = wl.weight((50, 512), 0, 3, bits)
     Q, s, z = quant.quantize_pack(W, bits, G)
     w = cl.QWeight(dev_u32(Q), dev_f16(s), dev_f16(z), 50, 512, bits, G)
     got = cl.dequantize(w).cpu().numpy().astype(np.float64)
     np.testing.assert_array_equal(got, quant.dequant_packed(Q, s, z, bits, G, 512))
+
+
+def test_quantize_pack_3bit_llama_rows_bit_exact():
+    """3-bit codes (32 in 3 words, two of them straddling words) of a full
+    14336 x 4096 matrix quantized on the GPU, sampled rows bit-exact."""
+    W = wl.weight((14336, 4096), 7, 0, 4)
+    w = cl.quantize_pack(torch.from_numpy(W).cuda(), 3, 128)
+    torch.cuda.synchronize()
+    assert tuple(w.q.shape) == (14336, 384)
+    rows = np.r_[0:2, np.random.default_rng(3).choice(14336, 40, replace=False), 14334:14336]
+    Q, s, z = quant.quantize_pack(W[rows], 3, 128)
+    np.testing.assert_array_equal(host_u32(w.q)[rows], Q)
+    np.testing.assert_array_equal(host_u16(w.scales)[rows], s.view(np.uint16))
+    np.testing.assert_array_equal(host_u16(w.zeros)[rows], z.view(np.uint16))
