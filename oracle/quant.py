@@ -84,6 +84,9 @@ def quantize(W, bits, group_size):
     return codes, s16.astype(np.float16), z.astype(np.float16)
 
 
+ROW_BLOCK = 256   # rows per step of pack/unpack (bounds the bit-string temporaries)
+
+
 def pack(codes, bits):
     """Pack integer codes ``[d_out][d_in]`` LSB-first into uint32 words: the
     row's codes are written out as a bit string (code ``c`` at bits
@@ -96,21 +99,38 @@ def pack(codes, bits):
         raise ValueError("d_in * bits must be a multiple of 32")
     if codes.min(initial=0) < 0 or codes.max(initial=0) >= (1 << bits):
         raise ValueError("codes out of range")
-    # bit j of code c is bit bits * c + j of the row
-    bitstr = ((codes[:, :, None] >> np.arange(bits)) & 1).reshape(d_out, d_in * bits)
-    # bit i of the row is bit i % 32 of word i // 32
-    w = bitstr.reshape(d_out, d_in * bits // 32, 32).astype(np.uint64)
-    words = (w << np.arange(32, dtype=np.uint64)).sum(axis=2, dtype=np.uint64)
-    return words.astype(np.uint32)
+    out = np.empty((d_out, d_in * bits // 32), dtype=np.uint32)
+    for r0 in range(0, d_out, ROW_BLOCK):
+        c = codes[r0:r0 + ROW_BLOCK]
+        n = c.shape[0]
+        # bit j of code c is bit bits * c + j of the row
+        bitstr = ((c[:, :, None] >> np.arange(bits)) & 1).reshape(n, d_in * bits)
+        # bit i of the row is bit i % 32 of word i // 32
+        w = bitstr.reshape(n, d_in * bits // 32, 32).astype(np.uint64)
+        out[r0:r0 + n] = (w << np.arange(32, dtype=np.uint64)).sum(axis=2, dtype=np.uint64).astype(np.uint32)
+    return out
 
 
 def unpack(Q, bits, d_in):
-    """Inverse of :func:`pack`: uint32 ``[d_out][d_in*bits/32]`` -> int64 codes."""
+    """Inverse of :func:`pack`: uint32 ``[d_out][d_in*bits/32]`` -> int64
+    codes.  Code ``c`` starts at bit ``p = bits * c`` of the row: read the
+    64-bit value of words ``p // 32`` (low) and ``p // 32 + 1`` (high),
+    shift it right by ``p % 32`` and keep ``bits`` bits (a code of at most
+    32 bits never spans more than those two words)."""
     Q = np.asarray(Q, dtype=np.uint32)
-    d_out = Q.shape[0]
-    bitstr = ((Q[:, :, None].astype(np.int64) >> np.arange(32)) & 1).reshape(d_out, -1)[:, :d_in * bits]
-    b = bitstr.reshape(d_out, d_in, bits)
-    return (b << np.arange(bits)).sum(axis=2).astype(np.int64)
+    d_out, nw = Q.shape
+    p = bits * np.arange(d_in)
+    w0 = p // 32
+    w1 = np.minimum(w0 + 1, nw - 1)
+    has_hi = (w0 + 1 < nw).astype(np.uint64)
+    shift = (p % 32).astype(np.uint64)
+    mask = np.uint64((1 << bits) - 1)
+    out = np.empty((d_out, d_in), dtype=np.int64)
+    for r0 in range(0, d_out, ROW_BLOCK):
+        q = Q[r0:r0 + ROW_BLOCK].astype(np.uint64)
+        v = (q[:, w0] | ((q[:, w1] * has_hi) << np.uint64(32))) >> shift
+        out[r0:r0 + ROW_BLOCK] = (v & mask).astype(np.int64)
+    return out
 
 
 def dequant(codes, scales, zeros, group_size):
