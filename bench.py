@@ -78,7 +78,8 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-extras", action="store_true")
     p.add_argument("--copy-calibration", action="store_true")
-    p.add_argument("--only", choices=("decode", "tokens", "glu", "layer2bit", "layer3bit", "prefill", "moe"),
+    p.add_argument("--only", choices=("decode", "single", "tokens", "glu", "layer2bit", "layer3bit", "prefill",
+                                       "moe", "cpu"),
                    default=None,
                    help="run one workload and print its own JSON line (for profiling)")
     return p.parse_args()
@@ -264,6 +265,34 @@ def bench_layer2bit(torch, cl, wl, timer, dev, rotate_gib):
             "ranks": "/".join(str(s.rank) for s in layer2.linears), "gate_rank_sweep": sweep}
 
 
+def bench_single(torch, cl, wl, timer, dev, rotate_gib):
+    """The 1024 x 1024 linear (4-bit g128, rank 16, one token): us per call
+    over enough copies to exceed the Infinity Cache, one graph of every
+    copy's call replayed."""
+    spec = wl.single_linear().linears[0]
+    W = torch.from_numpy(wl.weight((spec.d_out, spec.d_in), 0)).to(dev)
+    w = cl.quantize_pack(W, spec.bits, spec.group_size)
+    A, B = wl.standin_factors(spec.d_out, spec.d_in, spec.r_max, 0)
+    c = cl.LowRank(torch.from_numpy(A).to(dev), torch.from_numpy(B).to(dev), spec.r_max, spec.rank)
+    per = w.q.numel() * 4 + w.scales.numel() * 4 + c.A.numel() * 2 + c.B.numel() * 2
+    n = max(2, int(np.ceil(rotate_gib * 2 ** 30 / per)))
+    copies = [(w, c)] + [(cl.QWeight(w.q.clone(), w.scales.clone(), w.zeros.clone(), w.d_out, w.d_in, w.bits,
+                                      w.group_size), cl.LowRank(c.A.clone(), c.B.clone(), c.r_max, c.rank))
+                         for _ in range(n - 1)]
+    x = torch.from_numpy(wl.activation((1, spec.d_in), 0).bits.view(np.int16)).view(torch.float16).to(dev)
+    y = torch.empty((1, spec.d_out), dtype=torch.float16, device=dev)
+    ws = cl.workspace(cl.linear_workspace(w, c, 1), dev)
+
+    def run():
+        for wk, ck in copies:
+            cl.linear_decode(wk, ck, x, y=y, ws=ws, stream=timer.stream)
+    g = timer.capture(run)
+    us = timer.time([g], 5) * 1e3 / n
+    nbytes = algorithmic_bytes(spec, 1)
+    return {"us_per_call": round(us, 3), "gbs": round(nbytes / us / 1e3, 1), "bytes_per_call": nbytes,
+            "copies": n}
+
+
 def bench_layer3bit(torch, cl, wl, timer, dev, rotate_gib):
     """The 3-bit group-128 layer (the paper's INT3 dense setting; ranks
     from {0, 16, 32, 64, 128} under 64 x 7) at one and four tokens, on the
@@ -395,6 +424,10 @@ def main():
               "multi-GPU sharding is described in DESIGN.md and not run.", file=sys.stderr)
         sys.exit(2)
 
+    if args.only == "cpu":                          # the oracle baselines alone (no GPU)
+        print(json.dumps({"cpu_oracle": cpu_oracle_workloads()}))
+        return
+
     import torch
     from paper_2605_05819_amd import cl, workloads as wl
 
@@ -418,6 +451,10 @@ def main():
     if only == "layer3bit":
         print(json.dumps({"layer_3bit_g128": bench_layer3bit(torch, cl, wl, timer, dev, args.rotate_gib)}))
         return
+    if only == "single":
+        print(json.dumps({"single_1024x1024_r16": bench_single(torch, cl, wl, timer, dev, args.rotate_gib)}))
+        return
+
     copies = device_layer(torch, cl, wl, layer, dev, args.rotate_gib)
     ncopies = len(copies)
     if only == "tokens":
@@ -441,7 +478,8 @@ def main():
 
     extras = None
     if only is None and not args.no_extras:
-        extras = bench_tokens(torch, cl, wl, timer, copies, layer, dev)
+        extras = {"single_1024x1024_r16": bench_single(torch, cl, wl, timer, dev, args.rotate_gib)}
+        extras.update(bench_tokens(torch, cl, wl, timer, copies, layer, dev))
         extras["gate_up_window_vs_glu"] = bench_glu(torch, cl, wl, timer, copies, layer, dev)
         del copies
         torch.cuda.empty_cache()
@@ -453,6 +491,8 @@ def main():
         extras["moe_48_layers"] = bench_moe(torch, cl, wl, timer, dev)
 
     cpu = None if (args.no_cpu_baseline or only) else cpu_baseline(layer, T)
+    if extras is not None and not args.no_cpu_baseline:
+        extras["cpu_oracle"] = cpu_oracle_workloads()
 
     out = {
         "metric": "achieved HBM GB/s + us/call, compensated W4A16 decode linear; prefill TFLOP/s",
@@ -512,14 +552,103 @@ def cpu_baseline(layer, T):
         run()
         times.append(time.perf_counter() - t0)
     sec = float(np.median(times))
+    threads, ncpu = host_threads()
+    return {"value": round(nbytes / sec / 1e9, 4), "unit": "GB/s", "cores": threads, "kind": "oracle",
+            "cpu_count": ncpu,
+            "sample": "whole layer (7 matrices, all rows, %d bytes), T=%d, median of 3 runs of %.2f s; "
+                      "numpy elementwise steps on one thread, BLAS products on %d threads of %d host CPUs"
+                      % (nbytes, T, sec, threads, ncpu)}
+
+
+def host_threads():
+    """(BLAS threads the oracle's matrix products use, os.cpu_count())."""
     try:
         import threadpoolctl
         threads = max(i.get("num_threads", 1) for i in threadpoolctl.threadpool_info()) or 1
     except Exception:
         threads = os.cpu_count()
-    return {"value": round(nbytes / sec / 1e9, 4), "unit": "GB/s", "cores": threads, "kind": "oracle",
-            "sample": "whole layer (7 matrices, all rows, %d bytes), T=%d, median of 3 runs of %.2f s"
-                      % (nbytes, T, sec)}
+    return threads, os.cpu_count()
+
+
+def _median_time(fn, reps, warm=True):
+    if warm:
+        fn()
+    ts = []
+    for _ in range(reps):
+        t0 = time.perf_counter()
+        fn()
+        ts.append(time.perf_counter() - t0)
+    return float(np.median(ts))
+
+
+def cpu_oracle_workloads():
+    """The fp64 oracle (unpack + dequantize + forward, as it stands) timed on
+    bounded samples of the other workloads, in each workload's unit: the
+    1024 x 1024 linear (median of 5), the 2-bit gate rank sweep (one run per
+    rank, one warm-up run before the first), prefill on a 256-token sample of
+    the 2048 tokens (TFLOP/s; the cost is linear in tokens) and the
+    128-expert MoE gate and down at 1 and 8 tokens (routed bytes / time; one
+    warm-up run at 1 token)."""
+    from oracle import linear, moe, quant
+    from paper_2605_05819_amd import workloads as wl
+    threads, ncpu = host_threads()
+    out = {"cores": threads, "cpu_count": ncpu}
+    # 1024 x 1024, rank 16, one token
+    spec = wl.single_linear().linears[0]
+    W = wl.weight((spec.d_out, spec.d_in), 0)
+    Q, s, z = quant.quantize_pack(W, 4, 128)
+    A, B = wl.standin_factors(spec.d_out, spec.d_in, spec.r_max, 0)
+    x = wl.activation((1, spec.d_in), 0).values
+    sec = _median_time(lambda: linear.forward_packed(Q, s, z, 4, 128, A, B, spec.rank, x), 5)
+    out["single_1024x1024_r16"] = {"us_per_call": round(sec * 1e6, 1),
+                                   "gbs": round(algorithmic_bytes(spec, 1) / sec / 1e9, 4)}
+    # 2-bit gate, rank sweep
+    layer2 = wl.llama_layer_2bit()
+    g2 = [l.name for l in layer2.linears].index("gate")
+    sp2 = layer2.linears[g2]
+    W = wl.weight((sp2.d_out, sp2.d_in), layer2.index, 0, g2)
+    Q, s, z = quant.quantize_pack(W, 2, 64)
+    A, B = wl.standin_factors(sp2.d_out, sp2.d_in, 256, layer2.index, 0, g2)
+    x = wl.activation((1, sp2.d_in), layer2.index, 0, g2).values
+    sweep = {}
+    for r in (0, 32, 128, 256):
+        sec = _median_time(lambda: linear.forward_packed(Q, s, z, 2, 64, A, B, r, x), 1, warm=r == 0)
+        sweep["r%d" % r] = {"s": round(sec, 3), "gbs": round(algorithmic_bytes(sp2, 1, r) / sec / 1e9, 4)}
+    out["gate_2bit_rank_sweep"] = sweep
+    # prefill, 256 of the 2048 tokens, rank 64
+    Ms, r = 256, 64
+    pf = {}
+    for (N, K) in ((4096, 4096), (14336, 4096)):
+        W = wl.weight((N, K), 3, 0, N)
+        Q, s, z = quant.quantize_pack(W, 4, 128)
+        A, B = wl.standin_factors(N, K, r, 3, 0, N)
+        X = wl.activation((Ms, K), 3, 0, N).values
+        sec = _median_time(lambda: linear.forward_packed(Q, s, z, 4, 128, A, B, r, X), 1)
+        flops = 2.0 * Ms * N * K + 2.0 * Ms * r * (K + N)
+        pf["%dx%d" % (N, K)] = {"s": round(sec, 3), "tflops": round(flops / sec / 1e12, 5)}
+    out["prefill_sample_M256_r64"] = pf
+    # MoE: 128 stand-in experts of gate (shared input) and down (per-slot input)
+    E, k = wl.MOE_EXPERTS, wl.MOE_TOPK
+    mo = {}
+    for name, m in (("gate", 0), ("down", 2)):
+        d_out, d_in = wl.MOE_SHAPES[name]
+        Qe, se, ze = wl.standin_codes(E, d_out, d_in, 4, 128, 5, 0, m)
+        ranks = wl.moe_expert_ranks(5, 0, m)
+        packed = []
+        for e in range(E):
+            Ae, Be = wl.standin_factors(d_out, d_in, 32, 5, 0, m, e)
+            packed.append((Qe[e], se[e], ze[e], Ae, Be))
+        rows = np.arange(d_out)
+        for T in (1, 8):
+            ids, _ = wl.routing(T, 5, 0)
+            X = wl.activation((T, k, d_in) if name == "down" else (T, d_in), 5, 0, m).values
+            sec = _median_time(lambda: moe.forward_rows(packed, ranks, X, ids, name == "down", rows, 4, 128), 1,
+                               warm=T == 1)
+            nbytes = sum(d_out * d_in // 2 + 4 * d_out * (d_in // 128) + 2 * int(ranks[e]) * (d_in + d_out)
+                         for e in np.unique(ids)) + 2 * X.size + 2 * T * k * d_out
+            mo["%s_T%d" % (name, T)] = {"s": round(sec, 3), "gbs": round(nbytes / sec / 1e9, 4)}
+    out["moe_layer_sample"] = mo
+    return out
 
 
 if __name__ == "__main__":
