@@ -600,17 +600,21 @@ __global__ __launch_bounds__(1024) void decode_prep_mfma_kernel(PrepMArgs a) {
     }
     // activations: item (pass, word wi, token lane r) -> 16 bytes, the 8
     // activations of codes 8 wi .. 8 wi + 7 of token 16 pass + r in the
-    // unpack's pair order (x0, x4), (x1, x5), (x2, x6), (x3, x7); absent
-    // tokens are zero
+    // unpack's pair order (x0, x4), (x1, x5), (x2, x6), (x3, x7); a pass of
+    // tp <= 16 tokens stores its words tp entries apart (word wi of token r at
+    // wi tp + r), so fewer tokens are fewer bytes for the backbone to read
     const int wpr = d_in / CPW;
     const int npass = (T + 15) / 16;
     const long long item = static_cast<long long>(blk - ntile) * blockDim.x + tid;
     if (item >= static_cast<long long>(npass) * wpr * 16) return;
     const int rt = static_cast<int>(item & 15);
     const int wi = static_cast<int>((item >> 4) % wpr);
-    const int tok = static_cast<int>(item / (16ll * wpr)) * 16 + rt;
+    const int pass = static_cast<int>(item / (16ll * wpr));
+    const int tp = min(16, T - 16 * pass);
+    if (rt >= tp) return;
+    const int tok = pass * 16 + rt;
     u32x4 o = {0u, 0u, 0u, 0u};
-    if (tok < T) {
+    {
         const u32x4 u = act8_to_f16(*reinterpret_cast<const u32x4*>(a.x + static_cast<size_t>(tok) * d_in + 8 * wi),
                                  a.act);
         // u[i] holds (x[2i], x[2i + 1]); pair p needs (x[p], x[p + 4])
@@ -622,7 +626,7 @@ __global__ __launch_bounds__(1024) void decode_prep_mfma_kernel(PrepMArgs a) {
             o[pp] = av | bv;
         }
     }
-    a.xf[item] = o;
+    a.xf[static_cast<size_t>(pass) * wpr * 16 + static_cast<size_t>(wi) * tp + rt] = o;
     (void)PPC;
 }
 
@@ -687,32 +691,30 @@ __global__ __launch_bounds__(GLU ? 512 : 256) void decode_mfma_kernel(DecodeArgs
     const uint32_t mlo = __builtin_amdgcn_readfirstlane(0x000F000Fu);
     const uint32_t mhi = __builtin_amdgcn_readfirstlane(0x00F000F0u);
     const uint32_t bias = 0x64006400u;
-    // this pass's activations; absent tokens were written as zero
-    const u32x4* xf = a.xf + static_cast<size_t>(a.tok0 / 16) * words_row * 16 + r;
-    // the workgroup's scales and zeros into LDS (rows are consecutive, so
-    // each array's part is one contiguous run): whole 16-byte pieces, then
-    // the last few values one by one; rows past the matrix are not loaded
-    // and never used
-    {
-        const int nrows = min(16 * TPW, L.d_out - row0);
-        const int nval = nrows * groups;
-        const uint16_t* ssrc = L.s + static_cast<size_t>(row0) * groups;
-        const uint16_t* zsrc = L.z + static_cast<size_t>(row0) * groups;
-        // 16-byte pieces only where both runs start 16-byte aligned (the
-        // caller's arrays need only 2-byte alignment)
-        const bool al = ((reinterpret_cast<uintptr_t>(ssrc) | reinterpret_cast<uintptr_t>(zsrc)) & 15) == 0;
-        const int n16 = al ? nval / 8 : 0;
-        uint16_t* zl = szl + 16 * TPW * groups;
-        for (int i = tid; i < n16; i += 256) {
-            reinterpret_cast<u32x4*>(szl)[i] = reinterpret_cast<const u32x4*>(ssrc)[i];
-            reinterpret_cast<u32x4*>(zl)[i] = reinterpret_cast<const u32x4*>(zsrc)[i];
-        }
-        for (int i = 8 * n16 + tid; i < nval; i += 256) {
-            szl[i] = ssrc[i];
-            zl[i] = zsrc[i];
-        }
-        __syncthreads();
-    }
+    // this pass's activations, tp tokens per word: lane row r reads token
+    // min(r, tp - 1) (rows past the pass's tokens repeat the last one; their
+    // output rows are never stored)
+    const int tp = min(16, a.T - a.tok0);
+    const u32x4* xf = a.xf + static_cast<size_t>(a.tok0 / 16) * words_row * 16 + (r < tp ? r : tp - 1);
+    // the workgroup's scales and zeros go to LDS (rows are consecutive, so
+    // each array's part is one contiguous run; rows past the matrix are not
+    // loaded and never used).  Vector loads complete in issue order, so the
+    // first 16-byte piece of each array is loaded here, before the K loop's
+    // first code blocks, and stored to LDS after those are issued: the copy
+    // waits for the scales and zeros only.
+    const int nval = min(16 * TPW, L.d_out - row0) * groups;
+    const uint16_t* ssrc = L.s + static_cast<size_t>(row0) * groups;
+    const uint16_t* zsrc = L.z + static_cast<size_t>(row0) * groups;
+    // 16-byte pieces only where both runs start 16-byte aligned (the caller's
+    // arrays need only 2-byte alignment)
+    const bool al = ((reinterpret_cast<uintptr_t>(ssrc) | reinterpret_cast<uintptr_t>(zsrc)) & 15) == 0;
+    const int n16 = al ? nval / 8 : 0;
+    uint16_t* const zl = szl + 16 * TPW * groups;
+    const u32x4* s16p = n16 ? reinterpret_cast<const u32x4*>(ssrc) + min(tid, n16 - 1)
+                            : reinterpret_cast<const u32x4*>(a.xf);
+    const u32x4* z16p = n16 ? reinterpret_cast<const u32x4*>(zsrc) + min(tid, n16 - 1)
+                            : reinterpret_cast<const u32x4*>(a.xf);
+    const u32x4 s_first = *s16p, z_first = *z16p;
 
     struct Blk {
         u32x4 w[TPW];
@@ -810,7 +812,7 @@ __global__ __launch_bounds__(GLU ? 512 : 256) void decode_mfma_kernel(DecodeArgs
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
             const int xw = GPB == 1 ? wi + t : (kb * 128 + 32 * t < K ? kb * 16 + 4 * t + g : g);
-            b.x[t] = xf[static_cast<size_t>(xw) * 16];
+            b.x[t] = xf[static_cast<size_t>(xw) * tp];
         }
     };
     auto compute = [&](int kb, const Blk& b) {
@@ -849,6 +851,20 @@ __global__ __launch_bounds__(GLU ? 512 : 256) void decode_mfma_kernel(DecodeArgs
     Blk b[NBUF];
 #pragma unroll
     for (int j = 0; j < NBUF; ++j) load(wave + 4 * j < nkb ? wave + 4 * j : 0, b[j]);
+    // the scales and zeros into LDS (the code loads stay in flight)
+    if (tid < n16) {
+        reinterpret_cast<u32x4*>(szl)[tid] = s_first;
+        reinterpret_cast<u32x4*>(zl)[tid] = z_first;
+    }
+    for (int i = tid + 256; i < n16; i += 256) {           // rows of more than 32 groups
+        reinterpret_cast<u32x4*>(szl)[i] = reinterpret_cast<const u32x4*>(ssrc)[i];
+        reinterpret_cast<u32x4*>(zl)[i] = reinterpret_cast<const u32x4*>(zsrc)[i];
+    }
+    for (int i = 8 * n16 + tid; i < nval; i += 256) {      // misaligned runs, the last few values
+        szl[i] = ssrc[i];
+        zl[i] = zsrc[i];
+    }
+    __syncthreads();
     for (int rd = 0; rd < rounds; ++rd) {
 #pragma unroll
         for (int j = 0; j < NBUF; ++j) {

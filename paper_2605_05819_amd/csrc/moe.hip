@@ -59,11 +59,13 @@ constexpr int kMaxExperts = 1024;
 constexpr int kTab = 8;              // ints per active-expert table entry
 constexpr int kMaxMoeWin = 4;        // linears per window
 // MFMA path: 16-row tiles per workgroup and K blocks in flight per wave.
-// Measured on the 48-layer T = 64 step: 4 x 2 199.6 us, 8 x 1 202.4, 2 x 2
-// 208.4, 4 x 4 287.1, 2 x 4 331.9 (one tile of 16 rows: 389, every
-// workgroup re-reading its slots' activations).
-constexpr int kMoeTpw = 4;
-constexpr int kMoeNbuf = 2;
+// Measured on the 48-layer T = 64 step with the workgroup's loads issued in
+// need order (scales and zeros, slot ids, code blocks): 8 x 1 166 us per
+// layer, 4 x 2 191, 8 x 2 229, 12 x 1 230, 16 x 1 227 (with the code loads
+// issued after the scale/zero copy: 4 x 2 213 us; one tile of 16 rows had
+// taken 389, every workgroup re-reading its slots' activations).
+constexpr int kMoeTpw = 8;
+constexpr int kMoeNbuf = 1;
 
 // One linear of a window: its stacked experts and its share of the grids.
 struct MoeLin {
@@ -131,16 +133,28 @@ __global__ __launch_bounds__(256) void moe_prep_kernel(MoeArgs a) {
         // slots per expert (LDS atomics contend only within one expert)
         // the ranks are loaded together with the ids: the selected expert's
         // rank then costs no further memory round trip
-        for (int i = tid; i < a.E; i += 256) {
-            hist[i] = 0;
-            rk[i] = L.r_max > 0 ? L.ranks[i] : 0;     // ranks may be null when r_max is 0
-        }
+        // the ranks and the routing ids are loaded in one round trip (their
+        // loads are issued before either is stored); the histogram is
+        // cleared meanwhile
+        for (int i = tid; i < a.E; i += 256) hist[i] = 0;
         if (tid == 0) sel = -1;
+        constexpr int kPer = kMaxExperts / 256;       // experts and slots per thread, at most
+        int rkv[kPer], idv[kPer];
+#pragma unroll
+        for (int u = 0; u < kPer; ++u) {
+            const int i = tid + 256 * u;
+            rkv[u] = (L.r_max > 0 && i < a.E) ? L.ranks[i] : 0;   // ranks may be null when r_max is 0
+            idv[u] = i < S ? a.ids[i] : -1;
+        }
         __syncthreads();
-        for (int sl = tid; sl < S; sl += 256) {
-            const int id = a.ids[sl];
-            sids[sl] = id;
-            if (id >= 0 && id < a.E) atomicAdd(&hist[id], 1);
+#pragma unroll
+        for (int u = 0; u < kPer; ++u) {
+            const int i = tid + 256 * u;
+            if (i < a.E) rk[i] = rkv[u];
+            if (i < S) {
+                sids[i] = idv[u];
+                if (idv[u] >= 0 && idv[u] < a.E) atomicAdd(&hist[idv[u]], 1);
+            }
         }
         __syncthreads();
         // block scan over the experts (thread t owns experts 4 t .. 4 t + 3):
@@ -583,6 +597,7 @@ __global__ __launch_bounds__(256) void moe_mfma_kernel(MoeArgs a) {
     if (ae >= n_active) return;                   // whole workgroup: no routed expert here
     const int row0 = (local - ae * L.bpe) * 16 * TPW;
     const int lane = threadIdx.x & 63;
+    const int tid = threadIdx.x;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int g = lane >> 4, r = lane & 15;
     int row[TPW];
@@ -599,75 +614,151 @@ __global__ __launch_bounds__(256) void moe_mfma_kernel(MoeArgs a) {
     const uint32_t* qe = L.q + static_cast<size_t>(e) * L.q_stride;
     const uint16_t* se = L.s + static_cast<size_t>(e) * L.sz_stride;
     const uint16_t* ze = L.z + static_cast<size_t>(e) * L.sz_stride;
+    const uint16_t* Be = L.B + static_cast<size_t>(e) * L.b_stride;
     const uint32_t mlo = __builtin_amdgcn_readfirstlane(0x000F000Fu);
     const uint32_t mhi = __builtin_amdgcn_readfirstlane(0x00F000F0u);
     const uint32_t bias = 0x64006400u;
-    // the rows' scales and zeros into LDS (one contiguous run per array;
-    // rows past the matrix are not loaded and never used)
-    {
-        const int nval = min(16 * TPW, L.d_out - row0) * groups;
-        const uint16_t* ssrc = se + static_cast<size_t>(row0) * groups;
-        const uint16_t* zsrc = ze + static_cast<size_t>(row0) * groups;
-        uint16_t* zl = szl + 16 * TPW * groups;
-        const bool al = ((reinterpret_cast<uintptr_t>(ssrc) | reinterpret_cast<uintptr_t>(zsrc)) & 15) == 0;
-        const int n16 = al ? nval / 8 : 0;
-        for (int i = threadIdx.x; i < n16; i += 256) {
-            reinterpret_cast<u32x4*>(szl)[i] = reinterpret_cast<const u32x4*>(ssrc)[i];
-            reinterpret_cast<u32x4*>(zl)[i] = reinterpret_cast<const u32x4*>(zsrc)[i];
-        }
-        for (int i = 8 * n16 + static_cast<int>(threadIdx.x); i < nval; i += 256) {
-            szl[i] = ssrc[i];
-            zl[i] = zsrc[i];
-        }
-        __syncthreads();
-    }
+    const u32x4 zero = {0u, 0u, 0u, 0u};
+
     struct Blk {
         u32x4 w[TPW];
         u32x4 x[4];
     };
+    // codes of block kb for this lane's tiles, and the activations of the
+    // words it feeds to MFMA step t: 4 g + t of the block, or 4 t + g once
+    // the codes are transposed (a word past K reads word g, met by a zero
+    // scale).  Loads are unconditional (clamped addresses) and nothing
+    // consumes a loaded value before compute.
+    auto load_w = [&](int kb, Blk& b) {
+        const int wi = min(kb * 16 + 4 * g, words_row - 4);
+#pragma unroll
+        for (int j = 0; j < TPW; ++j)
+            b.w[j] = __builtin_nontemporal_load(
+                reinterpret_cast<const u32x4*>(qe + static_cast<size_t>(row[j]) * words_row + wi));
+    };
+    auto load_x = [&](int kb, Blk& b, const u32x4* xr) {
+        const int wi = min(kb * 16 + 4 * g, words_row - 4);
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+            b.x[t] = xr[GPB == 1 ? wi + t : (kb * 128 + 32 * t < K ? kb * 16 + 4 * t + g : g)];
+    };
+    // rank-term operands of the step at factor column kr: this lane's slot's
+    // t (8 floats, zero past its rank) and the tiles' B entries
+    struct RankOp {
+        float t[8];
+        uint32_t bw[TPW][4];
+    };
+    // 16-byte loads when every row of t and B starts 16-byte aligned (r_max a
+    // multiple of 8: t rows of r_max floats in the 256-byte aligned
+    // workspace, B rows of r_max halves); a step past r_max reads column 0
+    const bool rvec = (L.r_max & 7) == 0 && (reinterpret_cast<uintptr_t>(L.B) & 15) == 0;
+    auto rank_load = [&](int kr, int sl, RankOp& o) {
+        const int k = kr + 8 * g;
+        const float* trow = L.t + static_cast<size_t>(sl) * L.r_max;
+        if (rvec) {
+            const int kk = k + 8 <= L.r_max ? k : 0;
+            const f32x4 t0 = *reinterpret_cast<const f32x4*>(trow + kk);
+            const f32x4 t1 = *reinterpret_cast<const f32x4*>(trow + kk + 4);
+#pragma unroll
+            for (int q = 0; q < 4; ++q) { o.t[q] = t0[q]; o.t[4 + q] = t1[q]; }
+#pragma unroll
+            for (int j = 0; j < TPW; ++j) {
+                const u32x4 v = *reinterpret_cast<const u32x4*>(Be + static_cast<size_t>(row[j]) * L.r_max + kk);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) { const uint32_t vq = v[q]; o.bw[j][q] = vq; }
+            }
+            return;
+        }
+#pragma unroll
+        for (int q = 0; q < 8; ++q) o.t[q] = trow[k + q < L.r_max ? k + q : 0];
+#pragma unroll
+        for (int j = 0; j < TPW; ++j) {
+            const uint16_t* brow = Be + static_cast<size_t>(row[j]) * L.r_max;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int k0 = k + 2 * q, k1 = k0 + 1;
+                const uint32_t lo = brow[k0 < L.r_max ? k0 : 0];
+                const uint32_t hi = brow[k1 < L.r_max ? k1 : 0];
+                o.bw[j][q] = lo | (hi << 16);
+            }
+        }
+    };
+
+    // What is needed first is issued first (vector loads complete in issue
+    // order): the scales and zeros of the workgroup's rows, then this lane's
+    // slot of the first pass, then the first round of code blocks; the LDS
+    // copy of the scales and zeros then waits only for them, and the code
+    // loads stay in flight across the barrier.  (Issued after the copy, the
+    // code loads had one more dependent round trip per workgroup.)
+    const int nval = min(16 * TPW, L.d_out - row0) * groups;
+    const uint16_t* ssrc = se + static_cast<size_t>(row0) * groups;
+    const uint16_t* zsrc = ze + static_cast<size_t>(row0) * groups;
+    uint16_t* zl = szl + 16 * TPW * groups;
+    const bool al = ((reinterpret_cast<uintptr_t>(ssrc) | reinterpret_cast<uintptr_t>(zsrc)) & 15) == 0;
+    const int n16 = al ? nval / 8 : 0;
+    // first 16-byte piece of each array per thread (a valid aligned address
+    // when this thread has none)
+    const u32x4* s16p = n16 ? reinterpret_cast<const u32x4*>(ssrc) + min(tid, n16 - 1)
+                            : reinterpret_cast<const u32x4*>(a.table);
+    const u32x4* z16p = n16 ? reinterpret_cast<const u32x4*>(zsrc) + min(tid, n16 - 1)
+                            : reinterpret_cast<const u32x4*>(a.table);
+    const u32x4 s_first = *s16p, z_first = *z16p;
+    int sl = a.sorted[sbeg + (r < scnt ? r : 0)];
+    constexpr int SPAN = 4 * NBUF;
+    const int rounds = (nkb + SPAN - 1) / SPAN;
+    Blk b[NBUF];
+#pragma unroll
+    for (int j = 0; j < NBUF; ++j) load_w(wave + 4 * j < nkb ? wave + 4 * j : 0, b[j]);
+    if (tid < n16) {
+        reinterpret_cast<u32x4*>(szl)[tid] = s_first;
+        reinterpret_cast<u32x4*>(zl)[tid] = z_first;
+    }
+    for (int i = tid + 256; i < n16; i += 256) {           // rows with more than 32 groups
+        reinterpret_cast<u32x4*>(szl)[i] = reinterpret_cast<const u32x4*>(ssrc)[i];
+        reinterpret_cast<u32x4*>(zl)[i] = reinterpret_cast<const u32x4*>(zsrc)[i];
+    }
+    for (int i = 8 * n16 + tid; i < nval; i += 256) {      // misaligned runs, the last few values
+        szl[i] = ssrc[i];
+        zl[i] = zsrc[i];
+    }
+    __syncthreads();
+
     for (int p0 = 0; p0 < scnt; p0 += 16) {
-        // this lane's slot (MFMA column r) of the pass; absent slots read a
-        // present one and are masked to zero
+        if (p0 > 0) {
+            // a later pass of 16 slots: its slots and its first code round
+            sl = a.sorted[sbeg + (p0 + r < scnt ? p0 + r : 0)];
+#pragma unroll
+            for (int j = 0; j < NBUF; ++j) load_w(wave + 4 * j < nkb ? wave + 4 * j : 0, b[j]);
+        }
+        // this lane's slot (MFMA row r of the activations); absent slots read
+        // a present one and are masked to zero
         const bool sv = p0 + r < scnt;
-        const int sl = a.sorted[sbeg + (sv ? p0 + r : 0)];
         const int xrow = a.x_per_slot ? sl : sl / a.k;
         const u32x4* xr = reinterpret_cast<const u32x4*>(a.xp + static_cast<size_t>(xrow) * (K / 2));
+#pragma unroll
+        for (int j = 0; j < NBUF; ++j) load_x(wave + 4 * j < nkb ? wave + 4 * j : 0, b[j], xr);
         // this lane's slot's rank: its own (per-slot ranks) or the expert's
         int rs = rank;
         if (L.slot_rank) {
             const int v = L.slot_rank[sl];
             rs = v < 0 ? 0 : (v > L.r_max ? L.r_max : v);
         }
-        const u32x4 zero = {0u, 0u, 0u, 0u};
         f32x4 acc[TPW];
 #pragma unroll
         for (int j = 0; j < TPW; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
-        auto load = [&](int kb, Blk& b) {
-            const int wi = min(kb * 16 + 4 * g, words_row - 4);   // first of this lane's 4 words
-#pragma unroll
-            for (int j = 0; j < TPW; ++j)
-                b.w[j] = __builtin_nontemporal_load(
-                    reinterpret_cast<const u32x4*>(qe + static_cast<size_t>(row[j]) * words_row + wi));
-            // activations of the word this lane feeds to MFMA step t: 4 g + t
-            // of the block, or 4 t + g once the codes are transposed (a word
-            // past K reads word g, met by a zero scale)
-#pragma unroll
-            for (int t = 0; t < 4; ++t)
-                b.x[t] = xr[GPB == 1 ? wi + t : (kb * 128 + 32 * t < K ? kb * 16 + 4 * t + g : g)];
-        };
-        auto compute = [&](int kb, const Blk& b) {
+        auto compute = [&](int kb, const Blk& bk) {
             // per group: MFMA steps into a fresh partial of sum (q - z) x,
             // then acc += s * partial in fp32; past K, past the matrix or a
             // padding block the scale is 0
             constexpr int SPG = 4 / GPB;
             u32x4 xv[4];
 #pragma unroll
-            for (int t = 0; t < 4; ++t) xv[t] = sv ? b.x[t] : zero;
+            for (int t = 0; t < 4; ++t) xv[t] = sv ? bk.x[t] : zero;
 #pragma unroll
             for (int j = 0; j < TPW; ++j) {
                 uint32_t w[4];
 #pragma unroll
-                for (int t = 0; t < 4; ++t) { const uint32_t v = b.w[j][t]; w[t] = v; }
+                for (int t = 0; t < 4; ++t) { const uint32_t v = bk.w[j][t]; w[t] = v; }
                 if constexpr (GPB > 1) transpose_words(w);
 #pragma unroll
                 for (int q = 0; q < GPB; ++q) {
@@ -675,55 +766,59 @@ __global__ __launch_bounds__(256) void moe_mfma_kernel(MoeArgs a) {
                     const bool on = kb < nkb && kc < K && rowv[j];
                     const int lr = (16 * j + r) * groups + (on ? kc / a.G : 0);
                     const Zq zq = make_zq(szl[16 * TPW * groups + lr]);
-                    f32x4 p = mfma(xv[SPG * q], codes_minus_zero(w[SPG * q], zq, mlo, mhi, bias),
-                                   f32x4{0.f, 0.f, 0.f, 0.f});
+                    f32x4 pp = mfma(xv[SPG * q], codes_minus_zero(w[SPG * q], zq, mlo, mhi, bias),
+                                    f32x4{0.f, 0.f, 0.f, 0.f});
 #pragma unroll
                     for (int t = SPG * q + 1; t < SPG * q + SPG; ++t)
-                        p = mfma(xv[t], codes_minus_zero(w[t], zq, mlo, mhi, bias), p);
-                    acc[j] = fma4(on ? f16_bits_to_f32(szl[lr]) : 0.f, p, acc[j]);
+                        pp = mfma(xv[t], codes_minus_zero(w[t], zq, mlo, mhi, bias), pp);
+                    acc[j] = fma4(on ? f16_bits_to_f32(szl[lr]) : 0.f, pp, acc[j]);
                 }
             }
         };
-        constexpr int SPAN = 4 * NBUF;
-        const int rounds = (nkb + SPAN - 1) / SPAN;
-        Blk b[NBUF];
-#pragma unroll
-        for (int j = 0; j < NBUF; ++j) load(wave + 4 * j < nkb ? wave + 4 * j : 0, b[j]);
         for (int rd = 0; rd < rounds; ++rd) {
 #pragma unroll
             for (int j = 0; j < NBUF; ++j) {
                 const int kb = wave + SPAN * rd + 4 * j;
                 compute(kb, b[j]);
                 const int kn = kb + SPAN;
-                load(kn < nkb ? kn : (kb < nkb ? kb : 0), b[j]);
+                const int kl = kn < nkb ? kn : (kb < nkb ? kb : 0);
+                load_w(kl, b[j]);
+                load_x(kl, b[j], xr);
             }
         }
         // rank-r term: 32 factor columns per step, wave w taking steps w, w + 4
-        for (int kr = 32 * wave; kr < rank; kr += 128) {
+        // (t as fp16 hi + lo parts, two MFMA steps; entries past the slot's
+        // rank, past the expert's rank or of absent slots and rows are zero)
+        auto rank_mma = [&](int kr, const RankOp& o) {
             const int k = kr + 8 * g;
-            const float* trow = L.t + static_cast<size_t>(sl) * L.r_max;
-            // t as fp16 hi + lo parts, two MFMA steps
             uint32_t tw[4], tlo[4];
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
-                const int k0 = k + 2 * q, k1 = k + 2 * q + 1;
-                split_f16x2((sv && k0 < rs) ? trow[k0] : 0.f, (sv && k1 < rs) ? trow[k1] : 0.f, tw[q], tlo[q]);
+                const int k0 = k + 2 * q, k1 = k0 + 1;
+                split_f16x2((sv && k0 < rs) ? o.t[2 * q] : 0.f, (sv && k1 < rs) ? o.t[2 * q + 1] : 0.f, tw[q],
+                            tlo[q]);
             }
 #pragma unroll
             for (int j = 0; j < TPW; ++j) {
-                const uint16_t* brow = L.B + static_cast<size_t>(e) * L.b_stride + static_cast<size_t>(row[j]) * L.r_max;
                 uint32_t aw[4];
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
-                    const int k0 = k + 2 * q, k1 = k + 2 * q + 1;
-                    const uint32_t lo = (rowv[j] && k0 < rank) ? brow[k0] : 0u;
-                    const uint32_t hi = (rowv[j] && k1 < rank) ? brow[k1] : 0u;
+                    const int k0 = k + 2 * q, k1 = k0 + 1;
+                    const uint32_t lo = (rowv[j] && k0 < rank) ? (o.bw[j][q] & 0xffffu) : 0u;
+                    const uint32_t hi = (rowv[j] && k1 < rank) ? (o.bw[j][q] >> 16) : 0u;
                     aw[q] = lo | (hi << 16);
                 }
                 const u32x4 bop = {aw[0], aw[1], aw[2], aw[3]};
                 acc[j] = mfma(u32x4{tw[0], tw[1], tw[2], tw[3]}, bop, acc[j]);
                 acc[j] = mfma(u32x4{tlo[0], tlo[1], tlo[2], tlo[3]}, bop, acc[j]);
             }
+        };
+        // (prefetching the first step's operands ahead of the K loop kept
+        // them live through it: 256 VGPRs plus 72 AGPRs, one wave per SIMD)
+        for (int kr = 32 * wave; kr < rank; kr += 128) {
+            RankOp o2;
+            rank_load(kr, sl, o2);
+            rank_mma(kr, o2);
         }
 #pragma unroll
         for (int j = 0; j < TPW; ++j) red[wave][j][lane] = acc[j];
@@ -732,14 +827,14 @@ __global__ __launch_bounds__(256) void moe_mfma_kernel(MoeArgs a) {
         // v[e] = y[slot of pass row 4 g + e][row0 + 16 j + r]
         int osl[4];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) osl[e] = __shfl(sl, 4 * g + e, 64);
+        for (int q = 0; q < 4; ++q) osl[q] = __shfl(sl, 4 * g + q, 64);
 #pragma unroll
         for (int j = 0; j < TPW; ++j) {
             if (j % 4 != wave || !rowv[j]) continue;
             const f32x4 v = red[0][j][lane] + red[1][j][lane] + red[2][j][lane] + red[3][j][lane];
 #pragma unroll
-            for (int e = 0; e < 4; ++e)
-                if (p0 + 4 * g + e < scnt) store_out(L.y, static_cast<size_t>(osl[e]) * L.d_out + row[j], v[e], a.out);
+            for (int q = 0; q < 4; ++q)
+                if (p0 + 4 * g + q < scnt) store_out(L.y, static_cast<size_t>(osl[q]) * L.d_out + row[j], v[q], a.out);
         }
         __syncthreads();                           // red is reused by the next pass
     }
