@@ -654,20 +654,21 @@ __global__ __launch_bounds__(1024) void decode_prep_mfma_kernel(PrepMArgs a) {
 // fixed order and split into fp16 hi and lo parts, one step each); the
 // waves' tiles are summed through LDS in a fixed order; one rounding to the
 // output dtype.
-template <int TPW, int NBUF, bool GLU, int GPB>
-__global__ __launch_bounds__(GLU ? 512 : 256) void decode_mfma_kernel(DecodeArgs a) {
-    // GLU: eight waves, the first four on the gate's tiles and the other four
-    // on the up tiles of the same rows (phase 1); the two sets of sums meet
-    // in LDS and the first four waves store SiLU(gate) * up
+template <int TPW, int NBUF, bool GLU, int GPB, int NW>
+__global__ __launch_bounds__((GLU ? 2 : 1) * 64 * NW) void decode_mfma_kernel(DecodeArgs a) {
+    // NW waves split K.  GLU: 2 NW waves, the first NW on the gate's tiles
+    // and the other NW on the up tiles of the same rows (phase 1); the two
+    // sets of sums meet in LDS and the first NW waves store SiLU(gate) * up
     constexpr int NPH = GLU ? 2 : 1;
-    static_assert(TPW <= 4, "one stored tile per wave");
-    __shared__ f32x4 red[4 * NPH][TPW][64];
+    constexpr int TPH = 64 * NW;                  // threads per phase
+    static_assert(TPW <= NW, "one stored tile per wave");
+    __shared__ f32x4 red[NW * NPH][TPW][64];
     extern __shared__ uint16_t szl_all[];         // per phase [2][16 TPW][groups]: the rows' scales, then zeros
     const int lane = threadIdx.x & 63;
     const int wave_all = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int ph = GLU ? wave_all >> 2 : 0;
-    const int wave = wave_all & 3;                // wave within the phase
-    const int tid = threadIdx.x & 255;            // thread within the phase
+    const int ph = GLU ? wave_all / NW : 0;
+    const int wave = wave_all % NW;               // wave within the phase
+    const int tid = threadIdx.x % TPH;            // thread within the phase
     const int g = lane >> 4, r = lane & 15;
     // workgroup -> (linear, TPW tiles of 16 rows); batch_end counts workgroups
     int li0 = 0;
@@ -842,25 +843,25 @@ __global__ __launch_bounds__(GLU ? 512 : 256) void decode_mfma_kernel(DecodeArgs
             }
         }
     };
-    // blocks of this wave: kb = wave + 4 i, NBUF in flight.  Rounds of NBUF:
+    // blocks of this wave: kb = wave + NW i, NBUF in flight.  Rounds of NBUF:
     // block j of a round is computed, then its registers take block
     // j + NBUF (past the last block they reload the current one, already
     // cached).
-    constexpr int SPAN = 4 * NBUF;                 // blocks per round over the four waves
+    constexpr int SPAN = NW * NBUF;                // blocks per round over the NW waves
     const int rounds = (nkb + SPAN - 1) / SPAN;
     Blk b[NBUF];
 #pragma unroll
-    for (int j = 0; j < NBUF; ++j) load(wave + 4 * j < nkb ? wave + 4 * j : 0, b[j]);
+    for (int j = 0; j < NBUF; ++j) load(wave + NW * j < nkb ? wave + NW * j : 0, b[j]);
     // the scales and zeros into LDS (the code loads stay in flight)
     if (tid < n16) {
         reinterpret_cast<u32x4*>(szl)[tid] = s_first;
         reinterpret_cast<u32x4*>(zl)[tid] = z_first;
     }
-    for (int i = tid + 256; i < n16; i += 256) {           // rows of more than 32 groups
+    for (int i = tid + TPH; i < n16; i += TPH) {           // more pieces than threads
         reinterpret_cast<u32x4*>(szl)[i] = reinterpret_cast<const u32x4*>(ssrc)[i];
         reinterpret_cast<u32x4*>(zl)[i] = reinterpret_cast<const u32x4*>(zsrc)[i];
     }
-    for (int i = 8 * n16 + tid; i < nval; i += 256) {      // misaligned runs, the last few values
+    for (int i = 8 * n16 + tid; i < nval; i += TPH) {      // misaligned runs, the last few values
         szl[i] = ssrc[i];
         zl[i] = zsrc[i];
     }
@@ -868,7 +869,7 @@ __global__ __launch_bounds__(GLU ? 512 : 256) void decode_mfma_kernel(DecodeArgs
     for (int rd = 0; rd < rounds; ++rd) {
 #pragma unroll
         for (int j = 0; j < NBUF; ++j) {
-            const int kb = wave + SPAN * rd + 4 * j;
+            const int kb = wave + SPAN * rd + NW * j;
             compute(kb, b[j]);
             const int kn = kb + SPAN;
             load(kn < nkb ? kn : (kb < nkb ? kb : 0), b[j]);
@@ -876,22 +877,28 @@ __global__ __launch_bounds__(GLU ? 512 : 256) void decode_mfma_kernel(DecodeArgs
     }
     // rank-r term (operands loaded before the K loop, see rank_load)
     rank_mma(32 * wave, rb);
-    for (int kr = 32 * wave + 128; kr < L.rank; kr += 128) {
+    for (int kr = 32 * wave + 32 * NW; kr < L.rank; kr += 32 * NW) {
         RankOp ro;
         rank_load(kr, ro);
         rank_mma(kr, ro);
     }
 #pragma unroll
-    for (int j = 0; j < TPW; ++j) red[4 * ph + wave][j][lane] = acc[j];
+    for (int j = 0; j < TPW; ++j) red[NW * ph + wave][j][lane] = acc[j];
     __syncthreads();
-    // wave w sums and stores tiles w, w + 4, ... in a fixed order
+    // wave w sums and stores tiles w, w + NW, ... in a fixed order
     if (ph == 0) {
 #pragma unroll
         for (int j = 0; j < TPW; ++j) {
-            if (j % 4 != wave || !rowv[j]) continue;
-            const f32x4 v = red[0][j][lane] + red[1][j][lane] + red[2][j][lane] + red[3][j][lane];
+            if (j % NW != wave || !rowv[j]) continue;
+            f32x4 v = red[0][j][lane];
+#pragma unroll
+            for (int w2 = 1; w2 < NW; ++w2) v += red[w2][j][lane];
             f32x4 u = {0.f, 0.f, 0.f, 0.f};
-            if constexpr (GLU) u = red[4][j][lane] + red[5][j][lane] + red[6][j][lane] + red[7][j][lane];
+            if constexpr (GLU) {
+                u = red[NW][j][lane];
+#pragma unroll
+                for (int w2 = 1; w2 < NW; ++w2) u += red[NW + w2][j][lane];
+            }
             // v[e] = y[tok0 + 4 g + e][row0 + 16 j + r] (GLU: the gate's; u the up's)
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
@@ -1037,21 +1044,36 @@ int pad32(int r) { return (r + 31) / 32 * 32; }
 // half of a block lies in one group), else 4 (each 32-code step does)
 int mfma_groups_per_block(int G) { return G % 128 == 0 ? 1 : (G % 64 == 0 ? 2 : 4); }
 
-// blocks in flight per wave: 2 with four tiles per wave, 4 with one; halved
-// when a block holds several groups (their partials and scales need the
-// registers)
+// Launch shape of the MFMA backbone: 16-row tiles per wave (tpw), K blocks
+// in flight per wave (nbuf; halved when a block holds several groups, whose
+// partials and scales need the registers) and waves splitting K (nw).
+struct MfmaCfg {
+    int tpw, nbuf, nw;
+};
+
+MfmaCfg mfma_cfg(int tiles, int groups) {
+    if (tiles >= 1024 && 2 * 64 * groups * 2 <= 32768) return MfmaCfg{4, 2, 4};
+    return MfmaCfg{1, 4, 4};
+}
+
 template <bool GLU, int GPB>
-auto pick_tpw(int tpw) {
-    return tpw == 4 ? decode_mfma_kernel<4, GPB == 1 ? 2 : 1, GLU, GPB>
-                    : decode_mfma_kernel<1, GPB == 1 ? 4 : 2, GLU, GPB>;
+auto pick_cfg(const MfmaCfg& c) {
+    constexpr int H = GPB == 1 ? 1 : 2;           // nbuf divisor
+    if (c.tpw == 4 && c.nw == 16) return decode_mfma_kernel<4, 2 / H, GLU, GPB, 16>;
+    if (c.tpw == 4) return decode_mfma_kernel<4, 2 / H, GLU, GPB, 4>;
+    if (c.tpw == 2 && c.nw == 8) return decode_mfma_kernel<2, 2 / H, GLU, GPB, 8>;
+    if (c.tpw == 2) return decode_mfma_kernel<2, 2 / H, GLU, GPB, 4>;
+    return decode_mfma_kernel<1, 4 / H, GLU, GPB, 4>;
 }
 
 template <bool GLU>
-auto pick_gpb(int tpw, int gpb) {
-    return gpb == 1 ? pick_tpw<GLU, 1>(tpw) : (gpb == 2 ? pick_tpw<GLU, 2>(tpw) : pick_tpw<GLU, 4>(tpw));
+auto pick_gpb(const MfmaCfg& c, int gpb) {
+    return gpb == 1 ? pick_cfg<GLU, 1>(c) : (gpb == 2 ? pick_cfg<GLU, 2>(c) : pick_cfg<GLU, 4>(c));
 }
 
-auto pick_mfma_kernel(int tpw, bool glu, int gpb) { return glu ? pick_gpb<true>(tpw, gpb) : pick_gpb<false>(tpw, gpb); }
+auto pick_mfma_kernel(const MfmaCfg& c, bool glu, int gpb) {
+    return glu ? pick_gpb<true>(c, gpb) : pick_gpb<false>(c, gpb);
+}
 
 }  // namespace
 
@@ -1094,7 +1116,8 @@ hipError_t launch_decode_mfma(int n, const QW* w, const LR* c, const void* x, in
     for (int i = 0; i < n; ++i) tiles += (w[i].d_out + 15) / 16;
     const int groups = d_in / w[0].G;
     // four tiles per wave when the workgroup's scales and zeros fit 32 KB of LDS
-    const int tpw = tiles >= 1024 && 2 * 64 * groups * 2 <= 32768 ? 4 : 1;
+    const MfmaCfg cfg = mfma_cfg(tiles, groups);
+    const int tpw = cfg.tpw;
     int wg_end = 0, rtiles = 0, wg_first = 0;
     for (int i = 0; i < n; ++i) {
         float* tp = reinterpret_cast<float*>(wsb + off);
@@ -1137,7 +1160,7 @@ hipError_t launch_decode_mfma(int n, const QW* w, const LR* c, const void* x, in
     a.kp = mp.kp;
     a.h = glu ? y[0] : nullptr;
     const int gpb = mfma_groups_per_block(w[0].G);
-    auto kern = pick_mfma_kernel(tpw, glu, gpb);
+    auto kern = pick_mfma_kernel(cfg, glu, gpb);
     // a gated window runs one workgroup of eight waves per gate workgroup
     // (four waves on the gate's tiles, four on the up tiles of the same rows),
     // with both linears' scales and zeros in LDS
@@ -1145,7 +1168,7 @@ hipError_t launch_decode_mfma(int n, const QW* w, const LR* c, const void* x, in
     const int bgrid = glu ? wg_first : wg_end;
     for (int tok0 = 0; tok0 < T && e == hipSuccess; tok0 += 16) {
         a.tok0 = tok0;
-        hipLaunchKernelGGL(kern, dim3(bgrid), dim3(glu ? 512 : 256), lds, st, a);
+        hipLaunchKernelGGL(kern, dim3(bgrid), dim3((glu ? 2 : 1) * 64 * cfg.nw), lds, st, a);
         e = hipGetLastError();
     }
     return e;

@@ -11,8 +11,10 @@
 //     X' = X as fp16 (bf16 converted) with every 8 consecutive k reordered
 //     (k0,k4,k1,k5,k2,k6,k3,k7): the order in which the code unpack below
 //     produces weights, so the contraction is unchanged.
-//  2. prefill_kernel: 128 x 256 output tiles (tokens x weight rows), K in
-//     steps of 128 codes.  X' tiles go from global memory straight into LDS
+//  2. prefill_kernel: 128 x 256 output tiles (tokens x weight rows; 128 x 128
+//     when 256-row tiles would leave CUs without two workgroups: 4096 x 4096
+//     at M = 2048 went from 133 to 117 us, while 14336 x 4096 stays faster
+//     with 256 rows, 322 against 350 us), K in steps of 128 codes.  X' tiles go from global memory straight into LDS
 //     (global_load_lds, 16 bytes per lane, two 32 KB stages, chunks XOR-
 //     swizzled by row so the MFMA operand reads are bank-conflict free).  Each
 //     of the four waves owns 128 tokens x 64 weight rows (8 x 4 MFMA tiles):
@@ -37,7 +39,7 @@ namespace cl {
 
 namespace {
 
-constexpr int BM = 128, BN = 256, BK = 128;
+constexpr int BM = 128, BK = 128;
 
 // 8 activations -> fp16, in the pair order (x0,x4),(x1,x5),(x2,x6),(x3,x7)
 __device__ __forceinline__ u32x4 act8_permuted(u32x4 u, int act) {
@@ -210,14 +212,16 @@ struct WStep {
     uint32_t w[BITS];        // 4-bit: 4 words, 2-bit: 2 words
 };
 
-template <int BITS>
+template <int BITS, int JT>
 __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
+    // JT row tiles of 16 per wave: the workgroup covers BM tokens x 64 JT weight rows
+    constexpr int BNT = 64 * JT;
     // two stages of X': [BM rows][16 chunks of 8 k], chunk c of row r stored
     // at slot c ^ xswz(r & 15)
     __shared__ u32x4 xs[2][BM * 16];
-    // scales and zeros of the workgroup's BN rows, windows of 8 consecutive
+    // scales and zeros of the workgroup's BNT rows, windows of 8 consecutive
     // groups, double-buffered: [buffer][scale, zero][row][8]
-    __shared__ uint16_t szw[2][2][BN][8];
+    __shared__ uint16_t szw[2][2][BNT][8];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -227,7 +231,7 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
     // XCD-aware order: consecutive workgroups take consecutive M blocks
     const int mb = blockIdx.x % a.mblocks;
     const int nb = blockIdx.x / a.mblocks;
-    const int m0 = mb * BM, n0 = nb * BN + wave * 64;
+    const int m0 = mb * BM, n0 = nb * BNT + wave * 16 * JT;
     const int nk = (a.K + BK - 1) / BK;
     const int groups = a.K / a.G;
     const int words_row = a.K * BITS / 32;
@@ -249,7 +253,7 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
         }
     };
     // scales and zeros, window wnd (groups 8 wnd .. 8 wnd + 7) of the
-    // workgroup's rows: thread tid takes row nb BN + tid.  fetch_sz issues
+    // workgroup's rows: thread tid < BNT takes row nb BNT + tid.  fetch_sz issues
     // the loads (one 16-byte load per array when the rows are 16-byte
     // aligned); store_sz writes them to LDS buffer wnd % 2 a step later,
     // when they have landed, so no wave waits on them (direct global-to-LDS
@@ -258,7 +262,7 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
                       (reinterpret_cast<uintptr_t>(a.z) & 15) == 0;
     u32x4 szs, szz;
     auto fetch_sz = [&](int wnd) {
-        const int n = nb * BN + tid;
+        const int n = nb * BNT + (tid < BNT ? tid : 0);
         const int nc = n < a.N ? n : a.N - 1;
         const unsigned base = static_cast<unsigned>(nc) * static_cast<unsigned>(groups) + 8u * wnd;
         if (sz16 && 8 * wnd + 8 <= groups) {
@@ -280,18 +284,19 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
         }
     };
     auto store_sz = [&](int wnd) {
+        if (tid >= BNT) return;
         *reinterpret_cast<u32x4*>(szw[wnd & 1][0][tid]) = szs;
         *reinterpret_cast<u32x4*>(szw[wnd & 1][1][tid]) = szz;
     };
     // K steps per window of 8 groups (G / 16 >= 2: G is a multiple of 128 / bits)
     const int spw = a.G / 16;
 
-    // this lane's codes of K step kb for its four weight rows
-    auto load_w = [&](int kb, WStep<BITS> (&ws)[4]) {
+    // this lane's codes of K step kb for its JT weight rows
+    auto load_w = [&](int kb, WStep<BITS> (&ws)[JT]) {
         const int kc = kb * BK + 32 * g;                   // first code of this lane's 32
         const bool kval = kc < a.K;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
+        for (int j = 0; j < JT; ++j) {
             const int n = n0 + 16 * j + r;
             const int nc = n < a.N ? n : a.N - 1;
             const uint32_t* src = a.q + (static_cast<unsigned>(nc) * static_cast<unsigned>(words_row) +
@@ -310,11 +315,11 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
         }
     };
 
-    f32x4 acc[8][4];
+    f32x4 acc[8][JT];
 #pragma unroll
     for (int i = 0; i < 8; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int j = 0; j < JT; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
     // four MFMA steps of 32 codes: lane group g's 8 codes of step t are codes
     // 32 g + 8 t .. + 7 of the K step, X' chunk 4 g + t
@@ -323,16 +328,16 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
     const uint32_t mhi = __builtin_amdgcn_readfirstlane(0x00F000F0u);
     const uint32_t bias = 0x64006400u;
     const int fr = xswz(r);
-    auto compute = [&](int kb, int st, const WStep<BITS> (&ws)[4]) {
-        Zq zq[4];
-        f16x2 s2[4], zz[4];
+    auto compute = [&](int kb, int st, const WStep<BITS> (&ws)[JT]) {
+        Zq zq[JT];
+        f16x2 s2[JT], zz[JT];
         const bool kval = kb * BK + 32 * g < a.K;
         const int gi = kval ? (kb * BK + 32 * g) / a.G : 0;
         const int wb = (gi >> 3) & 1, we = gi & 7;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
+        for (int j = 0; j < JT; ++j) {
             // past K or N the scale is 0: q - z is finite, so the weight is 0
-            const int nl = wave * 64 + 16 * j + r;
+            const int nl = wave * 16 * JT + 16 * j + r;
             const uint32_t zb = szw[wb][1][nl][we];
             const uint32_t sb = (kval && n0 + 16 * j + r < a.N) ? static_cast<uint32_t>(szw[wb][0][nl][we]) : 0u;
             if constexpr (BITS == 4) {
@@ -348,9 +353,9 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
         }
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
-            u32x4 bf[4];
+            u32x4 bf[JT];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
+            for (int j = 0; j < JT; ++j) {
                 if constexpr (BITS == 4) bf[j] = dequant_word4x(ws[j].w[t], zq[j], s2[j], mlo, mhi, bias);
                 else bf[j] = dequant_half2(ws[j].w[t >> 1], t & 1, s2[j], zz[j]);
             }
@@ -359,7 +364,7 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
             for (int i = 0; i < 8; ++i) {
                 const u32x4 af = xs[st][(16 * i + r) * 16 + slot];
 #pragma unroll
-                for (int j = 0; j < 4; ++j) acc[i][j] = mfma(af, bf[j], acc[i][j]);
+                for (int j = 0; j < JT; ++j) acc[i][j] = mfma(af, bf[j], acc[i][j]);
             }
         }
     };
@@ -369,7 +374,7 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
     // the first step of each window (its buffer's previous window retired at
     // the barrier before) and is complete at the barrier after
     const int nwnd = (groups + 7) / 8;
-    WStep<BITS> wa[4], wb[4];
+    WStep<BITS> wa[JT], wb[JT];
     load_x(0, 0);
     load_w(0, wa);
     fetch_sz(0);
@@ -401,9 +406,9 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
     // ---- rank-r correction: MFMA steps of 32 over [T | B] (natural k order)
     for (int kr = 0; kr < a.r_pad; kr += 32) {
         const int k = kr + 8 * g;
-        u32x4 bf[4];
+        u32x4 bf[JT];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
+        for (int j = 0; j < JT; ++j) {
             const int n = n0 + 16 * j + r;
             uint32_t v[4] = {0, 0, 0, 0};
             if (n < a.N) {
@@ -420,7 +425,7 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
             const int m = m0 + 16 * i + r;
             const u32x4 af = *reinterpret_cast<const u32x4*>(a.T + static_cast<size_t>(m < a.M ? m : a.M - 1) * a.r_pad + k);
 #pragma unroll
-            for (int j = 0; j < 4; ++j) acc[i][j] = mfma(af, bf[j], acc[i][j]);
+            for (int j = 0; j < JT; ++j) acc[i][j] = mfma(af, bf[j], acc[i][j]);
         }
     }
 
@@ -428,7 +433,7 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
 #pragma unroll
     for (int i = 0; i < 8; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
+        for (int j = 0; j < JT; ++j) {
             const int n = n0 + 16 * j + r;
             if (n >= a.N) continue;
 #pragma unroll
@@ -440,6 +445,18 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
 }
 
 size_t up256(size_t n) { return (n + 255) / 256 * 256; }
+
+int prefill_cus() {
+    static int cus[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+    if (!cus[dev]) {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+        cus[dev] = n;
+    }
+    return cus[dev];
+}
 
 }  // namespace
 
@@ -478,11 +495,18 @@ hipError_t launch_linear_prefill(const QW& w, const LR& c, const void* X, int M,
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    const unsigned blocks = static_cast<unsigned>(a.mblocks * ((w.d_out + BN - 1) / BN));
-    if (w.bits == 4)
-        hipLaunchKernelGGL(prefill_kernel<4>, dim3(blocks), dim3(256), 0, st, a);
-    else
-        hipLaunchKernelGGL(prefill_kernel<2>, dim3(blocks), dim3(256), 0, st, a);
+    // 256-row workgroup tiles, or 128-row ones when 256-row tiles would not
+    // give every CU two workgroups (4096 x 4096 at M = 2048: 256 tiles)
+    const long long tiles256 = static_cast<long long>(a.mblocks) * ((w.d_out + 255) / 256);
+    const int jt = tiles256 < 2ll * prefill_cus() ? 2 : 4;
+    const unsigned blocks = static_cast<unsigned>(a.mblocks * ((w.d_out + 64 * jt - 1) / (64 * jt)));
+    if (w.bits == 4) {
+        if (jt == 2) hipLaunchKernelGGL((prefill_kernel<4, 2>), dim3(blocks), dim3(256), 0, st, a);
+        else hipLaunchKernelGGL((prefill_kernel<4, 4>), dim3(blocks), dim3(256), 0, st, a);
+    } else {
+        if (jt == 2) hipLaunchKernelGGL((prefill_kernel<2, 2>), dim3(blocks), dim3(256), 0, st, a);
+        else hipLaunchKernelGGL((prefill_kernel<2, 4>), dim3(blocks), dim3(256), 0, st, a);
+    }
     return hipGetLastError();
 }
 
