@@ -62,6 +62,18 @@ __device__ __forceinline__ u32x4 dequant_word4x(uint32_t w, const Zq& zq, f16x2 
     return r;
 }
 
+// One half of dequant_word4x: h = 0 gives r[0], r[1] (codes of the low
+// byte of each half-word), h = 1 gives r[2], r[3]; the same values.
+__device__ __forceinline__ void dequant_half4x(uint32_t w, int h, const Zq& zq, f16x2 s2, uint32_t mlo, uint32_t mhi,
+                                               uint32_t bias, uint32_t& lo, uint32_t& hi) {
+    const uint32_t v = h ? w >> 8 : w;
+    const f16x2 sixteenth = {static_cast<f16>(0.0625f), static_cast<f16>(0.0625f)};
+    const f16x2 a = __builtin_bit_cast(f16x2, and_or(v, mlo, bias)) + zq.lo;
+    const f16x2 b = __builtin_elementwise_fma(__builtin_bit_cast(f16x2, and_or(v, mhi, bias)), sixteenth, zq.hi);
+    lo = __builtin_bit_cast(uint32_t, a * s2);
+    hi = __builtin_bit_cast(uint32_t, b * s2);
+}
+
 // 4 x 4 transpose across the four 16-lane groups of a wave: on entry lane
 // group g holds words 4 g .. 4 g + 3 of a 16-word run in w[0..3]; on return
 // w[t] holds word 4 t + g.  v_permlane32_swap exchanges rows 2-3 of its first

@@ -14,20 +14,31 @@
 //  2. prefill_kernel: 128 x 256 output tiles (tokens x weight rows; 128 x 128
 //     when 256-row tiles would leave CUs without two workgroups: 4096 x 4096
 //     at M = 2048 went from 133 to 117 us, while 14336 x 4096 stays faster
-//     with 256 rows, 322 against 350 us), K in steps of 128 codes.  X' tiles go from global memory straight into LDS
-//     (global_load_lds, 16 bytes per lane, two 32 KB stages, chunks XOR-
-//     swizzled by row so the MFMA operand reads are bank-conflict free).  Each
-//     of the four waves owns 128 tokens x 64 weight rows (8 x 4 MFMA tiles):
-//     it loads its rows' packed codes for the next K step into registers (one
-//     16-byte load per lane and fragment: 32 codes of one quantization group,
-//     so one scale and zero per lane) and dequantizes them per MFMA step as
-//     s * (q - z) in fp16 (the integer q - z is formed exactly from the code
-//     OR-ed into the mantissa of 1024.0, then one rounding for the scale).  No weight tile goes through LDS and no wave repeats
-//     another's dequantization.  The workgroup's scales and zeros do go
-//     through LDS, in double-buffered windows of 8 groups per row (one
+//     with 256 rows, 322 against 350 us), K in steps of 128 codes.  X' tiles
+//     go from global memory straight into LDS (global_load_lds, 16 bytes per
+//     lane, two 32 KB stages, chunks XOR-swizzled by row so the MFMA operand
+//     reads are bank-conflict free).  Each of the four waves owns 128 tokens
+//     x 16 JT weight rows (8 x JT MFMA tiles): it loads its rows' packed
+//     codes for the next K step into registers (one 16-byte load per lane
+//     and fragment: 32 codes of one quantization group, so one scale and zero
+//     per lane) and dequantizes them as s * (q - z) in fp16 (the integer
+//     q - z is formed exactly from the code OR-ed into the mantissa of
+//     1024.0, then one rounding for the scale).  The K step is software-
+//     pipelined: the code words of MFMA step t + 1 are dequantized in halves
+//     between the MFMAs of step t, and each X' operand is read from LDS a
+//     few MFMA groups before its use (14336 x 4096: 320 -> 308 us; 4096 x
+//     4096: 122 -> 113 us).  No weight tile goes through LDS and no wave
+//     repeats another's dequantization.  The workgroup's scales and zeros do
+//     go through LDS, in double-buffered windows of 8 groups per row (one
 //     16-byte load per thread and array per window): per-lane 2-byte
-//     gathers had cost 13 % of the kernel's time.  The rank-r correction is extra MFMA steps
-//     over [T | B] (read from global memory) into the same accumulators.
+//     gathers had cost 13 % of the kernel's time.  The rank-r correction is
+//     extra MFMA steps over [T | B] (read from global memory) into the same
+//     accumulators.
+//     A 256-token tile (one workgroup per CU, 16 token tiles per wave, so
+//     each dequantized operand feeds 16 MFMAs) was built and measured: with
+//     32 rows per wave it ran 401 us on 14336 x 4096 (X' operand reads at
+//     512 bytes of LDS per MFMA, one wave per SIMD to hide latency), and 64
+//     rows per wave need more than the 512 registers a lane can hold.
 //  Workgroups are numbered so that the N tiles of one 128-token block run on
 //  one XCD (workgroup i runs on XCD i mod 8) and share its L2 copy of X'.
 
@@ -39,7 +50,7 @@ namespace cl {
 
 namespace {
 
-constexpr int BM = 128, BK = 128;
+constexpr int BK = 128;
 
 // 8 activations -> fp16, in the pair order (x0,x4),(x1,x5),(x2,x6),(x3,x7)
 __device__ __forceinline__ u32x4 act8_permuted(u32x4 u, int act) {
@@ -78,7 +89,7 @@ struct PrefillArgs {
     const uint16_t* T;       // [M][r_pad] fp16 (workspace)
     void* Y;                 // [M][N]
     int M, N, K, G, rank, r_max, r_pad, out;
-    int mblocks;             // ceil(M / BM)
+    int mblocks;             // ceil(M / tokens per workgroup)
 };
 
 // X' for 8 activations of a 16-byte chunk: fp16, order (k0,k4,k1,k5,...).
@@ -197,6 +208,14 @@ __global__ __launch_bounds__(NW * 64) void lowrank_t_kernel(const uint16_t* __re
     }
 }
 
+// 16 bytes per lane from global memory straight into LDS (lane l's bytes
+// land at dst + 16 l; dst is wave-uniform).  A plain function, so the
+// builtin never sees a template-dependent LDS operand (the host compiler
+// then drops the kernel's launch stub).
+__device__ __forceinline__ void global_to_lds16(const uint16_t* src, u32x4* dst) {
+    __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)dst, 16, 0, 0);
+}
+
 // LDS slot of X' chunk c in a row whose low four index bits are r: c ^ f(r)
 // with f(r) = (r >> 1 & 3) | (r & 1) << 2 | (r & 8), a permutation of 0..15.
 // An MFMA operand read has lanes r = 0..15 of lane group g on chunk 4 g + t;
@@ -214,14 +233,18 @@ struct WStep {
 
 template <int BITS, int JT>
 __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
-    // JT row tiles of 16 per wave: the workgroup covers BM tokens x 64 JT weight rows
+    // MT token tiles and JT row tiles of 16 per wave: the workgroup covers
+    // BM = 16 MT tokens x 64 JT weight rows
+    constexpr int MT = 8;
+    constexpr int BM = 16 * MT;
     constexpr int BNT = 64 * JT;
-    // two stages of X': [BM rows][16 chunks of 8 k], chunk c of row r stored
-    // at slot c ^ xswz(r & 15)
-    __shared__ u32x4 xs[2][BM * 16];
-    // scales and zeros of the workgroup's BNT rows, windows of 8 consecutive
-    // groups, double-buffered: [buffer][scale, zero][row][8]
-    __shared__ uint16_t szw[2][2][BNT][8];
+    // LDS (dynamic, prefill_lds_bytes): two stages of X', [BM rows][16
+    // chunks of 8 k], chunk c of row r stored at slot c ^ xswz(r & 15); then
+    // the scales and zeros of the workgroup's BNT rows, windows of 8
+    // consecutive groups, double-buffered: [buffer][scale, zero][row][8]
+    extern __shared__ u32x4 smem[];
+    u32x4 (*xs)[BM * 16] = reinterpret_cast<u32x4 (*)[BM * 16]>(smem);
+    uint16_t (*szw)[2][BNT][8] = reinterpret_cast<uint16_t (*)[2][BNT][8]>(smem + 2 * BM * 16);
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -236,20 +259,26 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
     const int groups = a.K / a.G;
     const int words_row = a.K * BITS / 32;
 
-    // X' tile of K step kb into stage st: wave w fills slots [512 w, 512 w + 512)
+    // X' tile of K step kb into stage st: wave w fills slots [64 MT w, 64 MT (w + 1))
+    // Rows past M read the workspace's padding (X' holds a whole number of
+    // 128-token blocks): their values only reach output rows that are never
+    // stored, so the row offset splits into a wave-uniform part and one of
+    // four per-lane patterns, and no per-load offset stays live in a
+    // register.
     auto load_x = [&](int kb, int st) {
         const int k0 = kb * BK;
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            const int blk = wave * 8 + j;                  // 64 slots = 4 rows
-            const int row = 4 * blk + (lane >> 4);
-            const int chunk = (lane & 15) ^ xswz(row & 15);
-            const int m = m0 + row < a.M ? m0 + row : a.M - 1;
-            int k = k0 + 8 * chunk;
-            if (k >= a.K) k = k0;                          // half K step: weights there are zero
-            // 32-bit element offsets (the entry point bounds M K): scalar base + vector offset
-            const unsigned off = static_cast<unsigned>(m) * static_cast<unsigned>(a.K) + static_cast<unsigned>(k);
-            __builtin_amdgcn_global_load_lds(a.Xp + off, &xs[st][blk * 64], 16, 0, 0);
+        for (int j = 0; j < MT; ++j) {
+            const int blk = wave * MT + j;                 // 64 slots = 4 rows
+            const int rl = lane >> 4;
+            // (4 blk + rl) & 15 == (4 j + rl) & 15: MT is a multiple of 4
+            const int chunk = (lane & 15) ^ xswz((4 * j + rl) & 15);
+            int k = 8 * chunk;
+            if (k0 + k >= a.K) k = 0;                      // half K step: weights there are zero
+            // 32-bit element offsets (the entry point bounds M K): uniform + per lane
+            const unsigned ubase = static_cast<unsigned>(m0 + 4 * blk) * static_cast<unsigned>(a.K) + k0;
+            const unsigned voff = static_cast<unsigned>(rl) * static_cast<unsigned>(a.K) + static_cast<unsigned>(k);
+            global_to_lds16(a.Xp + ubase + voff, &xs[st][blk * 64]);
         }
     };
     // scales and zeros, window wnd (groups 8 wnd .. 8 wnd + 7) of the
@@ -315,9 +344,9 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
         }
     };
 
-    f32x4 acc[8][JT];
+    f32x4 acc[MT][JT];
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
+    for (int i = 0; i < MT; ++i)
 #pragma unroll
         for (int j = 0; j < JT; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
@@ -351,20 +380,70 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
                 zz[j] = f16x2{zf, zf};
             }
         }
+        if constexpr (BITS == 4) {
+            // Software pipeline over the 4 MT regions of the step (region =
+            // MFMA step t, token tile i: one X' operand, JT MFMAs): the X'
+            // operand of the region PD ahead is read from LDS (PD regions
+            // of MFMAs cover the read's latency), and the code words of step
+            // t + 1 are dequantized in halves spread over the regions of
+            // step t, so MFMA, LDS and VALU work interleave.  The
+            // scheduling fence after each region keeps that order.
+            constexpr int PD = 8 / JT;
+            constexpr int NREG = 4 * MT;
+            auto xop = [&](int reg) {
+                const int i = reg % MT, t = reg / MT;
+                return xs[st][(16 * i + r) * 16 + ((4 * g + t) ^ fr)];
+            };
+            u32x4 bc[JT], bn[JT], ap[PD];
 #pragma unroll
-        for (int t = 0; t < 4; ++t) {
-            u32x4 bf[JT];
+            for (int q = 0; q < PD; ++q) ap[q] = xop(q);
 #pragma unroll
-            for (int j = 0; j < JT; ++j) {
-                if constexpr (BITS == 4) bf[j] = dequant_word4x(ws[j].w[t], zq[j], s2[j], mlo, mhi, bias);
-                else bf[j] = dequant_half2(ws[j].w[t >> 1], t & 1, s2[j], zz[j]);
+            for (int j = 0; j < JT; ++j) bc[j] = dequant_word4x(ws[j].w[0], zq[j], s2[j], mlo, mhi, bias);
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+#pragma unroll
+                for (int i = 0; i < MT; ++i) {
+                    const int reg = t * MT + i;
+                    const u32x4 a0 = ap[reg % PD];
+                    if (reg + PD < NREG) ap[reg % PD] = xop(reg + PD);
+#pragma unroll
+                    for (int j = 0; j < JT; ++j) acc[i][j] = mfma(a0, bc[j], acc[i][j]);
+                    constexpr int NH = 2 * JT;             // word halves per step
+                    if (t < 3 && (i * NH) % MT == 0) {
+                        const int hx = i * NH / MT, j = hx / 2, h = hx % 2;
+                        uint32_t lo, hi;
+                        dequant_half4x(ws[j].w[t + 1], h, zq[j], s2[j], mlo, mhi, bias, lo, hi);
+                        bn[j][2 * h] = lo;
+                        bn[j][2 * h + 1] = hi;
+                    }
+                    // region order: MFMA, the prefetch read, then VALU work
+                    // between the MFMAs (masks: 0x008 MFMA, 0x100 LDS read,
+                    // 0x002 VALU)
+#pragma unroll
+                    for (int m = 0; m < JT; ++m) {
+                        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                        if (m == 0) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+                        __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
+                    }
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+                if (t < 3)
+#pragma unroll
+                    for (int j = 0; j < JT; ++j) bc[j] = bn[j];
             }
-            const int slot = (4 * g + t) ^ fr;
+        } else {
 #pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                const u32x4 af = xs[st][(16 * i + r) * 16 + slot];
+            for (int t = 0; t < 4; ++t) {
+                u32x4 bf[JT];
 #pragma unroll
-                for (int j = 0; j < JT; ++j) acc[i][j] = mfma(af, bf[j], acc[i][j]);
+                for (int j = 0; j < JT; ++j) bf[j] = dequant_half2(ws[j].w[t >> 1], t & 1, s2[j], zz[j]);
+                const int slot = (4 * g + t) ^ fr;
+#pragma unroll
+                for (int i = 0; i < MT; ++i) {
+                    const u32x4 af = xs[st][(16 * i + r) * 16 + slot];
+#pragma unroll
+                    for (int j = 0; j < JT; ++j) acc[i][j] = mfma(af, bf[j], acc[i][j]);
+                }
             }
         }
     };
@@ -385,6 +464,7 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
     // first step and stored at its end (its buffer's previous window retired
     // at the barrier before the fetch; the barrier after the store publishes
     // it)
+    {
     for (int kb = 0; kb < nk; kb += 2) {
         const bool f0 = kb % spw == 0 && kb / spw + 1 < nwnd;
         if (f0) fetch_sz(kb / spw + 1);
@@ -401,6 +481,8 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
         if (f1) store_sz((kb + 1) / spw + 1);
         __builtin_amdgcn_s_waitcnt(0);
         __syncthreads();
+    }
+
     }
 
     // ---- rank-r correction: MFMA steps of 32 over [T | B] (natural k order)
@@ -421,7 +503,7 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
             bf[j] = u32x4{v[0], v[1], v[2], v[3]};
         }
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
+        for (int i = 0; i < MT; ++i) {
             const int m = m0 + 16 * i + r;
             const u32x4 af = *reinterpret_cast<const u32x4*>(a.T + static_cast<size_t>(m < a.M ? m : a.M - 1) * a.r_pad + k);
 #pragma unroll
@@ -431,7 +513,7 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
 
     // ---- store: acc[i][j][e] = Y[m0 + 16 i + 4 g + e][n0 + 16 j + r]
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
+    for (int i = 0; i < MT; ++i)
 #pragma unroll
         for (int j = 0; j < JT; ++j) {
             const int n = n0 + 16 * j + r;
@@ -458,17 +540,29 @@ int prefill_cus() {
     return cus[dev];
 }
 
+// Row tiles per wave: 256-row workgroup tiles, or 128-row ones when 256-row
+// tiles would not give every CU two workgroups (4096 x 4096 at M = 2048:
+// 256 tiles; 117 against 133 us, while 14336 x 4096 stays faster with 256
+// rows, 322 against 350 us)
+int prefill_jt(int M, int N) {
+    const long long tiles256 = static_cast<long long>((M + 127) / 128) * ((N + 255) / 256);
+    return tiles256 < 2ll * prefill_cus() ? 2 : 4;
+}
+
 }  // namespace
+
+// X' rows padded to whole 128-token blocks (prefill_kernel reads them)
+size_t xp_rows(int M) { return (static_cast<size_t>(M) + 127) / 128 * 128; }
 
 size_t prefill_workspace_bytes(const QW& w, const LR& c, int M) {
     const int r_pad = (c.rank + 31) / 32 * 32;
-    return up256(static_cast<size_t>(M) * w.d_in * 2) + up256(static_cast<size_t>(M) * r_pad * 2);
+    return up256(xp_rows(M) * w.d_in * 2) + up256(static_cast<size_t>(M) * r_pad * 2);
 }
 
 hipError_t launch_linear_prefill(const QW& w, const LR& c, const void* X, int M, int act, void* Y, int out,
                                  void* ws, hipStream_t st) {
     uint16_t* Xp = static_cast<uint16_t*>(ws);
-    uint16_t* T = reinterpret_cast<uint16_t*>(static_cast<char*>(ws) + up256(static_cast<size_t>(M) * w.d_in * 2));
+    uint16_t* T = reinterpret_cast<uint16_t*>(static_cast<char*>(ws) + up256(xp_rows(M) * w.d_in * 2));
     PrefillArgs a;
     a.q = w.q; a.s = w.s; a.z = w.z; a.B = c.B;
     a.Xp = Xp;
@@ -477,7 +571,8 @@ hipError_t launch_linear_prefill(const QW& w, const LR& c, const void* X, int M,
     a.M = M; a.N = w.d_out; a.K = w.d_in; a.G = w.G;
     a.rank = c.rank; a.r_max = c.r_max; a.r_pad = (c.rank + 31) / 32 * 32;
     a.out = out;
-    a.mblocks = (M + BM - 1) / BM;
+    const int jt = prefill_jt(M, w.d_out);
+    a.mblocks = (M + 127) / 128;
     const uint16_t* Xa = static_cast<const uint16_t*>(X);
     if (c.rank > 0) {
         constexpr int NW = 8;
@@ -495,18 +590,14 @@ hipError_t launch_linear_prefill(const QW& w, const LR& c, const void* X, int M,
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    // 256-row workgroup tiles, or 128-row ones when 256-row tiles would not
-    // give every CU two workgroups (4096 x 4096 at M = 2048: 256 tiles)
-    const long long tiles256 = static_cast<long long>(a.mblocks) * ((w.d_out + 255) / 256);
-    const int jt = tiles256 < 2ll * prefill_cus() ? 2 : 4;
     const unsigned blocks = static_cast<unsigned>(a.mblocks * ((w.d_out + 64 * jt - 1) / (64 * jt)));
-    if (w.bits == 4) {
-        if (jt == 2) hipLaunchKernelGGL((prefill_kernel<4, 2>), dim3(blocks), dim3(256), 0, st, a);
-        else hipLaunchKernelGGL((prefill_kernel<4, 4>), dim3(blocks), dim3(256), 0, st, a);
-    } else {
-        if (jt == 2) hipLaunchKernelGGL((prefill_kernel<2, 2>), dim3(blocks), dim3(256), 0, st, a);
-        else hipLaunchKernelGGL((prefill_kernel<2, 4>), dim3(blocks), dim3(256), 0, st, a);
-    }
+    const dim3 grid(blocks), block(256);
+    // X' stages and scale/zero windows (see prefill_kernel)
+    const size_t lds = (2 * 128 * 16 + 64 * jt * 4) * sizeof(u32x4);
+    if (w.bits == 4 && jt == 4) hipLaunchKernelGGL((prefill_kernel<4, 4>), grid, block, lds, st, a);
+    else if (w.bits == 4) hipLaunchKernelGGL((prefill_kernel<4, 2>), grid, block, lds, st, a);
+    else if (jt == 4) hipLaunchKernelGGL((prefill_kernel<2, 4>), grid, block, lds, st, a);
+    else hipLaunchKernelGGL((prefill_kernel<2, 2>), grid, block, lds, st, a);
     return hipGetLastError();
 }
 
