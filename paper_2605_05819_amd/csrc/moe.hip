@@ -58,6 +58,11 @@ constexpr int kMaxSlots = 1024;      // T * k
 constexpr int kMaxExperts = 1024;
 constexpr int kTab = 8;              // ints per active-expert table entry
 constexpr int kMaxMoeWin = 4;        // linears per window
+// Direct path (moe_direct_kernel): at most this many slots; row batches per
+// wave (4 waves, 4 rows per row set of LG lanes: 64 rows per workgroup, 32
+// with two chunks per lane)
+constexpr int kDirectMaxSlots = 8;
+constexpr int direct_batches(int lg, int cpl) { return cpl == 2 ? 2 : (lg == 64 ? 4 : 2); }
 // MFMA path: 16-row tiles per workgroup and K blocks in flight per wave.
 // Measured on the 48-layer T = 64 step with the workgroup's loads issued in
 // need order (scales and zeros, slot ids, code blocks): 8 x 1 166 us per
@@ -84,6 +89,8 @@ struct MoeLin {
     int bpe;                 // backbone batches per expert
     int prep_end;            // rank workgroups of linears 0 .. this one (prefix sum)
     int blk_end;             // backbone workgroups of linears 0 .. this one (prefix sum)
+    int nrb;                 // direct path: row blocks per slot
+    int dblk_end;            // direct path: workgroups of linears 0 .. this one (prefix sum)
 };
 
 // A window of n linears over the same routing and activations (one linear
@@ -102,6 +109,7 @@ struct MoeArgs {
     f16x2* xp;               // [rows][d_in/2]
     float* sx;               // [rows][chunks]
     int ks, cps;             // K slices, chunks per slice
+    int rb;                  // direct path: rows per workgroup
 };
 
 template <int BITS>
@@ -328,8 +336,8 @@ __global__ __launch_bounds__(256) void moe_prep_kernel(MoeArgs a) {
 // HOIST: unpack the codes once into fp16 lanes held in registers (for
 // experts that meet several slots); otherwise unpack per slot.
 // Sum R values over each group of LG consecutive lanes (LG = 16, 32 or 64,
-// a power of two >= R) with a transposing butterfly; on return lane l holds
-// the total of value index (l % LG) / (LG / R) of its group.
+// a power of two >= R, R <= 16) with a transposing butterfly; on return lane
+// l holds the total of value index (l % LG) / (LG / R) of its group.
 template <int R, int LG>
 __device__ __forceinline__ float group_sum_multi(float (&v)[R]) {
     const int lane = threadIdx.x & 63;
@@ -339,7 +347,7 @@ __device__ __forceinline__ float group_sum_multi(float (&v)[R]) {
     int n = R;
     int bit = LG / 2;
 #pragma unroll
-    for (int step = 0; step < 3; ++step) {
+    for (int step = 0; step < 4; ++step) {
         if (n > 1) {
             const bool up = (lane & bit) != 0;
             const int h = n / 2;
@@ -560,6 +568,252 @@ void moe_kernel(MoeArgs a) {
             }
             __syncthreads();
         }
+    }
+}
+
+// Few slots, 4-bit codes: one launch and no preparation.  Workgroup =
+// (linear, slot, block of a.rb rows).  It reads the slot's expert id, forms
+// the slot's activations in registers (the same fp16 pairs and chunk sums the
+// preparation writes), computes t = A_e[:r] x itself (each of its waves takes
+// rows i = wave + 4 p up to r_max, UR rows with all their loads in flight,
+// one butterfly sum per row; the slot's other workgroups repeat this small
+// product, r x d_in multiply-adds over A_e rows that L2 serves after the
+// first), and then applies its rows' codes with the arithmetic of
+// moe_kernel: row batches of 4 rows per row set of LG lanes, CPL chunks per
+// lane.  Every load of the workgroup's NBW batches per wave is issued right
+// after the id arrives, before the A_e x product: with one batch in flight
+// per wave the layer waited one memory round trip per batch.  At one
+// token with 8 routed experts this replaces the preparation launch and its
+// dependent memory round trips (ids, A_e rows, then the backbone's reads of
+// t and the activations).
+template <int LG, int CPL, int NB, int QX, int NBW>
+__global__ __launch_bounds__(256) void moe_direct_kernel(MoeArgs a) {
+    constexpr int R = 4, CPC = 32, PPC = 16, HPW = 4, NACC = 2;
+    constexpr int SETS = 64 / LG;
+    constexpr int NBA = NB > 0 ? NB : 1;
+    constexpr int UR = QX > 4 ? 4 : 8;             // rank rows per wave in flight
+    __shared__ float tsh[NBA * LG];                // t of the slot, zero past its rank
+    const int blk = blockIdx.x;
+    int li = 0;
+    while (blk >= a.lin[li].dblk_end) ++li;
+    const MoeLin& L = a.lin[li];
+    const int local = blk - (li ? a.lin[li - 1].dblk_end : 0);
+    const int sl = local / L.nrb;
+    const int rbi = local - sl * L.nrb;
+    const int rfirst = rbi * a.rb;
+    const int rend = min(L.d_out, rfirst + a.rb);
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int lg = lane % LG;
+    const int chunks = a.d_in / CPC;
+    const int words = a.d_in / 8;
+    const int groups = a.d_in / a.G;
+
+    const int e = a.ids[sl];
+    const int xrow = a.x_per_slot ? sl : sl / a.k;
+    const uint16_t* xr = a.x + static_cast<size_t>(xrow) * a.d_in;
+    // activations of this lane's chunks (unpack pair order) and their sums
+    int cidx[CPL];
+    float cmask[CPL];
+#pragma unroll
+    for (int j = 0; j < CPL; ++j) {
+        cidx[j] = lg + LG * j;
+        cmask[j] = cidx[j] < chunks ? 1.f : 0.f;
+        if (cidx[j] >= chunks) cidx[j] = 0;
+    }
+    // raw loads here; the conversion (load_chunk_x's pairs and the chunk
+    // sums) waits until the other loads are out
+    u32x4 xraw[CPL][4];
+#pragma unroll
+    for (int j = 0; j < CPL; ++j)
+#pragma unroll
+        for (int w = 0; w < 4; ++w) xraw[j][w] = *reinterpret_cast<const u32x4*>(xr + (cidx[j] * 4 + w) * 8);
+    if (e < 0 || e >= a.E) {
+        // out-of-range id: this slot's rows are zero, and the device's
+        // routing-error record notes it (as the preparation does)
+        if (li == 0 && rbi == 0 && tid == 0)
+            __hip_atomic_store(&moe_routing_error,
+                               (1ull << 63) | (static_cast<unsigned long long>(sl) << 32) | static_cast<uint32_t>(e),
+                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        for (int o = rfirst + tid; o < rend; o += 256) store_out(L.y, static_cast<size_t>(sl) * L.d_out + o, 0.f, a.out);
+        return;
+    }
+
+    // row batches: batch b covers rows rfirst + b R SETS .. + R SETS - 1, a
+    // row set of LG lanes R consecutive rows; wave w takes b = w, w + 4, ...
+    const uint32_t* qe = L.q + static_cast<size_t>(e) * L.q_stride;
+    const uint16_t* se = L.s + static_cast<size_t>(e) * L.sz_stride;
+    const uint16_t* ze = L.z + static_cast<size_t>(e) * L.sz_stride;
+    const uint16_t* Be = L.B + static_cast<size_t>(e) * L.b_stride;
+    const int nbatch = (rend - rfirst + R * SETS - 1) / (R * SETS);
+    // scales, zeros and factor entries one per register: 16-bit loads into
+    // register halves make each load wait for the one before
+    struct Bt {
+        u32x4 q[R][CPL];
+        uint32_t s[R][CPL], z[R][CPL], b[R][NBA];
+    };
+    auto row_of = [&](int b, int& row0, int& nrows) {
+        row0 = rfirst + b * R * SETS + (lane / LG) * R;
+        nrows = row0 < rend ? min(R, rend - row0) : 0;
+    };
+    auto load_batch = [&](int b, Bt& bt) {
+        int row0, nrows;
+        row_of(b, row0, nrows);
+        const int base = nrows > 0 ? row0 : rfirst;
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const int row = base + (r < nrows ? r : 0);
+#pragma unroll
+            for (int j = 0; j < CPL; ++j) {
+                bt.q[r][j] = __builtin_nontemporal_load(
+                    reinterpret_cast<const u32x4*>(qe + static_cast<size_t>(row) * words) + cidx[j]);
+                const size_t gi = static_cast<size_t>(row) * groups + (cidx[j] * CPC) / a.G;
+                bt.s[r][j] = se[gi];
+                bt.z[r][j] = ze[gi];
+            }
+#pragma unroll
+            for (int m = 0; m < NB; ++m) {
+                const int i = lg + LG * m;
+                bt.b[r][m] = Be[static_cast<size_t>(row) * L.r_max + (i < L.r_max ? i : 0)];
+            }
+        }
+    };
+    // all of this wave's batches (b = wave + 4 u) load before the t product,
+    // unconditionally (a batch past the last reads the last one's rows): a
+    // load under a branch is waited for where the branches meet
+    Bt bts[NBW];
+#pragma unroll
+    for (int u = 0; u < NBW; ++u) load_batch(min(wave + 4 * u, nbatch - 1), bts[u]);
+
+    // t = A_e[:rank] x: x as fp16 runs, lane l and pass q holding columns
+    // 512 q + 8 l .. + 7
+    // raw loads now, the conversion after the A loads are out
+    u32x4 xw[QX];
+#pragma unroll
+    for (int q = 0; q < QX; ++q) {
+        const int c = 512 * q + 8 * lane;
+        xw[q] = *reinterpret_cast<const u32x4*>(xr + (c < a.d_in ? c : 0));
+    }
+    bool xconv = false;
+    // the rank through one selected pointer (no load under a branch; without
+    // factors any valid word stands in and the rank is 0), used only after
+    // the A x product so that no load waits for it
+    const int32_t* rp = L.r_max == 0 ? a.ids + sl : (L.slot_rank ? L.slot_rank + sl : L.ranks + e);
+    const int rank_raw = *rp;
+    const uint16_t* Ae = L.A + static_cast<size_t>(e) * L.a_stride;
+    // rows up to r_max, not the rank: the A loads then need not wait for the
+    // rank's load (rows past the rank are dropped below)
+    for (int p0 = 0; wave + 4 * p0 < L.r_max; p0 += UR) {
+        // clamped addresses and selects: the loads carry no branches
+        u32x4 av[UR][QX];
+#pragma unroll
+        for (int u = 0; u < UR; ++u) {
+            const int i = wave + 4 * (p0 + u);
+            const int ic = i < L.r_max ? i : wave;
+#pragma unroll
+            for (int q = 0; q < QX; ++q) {
+                const int c = 512 * q + 8 * lane;
+                av[u][q] = *reinterpret_cast<const u32x4*>(Ae + static_cast<size_t>(ic) * a.d_in + (c < a.d_in ? c : 0));
+            }
+        }
+        // keep the value work below the loads above (hoisted, it waited for
+        // earlier loads before these were issued)
+        __builtin_amdgcn_sched_barrier(0);
+        if (!xconv) {
+#pragma unroll
+            for (int q = 0; q < QX; ++q)
+                xw[q] = 512 * q + 8 * lane < a.d_in ? act8_to_f16(xw[q], a.act) : u32x4{0u, 0u, 0u, 0u};
+            xconv = true;
+        }
+        float d[UR];
+#pragma unroll
+        for (int u = 0; u < UR; ++u) {
+            d[u] = 0.f;
+#pragma unroll
+            for (int q = 0; q < QX; ++q)
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    // copy the vector elements to scalars first: a bit_cast
+                    // of a subscripted ext_vector reads element 0
+                    const uint32_t ak = av[u][q][k], xk = xw[q][k];
+                    d[u] = dot2(__builtin_bit_cast(f16x2, ak), __builtin_bit_cast(f16x2, xk), d[u]);
+                }
+        }
+        // lane l holds the total of row p0 + l / (64 / UR)
+        const float tot = wave_sum_multi<UR>(d);
+        const int u = lane / (64 / UR);
+        const int i = wave + 4 * (p0 + u);
+        if (lane % (64 / UR) == 0 && i < L.r_max) tsh[i] = tot;
+    }
+    for (int i = L.r_max + tid; i < NBA * LG; i += 256) tsh[i] = 0.f;
+    __syncthreads();
+    // the rank masks t and B only here (rows of A past the rank may hold
+    // anything: their products are never used)
+    // (the empty asm takes the loaded word as a vector value here: treated as
+    // uniform, it was moved to a scalar register right after its load, and
+    // that move waited for every load issued before it)
+    int rank_v = rank_raw;
+    asm volatile("" : "+v"(rank_v));
+    const int rank = L.r_max == 0 ? 0 : (rank_v < 0 ? 0 : (rank_v > L.r_max ? L.r_max : rank_v));
+    // the activations of this lane's chunks in the unpack's pair order,
+    // (x[w 8 + p], x[w 8 + p + 4]) for word w and pair p, and their sums
+    f16x2 xv[CPL][PPC];
+    float sxv[CPL];
+    const f16x2 one = {static_cast<f16>(1.0f), static_cast<f16>(1.0f)};
+#pragma unroll
+    for (int j = 0; j < CPL; ++j) {
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+            const u32x4 u = act8_to_f16(xraw[j][w], a.act);
+#pragma unroll
+            for (int pp = 0; pp < 4; ++pp) {
+                const uint32_t lo = u[pp / 2], hi = u[(pp + 4) / 2];
+                const uint32_t va = (pp & 1) ? (lo >> 16) : (lo & 0xffff);
+                const uint32_t vb = (pp & 1) ? (hi & 0xffff0000u) : (hi << 16);
+                xv[j][w * HPW + pp] = __builtin_bit_cast(f16x2, va | vb);
+            }
+        }
+        float sum = 0.f;
+#pragma unroll
+        for (int p = 0; p < PPC; ++p) sum = dot2(xv[j][p], one, sum);
+        sxv[j] = sum;
+    }
+    float tv[NBA];
+#pragma unroll
+    for (int m = 0; m < NBA; ++m) tv[m] = NB > 0 && lg + LG * m < rank ? tsh[lg + LG * m] : 0.f;
+
+#pragma unroll
+    for (int u = 0; u < NBW; ++u) {
+        const int b = wave + 4 * u;
+        if (b >= nbatch) break;
+        const Bt& cur = bts[u];
+        int row0, nrows;
+        row_of(b, row0, nrows);
+        float acc[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            acc[r] = 0.f;
+#pragma unroll
+            for (int j = 0; j < CPL; ++j) {
+                float d[NACC];
+#pragma unroll
+                for (int q = 0; q < NACC; ++q) d[q] = 0.f;
+#pragma unroll
+                for (int w = 0; w < 4; ++w) dot_word<4>(cur.q[r][j][w], xv[j] + w * HPW, d);
+                const float v = fmaf(combine<4>(d), 16777216.0f, -f16_bits_to_f32(cur.z[r][j]) * sxv[j]);
+                acc[r] = fmaf(f16_bits_to_f32(cur.s[r][j]) * cmask[j], v, acc[r]);
+            }
+#pragma unroll
+            for (int m = 0; m < NB; ++m) {
+                const float bvm = lg + LG * m < rank ? f16_bits_to_f32(cur.b[r][m]) : 0.f;
+                acc[r] = fmaf(bvm, tv[m], acc[r]);
+            }
+        }
+        const float tot = group_sum_multi<R, LG>(acc);
+        constexpr int SPAN = LG / R;
+        const int rr = (lg / SPAN) & (R - 1);
+        if ((lane & (SPAN - 1)) == 0 && rr < nrows)
+            store_out(L.y, static_cast<size_t>(sl) * L.d_out + row0 + rr, tot, a.out);
     }
 }
 
@@ -892,6 +1146,23 @@ hipError_t launch_moe2(const MoeArgs& a, int lg, int nb, bool hoist, int blocks,
     return launch_moe3<BITS, 64>(a, nb, hoist, blocks, threads, st);
 }
 
+template <int LG, int CPL, int QX>
+hipError_t launch_direct3(const MoeArgs& a, int nb, int blocks, hipStream_t st) {
+    constexpr int NBW = direct_batches(LG, CPL);
+    if (nb == 0) hipLaunchKernelGGL((moe_direct_kernel<LG, CPL, 0, QX, NBW>), dim3(blocks), dim3(256), 0, st, a);
+    else if (nb == 1) hipLaunchKernelGGL((moe_direct_kernel<LG, CPL, 1, QX, NBW>), dim3(blocks), dim3(256), 0, st, a);
+    else hipLaunchKernelGGL((moe_direct_kernel<LG, CPL, 2, QX, NBW>), dim3(blocks), dim3(256), 0, st, a);
+    return hipGetLastError();
+}
+
+// (LG, CPL, QX) instances: 24-32 chunk rows (d_in <= 1024), 64-chunk rows
+// (d_in <= 2048), 128-chunk rows (d_in <= 4096)
+hipError_t launch_direct(const MoeArgs& a, int lg, int cpl, int nb, int qx, int blocks, hipStream_t st) {
+    if (lg == 32) return launch_direct3<32, 1, 2>(a, nb, blocks, st);
+    if (cpl == 1 && qx <= 4) return launch_direct3<64, 1, 4>(a, nb, blocks, st);
+    return launch_direct3<64, 2, 8>(a, nb, blocks, st);
+}
+
 }  // namespace
 
 bool moe_fits(const QW& w, int E, int T, int k) {
@@ -969,6 +1240,23 @@ hipError_t launch_moe_decode(int n, const QW* w, const uint16_t* const* A, const
         blk_end += max_active * L.bpe;
         L.prep_end = prep_end;
         L.blk_end = blk_end;
+    }
+    // few slots, 4-bit codes, rows of at most 4096 codes: the direct path
+    // (one launch, no preparation, no workspace)
+    const int dlg = chunks <= 32 ? 32 : 64;
+    const int dcpl = (chunks + dlg - 1) / dlg;
+    if (bits == 4 && S <= kDirectMaxSlots && dcpl <= 2 && rmax <= 2 * dlg) {
+        a.rb = 16 * (64 / dlg) * direct_batches(dlg, dcpl);
+        int dblk = 0;
+        for (int i = 0; i < n; ++i) {
+            MoeLin& L = a.lin[i];
+            L.nrb = (w[i].d_out + a.rb - 1) / a.rb;
+            dblk += S * L.nrb;
+            L.dblk_end = dblk;
+        }
+        const int dnb = rmax == 0 ? 0 : (rmax <= dlg ? 1 : 2);
+        const int qx = d_in <= 1024 ? 2 : (d_in <= 2048 ? 4 : 8);
+        return launch_direct(a, dlg, dcpl, dnb, qx, dblk, st);
     }
     const int per = lg * a.ks;                     // factor columns per lane pass
     const int nb = rmax == 0 ? 0 : (rmax <= per ? 1 : (rmax <= 2 * per ? 2 : 4));

@@ -340,3 +340,47 @@ def test_out_of_range_ids_are_recorded_and_reported():
         assert e.value.status == cl.CL_EINVAL
         assert "routing id %d in slot 3" % bad_id in str(e.value), str(e.value)
         cl.moe_status()                               # the record was cleared
+
+
+@pytest.mark.parametrize("d_in,G,r_max,d_out", [(512, 128, 16, 100), (768, 64, 48, 333), (2048, 32, 128, 130),
+                                                (4096, 128, 64, 77), (1536, 64, 0, 50)])
+@pytest.mark.parametrize("x_per_slot", [False, True])
+def test_direct_path_few_slots(d_in, G, r_max, d_out, x_per_slot):
+    """At most 8 slots with 4-bit codes take the one-launch path (each
+    workgroup forms its slot's activations and A_e x itself): rows of 16 to
+    128 chunks (32- and 64-lane row sets, one or two chunks per lane), factor
+    columns up to 128 (two per lane), rank 0, ragged row counts; one token
+    of top-8 and two tokens of top-3 with an out-of-range id; static and
+    per-slot ranks; fp16 and bf16 activations."""
+    E = 10
+    Q, s, z, A, B = _oracle_experts(E, d_out, d_in, 4, G, max(r_max, 1), 80 + d_in, svd=False)
+    levels = (0, r_max // 4, r_max // 2, r_max) if r_max else (0,)
+    ranks = wl.moe_expert_ranks(80, 0, d_in, E, levels=levels)
+    ex = _device_experts(Q, s, z, A, B, ranks, d_out, d_in, 4, G, r_max)
+    experts = [(quant.dequant_packed(Q[e], s[e], z[e], 4, G, d_in), A[e], B[e]) for e in range(E)]
+    for (T, k), act in (((1, 8), "fp16"), ((2, 3), "bf16")):
+        ids, w = wl.routing(T, 80, d_in, E, k)
+        if T == 2:
+            ids = ids.copy()
+            ids[1, 2] = E                             # out of range: a zero row
+        x = wl.activation((T, k, d_in) if x_per_slot else (T, d_in), 80, d_in, T, dtype=act)
+        dt = torch.float16 if act == "fp16" else torch.bfloat16
+        got = _run(ex, x.bits, dt, ids, torch.float32, x_per_slot)
+        ref = _full_ref(Q, s, z, A, B, ranks, x.values, ids, x_per_slot, 4, G, d_in)
+        assert_oracle(got, ref)
+        if T == 2:
+            assert (got[1, 2] == 0).all()
+            with pytest.raises(cl.ClError):
+                cl.moe_status()
+        if r_max:
+            valid = np.where((ids >= 0) & (ids < E), ids, 0)
+            slot = wl.dynamic_slot_ranks(valid, w, ranks, levels, r_max)
+            ys = cl.moe_linear_decode_window([ex], dev_u16(x.bits, dt), torch.from_numpy(ids).cuda(),
+                                             out_dtype=torch.float32, slot_ranks=[torch.from_numpy(slot).cuda()])
+            torch.cuda.synchronize()
+            sref = moe.forward(experts, ranks, x.values, valid, x_per_slot, slot_ranks=slot)
+            sref[(ids < 0) | (ids >= E)] = 0.0
+            assert_oracle(out_to_numpy(ys[0]), sref)
+            if T == 2:
+                with pytest.raises(cl.ClError):
+                    cl.moe_status()
