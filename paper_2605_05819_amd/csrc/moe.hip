@@ -593,6 +593,7 @@ __global__ __launch_bounds__(256) void moe_direct_kernel(MoeArgs a) {
     constexpr int NBA = NB > 0 ? NB : 1;
     constexpr int UR = QX > 4 ? 4 : 8;             // rank rows per wave in flight
     __shared__ float tsh[NBA * LG];                // t of the slot, zero past its rank
+    __shared__ int rks[256];                       // the experts' ranks (E <= 256)
     const int blk = blockIdx.x;
     int li = 0;
     while (blk >= a.lin[li].dblk_end) ++li;
@@ -628,6 +629,13 @@ __global__ __launch_bounds__(256) void moe_direct_kernel(MoeArgs a) {
     for (int j = 0; j < CPL; ++j)
 #pragma unroll
         for (int w = 0; w < 4; ++w) xraw[j][w] = *reinterpret_cast<const u32x4*>(xr + (cidx[j] * 4 + w) * 8);
+    // the rank comes with the id: per-slot ranks one word, static ranks the
+    // whole table (thread i its expert i, E <= 256) for an LDS lookup once e
+    // is known; both loads unconditional from selected pointers (a load
+    // under a branch is waited for where the branches meet)
+    const bool rtab = L.r_max > 0 && !L.slot_rank && a.E <= 256;
+    const int rk_tab = (rtab ? L.ranks : a.ids)[rtab ? min(tid, a.E - 1) : 0];
+    const int rk_slot = (L.slot_rank ? L.slot_rank : a.ids)[sl];
     if (e < 0 || e >= a.E) {
         // out-of-range id: this slot's rows are zero, and the device's
         // routing-error record notes it (as the preparation does)
@@ -695,21 +703,20 @@ __global__ __launch_bounds__(256) void moe_direct_kernel(MoeArgs a) {
         xw[q] = *reinterpret_cast<const u32x4*>(xr + (c < a.d_in ? c : 0));
     }
     bool xconv = false;
-    // the rank through one selected pointer (no load under a branch; without
-    // factors any valid word stands in and the rank is 0), used only after
-    // the A x product so that no load waits for it
-    const int32_t* rp = L.r_max == 0 ? a.ids + sl : (L.slot_rank ? L.slot_rank + sl : L.ranks + e);
-    const int rank_raw = *rp;
+    // the slot's rank (the batches' loads are out; the A rows wait for it)
+    rks[tid] = rk_tab;
+    __syncthreads();
+    int rank = L.slot_rank ? rk_slot : (rtab ? rks[e] : (L.r_max > 0 ? L.ranks[e] : 0));
+    rank = L.r_max == 0 ? 0 : (rank < 0 ? 0 : (rank > L.r_max ? L.r_max : rank));
     const uint16_t* Ae = L.A + static_cast<size_t>(e) * L.a_stride;
-    // rows up to r_max, not the rank: the A loads then need not wait for the
-    // rank's load (rows past the rank are dropped below)
-    for (int p0 = 0; wave + 4 * p0 < L.r_max; p0 += UR) {
+    // rows below the rank only
+    for (int p0 = 0; wave + 4 * p0 < rank; p0 += UR) {
         // clamped addresses and selects: the loads carry no branches
         u32x4 av[UR][QX];
 #pragma unroll
         for (int u = 0; u < UR; ++u) {
             const int i = wave + 4 * (p0 + u);
-            const int ic = i < L.r_max ? i : wave;
+            const int ic = i < rank ? i : wave;
 #pragma unroll
             for (int q = 0; q < QX; ++q) {
                 const int c = 512 * q + 8 * lane;
@@ -743,18 +750,10 @@ __global__ __launch_bounds__(256) void moe_direct_kernel(MoeArgs a) {
         const float tot = wave_sum_multi<UR>(d);
         const int u = lane / (64 / UR);
         const int i = wave + 4 * (p0 + u);
-        if (lane % (64 / UR) == 0 && i < L.r_max) tsh[i] = tot;
+        if (lane % (64 / UR) == 0 && i < rank) tsh[i] = tot;
     }
-    for (int i = L.r_max + tid; i < NBA * LG; i += 256) tsh[i] = 0.f;
+    for (int i = rank + tid; i < NBA * LG; i += 256) tsh[i] = 0.f;
     __syncthreads();
-    // the rank masks t and B only here (rows of A past the rank may hold
-    // anything: their products are never used)
-    // (the empty asm takes the loaded word as a vector value here: treated as
-    // uniform, it was moved to a scalar register right after its load, and
-    // that move waited for every load issued before it)
-    int rank_v = rank_raw;
-    asm volatile("" : "+v"(rank_v));
-    const int rank = L.r_max == 0 ? 0 : (rank_v < 0 ? 0 : (rank_v > L.r_max ? L.r_max : rank_v));
     // the activations of this lane's chunks in the unpack's pair order,
     // (x[w 8 + p], x[w 8 + p + 4]) for word w and pair p, and their sums
     f16x2 xv[CPL][PPC];
@@ -780,7 +779,7 @@ __global__ __launch_bounds__(256) void moe_direct_kernel(MoeArgs a) {
     }
     float tv[NBA];
 #pragma unroll
-    for (int m = 0; m < NBA; ++m) tv[m] = NB > 0 && lg + LG * m < rank ? tsh[lg + LG * m] : 0.f;
+    for (int m = 0; m < NBA; ++m) tv[m] = NB > 0 ? tsh[lg + LG * m] : 0.f;
 
 #pragma unroll
     for (int u = 0; u < NBW; ++u) {
