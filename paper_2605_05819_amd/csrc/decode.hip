@@ -260,14 +260,15 @@ struct Batch {
 // NB: factor columns of B per lane (rank <= NB * 64 * ks); 0 when every
 // linear of the window has rank 0.
 // The one-token 4-bit kernel with at most one factor column per lane fits
-// 72 VGPRs without spills: it is held to that (7 waves per SIMD).
+// 72 VGPRs without spills: it is held to that (7 waves per SIMD); its gated
+// instance needs one more and is held to 80 (6 waves per SIMD).
 // GLU: a gated window of two linears with the same d_out (gate, up) launched
 // with one workgroup per batch of the gate, so a workgroup's second batch is
 // the up batch of the same rows: the lanes that hold a gate total keep it and
 // write SiLU(gate) * up for the same row and token to a.h.
 template <int BITS, int NT, int CPL, int R, int NB, bool GLU>
 __global__ __launch_bounds__(512)
-__attribute__((amdgpu_waves_per_eu(BITS == 4 && NT == 1 && CPL == 1 && NB <= 1 ? 7 : 1)))
+__attribute__((amdgpu_waves_per_eu(BITS == 4 && NT == 1 && CPL == 1 && NB <= 1 ? (GLU ? 6 : 7) : 1)))
 void decode_kernel(DecodeArgs a) {
     // a chunk is one lane's unit of codes: 16 bytes = 4 words of 32 / BITS
     // codes at 2 and 4 bits, 3 words = 32 codes at 3 bits
@@ -1059,10 +1060,7 @@ MfmaCfg mfma_cfg(int tiles, int groups) {
 template <bool GLU, int GPB>
 auto pick_cfg(const MfmaCfg& c) {
     constexpr int H = GPB == 1 ? 1 : 2;           // nbuf divisor
-    if (c.tpw == 4 && c.nw == 16) return decode_mfma_kernel<4, 2 / H, GLU, GPB, 16>;
     if (c.tpw == 4) return decode_mfma_kernel<4, 2 / H, GLU, GPB, 4>;
-    if (c.tpw == 2 && c.nw == 8) return decode_mfma_kernel<2, 2 / H, GLU, GPB, 8>;
-    if (c.tpw == 2) return decode_mfma_kernel<2, 2 / H, GLU, GPB, 4>;
     return decode_mfma_kernel<1, 4 / H, GLU, GPB, 4>;
 }
 

@@ -370,8 +370,11 @@ __device__ __forceinline__ float group_sum_multi(float (&v)[R]) {
 
 // Without the hoisted unpack the kernel keeps no next-slot prefetch (it
 // cost 19 VGPRs) and the 4-bit, one-factor-column instance is held to 128
-// VGPRs (4 waves per SIMD, no spills): measured on MI355X, the 48-layer
-// T = 1 and T = 8 steps went from 39.3 and 102.9 us to 37.3 and 94.1 us.
+// VGPRs (4 waves per SIMD): measured on MI355X, the 48-layer T = 1 and
+// T = 8 steps went from 39.3 and 102.9 us to 37.3 and 94.1 us.  The
+// 64-lane instance then keeps one register in scratch (one store and one
+// load per wave); held to 168 VGPRs instead (3 waves per SIMD) it has none,
+// but the T = 8 step takes 79.7 us against 75.1.
 //
 // LG: lanes per row set.  Rows of at least 64 chunks use the whole wave
 // (LG = 64); shorter rows (the 768-wide down projection: 24 chunks) give
