@@ -147,6 +147,13 @@ cl_status cl_build_compensation(const float* W, const cl_qweight* w, int32_t r_m
 size_t cl_build_compensation_workspace(int32_t d_out, int32_t d_in, int32_t r_max);
 
 /*
+ * Jacobi sweeps the calling thread's last cl_build_compensation call ran
+ * (including the final sweep without rotations; 0 before any call).  A
+ * report of the eigensolver's work, for timing and tuning.
+ */
+int32_t cl_build_compensation_sweeps(void);
+
+/*
  * cl_linear_workspace -- bytes of device workspace that cl_linear_decode needs
  * for this weight, factor set (NULL for none) and token count.  Returns 0 for
  * arguments cl_linear_decode would reject.

@@ -59,6 +59,7 @@ _SIGNATURES = {
                                            ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32,
                                            ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
     "cl_build_compensation_workspace": (ctypes.c_size_t, [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32]),
+    "cl_build_compensation_sweeps": (ctypes.c_int32, []),
     "cl_build_compensation": (ctypes.c_int32, [ctypes.c_void_p, ctypes.POINTER(QWeightC), ctypes.c_int32,
                                                ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                                ctypes.c_size_t, ctypes.c_void_p]),
@@ -562,6 +563,12 @@ def moe_status(stream=None):
     (CL_EINVAL) if a MoE call on this device met a routing id outside
     0..E-1 since the last check (the record is cleared)."""
     _check(lib().cl_moe_status(_stream(stream)))
+
+
+def build_compensation_sweeps():
+    """``cl_build_compensation_sweeps``: Jacobi sweeps of this thread's last
+    :func:`build_compensation` call."""
+    return int(lib().cl_build_compensation_sweeps())
 
 
 def build_compensation(W, w, r_max, stream=None):

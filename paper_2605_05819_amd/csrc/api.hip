@@ -16,6 +16,8 @@
 namespace {
 
 thread_local char g_err[512] = "no error";
+// Jacobi sweeps of the calling thread's last cl_build_compensation call
+thread_local int g_last_sweeps = 0;
 
 cl_status fail(cl_status code, const char* fmt, ...) {
     va_list ap;
@@ -99,6 +101,8 @@ cl_status cl_dequantize(const cl_qweight* w, float* W_hat, void* stream) {
     return hip_status(cl::launch_dequantize(qw, W_hat, static_cast<hipStream_t>(stream)), who);
 }
 
+int32_t cl_build_compensation_sweeps(void) { return g_last_sweeps; }
+
 size_t cl_build_compensation_workspace(int32_t d_out, int32_t d_in, int32_t r_max) {
     const int n = d_in <= d_out ? d_in : d_out;
     if (d_out < 1 || d_in < 1 || r_max < 0 || r_max > 256 || r_max > n || !cl::comp_fits(d_out, d_in)) return 0;
@@ -127,6 +131,8 @@ cl_status cl_build_compensation(const float* W, const cl_qweight* w, int32_t r_m
     int sweeps = 0;
     const hipError_t e = cl::launch_build_compensation(W, qw, r_max, A, B, sigma, ws,
                                                        static_cast<hipStream_t>(stream), &sweeps);
+    // the loop stops at the first sweep without rotations: count it
+    g_last_sweeps = e == hipSuccess ? sweeps + 1 : sweeps;
     if (e == hipErrorNotReady)
         return fail(CL_EUNSUPPORTED, "%s: the Jacobi eigensolver did not converge in %d sweeps", who, sweeps);
     return hip_status(e, who);
