@@ -68,8 +68,11 @@ constexpr int direct_batches(int lg, int cpl) { return cpl == 2 ? 2 : (lg == 64 
 // need order (scales and zeros, slot ids, code blocks): 8 x 1 166 us per
 // layer, 4 x 2 191, 8 x 2 229, 12 x 1 230, 16 x 1 227 (with the code loads
 // issued after the scale/zero copy: 4 x 2 213 us; one tile of 16 rows had
-// taken 389, every workgroup re-reading its slots' activations).
-constexpr int kMoeTpw = 8;
+// taken 389, every workgroup re-reading its slots' activations).  Once the
+// pipeline's tail stopped re-reading code blocks: 4 x 1 143.7 us, 8 x 1
+// 150.5, 2 x 1 153.0, 6 x 1 161.7, 4 x 2 ~160 (165 VGPRs at 4 x 1: three
+// waves per SIMD against two).
+constexpr int kMoeTpw = 4;
 constexpr int kMoeNbuf = 1;
 
 // One linear of a window: its stacked experts and its share of the grids.
@@ -138,27 +141,30 @@ __global__ __launch_bounds__(256) void moe_prep_kernel(MoeArgs a) {
         const int local = blk - (li ? a.lin[li - 1].prep_end : 0);
         const int j = local / L.rq;
         const int quad = local - j * L.rq;
-        // slots per expert (LDS atomics contend only within one expert)
-        // the ranks are loaded together with the ids: the selected expert's
-        // rank then costs no further memory round trip
-        // the ranks and the routing ids are loaded in one round trip (their
-        // loads are issued before either is stored); the histogram is
-        // cleared meanwhile
+        // The experts' ranks, the routing ids and the per-slot ranks are
+        // loaded in one round trip: every load is unconditional (clamped
+        // index, out-of-range values replaced afterwards), so none waits at
+        // a branch for the ones before it.  The histogram is cleared
+        // meanwhile.
         for (int i = tid; i < a.E; i += 256) hist[i] = 0;
         if (tid == 0) sel = -1;
         constexpr int kPer = kMaxExperts / 256;       // experts and slots per thread, at most
-        int rkv[kPer], idv[kPer];
+        const bool dyn = L.slot_rank != nullptr;
+        const int32_t* rsrc = L.r_max > 0 ? L.ranks : a.ids;    // ranks may be null when r_max is 0
+        const int32_t* ssrc = dyn ? L.slot_rank : a.ids;
+        int rkv[kPer], idv[kPer], srv[kPer];
 #pragma unroll
         for (int u = 0; u < kPer; ++u) {
             const int i = tid + 256 * u;
-            rkv[u] = (L.r_max > 0 && i < a.E) ? L.ranks[i] : 0;   // ranks may be null when r_max is 0
-            idv[u] = i < S ? a.ids[i] : -1;
+            rkv[u] = rsrc[min(i, a.E - 1)];
+            idv[u] = a.ids[min(i, S - 1)];
+            srv[u] = ssrc[min(i, S - 1)];
         }
         __syncthreads();
 #pragma unroll
         for (int u = 0; u < kPer; ++u) {
             const int i = tid + 256 * u;
-            if (i < a.E) rk[i] = rkv[u];
+            if (i < a.E) rk[i] = L.r_max > 0 ? rkv[u] : 0;
             if (i < S) {
                 sids[i] = idv[u];
                 if (idv[u] >= 0 && idv[u] < a.E) atomicAdd(&hist[idv[u]], 1);
@@ -225,12 +231,13 @@ __global__ __launch_bounds__(256) void moe_prep_kernel(MoeArgs a) {
         rank = rank < 0 ? 0 : (rank > L.r_max ? L.r_max : rank);
         // per-slot ranks: the expert's rank here is the largest of its slots'
         // (A_e x is computed that far; each slot reads its own prefix)
-        const bool dyn = L.slot_rank != nullptr;
         if (dyn && tid == 0) srank = 0;
         // this expert's slots in slot order (ballots, 256 slots per pass)
         int base_pos = 0;
-        for (int b0 = 0; b0 < S; b0 += 256) {
-            const int sl = b0 + tid;
+#pragma unroll
+        for (int u = 0; u < kPer; ++u) {
+            if (256 * u >= S) break;
+            const int sl = 256 * u + tid;
             const bool mine = sl < S && sids[sl] == e;
             const unsigned long long m = __ballot(mine);
             if (lane == 0) wcnt[wave] = __popcll(m);
@@ -245,7 +252,7 @@ __global__ __launch_bounds__(256) void moe_prep_kernel(MoeArgs a) {
                 }
                 mys[pos] = sl;
                 if (dyn) {
-                    const int rs = L.slot_rank[sl];
+                    const int rs = srv[u];
                     atomicMax(&srank, rs < 0 ? 0 : (rs > L.r_max ? L.r_max : rs));
                 }
             }
@@ -892,13 +899,19 @@ __global__ __launch_bounds__(256) void moe_mfma_kernel(MoeArgs a) {
     // words it feeds to MFMA step t: 4 g + t of the block, or 4 t + g once
     // the codes are transposed (a word past K reads word g, met by a zero
     // scale).  Loads are unconditional (clamped addresses) and nothing
-    // consumes a loaded value before compute.
+    // consumes a loaded value before compute.  A block past the last one
+    // (the pipeline's tail) reads one line, the expert's first 16 bytes, on
+    // every lane: reloading a block already computed fetched its lines from
+    // HBM a second time (the streamed code lines have left L2 by then; the
+    // down linear's 6 blocks on 4 waves had fetched 2.25 times its bytes).
     auto load_w = [&](int kb, Blk& b) {
+        const bool live = kb < nkb;
         const int wi = min(kb * 16 + 4 * g, words_row - 4);
 #pragma unroll
         for (int j = 0; j < TPW; ++j)
             b.w[j] = __builtin_nontemporal_load(
-                reinterpret_cast<const u32x4*>(qe + static_cast<size_t>(row[j]) * words_row + wi));
+                live ? reinterpret_cast<const u32x4*>(qe + static_cast<size_t>(row[j]) * words_row + wi)
+                     : reinterpret_cast<const u32x4*>(qe));
     };
     auto load_x = [&](int kb, Blk& b, const u32x4* xr) {
         const int wi = min(kb * 16 + 4 * g, words_row - 4);
@@ -972,7 +985,7 @@ __global__ __launch_bounds__(256) void moe_mfma_kernel(MoeArgs a) {
     const int rounds = (nkb + SPAN - 1) / SPAN;
     Blk b[NBUF];
 #pragma unroll
-    for (int j = 0; j < NBUF; ++j) load_w(wave + 4 * j < nkb ? wave + 4 * j : 0, b[j]);
+    for (int j = 0; j < NBUF; ++j) load_w(wave + 4 * j, b[j]);
     if (tid < n16) {
         reinterpret_cast<u32x4*>(szl)[tid] = s_first;
         reinterpret_cast<u32x4*>(zl)[tid] = z_first;
@@ -992,7 +1005,7 @@ __global__ __launch_bounds__(256) void moe_mfma_kernel(MoeArgs a) {
             // a later pass of 16 slots: its slots and its first code round
             sl = a.sorted[sbeg + (p0 + r < scnt ? p0 + r : 0)];
 #pragma unroll
-            for (int j = 0; j < NBUF; ++j) load_w(wave + 4 * j < nkb ? wave + 4 * j : 0, b[j]);
+            for (int j = 0; j < NBUF; ++j) load_w(wave + 4 * j, b[j]);
         }
         // this lane's slot (MFMA row r of the activations); absent slots read
         // a present one and are masked to zero
@@ -1045,9 +1058,8 @@ __global__ __launch_bounds__(256) void moe_mfma_kernel(MoeArgs a) {
                 const int kb = wave + SPAN * rd + 4 * j;
                 compute(kb, b[j]);
                 const int kn = kb + SPAN;
-                const int kl = kn < nkb ? kn : (kb < nkb ? kb : 0);
-                load_w(kl, b[j]);
-                load_x(kl, b[j], xr);
+                load_w(kn, b[j]);
+                load_x(kn < nkb ? kn : 0, b[j], xr);
             }
         }
         // rank-r term: 32 factor columns per step, wave w taking steps w, w + 4
