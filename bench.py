@@ -352,7 +352,8 @@ def bench_moe(torch, cl, wl, timer, dev):
     """48 stacked MoE layers (128 experts, gate/up 768 x 2048, down
     2048 x 768, 4-bit g128, per-expert ranks from {0, 8, 16, 32}), top-8
     routing: per layer gate and up as one window on the token's input, down
-    on each slot's input.  Codes, scales and factors of the stacked experts are seeded random
+    on each slot's input; and the same layers chained as in a model (down on
+    SiLU(gate) * up of the window's outputs, formed by the gated down call).  Codes, scales and factors of the stacked experts are seeded random
     device data (the cost does not depend on the values).  GB/s counts only the
     routed experts' bytes."""
     L, E, K = wl.MOE_LAYERS, wl.MOE_EXPERTS, wl.MOE_TOPK
@@ -382,6 +383,7 @@ def bench_moe(torch, cl, wl, timer, dev):
         ys = {n: torch.empty((T, K, wl.MOE_SHAPES[n][0]), dtype=torch.float16, device=dev) for n, _ in mats}
         ws_gu = cl.workspace(cl.moe_window_workspace([layers["gate"][0], layers["up"][0]], T, K, False), dev)
         ws_dn = cl.workspace(cl.moe_workspace(layers["down"][0], T, K, True), dev)
+        ws_gd = cl.workspace(cl.moe_gated_workspace(layers["down"][0], T, K), dev)
 
         def run():
             # gate and up share the token's input and routing: one window
@@ -390,8 +392,17 @@ def bench_moe(torch, cl, wl, timer, dev):
                                             ys=[ys["gate"], ys["up"]], ws=ws_gu, stream=timer.stream)
                 cl.moe_linear_decode(layers["down"][l], xs["down"], ids[l], y=ys["down"], ws=ws_dn,
                                      stream=timer.stream)
+        def chain():
+            # the FFN as it runs in a model: the gate/up window's outputs feed
+            # the down call, which forms SiLU(gate) * up as it reads them
+            for l in range(L):
+                cl.moe_linear_decode_window([layers["gate"][l], layers["up"][l]], xs["gate"], ids[l],
+                                            ys=[ys["gate"], ys["up"]], ws=ws_gu, stream=timer.stream)
+                cl.moe_linear_decode_gated(layers["down"][l], ys["gate"], ys["up"], ids[l], y=ys["down"], ws=ws_gd,
+                                           stream=timer.stream)
         g = timer.capture(run)
         us = timer.time([g], 10) * 1e3
+        us_chain = timer.time([timer.capture(chain)], 10) * 1e3
         nbytes = 0
         for l in range(L):
             routed = np.unique(ids[l].cpu().numpy())
@@ -402,7 +413,7 @@ def bench_moe(torch, cl, wl, timer, dev):
                     nbytes += d_out * d_in // 2 + 4 * d_out * (d_in // 128) + 2 * int(rk[e]) * (d_in + d_out)
                 nbytes += 2 * xs[n].numel() + 2 * ys[n].numel()
         res["T%d" % T] = {"us_per_layer": round(us / L, 2), "gbs": round(nbytes / us / 1e3, 1),
-                          "bytes_per_layer": nbytes // L}
+                          "bytes_per_layer": nbytes // L, "gated_chain_us_per_layer": round(us_chain / L, 2)}
     return res
 
 

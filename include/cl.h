@@ -385,6 +385,43 @@ size_t cl_moe_window_workspace(int32_t n, const cl_qweight* w_expert0, const int
                                int32_t num_experts, int32_t T, int32_t k, int32_t x_per_slot);
 
 /*
+ * cl_moe_linear_decode_gated -- the down projection of a MoE layer applied to
+ * the experts' gated activations: for every slot (t, j) with e = ids[t][j],
+ *     h = SiLU(g[t][j]) * u[t][j]  (elementwise, SiLU(v) = v / (1 + e^-v)),
+ *     y[t][j] = deq(Q_e) h + B_e[:, :r] (A_e[:r] h),
+ * with g and u the slot's gate and up outputs (cl_moe_linear_decode_window
+ * over the gate and up linears with fp16 or bf16 outputs).  The expert
+ * nonlinearity between the gate/up and down windows of the cross-expert
+ * reorganisation (Section 4.2.2; Appendix A.1, MoE Layer) is formed by the
+ * down call: with few slots (the one-launch path of cl_moe_linear_decode) as
+ * each workgroup reads its activations, otherwise by one small kernel that
+ * writes h for every slot into the workspace ahead of the preparation and
+ * backbone kernels.  Each h is computed in fp32, saturated at +-65504 and
+ * rounded to fp16, the activation precision of every decode path.
+ *
+ *  g, u       device [T][k][d_in] of act_dtype (fp16 or bf16), 16-byte
+ *             aligned; d_in is the down projection's input (the FFN width)
+ *  slot_ranks device int32 [T][k] per-slot ranks (clamped to 0..r_max) used in
+ *             place of ranks[e], or NULL
+ *  ws         device workspace of cl_moe_gated_workspace(w_expert0, r_max, E,
+ *             T, k) bytes, 256-byte aligned
+ * Everything else, the limits and the routing-error record are as for
+ * cl_moe_linear_decode with x_per_slot = 1.
+ * Errors: as cl_moe_linear_decode; CL_EINVAL for a null g or u.
+ */
+cl_status cl_moe_linear_decode_gated(const cl_qweight* w_expert0, const uint16_t* A, const uint16_t* B,
+                                     int32_t r_max, const int32_t* ranks, const int32_t* slot_ranks,
+                                     int32_t num_experts, const void* g, const void* u, const int32_t* topk_ids,
+                                     int32_t T, int32_t k, int32_t act_dtype, void* y, int32_t out_dtype, void* ws,
+                                     size_t ws_bytes, void* stream);
+
+/* Workspace bytes for cl_moe_linear_decode_gated: those of the down call with
+ * per-slot activations plus T * k * d_in fp16 values (0 for rejected
+ * arguments). */
+size_t cl_moe_gated_workspace(const cl_qweight* w_expert0, int32_t r_max, int32_t num_experts, int32_t T,
+                              int32_t k);
+
+/*
  * cl_allocate_ranks -- compensation ranks of the n linears of one
  * compensation window from their residual spectra (host code; no GPU).
  * Section 4.3.1 (intrinsic recoverability), Section 4.3.4 (priority and

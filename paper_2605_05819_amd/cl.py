@@ -70,6 +70,13 @@ _SIGNATURES = {
                                               ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
                                               ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p,
                                               ctypes.c_size_t, ctypes.c_void_p]),
+    "cl_moe_linear_decode_gated": (ctypes.c_int32, [ctypes.POINTER(QWeightC), ctypes.c_void_p, ctypes.c_void_p,
+                                                    ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
+                                                    ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
+                                                    ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32,
+                                                    ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
+    "cl_moe_gated_workspace": (ctypes.c_size_t, [ctypes.POINTER(QWeightC), ctypes.c_int32, ctypes.c_int32,
+                                                  ctypes.c_int32, ctypes.c_int32]),
     "cl_moe_window_workspace": (ctypes.c_size_t, [ctypes.c_int32, ctypes.POINTER(QWeightC), ctypes.c_void_p,
                                                   ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32]),
     "cl_moe_linear_decode_window": (ctypes.c_int32, [ctypes.c_int32, ctypes.POINTER(QWeightC), ctypes.c_void_p,
@@ -506,6 +513,42 @@ def moe_linear_decode(ex, x, topk_ids, out_dtype=torch.float16, y=None, ws=None,
                                       ex.num_experts, _ptr(x), int(x_per_slot), _ptr(topk_ids), T, k,
                                       _DTYPE_CODE[x.dtype], _ptr(y), _DTYPE_CODE[y.dtype], _ptr(ws), ws.numel(),
                                       _stream(stream)))
+    return y
+
+
+def moe_gated_workspace(ex, T, k):
+    q0 = ex.expert0()
+    return lib().cl_moe_gated_workspace(ctypes.byref(q0), ex.r_max, ex.num_experts, T, k)
+
+
+def moe_linear_decode_gated(ex, g, u, topk_ids, out_dtype=torch.float16, y=None, ws=None, stream=None,
+                            slot_ranks=None):
+    """``cl_moe_linear_decode_gated``: the down projection of SiLU(g) * u,
+    with g and u the slots' gate and up outputs [T][k][d_in] (fp16 or bf16,
+    one dtype), topk_ids int32 [T][k] -> y [T][k][d_out].  ``slot_ranks``:
+    None or a device int32 [T][k] tensor used in place of the experts'
+    ranks."""
+    _need(isinstance(topk_ids, torch.Tensor) and topk_ids.dim() == 2, "topk_ids must be a [T][k] tensor")
+    T, k = topk_ids.shape
+    _need(isinstance(g, torch.Tensor) and isinstance(u, torch.Tensor) and g.dim() == 3 and
+          tuple(u.shape) == tuple(g.shape) and u.dtype == g.dtype, "g and u must be [T][k][d_in] of one dtype")
+    if y is None:
+        y = torch.empty((T, k, ex.d_out), dtype=out_dtype, device=g.device)
+    chk = _Checked()
+    _check_moe_inputs([ex], g, topk_ids, [y], chk)
+    _check_act(u, chk, "u", ex.d_in)
+    if slot_ranks is not None:
+        _dev_tensor(slot_ranks, "slot_ranks", _I32, (T, k), chk)
+    chk.on_gpu()
+    need = moe_gated_workspace(ex, T, k)
+    if ws is None:
+        ws = workspace(need, g.device)
+    _check_ws(ws, need, None)
+    q0 = ex.expert0()
+    _check(lib().cl_moe_linear_decode_gated(ctypes.byref(q0), _ptr(ex.A), _ptr(ex.B), ex.r_max, _ptr(ex.ranks),
+                                            _ptr(slot_ranks), ex.num_experts, _ptr(g), _ptr(u), _ptr(topk_ids), T,
+                                            k, _DTYPE_CODE[g.dtype], _ptr(y), _DTYPE_CODE[y.dtype], _ptr(ws),
+                                            ws.numel(), _stream(stream)))
     return y
 
 

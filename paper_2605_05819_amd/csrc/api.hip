@@ -314,7 +314,7 @@ namespace {
 // one activation tensor (same d_in, bits and group size).
 cl_status moe_common(int32_t n, const cl_qweight* w, const uint16_t* const* A, const uint16_t* const* B,
                      const int32_t* r_max, const int32_t* const* ranks, const int32_t* const* slot_ranks,
-                     int32_t num_experts, const void* x,
+                     int32_t num_experts, const void* x, const void* u,
                      int32_t x_per_slot, const int32_t* topk_ids, int32_t T, int32_t k, int32_t act_dtype,
                      void* const* y, int32_t out_dtype, void* ws, size_t ws_bytes, void* stream, const char* who) {
     if (n < 1 || n > 4) return fail(CL_EINVAL, "%s: n must be in 1..4 (got %d)", who, n);
@@ -351,12 +351,13 @@ cl_status moe_common(int32_t n, const cl_qweight* w, const uint16_t* const* A, c
         return fail(CL_EINVAL, "%s: out_dtype must be CL_FP16, CL_BF16 or CL_FP32", who);
     if (!x) return fail(CL_EINVAL, "%s: null x", who);
     if (!aligned(x, 16)) return fail(CL_EINVAL, "%s: x must be 16-byte aligned", who);
-    const int xs = x_per_slot ? 1 : 0;
+    if (u && !aligned(u, 16)) return fail(CL_EINVAL, "%s: u must be 16-byte aligned", who);
+    const int xs = u ? 2 : (x_per_slot ? 1 : 0);       // 2: gated per-slot input
     const size_t need = cl::moe_workspace_bytes(n, qw, rm, num_experts, T, k, xs);
     if (!ws || ws_bytes < need)
         return fail(CL_EWORKSPACE, "%s: workspace of %zu bytes needed (got %zu)", who, need, ws ? ws_bytes : 0);
     if (!aligned(ws, 256)) return fail(CL_EINVAL, "%s: workspace must be 256-byte aligned", who);
-    return hip_status(cl::launch_moe_decode(n, qw, A, B, rm, ranks, slot_ranks, num_experts, x, xs, topk_ids, T, k,
+    return hip_status(cl::launch_moe_decode(n, qw, A, B, rm, ranks, slot_ranks, num_experts, x, u, xs, topk_ids, T, k,
                                             act_dtype,
                                             y, out_dtype, ws, static_cast<hipStream_t>(stream)),
                       who);
@@ -376,7 +377,7 @@ size_t moe_ws(int32_t n, const cl_qweight* w, const int32_t* r_max, int32_t num_
         rm[i] = ok ? r_max[i] : 0;
     }
     if (ok && cl::moe_fits(qw[0], num_experts, T, k))
-        bytes = cl::moe_workspace_bytes(n, qw, rm, num_experts, T, k, x_per_slot ? 1 : 0);
+        bytes = cl::moe_workspace_bytes(n, qw, rm, num_experts, T, k, x_per_slot);
     memcpy(g_err, saved, sizeof(g_err));
     return bytes;
 }
@@ -387,20 +388,36 @@ extern "C" {
 
 size_t cl_moe_workspace(const cl_qweight* w_expert0, int32_t r_max, int32_t num_experts, int32_t T, int32_t k,
                         int32_t x_per_slot) {
-    return moe_ws(1, w_expert0, &r_max, num_experts, T, k, x_per_slot);
+    return moe_ws(1, w_expert0, &r_max, num_experts, T, k, x_per_slot ? 1 : 0);
+}
+
+size_t cl_moe_gated_workspace(const cl_qweight* w_expert0, int32_t r_max, int32_t num_experts, int32_t T,
+                              int32_t k) {
+    return moe_ws(1, w_expert0, &r_max, num_experts, T, k, 2);
 }
 
 size_t cl_moe_window_workspace(int32_t n, const cl_qweight* w_expert0, const int32_t* r_max, int32_t num_experts,
                                int32_t T, int32_t k, int32_t x_per_slot) {
-    return moe_ws(n, w_expert0, r_max, num_experts, T, k, x_per_slot);
+    return moe_ws(n, w_expert0, r_max, num_experts, T, k, x_per_slot ? 1 : 0);
 }
 
 cl_status cl_moe_linear_decode(const cl_qweight* w_expert0, const uint16_t* A, const uint16_t* B, int32_t r_max,
                                const int32_t* ranks, int32_t num_experts, const void* x, int32_t x_per_slot,
                                const int32_t* topk_ids, int32_t T, int32_t k, int32_t act_dtype, void* y,
                                int32_t out_dtype, void* ws, size_t ws_bytes, void* stream) {
-    return moe_common(1, w_expert0, &A, &B, &r_max, &ranks, nullptr, num_experts, x, x_per_slot, topk_ids, T, k,
-                      act_dtype, &y, out_dtype, ws, ws_bytes, stream, "cl_moe_linear_decode");
+    return moe_common(1, w_expert0, &A, &B, &r_max, &ranks, nullptr, num_experts, x, nullptr, x_per_slot, topk_ids,
+                      T, k, act_dtype, &y, out_dtype, ws, ws_bytes, stream, "cl_moe_linear_decode");
+}
+
+cl_status cl_moe_linear_decode_gated(const cl_qweight* w_expert0, const uint16_t* A, const uint16_t* B,
+                                     int32_t r_max, const int32_t* ranks, const int32_t* slot_ranks,
+                                     int32_t num_experts, const void* g, const void* u, const int32_t* topk_ids,
+                                     int32_t T, int32_t k, int32_t act_dtype, void* y, int32_t out_dtype, void* ws,
+                                     size_t ws_bytes, void* stream) {
+    const char* who = "cl_moe_linear_decode_gated";
+    if (!g || !u) return fail(CL_EINVAL, "%s: null g or u", who);
+    return moe_common(1, w_expert0, &A, &B, &r_max, &ranks, &slot_ranks, num_experts, g, u, 1, topk_ids, T, k,
+                      act_dtype, &y, out_dtype, ws, ws_bytes, stream, who);
 }
 
 cl_status cl_moe_linear_decode_window(int32_t n, const cl_qweight* w_expert0, const uint16_t* const* A,
@@ -409,8 +426,8 @@ cl_status cl_moe_linear_decode_window(int32_t n, const cl_qweight* w_expert0, co
                                       int32_t x_per_slot,
                                       const int32_t* topk_ids, int32_t T, int32_t k, int32_t act_dtype,
                                       void* const* y, int32_t out_dtype, void* ws, size_t ws_bytes, void* stream) {
-    return moe_common(n, w_expert0, A, B, r_max, ranks, slot_ranks, num_experts, x, x_per_slot, topk_ids, T, k,
-                      act_dtype, y, out_dtype, ws, ws_bytes, stream, "cl_moe_linear_decode_window");
+    return moe_common(n, w_expert0, A, B, r_max, ranks, slot_ranks, num_experts, x, nullptr, x_per_slot, topk_ids,
+                      T, k, act_dtype, y, out_dtype, ws, ws_bytes, stream, "cl_moe_linear_decode_window");
 }
 
 cl_status cl_linear_decode_window(int32_t n, const cl_qweight* w, const cl_lowrank* c, const void* x,

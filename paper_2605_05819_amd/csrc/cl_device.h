@@ -90,6 +90,28 @@ __device__ __forceinline__ float act_to_f32(uint16_t b, int act) {
 // the result a signed zero
 __device__ __forceinline__ float silu_mul(float g, float u) { return __fdividef(g, 1.f + __expf(-g)) * u; }
 
+// 8 gated activations h = SiLU(g) u from one 16-byte load of each input
+// (fp16 or bf16, natural order) as fp16: each product in fp32, saturated at
+// +-65504 like a converted bf16 activation, then rounded to nearest even.
+__device__ __forceinline__ u32x4 gated8_to_f16(u32x4 g, u32x4 u, int act) {
+    u32x4 o;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const uint32_t gk = g[k], uk = u[k];
+        float h0 = silu_mul(act_to_f32(static_cast<uint16_t>(gk & 0xffff), act),
+                            act_to_f32(static_cast<uint16_t>(uk & 0xffff), act));
+        float h1 = silu_mul(act_to_f32(static_cast<uint16_t>(gk >> 16), act),
+                            act_to_f32(static_cast<uint16_t>(uk >> 16), act));
+        h0 = fminf(fmaxf(h0, -65504.0f), 65504.0f);
+        h1 = fminf(fmaxf(h1, -65504.0f), 65504.0f);
+        f16x2 h;
+        h.x = static_cast<f16>(h0);
+        h.y = static_cast<f16>(h1);
+        o[k] = __builtin_bit_cast(uint32_t, h);
+    }
+    return o;
+}
+
 __device__ __forceinline__ void store_out(void* y, size_t idx, float v, int out) {
     if (out == DT_FP32) {
         static_cast<float*>(y)[idx] = v;

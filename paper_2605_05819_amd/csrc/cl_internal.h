@@ -55,7 +55,7 @@ bool moe_fits(const QW& w, int E, int T, int k);
 size_t moe_workspace_bytes(int n, const QW* w, const int* r_max, int E, int T, int k, int x_per_slot);
 hipError_t launch_moe_decode(int n, const QW* w, const uint16_t* const* A, const uint16_t* const* B,
                              const int* r_max, const int32_t* const* ranks, const int32_t* const* slot_ranks,
-                             int E, const void* x, int x_per_slot,
+                             int E, const void* x, const void* u, int x_per_slot,
                              const int32_t* ids, int T, int k, int act, void* const* y, int out, void* ws,
                              hipStream_t st);
 

@@ -102,6 +102,7 @@ struct MoeArgs {
     int n;
     const int32_t* ids;
     const uint16_t* x;
+    const uint16_t* u;       // gated input: the activations are SiLU(x) u elementwise (null: x)
     int E, T, k, d_in, G, act, out, x_per_slot;
     // workspace
     int* n_active;
@@ -597,7 +598,17 @@ void moe_kernel(MoeArgs a) {
 // token with 8 routed experts this replaces the preparation launch and its
 // dependent memory round trips (ids, A_e rows, then the backbone's reads of
 // t and the activations).
-template <int LG, int CPL, int NB, int QX, int NBW>
+// The gated activations h = SiLU(g) u of every slot, 8 per thread, as fp16:
+// the input of the preparation and backbone kernels for a gated call.
+__global__ __launch_bounds__(256) void moe_gate_kernel(const uint16_t* g, const uint16_t* u, uint16_t* h, size_t n8,
+                                                       int act) {
+    const size_t i = static_cast<size_t>(blockIdx.x) * 256 + threadIdx.x;
+    if (i >= n8) return;
+    reinterpret_cast<u32x4*>(h)[i] =
+        gated8_to_f16(reinterpret_cast<const u32x4*>(g)[i], reinterpret_cast<const u32x4*>(u)[i], act);
+}
+
+template <int LG, int CPL, int NB, int QX, int NBW, bool GATED>
 __global__ __launch_bounds__(256) void moe_direct_kernel(MoeArgs a) {
     constexpr int R = 4, CPC = 32, PPC = 16, HPW = 4, NACC = 2;
     constexpr int SETS = 64 / LG;
@@ -647,6 +658,16 @@ __global__ __launch_bounds__(256) void moe_direct_kernel(MoeArgs a) {
     for (int j = 0; j < CPL; ++j)
 #pragma unroll
         for (int w = 0; w < 4; ++w) xraw[j][w] = *reinterpret_cast<const u32x4*>(xr + (cidx[j] * 4 + w) * 8);
+    // gated input: the up rows beside the gate rows, SiLU(g) u formed at
+    // the conversions below
+    const uint16_t* ur = GATED ? a.u + static_cast<size_t>(xrow) * a.d_in : xr;
+    u32x4 uraw[GATED ? CPL : 1][4];
+    if constexpr (GATED) {
+#pragma unroll
+        for (int j = 0; j < CPL; ++j)
+#pragma unroll
+            for (int w = 0; w < 4; ++w) uraw[j][w] = *reinterpret_cast<const u32x4*>(ur + (cidx[j] * 4 + w) * 8);
+    }
     // the rank comes with the id: per-slot ranks one word, static ranks the
     // whole table (thread i its expert i, E <= 256) for an LDS lookup once e
     // is known; both loads unconditional from selected pointers (a load
@@ -714,11 +735,12 @@ __global__ __launch_bounds__(256) void moe_direct_kernel(MoeArgs a) {
     // t = A_e[:rank] x: x as fp16 runs, lane l and pass q holding columns
     // 512 q + 8 l .. + 7
     // raw loads now, the conversion after the A loads are out
-    u32x4 xw[QX];
+    u32x4 xw[QX], uw[GATED ? QX : 1];
 #pragma unroll
     for (int q = 0; q < QX; ++q) {
         const int c = 512 * q + 8 * lane;
         xw[q] = *reinterpret_cast<const u32x4*>(xr + (c < a.d_in ? c : 0));
+        if constexpr (GATED) uw[q] = *reinterpret_cast<const u32x4*>(ur + (c < a.d_in ? c : 0));
     }
     bool xconv = false;
     // the slot's rank (the batches' loads are out; the A rows wait for it)
@@ -746,8 +768,12 @@ __global__ __launch_bounds__(256) void moe_direct_kernel(MoeArgs a) {
         __builtin_amdgcn_sched_barrier(0);
         if (!xconv) {
 #pragma unroll
-            for (int q = 0; q < QX; ++q)
-                xw[q] = 512 * q + 8 * lane < a.d_in ? act8_to_f16(xw[q], a.act) : u32x4{0u, 0u, 0u, 0u};
+            for (int q = 0; q < QX; ++q) {
+                u32x4 v;
+                if constexpr (GATED) v = gated8_to_f16(xw[q], uw[q], a.act);
+                else v = act8_to_f16(xw[q], a.act);
+                xw[q] = 512 * q + 8 * lane < a.d_in ? v : u32x4{0u, 0u, 0u, 0u};
+            }
             xconv = true;
         }
         float d[UR];
@@ -781,7 +807,9 @@ __global__ __launch_bounds__(256) void moe_direct_kernel(MoeArgs a) {
     for (int j = 0; j < CPL; ++j) {
 #pragma unroll
         for (int w = 0; w < 4; ++w) {
-            const u32x4 u = act8_to_f16(xraw[j][w], a.act);
+            u32x4 u;
+            if constexpr (GATED) u = gated8_to_f16(xraw[j][w], uraw[j][w], a.act);
+            else u = act8_to_f16(xraw[j][w], a.act);
 #pragma unroll
             for (int pp = 0; pp < 4; ++pp) {
                 const uint32_t lo = u[pp / 2], hi = u[(pp + 4) / 2];
@@ -1119,7 +1147,7 @@ __global__ __launch_bounds__(256) void moe_mfma_kernel(MoeArgs a) {
 size_t up256(size_t n) { return (n + 255) / 256 * 256; }
 
 struct MoeLayout {
-    size_t n_active, table, sorted, t[kMaxMoeWin], xp, sx, total;
+    size_t n_active, table, sorted, t[kMaxMoeWin], xp, sx, h, total;
 };
 
 MoeLayout moe_layout(int n, const QW* w, const int* r_max, int E, int T, int k, int x_per_slot) {
@@ -1138,7 +1166,9 @@ MoeLayout moe_layout(int n, const QW* w, const int* r_max, int E, int T, int k, 
     }
     l.xp = off;
     l.sx = l.xp + up256(static_cast<size_t>(rows) * w[0].d_in * 2);
-    l.total = l.sx + up256(static_cast<size_t>(rows) * chunks * sizeof(float));
+    l.h = l.sx + up256(static_cast<size_t>(rows) * chunks * sizeof(float));
+    // gated per-slot input (x_per_slot 2): SiLU(g) u of every slot in fp16
+    l.total = l.h + (x_per_slot == 2 ? up256(static_cast<size_t>(S) * w[0].d_in * 2) : 0);
     return l;
 }
 
@@ -1168,13 +1198,19 @@ hipError_t launch_moe2(const MoeArgs& a, int lg, int nb, bool hoist, int blocks,
     return launch_moe3<BITS, 64>(a, nb, hoist, blocks, threads, st);
 }
 
+template <int LG, int CPL, int QX, bool G>
+hipError_t launch_direct4(const MoeArgs& a, int nb, int blocks, hipStream_t st) {
+    constexpr int NBW = direct_batches(LG, CPL);
+    if (nb == 0) hipLaunchKernelGGL((moe_direct_kernel<LG, CPL, 0, QX, NBW, G>), dim3(blocks), dim3(256), 0, st, a);
+    else if (nb == 1) hipLaunchKernelGGL((moe_direct_kernel<LG, CPL, 1, QX, NBW, G>), dim3(blocks), dim3(256), 0, st, a);
+    else hipLaunchKernelGGL((moe_direct_kernel<LG, CPL, 2, QX, NBW, G>), dim3(blocks), dim3(256), 0, st, a);
+    return hipGetLastError();
+}
+
 template <int LG, int CPL, int QX>
 hipError_t launch_direct3(const MoeArgs& a, int nb, int blocks, hipStream_t st) {
-    constexpr int NBW = direct_batches(LG, CPL);
-    if (nb == 0) hipLaunchKernelGGL((moe_direct_kernel<LG, CPL, 0, QX, NBW>), dim3(blocks), dim3(256), 0, st, a);
-    else if (nb == 1) hipLaunchKernelGGL((moe_direct_kernel<LG, CPL, 1, QX, NBW>), dim3(blocks), dim3(256), 0, st, a);
-    else hipLaunchKernelGGL((moe_direct_kernel<LG, CPL, 2, QX, NBW>), dim3(blocks), dim3(256), 0, st, a);
-    return hipGetLastError();
+    return a.u ? launch_direct4<LG, CPL, QX, true>(a, nb, blocks, st)
+               : launch_direct4<LG, CPL, QX, false>(a, nb, blocks, st);
 }
 
 // (LG, CPL, QX) instances: 24-32 chunk rows (d_in <= 1024), 64-chunk rows
@@ -1199,7 +1235,7 @@ size_t moe_workspace_bytes(int n, const QW* w, const int* r_max, int E, int T, i
 
 hipError_t launch_moe_decode(int n, const QW* w, const uint16_t* const* A, const uint16_t* const* B,
                              const int* r_max, const int32_t* const* ranks, const int32_t* const* slot_ranks,
-                             int E, const void* x, int x_per_slot,
+                             int E, const void* x, const void* u, int x_per_slot,
                              const int32_t* ids, int T, int k, int act, void* const* y, int out, void* ws,
                              hipStream_t st) {
     if (n < 1 || n > kMaxMoeWin) return hipErrorInvalidConfiguration;
@@ -1210,8 +1246,9 @@ hipError_t launch_moe_decode(int n, const QW* w, const uint16_t* const* A, const
     a.n = n;
     a.ids = ids;
     a.x = static_cast<const uint16_t*>(x);
+    a.u = static_cast<const uint16_t*>(u);
     a.E = E; a.T = T; a.k = k; a.d_in = d_in; a.G = w[0].G;
-    a.act = act; a.out = out; a.x_per_slot = x_per_slot;
+    a.act = act; a.out = out; a.x_per_slot = x_per_slot ? 1 : 0;
     a.n_active = reinterpret_cast<int*>(wsb + l.n_active);
     a.table = reinterpret_cast<int*>(wsb + l.table);
     a.sorted = reinterpret_cast<int*>(wsb + l.sorted);
@@ -1285,6 +1322,21 @@ hipError_t launch_moe_decode(int n, const QW* w, const uint16_t* const* A, const
     const int nb = rmax == 0 ? 0 : (rmax <= per ? 1 : (rmax <= 2 * per ? 2 : 4));
     if (rmax > 4 * per) return hipErrorInvalidConfiguration;
 
+    if (a.u) {
+        // gated input off the one-launch path: SiLU(g) u once for every slot
+        // (each preparation workgroup forming it for its slots had repeated
+        // the exponentials once per rank row: 52 against 11 us at 512 slots),
+        // then the plain path on it
+        uint16_t* h = reinterpret_cast<uint16_t*>(wsb + l.h);
+        const size_t n8 = static_cast<size_t>(S) * d_in / 8;
+        hipLaunchKernelGGL(moe_gate_kernel, dim3(static_cast<unsigned>((n8 + 255) / 256)), dim3(256), 0, st, a.x, a.u,
+                           h, n8, a.act);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        a.x = h;
+        a.u = nullptr;
+        a.act = DT_FP16;
+    }
     const int rows = x_per_slot ? S : T;
     const long long items = static_cast<long long>(rows) * chunks;
     const unsigned pgrid = static_cast<unsigned>(prep_end + (items + 255) / 256);

@@ -223,6 +223,32 @@ def test_moe_window_validation():
     assert lib.cl_moe_window_workspace(0, qws, (ctypes.c_int32 * 2)(32, 16), 128, 8, 8, 0) == 0
 
 
+def test_moe_gated_validation():
+    lib = cl.lib()
+    v = ctypes.c_void_p
+
+    def call(g=FAKE, u=FAKE, slot=None, act=cl.CL_FP16, ws_bytes=1 << 22, r_max=8):
+        qw = _qw()
+        return lib.cl_moe_linear_decode_gated(ctypes.byref(qw), v(FAKE), v(FAKE), r_max, v(FAKE), v(slot), 16, v(g),
+                                              v(u), v(FAKE), 2, 4, act, v(FAKE), cl.CL_FP16, v(FAKE), ws_bytes, None)
+
+    assert call(g=0) == cl.CL_EINVAL and b"null g or u" in lib.cl_last_error()
+    assert call(u=0) == cl.CL_EINVAL
+    assert call(u=FAKE + 8) == cl.CL_EINVAL and b"u must be 16-byte" in lib.cl_last_error()
+    assert call(g=FAKE + 8) == cl.CL_EINVAL
+    assert call(act=cl.CL_FP32) == cl.CL_EINVAL
+    assert call(slot=FAKE + 2) == cl.CL_EINVAL
+    assert call(r_max=300) == cl.CL_EINVAL
+    # the workspace: the down call's with per-slot activations, plus T k d_in
+    # fp16 values
+    qw = _qw()
+    need = lib.cl_moe_gated_workspace(ctypes.byref(qw), 8, 16, 2, 4)
+    assert need >= lib.cl_moe_workspace(ctypes.byref(qw), 8, 16, 2, 4, 1) + 2 * 4 * qw.d_in * 2
+    assert call(ws_bytes=need - 1) == cl.CL_EWORKSPACE
+    assert call(ws_bytes=need - 1, slot=FAKE) == cl.CL_EWORKSPACE
+    assert lib.cl_moe_gated_workspace(ctypes.byref(_qw(bits=3)), 8, 16, 2, 4) == 0
+
+
 def test_build_compensation_validation():
     lib = cl.lib()
     v = ctypes.c_void_p

@@ -10,7 +10,7 @@ import numpy as np
 import pytest
 import torch
 
-from oracle import moe, quant
+from oracle import linear, moe, quant
 from paper_2605_05819_amd import cl, workloads as wl
 from tests.helpers import REL_L2_TOL, assert_oracle, dev_f16, dev_u16, dev_u32, oracle_layer, out_to_numpy, rel_l2
 
@@ -384,3 +384,104 @@ def test_direct_path_few_slots(d_in, G, r_max, d_out, x_per_slot):
             if T == 2:
                 with pytest.raises(cl.ClError):
                     cl.moe_status()
+
+
+# ------------------------- the down projection of the gated activations
+
+def _abs_experts(Q, s, z, A, B, bits, G, d_in):
+    """|W_e|, |A_e|, |B_e|: a forward over these and |h| bounds sum |W_eff h|."""
+    return [(np.abs(quant.dequant_packed(Q[e], s[e], z[e], bits, G, d_in)), np.abs(A[e].astype(np.float64)),
+             np.abs(B[e].astype(np.float64))) for e in range(len(Q))]
+
+
+def _h_rounding_bound(absx, ranks, h, ids):
+    """Elementwise bound of the output error that rounding each h to fp16
+    (relative error <= 2^-11) can cause: 2^-11 sum_j |W_eff[i, j]| |h_j|."""
+    return 2.0 ** -11 * moe.forward(absx, ranks, np.abs(h), ids, True)
+
+
+@pytest.mark.parametrize("act", [torch.float16, torch.bfloat16])
+@pytest.mark.parametrize("T,k", [(1, 4), (5, 3), (16, 8)])
+def test_gated_down_full_outputs(T, k, act):
+    """cl_moe_linear_decode_gated against the oracle down projection of
+    h = SiLU(g) u (the expert nonlinearity between the gate/up and down
+    windows, Section 4.2.2): the one-launch path (4 slots), the VALU path (15
+    slots over 12 experts) and the MFMA path (128 slots), every output dtype,
+    fp16 and bf16 gate/up values.  The kernel rounds each h to fp16; the
+    elementwise bound adds what that rounding can move an output."""
+    E, d_out, d_in, bits, G, r_max = 12, 100, 512, 4, 128, 16
+    Q, s, z, A, B = _oracle_experts(E, d_out, d_in, bits, G, r_max, 80)
+    ranks = wl.moe_expert_ranks(80, 0, 0, E, levels=(0, 4, 8, 16))
+    ids, _ = wl.routing(T, 80, 0, E, k)
+    dt = "bf16" if act == torch.bfloat16 else "fp16"
+    g = wl.activation((T, k, d_in), 80, 0, 1, dtype=dt)
+    u = wl.activation((T, k, d_in), 80, 0, 2, dtype=dt)
+    h = linear.silu(g.values) * u.values
+    ref = _full_ref(Q, s, z, A, B, ranks, h, ids, True, bits, G, d_in)
+    extra = _h_rounding_bound(_abs_experts(Q, s, z, A, B, bits, G, d_in), ranks, h, ids)
+    ex = _device_experts(Q, s, z, A, B, ranks, d_out, d_in, bits, G, r_max)
+    gd, ud, idd = dev_u16(g.bits, act), dev_u16(u.bits, act), torch.from_numpy(ids).cuda()
+    for od in OUT_DTYPES:
+        y = cl.moe_linear_decode_gated(ex, gd, ud, idd, out_dtype=od)
+        torch.cuda.synchronize()
+        assert_oracle(out_to_numpy(y), ref, od, extra=extra)
+    # the gating is applied: the plain down projection of g misses the reference
+    assert rel_l2(_full_ref(Q, s, z, A, B, ranks, g.values, ids, True, bits, G, d_in), ref) > 0.5
+
+
+@pytest.mark.parametrize("T", [1, 8, 64])
+def test_gated_down_layer_sampled_rows(moe_layer, T):
+    """The 128-expert down projection (2048 x 768) of gated activations at
+    1, 8 and 64 tokens with top-8 routing, sampled rows; per-slot ranks."""
+    ex, Q, s, z, A, B, ranks = moe_layer["down"]
+    ids, w = wl.routing(T, 81, 0)
+    g = wl.activation((T, wl.MOE_TOPK, ex.d_in), 81, 0, 1)
+    u = wl.activation((T, wl.MOE_TOPK, ex.d_in), 81, 0, 2)
+    slot = wl.dynamic_slot_ranks(ids, w, ranks, (0, 8, 16, 32), 32)
+    idd = torch.from_numpy(ids).cuda()
+    y = cl.moe_linear_decode_gated(ex, dev_u16(g.bits, torch.float16), dev_u16(u.bits, torch.float16), idd,
+                                   out_dtype=torch.float32, slot_ranks=torch.from_numpy(slot).cuda())
+    torch.cuda.synchronize()
+    rows = np.unique(np.concatenate([[0, ex.d_out - 1], np.random.default_rng(T).integers(0, ex.d_out, 40)]))
+    h = linear.silu(g.values) * u.values
+    experts = [(quant.dequant_packed(Q[e], s[e], z[e], 4, 128, ex.d_in)[rows], A[e], B[e][rows])
+               for e in range(wl.MOE_EXPERTS)]
+    ref = moe.forward(experts, ranks, h, ids, True, slot_ranks=slot)
+    absx = [(np.abs(W), np.abs(a.astype(np.float64)), np.abs(b.astype(np.float64))) for W, a, b in experts]
+    extra = 2.0 ** -11 * moe.forward(absx, ranks, np.abs(h), ids, True, slot_ranks=slot)
+    assert_oracle(out_to_numpy(y)[:, :, rows], ref, extra=extra)
+
+
+@pytest.mark.parametrize("T,k", [(1, 8), (16, 8)])
+def test_gate_up_window_into_gated_down(T, k):
+    """The MoE FFN chain: the gate/up window (fp16 outputs) feeds the gated
+    down call directly.  Each stage against the oracle on the values it was
+    handed: the window's outputs against the oracle gate and up projections,
+    the down output against the oracle down projection of SiLU(g) u formed
+    from the window's fp16 outputs; and the chain end to end against the
+    oracle's own chain (intermediates in fp64)."""
+    E, hid, ffn, bits, G = 16, 512, 256, 4, 128
+    host, exs = [], []
+    for m, (d_out, d_in, r_max) in enumerate(((ffn, hid, 16), (ffn, hid, 8), (hid, ffn, 16))):
+        Q, s, z, A, B = _oracle_experts(E, d_out, d_in, bits, G, r_max, 82 + m)
+        ranks = wl.moe_expert_ranks(82 + m, 0, m, E, levels=(0, 4, 8, r_max))
+        host.append((Q, s, z, A, B, ranks, d_in))
+        exs.append(_device_experts(Q, s, z, A, B, ranks, d_out, d_in, bits, G, r_max))
+    ids, _ = wl.routing(T, 85, 0, E, k)
+    x = wl.activation((T, hid), 85, 0, 1)
+    idd = torch.from_numpy(ids).cuda()
+    gy, uy = cl.moe_linear_decode_window(exs[:2], dev_u16(x.bits, torch.float16), idd, out_dtype=torch.float16)
+    y = cl.moe_linear_decode_gated(exs[2], gy, uy, idd, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    refs = []
+    for (Q, s, z, A, B, ranks, d_in), got in zip(host[:2], (gy, uy)):
+        ref = _full_ref(Q, s, z, A, B, ranks, x.values, ids, False, bits, G, d_in)
+        assert_oracle(out_to_numpy(got), ref, torch.float16)
+        refs.append(ref)
+    Q, s, z, A, B, ranks, d_in = host[2]
+    h = linear.silu(out_to_numpy(gy)) * out_to_numpy(uy)
+    ref = _full_ref(Q, s, z, A, B, ranks, h, ids, True, bits, G, d_in)
+    extra = _h_rounding_bound(_abs_experts(Q, s, z, A, B, bits, G, d_in), ranks, h, ids)
+    assert_oracle(out_to_numpy(y), ref, extra=extra)
+    chain = _full_ref(Q, s, z, A, B, ranks, linear.silu(refs[0]) * refs[1], ids, True, bits, G, d_in)
+    assert rel_l2(out_to_numpy(y), chain) <= REL_L2_TOL
