@@ -59,7 +59,8 @@ namespace cl {
 namespace {
 
 constexpr int kMaxWin = 8;   // linears per window
-constexpr int kMaxKp = 4;    // K parts of the many-token A x partials
+constexpr int kMaxKp = 16;   // K parts of the many-token A x partials
+constexpr int kPrefKp = 4;   // of them loaded ahead of the backbone's K loop
 // 4-bit windows with this many tokens use the MFMA backbone (measured on the
 // Llama-8B layer: 2 tokens 72 us on the dot2 backbone against 88 us on MFMA,
 // 3 tokens 123 against 88, 5-7 tokens ~185 against ~90)
@@ -655,7 +656,7 @@ __global__ __launch_bounds__(1024) void decode_prep_mfma_kernel(PrepMArgs a) {
 // fixed order and split into fp16 hi and lo parts, one step each); the
 // waves' tiles are summed through LDS in a fixed order; one rounding to the
 // output dtype.
-template <int TPW, int NBUF, bool GLU, int GPB, int NW>
+template <int TPW, int NBUF, bool GLU, int GPB, int NW, bool LONGK>
 __global__ __launch_bounds__((GLU ? 2 : 1) * 64 * NW) void decode_mfma_kernel(DecodeArgs a) {
     // NW waves split K.  GLU: 2 NW waves, the first NW on the gate's tiles
     // and the other NW on the up tiles of the same rows (phase 1); the two
@@ -733,7 +734,7 @@ __global__ __launch_bounds__((GLU ? 2 : 1) * 64 * NW) void decode_mfma_kernel(De
     for (int j = 0; j < TPW; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
     struct RankOp {
         uint32_t bw[TPW][4];
-        f32x4 tp[kMaxKp][2];
+        f32x4 tp[kPrefKp][2];
     };
     auto rank_load = [&](int kr, RankOp& o) {
         const int k = kr + 8 * g;
@@ -756,7 +757,7 @@ __global__ __launch_bounds__((GLU ? 2 : 1) * 64 * NW) void decode_mfma_kernel(De
         }
         const int tk = tokv ? tok : 0;
 #pragma unroll
-        for (int p = 0; p < kMaxKp; ++p) {
+        for (int p = 0; p < kPrefKp; ++p) {
             const int pp = p < a.kp ? p : 0;
             const f32x4* src = reinterpret_cast<const f32x4*>(L.t + (static_cast<size_t>(pp) * a.T + tk) * L.rpad + k);
             o.tp[p][0] = src[0];
@@ -768,10 +769,36 @@ __global__ __launch_bounds__((GLU ? 2 : 1) * 64 * NW) void decode_mfma_kernel(De
         const int k = kr + 8 * g;
         float tsum[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int p = 0; p < kMaxKp; ++p) {
+        for (int p = 0; p < kPrefKp; ++p) {
             if (p >= a.kp) break;
 #pragma unroll
             for (int e = 0; e < 4; ++e) { tsum[e] += o.tp[p][0][e]; tsum[4 + e] += o.tp[p][1][e]; }
+        }
+        // long rows (more than kPrefKp K parts): the other partials now, in
+        // the same order (holding them through the K loop cost a wave per
+        // SIMD; fewer parts had made each preparation workgroup read ~230 KB
+        // of scattered 64-byte runs: the 14336-wide down took 9.9 us to prepare
+        // at 16 tokens, 5.1 with 14 parts)
+        if (LONGK && a.kp > kPrefKp) {
+            f32x4 more[kMaxKp - kPrefKp][2];
+            const int tk = tokv ? tok : 0;
+#pragma unroll
+            for (int p = kPrefKp; p < kMaxKp; ++p) {
+                const int pp = p < a.kp ? p : 0;
+                const f32x4* src =
+                    reinterpret_cast<const f32x4*>(L.t + (static_cast<size_t>(pp) * a.T + tk) * L.rpad + k);
+                more[p - kPrefKp][0] = src[0];
+                more[p - kPrefKp][1] = src[1];
+            }
+#pragma unroll
+            for (int p = kPrefKp; p < kMaxKp; ++p) {
+                if (p >= a.kp) break;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    tsum[e] += more[p - kPrefKp][0][e];
+                    tsum[4 + e] += more[p - kPrefKp][1][e];
+                }
+            }
         }
         // t as fp16 hi + lo parts, two MFMA steps (absent tokens zero)
         uint32_t tw[4], tl[4];
@@ -1021,7 +1048,7 @@ namespace {
 // (the MFMA backbone keeps its rows' scales and zeros in LDS)
 bool use_mfma(const QW& w, int T) { return w.bits == 4 && T >= kMfmaMinTokens && w.d_in / w.G <= 512; }
 
-// K parts of the MFMA preparation (at most 4, about 1024 codes each), the
+// K parts of the MFMA preparation (at most 16, about 1024 codes each), the
 // waves of a part's workgroup (4, 8 or 16: enough that each wave has at most
 // eight 32-code steps, one round of loads -- the 14336-code rows took four
 // dependent rounds on four waves) and the steps each wave takes
@@ -1029,10 +1056,10 @@ struct MfmaPlan {
     int kp, nw, spw;
 };
 
-MfmaPlan mfma_plan(int d_in) {
+MfmaPlan mfma_plan(int d_in, int max_kp = kMaxKp) {
     const int nsteps = d_in / 32;
     int kp = (d_in + 1023) / 1024;
-    if (kp > kMaxKp) kp = kMaxKp;
+    if (kp > max_kp) kp = max_kp;
     int nw = 4;
     while (nw < 16 && nsteps > nw * kp * 8) nw *= 2;
     return MfmaPlan{kp, nw, (nsteps + nw * kp - 1) / (nw * kp)};
@@ -1057,20 +1084,27 @@ MfmaCfg mfma_cfg(int tiles, int groups) {
     return MfmaCfg{1, 4, 4};
 }
 
+// More than kPrefKp K parts (rows longer than 4096 codes) only on the
+// one-tile instance with one group per block, the only one whose registers
+// take the extra partials without losing a wave per SIMD.
+bool long_k_ok(const MfmaCfg& c, int gpb) { return c.tpw == 1 && gpb == 1; }
+
 template <bool GLU, int GPB>
-auto pick_cfg(const MfmaCfg& c) {
+auto pick_cfg(const MfmaCfg& c, bool longk) {
     constexpr int H = GPB == 1 ? 1 : 2;           // nbuf divisor
-    if (c.tpw == 4) return decode_mfma_kernel<4, 2 / H, GLU, GPB, 4>;
-    return decode_mfma_kernel<1, 4 / H, GLU, GPB, 4>;
+    if (c.tpw == 4) return decode_mfma_kernel<4, 2 / H, GLU, GPB, 4, false>;
+    if (GPB == 1 && longk) return decode_mfma_kernel<1, 4, GLU, 1, 4, true>;
+    return decode_mfma_kernel<1, 4 / H, GLU, GPB, 4, false>;
 }
 
 template <bool GLU>
-auto pick_gpb(const MfmaCfg& c, int gpb) {
-    return gpb == 1 ? pick_cfg<GLU, 1>(c) : (gpb == 2 ? pick_cfg<GLU, 2>(c) : pick_cfg<GLU, 4>(c));
+auto pick_gpb(const MfmaCfg& c, int gpb, bool longk) {
+    if (gpb == 1) return pick_cfg<GLU, 1>(c, longk);
+    return gpb == 2 ? pick_cfg<GLU, 2>(c, longk) : pick_cfg<GLU, 4>(c, longk);
 }
 
-auto pick_mfma_kernel(const MfmaCfg& c, bool glu, int gpb) {
-    return glu ? pick_gpb<true>(c, gpb) : pick_gpb<false>(c, gpb);
+auto pick_mfma_kernel(const MfmaCfg& c, bool glu, int gpb, bool longk) {
+    return glu ? pick_gpb<true>(c, gpb, longk) : pick_gpb<false>(c, gpb, longk);
 }
 
 }  // namespace
@@ -1101,7 +1135,6 @@ namespace {
 hipError_t launch_decode_mfma(int n, const QW* w, const LR* c, const void* x, int T, int act, void* const* y,
                               int out, void* ws, hipStream_t st, bool glu) {
     const int d_in = w[0].d_in;
-    const MfmaPlan mp = mfma_plan(d_in);
     char* wsb = static_cast<char*>(ws);
     PrepMArgs pa{};
     DecodeArgs a{};
@@ -1116,6 +1149,9 @@ hipError_t launch_decode_mfma(int n, const QW* w, const LR* c, const void* x, in
     // four tiles per wave when the workgroup's scales and zeros fit 32 KB of LDS
     const MfmaCfg cfg = mfma_cfg(tiles, groups);
     const int tpw = cfg.tpw;
+    const int gpb = mfma_groups_per_block(w[0].G);
+    // (the workspace query sizes the partials for the most parts)
+    const MfmaPlan mp = mfma_plan(d_in, long_k_ok(cfg, gpb) ? kMaxKp : kPrefKp);
     int wg_end = 0, rtiles = 0, wg_first = 0;
     for (int i = 0; i < n; ++i) {
         float* tp = reinterpret_cast<float*>(wsb + off);
@@ -1157,8 +1193,7 @@ hipError_t launch_decode_mfma(int n, const QW* w, const LR* c, const void* x, in
     a.cps = 0;
     a.kp = mp.kp;
     a.h = glu ? y[0] : nullptr;
-    const int gpb = mfma_groups_per_block(w[0].G);
-    auto kern = pick_mfma_kernel(cfg, glu, gpb);
+    auto kern = pick_mfma_kernel(cfg, glu, gpb, mp.kp > kPrefKp);
     // a gated window runs one workgroup of eight waves per gate workgroup
     // (four waves on the gate's tiles, four on the up tiles of the same rows),
     // with both linears' scales and zeros in LDS
