@@ -275,8 +275,9 @@ cl_status cl_linear_decode_glu(const cl_qweight* w, const cl_lowrank* c, const v
  *  M          >= 1 tokens, M * d_in < 2^31
  *  Y          device [M][d_out] of out_dtype
  *  ws         device workspace of cl_prefill_workspace(w, c, M) bytes
- *             (2 M d_in for X' plus 2 M rank rounded up to 32 for T),
- *             256-byte aligned
+ *             (2 M d_in for X'; with a rank term, 2 M r32 for T and
+ *             4 M r32 ceil(d_in / 512) for its partial products, r32 the
+ *             rank rounded up to 32), 256-byte aligned
  * Errors: as cl_linear_decode; CL_EUNSUPPORTED if d_in is not a multiple of
  * 64 or M * d_in >= 2^31.
  */

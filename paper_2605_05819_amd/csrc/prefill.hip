@@ -5,9 +5,10 @@
 // X [M][K] activations, Q [N][K] packed codes, A [r_max][K], B [N][r_max].
 // This is a dense contraction, so it runs on MFMA (v_mfma_f32_16x16x32_f16):
 //
-//  1. lowrank_t_kernel: T = X A[:r]^T in fp32, rounded to fp16, zero-padded
-//     to a multiple of 32 columns; it also writes X' (below).  Without a
-//     rank term, xprep_kernel writes X' alone.
+//  1. xt_partial_kernel writes X' (below) and the fp32 partial products of
+//     X A[:r]^T over 512-column parts of K; t_reduce_kernel sums the parts
+//     in order into T, rounded to fp16 and zero-padded to a multiple of 32
+//     columns.  Without a rank term, xprep_kernel writes X' alone.
 //     X' = X as fp16 (bf16 converted) with every 8 consecutive k reordered
 //     (k0,k4,k1,k5,k2,k6,k3,k7): the order in which the code unpack below
 //     produces weights, so the contraction is unchanged.
@@ -105,107 +106,111 @@ __global__ __launch_bounds__(256) void xprep_kernel(const uint16_t* __restrict__
     store_xp(Xp, static_cast<size_t>(c) * 8, *reinterpret_cast<const u32x4*>(X + static_cast<size_t>(c) * 8), act);
 }
 
-// One launch, two roles.  Workgroups [0, t_blocks): T = X A[:r]^T for 16
-// tokens x 16 NJ factor columns each; the NW waves split K, every wave keeps
-// 8 k-blocks of loads in flight, and the partial tiles are summed through
-// LDS in a fixed order.  MFMA A operand = X rows, B operand = rows of A.
-// Output fp16, zero for columns >= rank.  The remaining workgroups write X'
-// (four 16-byte chunks per thread), so the X' stream runs beside T (X'
-// written by the T workgroups themselves took 27 us for the pair at
-// M = 2048, K = 4096; apart, about 22 us, bound by T's reads of 16 rows x
-// 64 bytes per load instruction: the same bytes read as contiguous 1 KB
-// rows take half the time).  32 factor columns per workgroup (NJ = 2)
-// spread those reads over twice the workgroups: 20.4 us against 22.7 us
-// with 64, the same output bit for bit.
-template <int NW, int NJ>
-__global__ __launch_bounds__(NW * 64) void lowrank_t_kernel(const uint16_t* __restrict__ X,
-                                                            const uint16_t* __restrict__ A,
-                                                            uint16_t* __restrict__ T, uint16_t* __restrict__ Xp,
-                                                            int M, int K, int rank, int r_pad, int act, int t_blocks,
-                                                            int mtiles, long long chunks) {
-    constexpr int U = 8;                               // k blocks of 32 per batch
-    constexpr int XC = 4;                              // X' chunks per thread
-    __shared__ f32x4 part[NW][NJ][64];
-    const int tid = threadIdx.x;
-    if (static_cast<int>(blockIdx.x) >= t_blocks) {
-        const long long base = static_cast<long long>(blockIdx.x - t_blocks) * (NW * 64 * XC) + tid;
-        u32x4 v[XC];
+// One launch for X' and the partial low-rank products: workgroup (64-token
+// tile, 256-column part of K).  Its threads convert the tile's X to X' and
+// write it both to the workspace (the GEMM's operand) and to LDS (each row's
+// 16-byte chunk c at c ^ (row % 16), so the 16 rows of an MFMA operand read
+// land in distinct banks); then wave w multiplies the tile by rank rows
+// 16 w .. 16 w + 15 (then + 64, ...) of A over the part's columns on MFMA
+// (A's 8-element runs reordered in registers as X' is, so each product pairs
+// the same elements) and writes the fp32 partial P[part][token][column].
+// Each X element is read once and each A row once per 64 tokens (one
+// workgroup per 16 tokens and 32 factor columns over all of K had read A 128
+// times and X twice, 16 rows x 64 bytes per load instruction: 20.4 us for
+// M = 2048, K = 4096 with X' written beside it; now 11.3 us, and 12.4 /
+// 13.3 / 11.6 us with 512 columns / 32 tokens and 512 columns / 128 tokens
+// per workgroup).
+constexpr int XT_M = 64, XT_K = 256;
+
+__global__ __launch_bounds__(256) void xt_partial_kernel(const uint16_t* __restrict__ X,
+                                                         const uint16_t* __restrict__ A, uint16_t* __restrict__ Xp,
+                                                         float* __restrict__ P, int M, int K, int rank, int r_pad,
+                                                         int act, int mtiles) {
+    constexpr int CPR = XT_K / 8;                  // 16-byte chunks per tile row
+    constexpr int PER = XT_M * CPR / 256;          // chunks per thread
+    constexpr int MTL = XT_M / 16;                 // MFMA token tiles
+    __shared__ u32x4 xs[XT_M * CPR];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int mt = static_cast<int>(blockIdx.x) % mtiles, part = static_cast<int>(blockIdx.x) / mtiles;
+    const int m0 = mt * XT_M, k0 = part * XT_K;
+    const int kw = min(XT_K, K - k0);              // a multiple of 64
+    const u32x4 zero = {0u, 0u, 0u, 0u};
+    // X' of the tile: every load first (clamped addresses), then the stores
+    u32x4 v[PER];
 #pragma unroll
-        for (int j = 0; j < XC; ++j) {
-            const long long c = base + static_cast<long long>(j) * NW * 64;
-            v[j] = *reinterpret_cast<const u32x4*>(X + static_cast<size_t>(c < chunks ? c : 0) * 8);
-        }
-#pragma unroll
-        for (int j = 0; j < XC; ++j) {
-            const long long c = base + static_cast<long long>(j) * NW * 64;
-            if (c < chunks) store_xp(Xp, static_cast<size_t>(c) * 8, v[j], act);
-        }
-        return;
+    for (int i = 0; i < PER; ++i) {
+        const int c = tid + 256 * i, row = c / CPR, cc = c % CPR;
+        const bool ok = m0 + row < M && 8 * cc < kw;
+        v[i] = *reinterpret_cast<const u32x4*>(X + static_cast<size_t>(ok ? m0 + row : 0) * K + k0 + (ok ? 8 * cc : 0));
     }
-    const int lane = tid & 63;
-    const int wave = tid >> 6;
-    const int mtile = static_cast<int>(blockIdx.x) % mtiles;   // 16 tokens
-    const int ntile = static_cast<int>(blockIdx.x) / mtiles;   // 16 NJ factor columns
-    const int m = mtile * 16 + (lane & 15);
-    const int kq = 8 * (lane >> 4);                    // this lane's 8 k within a 32 block
-    const bool mval = m < M;
-    const uint16_t* xr = X + static_cast<size_t>(mval ? m : 0) * K;
-    f32x4 acc[NJ];
 #pragma unroll
-    for (int j = 0; j < NJ; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
-    const uint16_t* ar[NJ];
-    bool nval[NJ];
-#pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-        const int n = ntile * (16 * NJ) + j * 16 + (lane & 15);
-        nval[j] = n < rank;
-        ar[j] = A + static_cast<size_t>(nval[j] ? n : 0) * K;
+    for (int i = 0; i < PER; ++i) {
+        const int c = tid + 256 * i, row = c / CPR, cc = c % CPR;
+        const bool ok = m0 + row < M && 8 * cc < kw;
+        const u32x4 xp = act8_permuted(v[i], act);
+        if (ok) *reinterpret_cast<u32x4*>(Xp + static_cast<size_t>(m0 + row) * K + k0 + 8 * cc) = xp;
+        xs[row * CPR + (cc ^ (row & 15))] = ok ? xp : zero;
     }
-    const int nkb = K / 32;                            // k blocks of 32; this wave takes 1 / NW
-    const int kbeg = 32 * (wave * nkb / NW), kend = 32 * ((wave + 1) * nkb / NW);
-    for (int k0 = kbeg; k0 < kend; k0 += 32 * U) {
-        u32x4 xa[U], av[U][NJ];
+    __syncthreads();
+    const int g = lane >> 4, r = lane & 15;
+    const int nsteps = kw / 32;
+    for (int nt = wave; nt * 16 < r_pad; nt += 4) {
+        const int n = nt * 16 + r;
+        const bool nv = n < rank;
+        const uint16_t* ar = A + static_cast<size_t>(nv ? n : 0) * K + k0;
+        f32x4 acc[MTL];
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int k = k0 + 32 * u;
-            const int kc = k < kend ? k : (kbeg < kend ? kbeg : 0);
-            xa[u] = *reinterpret_cast<const u32x4*>(xr + kc + kq);
+        for (int i = 0; i < MTL; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int s0 = 0; s0 < nsteps; s0 += 8) {
+            u32x4 av[8];                           // 8 steps of A loads in flight
 #pragma unroll
-            for (int j = 0; j < NJ; ++j) av[u][j] = *reinterpret_cast<const u32x4*>(ar[j] + kc + kq);
-        }
+            for (int u = 0; u < 8; ++u) {
+                const int st = s0 + u < nsteps ? s0 + u : 0;
+                av[u] = *reinterpret_cast<const u32x4*>(ar + st * 32 + 8 * g);
+            }
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const bool live = k0 + 32 * u < kend;
-            u32x4 x8 = act8_to_f16(xa[u], act);
-            if (!mval || !live) x8 = u32x4{0, 0, 0, 0};
+            for (int u = 0; u < 8; ++u) {
+                const bool live = s0 + u < nsteps;
+                const int ch = (live ? s0 + u : 0) * 4 + g;
+                const u32x4 a8 = (nv && live) ? act8_permuted(av[u], DT_FP16) : zero;
 #pragma unroll
-            for (int j = 0; j < NJ; ++j) {
-                u32x4 a8 = av[u][j];
-                if (!nval[j]) a8 = u32x4{0, 0, 0, 0};
-                acc[j] = mfma(x8, a8, acc[j]);
+                for (int i = 0; i < MTL; ++i) acc[i] = mfma(xs[(16 * i + r) * CPR + (ch ^ r)], a8, acc[i]);
             }
         }
+        // acc[i][e] = partial T[m0 + 16 i + 4 g + e][n]
+#pragma unroll
+        for (int i = 0; i < MTL; ++i)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int m = m0 + 16 * i + 4 * g + e;
+                if (m < M) P[(static_cast<size_t>(part) * M + m) * r_pad + n] = acc[i][e];
+            }
     }
+}
+
+// T = the partials summed in part order, rounded to fp16 (zero for columns
+// at or past the rank): four elements of T per thread (r_pad is a multiple
+// of 32, so four never straddle a row), eight parts' loads in flight.
+__global__ __launch_bounds__(256) void t_reduce_kernel(const float* __restrict__ P, uint16_t* __restrict__ T, int M,
+                                                       int rank, int r_pad, int parts) {
+    const long long i4 = static_cast<long long>(blockIdx.x) * 256 + threadIdx.x;
+    const long long n_all = static_cast<long long>(M) * r_pad;
+    if (4 * i4 >= n_all) return;
+    const f32x4* P4 = reinterpret_cast<const f32x4*>(P);
+    f32x4 sum = {0.f, 0.f, 0.f, 0.f};
+    for (int p0 = 0; p0 < parts; p0 += 8) {
+        f32x4 v[8];
 #pragma unroll
-    for (int j = 0; j < NJ; ++j) part[wave][j][lane] = acc[j];
-    __syncthreads();
-    if (wave != 0) return;
+        for (int u = 0; u < 8; ++u) v[u] = P4[static_cast<size_t>(p0 + u < parts ? p0 + u : 0) * (n_all / 4) + i4];
 #pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-        acc[j] = part[0][j][lane];
-        for (int w = 1; w < NW; ++w) acc[j] += part[w][j][lane];
+        for (int u = 0; u < 8; ++u)
+            if (p0 + u < parts) sum += v[u];
     }
-    // acc[j][e] = T[mtile*16 + 4*(lane/16) + e][ntile*64 + j*16 + lane%16]
+    const int n0 = static_cast<int>((4 * i4) % r_pad);
+    uint32_t h[4];
 #pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-        const int n = ntile * (16 * NJ) + j * 16 + (lane & 15);
-        if (n >= r_pad) continue;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const int mm = mtile * 16 + 4 * (lane >> 4) + e;
-            if (mm < M) T[static_cast<size_t>(mm) * r_pad + n] = f32_to_f16_bits(n < rank ? acc[j][e] : 0.f);
-        }
-    }
+    for (int e = 0; e < 4; ++e) h[e] = f32_to_f16_bits(n0 + e < rank ? sum[e] : 0.f);
+    reinterpret_cast<uint2*>(T)[i4] = make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
 }
 
 // 16 bytes per lane from global memory straight into LDS (lane l's bytes
@@ -554,15 +559,20 @@ int prefill_jt(int M, int N) {
 // X' rows padded to whole 128-token blocks (prefill_kernel reads them)
 size_t xp_rows(int M) { return (static_cast<size_t>(M) + 127) / 128 * 128; }
 
+int xt_parts(int K) { return (K + XT_K - 1) / XT_K; }
+
 size_t prefill_workspace_bytes(const QW& w, const LR& c, int M) {
     const int r_pad = (c.rank + 31) / 32 * 32;
-    return up256(xp_rows(M) * w.d_in * 2) + up256(static_cast<size_t>(M) * r_pad * 2);
+    return up256(xp_rows(M) * w.d_in * 2) + up256(static_cast<size_t>(M) * r_pad * 2) +
+           (c.rank > 0 ? up256(static_cast<size_t>(xt_parts(w.d_in)) * M * r_pad * 4) : 0);
 }
 
 hipError_t launch_linear_prefill(const QW& w, const LR& c, const void* X, int M, int act, void* Y, int out,
                                  void* ws, hipStream_t st) {
     uint16_t* Xp = static_cast<uint16_t*>(ws);
     uint16_t* T = reinterpret_cast<uint16_t*>(static_cast<char*>(ws) + up256(xp_rows(M) * w.d_in * 2));
+    float* P = reinterpret_cast<float*>(reinterpret_cast<char*>(T) +
+                                        up256(static_cast<size_t>(M) * ((c.rank + 31) / 32 * 32) * 2));
     PrefillArgs a;
     a.q = w.q; a.s = w.s; a.z = w.z; a.B = c.B;
     a.Xp = Xp;
@@ -575,14 +585,14 @@ hipError_t launch_linear_prefill(const QW& w, const LR& c, const void* X, int M,
     a.mblocks = (M + 127) / 128;
     const uint16_t* Xa = static_cast<const uint16_t*>(X);
     if (c.rank > 0) {
-        constexpr int NW = 8;
-        const int mtiles = (M + 15) / 16;
-        constexpr int NJ = 2;                 // 32 factor columns per workgroup
-        const int t_blocks = mtiles * ((a.r_pad + 16 * NJ - 1) / (16 * NJ));
-        const long long chunks = static_cast<long long>(M) * w.d_in / 8;
-        const long long x_blocks = (chunks + NW * 64 * 4 - 1) / (NW * 64 * 4);
-        hipLaunchKernelGGL((lowrank_t_kernel<NW, NJ>), dim3(static_cast<unsigned>(t_blocks + x_blocks)), dim3(NW * 64), 0, st,
-                           Xa, c.A, T, Xp, M, w.d_in, c.rank, a.r_pad, act, t_blocks, mtiles, chunks);
+        const int mtiles = (M + XT_M - 1) / XT_M, parts = xt_parts(w.d_in);
+        hipLaunchKernelGGL(xt_partial_kernel, dim3(static_cast<unsigned>(mtiles * parts)), dim3(256), 0, st, Xa, c.A,
+                           Xp, P, M, w.d_in, c.rank, a.r_pad, act, mtiles);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        const long long n_all = static_cast<long long>(M) * a.r_pad;
+        hipLaunchKernelGGL(t_reduce_kernel, dim3(static_cast<unsigned>((n_all / 4 + 255) / 256)), dim3(256), 0, st, P,
+                           T, M, c.rank, a.r_pad, parts);
     } else {
         const long long chunks = static_cast<long long>(M) * w.d_in / 8;
         hipLaunchKernelGGL(xprep_kernel, dim3(static_cast<unsigned>((chunks + 255) / 256)), dim3(256), 0, st, Xa, Xp,
