@@ -119,18 +119,23 @@ struct MoeArgs {
 template <int BITS>
 __global__ __launch_bounds__(256) void moe_prep_kernel(MoeArgs a) {
     constexpr int CPW = 32 / BITS, HPW = CPW / 2, PPC = 4 * HPW;
-    __shared__ int sids[kMaxSlots];
-    __shared__ int mys[kMaxSlots];          // this expert's slots, in slot order
-    __shared__ int hist[kMaxExperts];       // slots per expert
-    __shared__ int rk[kMaxExperts];         // the experts' ranks, loaded beside the ids
+    // sids[S], mys[S] (this expert's slots, in slot order), hist[E] (slots
+    // per expert), rk[E] (the experts' ranks): sized by the call, so more
+    // workgroups fit a CU
+    extern __shared__ int prep_lds[];
     __shared__ int wsum[4][2];
     __shared__ int wcnt[4];
     __shared__ int sel, sel_lt, sel_n, srank;
+    __shared__ u32x4 xsh[4][256];          // a pass's activations, 4 slots x 2048 columns
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
     const int S = a.T * a.k;
     const int blk = blockIdx.x;
+    int* const sids = prep_lds;
+    int* const mys = sids + S;
+    int* const hist = mys + S;
+    int* const rk = hist + a.E;
 
     if (blk < a.lin[a.n - 1].prep_end) {
         // workgroup (linear li, j, quad): the j-th routed expert (ascending
@@ -269,10 +274,13 @@ __global__ __launch_bounds__(256) void moe_prep_kernel(MoeArgs a) {
             }
             a.table[kTab * j + 4 + li] = rank;
         }
-        // t[slot][i] = A_e[i] . x_slot: one wave per rank row, four slots at a time
+        // t[slot][i] = A_e[i] . x_slot: wave w takes rank row i = 4 quad + w;
+        // each pass's activations (4 slots x 2048 columns) go into LDS once
+        // for the workgroup's four waves
         const int i = 4 * quad + wave;
-        if (i >= rank) return;
-        const uint16_t* ar = L.A + static_cast<size_t>(e) * L.a_stride + static_cast<size_t>(i) * a.d_in;
+        if (4 * quad >= rank) return;
+        const bool has = i < rank;
+        const uint16_t* ar = L.A + static_cast<size_t>(e) * L.a_stride + static_cast<size_t>(has ? i : 4 * quad) * a.d_in;
         for (int j0 = 0; j0 < ne; j0 += 4) {
             const uint16_t* xr[4];
             int sl4[4];
@@ -283,40 +291,43 @@ __global__ __launch_bounds__(256) void moe_prep_kernel(MoeArgs a) {
                 xr[u] = a.x + static_cast<size_t>(xrow) * a.d_in;
             }
             float acc[4] = {0.f, 0.f, 0.f, 0.f};
-            // passes of 2048 columns: every load of a pass is issued before
-            // any is used (a conversion branch between the loads had made
-            // each load wait for the one before: ~3 us per call at T = 1)
             for (int c0 = 0; c0 < a.d_in; c0 += 4 * 512) {
-                u32x4 av[4], xv[4][4];
+                u32x4 av[4], xl[4];
+                const int cx = c0 + 8 * tid;
+#pragma unroll
+                for (int u = 0; u < 4; ++u) xl[u] = *reinterpret_cast<const u32x4*>(xr[u] + (cx < a.d_in ? cx : 0));
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
                     const int c = c0 + 512 * q + 8 * lane;
-                    const int cc = c < a.d_in ? c : 0;
-                    av[q] = *reinterpret_cast<const u32x4*>(ar + cc);
-#pragma unroll
-                    for (int u = 0; u < 4; ++u) xv[u][q] = *reinterpret_cast<const u32x4*>(xr[u] + cc);
+                    av[q] = *reinterpret_cast<const u32x4*>(ar + (c < a.d_in ? c : 0));
                 }
+                __syncthreads();                 // the previous pass's reads are done
 #pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const bool valid = c0 + 512 * q + 8 * lane < a.d_in;
+                for (int u = 0; u < 4; ++u)
+                    xsh[u][tid] = cx < a.d_in ? act8_to_f16(xl[u], a.act) : u32x4{0u, 0u, 0u, 0u};
+                __syncthreads();
+                if (has) {
 #pragma unroll
-                    for (int u = 0; u < 4; ++u) {
-                        const u32x4 xw = act8_to_f16(xv[u][q], a.act);
-                        float d = 0.f;
+                    for (int q = 0; q < 4; ++q) {
 #pragma unroll
-                        for (int e = 0; e < 4; ++e) {
-                            // copy the vector elements to scalars first: a
-                            // bit_cast of a subscripted ext_vector reads element 0
-                            const uint32_t ae = av[q][e], xe = xw[e];
-                            d = dot2(__builtin_bit_cast(f16x2, ae), __builtin_bit_cast(f16x2, xe), d);
+                        for (int u = 0; u < 4; ++u) {
+                            const u32x4 xw = xsh[u][64 * q + lane];
+                            float d = 0.f;
+#pragma unroll
+                            for (int h = 0; h < 4; ++h) {
+                                const uint32_t ae = av[q][h], xe = xw[h];
+                                d = dot2(__builtin_bit_cast(f16x2, ae), __builtin_bit_cast(f16x2, xe), d);
+                            }
+                            acc[u] += d;
                         }
-                        acc[u] += valid ? d : 0.f;
                     }
                 }
             }
-            const float tot = wave_sum_multi<4>(acc);      // lane l: slot j0 + l / 16
-            const int u = lane >> 4;
-            if ((lane & 15) == 0 && j0 + u < ne) L.t[static_cast<size_t>(sl4[u]) * L.r_max + i] = tot;
+            if (has) {
+                const float tot = wave_sum_multi<4>(acc);      // lane l: slot j0 + l / 16
+                const int u = lane >> 4;
+                if ((lane & 15) == 0 && j0 + u < ne) L.t[static_cast<size_t>(sl4[u]) * L.r_max + i] = tot;
+            }
         }
         return;
     }
@@ -1340,10 +1351,11 @@ hipError_t launch_moe_decode(int n, const QW* w, const uint16_t* const* A, const
     const int rows = x_per_slot ? S : T;
     const long long items = static_cast<long long>(rows) * chunks;
     const unsigned pgrid = static_cast<unsigned>(prep_end + (items + 255) / 256);
+    const size_t plds = static_cast<size_t>(2 * S + 2 * E) * sizeof(int);
     if (bits == 4)
-        hipLaunchKernelGGL(moe_prep_kernel<4>, dim3(pgrid), dim3(256), 0, st, a);
+        hipLaunchKernelGGL(moe_prep_kernel<4>, dim3(pgrid), dim3(256), plds, st, a);
     else
-        hipLaunchKernelGGL(moe_prep_kernel<2>, dim3(pgrid), dim3(256), 0, st, a);
+        hipLaunchKernelGGL(moe_prep_kernel<2>, dim3(pgrid), dim3(256), plds, st, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     if (on_mfma) {
