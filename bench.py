@@ -208,7 +208,7 @@ def bench_tokens(torch, cl, wl, timer, copies, layer, dev):
     """The layer step at 4 and 16 decode tokens."""
     res = {}
     for T in (4, 16):
-        ms, _, _ = layer_step(torch, cl, wl, timer, copies, layer, T, dev, 40, 8)
+        ms, _, _ = layer_step(torch, cl, wl, timer, copies, layer, T, dev, 200, 24)
         b = sum(algorithmic_bytes(s, T) for s in layer.linears)
         res["layer_T%d" % T] = {"ms_per_step": round(ms, 5), "gbs": round(b / (ms * 1e-3) / 1e9, 1)}
     return res

@@ -598,8 +598,8 @@ void moe_kernel(MoeArgs a) {
 // (linear, slot, block of a.rb rows), the row blocks of one (linear, slot)
 // unit on one XCD (48-layer T = 1 step 18.8 -> 18.5 us).  It reads the slot's expert id, forms
 // the slot's activations in registers (the same fp16 pairs and chunk sums the
-// preparation writes), computes t = A_e[:r] x itself (each of its waves takes
-// rows i = wave + 4 p up to r_max, UR rows with all their loads in flight,
+// preparation writes), computes t = A_e[:r] x itself (each of its NWV waves
+// takes rows i = wave + NWV p below the rank, UR rows with all their loads in flight,
 // one butterfly sum per row; the slot's other workgroups repeat this small
 // product, r x d_in multiply-adds over A_e rows that L2 serves after the
 // first), and then applies its rows' codes with the arithmetic of
