@@ -275,9 +275,10 @@ cl_status cl_linear_decode_glu(const cl_qweight* w, const cl_lowrank* c, const v
  *  M          >= 1 tokens, M * d_in < 2^31
  *  Y          device [M][d_out] of out_dtype
  *  ws         device workspace of cl_prefill_workspace(w, c, M) bytes
- *             (2 M d_in for X'; with a rank term, 2 M r32 for T and
- *             4 M r32 ceil(d_in / 512) for its partial products, r32 the
- *             rank rounded up to 32), 256-byte aligned
+ *             (2 M128 d_in for X', M128 the tokens rounded up to 128;
+ *             2 M r32 for T, r32 the rank rounded up to 32; with a rank
+ *             term, 4 M r32 ceil(d_in / 256) for its partial products;
+ *             each part rounded up to 256 bytes), 256-byte aligned
  * Errors: as cl_linear_decode; CL_EUNSUPPORTED if d_in is not a multiple of
  * 64 or M * d_in >= 2^31.
  */
@@ -285,7 +286,7 @@ cl_status cl_linear_prefill(const cl_qweight* w, const cl_lowrank* c, const void
                             int32_t act_dtype, void* Y, int32_t out_dtype, void* ws, size_t ws_bytes,
                             void* stream);
 
-/* Workspace bytes for cl_linear_prefill (0 for rank 0 or rejected arguments). */
+/* Workspace bytes for cl_linear_prefill (0 for rejected arguments). */
 size_t cl_prefill_workspace(const cl_qweight* w, const cl_lowrank* c, int32_t M);
 
 /*

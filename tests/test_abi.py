@@ -101,6 +101,23 @@ def test_workspace_query_is_pure_and_sized_by_rank_and_tokens():
     assert lib.cl_last_error() == before
 
 
+def test_prefill_workspace_matches_its_documented_size():
+    """X' for the tokens rounded up to 128, T for the rank rounded up to 32,
+    and one fp32 partial product of T per 256 input columns, each part
+    rounded up to 256 bytes."""
+    lib = cl.lib()
+    up = lambda n: (n + 255) // 256 * 256
+    for d_in, M, rank in [(256, 16, 32), (4096, 2048, 64), (1024, 200, 17), (512, 1, 0)]:
+        qw = _qw(d_in=d_in)
+        lr = cl.LowRankC(FAKE, FAKE, max(rank, 1), rank)
+        r32 = (rank + 31) // 32 * 32
+        want = up((M + 127) // 128 * 128 * d_in * 2) + up(M * r32 * 2)
+        if rank:
+            want += up((d_in + 255) // 256 * M * r32 * 4)
+        assert lib.cl_prefill_workspace(ctypes.byref(qw), ctypes.byref(lr), M) == want, (d_in, M, rank)
+    assert lib.cl_prefill_workspace(ctypes.byref(_qw()), None, 0) == 0
+
+
 def test_quantize_pack_and_dequantize_validate():
     lib = cl.lib()
     p = ctypes.c_void_p(FAKE)
