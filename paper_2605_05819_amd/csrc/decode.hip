@@ -267,8 +267,12 @@ struct Batch {
 // with one workgroup per batch of the gate, so a workgroup's second batch is
 // the up batch of the same rows: the lanes that hold a gate total keep it and
 // write SiLU(gate) * up for the same row and token to a.h.
-template <int BITS, int NT, int CPL, int R, int NB, bool GLU>
-__global__ __launch_bounds__(512)
+// MAXT: the largest block the instance is launched with.  Instances for
+// several tokens per pass launched with 256 threads (one wave per SIMD per
+// workgroup) are built for that size, so registers beyond 256 per lane come
+// from the accumulation registers rather than from scratch memory.
+template <int BITS, int NT, int CPL, int R, int NB, bool GLU, int MAXT = 512>
+__global__ __launch_bounds__(MAXT)
 __attribute__((amdgpu_waves_per_eu(BITS == 4 && NT == 1 && CPL == 1 && NB <= 1 ? (GLU ? 6 : 7) : 1)))
 void decode_kernel(DecodeArgs a) {
     // a chunk is one lane's unit of codes: 16 bytes = 4 words of 32 / BITS
@@ -770,9 +774,10 @@ __global__ __launch_bounds__((GLU ? 2 : 1) * 64 * NW) void decode_mfma_kernel(De
         float tsum[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int p = 0; p < kPrefKp; ++p) {
-            if (p >= a.kp) break;
+            if (p < a.kp) {
 #pragma unroll
-            for (int e = 0; e < 4; ++e) { tsum[e] += o.tp[p][0][e]; tsum[4 + e] += o.tp[p][1][e]; }
+                for (int e = 0; e < 4; ++e) { tsum[e] += o.tp[p][0][e]; tsum[4 + e] += o.tp[p][1][e]; }
+            }
         }
         // long rows (more than kPrefKp K parts): the other partials now, in
         // the same order (holding them through the K loop cost a wave per
@@ -792,11 +797,12 @@ __global__ __launch_bounds__((GLU ? 2 : 1) * 64 * NW) void decode_mfma_kernel(De
             }
 #pragma unroll
             for (int p = kPrefKp; p < kMaxKp; ++p) {
-                if (p >= a.kp) break;
+                if (p < a.kp) {
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    tsum[e] += more[p - kPrefKp][0][e];
-                    tsum[4 + e] += more[p - kPrefKp][1][e];
+                    for (int e = 0; e < 4; ++e) {
+                        tsum[e] += more[p - kPrefKp][0][e];
+                        tsum[4 + e] += more[p - kPrefKp][1][e];
+                    }
                 }
             }
         }
@@ -984,13 +990,19 @@ int device_cus() {
 
 template <int BITS, int NT, int CPL, int R, int NB>
 hipError_t launch5(const DecodeArgs& a, const Plan& p, hipStream_t st) {
+    // the 256-thread build of the multi-token one-chunk instances (the rest
+    // are built for 512 threads only)
+    constexpr bool kSmall = NT > 1 && CPL == 1;
+    const bool small = kSmall && p.threads <= 256;
     if (a.h) {
         // gated window: workgroup i takes gate batch i, then up batch i
-        hipLaunchKernelGGL((decode_kernel<BITS, NT, CPL, R, NB, true>), dim3(a.lin[0].batch_end), dim3(p.threads), 0,
-                           st, a);
+        auto gk = small ? decode_kernel<BITS, NT, CPL, R, NB, true, kSmall ? 256 : 512>
+                        : decode_kernel<BITS, NT, CPL, R, NB, true>;
+        hipLaunchKernelGGL(gk, dim3(a.lin[0].batch_end), dim3(p.threads), 0, st, a);
         return hipGetLastError();
     }
-    auto kern = decode_kernel<BITS, NT, CPL, R, NB, false>;
+    auto kern = small ? decode_kernel<BITS, NT, CPL, R, NB, false, kSmall ? 256 : 512>
+                      : decode_kernel<BITS, NT, CPL, R, NB, false>;
     // resident workgroups per CU for this instance and block size (cached
     // once per process)
     static int occ[2] = {0, 0};
