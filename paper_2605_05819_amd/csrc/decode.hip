@@ -61,8 +61,8 @@ namespace {
 constexpr int kMaxWin = 8;   // linears per window
 constexpr int kMaxKp = 16;   // K parts of the many-token A x partials
 constexpr int kPrefKp = 4;   // of them loaded ahead of the backbone's K loop
-// 4-bit windows with this many tokens use the MFMA backbone (measured on the
-// Llama-8B layer: 2 tokens 72 us on the dot2 backbone against 88 us on MFMA,
+// 4- and 2-bit windows with this many tokens use the MFMA backbone (measured
+// on the 4-bit Llama-8B layer: 2 tokens 72 us on the dot2 backbone against 88 us on MFMA,
 // 3 tokens 123 against 88, 5-7 tokens ~185 against ~90)
 constexpr int kMfmaMinTokens = 3;
 
@@ -549,7 +549,7 @@ void decode_kernel(DecodeArgs a) {
 // tokens' 8 activations (16 bytes each, unpack order) side by side, so one
 // load instruction reads 256 contiguous bytes per lane group.
 __global__ __launch_bounds__(1024) void decode_prep_mfma_kernel(PrepMArgs a) {
-    constexpr int CPW = 8, HPW = 4, PPC = 16;        // 4-bit codes
+    constexpr int CPW = 8, HPW = 4, PPC = 16;        // 8-code units, the backbone's unpack order
     __shared__ f32x4 red[16][64];
     const int nw = blockDim.x >> 6;                  // waves per K part: 4, 8 or 16
     const int lane = threadIdx.x & 63;
@@ -636,16 +636,19 @@ __global__ __launch_bounds__(1024) void decode_prep_mfma_kernel(PrepMArgs a) {
     (void)PPC;
 }
 
-// Many-token backbone (4-bit codes, T >= 3): the contraction has enough
+// Many-token backbone (4- or 2-bit codes, T >= 3): the contraction has enough
 // columns to use MFMA (tokens padded to 16).  One workgroup per TPW 16-row
 // tiles of one linear; its four waves split the 128-code blocks of K (wave w
 // takes blocks w, w + 4, ...), NBUF blocks per wave in flight.  Per block a
-// lane loads, for each of its TPW tiles, 16 bytes of codes of row r = lane %
-// 16, and once for all tiles the matching activations of token r (four
+// lane loads, for each of its TPW tiles, its 32 codes of row r = lane % 16
+// (16 bytes at 4 bits, 8 at 2 bits), and once for all tiles the matching
+// activations of token r (four
 // 16-byte loads from the word-major layout, 256 or 1024 contiguous bytes per
 // load instruction).  The MFMA takes the activations as its A operand and the
 // codes as its B operand, so lane (g, r) accumulates tokens 4 g .. 4 g + 3 of
-// weight row r.  The codes become the exact fp16 integers q - z, and every
+// weight row r.  The codes become the exact fp16 integers q - z (2-bit
+// codes: each 8-code half of a word spread by a byte permute, then one mask
+// and one packed add or FMA per pair, codes2_minus_zero), and every
 // quantization group's MFMA steps run into a fresh fp32 partial that is
 // scaled by the group's fp16 scale in fp32 and added to the accumulator:
 // the backbone is s (sum (q - z) x) with fp32 rounding only, whatever the
@@ -660,8 +663,9 @@ __global__ __launch_bounds__(1024) void decode_prep_mfma_kernel(PrepMArgs a) {
 // fixed order and split into fp16 hi and lo parts, one step each); the
 // waves' tiles are summed through LDS in a fixed order; one rounding to the
 // output dtype.
-template <int TPW, int NBUF, bool GLU, int GPB, int NW, bool LONGK>
+template <int BITS, int TPW, int NBUF, bool GLU, int GPB, int NW, bool LONGK>
 __global__ __launch_bounds__((GLU ? 2 : 1) * 64 * NW) void decode_mfma_kernel(DecodeArgs a) {
+    static_assert(BITS == 4 || BITS == 2, "4- or 2-bit codes");
     // NW waves split K.  GLU: 2 NW waves, the first NW on the gate's tiles
     // and the other NW on the up tiles of the same rows (phase 1); the two
     // sets of sums meet in LDS and the first NW waves store SiLU(gate) * up
@@ -692,11 +696,15 @@ __global__ __launch_bounds__((GLU ? 2 : 1) * 64 * NW) void decode_mfma_kernel(De
     const bool tokv = tok < a.T;
     const int K = a.d_in;
     const int nkb = (K + 127) / 128;
-    const int words_row = K / 8;
+    const int words_row = K / 8;                  // 8-code units of a row (activation words)
+    const int qwords_row = K * BITS / 32;         // 32-bit code words of a row
     const int groups = K / a.G;
     uint16_t* const szl = szl_all + ph * (2 * 16 * TPW * groups);
     const uint32_t mlo = __builtin_amdgcn_readfirstlane(0x000F000Fu);
     const uint32_t mhi = __builtin_amdgcn_readfirstlane(0x00F000F0u);
+    uint32_t m2[4];
+#pragma unroll
+    for (int p = 0; p < 4; ++p) m2[p] = __builtin_amdgcn_readfirstlane(0x00030003u << (2 * p));
     const uint32_t bias = 0x64006400u;
     // this pass's activations, tp tokens per word: lane row r reads token
     // min(r, tp - 1) (rows past the pass's tokens repeat the last one; their
@@ -723,8 +731,10 @@ __global__ __launch_bounds__((GLU ? 2 : 1) * 64 * NW) void decode_mfma_kernel(De
                             : reinterpret_cast<const u32x4*>(a.xf);
     const u32x4 s_first = *s16p, z_first = *z16p;
 
+    // the lane's 32 codes of each tile row: 4 words (4-bit) or 2 (2-bit)
+    using CodeW = std::conditional_t<BITS == 4, u32x4, u32x2>;
     struct Blk {
-        u32x4 w[TPW];
+        CodeW w[TPW];
         u32x4 x[4];
     };
     // rank-r term, 32 factor columns per step, wave w taking steps w, w + 4:
@@ -836,11 +846,16 @@ __global__ __launch_bounds__((GLU ? 2 : 1) * 64 * NW) void decode_mfma_kernel(De
     // prefetched block stay in flight
     auto load = [&](int kb, Blk& b) {
         const int kc = kb * 128 + 32 * g;          // first of this lane's 32 codes
-        const int wi = kc < K ? kc / 8 : 0;
+        const int wi = kc < K ? kc / 8 : 0;        // its first 8-code unit
 #pragma unroll
-        for (int j = 0; j < TPW; ++j)
-            b.w[j] = __builtin_nontemporal_load(
-                reinterpret_cast<const u32x4*>(L.q + static_cast<size_t>(row[j]) * words_row + wi));
+        for (int j = 0; j < TPW; ++j) {
+            if constexpr (BITS == 4)
+                b.w[j] = __builtin_nontemporal_load(
+                    reinterpret_cast<const u32x4*>(L.q + static_cast<size_t>(row[j]) * words_row + wi));
+            else
+                b.w[j] = __builtin_nontemporal_load(
+                    reinterpret_cast<const u32x2*>(L.q + static_cast<size_t>(row[j]) * qwords_row + wi / 2));
+        }
         // the activations of the words this lane feeds to MFMA step t: word
         // 4 g + t of the block, or 4 t + g once the codes are transposed
         // (a word past K reads word g, met by a zero scale)
@@ -857,9 +872,15 @@ __global__ __launch_bounds__((GLU ? 2 : 1) * 64 * NW) void decode_mfma_kernel(De
         constexpr int SPG = 4 / GPB;               // MFMA steps per group
 #pragma unroll
         for (int j = 0; j < TPW; ++j) {
+            // w[t]: the lane's 8-code unit t (2-bit: spread for the masks)
             uint32_t w[4];
+            if constexpr (BITS == 4) {
 #pragma unroll
-            for (int t = 0; t < 4; ++t) { const uint32_t v = b.w[j][t]; w[t] = v; }
+                for (int t = 0; t < 4; ++t) { const uint32_t v = b.w[j][t]; w[t] = v; }
+            } else {
+#pragma unroll
+                for (int t = 0; t < 4; ++t) w[t] = spread_half2(b.w[j][t >> 1], t & 1);
+            }
             if constexpr (GPB > 1) transpose_words(w);
 #pragma unroll
             for (int q = 0; q < GPB; ++q) {
@@ -867,12 +888,21 @@ __global__ __launch_bounds__((GLU ? 2 : 1) * 64 * NW) void decode_mfma_kernel(De
                 const bool on = kb < nkb && kc < K && rowv[j];
                 const int lr = (16 * j + r) * groups + (on ? kc / a.G : 0);
                 const uint32_t sb = szl[lr], zb = szl[16 * TPW * groups + lr];
-                const Zq zq = make_zq(zb);
-                f32x4 p = mfma(b.x[SPG * q], codes_minus_zero(w[SPG * q], zq, mlo, mhi, bias),
-                               f32x4{0.f, 0.f, 0.f, 0.f});
+                f32x4 p;
+                if constexpr (BITS == 4) {
+                    const Zq zq = make_zq(zb);
+                    p = mfma(b.x[SPG * q], codes_minus_zero(w[SPG * q], zq, mlo, mhi, bias),
+                             f32x4{0.f, 0.f, 0.f, 0.f});
 #pragma unroll
-                for (int t = SPG * q + 1; t < SPG * q + SPG; ++t)
-                    p = mfma(b.x[t], codes_minus_zero(w[t], zq, mlo, mhi, bias), p);
+                    for (int t = SPG * q + 1; t < SPG * q + SPG; ++t)
+                        p = mfma(b.x[t], codes_minus_zero(w[t], zq, mlo, mhi, bias), p);
+                } else {
+                    const Zq2 zq = make_zq2(zb);
+                    p = mfma(b.x[SPG * q], codes2_minus_zero(w[SPG * q], zq, m2, bias), f32x4{0.f, 0.f, 0.f, 0.f});
+#pragma unroll
+                    for (int t = SPG * q + 1; t < SPG * q + SPG; ++t)
+                        p = mfma(b.x[t], codes2_minus_zero(w[t], zq, m2, bias), p);
+                }
                 acc[j] = fma4(on ? f16_bits_to_f32(static_cast<uint16_t>(sb)) : 0.f, p, acc[j]);
             }
         }
@@ -1056,9 +1086,11 @@ size_t up256(size_t n) { return (n + 255) / 256 * 256; }
 
 namespace {
 
-// 4-bit codes, enough tokens, and at most 512 quantization groups per row
-// (the MFMA backbone keeps its rows' scales and zeros in LDS)
-bool use_mfma(const QW& w, int T) { return w.bits == 4 && T >= kMfmaMinTokens && w.d_in / w.G <= 512; }
+// 4- or 2-bit codes, enough tokens, and at most 512 quantization groups per
+// row (the MFMA backbone keeps its rows' scales and zeros in LDS)
+bool use_mfma(const QW& w, int T) {
+    return (w.bits == 4 || w.bits == 2) && T >= kMfmaMinTokens && w.d_in / w.G <= 512;
+}
 
 // K parts of the MFMA preparation (at most 16, about 1024 codes each), the
 // waves of a part's workgroup (4, 8 or 16: enough that each wave has at most
@@ -1101,22 +1133,27 @@ MfmaCfg mfma_cfg(int tiles, int groups) {
 // take the extra partials without losing a wave per SIMD.
 bool long_k_ok(const MfmaCfg& c, int gpb) { return c.tpw == 1 && gpb == 1; }
 
-template <bool GLU, int GPB>
+template <int BITS, bool GLU, int GPB>
 auto pick_cfg(const MfmaCfg& c, bool longk) {
     constexpr int H = GPB == 1 ? 1 : 2;           // nbuf divisor
-    if (c.tpw == 4) return decode_mfma_kernel<4, 2 / H, GLU, GPB, 4, false>;
-    if (GPB == 1 && longk) return decode_mfma_kernel<1, 4, GLU, 1, 4, true>;
-    return decode_mfma_kernel<1, 4 / H, GLU, GPB, 4, false>;
+    if (c.tpw == 4) return decode_mfma_kernel<BITS, 4, 2 / H, GLU, GPB, 4, false>;
+    if (GPB == 1 && longk) return decode_mfma_kernel<BITS, 1, 4, GLU, 1, 4, true>;
+    return decode_mfma_kernel<BITS, 1, 4 / H, GLU, GPB, 4, false>;
 }
 
-template <bool GLU>
+template <int BITS, bool GLU>
 auto pick_gpb(const MfmaCfg& c, int gpb, bool longk) {
-    if (gpb == 1) return pick_cfg<GLU, 1>(c, longk);
-    return gpb == 2 ? pick_cfg<GLU, 2>(c, longk) : pick_cfg<GLU, 4>(c, longk);
+    if (gpb == 1) return pick_cfg<BITS, GLU, 1>(c, longk);
+    return gpb == 2 ? pick_cfg<BITS, GLU, 2>(c, longk) : pick_cfg<BITS, GLU, 4>(c, longk);
 }
 
-auto pick_mfma_kernel(const MfmaCfg& c, bool glu, int gpb, bool longk) {
-    return glu ? pick_gpb<true>(c, gpb, longk) : pick_gpb<false>(c, gpb, longk);
+template <int BITS>
+auto pick_glu(const MfmaCfg& c, bool glu, int gpb, bool longk) {
+    return glu ? pick_gpb<BITS, true>(c, gpb, longk) : pick_gpb<BITS, false>(c, gpb, longk);
+}
+
+auto pick_mfma_kernel(const MfmaCfg& c, int bits, bool glu, int gpb, bool longk) {
+    return bits == 2 ? pick_glu<2>(c, glu, gpb, longk) : pick_glu<4>(c, glu, gpb, longk);
 }
 
 }  // namespace
@@ -1205,7 +1242,7 @@ hipError_t launch_decode_mfma(int n, const QW* w, const LR* c, const void* x, in
     a.cps = 0;
     a.kp = mp.kp;
     a.h = glu ? y[0] : nullptr;
-    auto kern = pick_mfma_kernel(cfg, glu, gpb, mp.kp > kPrefKp);
+    auto kern = pick_mfma_kernel(cfg, w[0].bits, glu, gpb, mp.kp > kPrefKp);
     // a gated window runs one workgroup of eight waves per gate workgroup
     // (four waves on the gate's tiles, four on the up tiles of the same rows),
     // with both linears' scales and zeros in LDS

@@ -1,5 +1,5 @@
 // Device helpers shared by the MFMA kernels (prefill GEMM, many-token decode,
-// MoE): in-register unpack of 4-bit codes to exact fp16 integers q - z, the
+// MoE): in-register unpack of 4- and 2-bit codes to exact fp16 integers q - z, the
 // 4 x 4 transpose of code words across lane groups, and the fp16 MFMA.
 #pragma once
 
@@ -45,6 +45,49 @@ __device__ __forceinline__ u32x4 codes_minus_zero(uint32_t w, const Zq& zq, uint
     r[2] = __builtin_bit_cast(uint32_t, __builtin_bit_cast(f16x2, and_or(w8, mlo, bias)) + zq.lo);
     r[3] = __builtin_bit_cast(
         uint32_t, __builtin_elementwise_fma(__builtin_bit_cast(f16x2, and_or(w8, mhi, bias)), sixteenth, zq.hi));
+    return r;
+}
+
+// 2-bit codes.  One 8-code half of a word (h = 0: codes 0..7, h = 1: codes
+// 8..15) laid out for a mask per pair: bytes (b_2h, b_2h+1 | b_2h+1, 0), so
+// bits 2p..2p+1 of the low fp16 half hold code p and those of the high half
+// code p + 4 (one byte permute).
+__device__ __forceinline__ uint32_t spread_half2(uint32_t w, int h) {
+    return __builtin_amdgcn_perm(0u, w, h ? 0x0C030302u : 0x0C010100u);
+}
+
+// Zero-point constants of one 2-bit group: -(1024 / 4^p + z), p = 0..3, both
+// halves equal (exact: z < 4).
+struct Zq2 {
+    f16x2 c[4];
+};
+
+__device__ __forceinline__ Zq2 make_zq2(uint32_t zbits) {
+    const f16 z = __builtin_bit_cast(f16, static_cast<uint16_t>(zbits));
+    Zq2 r;
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+        const f16 v = -(static_cast<f16>(1024.0f / static_cast<float>(1 << (2 * p))) + z);
+        r.c[p] = f16x2{v, v};
+    }
+    return r;
+}
+
+// A spread 8-code half (spread_half2) -> 8 fp16 values q - z, exact integers
+// in -3..3, pair order (q0,q4),(q1,q5),(q2,q6),(q3,q7) as codes_minus_zero.
+// Pair p masked in place and OR-ed into the mantissa of 1024.0 reads as
+// 1024 + 4^p q; one fused multiply-add (1024 + 4^p q) 4^-p - (1024 4^-p + z)
+// is exact (p = 0: one add).  m[p] = 0x00030003 << 2p from scalar registers.
+__device__ __forceinline__ u32x4 codes2_minus_zero(uint32_t v, const Zq2& zq, const uint32_t (&m)[4],
+                                                   uint32_t bias) {
+    u32x4 r;
+    r[0] = __builtin_bit_cast(uint32_t, __builtin_bit_cast(f16x2, and_or(v, m[0], bias)) + zq.c[0]);
+#pragma unroll
+    for (int p = 1; p < 4; ++p) {
+        const f16 sc = static_cast<f16>(1.0f / static_cast<float>(1 << (2 * p)));
+        r[p] = __builtin_bit_cast(uint32_t, __builtin_elementwise_fma(__builtin_bit_cast(f16x2, and_or(v, m[p], bias)),
+                                                                      f16x2{sc, sc}, zq.c[p]));
+    }
     return r;
 }
 

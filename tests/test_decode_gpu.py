@@ -42,7 +42,7 @@ def test_single_linear_1024_rank16_all_out_dtypes():
         _check(w, c, Q, s, z, A, B, 16, x, torch.float16, od, 4, 128)
 
 
-@pytest.mark.parametrize("bits,G", [(4, 128), (2, 64), (4, 32), (3, 128), (3, 32)])
+@pytest.mark.parametrize("bits,G", [(4, 128), (2, 64), (2, 128), (4, 32), (3, 128), (3, 32)])
 @pytest.mark.parametrize("d_out,d_in", [(37, 256), (1000, 768), (4099, 1536)])
 @pytest.mark.parametrize("T", [1, 3, 4, 5, 16])
 def test_ragged_shapes_tokens_and_bits(bits, G, d_out, d_in, T):
@@ -150,6 +150,29 @@ def test_llama_layer_3bit_full_size_sampled_rows(mat, T):
         Q, s, z = quant.quantize_pack(W[rows], 3, 128)
         ref = linear.forward_packed(Q, s, z, 3, 128, A, B[rows], spec.rank, x.values)
         assert_oracle(out_to_numpy(y)[:, rows], ref, od)
+
+
+@pytest.mark.parametrize("mat", wl.LLAMA_MATS)
+@pytest.mark.parametrize("T", [4, 16])
+def test_llama_layer_2bit_many_tokens_full_size_sampled_rows(mat, T):
+    """Every Llama-8B layer linear with 2-bit codes (group 64) at full size,
+    quantized on the GPU, with its allocated rank, at 4 and 16 tokens (the
+    MFMA backbone with two quantization groups per 128-code block); sampled
+    rows against the oracle, which quantizes those rows itself."""
+    layer = wl.llama_layer_2bit()
+    spec = [l for l in layer.linears if l.name == mat][0]
+    m = wl.LLAMA_MATS.index(mat)
+    W = wl.weight((spec.d_out, spec.d_in), layer.index, 0, m)
+    w = cl.quantize_pack(torch.from_numpy(W).cuda(), 2, 64)
+    A, B = wl.standin_factors(spec.d_out, spec.d_in, spec.r_max, layer.index, 0, m)
+    c = cl.LowRank(dev_f16(A), dev_f16(B), spec.r_max, spec.rank)
+    x = wl.activation((T, spec.d_in), layer.index, 0, m)
+    y = cl.linear_decode(w, c, dev_u16(x.bits, torch.float16), out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    rows = np.r_[0:4, np.random.default_rng(m).choice(spec.d_out, 120, replace=False), spec.d_out - 4:spec.d_out]
+    Q, s, z = quant.quantize_pack(W[rows], 2, 64)
+    ref = linear.forward_packed(Q, s, z, 2, 64, A, B[rows], spec.rank, x.values)
+    assert_oracle(out_to_numpy(y)[:, rows], ref)
 
 
 @pytest.mark.parametrize("T", [9, 16, 40])
@@ -304,11 +327,13 @@ def _glu_ref_rows(host, ranks, bits, G, d_in, X, rows):
     (1, torch.float16, torch.float16, 4, 128, 1000, 2048),      # one token per pass, one K slice
     (2, torch.bfloat16, torch.float32, 4, 128, 1000, 4096),     # two tokens per pass (prefetch), 2 K slices
     (3, torch.float16, torch.bfloat16, 4, 128, 1000, 2048),     # MFMA backbone, ragged last tile
-    (5, torch.float16, torch.float16, 2, 64, 700, 1024),        # 2-bit, two passes of 4 tokens
+    (5, torch.float16, torch.float16, 2, 64, 700, 1024),        # 2-bit, MFMA, two groups per block
     (1, torch.float16, torch.float32, 4, 128, 14336, 4096),     # Llama-8B gate/up, one token
     (16, torch.float16, torch.float32, 4, 128, 14336, 4096),    # Llama-8B gate/up, MFMA with 4 tiles per wave
     (64, torch.bfloat16, torch.float16, 4, 128, 1000, 2048),    # the most tokens: four MFMA passes
-    (4, torch.float16, torch.bfloat16, 2, 64, 1000, 4096),      # 2-bit, one pass of 4 tokens
+    (4, torch.float16, torch.bfloat16, 2, 64, 1000, 4096),      # 2-bit, MFMA, one tile per wave
+    (2, torch.float16, torch.float16, 2, 64, 1000, 4096),       # 2-bit, two tokens per pass (dot2)
+    (16, torch.float16, torch.float32, 2, 64, 14336, 4096),     # 2-bit Llama-8B gate/up, MFMA, 4 tiles per wave
     (1, torch.float16, torch.bfloat16, 3, 128, 1000, 2048),     # 3-bit, one token
     (6, torch.bfloat16, torch.float16, 3, 32, 700, 1024),       # 3-bit, passes of 4 and 2 tokens
 ])
