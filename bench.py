@@ -251,7 +251,8 @@ def bench_glu(torch, cl, wl, timer, copies, layer, dev):
 
 def bench_layer2bit(torch, cl, wl, timer, dev, rotate_gib):
     """The 2-bit group-64 layer (ranks up to 256 under 128 x 7) at one token,
-    and the rank sweep r in {0, 32, 128, 256} on its 14336 x 4096 gate."""
+    the rank sweep r in {0, 32, 128, 256} on its 14336 x 4096 gate, and the
+    layer at 4 and 16 tokens (MFMA backbone)."""
     layer2 = wl.llama_layer_2bit()
     copies2 = device_layer(torch, cl, wl, layer2, dev, rotate_gib)
     ms2, xs2, ys2 = layer_step(torch, cl, wl, timer, copies2, layer2, 1, dev, 80, 8)
@@ -261,8 +262,13 @@ def bench_layer2bit(torch, cl, wl, timer, dev, rotate_gib):
     for r in (0, 32, 128, 256):
         u = per_matrix(torch, cl, timer, copies2, layer2.linears, xs2, ys2, 1, dev, rank=r, m_only=g2)["gate"]
         sweep["r%d" % r] = {"us": round(u, 3), "gbs": round(algorithmic_bytes(layer2.linears[g2], 1, r) / u / 1e3, 1)}
+    many = {}
+    for T in (4, 16):
+        msT, _, _ = layer_step(torch, cl, wl, timer, copies2, layer2, T, dev, 80, 8)
+        bT = sum(algorithmic_bytes(s, T) for s in layer2.linears)
+        many["T%d" % T] = {"ms_per_step": round(msT, 5), "gbs": round(bT / (msT * 1e-3) / 1e9, 1)}
     return {"ms_per_step": round(ms2, 5), "gbs": round(b2 / (ms2 * 1e-3) / 1e9, 1),
-            "ranks": "/".join(str(s.rank) for s in layer2.linears), "gate_rank_sweep": sweep}
+            "ranks": "/".join(str(s.rank) for s in layer2.linears), "gate_rank_sweep": sweep, **many}
 
 
 def bench_single(torch, cl, wl, timer, dev, rotate_gib):
@@ -295,12 +301,12 @@ def bench_single(torch, cl, wl, timer, dev, rotate_gib):
 
 def bench_layer3bit(torch, cl, wl, timer, dev, rotate_gib):
     """The 3-bit group-128 layer (the paper's INT3 dense setting; ranks
-    from {0, 16, 32, 64, 128} under 64 x 7) at one and four tokens, on the
-    dot2 backbone."""
+    from {0, 16, 32, 64, 128} under 64 x 7) at 1, 4 and 16 tokens (dot2
+    backbone at one token, MFMA from three)."""
     layer3 = wl.llama_layer_3bit()
     copies3 = device_layer(torch, cl, wl, layer3, dev, rotate_gib)
     res = {"ranks": "/".join(str(s.rank) for s in layer3.linears)}
-    for T in (1, 4):
+    for T in (1, 4, 16):
         ms3, xs3, ys3 = layer_step(torch, cl, wl, timer, copies3, layer3, T, dev, 80, 8)
         b3 = sum(algorithmic_bytes(s, T) for s in layer3.linears)
         res["T%d" % T] = {"ms_per_step": round(ms3, 5), "gbs": round(b3 / (ms3 * 1e-3) / 1e9, 1),

@@ -61,8 +61,8 @@ namespace {
 constexpr int kMaxWin = 8;   // linears per window
 constexpr int kMaxKp = 16;   // K parts of the many-token A x partials
 constexpr int kPrefKp = 4;   // of them loaded ahead of the backbone's K loop
-// 4- and 2-bit windows with this many tokens use the MFMA backbone (measured
-// on the 4-bit Llama-8B layer: 2 tokens 72 us on the dot2 backbone against 88 us on MFMA,
+// Windows with this many tokens use the MFMA backbone (measured on the 4-bit
+// Llama-8B layer: 2 tokens 72 us on the dot2 backbone against 88 us on MFMA,
 // 3 tokens 123 against 88, 5-7 tokens ~185 against ~90)
 constexpr int kMfmaMinTokens = 3;
 
@@ -636,19 +636,20 @@ __global__ __launch_bounds__(1024) void decode_prep_mfma_kernel(PrepMArgs a) {
     (void)PPC;
 }
 
-// Many-token backbone (4- or 2-bit codes, T >= 3): the contraction has enough
+// Many-token backbone (4-, 3- or 2-bit codes, T >= 3): the contraction has enough
 // columns to use MFMA (tokens padded to 16).  One workgroup per TPW 16-row
 // tiles of one linear; its four waves split the 128-code blocks of K (wave w
 // takes blocks w, w + 4, ...), NBUF blocks per wave in flight.  Per block a
 // lane loads, for each of its TPW tiles, its 32 codes of row r = lane % 16
-// (16 bytes at 4 bits, 8 at 2 bits), and once for all tiles the matching
+// (16 bytes at 4 bits, 12 at 3, 8 at 2), and once for all tiles the matching
 // activations of token r (four
 // 16-byte loads from the word-major layout, 256 or 1024 contiguous bytes per
 // load instruction).  The MFMA takes the activations as its A operand and the
 // codes as its B operand, so lane (g, r) accumulates tokens 4 g .. 4 g + 3 of
-// weight row r.  The codes become the exact fp16 integers q - z (2-bit
-// codes: each 8-code half of a word spread by a byte permute, then one mask
-// and one packed add or FMA per pair, codes2_minus_zero), and every
+// weight row r.  The codes become the exact fp16 integers q - z (2- and
+// 3-bit codes: each 8-code unit spread by a byte permute, then one mask and
+// one packed add or FMA per pair, codes2_minus_zero, codes3_minus_zero), and
+// every
 // quantization group's MFMA steps run into a fresh fp32 partial that is
 // scaled by the group's fp16 scale in fp32 and added to the accumulator:
 // the backbone is s (sum (q - z) x) with fp32 rounding only, whatever the
@@ -665,7 +666,7 @@ __global__ __launch_bounds__(1024) void decode_prep_mfma_kernel(PrepMArgs a) {
 // output dtype.
 template <int BITS, int TPW, int NBUF, bool GLU, int GPB, int NW, bool LONGK>
 __global__ __launch_bounds__((GLU ? 2 : 1) * 64 * NW) void decode_mfma_kernel(DecodeArgs a) {
-    static_assert(BITS == 4 || BITS == 2, "4- or 2-bit codes");
+    static_assert(BITS == 4 || BITS == 3 || BITS == 2, "4-, 3- or 2-bit codes");
     // NW waves split K.  GLU: 2 NW waves, the first NW on the gate's tiles
     // and the other NW on the up tiles of the same rows (phase 1); the two
     // sets of sums meet in LDS and the first NW waves store SiLU(gate) * up
@@ -702,9 +703,11 @@ __global__ __launch_bounds__((GLU ? 2 : 1) * 64 * NW) void decode_mfma_kernel(De
     uint16_t* const szl = szl_all + ph * (2 * 16 * TPW * groups);
     const uint32_t mlo = __builtin_amdgcn_readfirstlane(0x000F000Fu);
     const uint32_t mhi = __builtin_amdgcn_readfirstlane(0x00F000F0u);
-    uint32_t m2[4];
+    uint32_t m2[4], m3[3];
 #pragma unroll
     for (int p = 0; p < 4; ++p) m2[p] = __builtin_amdgcn_readfirstlane(0x00030003u << (2 * p));
+#pragma unroll
+    for (int p = 0; p < 3; ++p) m3[p] = __builtin_amdgcn_readfirstlane(0x00070007u << (3 * p));
     const uint32_t bias = 0x64006400u;
     // this pass's activations, tp tokens per word: lane row r reads token
     // min(r, tp - 1) (rows past the pass's tokens repeat the last one; their
@@ -731,8 +734,13 @@ __global__ __launch_bounds__((GLU ? 2 : 1) * 64 * NW) void decode_mfma_kernel(De
                             : reinterpret_cast<const u32x4*>(a.xf);
     const u32x4 s_first = *s16p, z_first = *z16p;
 
-    // the lane's 32 codes of each tile row: 4 words (4-bit) or 2 (2-bit)
-    using CodeW = std::conditional_t<BITS == 4, u32x4, u32x2>;
+    // the lane's 32 codes of each tile row: 4 words (4-bit), 3 (3-bit) or 2
+    // (2-bit)
+    struct U3 {
+        uint32_t e[3];
+        __device__ uint32_t operator[](int i) const { return e[i]; }
+    };
+    using CodeW = std::conditional_t<BITS == 4, u32x4, std::conditional_t<BITS == 3, U3, u32x2>>;
     struct Blk {
         CodeW w[TPW];
         u32x4 x[4];
@@ -849,12 +857,18 @@ __global__ __launch_bounds__((GLU ? 2 : 1) * 64 * NW) void decode_mfma_kernel(De
         const int wi = kc < K ? kc / 8 : 0;        // its first 8-code unit
 #pragma unroll
         for (int j = 0; j < TPW; ++j) {
-            if constexpr (BITS == 4)
+            if constexpr (BITS == 4) {
                 b.w[j] = __builtin_nontemporal_load(
                     reinterpret_cast<const u32x4*>(L.q + static_cast<size_t>(row[j]) * words_row + wi));
-            else
+            } else if constexpr (BITS == 3) {
+                // chunk wi / 4 of the row: words 3 (wi / 4) .. + 2
+                const uint32_t* src = L.q + static_cast<size_t>(row[j]) * qwords_row + 3 * (wi / 4);
+#pragma unroll
+                for (int e = 0; e < 3; ++e) b.w[j].e[e] = __builtin_nontemporal_load(src + e);
+            } else {
                 b.w[j] = __builtin_nontemporal_load(
                     reinterpret_cast<const u32x2*>(L.q + static_cast<size_t>(row[j]) * qwords_row + wi / 2));
+            }
         }
         // the activations of the words this lane feeds to MFMA step t: word
         // 4 g + t of the block, or 4 t + g once the codes are transposed
@@ -877,6 +891,9 @@ __global__ __launch_bounds__((GLU ? 2 : 1) * 64 * NW) void decode_mfma_kernel(De
             if constexpr (BITS == 4) {
 #pragma unroll
                 for (int t = 0; t < 4; ++t) { const uint32_t v = b.w[j][t]; w[t] = v; }
+            } else if constexpr (BITS == 3) {
+#pragma unroll
+                for (int t = 0; t < 4; ++t) w[t] = spread_unit3(b.w[j][0], b.w[j][1], b.w[j][2], t);
             } else {
 #pragma unroll
                 for (int t = 0; t < 4; ++t) w[t] = spread_half2(b.w[j][t >> 1], t & 1);
@@ -896,6 +913,12 @@ __global__ __launch_bounds__((GLU ? 2 : 1) * 64 * NW) void decode_mfma_kernel(De
 #pragma unroll
                     for (int t = SPG * q + 1; t < SPG * q + SPG; ++t)
                         p = mfma(b.x[t], codes_minus_zero(w[t], zq, mlo, mhi, bias), p);
+                } else if constexpr (BITS == 3) {
+                    const Zq3 zq = make_zq3(zb);
+                    p = mfma(b.x[SPG * q], codes3_minus_zero(w[SPG * q], zq, m3, bias), f32x4{0.f, 0.f, 0.f, 0.f});
+#pragma unroll
+                    for (int t = SPG * q + 1; t < SPG * q + SPG; ++t)
+                        p = mfma(b.x[t], codes3_minus_zero(w[t], zq, m3, bias), p);
                 } else {
                     const Zq2 zq = make_zq2(zb);
                     p = mfma(b.x[SPG * q], codes2_minus_zero(w[SPG * q], zq, m2, bias), f32x4{0.f, 0.f, 0.f, 0.f});
@@ -1086,11 +1109,9 @@ size_t up256(size_t n) { return (n + 255) / 256 * 256; }
 
 namespace {
 
-// 4- or 2-bit codes, enough tokens, and at most 512 quantization groups per
-// row (the MFMA backbone keeps its rows' scales and zeros in LDS)
-bool use_mfma(const QW& w, int T) {
-    return (w.bits == 4 || w.bits == 2) && T >= kMfmaMinTokens && w.d_in / w.G <= 512;
-}
+// Enough tokens, and at most 512 quantization groups per row (the MFMA
+// backbone keeps its rows' scales and zeros in LDS)
+bool use_mfma(const QW& w, int T) { return T >= kMfmaMinTokens && w.d_in / w.G <= 512; }
 
 // K parts of the MFMA preparation (at most 16, about 1024 codes each), the
 // waves of a part's workgroup (4, 8 or 16: enough that each wave has at most
@@ -1144,7 +1165,9 @@ auto pick_cfg(const MfmaCfg& c, bool longk) {
 template <int BITS, bool GLU>
 auto pick_gpb(const MfmaCfg& c, int gpb, bool longk) {
     if (gpb == 1) return pick_cfg<BITS, GLU, 1>(c, longk);
-    return gpb == 2 ? pick_cfg<BITS, GLU, 2>(c, longk) : pick_cfg<BITS, GLU, 4>(c, longk);
+    // 2-bit groups are multiples of 64 codes: at most two per block
+    if constexpr (BITS == 2) return pick_cfg<BITS, GLU, 2>(c, longk);
+    else return gpb == 2 ? pick_cfg<BITS, GLU, 2>(c, longk) : pick_cfg<BITS, GLU, 4>(c, longk);
 }
 
 template <int BITS>
@@ -1153,6 +1176,7 @@ auto pick_glu(const MfmaCfg& c, bool glu, int gpb, bool longk) {
 }
 
 auto pick_mfma_kernel(const MfmaCfg& c, int bits, bool glu, int gpb, bool longk) {
+    if (bits == 3) return pick_glu<3>(c, glu, gpb, longk);
     return bits == 2 ? pick_glu<2>(c, glu, gpb, longk) : pick_glu<4>(c, glu, gpb, longk);
 }
 

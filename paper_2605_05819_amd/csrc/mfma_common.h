@@ -1,5 +1,5 @@
 // Device helpers shared by the MFMA kernels (prefill GEMM, many-token decode,
-// MoE): in-register unpack of 4- and 2-bit codes to exact fp16 integers q - z, the
+// MoE): in-register unpack of 4-, 3- and 2-bit codes to exact fp16 integers q - z, the
 // 4 x 4 transpose of code words across lane groups, and the fp16 MFMA.
 #pragma once
 
@@ -88,6 +88,55 @@ __device__ __forceinline__ u32x4 codes2_minus_zero(uint32_t v, const Zq2& zq, co
         r[p] = __builtin_bit_cast(uint32_t, __builtin_elementwise_fma(__builtin_bit_cast(f16x2, and_or(v, m[p], bias)),
                                                                       f16x2{sc, sc}, zq.c[p]));
     }
+    return r;
+}
+
+// 3-bit codes.  A lane's 32 codes are three words; 8-code unit t (codes
+// 8t .. 8t + 7) is bytes 3t .. 3t + 2, code i at bits 3i of those 24.
+// Spread for a mask per pair: a byte permute gives x = (b0 b1 | b1 b2) (bits
+// 0..15 and 8..23 of the unit), then the low half keeps x's low half and the
+// high half takes x >> 4, so codes 0..3 sit at bits 0, 3, 6, 9 of the low
+// fp16 half and codes 4..7 at the same offsets of the high half.
+__device__ __forceinline__ uint32_t spread_unit3(uint32_t w0, uint32_t w1, uint32_t w2, int t) {
+    const uint32_t x = t == 0   ? __builtin_amdgcn_perm(w1, w0, 0x02010100u)
+                       : t == 1 ? __builtin_amdgcn_perm(w1, w0, 0x05040403u)
+                       : t == 2 ? __builtin_amdgcn_perm(w2, w1, 0x04030302u)
+                                : __builtin_amdgcn_perm(0u, w2, 0x03020201u);
+    return (x & 0x0000FFFFu) | ((x >> 4) & 0xFFFF0000u);
+}
+
+// Zero-point constants of one 3-bit group: -(1024 + z), -(128 + z), -(16 + z)
+// in both halves (exact: z < 8).
+struct Zq3 {
+    f16x2 c[3];
+};
+
+__device__ __forceinline__ Zq3 make_zq3(uint32_t zbits) {
+    const f16 z = __builtin_bit_cast(f16, static_cast<uint16_t>(zbits));
+    const f16 a = -(static_cast<f16>(1024.0f) + z), b = -(static_cast<f16>(128.0f) + z),
+              c = -(static_cast<f16>(16.0f) + z);
+    return Zq3{{f16x2{a, a}, f16x2{b, b}, f16x2{c, c}}};
+}
+
+// A spread 3-bit unit (spread_unit3) -> 8 fp16 values q - z, exact integers
+// in -7..7, pair order (q0,q4),(q1,q5),(q2,q6),(q3,q7) as codes_minus_zero.
+// Pairs 0, 1, 2 are masked in place at bits 0, 3, 6 and OR-ed into 1024.0
+// (1024 + q, 1024 + 8 q, 1024 + 64 q); pair 3 (bits 9..11, past the fp16
+// mantissa) is shifted down to bits 6..8 first.  One add or fused
+// multiply-add by 8^-p per pair is exact.  m[p] = 0x00070007 << 3p (p < 3)
+// from scalar registers.
+__device__ __forceinline__ u32x4 codes3_minus_zero(uint32_t v, const Zq3& zq, const uint32_t (&m)[3],
+                                                   uint32_t bias) {
+    const f16x2 e8 = {static_cast<f16>(0.125f), static_cast<f16>(0.125f)};
+    const f16x2 e64 = {static_cast<f16>(0.015625f), static_cast<f16>(0.015625f)};
+    u32x4 r;
+    r[0] = __builtin_bit_cast(uint32_t, __builtin_bit_cast(f16x2, and_or(v, m[0], bias)) + zq.c[0]);
+    r[1] = __builtin_bit_cast(uint32_t,
+                              __builtin_elementwise_fma(__builtin_bit_cast(f16x2, and_or(v, m[1], bias)), e8, zq.c[1]));
+    r[2] = __builtin_bit_cast(uint32_t,
+                              __builtin_elementwise_fma(__builtin_bit_cast(f16x2, and_or(v, m[2], bias)), e64, zq.c[2]));
+    r[3] = __builtin_bit_cast(
+        uint32_t, __builtin_elementwise_fma(__builtin_bit_cast(f16x2, and_or(v >> 3, m[2], bias)), e64, zq.c[2]));
     return r;
 }
 

@@ -130,7 +130,7 @@ def test_llama_layer_full_size_sampled_rows(mat, T):
 
 
 @pytest.mark.parametrize("mat", wl.LLAMA_MATS)
-@pytest.mark.parametrize("T", [1, 4])
+@pytest.mark.parametrize("T", [1, 4, 16])
 def test_llama_layer_3bit_full_size_sampled_rows(mat, T):
     """The paper's INT3 setting: every Llama-8B layer linear with 3-bit codes
     (group 128) at full size, quantized on the GPU, with its allocated rank;
@@ -335,7 +335,9 @@ def _glu_ref_rows(host, ranks, bits, G, d_in, X, rows):
     (2, torch.float16, torch.float16, 2, 64, 1000, 4096),       # 2-bit, two tokens per pass (dot2)
     (16, torch.float16, torch.float32, 2, 64, 14336, 4096),     # 2-bit Llama-8B gate/up, MFMA, 4 tiles per wave
     (1, torch.float16, torch.bfloat16, 3, 128, 1000, 2048),     # 3-bit, one token
-    (6, torch.bfloat16, torch.float16, 3, 32, 700, 1024),       # 3-bit, passes of 4 and 2 tokens
+    (6, torch.bfloat16, torch.float16, 3, 32, 700, 1024),       # 3-bit, MFMA, four groups per block
+    (2, torch.bfloat16, torch.float16, 3, 64, 700, 1024),       # 3-bit, two tokens per pass (dot2)
+    (16, torch.float16, torch.float32, 3, 128, 14336, 4096),    # 3-bit Llama-8B gate/up, MFMA, 4 tiles per wave
 ])
 def test_glu_matches_oracle(T, act, out, bits, G, d_out, d_in):
     """cl_linear_decode_glu = SiLU(gate x) * (up x) of the fp64 oracle (gate
