@@ -319,18 +319,20 @@ def bench_layer3bit(torch, cl, wl, timer, dev, rotate_gib):
 
 
 def bench_prefill(torch, cl, wl, timer, dev):
-    """M = 2048 tokens through 4096 x 4096 and 14336 x 4096, rank 64, fp16
-    and bf16 activations: us per call and TFLOP/s (2MNK + 2Mr(K + N)); and,
-    for scale, torch's fp16 matrix product of the same shape (2MNK)."""
+    """M = 2048 tokens through 4096 x 4096 and 14336 x 4096, rank 64, 4-bit
+    codes with fp16 and bf16 activations, and 3-bit codes (the paper's INT3
+    setting) with fp16 activations through 14336 x 4096: us per call and
+    TFLOP/s (2MNK + 2Mr(K + N)); and, for scale, torch's fp16 matrix
+    product of the same shape (2MNK)."""
     M, r = 2048, 64
     res = {}
-    for (N, K) in ((4096, 4096), (14336, 4096)):
+    for (N, K, bits) in ((4096, 4096, 4), (14336, 4096, 4), (14336, 4096, 3)):
         W = torch.from_numpy(wl.weight((N, K), 3, 0, N)).to(dev)
-        w = cl.quantize_pack(W, 4, 128)
+        w = cl.quantize_pack(W, bits, 128)
         del W
         A, B = wl.standin_factors(N, K, r, 3, 0, N)
         c = cl.LowRank(torch.from_numpy(A).to(dev), torch.from_numpy(B).to(dev), r, r)
-        for act in ("fp16", "bf16"):
+        for act in (("fp16", "bf16") if bits == 4 else ("fp16",)):
             x = wl.activation((M, K), 3, 0, N, dtype=act)
             dt = torch.float16 if act == "fp16" else torch.bfloat16
             X = torch.from_numpy(x.bits.view(np.int16)).view(dt).to(dev)
@@ -340,7 +342,10 @@ def bench_prefill(torch, cl, wl, timer, dev):
             g = timer.capture(lambda: cl.linear_prefill(w, c, X, Y=Y, ws=ws, stream=timer.stream))
             us = timer.time([g], 30) * 1e3
             flops = 2.0 * M * N * K + 2.0 * M * r * (K + N)
-            res["%dx%d_%s" % (N, K, act)] = {"us": round(us, 2), "tflops": round(flops / us / 1e6, 1)}
+            key = "%dx%d_%s" % (N, K, act) if bits == 4 else "%dx%d_w3_%s" % (N, K, act)
+            res[key] = {"us": round(us, 2), "tflops": round(flops / us / 1e6, 1)}
+        if bits != 4:
+            continue
         # reference: the bare fp16 contraction through torch (hipBLASLt) on
         # the same shape, no dequantization and no rank term
         Xr = torch.randn((M, K), dtype=torch.float16, device=dev)

@@ -29,13 +29,16 @@
  *
  * Packed backbone layout (cl_qweight)
  * -----------------------------------
- *  q       uint32 [d_out][d_in * bits / 32]; the code of column c is in word
- *          c / (32/bits) of its row at bit offset bits * (c % (32/bits))
- *          (LSB first).  16-byte aligned.
+ *  q       uint32 [d_out][d_in * bits / 32].  2 and 4 bits: the code of
+ *          column c is in word c / (32/bits) of its row at bit offset
+ *          bits * (c % (32/bits)) (LSB first).  3 bits: columns 32 j ..
+ *          32 j + 31 fill words 3 j .. 3 j + 2 of the row, column 32 j + i at
+ *          bit offset 3 i of those 96 bits (little-endian).  16-byte aligned.
  *  scales  fp16   [d_out][d_in / group_size], the group's step size.
  *  zeros   fp16   [d_out][d_in / group_size], integer zero point 0..2^bits-1.
- *  bits in {2, 4}; group_size a multiple of 128/bits (a 16-byte run of codes
- *  never straddles two groups); d_in a multiple of group_size.
+ *  bits in {2, 3, 4}; group_size a multiple of 128/bits at 2 and 4 bits (a
+ *  16-byte run of codes never straddles two groups) and of 32 at 3 bits;
+ *  d_in a multiple of group_size, and of 128 at 3 bits.
  *
  * Compensation factors (cl_lowrank)
  * ---------------------------------
@@ -57,7 +60,7 @@ typedef int32_t cl_status;
 enum {
     CL_OK = 0,
     CL_EINVAL = 1,        /* bad argument: null pointer, bad size, misalignment */
-    CL_EUNSUPPORTED = 2,  /* well-formed but not implemented (e.g. bits = 3)    */
+    CL_EUNSUPPORTED = 2,  /* well-formed but not implemented (e.g. bits = 5)    */
     CL_EWORKSPACE = 3,    /* workspace missing or smaller than required         */
     CL_EHIP = 4           /* the HIP runtime reported an error at launch        */
 };
@@ -99,7 +102,7 @@ typedef struct cl_lowrank {
  *  scales, zeros  device fp16 [d_out][d_in/group_size] (outputs)
  * Errors: CL_EINVAL for null pointers, non-positive sizes, misaligned q or a
  * group_size / d_in that breaks the layout rules above; CL_EUNSUPPORTED for
- * bits other than 2 and 4.
+ * bits other than 2, 3 and 4.
  */
 cl_status cl_quantize_pack(const float* W, int32_t d_out, int32_t d_in, int32_t bits,
                            int32_t group_size, uint32_t* q, uint16_t* scales, uint16_t* zeros,

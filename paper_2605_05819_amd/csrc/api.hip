@@ -271,7 +271,7 @@ size_t cl_prefill_workspace(const cl_qweight* w, const cl_lowrank* c, int32_t M)
     cl::QW qw;
     cl::LR lr;
     size_t bytes = 0;
-    if (M >= 1 && check_qweight(w, &qw, "") == CL_OK && qw.bits != 3 && check_lowrank(c, qw, &lr, "") == CL_OK)
+    if (M >= 1 && check_qweight(w, &qw, "") == CL_OK && check_lowrank(c, qw, &lr, "") == CL_OK)
         bytes = cl::prefill_workspace_bytes(qw, lr, M);
     memcpy(g_err, saved, sizeof(g_err));
     return bytes;
@@ -286,7 +286,6 @@ cl_status cl_linear_prefill(const cl_qweight* w, const cl_lowrank* c, const void
     if (st) return st;
     st = check_lowrank(c, qw, &lr, who);
     if (st) return st;
-    if (qw.bits == 3) return fail(CL_EUNSUPPORTED, "%s: 3-bit codes run on the decode entry points only", who);
     if (qw.d_in % 64) return fail(CL_EUNSUPPORTED, "%s: d_in must be a multiple of 64 (got %d)", who, qw.d_in);
     if (M < 1) return fail(CL_EINVAL, "%s: M must be >= 1 (got %d)", who, M);
     if (static_cast<long long>(M) * qw.d_in > (1ll << 31) - 1)

@@ -81,6 +81,20 @@ __device__ __forceinline__ u32x4 dequant_half2(uint32_t w, int h, f16x2 s2, f16x
     return r;
 }
 
+// One 8-code unit t (codes 8t .. 8t + 7) of a lane's 3-bit chunk -> 8 fp16
+// values s * (q - z), pair order as above: q - z exact (codes3_minus_zero),
+// then one rounding per value.
+__device__ __forceinline__ u32x4 dequant_unit3(const uint32_t (&w)[3], int t, const Zq3& zq, f16x2 s2,
+                                               const uint32_t (&m)[3], uint32_t bias) {
+    u32x4 r = codes3_minus_zero(spread_unit3(w[0], w[1], w[2], t), zq, m, bias);
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+        const uint32_t v = r[p];
+        r[p] = __builtin_bit_cast(uint32_t, __builtin_bit_cast(f16x2, v) * s2);
+    }
+    return r;
+}
+
 struct PrefillArgs {
     const uint32_t* q;
     const uint16_t* s;
@@ -230,10 +244,10 @@ __device__ __forceinline__ void global_to_lds16(const uint16_t* src, u32x4* dst)
 __device__ __forceinline__ int xswz(int r) { return ((r >> 1) & 3) | ((r & 1) << 2) | (r & 8); }
 
 // One K step's packed codes of a lane: 32 codes of one weight row (4-bit:
-// four words; 2-bit: two words), with their group's scale and zero.
+// four words; 3-bit: three; 2-bit: two), with their group's scale and zero.
 template <int BITS>
 struct WStep {
-    uint32_t w[BITS];        // 4-bit: 4 words, 2-bit: 2 words
+    uint32_t w[BITS];        // 32 codes = BITS words
 };
 
 template <int BITS, int JT>
@@ -339,6 +353,10 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
                 const u32x4 v = *reinterpret_cast<const u32x4*>(src);
 #pragma unroll
                 for (int e = 0; e < 4; ++e) { const uint32_t ve = v[e]; ws[j].w[e] = ve; }
+            } else if constexpr (BITS == 3) {
+                // the 32 codes are the row's 3-word chunk kc / 32
+#pragma unroll
+                for (int e = 0; e < 3; ++e) ws[j].w[e] = src[e];
             } else {
                 const uint2 v = *reinterpret_cast<const uint2*>(src);
                 ws[j].w[0] = v.x;
@@ -360,10 +378,14 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
     // loop-invariant operands of the unpack: masks in scalar registers
     const uint32_t mlo = __builtin_amdgcn_readfirstlane(0x000F000Fu);
     const uint32_t mhi = __builtin_amdgcn_readfirstlane(0x00F000F0u);
+    uint32_t m3[3];
+#pragma unroll
+    for (int p = 0; p < 3; ++p) m3[p] = __builtin_amdgcn_readfirstlane(0x00070007u << (3 * p));
     const uint32_t bias = 0x64006400u;
     const int fr = xswz(r);
     auto compute = [&](int kb, int st, const WStep<BITS> (&ws)[JT]) {
         Zq zq[JT];
+        Zq3 zq3[JT];
         f16x2 s2[JT], zz[JT];
         const bool kval = kb * BK + 32 * g < a.K;
         const int gi = kval ? (kb * BK + 32 * g) / a.G : 0;
@@ -377,6 +399,10 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
             if constexpr (BITS == 4) {
                 const f16 sv = __builtin_bit_cast(f16, static_cast<uint16_t>(sb));
                 zq[j] = make_zq(zb);
+                s2[j] = f16x2{sv, sv};
+            } else if constexpr (BITS == 3) {
+                const f16 sv = __builtin_bit_cast(f16, static_cast<uint16_t>(sb));
+                zq3[j] = make_zq3(zb);
                 s2[j] = f16x2{sv, sv};
             } else {
                 const f16 sv = __builtin_bit_cast(f16, static_cast<uint16_t>(sb));
@@ -441,7 +467,10 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
             for (int t = 0; t < 4; ++t) {
                 u32x4 bf[JT];
 #pragma unroll
-                for (int j = 0; j < JT; ++j) bf[j] = dequant_half2(ws[j].w[t >> 1], t & 1, s2[j], zz[j]);
+                for (int j = 0; j < JT; ++j) {
+                    if constexpr (BITS == 3) bf[j] = dequant_unit3(ws[j].w, t, zq3[j], s2[j], m3, bias);
+                    else bf[j] = dequant_half2(ws[j].w[t >> 1], t & 1, s2[j], zz[j]);
+                }
                 const int slot = (4 * g + t) ^ fr;
 #pragma unroll
                 for (int i = 0; i < MT; ++i) {
@@ -606,6 +635,8 @@ hipError_t launch_linear_prefill(const QW& w, const LR& c, const void* X, int M,
     const size_t lds = (2 * 128 * 16 + 64 * jt * 4) * sizeof(u32x4);
     if (w.bits == 4 && jt == 4) hipLaunchKernelGGL((prefill_kernel<4, 4>), grid, block, lds, st, a);
     else if (w.bits == 4) hipLaunchKernelGGL((prefill_kernel<4, 2>), grid, block, lds, st, a);
+    else if (w.bits == 3 && jt == 4) hipLaunchKernelGGL((prefill_kernel<3, 4>), grid, block, lds, st, a);
+    else if (w.bits == 3) hipLaunchKernelGGL((prefill_kernel<3, 2>), grid, block, lds, st, a);
     else if (jt == 4) hipLaunchKernelGGL((prefill_kernel<2, 4>), grid, block, lds, st, a);
     else hipLaunchKernelGGL((prefill_kernel<2, 2>), grid, block, lds, st, a);
     return hipGetLastError();

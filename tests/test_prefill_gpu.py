@@ -1,6 +1,6 @@
 """cl_linear_prefill against the fp64 oracle (Section 4.1 forward, many
 tokens): relative L2 <= 1e-3 for every output dtype over ragged token and row
-counts, ranks including 0 and non-multiples of 32, 2/4-bit codes and
+counts, ranks including 0 and non-multiples of 32, 2/3/4-bit codes and
 fp16/bf16 activations; the Llama-8B prefill shapes (M = 2048) on sampled
 outputs; agreement with the decode path; bitwise determinism.  The GEMM
 multiplies dequantized weight tiles rounded to fp16 (and T = X A^T rounded
@@ -26,7 +26,7 @@ def _layer(d_out, d_in, bits, G, r_max, seed):
     return w, (Q, s, z, A, B)
 
 
-@pytest.mark.parametrize("bits,G", [(4, 128), (2, 64), (4, 64), (4, 32)])
+@pytest.mark.parametrize("bits,G", [(4, 128), (2, 64), (4, 64), (4, 32), (3, 128), (3, 32)])
 @pytest.mark.parametrize("M,d_out,d_in", [(37, 300, 256), (256, 128, 512), (300, 1000, 1024), (70, 260, 2560)])
 @pytest.mark.parametrize("rank", [0, 17, 64])
 def test_prefill_ragged_vs_oracle(bits, G, M, d_out, d_in, rank):
@@ -78,6 +78,27 @@ def test_prefill_llama_shapes_sampled(d_out, act):
     assert_oracle(got, ref, extra=fp16_tile_bound(W_hat, x.values[toks], A, B[rows], rank))
 
 
+def test_prefill_llama_3bit_sampled():
+    """The paper's INT3 setting: M = 2048 tokens through the 14336 x 4096
+    gate with 3-bit codes (group 128) at rank 64, sampled rows and tokens."""
+    M, d_out, d_in, rank = 2048, 14336, 4096, 64
+    W = wl.weight((d_out, d_in), 4, 3, d_out)
+    w = cl.quantize_pack(torch.from_numpy(W).cuda(), 3, 128)
+    A, B = wl.standin_factors(d_out, d_in, 64, 4, 3, d_out)
+    c = cl.LowRank(dev_f16(A), dev_f16(B), 64, rank)
+    x = wl.activation((M, d_in), 4, 3, d_out)
+    y = cl.linear_prefill(w, c, dev_u16(x.bits, torch.float16), out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    g = np.random.default_rng(3)
+    rows = np.r_[0:2, g.choice(d_out, 100, replace=False), d_out - 2:d_out]
+    toks = np.r_[0:2, g.choice(M, 60, replace=False), M - 2:M]
+    Q, s, z = quant.quantize_pack(W[rows], 3, 128)
+    ref = linear.forward_packed(Q, s, z, 3, 128, A, B[rows], rank, x.values[toks])
+    got = out_to_numpy(y)[np.ix_(toks, rows)]
+    W_hat = quant.dequant_packed(Q, s, z, 3, 128, d_in)
+    assert_oracle(got, ref, extra=fp16_tile_bound(W_hat, x.values[toks], A, B[rows], rank))
+
+
 def test_prefill_matches_decode():
     M, d_out, d_in = 16, 1024, 2048
     w, (Q, s, z, A, B) = _layer(d_out, d_in, 4, 128, 64, 99)
@@ -97,7 +118,7 @@ def test_prefill_deterministic():
                        cl.linear_prefill(w, c, xd, out_dtype=torch.float32))
 
 
-@pytest.mark.parametrize("bits,G", [(4, 128), (4, 64), (4, 32), (2, 64)])
+@pytest.mark.parametrize("bits,G", [(4, 128), (4, 64), (4, 32), (2, 64), (3, 128), (3, 32)])
 def test_prefill_small_weight_scales(bits, G):
     """Weights N(0, (5e-4)^2): group scales near 2^-12, below 2^-10 where
     s / 16 leaves the fp16 normal range.  The dequantized tile forms q - z
