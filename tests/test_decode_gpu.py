@@ -238,6 +238,21 @@ def _layer_dev(d_out, d_in, bits, G, r_max, rank, seed):
     return w, c, (Q, s, z, A, B)
 
 
+@pytest.mark.parametrize("bits,G,d_in", [(4, 32, 192), (4, 64, 320), (2, 64, 192), (2, 64, 320), (4, 32, 384),
+                                          (3, 32, 384), (3, 64, 384)])
+@pytest.mark.parametrize("T", [3, 16])
+def test_mfma_rows_ending_in_a_partial_block(bits, G, d_in, T):
+    """Rows whose width is not a multiple of the 128-code block (2- and
+    4-bit: an odd multiple of 64 codes) on the MFMA backbone: the last
+    block's missing groups have clamped loads and a zero scale; 3-bit rows
+    (multiples of 128 codes) with two and four groups per block; every
+    output dtype."""
+    w, c, (Q, s, z, A, B) = _layer_dev(300, d_in, bits, G, 64, 37, d_in + bits + T)
+    x = wl.activation((T, d_in), 12, d_in, T)
+    for od in OUT_DTYPES:
+        _check(w, c, Q, s, z, A, B, 37, x, torch.float16, od, bits, G)
+
+
 def test_one_workspace_reused_across_shapes_ranks_and_token_counts():
     """One workspace serves consecutive calls of different shapes, ranks and
     token counts."""
