@@ -117,6 +117,20 @@ class Timer:
         torch.cuda.synchronize()
         return g
 
+    def spread(self, graphs, n):
+        """p10 / p50 / p90 of single replays, in ms: an event after every
+        replay (a separate pass, after the timed region)."""
+        torch = self.torch
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
+        with torch.cuda.stream(self.stream):
+            evs[0].record(self.stream)
+            for i in range(n):
+                graphs[i % len(graphs)].replay()
+                evs[i + 1].record(self.stream)
+        torch.cuda.synchronize()
+        d = sorted(evs[i].elapsed_time(evs[i + 1]) for i in range(n))
+        return d[n // 10], d[n // 2], d[(9 * n) // 10]
+
     def time(self, graphs, n, warm=None):
         """Average ms per replay of n replays cycling through graphs."""
         torch = self.torch
@@ -156,9 +170,10 @@ def device_layer(torch, cl, wl, layer, dev, rotate_gib):
 WINDOWS = (("q", "k", "v"), ("o",), ("gate", "up"), ("down",))
 
 
-def layer_step(torch, cl, wl, timer, copies, layer, T, dev, steps, warmup):
+def layer_step(torch, cl, wl, timer, copies, layer, T, dev, steps, warmup, spread=None):
     """ms per step of the layer's four windows (graph per copy), and the
-    inputs/outputs used."""
+    inputs/outputs used; with a dict as spread, also the p10 / p50 / p90 of
+    single steps from a separate pass of as many steps."""
     specs = layer.linears
     names = [s.name for s in specs]
     windows = [[names.index(n) for n in grp] for grp in WINDOWS]
@@ -181,6 +196,8 @@ def layer_step(torch, cl, wl, timer, copies, layer, T, dev, steps, warmup):
 
     graphs = [timer.capture(calls(k)) for k in range(len(copies))]
     ms = timer.time(graphs, steps, warm=warmup)
+    if spread is not None:
+        spread["p10"], spread["p50"], spread["p90"] = (round(v, 5) for v in timer.spread(graphs, steps))
     return ms, xs, ys
 
 
@@ -486,7 +503,9 @@ def main():
         print(json.dumps({"gate_up_window_vs_glu": bench_glu(torch, cl, wl, timer, copies, layer, dev)}))
         return
 
-    ms_step, xs, ys = layer_step(torch, cl, wl, timer, copies, layer, T, dev, args.steps, args.warmup)
+    step_spread = {}
+    ms_step, xs, ys = layer_step(torch, cl, wl, timer, copies, layer, T, dev, args.steps, args.warmup,
+                                 spread=step_spread)
     step_bytes = sum(algorithmic_bytes(s, T) for s in specs)
     value = step_bytes / (ms_step * 1e-3) / 1e9
 
@@ -524,6 +543,9 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms_step, 5),
+        "step_ms_spread": dict(step_spread, note="single steps of a separate pass after the timed region, an "
+                                                 "event after each (each event lengthens its step: compare "
+                                                 "the spread's width, not its level, with ms_per_step)"),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
