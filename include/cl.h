@@ -170,7 +170,11 @@ size_t cl_linear_workspace(const cl_qweight* w, const cl_lowrank* c, int32_t tok
  * activations in the layout the backbone consumes (in the workspace), then
  * one memory-bound kernel that unpacks, dequantizes and multiplies the
  * backbone and folds in the rank-r up-projection B t.  Accumulation is
- * float32; the result is rounded once to out_dtype.
+ * float32; the result is rounded once to out_dtype.  t = A x is float32 for
+ * one and two tokens; from three tokens (the MFMA backbone) it enters the
+ * contraction as an fp16 pair hi + lo (about 2^-22 relative), so |A x| must
+ * stay below 65504, and below 2^-14 it keeps fp16's subnormal resolution
+ * (2^-25 absolute).
  *
  *  w, c       the packed backbone and its factors (c may be NULL for rank 0)
  *  x          device [T][d_in] of act_dtype (CL_FP16 or CL_BF16), 16-byte
@@ -272,7 +276,8 @@ cl_status cl_linear_decode_glu(const cl_qweight* w, const cl_lowrank* c, const v
  * accumulation, folds the rank-r term in as extra K steps over [T | B] into
  * the same output tile and rounds once to out_dtype.  bf16 activations are
  * converted to fp16 (exact for 2^-17 <= |x| <= 65504, as in
- * cl_linear_decode).
+ * cl_linear_decode).  T is rounded once to fp16, so |X A^T| must stay below
+ * 65504 (below 2^-14 its resolution is fp16's, 2^-25 absolute).
  *
  *  X          device [M][d_in] of act_dtype, 16-byte aligned
  *  M          >= 1 tokens, M * d_in < 2^31

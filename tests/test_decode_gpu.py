@@ -107,6 +107,42 @@ def test_bf16_activations(bits, G):
         _check(w, c, Q, s, z, A, B, 32, x, torch.bfloat16, od, bits, G)
 
 
+def _bf16_out_of_fp16_range(T, d_in, seed):
+    """bf16 activations outside fp16's normal range: even tokens at scale
+    1e5 (most beyond 65504), odd tokens at scale 1e-6 (all below 2^-17 but a
+    few, fp16 subnormals), and the fp16 values the kernels are documented to
+    see: clamped to +-65504, then rounded to nearest even."""
+    g = np.random.default_rng(seed)
+    scale = np.where(np.arange(T) % 2 == 0, 1e5, 1e-6)[:, None]
+    bits = wl.fp32_to_bf16_bits((scale * g.standard_normal((T, d_in))).astype(np.float32))
+    seen = np.clip(wl.bf16_bits_to_f64(bits), -65504.0, 65504.0).astype(np.float16).astype(np.float64)
+    return bits, seen
+
+
+@pytest.mark.parametrize("bits,G", [(4, 128), (3, 128), (2, 64)])
+@pytest.mark.parametrize("T", [2, 4])
+def test_bf16_activations_beyond_the_fp16_range(bits, G, T):
+    """The documented bf16 conversion on the dot2 (2 tokens) and MFMA (4
+    tokens) backbones: saturated at +-65504, rounded to multiples of 2^-24
+    below 2^-17.  Two tokens carry the rank term too (t = A x in float32, so
+    it sees the same converted values); on the MFMA backbone t is an fp16
+    pair whose range these scales leave (|A x| ~ 1e5 and ~ 1e-6), so that
+    case runs the backbone alone.  Each token is checked on its own (the
+    subnormal tokens' outputs are ~1e-6)."""
+    d_out, d_in = 500, 1024
+    rank = 24 if T < 3 else 0
+    W = wl.weight((d_out, d_in), 14, bits, T)
+    Q, s, z = quant.quantize_pack(W, bits, G)
+    A, B = wl.standin_factors(d_out, d_in, 32, 14, bits, T)
+    w, c = _device_layer(Q, s, z, A, B, d_out, d_in, bits, G, 32, rank)
+    xb, seen = _bf16_out_of_fp16_range(T, d_in, 40 + T + bits)
+    assert np.abs(seen[0]).max() == 65504.0 and np.abs(seen[1]).max() < 2.0 ** -14
+    y = out_to_numpy(cl.linear_decode(w, c, dev_u16(xb, torch.bfloat16), out_dtype=torch.float32))
+    ref = linear.forward_packed(Q, s, z, bits, G, A, B, rank, seen)
+    for tk in range(T):
+        assert_oracle(y[tk], ref[tk])
+
+
 @pytest.mark.parametrize("mat", wl.LLAMA_MATS)
 @pytest.mark.parametrize("T", [1, 4, 16])
 def test_llama_layer_full_size_sampled_rows(mat, T):

@@ -99,6 +99,25 @@ def test_prefill_llama_3bit_sampled():
     assert_oracle(got, ref, extra=fp16_tile_bound(W_hat, x.values[toks], A, B[rows], rank))
 
 
+def test_prefill_bf16_activations_beyond_the_fp16_range():
+    """The documented bf16 conversion in prefill's X': tokens at scale 1e5
+    saturate at +-65504, tokens at scale 1e-6 round to multiples of 2^-24;
+    each token against the oracle on the converted values.  The backbone
+    alone: T = X A^T is fp16, whose range these scales leave."""
+    M, d_out, d_in, rank = 40, 300, 1024, 0
+    w, (Q, s, z, A, B) = _layer(d_out, d_in, 4, 128, 32, 41)
+    c = None
+    g = np.random.default_rng(41)
+    scale = np.where(np.arange(M) % 2 == 0, 1e5, 1e-6)[:, None]
+    xb = wl.fp32_to_bf16_bits((scale * g.standard_normal((M, d_in))).astype(np.float32))
+    seen = np.clip(wl.bf16_bits_to_f64(xb), -65504.0, 65504.0).astype(np.float16).astype(np.float64)
+    y = out_to_numpy(cl.linear_prefill(w, c, dev_u16(xb, torch.bfloat16), out_dtype=torch.float32))
+    ref = linear.forward_packed(Q, s, z, 4, 128, A, B, rank, seen)
+    W_hat = quant.dequant_packed(Q, s, z, 4, 128, d_in)
+    for m in range(M):
+        assert_oracle(y[m], ref[m], extra=fp16_tile_bound(W_hat, seen[m:m + 1])[0])
+
+
 def test_prefill_matches_decode():
     M, d_out, d_in = 16, 1024, 2048
     w, (Q, s, z, A, B) = _layer(d_out, d_in, 4, 128, 64, 99)
