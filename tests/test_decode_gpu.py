@@ -254,13 +254,16 @@ def test_2bit_gate_rank_sweep_sampled_rows():
         assert_oracle(out_to_numpy(y)[:, rows], ref)
 
 
-def test_deterministic_bitwise():
+@pytest.mark.parametrize("bits,G,T", [(4, 128, 4), (4, 128, 1), (2, 64, 16), (3, 128, 16), (3, 32, 2)])
+def test_deterministic_bitwise(bits, G, T):
+    """Two calls on the same inputs give the same bits (every backbone: the
+    K slices and waves' partial sums meet in a fixed order)."""
     d_out, d_in = 4096, 4096
     W = wl.weight((d_out, d_in), 11)
-    w = cl.quantize_pack(torch.from_numpy(W).cuda(), 4, 128)
+    w = cl.quantize_pack(torch.from_numpy(W).cuda(), bits, G)
     A, B = wl.standin_factors(d_out, d_in, 64, 11)
     c = cl.LowRank(dev_f16(A), dev_f16(B), 64, 64)
-    x = dev_u16(wl.activation((4, d_in), 11).bits, torch.float16)
+    x = dev_u16(wl.activation((T, d_in), 11).bits, torch.float16)
     y1 = cl.linear_decode(w, c, x, out_dtype=torch.float32)
     y2 = cl.linear_decode(w, c, x, out_dtype=torch.float32)
     assert torch.equal(y1, y2)
