@@ -95,6 +95,25 @@ __device__ __forceinline__ u32x4 dequant_unit3(const uint32_t (&w)[3], int t, co
     return r;
 }
 
+// One half of dequant_unit3: h = 0 gives pairs 0 and 1 (r[0], r[1]), h = 1
+// pairs 2 and 3; the same values.
+__device__ __forceinline__ void dequant_half3(const uint32_t (&w)[3], int t, int h, const Zq3& zq, f16x2 s2,
+                                              const uint32_t (&m)[3], uint32_t bias, uint32_t& lo, uint32_t& hi) {
+    const uint32_t v = spread_unit3(w[0], w[1], w[2], t);
+    const f16x2 e8 = {static_cast<f16>(0.125f), static_cast<f16>(0.125f)};
+    const f16x2 e64 = {static_cast<f16>(0.015625f), static_cast<f16>(0.015625f)};
+    f16x2 a, b;
+    if (h == 0) {
+        a = __builtin_bit_cast(f16x2, and_or(v, m[0], bias)) + zq.c[0];
+        b = __builtin_elementwise_fma(__builtin_bit_cast(f16x2, and_or(v, m[1], bias)), e8, zq.c[1]);
+    } else {
+        a = __builtin_elementwise_fma(__builtin_bit_cast(f16x2, and_or(v, m[2], bias)), e64, zq.c[2]);
+        b = __builtin_elementwise_fma(__builtin_bit_cast(f16x2, and_or(v >> 3, m[2], bias)), e64, zq.c[2]);
+    }
+    lo = __builtin_bit_cast(uint32_t, a * s2);
+    hi = __builtin_bit_cast(uint32_t, b * s2);
+}
+
 struct PrefillArgs {
     const uint32_t* q;
     const uint16_t* s;
@@ -411,7 +430,7 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
                 zz[j] = f16x2{zf, zf};
             }
         }
-        if constexpr (BITS == 4) {
+        if constexpr (BITS == 4 || BITS == 3) {
             // Software pipeline over the 4 MT regions of the step (region =
             // MFMA step t, token tile i: one X' operand, JT MFMAs): the X'
             // operand of the region PD ahead is read from LDS (PD regions
@@ -428,8 +447,18 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
             u32x4 bc[JT], bn[JT], ap[PD];
 #pragma unroll
             for (int q = 0; q < PD; ++q) ap[q] = xop(q);
+            // the 8-code unit of step t of row tile j (4-bit: word t; 3-bit:
+            // unit t of the 3-word chunk), whole or one half of its pairs
+            auto deq_full = [&](int j, int t) {
+                if constexpr (BITS == 4) return dequant_word4x(ws[j].w[t], zq[j], s2[j], mlo, mhi, bias);
+                else return dequant_unit3(ws[j].w, t, zq3[j], s2[j], m3, bias);
+            };
+            auto deq_half = [&](int j, int t, int h, uint32_t& lo, uint32_t& hi) {
+                if constexpr (BITS == 4) dequant_half4x(ws[j].w[t], h, zq[j], s2[j], mlo, mhi, bias, lo, hi);
+                else dequant_half3(ws[j].w, t, h, zq3[j], s2[j], m3, bias, lo, hi);
+            };
 #pragma unroll
-            for (int j = 0; j < JT; ++j) bc[j] = dequant_word4x(ws[j].w[0], zq[j], s2[j], mlo, mhi, bias);
+            for (int j = 0; j < JT; ++j) bc[j] = deq_full(j, 0);
 #pragma unroll
             for (int t = 0; t < 4; ++t) {
 #pragma unroll
@@ -443,7 +472,7 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
                     if (t < 3 && (i * NH) % MT == 0) {
                         const int hx = i * NH / MT, j = hx / 2, h = hx % 2;
                         uint32_t lo, hi;
-                        dequant_half4x(ws[j].w[t + 1], h, zq[j], s2[j], mlo, mhi, bias, lo, hi);
+                        deq_half(j, t + 1, h, lo, hi);
                         bn[j][2 * h] = lo;
                         bn[j][2 * h + 1] = hi;
                     }
@@ -467,10 +496,7 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
             for (int t = 0; t < 4; ++t) {
                 u32x4 bf[JT];
 #pragma unroll
-                for (int j = 0; j < JT; ++j) {
-                    if constexpr (BITS == 3) bf[j] = dequant_unit3(ws[j].w, t, zq3[j], s2[j], m3, bias);
-                    else bf[j] = dequant_half2(ws[j].w[t >> 1], t & 1, s2[j], zz[j]);
-                }
+                for (int j = 0; j < JT; ++j) bf[j] = dequant_half2(ws[j].w[t >> 1], t & 1, s2[j], zz[j]);
                 const int slot = (4 * g + t) ^ fr;
 #pragma unroll
                 for (int i = 0; i < MT; ++i) {
