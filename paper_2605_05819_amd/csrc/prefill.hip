@@ -95,6 +95,17 @@ __device__ __forceinline__ u32x4 dequant_unit3(const uint32_t (&w)[3], int t, co
     return r;
 }
 
+// One half of dequant_half2's result: pairs 2 h and 2 h + 1 of the 8-code
+// half u of the word; the same values.
+__device__ __forceinline__ void dequant_quarter2(uint32_t w, int u, int h, f16x2 s2, f16x2 zz, uint32_t& lo,
+                                                 uint32_t& hi) {
+    const uint32_t v = u == 0 ? ((w & 0xFFFFu) | ((w & 0xFF00u) << 8)) : ((w >> 16) | ((w >> 24) << 16));
+    const f16x2 a = __builtin_bit_cast(f16x2, ((v >> (4 * h)) & 0x00030003u) | 0x64006400u);
+    const f16x2 b = __builtin_bit_cast(f16x2, ((v >> (4 * h + 2)) & 0x00030003u) | 0x64006400u);
+    lo = __builtin_bit_cast(uint32_t, (a - zz) * s2);
+    hi = __builtin_bit_cast(uint32_t, (b - zz) * s2);
+}
+
 // One half of dequant_unit3: h = 0 gives pairs 0 and 1 (r[0], r[1]), h = 1
 // pairs 2 and 3; the same values.
 __device__ __forceinline__ void dequant_half3(const uint32_t (&w)[3], int t, int h, const Zq3& zq, f16x2 s2,
@@ -430,7 +441,7 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
                 zz[j] = f16x2{zf, zf};
             }
         }
-        if constexpr (BITS == 4 || BITS == 3) {
+        {
             // Software pipeline over the 4 MT regions of the step (region =
             // MFMA step t, token tile i: one X' operand, JT MFMAs): the X'
             // operand of the region PD ahead is read from LDS (PD regions
@@ -448,14 +459,17 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
 #pragma unroll
             for (int q = 0; q < PD; ++q) ap[q] = xop(q);
             // the 8-code unit of step t of row tile j (4-bit: word t; 3-bit:
-            // unit t of the 3-word chunk), whole or one half of its pairs
+            // unit t of the 3-word chunk; 2-bit: half t % 2 of word t / 2),
+            // whole or one half of its pairs
             auto deq_full = [&](int j, int t) {
                 if constexpr (BITS == 4) return dequant_word4x(ws[j].w[t], zq[j], s2[j], mlo, mhi, bias);
-                else return dequant_unit3(ws[j].w, t, zq3[j], s2[j], m3, bias);
+                else if constexpr (BITS == 3) return dequant_unit3(ws[j].w, t, zq3[j], s2[j], m3, bias);
+                else return dequant_half2(ws[j].w[t >> 1], t & 1, s2[j], zz[j]);
             };
             auto deq_half = [&](int j, int t, int h, uint32_t& lo, uint32_t& hi) {
                 if constexpr (BITS == 4) dequant_half4x(ws[j].w[t], h, zq[j], s2[j], mlo, mhi, bias, lo, hi);
-                else dequant_half3(ws[j].w, t, h, zq3[j], s2[j], m3, bias, lo, hi);
+                else if constexpr (BITS == 3) dequant_half3(ws[j].w, t, h, zq3[j], s2[j], m3, bias, lo, hi);
+                else dequant_quarter2(ws[j].w[t >> 1], t & 1, h, s2[j], zz[j], lo, hi);
             };
 #pragma unroll
             for (int j = 0; j < JT; ++j) bc[j] = deq_full(j, 0);
@@ -490,20 +504,6 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
                 if (t < 3)
 #pragma unroll
                     for (int j = 0; j < JT; ++j) bc[j] = bn[j];
-            }
-        } else {
-#pragma unroll
-            for (int t = 0; t < 4; ++t) {
-                u32x4 bf[JT];
-#pragma unroll
-                for (int j = 0; j < JT; ++j) bf[j] = dequant_half2(ws[j].w[t >> 1], t & 1, s2[j], zz[j]);
-                const int slot = (4 * g + t) ^ fr;
-#pragma unroll
-                for (int i = 0; i < MT; ++i) {
-                    const u32x4 af = xs[st][(16 * i + r) * 16 + slot];
-#pragma unroll
-                    for (int j = 0; j < JT; ++j) acc[i][j] = mfma(af, bf[j], acc[i][j]);
-                }
             }
         }
     };
