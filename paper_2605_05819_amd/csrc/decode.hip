@@ -636,34 +636,33 @@ __global__ __launch_bounds__(1024) void decode_prep_mfma_kernel(PrepMArgs a) {
     (void)PPC;
 }
 
-// Many-token backbone (4-, 3- or 2-bit codes, T >= 3): the contraction has enough
-// columns to use MFMA (tokens padded to 16).  One workgroup per TPW 16-row
-// tiles of one linear; its four waves split the 128-code blocks of K (wave w
-// takes blocks w, w + 4, ...), NBUF blocks per wave in flight.  Per block a
-// lane loads, for each of its TPW tiles, its 32 codes of row r = lane % 16
-// (16 bytes at 4 bits, 12 at 3, 8 at 2), and once for all tiles the matching
-// activations of token r (four
-// 16-byte loads from the word-major layout, 256 or 1024 contiguous bytes per
-// load instruction).  The MFMA takes the activations as its A operand and the
-// codes as its B operand, so lane (g, r) accumulates tokens 4 g .. 4 g + 3 of
-// weight row r.  The codes become the exact fp16 integers q - z (2- and
-// 3-bit codes: each 8-code unit spread by a byte permute, then one mask and
-// one packed add or FMA per pair, codes2_minus_zero, codes3_minus_zero), and
-// every
-// quantization group's MFMA steps run into a fresh fp32 partial that is
-// scaled by the group's fp16 scale in fp32 and added to the accumulator:
-// the backbone is s (sum (q - z) x) with fp32 rounding only, whatever the
-// scale (a weight tile rounded to fp16 would carry 2^-11 relative error, and
-// lose precision once s / 16 falls below the fp16 normal range).  GPB
-// (groups per 128-code block) = 128 / G: with one group per block each MFMA
-// step takes word t of every lane group (the four steps cover the block);
-// with 2 or 4 groups the code words are transposed across the lane groups
-// first, so step t covers the 32 codes 32 t .. 32 t + 31, which lie in one
-// group.  The rank-r term is extra MFMA steps over [t | B] spread over the
-// waves (t from the K-part partials of decode_prep_mfma_kernel, summed in a
-// fixed order and split into fp16 hi and lo parts, one step each); the
-// waves' tiles are summed through LDS in a fixed order; one rounding to the
-// output dtype.
+// Many-token backbone (4-, 3- or 2-bit codes, T >= 3): the contraction has
+// enough columns to use MFMA (tokens padded to 16).  One workgroup per TPW
+// 16-row tiles of one linear; its four waves split the 128-code blocks of K
+// (wave w takes blocks w, w + 4, ...), NBUF blocks per wave in flight.  Per
+// block a lane loads, for each of its TPW tiles, its 32 codes of row
+// r = lane % 16 (16 bytes at 4 bits, 12 at 3, 8 at 2), and once for all
+// tiles the matching activations of token r (four 16-byte loads from the
+// word-major layout, 256 or 1024 contiguous bytes per load instruction).
+// The MFMA takes the activations as its A operand and the codes as its B
+// operand, so lane (g, r) accumulates tokens 4 g .. 4 g + 3 of weight row r.
+// The codes of each 8-code unit become the exact fp16 integers q - z (4-bit:
+// the unit is a word, codes_minus_zero; 2- and 3-bit: the unit is first
+// spread by a byte permute, then one mask and one packed add or FMA per
+// pair, codes2_minus_zero, codes3_minus_zero), and every quantization
+// group's MFMA steps run into a fresh fp32 partial that is scaled by the
+// group's fp16 scale in fp32 and added to the accumulator: the backbone is
+// s (sum (q - z) x) with fp32 rounding only, whatever the scale (a weight
+// tile rounded to fp16 would carry 2^-11 relative error, and lose precision
+// once s / 16 falls below the fp16 normal range).  GPB (groups per 128-code
+// block) = 128 / G: with one group per block each MFMA step takes unit t of
+// every lane group (the four steps cover the block); with 2 or 4 groups the
+// units are transposed across the lane groups first, so step t covers the
+// 32 codes 32 t .. 32 t + 31, which lie in one group.  The rank-r term is
+// extra MFMA steps over [t | B] spread over the waves (t from the K-part
+// partials of decode_prep_mfma_kernel, summed in a fixed order and split
+// into fp16 hi and lo parts, one step each); the waves' tiles are summed
+// through LDS in a fixed order; one rounding to the output dtype.
 template <int BITS, int TPW, int NBUF, bool GLU, int GPB, int NW, bool LONGK>
 __global__ __launch_bounds__((GLU ? 2 : 1) * 64 * NW) void decode_mfma_kernel(DecodeArgs a) {
     static_assert(BITS == 4 || BITS == 3 || BITS == 2, "4-, 3- or 2-bit codes");
