@@ -50,7 +50,7 @@ MFMA_F16_PEAK_TFLOPS = 2500.0
 GATE_TRAFFIC = {"fetch_bytes": (32411 + 710) * 1024, "write_bytes": (56 + 9) * 1024,
                 "sources": ("paper_2605_05819_amd/csrc/decode.hip", "paper_2605_05819_amd/csrc/gemv_common.h",
                             "paper_2605_05819_amd/csrc/cl_device.h"),
-                "sha256": "2850f17221a0aec4e59c2363eb6fc59ce62650c96bbed53033d987763b08358b"}
+                "sha256": "f000f300dba273dffb835d4d5b2a1926bebf4fa85087fe420be13cbf2c1b752a"}
 
 
 def sources_sha256(paths):
