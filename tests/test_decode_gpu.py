@@ -32,6 +32,46 @@ def _check(w, c, Q, s, z, A, B, rank, x, act_dtype, out_dtype, bits, G):
     return y, ref
 
 
+def _random_decode_cases(n, seed):
+    """Seeded random shapes over the decode paths: rows 1..5000, widths up to
+    8192 codes (at most 2^23 weights a case), 2/3/4-bit codes with every
+    allowed group size up to 256, 1..40 tokens (dot2 and MFMA backbones),
+    ranks 0..r_max, every dtype."""
+    g = np.random.default_rng(seed)
+    cases = []
+    while len(cases) < n:
+        bits = int(g.choice([2, 3, 4]))
+        G = int(g.choice([32, 64, 128, 256]))
+        if G % (32 if bits == 3 else 128 // bits):
+            continue
+        step = max(G, 128 if bits == 3 else G)
+        d_in = int(step * g.integers(1, 8192 // step + 1))
+        d_out = int(g.integers(1, 5001))
+        if d_out * d_in > (8 << 20):              # keep the fp64 oracle to seconds
+            continue
+        T = int(g.choice([1, 2, 3, 4, 5, 9, 16, 17, 40]))
+        r_max = int(g.choice([8, 32, 64, 256]))
+        rank = int(g.integers(0, r_max + 1))
+        act = str(g.choice(["fp16", "bf16"]))
+        out = [torch.float32, torch.float16, torch.bfloat16][int(g.integers(0, 3))]
+        cases.append((bits, G, d_out, d_in, T, r_max, rank, act, out))
+    return cases
+
+
+@pytest.mark.parametrize("case", _random_decode_cases(100, 2024), ids=lambda c: "b%d_g%d_%dx%d_T%d_r%d_%d_%s" % c[:8])
+def test_random_shapes_against_the_oracle(case):
+    """A seeded sweep of random shapes, token counts, ranks and dtypes; each
+    output against the oracle rounded to its dtype."""
+    bits, G, d_out, d_in, T, r_max, rank, act, out = case
+    seed = (d_out * 7 + d_in * 3 + T * 11 + rank) % 100000
+    W = wl.weight((d_out, d_in), 16, seed)
+    Q, s, z = quant.quantize_pack(W, bits, G)
+    A, B = wl.standin_factors(d_out, d_in, r_max, 16, seed)
+    w, c = _device_layer(Q, s, z, A, B, d_out, d_in, bits, G, r_max, rank)
+    x = wl.activation((T, d_in), 16, seed, dtype=act)
+    _check(w, c, Q, s, z, A, B, rank, x, torch.float16 if act == "fp16" else torch.bfloat16, out, bits, G)
+
+
 def test_single_linear_1024_rank16_all_out_dtypes():
     spec = wl.single_linear().linears[0]
     W = wl.weight((spec.d_out, spec.d_in), 0)

@@ -118,6 +118,44 @@ def test_prefill_bf16_activations_beyond_the_fp16_range():
         assert_oracle(y[m], ref[m], extra=fp16_tile_bound(W_hat, seen[m:m + 1])[0])
 
 
+def _random_prefill_cases(n, seed):
+    """Seeded random prefill shapes: 1..600 tokens, rows 1..3000, widths of
+    64..4096 codes (odd multiples of 64 included where the group allows),
+    2/3/4-bit codes, ranks 0..r_max, fp16/bf16 in, every dtype out."""
+    g = np.random.default_rng(seed)
+    cases = []
+    while len(cases) < n:
+        bits = int(g.choice([2, 3, 4]))
+        G = int(g.choice([32, 64, 128, 256]))
+        if G % (32 if bits == 3 else 128 // bits):
+            continue
+        step = max(G, 128 if bits == 3 else 64)
+        d_in = int(step * g.integers(1, 4096 // step + 1))
+        if d_in % G:
+            continue
+        M, d_out = int(g.integers(1, 601)), int(g.integers(1, 3001))
+        r_max = int(g.choice([16, 64, 256]))
+        rank = int(g.integers(0, r_max + 1))
+        act = str(g.choice(["fp16", "bf16"]))
+        out = [torch.float32, torch.float16, torch.bfloat16][int(g.integers(0, 3))]
+        cases.append((bits, G, M, d_out, d_in, r_max, rank, act, out))
+    return cases
+
+
+@pytest.mark.parametrize("case", _random_prefill_cases(40, 2025), ids=lambda c: "b%d_g%d_M%d_%dx%d_r%d_%d_%s" % c[:8])
+def test_prefill_random_shapes_against_the_oracle(case):
+    """A seeded sweep of random prefill shapes against the oracle rounded to
+    the output dtype, with the fp16 weight-tile rounding bound."""
+    bits, G, M, d_out, d_in, r_max, rank, act, out = case
+    w, (Q, s, z, A, B) = _layer(d_out, d_in, bits, G, r_max, (M * 13 + d_out * 7 + d_in + rank) % 100000)
+    c = cl.LowRank(dev_f16(A), dev_f16(B), r_max, rank)
+    x = wl.activation((M, d_in), 25, M, d_out, dtype=act)
+    y = cl.linear_prefill(w, c, dev_u16(x.bits, torch.float16 if act == "fp16" else torch.bfloat16), out_dtype=out)
+    ref = linear.forward_packed(Q, s, z, bits, G, A, B, rank, x.values)
+    W_hat = quant.dequant_packed(Q, s, z, bits, G, d_in)
+    assert_oracle(out_to_numpy(y), ref, out, extra=fp16_tile_bound(W_hat, x.values, A, B, rank))
+
+
 def test_prefill_matches_decode():
     M, d_out, d_in = 16, 1024, 2048
     w, (Q, s, z, A, B) = _layer(d_out, d_in, 4, 128, 64, 99)
