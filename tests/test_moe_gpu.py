@@ -97,6 +97,54 @@ def test_bits_groups_and_bf16_activations(bits, G, act):
     assert_oracle(got, ref)
 
 
+def _random_moe_cases(n, seed):
+    """Seeded random MoE calls: 1..160 experts, top-1..8 (ids drawn
+    independently, so a token may repeat an expert), 1..64 tokens (the
+    one-launch, VALU and MFMA paths by slots per expert), 2/4-bit codes with
+    every group size to 256, widths to 4096, factor widths 0..64, ranks
+    0..r_max per expert, shared or per-slot inputs, every dtype; at most
+    2^24 expert weights a case."""
+    g = np.random.default_rng(seed)
+    cases = []
+    while len(cases) < n:
+        bits = int(g.choice([2, 4]))
+        G = int(g.choice([32, 64, 128, 256]))
+        if G % (128 // bits):
+            continue
+        d_in = int(G * g.integers(1, 4096 // G + 1))
+        E = int(g.integers(1, 161))
+        d_out = int(g.integers(1, 801))
+        if E * d_out * d_in > (1 << 24):
+            continue
+        k = int(g.integers(1, min(8, E) + 1))
+        T = int(g.choice([1, 2, 5, 8, 16, 33, 64]))
+        r_max = int(g.choice([0, 8, 32, 64]))
+        cases.append((bits, G, E, k, T, d_out, d_in, r_max, bool(g.integers(0, 2)),
+                      str(g.choice(["fp16", "bf16"])), int(g.integers(0, 3)), int(g.integers(0, 1 << 30))))
+    return cases
+
+
+@pytest.mark.parametrize("case", _random_moe_cases(80, 2026),
+                         ids=lambda c: "b%d_g%d_E%d_k%d_T%d_%dx%d_r%d_%s" % c[:9])
+def test_random_moe_calls_against_the_oracle(case):
+    """A seeded sweep of random MoE calls, each against the oracle rounded to
+    its output dtype."""
+    bits, G, E, k, T, d_out, d_in, r_max, per_slot, act, od, seed = case
+    Q, s, z, A, B = _oracle_experts(E, d_out, d_in, bits, G, max(r_max, 1), seed % 1000, svd=False)
+    g = np.random.default_rng(seed)
+    ranks = g.integers(0, r_max + 1, E).astype(np.int32)
+    ids = g.integers(0, E, (T, k)).astype(np.int32)
+    shape = (T, k, d_in) if per_slot else (T, d_in)
+    x = wl.activation(shape, seed % 1000, 1, 1, dtype=act)
+    if r_max == 0:
+        A, B = A[:, :0], B[:, :, :0]
+    ex = _device_experts(Q, s, z, A, B, ranks, d_out, d_in, bits, G, r_max)
+    ref = _full_ref(Q, s, z, A, B, ranks, x.values, ids, per_slot, bits, G, d_in)
+    out = OUT_DTYPES[od]
+    got = _run(ex, x.bits, torch.float16 if act == "fp16" else torch.bfloat16, ids, out, per_slot)
+    assert_oracle(got, ref, out)
+
+
 def test_duplicate_invalid_ids_and_clamped_ranks():
     E, d_out, d_in, bits, G, r_max, T, k = 6, 64, 256, 4, 128, 8, 4, 5
     Q, s, z, A, B = _oracle_experts(E, d_out, d_in, bits, G, r_max, 42, svd=False)
