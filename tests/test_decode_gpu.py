@@ -72,6 +72,46 @@ def test_random_shapes_against_the_oracle(case):
     _check(w, c, Q, s, z, A, B, rank, x, torch.float16 if act == "fp16" else torch.bfloat16, out, bits, G)
 
 
+def _random_window_cases(n, seed):
+    g = np.random.default_rng(seed)
+    cases = []
+    while len(cases) < n:
+        bits = int(g.choice([2, 3, 4]))
+        G = int(g.choice([32, 64, 128]))
+        if G % (32 if bits == 3 else 128 // bits):
+            continue
+        step = max(G, 128 if bits == 3 else G)
+        d_in = int(step * g.integers(1, 4096 // step + 1))
+        nl = int(g.integers(2, 9))
+        d_outs = [int(v) for v in g.integers(1, 2049, nl)]
+        if sum(d_outs) * d_in > (8 << 20):
+            continue
+        T = int(g.choice([1, 2, 3, 5, 16, 20]))
+        r_max = int(g.choice([8, 64, 256]))
+        ranks = [int(v) for v in g.integers(0, r_max + 1, nl)]
+        cases.append((bits, G, d_in, T, r_max, tuple(d_outs), tuple(ranks), str(g.choice(["fp16", "bf16"]))))
+    return cases
+
+
+@pytest.mark.parametrize("case", _random_window_cases(30, 2027),
+                         ids=lambda c: "b%d_g%d_K%d_T%d_r%d_n%d" % (c[0], c[1], c[2], c[3], c[4], len(c[5])))
+def test_random_windows_against_singles_and_the_oracle(case):
+    """A seeded sweep of windows (2..8 linears over one input, random row
+    counts and ranks): each output equals the single call bit for bit and
+    the oracle within tolerance."""
+    bits, G, d_in, T, r_max, d_outs, ranks, act = case
+    ws_, cs, host = [], [], []
+    for i, (d_out, rank) in enumerate(zip(d_outs, ranks)):
+        w, c, h = _layer_dev(d_out, d_in, bits, G, r_max, rank, 200 + i + d_in % 97)
+        ws_.append(w), cs.append(c), host.append(h)
+    x = wl.activation((T, d_in), 17, d_in, T, dtype=act)
+    xd = dev_u16(x.bits, torch.float16 if act == "fp16" else torch.bfloat16)
+    ys = cl.linear_decode_window(ws_, cs, xd, out_dtype=torch.float32)
+    for i, (w, c, (Q, s, z, A, B), rank) in enumerate(zip(ws_, cs, host, ranks)):
+        assert torch.equal(ys[i], cl.linear_decode(w, c, xd, out_dtype=torch.float32)), i
+        assert_oracle(out_to_numpy(ys[i]), linear.forward_packed(Q, s, z, bits, G, A, B, rank, x.values))
+
+
 def test_single_linear_1024_rank16_all_out_dtypes():
     spec = wl.single_linear().linears[0]
     W = wl.weight((spec.d_out, spec.d_in), 0)
