@@ -290,10 +290,12 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
     // LDS (dynamic, prefill_lds_bytes): two stages of X', [BM rows][16
     // chunks of 8 k], chunk c of row r stored at slot c ^ xswz(r & 15); then
     // the scales and zeros of the workgroup's BNT rows, windows of 8
-    // consecutive groups, double-buffered: [buffer][scale, zero][row][8]
+    // consecutive groups, double-buffered: [buffer][scale, zero][group][row]
+    // (a lane's read of its row's value is then one of 16 consecutive 2-byte
+    // entries: no bank conflicts, where [row][8] had 16-byte strides)
     extern __shared__ u32x4 smem[];
     u32x4 (*xs)[BM * 16] = reinterpret_cast<u32x4 (*)[BM * 16]>(smem);
-    uint16_t (*szw)[2][BNT][8] = reinterpret_cast<uint16_t (*)[2][BNT][8]>(smem + 2 * BM * 16);
+    uint16_t (*szw)[2][8][BNT] = reinterpret_cast<uint16_t (*)[2][8][BNT]>(smem + 2 * BM * 16);
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -363,8 +365,12 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
     };
     auto store_sz = [&](int wnd) {
         if (tid >= BNT) return;
-        *reinterpret_cast<u32x4*>(szw[wnd & 1][0][tid]) = szs;
-        *reinterpret_cast<u32x4*>(szw[wnd & 1][1][tid]) = szz;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const uint32_t se = szs[e / 2], ze = szz[e / 2];
+            szw[wnd & 1][0][e][tid] = static_cast<uint16_t>(se >> (16 * (e & 1)));
+            szw[wnd & 1][1][e][tid] = static_cast<uint16_t>(ze >> (16 * (e & 1)));
+        }
     };
     // K steps per window of 8 groups (G / 16 >= 2: G is a multiple of 128 / bits)
     const int spw = a.G / 16;
@@ -424,8 +430,8 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
         for (int j = 0; j < JT; ++j) {
             // past K or N the scale is 0: q - z is finite, so the weight is 0
             const int nl = wave * 16 * JT + 16 * j + r;
-            const uint32_t zb = szw[wb][1][nl][we];
-            const uint32_t sb = (kval && n0 + 16 * j + r < a.N) ? static_cast<uint32_t>(szw[wb][0][nl][we]) : 0u;
+            const uint32_t zb = szw[wb][1][we][nl];
+            const uint32_t sb = (kval && n0 + 16 * j + r < a.N) ? static_cast<uint32_t>(szw[wb][0][we][nl]) : 0u;
             if constexpr (BITS == 4) {
                 const f16 sv = __builtin_bit_cast(f16, static_cast<uint16_t>(sb));
                 zq[j] = make_zq(zb);
