@@ -663,6 +663,12 @@ __global__ __launch_bounds__(1024) void decode_prep_mfma_kernel(PrepMArgs a) {
 // partials of decode_prep_mfma_kernel, summed in a fixed order and split
 // into fp16 hi and lo parts, one step each); the waves' tiles are summed
 // through LDS in a fixed order; one rounding to the output dtype.
+// Row stride, in entries, of the MFMA backbone's scale and zero tables in
+// LDS: the groups rounded up to 16, plus 8.  Half of it is 4 mod 8 4-byte
+// banks, so the 16 rows one read instruction touches fall in 16 distinct
+// banks (a stride of 32 groups had put four rows in each bank).
+__host__ __device__ constexpr int szl_stride(int groups) { return (groups + 15) / 16 * 16 + 8; }
+
 template <int BITS, int TPW, int NBUF, bool GLU, int GPB, int NW, bool LONGK>
 __global__ __launch_bounds__((GLU ? 2 : 1) * 64 * NW) void decode_mfma_kernel(DecodeArgs a) {
     static_assert(BITS == 4 || BITS == 3 || BITS == 2, "4-, 3- or 2-bit codes");
@@ -673,7 +679,7 @@ __global__ __launch_bounds__((GLU ? 2 : 1) * 64 * NW) void decode_mfma_kernel(De
     constexpr int TPH = 64 * NW;                  // threads per phase
     static_assert(TPW <= NW, "one stored tile per wave");
     __shared__ f32x4 red[NW * NPH][TPW][64];
-    extern __shared__ uint16_t szl_all[];         // per phase [2][16 TPW][groups]: the rows' scales, then zeros
+    extern __shared__ uint16_t szl_all[];         // per phase [2][16 TPW][RS]: the rows' scales, then zeros
     const int lane = threadIdx.x & 63;
     const int wave_all = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int ph = GLU ? wave_all / NW : 0;
@@ -699,7 +705,8 @@ __global__ __launch_bounds__((GLU ? 2 : 1) * 64 * NW) void decode_mfma_kernel(De
     const int words_row = K / 8;                  // 8-code units of a row (activation words)
     const int qwords_row = K * BITS / 32;         // 32-bit code words of a row
     const int groups = K / a.G;
-    uint16_t* const szl = szl_all + ph * (2 * 16 * TPW * groups);
+    const int RS = szl_stride(groups);            // padded row stride of the tables
+    uint16_t* const szl = szl_all + ph * (2 * 16 * TPW * RS);
     const uint32_t mlo = __builtin_amdgcn_readfirstlane(0x000F000Fu);
     const uint32_t mhi = __builtin_amdgcn_readfirstlane(0x00F000F0u);
     uint32_t m2[4], m3[3];
@@ -723,10 +730,13 @@ __global__ __launch_bounds__((GLU ? 2 : 1) * 64 * NW) void decode_mfma_kernel(De
     const uint16_t* ssrc = L.s + static_cast<size_t>(row0) * groups;
     const uint16_t* zsrc = L.z + static_cast<size_t>(row0) * groups;
     // 16-byte pieces only where both runs start 16-byte aligned (the caller's
-    // arrays need only 2-byte alignment)
-    const bool al = ((reinterpret_cast<uintptr_t>(ssrc) | reinterpret_cast<uintptr_t>(zsrc)) & 15) == 0;
+    // arrays need only 2-byte alignment) and no piece spans two rows
+    const bool al = ((reinterpret_cast<uintptr_t>(ssrc) | reinterpret_cast<uintptr_t>(zsrc)) & 15) == 0 &&
+                    groups % 8 == 0;
     const int n16 = al ? nval / 8 : 0;
-    uint16_t* const zl = szl + 16 * TPW * groups;
+    uint16_t* const zl = szl + 16 * TPW * RS;
+    // table entry of the run's value i (row i / groups, column i % groups)
+    auto tix = [&](int i) { return i / groups * RS + i % groups; };
     const u32x4* s16p = n16 ? reinterpret_cast<const u32x4*>(ssrc) + min(tid, n16 - 1)
                             : reinterpret_cast<const u32x4*>(a.xf);
     const u32x4* z16p = n16 ? reinterpret_cast<const u32x4*>(zsrc) + min(tid, n16 - 1)
@@ -902,8 +912,8 @@ __global__ __launch_bounds__((GLU ? 2 : 1) * 64 * NW) void decode_mfma_kernel(De
             for (int q = 0; q < GPB; ++q) {
                 const int kc = kb * 128 + 32 * SPG * q;   // first code of the group's steps
                 const bool on = kb < nkb && kc < K && rowv[j];
-                const int lr = (16 * j + r) * groups + (on ? kc / a.G : 0);
-                const uint32_t sb = szl[lr], zb = szl[16 * TPW * groups + lr];
+                const int lr = (16 * j + r) * RS + (on ? kc / a.G : 0);
+                const uint32_t sb = szl[lr], zb = szl[16 * TPW * RS + lr];
                 f32x4 p;
                 if constexpr (BITS == 4) {
                     const Zq zq = make_zq(zb);
@@ -940,16 +950,16 @@ __global__ __launch_bounds__((GLU ? 2 : 1) * 64 * NW) void decode_mfma_kernel(De
     for (int j = 0; j < NBUF; ++j) load(wave + NW * j < nkb ? wave + NW * j : 0, b[j]);
     // the scales and zeros into LDS (the code loads stay in flight)
     if (tid < n16) {
-        reinterpret_cast<u32x4*>(szl)[tid] = s_first;
-        reinterpret_cast<u32x4*>(zl)[tid] = z_first;
+        *reinterpret_cast<u32x4*>(szl + tix(8 * tid)) = s_first;
+        *reinterpret_cast<u32x4*>(zl + tix(8 * tid)) = z_first;
     }
     for (int i = tid + TPH; i < n16; i += TPH) {           // more pieces than threads
-        reinterpret_cast<u32x4*>(szl)[i] = reinterpret_cast<const u32x4*>(ssrc)[i];
-        reinterpret_cast<u32x4*>(zl)[i] = reinterpret_cast<const u32x4*>(zsrc)[i];
+        *reinterpret_cast<u32x4*>(szl + tix(8 * i)) = reinterpret_cast<const u32x4*>(ssrc)[i];
+        *reinterpret_cast<u32x4*>(zl + tix(8 * i)) = reinterpret_cast<const u32x4*>(zsrc)[i];
     }
     for (int i = 8 * n16 + tid; i < nval; i += TPH) {      // misaligned runs, the last few values
-        szl[i] = ssrc[i];
-        zl[i] = zsrc[i];
+        szl[tix(i)] = ssrc[i];
+        zl[tix(i)] = zsrc[i];
     }
     __syncthreads();
     for (int rd = 0; rd < rounds; ++rd) {
@@ -1144,7 +1154,7 @@ struct MfmaCfg {
 };
 
 MfmaCfg mfma_cfg(int tiles, int groups) {
-    if (tiles >= 1024 && 2 * 64 * groups * 2 <= 32768) return MfmaCfg{4, 2, 4};
+    if (tiles >= 1024 && 2 * 64 * szl_stride(groups) * 2 <= 32768) return MfmaCfg{4, 2, 4};
     return MfmaCfg{1, 4, 4};
 }
 
@@ -1269,7 +1279,7 @@ hipError_t launch_decode_mfma(int n, const QW* w, const LR* c, const void* x, in
     // a gated window runs one workgroup of eight waves per gate workgroup
     // (four waves on the gate's tiles, four on the up tiles of the same rows),
     // with both linears' scales and zeros in LDS
-    const size_t lds = static_cast<size_t>(2) * 16 * tpw * groups * 2 * (glu ? 2 : 1);
+    const size_t lds = static_cast<size_t>(2) * 16 * tpw * szl_stride(groups) * 2 * (glu ? 2 : 1);
     const int bgrid = glu ? wg_first : wg_end;
     for (int tok0 = 0; tok0 < T && e == hipSuccess; tok0 += 16) {
         a.tok0 = tok0;
