@@ -50,7 +50,7 @@ MFMA_F16_PEAK_TFLOPS = 2500.0
 GATE_TRAFFIC = {"fetch_bytes": (32411 + 710) * 1024, "write_bytes": (56 + 9) * 1024,
                 "sources": ("paper_2605_05819_amd/csrc/decode.hip", "paper_2605_05819_amd/csrc/gemv_common.h",
                             "paper_2605_05819_amd/csrc/cl_device.h"),
-                "sha256": "222af45f24f9de97083d92db9f5a2115b7fb5d7f5661a69dd2317c4a39f364b9"}
+                "sha256": "76689c5865a48b68b7b4974a54f1e488aa645dd7171892eb4b680c3c3b1db176"}
 
 
 def sources_sha256(paths):

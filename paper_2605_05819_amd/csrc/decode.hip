@@ -663,12 +663,6 @@ __global__ __launch_bounds__(1024) void decode_prep_mfma_kernel(PrepMArgs a) {
 // partials of decode_prep_mfma_kernel, summed in a fixed order and split
 // into fp16 hi and lo parts, one step each); the waves' tiles are summed
 // through LDS in a fixed order; one rounding to the output dtype.
-// Row stride, in entries, of the MFMA backbone's scale and zero tables in
-// LDS: the groups rounded up to 16, plus 8.  Half of it is 4 mod 8 4-byte
-// banks, so the 16 rows one read instruction touches fall in 16 distinct
-// banks (a stride of 32 groups had put four rows in each bank).
-__host__ __device__ constexpr int szl_stride(int groups) { return (groups + 15) / 16 * 16 + 8; }
-
 template <int BITS, int TPW, int NBUF, bool GLU, int GPB, int NW, bool LONGK>
 __global__ __launch_bounds__((GLU ? 2 : 1) * 64 * NW) void decode_mfma_kernel(DecodeArgs a) {
     static_assert(BITS == 4 || BITS == 3 || BITS == 2, "4-, 3- or 2-bit codes");
@@ -730,13 +724,13 @@ __global__ __launch_bounds__((GLU ? 2 : 1) * 64 * NW) void decode_mfma_kernel(De
     const uint16_t* ssrc = L.s + static_cast<size_t>(row0) * groups;
     const uint16_t* zsrc = L.z + static_cast<size_t>(row0) * groups;
     // 16-byte pieces only where both runs start 16-byte aligned (the caller's
-    // arrays need only 2-byte alignment) and no piece spans two rows
-    const bool al = ((reinterpret_cast<uintptr_t>(ssrc) | reinterpret_cast<uintptr_t>(zsrc)) & 15) == 0 &&
-                    groups % 8 == 0;
+    // arrays need only 2-byte alignment)
+    const bool al = ((reinterpret_cast<uintptr_t>(ssrc) | reinterpret_cast<uintptr_t>(zsrc)) & 15) == 0;
     const int n16 = al ? nval / 8 : 0;
     uint16_t* const zl = szl + 16 * TPW * RS;
-    // table entry of the run's value i (row i / groups, column i % groups)
-    auto tix = [&](int i) { return i / groups * RS + i % groups; };
+    // table entry of the run's value i (row i / groups, column i % groups;
+    // the identity on an unpadded table, where pieces may span rows)
+    auto tix = [&](int i) { return RS == groups ? i : i / groups * RS + i % groups; };
     const u32x4* s16p = n16 ? reinterpret_cast<const u32x4*>(ssrc) + min(tid, n16 - 1)
                             : reinterpret_cast<const u32x4*>(a.xf);
     const u32x4* z16p = n16 ? reinterpret_cast<const u32x4*>(zsrc) + min(tid, n16 - 1)

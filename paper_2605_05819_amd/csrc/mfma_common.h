@@ -7,6 +7,17 @@
 
 namespace cl {
 
+// Row stride, in entries, of the MFMA backbones' scale and zero tables in
+// LDS (decode and MoE): for a multiple of 8 groups, the groups rounded up to
+// 16, plus 8 -- half of it is 4 mod 8 4-byte banks, so the 16 rows one read
+// instruction touches fall in 16 distinct banks (a stride of 32 groups had
+// put four rows in each bank) and 16-byte pieces of a row stay aligned;
+// otherwise the groups themselves (the table stays one contiguous run, which
+// 16-byte pieces fill across row boundaries).
+__host__ __device__ constexpr int szl_stride(int groups) {
+    return groups % 8 ? groups : (groups + 15) / 16 * 16 + 8;
+}
+
 // (x & m) | c in one instruction; m comes from a scalar register, c from a
 // vector register (one scalar operand per instruction on this target).
 __device__ __forceinline__ uint32_t and_or(uint32_t x, uint32_t m, uint32_t c) {

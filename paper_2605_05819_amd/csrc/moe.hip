@@ -896,7 +896,7 @@ __global__ __launch_bounds__(64 * NWV) void moe_direct_kernel(MoeArgs a) {
 template <int TPW, int NBUF, int GPB>
 __global__ __launch_bounds__(256) void moe_mfma_kernel(MoeArgs a) {
     __shared__ f32x4 red[4][TPW][64];
-    extern __shared__ uint16_t szl[];             // [2][16 TPW][groups]: the rows' scales, then zeros
+    extern __shared__ uint16_t szl[];             // [2][16 TPW][szl_stride(groups)]: the rows' scales, then zeros
     const int blk = blockIdx.x;
     int li = 0;
     while (blk >= a.lin[li].blk_end) ++li;
@@ -1011,9 +1011,13 @@ __global__ __launch_bounds__(256) void moe_mfma_kernel(MoeArgs a) {
     const int nval = min(16 * TPW, L.d_out - row0) * groups;
     const uint16_t* ssrc = se + static_cast<size_t>(row0) * groups;
     const uint16_t* zsrc = ze + static_cast<size_t>(row0) * groups;
-    uint16_t* zl = szl + 16 * TPW * groups;
+    const int RS = szl_stride(groups);            // padded row stride of the tables
+    uint16_t* zl = szl + 16 * TPW * RS;
     const bool al = ((reinterpret_cast<uintptr_t>(ssrc) | reinterpret_cast<uintptr_t>(zsrc)) & 15) == 0;
     const int n16 = al ? nval / 8 : 0;
+    // table entry of the run's value i (row i / groups, column i % groups;
+    // the identity on an unpadded table, where pieces may span rows)
+    auto tix = [&](int i) { return RS == groups ? i : i / groups * RS + i % groups; };
     // first 16-byte piece of each array per thread (a valid aligned address
     // when this thread has none)
     const u32x4* s16p = n16 ? reinterpret_cast<const u32x4*>(ssrc) + min(tid, n16 - 1)
@@ -1028,16 +1032,16 @@ __global__ __launch_bounds__(256) void moe_mfma_kernel(MoeArgs a) {
 #pragma unroll
     for (int j = 0; j < NBUF; ++j) load_w(wave + 4 * j, b[j]);
     if (tid < n16) {
-        reinterpret_cast<u32x4*>(szl)[tid] = s_first;
-        reinterpret_cast<u32x4*>(zl)[tid] = z_first;
+        *reinterpret_cast<u32x4*>(szl + tix(8 * tid)) = s_first;
+        *reinterpret_cast<u32x4*>(zl + tix(8 * tid)) = z_first;
     }
     for (int i = tid + 256; i < n16; i += 256) {           // rows with more than 32 groups
-        reinterpret_cast<u32x4*>(szl)[i] = reinterpret_cast<const u32x4*>(ssrc)[i];
-        reinterpret_cast<u32x4*>(zl)[i] = reinterpret_cast<const u32x4*>(zsrc)[i];
+        *reinterpret_cast<u32x4*>(szl + tix(8 * i)) = reinterpret_cast<const u32x4*>(ssrc)[i];
+        *reinterpret_cast<u32x4*>(zl + tix(8 * i)) = reinterpret_cast<const u32x4*>(zsrc)[i];
     }
     for (int i = 8 * n16 + tid; i < nval; i += 256) {      // misaligned runs, the last few values
-        szl[i] = ssrc[i];
-        zl[i] = zsrc[i];
+        szl[tix(i)] = ssrc[i];
+        zl[tix(i)] = zsrc[i];
     }
     __syncthreads();
 
@@ -1082,8 +1086,8 @@ __global__ __launch_bounds__(256) void moe_mfma_kernel(MoeArgs a) {
                 for (int q = 0; q < GPB; ++q) {
                     const int kc = kb * 128 + 32 * SPG * q;
                     const bool on = kb < nkb && kc < K && rowv[j];
-                    const int lr = (16 * j + r) * groups + (on ? kc / a.G : 0);
-                    const Zq zq = make_zq(szl[16 * TPW * groups + lr]);
+                    const int lr = (16 * j + r) * RS + (on ? kc / a.G : 0);
+                    const Zq zq = make_zq(szl[16 * TPW * RS + lr]);
                     f32x4 pp = mfma(xv[SPG * q], codes_minus_zero(w[SPG * q], zq, mlo, mhi, bias),
                                     f32x4{0.f, 0.f, 0.f, 0.f});
 #pragma unroll
@@ -1369,7 +1373,7 @@ hipError_t launch_moe_decode(int n, const QW* w, const uint16_t* const* A, const
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     if (on_mfma) {
-        const size_t lds = static_cast<size_t>(2) * 16 * kMoeTpw * (d_in / w[0].G) * 2;
+        const size_t lds = static_cast<size_t>(2) * 16 * kMoeTpw * szl_stride(d_in / w[0].G) * 2;
         // quantization groups a 128-code block can meet (see the kernel)
         const int G = w[0].G;
         if (G % 128 == 0)
