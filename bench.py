@@ -47,7 +47,7 @@ MFMA_F16_PEAK_TFLOPS = 2500.0
 # scaled by the same counters on a plain 256 MiB device copy (FETCH_SIZE
 # reads half the copied bytes: x2; WRITE_SIZE exact: x1).  Valid only for the
 # kernel sources it was measured on (their SHA-256 below); null otherwise.
-GATE_TRAFFIC = {"fetch_bytes": (32411 + 710) * 1024, "write_bytes": (56 + 9) * 1024,
+GATE_TRAFFIC = {"fetch_bytes": (32397 + 702) * 1024, "write_bytes": (56 + 9) * 1024,
                 "sources": ("paper_2605_05819_amd/csrc/decode.hip", "paper_2605_05819_amd/csrc/gemv_common.h",
                             "paper_2605_05819_amd/csrc/cl_device.h"),
                 "sha256": "76689c5865a48b68b7b4974a54f1e488aa645dd7171892eb4b680c3c3b1db176"}
