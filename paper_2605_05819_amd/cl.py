@@ -3,6 +3,8 @@
 Argument marshalling only: every step of the layer runs in the HIP kernels of
 the library.  PyTorch provides device memory and the current stream.  If the
 library has not been built, :func:`lib` raises -- there is no fallback path.
+The environment variable CL_LIBRARY, when set, names another build of the same
+library to load instead (the host-sanitized build, for instance).
 """
 
 import ctypes
@@ -13,7 +15,7 @@ from typing import Optional
 import numpy as np
 import torch
 
-LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libcl.so")
+LIB_PATH = os.environ.get("CL_LIBRARY") or os.path.join(os.path.dirname(os.path.abspath(__file__)), "libcl.so")
 
 CL_OK, CL_EINVAL, CL_EUNSUPPORTED, CL_EWORKSPACE, CL_EHIP = range(5)
 CL_FP16, CL_BF16, CL_FP32 = 1, 2, 3
@@ -110,7 +112,7 @@ def lib():
     global _lib
     if _lib is None:
         if not os.path.exists(LIB_PATH):
-            raise RuntimeError("libcl.so is not built; run `python -m paper_2605_05819_amd.build`")
+            raise RuntimeError("%s is not built; run `python -m paper_2605_05819_amd.build`" % LIB_PATH)
         handle = ctypes.CDLL(LIB_PATH)
         for name, (res, args) in _SIGNATURES.items():
             fn = getattr(handle, name)
